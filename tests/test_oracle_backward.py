@@ -1,0 +1,127 @@
+"""Pins of the backward oracle (reverse-time adjoint and App. B chunk backward).
+
+The adjoint is checked against central finite differences of the loss
+L = sum_t <o_t, do_t> + <S_T, dS_T> (all elements on tiny shapes, directional
+at larger ones), against the tied-gate identities of App. A.5, and the chunk
+backward of App. B is checked against the adjoint.  A planted mistake (the
+scalar post-scale App. B.6 rules out) must fail the finite-difference pin.
+CPU only.
+"""
+
+import numpy as np
+import pytest
+
+from oracle import gdr2_recurrent_fwd, gdr2_recurrent_bwd, gdr2_chunk_bwd_ref, fd, limits
+from tests.helpers import rel_l2, small_problem
+
+GRADS = {"q": "dq", "k": "dk", "v": "dv", "g": "dg", "b": "db", "w": "dw", "S0": "dS0"}
+
+
+def _inputs(d):
+    return dict(q=d["q"].astype(np.float64), k=d["k"].astype(np.float64),
+                v=d["v"].astype(np.float64), g=d["log_alpha"].astype(np.float64),
+                b=d["b"].astype(np.float64), w=d["w"].astype(np.float64),
+                S0=d["S0"].astype(np.float64))
+
+
+def _adj(d, dST, ckpt=64, scale=None):
+    x = _inputs(d)
+    return gdr2_recurrent_bwd(x["q"], x["k"], x["v"], x["g"], x["b"], x["w"], x["S0"],
+                              d["do"], dST, d["scale"] if scale is None else scale, ckpt=ckpt)
+
+
+def _fwd_fn(scale):
+    def f(q, k, v, g, b, w, S0):
+        return gdr2_recurrent_fwd(q, k, v, g, b, w, S0, scale)
+    return f
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_G1_adjoint_vs_full_finite_differences(seed):
+    d = small_problem(1, 10, 2, 4, 3, seed=100 + seed, dST=True)
+    dST = d["dST"].astype(np.float64)
+    grads = _adj(d, dST, ckpt=4)   # ckpt < T exercises the segment recompute
+    x = _inputs(d)
+    f = _fwd_fn(d["scale"])
+    for name, gname in GRADS.items():
+        g_fd = fd.fd_grad(f, x, name, d["do"], dST, h=1e-6)
+        assert rel_l2(grads[gname], g_fd) < 1e-7, name
+
+
+def test_G2_adjoint_directional_derivative():
+    d = small_problem(2, 96, 2, 16, 16, seed=7, dST=True)
+    dST = d["dST"].astype(np.float64)
+    grads = _adj(d, dST, ckpt=32)
+    x = _inputs(d)
+    rng = np.random.default_rng(3)
+    for _ in range(3):
+        dirs = {n: rng.standard_normal(x[n].shape) for n in GRADS}
+        pred = sum(float(np.sum(grads[GRADS[n]] * dirs[n])) for n in GRADS)
+        got = fd.fd_directional(_fwd_fn(d["scale"]), x, dirs, d["do"], dST, h=1e-5)
+        assert abs(pred - got) < 1e-7 * max(1.0, abs(got))
+
+
+@pytest.mark.parametrize("C,T", [(4, 16), (8, 20), (16, 64)])
+def test_G5_chunk_backward_equals_adjoint(C, T):
+    """App. B chunk equations (incl. a ragged last chunk) == token adjoint."""
+    d = small_problem(2, T, 2, 8, 6, seed=200 + C + T, dST=True)
+    dST = d["dST"].astype(np.float64)
+    ref = _adj(d, dST, ckpt=8)
+    x = _inputs(d)
+    got = gdr2_chunk_bwd_ref(x["q"], x["k"], x["v"], x["g"], x["b"], x["w"], x["S0"],
+                             d["do"], dST, d["scale"], C=C)
+    for gname in GRADS.values():
+        assert rel_l2(got[gname], ref[gname]) < 1e-10, gname
+
+
+def test_G3_beta_gradient_identity_against_KDA():
+    """Tied gates: sum_c db + sum_c dw equals dL/dbeta of an independent KDA
+    recurrence (eq. eq_app_beta_gradient), the latter by finite differences."""
+    d = small_problem(1, 12, 1, 5, 4, seed=31, gates="tied")
+    grads = _adj(d, None)
+    dbeta = grads["db"].sum(-1) + grads["dw"].sum(-1)
+    beta = d["beta"].astype(np.float64)
+
+    def kda(q, k, v, g, beta, S0):
+        return limits.kda_fwd(q, k, v, g, beta, S0, d["scale"])
+
+    x = dict(q=d["q"], k=d["k"], v=d["v"], g=d["log_alpha"], beta=beta, S0=d["S0"])
+    dbeta_fd = fd.fd_grad(kda, x, "beta", d["do"], None, h=1e-6)
+    assert rel_l2(dbeta, dbeta_fd) < 1e-7
+
+
+def test_G4_scalar_decay_gradient_against_GDN():
+    """Tied gates and scalar decay: sum_c dlog_alpha equals the scalar-decay
+    gradient of an independent Gated DeltaNet recurrence (finite differences)."""
+    d = small_problem(1, 12, 1, 5, 4, seed=32, gates="tied", decay="scalar")
+    grads = _adj(d, None)
+    dla = grads["dg"].sum(-1)
+
+    def gdn(q, k, v, g, beta, S0):
+        return limits.gdn_fwd(q, k, v, g, beta, S0, d["scale"])
+
+    x = dict(q=d["q"], k=d["k"], v=d["v"], g=d["log_alpha_scalar"].astype(np.float64),
+             beta=d["beta"], S0=d["S0"])
+    dla_fd = fd.fd_grad(gdn, x, "g", d["do"], None, h=1e-6)
+    assert rel_l2(dla, dla_fd) < 1e-7
+
+
+def test_G6_scalar_post_scaling_is_caught():
+    """App. B.6: a KDA-style post-scaled dA fails against finite differences when
+    the gates are untied, and coincides with the correct backward when tied."""
+    d = small_problem(1, 16, 1, 6, 5, seed=33)
+    x = _inputs(d)
+    bad = gdr2_chunk_bwd_ref(x["q"], x["k"], x["v"], x["g"], x["b"], x["w"], x["S0"],
+                             d["do"], None, d["scale"], C=8, mutation="scalar_post_scale")
+    f = _fwd_fn(d["scale"])
+    worst = max(rel_l2(bad[GRADS[n]], fd.fd_grad(f, x, n, d["do"], None)) for n in ("b", "w", "k", "v"))
+    assert worst > 1e-3
+
+    t = small_problem(1, 16, 1, 6, 5, seed=34, gates="tied")
+    xt = _inputs(t)
+    bad_t = gdr2_chunk_bwd_ref(xt["q"], xt["k"], xt["v"], xt["g"], xt["b"], xt["w"], xt["S0"],
+                               t["do"], None, t["scale"], C=8, mutation="scalar_post_scale")
+    good_t = gdr2_chunk_bwd_ref(xt["q"], xt["k"], xt["v"], xt["g"], xt["b"], xt["w"], xt["S0"],
+                                t["do"], None, t["scale"], C=8)
+    for gname in GRADS.values():
+        assert rel_l2(bad_t[gname], good_t[gname]) < 1e-12
