@@ -1,0 +1,130 @@
+/*
+ * gdr2.h -- C ABI of the MI355X (gfx950) chunkwise Gated Delta Rule-2 operator.
+ *
+ * Gated Delta Rule-2 (Gated DeltaNet-2, arXiv 2605.22791, Sec. 3.1, eqs.
+ * eq_gdn2_e_z, eq_gdn2_residual, eq_gdn2_recurrence).  For every batch row b
+ * and head h independently, with state S in R^{Dk x Dv}:
+ *
+ *     e_t = b_t * k_t,   z_t = w_t * v_t                 (erase / write factors)
+ *     S_t = (I - k_t e_t^T) Diag(exp(g_t)) S_{t-1} + k_t z_t^T
+ *     o_t = scale * S_t^T q_t                            (post-update read-out)
+ *
+ * g = log_alpha is the per-key-channel log-decay (the paper's g_t; alpha_t =
+ * exp(g_t)), b in [0,1]^Dk (or [0,2]^Dk for the negative-eigenvalue variant,
+ * Sec. 3.1) is the erase gate and w in [0,1]^Dv the write gate.  `scale`
+ * multiplies the output only (callers normally pass 1/sqrt(Dk); the paper's
+ * notation is scale = 1).  q and k are consumed as given: L2 normalisation,
+ * when wanted (App. D.2), is the caller's.
+ *
+ * Layout and dtypes (all tensors contiguous, row-major, device memory):
+ *     q, k, b, log_alpha           (B, T, H, Dk)
+ *     v, w, o                      (B, T, H, Dv)
+ *     S0, S_T, S, dS_T, dS0        (B, H, Dk, Dv)   always fp32
+ *     log_alpha, dlog_alpha        always fp32 (the decay is formed in fp32,
+ *                                  App. C.1 / App. D.1)
+ *     q, k, v, b, w, o, dout, dq, dk, dv, db, dw
+ *                                  problem->dtype (bf16 or fp32)
+ * The recurrent state is fp32 everywhere (App. D.3); every product inside the
+ * kernels accumulates in fp32.
+ *
+ * Ownership and errors:
+ *   * The caller owns every buffer; the library never allocates or frees and
+ *     keeps no mutable global state, so calls are re-entrant.  Work is
+ *     enqueued on `stream` and the call returns without waiting.
+ *   * Outputs are overwritten, never accumulated.  Workspace contents are
+ *     undefined after a call.  Inputs and outputs must not alias (except S in
+ *     gdr2_recurrent_step, which is updated in place).
+ *   * Every argument is validated before any HIP call; on error nothing is
+ *     launched and the status says why:
+ *       GDR2_EINVAL        null required pointer, pointer not 16-byte aligned,
+ *                          a dimension <= 0, non-finite scale, unknown dtype;
+ *       GDR2_EUNSUPPORTED  Dk or Dv not in {64, 128}, chunk != 64, T not a
+ *                          multiple of 64 (chunk calls), sizes beyond 2^31
+ *                          elements per tensor;
+ *       GDR2_EWORKSPACE    ws_bytes below gdr2_chunk_workspace_bytes();
+ *       GDR2_EHIP          a launch reported an error (hipGetLastError).
+ *   * No C++ exception crosses this interface.
+ *   * Inputs outside the documented domain (log_alpha > 0, NaN/Inf values)
+ *     are not checked; results are then undefined.
+ */
+#ifndef GDR2_H_
+#define GDR2_H_
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum gdr2_status {
+  GDR2_OK = 0,
+  GDR2_EINVAL = 1,
+  GDR2_EUNSUPPORTED = 2,
+  GDR2_EWORKSPACE = 3,
+  GDR2_EHIP = 4
+} gdr2_status;
+
+typedef enum gdr2_dtype { GDR2_BF16 = 0, GDR2_FP32 = 1 } gdr2_dtype;
+
+/* Problem description shared by every call.  `chunk` must be 64 (the chunk
+ * length C of Sec. 3.3; App. C.2 fixes C = 64). */
+typedef struct gdr2_problem {
+  int32_t B, T, H, Dk, Dv;
+  int32_t chunk;
+  float scale;
+  int32_t dtype; /* gdr2_dtype */
+} gdr2_problem;
+
+/* Bytes of device workspace a chunk call needs (for_backward = 0: forward,
+ * 1: backward).  Writes the size to *bytes.  Errors as in the calls. */
+gdr2_status gdr2_chunk_workspace_bytes(const gdr2_problem* problem, int for_backward,
+                                       size_t* bytes);
+
+/* Chunkwise WY forward (Sec. 3.3; App. A; App. C.2): the intra-chunk kernel
+ * forms the decay-weighted Gram T = tril(Ebar Kbar^T, -1) and the scores A_qk,
+ * solves A = (I + T)^{-1} in fp32 and builds Y = A Ebar and U = A (W*V); the
+ * state kernel then carries S across chunks (eq. eq_gdn2_chunk_state) and
+ * writes O (eq. eq_gdn2_chunk_output).
+ *   S0   may be NULL (zero start state).
+ *   o    receives (B,T,H,Dv) in problem->dtype.
+ *   S_T  may be NULL; otherwise receives the final state (fp32).
+ *   ws   device workspace of at least gdr2_chunk_workspace_bytes(p, 0). */
+gdr2_status gdr2_chunk_fwd(const gdr2_problem* problem, const void* q, const void* k,
+                           const void* v, const float* log_alpha, const void* b,
+                           const void* w, const float* S0, void* o, float* S_T, void* ws,
+                           size_t ws_bytes, hipStream_t stream);
+
+/* Gate-aware chunkwise backward (Sec. 3.4; App. B; App. C.3) of
+ *     L = sum_t <o_t, dout_t> + <S_T, dS_T>
+ * with respect to every input.  The forward intermediates are recomputed from
+ * the inputs (the memory-saving path of App. D.3), so the call takes exactly
+ * the forward's inputs plus the upstream gradients.
+ *   S0, dS_T   may be NULL (zero).
+ *   dq, dk, db (B,T,H,Dk) and dv, dw (B,T,H,Dv) in problem->dtype;
+ *   dlog_alpha (B,T,H,Dk) fp32; dS0 (B,H,Dk,Dv) fp32 or NULL (not wanted).
+ *   ws   device workspace of at least gdr2_chunk_workspace_bytes(p, 1). */
+gdr2_status gdr2_chunk_bwd(const gdr2_problem* problem, const void* q, const void* k,
+                           const void* v, const float* log_alpha, const void* b,
+                           const void* w, const float* S0, const void* dout,
+                           const float* dS_T, void* dq, void* dk, void* dv,
+                           float* dlog_alpha, void* db, void* dw, float* dS0, void* ws,
+                           size_t ws_bytes, hipStream_t stream);
+
+/* Recurrent (token-by-token) forward for decoding (App. C.5): applies the
+ * update to problem->T >= 1 consecutive tokens (T = 1 for one decode step),
+ * keeping S in fp32 and updating it in place; o (B,T,H,Dv) in problem->dtype.
+ * `chunk` is ignored and T need not be a multiple of 64.  No workspace. */
+gdr2_status gdr2_recurrent_step(const gdr2_problem* problem, const void* q, const void* k,
+                                const void* v, const float* log_alpha, const void* b,
+                                const void* w, float* S, void* o, hipStream_t stream);
+
+/* Static, human-readable name of a status code. */
+const char* gdr2_status_str(gdr2_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GDR2_H_ */

@@ -1,1 +1,207 @@
-"""MI355X-native chunkwise Gated Delta Rule-2 operator (binding loaded lazily)."""
+"""MI355X (gfx950) chunkwise Gated Delta Rule-2 operator -- Python binding.
+
+A thin ctypes layer over the C ABI in include/gdr2.h (libgdr2.so, built by
+``python -m paper_2605_22791_amd.build``).  It only marshals arguments:
+shapes and dtypes are read from the torch tensors, outputs and workspace are
+allocated with torch when the caller does not pass them, and every step of the
+operator runs in the HIP kernels of the library on the current torch stream.
+
+If the library is missing the functions raise; there is no fallback.
+"""
+
+import ctypes
+import os
+
+__all__ = [
+    "GDR2_OK", "GDR2_EINVAL", "GDR2_EUNSUPPORTED", "GDR2_EWORKSPACE", "GDR2_EHIP",
+    "GDR2_BF16", "GDR2_FP32", "Gdr2Problem", "Gdr2Error", "lib", "lib_path",
+    "gdr2_chunk_workspace_bytes", "gdr2_chunk_fwd", "gdr2_chunk_bwd",
+    "gdr2_recurrent_step", "gdr2_status_str", "CHUNK",
+]
+
+GDR2_OK, GDR2_EINVAL, GDR2_EUNSUPPORTED, GDR2_EWORKSPACE, GDR2_EHIP = 0, 1, 2, 3, 4
+GDR2_BF16, GDR2_FP32 = 0, 1
+CHUNK = 64
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def lib_path():
+    return os.path.join(_HERE, "libgdr2.so")
+
+
+class Gdr2Problem(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("T", ctypes.c_int32), ("H", ctypes.c_int32),
+                ("Dk", ctypes.c_int32), ("Dv", ctypes.c_int32), ("chunk", ctypes.c_int32),
+                ("scale", ctypes.c_float), ("dtype", ctypes.c_int32)]
+
+
+class Gdr2Error(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__(f"{where}: {gdr2_status_str(status)} ({status})")
+
+
+_LIB = None
+
+
+def lib():
+    """The loaded libgdr2.so (raises if it has not been built)."""
+    global _LIB
+    if _LIB is None:
+        path = lib_path()
+        if not os.path.exists(path):
+            raise ImportError(f"GDR-2 HIP library not built: {path} is missing "
+                              "(run python -m paper_2605_22791_amd.build)")
+        L = ctypes.CDLL(path)
+        P = ctypes.POINTER(Gdr2Problem)
+        vp = ctypes.c_void_p
+        L.gdr2_chunk_workspace_bytes.argtypes = [P, ctypes.c_int, ctypes.POINTER(ctypes.c_size_t)]
+        L.gdr2_chunk_workspace_bytes.restype = ctypes.c_int
+        L.gdr2_chunk_fwd.argtypes = [P] + [vp] * 10 + [ctypes.c_size_t, vp]
+        L.gdr2_chunk_fwd.restype = ctypes.c_int
+        L.gdr2_chunk_bwd.argtypes = [P] + [vp] * 17 + [ctypes.c_size_t, vp]
+        L.gdr2_chunk_bwd.restype = ctypes.c_int
+        L.gdr2_recurrent_step.argtypes = [P] + [vp] * 8 + [vp]
+        L.gdr2_recurrent_step.restype = ctypes.c_int
+        L.gdr2_status_str.argtypes = [ctypes.c_int]
+        L.gdr2_status_str.restype = ctypes.c_char_p
+        _LIB = L
+    return _LIB
+
+
+def gdr2_status_str(status):
+    return lib().gdr2_status_str(int(status)).decode()
+
+
+def _check(status, where):
+    if status != GDR2_OK:
+        raise Gdr2Error(status, where)
+
+
+# --------------------------------------------------------------------------- torch helpers
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t):
+    torch = _torch()
+    if t.dtype == torch.bfloat16:
+        return GDR2_BF16
+    if t.dtype == torch.float32:
+        return GDR2_FP32
+    raise TypeError(f"unsupported dtype {t.dtype} (bfloat16 or float32)")
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(_torch().cuda.current_stream().cuda_stream)
+
+
+def _problem(q, v, scale, chunk=CHUNK):
+    B, T, H, Dk = q.shape
+    Dv = v.shape[-1]
+    if scale is None:
+        scale = Dk ** -0.5
+    return Gdr2Problem(B, T, H, Dk, Dv, chunk, float(scale), _dtype_code(q))
+
+
+def _require(name, t, shape, dtype):
+    if t is None:
+        return
+    if tuple(t.shape) != tuple(shape) or t.dtype != dtype or not t.is_contiguous() or not t.is_cuda:
+        raise ValueError(f"{name}: expected contiguous {dtype} device tensor of shape {tuple(shape)}, "
+                         f"got {t.dtype} {tuple(t.shape)} (contiguous={t.is_contiguous()}, cuda={t.is_cuda})")
+
+
+def _validate(q, k, v, log_alpha, b, w):
+    torch = _torch()
+    B, T, H, Dk = q.shape
+    Dv = v.shape[-1]
+    for n, t in (("q", q), ("k", k), ("b", b)):
+        _require(n, t, (B, T, H, Dk), q.dtype)
+    for n, t in (("v", v), ("w", w)):
+        _require(n, t, (B, T, H, Dv), q.dtype)
+    _require("log_alpha", log_alpha, (B, T, H, Dk), torch.float32)
+    return B, T, H, Dk, Dv
+
+
+# --------------------------------------------------------------------------- public calls
+def gdr2_chunk_workspace_bytes(problem, for_backward):
+    """Bytes of workspace for a Gdr2Problem (for_backward: 0 forward, 1 backward)."""
+    n = ctypes.c_size_t(0)
+    _check(lib().gdr2_chunk_workspace_bytes(ctypes.byref(problem), int(for_backward), ctypes.byref(n)),
+           "gdr2_chunk_workspace_bytes")
+    return n.value
+
+
+def gdr2_chunk_fwd(q, k, v, log_alpha, b, w, S0=None, *, scale=None, o=None, S_T=None,
+                   want_state=True, ws=None):
+    """Chunkwise GDR-2 forward.  Returns (o, S_T) (S_T None unless wanted)."""
+    torch = _torch()
+    B, T, H, Dk, Dv = _validate(q, k, v, log_alpha, b, w)
+    _require("S0", S0, (B, H, Dk, Dv), torch.float32)
+    prob = _problem(q, v, scale)
+    if o is None:
+        o = torch.empty((B, T, H, Dv), dtype=q.dtype, device=q.device)
+    _require("o", o, (B, T, H, Dv), q.dtype)
+    if S_T is None and want_state:
+        S_T = torch.empty((B, H, Dk, Dv), dtype=torch.float32, device=q.device)
+    _require("S_T", S_T, (B, H, Dk, Dv), torch.float32)
+    need = gdr2_chunk_workspace_bytes(prob, 0)
+    if ws is None:
+        ws = torch.empty(need, dtype=torch.uint8, device=q.device)
+    st = lib().gdr2_chunk_fwd(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(b),
+                              _ptr(w), _ptr(S0), _ptr(o), _ptr(S_T), _ptr(ws), ws.numel(), _stream())
+    _check(st, "gdr2_chunk_fwd")
+    return o, S_T
+
+
+def gdr2_chunk_bwd(q, k, v, log_alpha, b, w, S0, dout, dS_T=None, *, scale=None, grads=None,
+                   want_dS0=True, ws=None):
+    """Gate-aware chunkwise backward.  Returns dict dq, dk, dv, dlog_alpha, db, dw, dS0."""
+    torch = _torch()
+    B, T, H, Dk, Dv = _validate(q, k, v, log_alpha, b, w)
+    _require("S0", S0, (B, H, Dk, Dv), torch.float32)
+    _require("dout", dout, (B, T, H, Dv), q.dtype)
+    _require("dS_T", dS_T, (B, H, Dk, Dv), torch.float32)
+    prob = _problem(q, v, scale)
+    g = dict(grads or {})
+    dev = q.device
+    g.setdefault("dq", torch.empty_like(q))
+    g.setdefault("dk", torch.empty_like(k))
+    g.setdefault("dv", torch.empty_like(v))
+    g.setdefault("dlog_alpha", torch.empty_like(log_alpha))
+    g.setdefault("db", torch.empty_like(b))
+    g.setdefault("dw", torch.empty_like(w))
+    if want_dS0:
+        g.setdefault("dS0", torch.empty((B, H, Dk, Dv), dtype=torch.float32, device=dev))
+    else:
+        g.setdefault("dS0", None)
+    need = gdr2_chunk_workspace_bytes(prob, 1)
+    if ws is None:
+        ws = torch.empty(need, dtype=torch.uint8, device=dev)
+    st = lib().gdr2_chunk_bwd(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(b),
+                              _ptr(w), _ptr(S0), _ptr(dout), _ptr(dS_T), _ptr(g["dq"]), _ptr(g["dk"]),
+                              _ptr(g["dv"]), _ptr(g["dlog_alpha"]), _ptr(g["db"]), _ptr(g["dw"]),
+                              _ptr(g["dS0"]), _ptr(ws), ws.numel(), _stream())
+    _check(st, "gdr2_chunk_bwd")
+    return g
+
+
+def gdr2_recurrent_step(q, k, v, log_alpha, b, w, S, *, scale=None, o=None):
+    """Token-by-token forward over q.shape[1] tokens; S (fp32) updated in place.  Returns o."""
+    torch = _torch()
+    B, T, H, Dk, Dv = _validate(q, k, v, log_alpha, b, w)
+    _require("S", S, (B, H, Dk, Dv), torch.float32)
+    prob = _problem(q, v, scale)
+    if o is None:
+        o = torch.empty((B, T, H, Dv), dtype=q.dtype, device=q.device)
+    st = lib().gdr2_recurrent_step(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha),
+                                   _ptr(b), _ptr(w), _ptr(S), _ptr(o), _stream())
+    _check(st, "gdr2_recurrent_step")
+    return o

@@ -1,0 +1,258 @@
+// C ABI of the GDR-2 operator: argument validation, workspace layout and the
+// launch sequence.  Every check runs before the first HIP call; on an error
+// nothing is enqueued.  See include/gdr2.h for the contract.
+
+#include "../../include/gdr2.h"
+
+#include <cmath>
+#include <cstdlib>
+
+#include "gdr2_kernels.hpp"
+
+using namespace gdr2;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+gdr2_status check_problem(const gdr2_problem* p, bool chunked) {
+  if (p == nullptr) return GDR2_EINVAL;
+  if (p->B <= 0 || p->T <= 0 || p->H <= 0 || p->Dk <= 0 || p->Dv <= 0) return GDR2_EINVAL;
+  if (!std::isfinite(p->scale)) return GDR2_EINVAL;
+  if (p->dtype != GDR2_BF16 && p->dtype != GDR2_FP32) return GDR2_EINVAL;
+  if ((p->Dk != 64 && p->Dk != 128) || (p->Dv != 64 && p->Dv != 128)) return GDR2_EUNSUPPORTED;
+  if (chunked) {
+    if (p->chunk != CH) return GDR2_EUNSUPPORTED;
+    if (p->T % CH != 0) return GDR2_EUNSUPPORTED;
+  }
+  const double rows = (double)p->B * (double)p->T * (double)p->H;
+  const int dmax = p->Dk > p->Dv ? p->Dk : p->Dv;
+  if (rows * dmax >= 2147483648.0) return GDR2_EUNSUPPORTED;
+  if ((double)p->B * p->H * (double)p->Dk * p->Dv >= 2147483648.0) return GDR2_EUNSUPPORTED;
+  return GDR2_OK;
+}
+
+// Workspace regions (fp32), chunk-head major: ch = (b*H + h)*NT + n.
+struct Layout {
+  size_t Y, U, Kt, Qg, Aqk, GC;          // forward tiles
+  size_t Hs, Rs, DH, DR, DAqk, DT, DEg;  // backward extras
+  size_t total;
+};
+
+Layout layout(const gdr2_problem* p, bool bwd) {
+  const size_t NC = (size_t)p->B * p->H * (size_t)(p->T / CH);
+  const size_t Dk = p->Dk, Dv = p->Dv;
+  Layout L{};
+  size_t off = 0;
+  auto take = [&](size_t floats) {
+    const size_t at = off;
+    off += round_up(floats * sizeof(float));
+    return at;
+  };
+  L.Y = take(NC * CH * Dk);
+  L.U = take(NC * CH * Dv);
+  L.Kt = take(NC * CH * Dk);
+  L.Qg = take(NC * CH * Dk);
+  L.Aqk = take(NC * CH * CH);
+  L.GC = take(NC * Dk);
+  if (bwd) {
+    L.Hs = take(NC * Dk * Dv);
+    L.Rs = take(NC * CH * Dv);
+    L.DH = take(NC * Dk * Dv);
+    L.DR = take(NC * CH * Dv);
+    L.DAqk = take(NC * CH * CH);
+    L.DT = take(NC * CH * CH);
+    L.DEg = take(NC * CH * Dk);
+  }
+  L.total = off;
+  return L;
+}
+
+template <typename T>
+T* at(void* ws, size_t off) {
+  return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
+}
+
+bool debug_sync() {
+  static const bool on = [] {
+    const char* e = std::getenv("GDR2_DEBUG_SYNC");
+    return e != nullptr && e[0] == '1';
+  }();
+  return on;
+}
+
+gdr2_status hip_status(hipError_t e, hipStream_t st) {
+  if (e != hipSuccess) return GDR2_EHIP;
+  if (debug_sync()) {
+    if (hipStreamSynchronize(st) != hipSuccess) return GDR2_EHIP;
+    if (hipGetLastError() != hipSuccess) return GDR2_EHIP;
+  }
+  return GDR2_OK;
+}
+
+// ---- dispatch over (Dk, Dv) ------------------------------------------------
+template <template <int, int, typename> class F, typename TIn, typename... A>
+hipError_t dispatch(int Dk, int Dv, A&&... args) {
+  if (Dk == 64 && Dv == 64) return F<64, 64, TIn>::run(args...);
+  if (Dk == 64 && Dv == 128) return F<64, 128, TIn>::run(args...);
+  if (Dk == 128 && Dv == 64) return F<128, 64, TIn>::run(args...);
+  return F<128, 128, TIn>::run(args...);
+}
+
+template <int DK, int DV, typename TIn>
+struct FwdRun {
+  static hipError_t run(const gdr2_problem* p, const void* q, const void* k, const void* v,
+                        const float* g, const void* b, const void* w, const float* S0, void* o,
+                        float* ST, void* ws, hipStream_t st) {
+    const Layout L = layout(p, false);
+    IntraArgs<TIn> ia{static_cast<const TIn*>(q), static_cast<const TIn*>(k),
+                      static_cast<const TIn*>(v), g, static_cast<const TIn*>(b),
+                      static_cast<const TIn*>(w), at<float>(ws, L.Y), at<float>(ws, L.U),
+                      at<float>(ws, L.Kt), at<float>(ws, L.Qg), at<float>(ws, L.Aqk),
+                      at<float>(ws, L.GC), p->T, p->H, p->T / CH};
+    hipError_t e = launch_fwd_intra<DK, DV, TIn>(ia, p->B, st);
+    if (e != hipSuccess) return e;
+    StateArgs<TIn> sa{ia.Y, ia.U, ia.Kt, ia.Qg, ia.Aqk, ia.GC, S0, ST, static_cast<TIn*>(o),
+                      nullptr, nullptr, p->T, p->H, p->T / CH, p->scale};
+    return launch_fwd_state<DK, DV, TIn, true, false>(sa, p->B, st);
+  }
+};
+
+template <int DK, int DV, typename TIn>
+struct BwdRun {
+  static hipError_t run(const gdr2_problem* p, const void* q, const void* k, const void* v,
+                        const float* g, const void* b, const void* w, const float* S0,
+                        const void* dout, const float* dST, void* dq, void* dk, void* dv,
+                        float* dg, void* db, void* dw, float* dS0, void* ws, hipStream_t st) {
+    const Layout L = layout(p, true);
+    const int NT = p->T / CH;
+    IntraArgs<TIn> ia{static_cast<const TIn*>(q), static_cast<const TIn*>(k),
+                      static_cast<const TIn*>(v), g, static_cast<const TIn*>(b),
+                      static_cast<const TIn*>(w), at<float>(ws, L.Y), at<float>(ws, L.U),
+                      at<float>(ws, L.Kt), at<float>(ws, L.Qg), at<float>(ws, L.Aqk),
+                      at<float>(ws, L.GC), p->T, p->H, NT};
+    hipError_t e = launch_fwd_intra<DK, DV, TIn>(ia, p->B, st);
+    if (e != hipSuccess) return e;
+    StateArgs<TIn> sa{ia.Y, ia.U, ia.Kt, ia.Qg, ia.Aqk, ia.GC, S0, nullptr, nullptr,
+                      at<float>(ws, L.Hs), at<float>(ws, L.Rs), p->T, p->H, NT, p->scale};
+    e = launch_fwd_state<DK, DV, TIn, false, true>(sa, p->B, st);
+    if (e != hipSuccess) return e;
+    BwdStateArgs<TIn> ba{ia.Qg, ia.Kt, ia.Y, ia.Aqk, ia.GC, static_cast<const TIn*>(dout), dST,
+                         dS0, at<float>(ws, L.DH), at<float>(ws, L.DR), p->T, p->H, NT, p->scale};
+    e = launch_bwd_state<DK, DV, TIn>(ba, p->B, st);
+    if (e != hipSuccess) return e;
+    BwdChunkArgs<TIn> ca{static_cast<const TIn*>(q), static_cast<const TIn*>(k),
+                         static_cast<const TIn*>(v), g, static_cast<const TIn*>(b),
+                         static_cast<const TIn*>(w), static_cast<const TIn*>(dout),
+                         sa.Hs, ba.DH, sa.Rs, ba.DR, at<float>(ws, L.DAqk), at<float>(ws, L.DT),
+                         at<float>(ws, L.DEg), static_cast<TIn*>(dq), static_cast<TIn*>(dk),
+                         static_cast<TIn*>(dv), static_cast<TIn*>(db), static_cast<TIn*>(dw), dg,
+                         p->T, p->H, NT, p->scale};
+    e = launch_bwd_wy<DK, DV, TIn>(ca, p->B, st);
+    if (e != hipSuccess) return e;
+    return launch_bwd_intra<DK, DV, TIn>(ca, p->B, st);
+  }
+};
+
+template <int DK, int DV, typename TIn>
+struct RecRun {
+  static hipError_t run(const gdr2_problem* p, const void* q, const void* k, const void* v,
+                        const float* g, const void* b, const void* w, float* S, void* o,
+                        hipStream_t st) {
+    RecurArgs<TIn> ra{static_cast<const TIn*>(q), static_cast<const TIn*>(k),
+                      static_cast<const TIn*>(v), g, static_cast<const TIn*>(b),
+                      static_cast<const TIn*>(w), S, static_cast<TIn*>(o), p->T, p->H, p->scale};
+    return launch_recurrent<DK, DV, TIn>(ra, p->B, st);
+  }
+};
+
+bool all_ok(std::initializer_list<const void*> req) {
+  for (const void* x : req)
+    if (x == nullptr || !aligned16(x)) return false;
+  return true;
+}
+
+bool opt_ok(std::initializer_list<const void*> opt) {
+  for (const void* x : opt)
+    if (x != nullptr && !aligned16(x)) return false;
+  return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+gdr2_status gdr2_chunk_workspace_bytes(const gdr2_problem* p, int for_backward, size_t* bytes) {
+  if (bytes == nullptr) return GDR2_EINVAL;
+  const gdr2_status s = check_problem(p, true);
+  if (s != GDR2_OK) return s;
+  *bytes = layout(p, for_backward != 0).total;
+  return GDR2_OK;
+}
+
+gdr2_status gdr2_chunk_fwd(const gdr2_problem* p, const void* q, const void* k, const void* v,
+                           const float* log_alpha, const void* b, const void* w, const float* S0,
+                           void* o, float* S_T, void* ws, size_t ws_bytes, hipStream_t stream) {
+  gdr2_status s = check_problem(p, true);
+  if (s != GDR2_OK) return s;
+  if (!all_ok({q, k, v, log_alpha, b, w, o, ws}) || !opt_ok({S0, S_T})) return GDR2_EINVAL;
+  if (ws_bytes < layout(p, false).total) return GDR2_EWORKSPACE;
+  hipError_t e;
+  if (p->dtype == GDR2_BF16)
+    e = dispatch<FwdRun, bf16_t>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S0, o, S_T, ws, stream);
+  else
+    e = dispatch<FwdRun, float>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S0, o, S_T, ws, stream);
+  return hip_status(e, stream);
+}
+
+gdr2_status gdr2_chunk_bwd(const gdr2_problem* p, const void* q, const void* k, const void* v,
+                           const float* log_alpha, const void* b, const void* w, const float* S0,
+                           const void* dout, const float* dS_T, void* dq, void* dk, void* dv,
+                           float* dlog_alpha, void* db, void* dw, float* dS0, void* ws,
+                           size_t ws_bytes, hipStream_t stream) {
+  gdr2_status s = check_problem(p, true);
+  if (s != GDR2_OK) return s;
+  if (!all_ok({q, k, v, log_alpha, b, w, dout, dq, dk, dv, dlog_alpha, db, dw, ws}) ||
+      !opt_ok({S0, dS_T, dS0}))
+    return GDR2_EINVAL;
+  if (ws_bytes < layout(p, true).total) return GDR2_EWORKSPACE;
+  hipError_t e;
+  if (p->dtype == GDR2_BF16)
+    e = dispatch<BwdRun, bf16_t>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S0, dout, dS_T, dq,
+                                 dk, dv, dlog_alpha, db, dw, dS0, ws, stream);
+  else
+    e = dispatch<BwdRun, float>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S0, dout, dS_T, dq,
+                                dk, dv, dlog_alpha, db, dw, dS0, ws, stream);
+  return hip_status(e, stream);
+}
+
+gdr2_status gdr2_recurrent_step(const gdr2_problem* p, const void* q, const void* k, const void* v,
+                                const float* log_alpha, const void* b, const void* w, float* S,
+                                void* o, hipStream_t stream) {
+  gdr2_status s = check_problem(p, false);
+  if (s != GDR2_OK) return s;
+  if (!all_ok({q, k, v, log_alpha, b, w, S, o})) return GDR2_EINVAL;
+  hipError_t e;
+  if (p->dtype == GDR2_BF16)
+    e = dispatch<RecRun, bf16_t>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S, o, stream);
+  else
+    e = dispatch<RecRun, float>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S, o, stream);
+  return hip_status(e, stream);
+}
+
+const char* gdr2_status_str(gdr2_status st) {
+  switch (st) {
+    case GDR2_OK: return "GDR2_OK";
+    case GDR2_EINVAL: return "GDR2_EINVAL: invalid argument";
+    case GDR2_EUNSUPPORTED: return "GDR2_EUNSUPPORTED: unsupported problem";
+    case GDR2_EWORKSPACE: return "GDR2_EWORKSPACE: workspace too small";
+    case GDR2_EHIP: return "GDR2_EHIP: HIP launch error";
+  }
+  return "GDR2_UNKNOWN";
+}
+
+}  // extern "C"

@@ -1,0 +1,110 @@
+// Recurrent (token-by-token) GDR-2 forward for decoding, App. C.5.
+//
+// One workgroup per (batch, head).  The fp32 state (DK x DV) stays in registers
+// for all T tokens of the call: each thread owns RPG rows x 4 columns.  Per token
+//     Sbar = Diag(exp g) S,  r = Sbar^T (b*k),  S = Sbar + k (w*v - r)^T,
+//     o    = scale * S^T q = scale * (Sbar^T q + (w*v - r) (k . q)),
+// so S is read and written once per call; the column sums r and Sbar^T q are
+// reduced across the row groups through LDS in a fixed order.
+
+#include "gdr2_kernels.hpp"
+
+namespace gdr2 {
+
+template <int DK, int DV, typename TIn>
+__global__ __launch_bounds__(256) void recurrent_kernel(RecurArgs<TIn> a) {
+  constexpr int NTHR = 256;
+  constexpr int CG = DV / 4;        // column groups of 4
+  constexpr int RG = NTHR / CG;     // row groups
+  constexpr int RPG = DK / RG;      // rows per thread
+  static_assert(NTHR % CG == 0 && DK % RG == 0, "thread split");
+  const int seq = blockIdx.x;
+  const int bb = seq / a.H, h = seq % a.H;
+  const int tid = threadIdx.x, cg = tid % CG, rg = tid / CG;
+  const int T = a.T, H = a.H;
+
+  __shared__ float sAl[DK], sE[DK], sK[DK], sQ[DK], sZ[DV];
+  __shared__ float redR[RG * DV], redP[RG * DV];
+  __shared__ float sRes[DV], sP[DV];
+  __shared__ float sKQ[NTHR / 64];
+
+  float* Sg = a.S + (size_t)seq * DK * DV;
+  float4 S[RPG];
+#pragma unroll
+  for (int i = 0; i < RPG; ++i) S[i] = ld4(Sg + (rg * RPG + i) * DV + 4 * cg);
+
+  for (int t = 0; t < T; ++t) {
+    const size_t row = ((size_t)bb * T + t) * H + h;
+    float kq = 0.f;
+    for (int c = tid; c < DK; c += NTHR) {
+      const float kv = to_f(a.k[row * DK + c]), qv = to_f(a.q[row * DK + c]);
+      sAl[c] = expf(a.g[row * DK + c]);
+      sK[c] = kv;
+      sQ[c] = qv;
+      sE[c] = to_f(a.b[row * DK + c]) * kv;
+      kq += kv * qv;
+    }
+    for (int v = tid; v < DV; v += NTHR) sZ[v] = to_f(a.w[row * DV + v]) * to_f(a.v[row * DV + v]);
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) kq += __shfl_xor(kq, m);
+    if ((tid & 63) == 0) sKQ[tid >> 6] = kq;
+    __syncthreads();
+
+    float4 pr = make_float4(0.f, 0.f, 0.f, 0.f), pp = pr;
+#pragma unroll
+    for (int i = 0; i < RPG; ++i) {
+      const int c = rg * RPG + i;
+      const float al = sAl[c], e = sE[c], q = sQ[c];
+      S[i].x *= al; S[i].y *= al; S[i].z *= al; S[i].w *= al;
+      pr.x += S[i].x * e; pr.y += S[i].y * e; pr.z += S[i].z * e; pr.w += S[i].w * e;
+      pp.x += S[i].x * q; pp.y += S[i].y * q; pp.z += S[i].z * q; pp.w += S[i].w * q;
+    }
+    *reinterpret_cast<float4*>(redR + rg * DV + 4 * cg) = pr;
+    *reinterpret_cast<float4*>(redP + rg * DV + 4 * cg) = pp;
+    __syncthreads();
+    for (int v = tid; v < DV; v += NTHR) {
+      float r = 0.f, p = 0.f;
+      for (int g2 = 0; g2 < RG; ++g2) {
+        r += redR[g2 * DV + v];
+        p += redP[g2 * DV + v];
+      }
+      const float res = sZ[v] - r;
+      sRes[v] = res;
+      sP[v] = p;
+    }
+    __syncthreads();
+    float kqa = 0.f;
+#pragma unroll
+    for (int w2 = 0; w2 < NTHR / 64; ++w2) kqa += sKQ[w2];
+    const float4 res = ld4(sRes + 4 * cg);
+#pragma unroll
+    for (int i = 0; i < RPG; ++i) {
+      const float kc = sK[rg * RPG + i];
+      S[i].x += kc * res.x; S[i].y += kc * res.y; S[i].z += kc * res.z; S[i].w += kc * res.w;
+    }
+    for (int v = tid; v < DV; v += NTHR) put(a.o + row * DV + v, a.scale * (sP[v] + sRes[v] * kqa));
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < RPG; ++i) *reinterpret_cast<float4*>(Sg + (rg * RPG + i) * DV + 4 * cg) = S[i];
+}
+
+template <int DK, int DV, typename TIn>
+hipError_t launch_recurrent(const RecurArgs<TIn>& a, int B, hipStream_t st) {
+  hipLaunchKernelGGL((recurrent_kernel<DK, DV, TIn>), dim3(B * a.H), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+#define GDR2_INST_REC(DK, DV, TIN) \
+  template hipError_t launch_recurrent<DK, DV, TIN>(const RecurArgs<TIN>&, int, hipStream_t);
+
+GDR2_INST_REC(64, 64, float)
+GDR2_INST_REC(64, 128, float)
+GDR2_INST_REC(128, 64, float)
+GDR2_INST_REC(128, 128, float)
+GDR2_INST_REC(64, 64, bf16_t)
+GDR2_INST_REC(64, 128, bf16_t)
+GDR2_INST_REC(128, 64, bf16_t)
+GDR2_INST_REC(128, 128, bf16_t)
+
+}  // namespace gdr2

@@ -1,0 +1,166 @@
+"""C-ABI checks that need no GPU: exports, argument validation, workspace sizes.
+
+Every call here is rejected by validation, which the library performs before
+any HIP call, so the (fake, never dereferenced) pointers are safe.
+"""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2605_22791_amd as g2
+from paper_2605_22791_amd.inputs import bf16_round, CONFIGS, config
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gdr2.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(g2.lib_path()),
+                                reason="libgdr2.so not built (python -m paper_2605_22791_amd.build)")
+
+FAKE = 0x10000  # 16-byte aligned, never dereferenced
+
+
+def _declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:gdr2_status|const char\*)\s+(gdr2_\w+)\s*\(", text, re.M)))
+
+
+def test_header_declares_the_entry_points():
+    assert _declared_symbols() == sorted(["gdr2_chunk_workspace_bytes", "gdr2_chunk_fwd",
+                                          "gdr2_chunk_bwd", "gdr2_recurrent_step",
+                                          "gdr2_status_str"])
+
+
+def test_library_exports_every_declared_symbol():
+    L = g2.lib()
+    for name in _declared_symbols():
+        assert hasattr(L, name), name
+
+
+def test_status_strings():
+    for code in range(5):
+        s = g2.gdr2_status_str(code)
+        assert s.startswith("GDR2_")
+    assert g2.gdr2_status_str(99) == "GDR2_UNKNOWN"
+
+
+def _prob(**kw):
+    d = dict(B=2, T=128, H=4, Dk=128, Dv=128, chunk=64, scale=128 ** -0.5, dtype=g2.GDR2_BF16)
+    d.update(kw)
+    return g2.Gdr2Problem(**d)
+
+
+def _fwd(prob, q=FAKE, ws_bytes=None, S0=None, ptrs=None):
+    L = g2.lib()
+    p = [q, FAKE, FAKE, FAKE, FAKE, FAKE, S0, FAKE, None, FAKE]
+    if ptrs:
+        for i, val in ptrs.items():
+            p[i] = val
+    n = ws_bytes if ws_bytes is not None else (1 << 40)
+    pp = ctypes.byref(prob) if prob is not None else None
+    return L.gdr2_chunk_fwd(pp, *[ctypes.c_void_p(x) if x else None for x in p], n, None)
+
+
+def _bwd(prob, ws_bytes=None, ptrs=None):
+    L = g2.lib()
+    p = [FAKE] * 6 + [None, FAKE, None] + [FAKE] * 6 + [None, FAKE]
+    if ptrs:
+        for i, val in ptrs.items():
+            p[i] = val
+    n = ws_bytes if ws_bytes is not None else (1 << 40)
+    return L.gdr2_chunk_bwd(ctypes.byref(prob), *[ctypes.c_void_p(x) if x else None for x in p], n, None)
+
+
+def _rec(prob, ptrs=None):
+    L = g2.lib()
+    p = [FAKE] * 8
+    if ptrs:
+        for i, val in ptrs.items():
+            p[i] = val
+    return L.gdr2_recurrent_step(ctypes.byref(prob), *[ctypes.c_void_p(x) if x else None for x in p], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(B=0), g2.GDR2_EINVAL), (dict(T=-64), g2.GDR2_EINVAL), (dict(H=0), g2.GDR2_EINVAL),
+    (dict(Dk=0), g2.GDR2_EINVAL), (dict(scale=float("nan")), g2.GDR2_EINVAL),
+    (dict(scale=float("inf")), g2.GDR2_EINVAL), (dict(dtype=7), g2.GDR2_EINVAL),
+    (dict(Dk=96), g2.GDR2_EUNSUPPORTED), (dict(Dv=256), g2.GDR2_EUNSUPPORTED),
+    (dict(chunk=32), g2.GDR2_EUNSUPPORTED), (dict(T=100), g2.GDR2_EUNSUPPORTED),
+    (dict(B=1 << 20, T=1 << 16), g2.GDR2_EUNSUPPORTED),
+])
+def test_problem_validation(kw, code):
+    assert _fwd(_prob(**kw)) == code
+    assert _bwd(_prob(**kw)) == code
+    n = ctypes.c_size_t(0)
+    assert g2.lib().gdr2_chunk_workspace_bytes(ctypes.byref(_prob(**kw)), 0, ctypes.byref(n)) == code
+
+
+def test_null_problem_and_null_out_size():
+    assert _fwd(None) == g2.GDR2_EINVAL
+    assert g2.lib().gdr2_chunk_workspace_bytes(ctypes.byref(_prob()), 0, None) == g2.GDR2_EINVAL
+
+
+@pytest.mark.parametrize("idx", range(10))
+def test_forward_pointer_checks(idx):
+    # required pointers: q k v log_alpha b w (0-5), o (7), ws (9); S0 (6) and S_T (8) optional
+    if idx in (6, 8):
+        assert _fwd(_prob(), ptrs={idx: FAKE + 4}) == g2.GDR2_EINVAL   # misaligned optional
+        return
+    assert _fwd(_prob(), ptrs={idx: None}) == g2.GDR2_EINVAL
+    assert _fwd(_prob(), ptrs={idx: FAKE + 8}) == g2.GDR2_EINVAL
+
+
+def test_backward_pointer_checks():
+    required = [0, 1, 2, 3, 4, 5, 7, 9, 10, 11, 12, 13, 14, 16]
+    for idx in required:
+        assert _bwd(_prob(), ptrs={idx: None}) == g2.GDR2_EINVAL, idx
+    for idx in (6, 8, 15):
+        assert _bwd(_prob(), ptrs={idx: FAKE + 4}) == g2.GDR2_EINVAL, idx
+
+
+def test_recurrent_validation():
+    assert _rec(_prob(B=0)) == g2.GDR2_EINVAL
+    assert _rec(_prob(Dk=32)) == g2.GDR2_EUNSUPPORTED
+    for idx in range(8):
+        assert _rec(_prob(T=1), ptrs={idx: None}) == g2.GDR2_EINVAL
+
+
+def test_workspace_size_and_check():
+    p = _prob(B=2, T=256, H=4, Dk=128, Dv=64)
+    fwd = g2.gdr2_chunk_workspace_bytes(p, 0)
+    bwd = g2.gdr2_chunk_workspace_bytes(p, 1)
+    NC = 2 * 4 * (256 // 64)
+    r = lambda n: (n * 4 + 255) // 256 * 256
+    exp_fwd = r(NC * 64 * 128) + r(NC * 64 * 64) + 2 * r(NC * 64 * 128) + r(NC * 64 * 64) + r(NC * 128)
+    exp_bwd = exp_fwd + 2 * r(NC * 128 * 64) + 2 * r(NC * 64 * 64) + 2 * r(NC * 64 * 64) + r(NC * 64 * 128)
+    assert fwd == exp_fwd and bwd == exp_bwd
+    assert _fwd(p, ws_bytes=fwd - 1) == g2.GDR2_EWORKSPACE
+    assert _bwd(p, ws_bytes=bwd - 1) == g2.GDR2_EWORKSPACE
+    assert _bwd(p, ws_bytes=fwd) == g2.GDR2_EWORKSPACE
+
+
+def test_bf16_round_is_nearest_even():
+    x = np.array([1.0, 1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, 1.0 + 2 ** -9, -2.5, 3.14159], dtype=np.float32)
+    y = bf16_round(x)
+    assert y[0] == 1.0
+    assert y[1] == 1.0                  # tie -> even (mantissa 0)
+    assert y[2] == 1.0 + 4 * 2 ** -8    # tie -> even (rounds up)
+    assert y[3] == 1.0
+    assert y[4] == -2.5
+    assert abs(y[5] - 3.140625) < 1e-7
+    assert np.all((y.view(np.uint32) & 0xFFFF) == 0)
+
+
+def test_input_recipes():
+    d0 = config(0)
+    assert d0["q"].shape == (1, 256, 2, 64) and d0["dtype"] == "fp32" and d0["S0"] is None
+    assert np.allclose(np.linalg.norm(d0["k"], axis=-1), 1.0, atol=1e-6)
+    assert np.all(d0["log_alpha"] <= 0) and np.all((d0["b"] > 0) & (d0["b"] < 1))
+    d1 = config(1, decay="scalar", T=128)
+    assert np.all(d1["b"] == d1["b"][..., :1]) and np.all(d1["w"][..., :1] == d1["b"][..., :1])
+    assert np.all(d1["log_alpha"] == d1["log_alpha"][..., :1])
+    assert np.all((d1["q"].view(np.uint32) & 0xFFFF) == 0)
+    assert set(CONFIGS) == {0, 1, 2, 3, 4}

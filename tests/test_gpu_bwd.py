@@ -1,0 +1,136 @@
+"""GPU parity of the gate-aware chunkwise backward against the fp64 adjoint.
+
+All seven gradients (dq, dk, dv, dlog_alpha, db, dw, dS0) are compared per
+tensor by rel-L2: 1e-5 in fp32 mode, 2e-3 for bf16 problems (dlog_alpha and
+dS0 are fp32 tensors but belong to a bf16 call and share its bound).
+"""
+
+import numpy as np
+import pytest
+
+from oracle import gdr2_recurrent_bwd, gdr2_chunk_bwd_ref
+from paper_2605_22791_amd.inputs import config, make_inputs
+from tests.helpers import rel_l2
+from tests.gpu_common import dev_inputs, host, heads, pick, ws_layout, ws_view, CH
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"fp32": 1e-5, "bf16": 2e-3}
+NAMES = [("dq", "dq"), ("dk", "dk"), ("dv", "dv"), ("dlog_alpha", "dg"), ("db", "db"), ("dw", "dw")]
+
+
+def _case(msg):
+    print(f"\n[gpu case] {msg}", flush=True)
+
+
+def _run_bwd(d, ws=None):
+    import paper_2605_22791_amd as g2
+    x = dev_inputs(d)
+    g = g2.gdr2_chunk_bwd(x["q"], x["k"], x["v"], x["log_alpha"], x["b"], x["w"], x["S0"], x["do"],
+                          x["dST"], scale=d["scale"], ws=ws)
+    return {n: host(t) for n, t in g.items()}
+
+
+def _adjoint(d):
+    return gdr2_recurrent_bwd(d["q"], d["k"], d["v"], d["log_alpha"], d["b"], d["w"], d["S0"], d["do"],
+                              d["dST"], d["scale"])
+
+
+def _compare(got, ref, tol, pairs=None):
+    worst = {}
+    for gn, rn in NAMES:
+        x = got[gn] if pairs is None else pick(got[gn], pairs)
+        worst[gn] = rel_l2(x, ref[rn])
+    x = got["dS0"] if pairs is None else pick(got["dS0"], pairs, state=True)
+    worst["dS0"] = rel_l2(x, ref["dS0"])
+    print({k: f"{v:.2e}" for k, v in worst.items()})
+    for k, v in worst.items():
+        assert v < tol, (k, v)
+
+
+@pytest.mark.parametrize("Dk,Dv", [(64, 64), (128, 128), (64, 128), (128, 64)])
+def test_fp32_backward_small(Dk, Dv):
+    d = make_inputs(1, 256, 2, Dk, Dv, seed=60 + Dk + Dv, dtype="fp32", s0_std=0.05, with_dST=True)
+    _case(f"fp32 bwd B1 H2 T256 Dk{Dk} Dv{Dv} with S0 and dS_T")
+    got = _run_bwd(d)
+    _compare(got, _adjoint(d), TOL["fp32"])
+
+
+def test_fp32_backward_workspace_intermediates():
+    """dA_qk, dT and the chunk states against App. B's chunk equations (scaled dO)."""
+    import torch
+    d = make_inputs(1, 192, 1, 64, 64, seed=61, dtype="fp32", s0_std=0.1, with_dST=True)
+    B, T, H, Dk, Dv = 1, 192, 1, 64, 64
+    lay, total = ws_layout(B, T, H, Dk, Dv, True)
+    ws = torch.full((total,), 0xFF, dtype=torch.uint8, device="cuda")
+    _case("fp32 bwd workspace intermediates")
+    _run_bwd(d, ws=ws)
+    torch.cuda.synchronize()
+    NT = T // CH
+    from oracle.chunkwise import gdr2_chunk_fwd_ref
+    _, _, it = gdr2_chunk_fwd_ref(d["q"], d["k"], d["v"], d["log_alpha"], d["b"], d["w"], d["S0"],
+                                  d["scale"], C=CH, keep=True)
+    Hs = host(ws_view(ws, lay, "Hs", (B, H, NT, Dk, Dv)))
+    Rs = host(ws_view(ws, lay, "Rs", (B, H, NT, CH, Dv)))
+    assert rel_l2(Hs, it["h"]) < TOL["fp32"] and rel_l2(Rs, it["R"]) < TOL["fp32"]
+    dAqk = host(ws_view(ws, lay, "DAqk", (B, H, NT, CH, CH)))
+    dO = d["scale"] * d["do"].astype(np.float64)
+    for n in range(NT):
+        ref = np.tril(dO[0, n * CH:(n + 1) * CH, 0] @ it["R"][0, 0, n].T)
+        assert rel_l2(dAqk[0, 0, n], ref) < TOL["fp32"]
+
+
+@pytest.mark.parametrize("decay", ["channel", "scalar"])
+def test_config1_bf16_backward_kda_gdn_limits(decay):
+    d = config(1, decay=decay)
+    _case(f"config1 bf16 bwd, tied gates, {decay} decay")
+    got = _run_bwd(d)
+    ref = _adjoint(d)
+    _compare(got, ref, TOL["bf16"])
+    # tied-gate identity on the GPU result: sum_c db + sum_c dw = dL/dbeta of the adjoint
+    dbeta = got["db"].sum(-1) + got["dw"].sum(-1)
+    dbeta_ref = ref["db"].sum(-1) + ref["dw"].sum(-1)
+    assert rel_l2(dbeta, dbeta_ref) < TOL["bf16"]
+
+
+def test_backward_determinism_and_poisoned_outputs():
+    import torch
+    import paper_2605_22791_amd as g2
+    d = make_inputs(2, 256, 2, 128, 128, seed=62, dtype="bf16", s0_std=0.02, with_dST=True)
+    _case("bwd determinism / poisoned outputs")
+    x = dev_inputs(d)
+    res = []
+    for _ in range(2):
+        grads = {n: torch.full_like(x[src], float("nan")) for n, src in
+                 [("dq", "q"), ("dk", "k"), ("dv", "v"), ("dlog_alpha", "log_alpha"), ("db", "b"), ("dw", "w")]}
+        grads["dS0"] = torch.full_like(x["S0"], float("nan"))
+        g = g2.gdr2_chunk_bwd(x["q"], x["k"], x["v"], x["log_alpha"], x["b"], x["w"], x["S0"], x["do"],
+                              x["dST"], scale=d["scale"], grads=grads)
+        res.append({n: t.clone() for n, t in g.items()})
+    for n in res[0]:
+        assert torch.isfinite(res[0][n].float()).all(), n
+        assert torch.equal(res[0][n], res[1][n]), n
+
+
+def test_extreme_decay_backward():
+    d = make_inputs(1, 128, 2, 64, 64, seed=63, dtype="fp32", s0_std=0.1, with_dST=True)
+    la = d["log_alpha"].copy()
+    la[0, 20, 0, :8] = -90.0
+    la[0, 70, 1, 5:40] = -200.0
+    d["log_alpha"] = la
+    _case("bwd extreme decay spike")
+    got = _run_bwd(d)
+    _compare(got, _adjoint(d), TOL["fp32"])
+
+
+def test_config2_full_size_backward_sampled_heads():
+    d = config(2)
+    pairs = [(0, 0), (5, 11)]
+    _case("config2 bwd full size; adjoint on 2 heads")
+    got = _run_bwd(d)
+    for n, t in got.items():
+        assert np.all(np.isfinite(t)), n
+    sub = heads(d, pairs)
+    ref = gdr2_recurrent_bwd(sub["q"], sub["k"], sub["v"], sub["log_alpha"], sub["b"], sub["w"], None,
+                             sub["do"], None, d["scale"])
+    _compare(got, ref, TOL["bf16"], pairs=pairs)
