@@ -1,0 +1,245 @@
+"""Throughput of the chunkwise GDR-2 operator (forward + gate-aware backward) on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-decode]
+
+One step = gdr2_chunk_fwd + gdr2_chunk_bwd over one batch of the 1.3B-layer
+training shape (B=8, H=16, T=4096, d_k=d_v=128, bf16 inputs, fp32 log-decay
+and state), inputs resident in HBM before the timed region.  Prints one JSON
+line with tokens/s (B*T per step over the K timed steps), the roofline of the
+dominant kernel (per-kernel durations from hipEvents recorded on the launch
+stream during the timed steps) and the CPU oracle timed on a bounded sample.
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+HBM_PEAK_GBS = 8000.0                    # MI355X HBM3E, GB/s
+PEAK_TFLOPS = {"fp32": 157.3, "bf16": 2500.0}
+MFMA_DTYPE = "fp32"                      # the kernels' MFMA operand type (v_mfma_f32_16x16x4_f32)
+
+
+def kernel_model(B, T, H, Dk, Dv, es):
+    """Algorithmic flops and HBM bytes per launch of each kernel.
+
+    Per chunk-head (C = 64 tokens of one head), causal triangles counted at
+    half; bytes are each kernel's inputs read once plus outputs written once
+    (es = bytes per element of q/k/v/b/w/o and their gradients; log-decay,
+    states and workspace tiles are fp32).
+    """
+    C = 64
+    NC = B * H * (T // C)
+    f = 4
+    tri = C * C * Dk           # a causal C x C x Dk product: C^2/2 * Dk * 2 flops
+    triv = C * C * Dv
+    kin = C * Dk * es          # one (C x Dk) input tile
+    vin = C * Dv * es
+    kf = C * Dk * f            # one (C x Dk) fp32 tile
+    vf = C * Dv * f
+    st = Dk * Dv * f           # one fp32 state
+    aq = C * C * f             # one fp32 C x C tile
+    solve = C ** 3 / 3
+    m = {}
+    m["fwd_intra"] = (tri + tri + solve + tri + triv,
+                      3 * kin + kf + 2 * vin + 3 * kf + vf + aq + Dk * f)
+    m["fwd_state"] = (2 * C * Dk * Dv * 3 + triv,
+                      3 * kf + vf + aq + Dk * f + vin)
+    m["bwd_recompute_intra"] = m["fwd_intra"]
+    m["bwd_recompute_state"] = (2 * C * Dk * Dv * 2,
+                                2 * kf + vf + Dk * f + st + vf)
+    m["bwd_state"] = (triv + 2 * C * Dk * Dv * 3,
+                      3 * kf + aq + Dk * f + vin + st + vf)
+    m["bwd_wy"] = (tri + solve + triv + 2 * C * Dk * Dv + triv + tri + triv + tri + 2 * solve * 2,
+                   2 * kin + kf + 3 * vin + 2 * vf + st + 2 * vin + 2 * aq + kf)
+    m["bwd_intra"] = (tri + tri + 2 * tri + 2 * 2 * C * Dk * Dv + 2 * Dk * Dv,
+                      3 * kin + kf + vin + 2 * st + vf + 2 * aq + kf + 3 * kin + kf)
+    return {k: (fl * NC, by * NC) for k, (fl, by) in m.items()}
+
+
+def _cpu_worker(args):
+    """Oracle forward + adjoint on one head (runs in a spawned process)."""
+    import numpy as np
+    from oracle import gdr2_recurrent_fwd, gdr2_recurrent_bwd
+    q, k, v, la, b, w, do, scale = args
+    gdr2_recurrent_fwd(q, k, v, la, b, w, None, scale)
+    gdr2_recurrent_bwd(q, k, v, la, b, w, None, do, None, scale)
+    return True
+
+
+def cpu_baseline(d, heads_sample):
+    """Time the oracle (fwd + bwd) on batch row 0, first `heads_sample` heads, full T."""
+    import multiprocessing as mp
+    try:
+        ncores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        ncores = os.cpu_count() or 1
+    workers = max(1, min(16, ncores, heads_sample))
+    jobs = [(d["q"][0:1, :, h:h + 1], d["k"][0:1, :, h:h + 1], d["v"][0:1, :, h:h + 1],
+             d["log_alpha"][0:1, :, h:h + 1], d["b"][0:1, :, h:h + 1], d["w"][0:1, :, h:h + 1],
+             d["do"][0:1, :, h:h + 1], d["scale"]) for h in range(heads_sample)]
+    env_keep = {k: os.environ.get(k) for k in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS")}
+    for k in env_keep:
+        os.environ[k] = "1"
+    ctx = mp.get_context("spawn")
+    with ctx.Pool(workers) as pool:
+        pool.map(_cpu_worker, jobs[:1])           # warm the workers' imports
+        t0 = time.perf_counter()
+        pool.map(_cpu_worker, jobs, chunksize=1)
+        wall = time.perf_counter() - t0
+    for k, v in env_keep.items():
+        if v is None:
+            os.environ.pop(k, None)
+        else:
+            os.environ[k] = v
+    H = d["H"]
+    tokens = d["T"] * heads_sample / H           # token = one (b, t) position across all H heads
+    return {"value": tokens / wall, "unit": "tokens/s", "cores": workers, "kind": "oracle",
+            "sample": f"fp64 numpy token recurrence + adjoint, batch row 0, {heads_sample} of {H} heads, "
+                      f"T={d['T']} (= {tokens:.0f} tokens of the workload), {workers} single-threaded workers",
+            "wall_s": wall}
+
+
+def decode_bench(steps, B=256, H=16, D=128):
+    """Decode: one-token recurrent calls on a 256 MiB fp32 state (synthetic inputs drawn on the GPU)."""
+    import torch
+    import paper_2605_22791_amd as g2
+    gen = torch.Generator(device="cuda").manual_seed(4)
+    n = lambda *s: torch.randn(*s, device="cuda", generator=gen)
+    q = torch.nn.functional.normalize(n(steps, B, 1, H, D), dim=-1).bfloat16()
+    k = torch.nn.functional.normalize(n(steps, B, 1, H, D), dim=-1).bfloat16()
+    v = n(steps, B, 1, H, D).bfloat16()
+    la = -torch.nn.functional.softplus(n(steps, B, 1, H, D) - 2.0)
+    b = torch.sigmoid(n(steps, B, 1, H, D)).bfloat16()
+    w = torch.sigmoid(n(steps, B, 1, H, D)).bfloat16()
+    S = torch.zeros(B, H, D, D, device="cuda")
+    o = torch.empty(B, 1, H, D, device="cuda", dtype=torch.bfloat16)
+    for t in range(min(8, steps)):
+        g2.gdr2_recurrent_step(q[t], k[t], v[t], la[t], b[t], w[t], S, o=o)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for t in range(steps):
+        g2.gdr2_recurrent_step(q[t], k[t], v[t], la[t], b[t], w[t], S, o=o)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    bytes_step = B * H * (2 * D * D * 4 + 5 * D * 2 + D * 4 + D * 2)
+    return {"steps_per_s": 1000.0 / ms, "us_per_step": ms * 1000.0,
+            "hbm_GBs": bytes_step / (ms * 1e-3) / 1e9, "hbm_frac": bytes_step / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "config": {"B": B, "H": H, "d": D, "steps": steps}}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--cpu-heads", type=int, default=16)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2605_22791_amd as g2
+    from paper_2605_22791_amd.inputs import config
+
+    print("[bench] generating config-2 inputs", file=sys.stderr, flush=True)
+    d = config(2)
+    B, T, H, Dk, Dv = d["B"], d["T"], d["H"], d["Dk"], d["Dv"]
+    dev = "cuda"
+    tb = lambda x: torch.from_numpy(x).to(dev).to(torch.bfloat16).contiguous()
+    q, k, v, b, w, do = (tb(d[n]) for n in ("q", "k", "v", "b", "w", "do"))
+    la = torch.from_numpy(d["log_alpha"]).to(dev).contiguous()
+    o = torch.empty_like(v)
+    ST = torch.empty(B, H, Dk, Dv, device=dev)
+    grads = {"dq": torch.empty_like(q), "dk": torch.empty_like(k), "dv": torch.empty_like(v),
+             "dlog_alpha": torch.empty_like(la), "db": torch.empty_like(b), "dw": torch.empty_like(w),
+             "dS0": torch.empty(B, H, Dk, Dv, device=dev)}
+    prob = g2.Gdr2Problem(B, T, H, Dk, Dv, 64, d["scale"], g2.GDR2_BF16)
+    ws = torch.empty(g2.gdr2_chunk_workspace_bytes(prob, 1), dtype=torch.uint8, device=dev)
+
+    def step():
+        g2.gdr2_chunk_fwd(q, k, v, la, b, w, None, scale=d["scale"], o=o, S_T=ST, ws=ws)
+        g2.gdr2_chunk_bwd(q, k, v, la, b, w, None, do, None, scale=d["scale"], grads=grads, ws=ws)
+
+    print("[bench] warmup", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # timed region: K steps, per-kernel hipEvents recorded on the launch stream
+    g2.gdr2_profile_enable(True)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_kernel = g2.gdr2_profile_collect()
+    g2.gdr2_profile_enable(False)
+    ms_total = e0.elapsed_time(e1)
+    ms_step = ms_total / args.steps
+    tokens_per_s = B * T / (ms_step * 1e-3)
+    print(f"[bench] {ms_step:.3f} ms/step ({wall / args.steps * 1e3:.3f} ms wall)", file=sys.stderr, flush=True)
+
+    model = kernel_model(B, T, H, Dk, Dv, 2)
+    kern = {}
+    for name, (ms, cnt) in per_kernel.items():
+        if cnt == 0:
+            continue
+        avg = ms / cnt
+        fl, by = model[name]
+        kern[name] = {"avg_us": avg * 1e3, "launches": cnt, "GBs": by / (avg * 1e-3) / 1e9,
+                      "TFLOPs": fl / (avg * 1e-3) / 1e12, "alg_bytes": by, "alg_flops": fl}
+    dom = max(kern, key=lambda n: kern[n]["avg_us"] * kern[n]["launches"])
+    kd = kern[dom]
+    peak_fl = PEAK_TFLOPS[MFMA_DTYPE]
+    ridge = peak_fl * 1e12 / (HBM_PEAK_GBS * 1e9)
+    ai = kd["alg_flops"] / kd["alg_bytes"]
+    if ai >= ridge:
+        roof = {"bound": "mfma", "achieved": kd["TFLOPs"], "peak": peak_fl, "unit": "TFLOP/s",
+                "frac": kd["TFLOPs"] / peak_fl}
+    else:
+        roof = {"bound": "hbm", "achieved": kd["GBs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": kd["GBs"] / HBM_PEAK_GBS}
+    roof.update({"kernel": dom, "avg_us": kd["avg_us"], "traffic": None,
+                 "mfma_dtype": MFMA_DTYPE, "arith_intensity": ai, "ridge": ridge})
+
+    fwd_flops = sum(model[n][0] for n in ("fwd_intra", "fwd_state"))
+    step_flops = sum(model[n][0] for n in model)
+    out = {
+        "metric": "tokens/s fwd+bwd GDR-2 chunked op (H=16,d=128,T=4096,bf16); % MFMA peak",
+        "value": tokens_per_s, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "GDR-2 chunkwise fwd+bwd, 1.3B-layer training shape",
+                   "B": B, "H": H, "T": T, "d_k": Dk, "d_v": Dv, "chunk": 64, "io": "bf16",
+                   "log_alpha": "fp32", "state": "fp32", "global_batch": B, "seq_len": T},
+        "mfma_pct_of_bf16_peak": 100.0 * step_flops / (ms_step * 1e-3) / 1e12 / PEAK_TFLOPS["bf16"],
+        "roofline": roof,
+        "kernels": {n: {kk: (round(vv, 3) if isinstance(vv, float) else vv) for kk, vv in kv.items()}
+                    for n, kv in kern.items()},
+        "fwd_ms": sum(kern[n]["avg_us"] for n in ("fwd_intra", "fwd_state") if n in kern) / 1e3,
+        "bwd_ms": sum(kern[n]["avg_us"] for n in kern if n.startswith("bwd")) / 1e3,
+        "alg_tflops_per_step": step_flops / 1e12, "fwd_alg_tflops": fwd_flops / 1e12,
+    }
+    if not args.no_decode:
+        print("[bench] decode", file=sys.stderr, flush=True)
+        out["decode"] = decode_bench(64)
+    if not args.no_cpu:
+        print("[bench] cpu oracle baseline", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(d, args.cpu_heads)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

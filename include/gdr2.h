@@ -28,9 +28,10 @@
  * kernels accumulates in fp32.
  *
  * Ownership and errors:
- *   * The caller owns every buffer; the library never allocates or frees and
- *     keeps no mutable global state, so calls are re-entrant.  Work is
- *     enqueued on `stream` and the call returns without waiting.
+ *   * The caller owns every buffer; the library never allocates device memory
+ *     and keeps no mutable global state (apart from the opt-in, per-thread
+ *     kernel timing at the end of this header), so calls are re-entrant.
+ *     Work is enqueued on `stream` and the call returns without waiting.
  *   * Outputs are overwritten, never accumulated.  Workspace contents are
  *     undefined after a call.  Inputs and outputs must not alias (except S in
  *     gdr2_recurrent_step, which is updated in place).
@@ -122,6 +123,29 @@ gdr2_status gdr2_recurrent_step(const gdr2_problem* problem, const void* q, cons
 
 /* Static, human-readable name of a status code. */
 const char* gdr2_status_str(gdr2_status status);
+
+/* ---- measurement support (not part of the operator) ----------------------
+ * Kernel identifiers used by the per-kernel timing below. */
+typedef enum gdr2_kernel_id {
+  GDR2_K_FWD_INTRA = 0,           /* forward: intra-chunk Gram / WY solve / Y, U   */
+  GDR2_K_FWD_STATE = 1,           /* forward: inter-chunk state scan + output      */
+  GDR2_K_BWD_RECOMPUTE_INTRA = 2, /* backward: intra-chunk recompute              */
+  GDR2_K_BWD_RECOMPUTE_STATE = 3, /* backward: chunk-state recompute              */
+  GDR2_K_BWD_STATE = 4,           /* backward: reverse state scan                 */
+  GDR2_K_BWD_WY = 5,              /* backward: gate-aware WY VJP                  */
+  GDR2_K_BWD_INTRA = 6,           /* backward: intra-chunk VJP + decay chain      */
+  GDR2_K_RECURRENT = 7,           /* recurrent / decode                           */
+  GDR2_NUM_KERNELS = 8
+} gdr2_kernel_id;
+
+/* Per-thread kernel timing for benchmarks: while enabled, each kernel launched
+ * by the calling thread is bracketed by two hipEvents recorded on its launch
+ * stream.  gdr2_profile_collect() waits for the recorded events, writes the
+ * accumulated milliseconds and launch counts of every kernel id into ms[] and
+ * launches[] (n >= GDR2_NUM_KERNELS entries, else GDR2_EINVAL) and resets the
+ * totals.  Off by default; costs nothing when off. */
+gdr2_status gdr2_profile_enable(int on);
+gdr2_status gdr2_profile_collect(double* ms, long long* launches, int n);
 
 #ifdef __cplusplus
 }

@@ -16,12 +16,16 @@ __all__ = [
     "GDR2_OK", "GDR2_EINVAL", "GDR2_EUNSUPPORTED", "GDR2_EWORKSPACE", "GDR2_EHIP",
     "GDR2_BF16", "GDR2_FP32", "Gdr2Problem", "Gdr2Error", "lib", "lib_path",
     "gdr2_chunk_workspace_bytes", "gdr2_chunk_fwd", "gdr2_chunk_bwd",
-    "gdr2_recurrent_step", "gdr2_status_str", "CHUNK",
+    "gdr2_recurrent_step", "gdr2_status_str", "CHUNK", "KERNEL_NAMES",
+    "gdr2_profile_enable", "gdr2_profile_collect",
 ]
 
 GDR2_OK, GDR2_EINVAL, GDR2_EUNSUPPORTED, GDR2_EWORKSPACE, GDR2_EHIP = 0, 1, 2, 3, 4
 GDR2_BF16, GDR2_FP32 = 0, 1
 CHUNK = 64
+# kernel ids of the measurement support (gdr2_kernel_id in include/gdr2.h)
+KERNEL_NAMES = ["fwd_intra", "fwd_state", "bwd_recompute_intra", "bwd_recompute_state",
+                "bwd_state", "bwd_wy", "bwd_intra", "recurrent"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 
@@ -64,6 +68,11 @@ def lib():
         L.gdr2_chunk_bwd.restype = ctypes.c_int
         L.gdr2_recurrent_step.argtypes = [P] + [vp] * 8 + [vp]
         L.gdr2_recurrent_step.restype = ctypes.c_int
+        L.gdr2_profile_enable.argtypes = [ctypes.c_int]
+        L.gdr2_profile_enable.restype = ctypes.c_int
+        L.gdr2_profile_collect.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_longlong),
+                                           ctypes.c_int]
+        L.gdr2_profile_collect.restype = ctypes.c_int
         L.gdr2_status_str.argtypes = [ctypes.c_int]
         L.gdr2_status_str.restype = ctypes.c_char_p
         _LIB = L
@@ -205,3 +214,17 @@ def gdr2_recurrent_step(q, k, v, log_alpha, b, w, S, *, scale=None, o=None):
                                    _ptr(b), _ptr(w), _ptr(S), _ptr(o), _stream())
     _check(st, "gdr2_recurrent_step")
     return o
+
+
+def gdr2_profile_enable(on=True):
+    """Enable / disable per-kernel hipEvent timing for the calling thread."""
+    _check(lib().gdr2_profile_enable(1 if on else 0), "gdr2_profile_enable")
+
+
+def gdr2_profile_collect():
+    """Wait for timed launches; return {kernel: (total_ms, launches)} and reset."""
+    n = len(KERNEL_NAMES)
+    ms = (ctypes.c_double * n)()
+    cnt = (ctypes.c_longlong * n)()
+    _check(lib().gdr2_profile_collect(ms, cnt, n), "gdr2_profile_collect")
+    return {KERNEL_NAMES[i]: (ms[i], cnt[i]) for i in range(n)}

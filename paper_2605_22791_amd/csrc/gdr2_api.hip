@@ -6,6 +6,7 @@
 
 #include <cmath>
 #include <cstdlib>
+#include <vector>
 
 #include "gdr2_kernels.hpp"
 
@@ -94,6 +95,50 @@ gdr2_status hip_status(hipError_t e, hipStream_t st) {
   return GDR2_OK;
 }
 
+// ---- measurement support ---------------------------------------------------
+// When a thread enables it, every kernel launch that thread makes is bracketed
+// by two hipEvents on the launch stream; gdr2_profile_collect() waits for them
+// and returns accumulated milliseconds and launch counts per kernel.  The state
+// is per calling thread and is only touched while profiling is on.
+struct ProfState {
+  bool on = false;
+  struct Pending {
+    int id;
+    hipEvent_t a, b;
+  };
+  std::vector<Pending> pending;
+  std::vector<hipEvent_t> pool;
+  double ms[GDR2_NUM_KERNELS] = {};
+  long long launches[GDR2_NUM_KERNELS] = {};
+};
+thread_local ProfState g_prof;
+
+hipEvent_t prof_event() {
+  if (!g_prof.pool.empty()) {
+    hipEvent_t e = g_prof.pool.back();
+    g_prof.pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+template <class F>
+hipError_t timed(int id, hipStream_t st, F&& launch) {
+  if (!g_prof.on) return launch();
+  hipEvent_t a = prof_event(), b = prof_event();
+  if (a == nullptr || b == nullptr) return hipErrorOutOfMemory;
+  hipError_t e = hipEventRecord(a, st);
+  if (e != hipSuccess) return e;
+  e = launch();
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(b, st);
+  if (e != hipSuccess) return e;
+  g_prof.pending.push_back({id, a, b});
+  return hipSuccess;
+}
+
 // ---- dispatch over (Dk, Dv) ------------------------------------------------
 template <template <int, int, typename> class F, typename TIn, typename... A>
 hipError_t dispatch(int Dk, int Dv, A&&... args) {
@@ -114,11 +159,12 @@ struct FwdRun {
                       static_cast<const TIn*>(w), at<float>(ws, L.Y), at<float>(ws, L.U),
                       at<float>(ws, L.Kt), at<float>(ws, L.Qg), at<float>(ws, L.Aqk),
                       at<float>(ws, L.GC), p->T, p->H, p->T / CH};
-    hipError_t e = launch_fwd_intra<DK, DV, TIn>(ia, p->B, st);
+    hipError_t e = timed(GDR2_K_FWD_INTRA, st, [&] { return launch_fwd_intra<DK, DV, TIn>(ia, p->B, st); });
     if (e != hipSuccess) return e;
     StateArgs<TIn> sa{ia.Y, ia.U, ia.Kt, ia.Qg, ia.Aqk, ia.GC, S0, ST, static_cast<TIn*>(o),
                       nullptr, nullptr, p->T, p->H, p->T / CH, p->scale};
-    return launch_fwd_state<DK, DV, TIn, true, false>(sa, p->B, st);
+    return timed(GDR2_K_FWD_STATE, st,
+                 [&] { return launch_fwd_state<DK, DV, TIn, true, false>(sa, p->B, st); });
   }
 };
 
@@ -135,15 +181,17 @@ struct BwdRun {
                       static_cast<const TIn*>(w), at<float>(ws, L.Y), at<float>(ws, L.U),
                       at<float>(ws, L.Kt), at<float>(ws, L.Qg), at<float>(ws, L.Aqk),
                       at<float>(ws, L.GC), p->T, p->H, NT};
-    hipError_t e = launch_fwd_intra<DK, DV, TIn>(ia, p->B, st);
+    hipError_t e = timed(GDR2_K_BWD_RECOMPUTE_INTRA, st,
+                         [&] { return launch_fwd_intra<DK, DV, TIn>(ia, p->B, st); });
     if (e != hipSuccess) return e;
     StateArgs<TIn> sa{ia.Y, ia.U, ia.Kt, ia.Qg, ia.Aqk, ia.GC, S0, nullptr, nullptr,
                       at<float>(ws, L.Hs), at<float>(ws, L.Rs), p->T, p->H, NT, p->scale};
-    e = launch_fwd_state<DK, DV, TIn, false, true>(sa, p->B, st);
+    e = timed(GDR2_K_BWD_RECOMPUTE_STATE, st,
+              [&] { return launch_fwd_state<DK, DV, TIn, false, true>(sa, p->B, st); });
     if (e != hipSuccess) return e;
     BwdStateArgs<TIn> ba{ia.Qg, ia.Kt, ia.Y, ia.Aqk, ia.GC, static_cast<const TIn*>(dout), dST,
                          dS0, at<float>(ws, L.DH), at<float>(ws, L.DR), p->T, p->H, NT, p->scale};
-    e = launch_bwd_state<DK, DV, TIn>(ba, p->B, st);
+    e = timed(GDR2_K_BWD_STATE, st, [&] { return launch_bwd_state<DK, DV, TIn>(ba, p->B, st); });
     if (e != hipSuccess) return e;
     BwdChunkArgs<TIn> ca{static_cast<const TIn*>(q), static_cast<const TIn*>(k),
                          static_cast<const TIn*>(v), g, static_cast<const TIn*>(b),
@@ -152,9 +200,9 @@ struct BwdRun {
                          at<float>(ws, L.DEg), static_cast<TIn*>(dq), static_cast<TIn*>(dk),
                          static_cast<TIn*>(dv), static_cast<TIn*>(db), static_cast<TIn*>(dw), dg,
                          p->T, p->H, NT, p->scale};
-    e = launch_bwd_wy<DK, DV, TIn>(ca, p->B, st);
+    e = timed(GDR2_K_BWD_WY, st, [&] { return launch_bwd_wy<DK, DV, TIn>(ca, p->B, st); });
     if (e != hipSuccess) return e;
-    return launch_bwd_intra<DK, DV, TIn>(ca, p->B, st);
+    return timed(GDR2_K_BWD_INTRA, st, [&] { return launch_bwd_intra<DK, DV, TIn>(ca, p->B, st); });
   }
 };
 
@@ -166,7 +214,7 @@ struct RecRun {
     RecurArgs<TIn> ra{static_cast<const TIn*>(q), static_cast<const TIn*>(k),
                       static_cast<const TIn*>(v), g, static_cast<const TIn*>(b),
                       static_cast<const TIn*>(w), S, static_cast<TIn*>(o), p->T, p->H, p->scale};
-    return launch_recurrent<DK, DV, TIn>(ra, p->B, st);
+    return timed(GDR2_K_RECURRENT, st, [&] { return launch_recurrent<DK, DV, TIn>(ra, p->B, st); });
   }
 };
 
@@ -242,6 +290,37 @@ gdr2_status gdr2_recurrent_step(const gdr2_problem* p, const void* q, const void
   else
     e = dispatch<RecRun, float>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S, o, stream);
   return hip_status(e, stream);
+}
+
+gdr2_status gdr2_profile_enable(int on) {
+  g_prof.on = on != 0;
+  return GDR2_OK;
+}
+
+gdr2_status gdr2_profile_collect(double* ms, long long* launches, int n) {
+  if (ms == nullptr || launches == nullptr || n < GDR2_NUM_KERNELS) return GDR2_EINVAL;
+  gdr2_status st = GDR2_OK;
+  for (const auto& p : g_prof.pending) {
+    float t = 0.f;
+    if (hipEventSynchronize(p.b) != hipSuccess || hipEventElapsedTime(&t, p.a, p.b) != hipSuccess) {
+      st = GDR2_EHIP;
+    } else {
+      g_prof.ms[p.id] += t;
+      g_prof.launches[p.id] += 1;
+    }
+    g_prof.pool.push_back(p.a);
+    g_prof.pool.push_back(p.b);
+  }
+  g_prof.pending.clear();
+  for (int i = 0; i < n; ++i) {
+    ms[i] = i < GDR2_NUM_KERNELS ? g_prof.ms[i] : 0.0;
+    launches[i] = i < GDR2_NUM_KERNELS ? g_prof.launches[i] : 0;
+  }
+  for (int i = 0; i < GDR2_NUM_KERNELS; ++i) {
+    g_prof.ms[i] = 0.0;
+    g_prof.launches[i] = 0;
+  }
+  return st;
 }
 
 const char* gdr2_status_str(gdr2_status st) {

@@ -31,7 +31,8 @@ def _declared_symbols():
 def test_header_declares_the_entry_points():
     assert _declared_symbols() == sorted(["gdr2_chunk_workspace_bytes", "gdr2_chunk_fwd",
                                           "gdr2_chunk_bwd", "gdr2_recurrent_step",
-                                          "gdr2_status_str"])
+                                          "gdr2_status_str", "gdr2_profile_enable",
+                                          "gdr2_profile_collect"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -45,6 +46,17 @@ def test_status_strings():
         s = g2.gdr2_status_str(code)
         assert s.startswith("GDR2_")
     assert g2.gdr2_status_str(99) == "GDR2_UNKNOWN"
+
+
+def test_profile_collect_without_launches():
+    L = g2.lib()
+    ms = (ctypes.c_double * 8)()
+    n = (ctypes.c_longlong * 8)()
+    assert L.gdr2_profile_collect(ms, n, 7) == g2.GDR2_EINVAL
+    assert L.gdr2_profile_enable(1) == g2.GDR2_OK
+    assert L.gdr2_profile_collect(ms, n, 8) == g2.GDR2_OK
+    assert L.gdr2_profile_enable(0) == g2.GDR2_OK
+    assert list(n) == [0] * 8 and list(ms) == [0.0] * 8
 
 
 def _prob(**kw):
