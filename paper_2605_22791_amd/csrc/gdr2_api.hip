@@ -5,6 +5,7 @@
 #include "../../include/gdr2.h"
 
 #include <cmath>
+#include <type_traits>
 #include <cstdlib>
 #include <vector>
 
@@ -153,6 +154,14 @@ struct FwdRun {
   static hipError_t run(const gdr2_problem* p, const void* q, const void* k, const void* v,
                         const float* g, const void* b, const void* w, const float* S0, void* o,
                         float* ST, void* ws, hipStream_t st) {
+    if (std::is_same<TIn, bf16_t>::value) {
+      // bf16: one fused scan kernel (intra-chunk products + state recurrence + output)
+      ScanFwdArgs sa{static_cast<const bf16_t*>(q), static_cast<const bf16_t*>(k),
+                     static_cast<const bf16_t*>(v), g, static_cast<const bf16_t*>(b),
+                     static_cast<const bf16_t*>(w), S0, ST, static_cast<bf16_t*>(o), nullptr, nullptr,
+                     p->B, p->T, p->H, p->T / CH, p->scale};
+      return timed(GDR2_K_FWD_STATE, st, [&] { return launch_fwd_scan<DK, DV, true, false>(sa, st); });
+    }
     const Layout L = layout(p, false);
     IntraArgs<TIn> ia{static_cast<const TIn*>(q), static_cast<const TIn*>(k),
                       static_cast<const TIn*>(v), g, static_cast<const TIn*>(b),

@@ -102,6 +102,27 @@ struct RecurArgs {
   float scale;
 };
 
+// Fused chunkwise scan of the bf16 path: intra-chunk WY products and the
+// inter-chunk state recurrence in one kernel, sequential over chunks.
+struct ScanFwdArgs {
+  const bf16_t* q;
+  const bf16_t* k;
+  const bf16_t* v;
+  const float* g;
+  const bf16_t* b;
+  const bf16_t* w;
+  const float* S0;  // nullable
+  float* ST;        // nullable
+  bf16_t* o;        // written when the output is fused in
+  float* Hs;        // chunk-start states (backward recompute)
+  float* Rs;        // R per chunk (backward recompute)
+  int B, T, H, NT;
+  float scale;
+};
+
+template <int DK, int DV, bool WITH_O, bool STORE_H>
+hipError_t launch_fwd_scan(const ScanFwdArgs& a, hipStream_t st);
+
 template <int DK, int DV, typename TIn>
 hipError_t launch_fwd_intra(const IntraArgs<TIn>& a, int B, hipStream_t st);
 template <int DK, int DV, typename TIn, bool WITH_O, bool STORE_H>
