@@ -38,10 +38,13 @@ gdr2_status check_problem(const gdr2_problem* p, bool chunked) {
   return GDR2_OK;
 }
 
-// Workspace regions (fp32), chunk-head major: ch = (b*H + h)*NT + n.
+// Workspace regions, chunk-head major: ch = (b*H + h)*NT + n.  The bf16
+// forward uses the fragment-order regions of WsBf16 (gdr2_kernels.hpp); the
+// fp32 path and the backward use fp32 tiles.
 struct Layout {
-  size_t Y, U, Kt, Qg, Aqk, GC;          // forward tiles
+  size_t Y, U, Kt, Qg, Aqk, GC;          // fp32 forward tiles
   size_t Hs, Rs, DH, DR, DAqk, DT, DEg;  // backward extras
+  size_t bY, bQ, bA, bK, bU, bG;         // bf16 forward (fragment order)
   size_t total;
 };
 
@@ -50,6 +53,21 @@ Layout layout(const gdr2_problem* p, bool bwd) {
   const size_t Dk = p->Dk, Dv = p->Dv;
   Layout L{};
   size_t off = 0;
+  if (p->dtype == GDR2_BF16 && !bwd) {
+    auto takeb = [&](size_t bytes) {
+      const size_t at = off;
+      off += round_up(bytes);
+      return at;
+    };
+    L.bY = takeb(NC * WsBf16::y(p->Dk));
+    L.bQ = takeb(NC * WsBf16::qg(p->Dk));
+    L.bA = takeb(NC * WsBf16::aqk());
+    L.bK = takeb(NC * WsBf16::ktt(p->Dk));
+    L.bU = takeb(NC * WsBf16::u(p->Dv));
+    L.bG = takeb(NC * WsBf16::gc(p->Dk));
+    L.total = off;
+    return L;
+  }
   auto take = [&](size_t floats) {
     const size_t at = off;
     off += round_up(floats * sizeof(float));
@@ -155,12 +173,19 @@ struct FwdRun {
                         const float* g, const void* b, const void* w, const float* S0, void* o,
                         float* ST, void* ws, hipStream_t st) {
     if (std::is_same<TIn, bf16_t>::value) {
-      // bf16: one fused scan kernel (intra-chunk products + state recurrence + output)
-      ScanFwdArgs sa{static_cast<const bf16_t*>(q), static_cast<const bf16_t*>(k),
-                     static_cast<const bf16_t*>(v), g, static_cast<const bf16_t*>(b),
-                     static_cast<const bf16_t*>(w), S0, ST, static_cast<bf16_t*>(o), nullptr, nullptr,
-                     p->B, p->T, p->H, p->T / CH, p->scale};
-      return timed(GDR2_K_FWD_STATE, st, [&] { return launch_fwd_scan<DK, DV, true, false>(sa, st); });
+      // bf16: chunk-parallel intra-chunk kernel, then the state scan with the output
+      const Layout L = layout(p, false);
+      IntraBf16Args ia{static_cast<const bf16_t*>(q), static_cast<const bf16_t*>(k),
+                       static_cast<const bf16_t*>(v), g, static_cast<const bf16_t*>(b),
+                       static_cast<const bf16_t*>(w), at<unsigned char>(ws, L.bY),
+                       at<unsigned char>(ws, L.bQ), at<unsigned char>(ws, L.bA),
+                       at<unsigned char>(ws, L.bK), at<float>(ws, L.bU), at<float>(ws, L.bG),
+                       p->B, p->T, p->H, p->T / CH};
+      hipError_t e = timed(GDR2_K_FWD_INTRA, st, [&] { return launch_intra_bf16<DK, DV>(ia, st); });
+      if (e != hipSuccess) return e;
+      ScanArgs sa{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.U, ia.GC, S0, ST, static_cast<bf16_t*>(o), nullptr, nullptr,
+                  p->B, p->T, p->H, p->T / CH, p->scale};
+      return timed(GDR2_K_FWD_STATE, st, [&] { return launch_scan_bf16<DK, DV, true, false>(sa, st); });
     }
     const Layout L = layout(p, false);
     IntraArgs<TIn> ia{static_cast<const TIn*>(q), static_cast<const TIn*>(k),

@@ -31,6 +31,9 @@ namespace gdr2 {
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf4 __attribute__((ext_vector_type(4)));
+// 16 raw bytes as a native vector (HIP's uint4 is a struct, whose copies go
+// through memory and keep staging arrays out of registers)
+typedef unsigned u4v __attribute__((ext_vector_type(4)));
 
 #define GDR2_LDS __attribute__((address_space(3)))
 
@@ -96,7 +99,9 @@ __device__ __forceinline__ void unpack8(bf8 x, float (&o)[8]) {
 #pragma unroll
   for (int e = 0; e < 8; ++e) o[e] = (float)x[e];
 }
-__device__ __forceinline__ void unpack8(uint4 u, float (&o)[8]) { unpack8(__builtin_bit_cast(bf8, u), o); }
+__device__ __forceinline__ void unpack8(u4v u, float (&o)[8]) { unpack8(__builtin_bit_cast(bf8, u), o); }
+__device__ __forceinline__ u4v ldg16(const void* p) { return *reinterpret_cast<const u4v*>(p); }
+__device__ __forceinline__ void sts16(void* p, u4v x) { *reinterpret_cast<u4v*>(p) = x; }
 
 // 16-byte LDS / global accessors
 __device__ __forceinline__ bf8 ld8(const __bf16* p) { return *reinterpret_cast<const bf8*>(p); }

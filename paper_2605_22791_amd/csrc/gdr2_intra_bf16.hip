@@ -1,0 +1,445 @@
+// Intra-chunk kernel of the bf16 path (gfx950): one 4-wave workgroup per
+// chunk-head, two workgroups per CU.  Per chunk of C = 64 tokens it forms
+//
+//   G2 = log2(e) * cumsum(g)                          eq. eq_gdn2_gamma (fp32)
+//   Q_g = q * gamma,  Ktail^T = (k * gamma_C / gamma)^T    eqs. eq_gdn2_gate_matrices,
+//                                                     eq_gdn2_chunk_state
+//   T = tril(Ebar Kbar^T, -1), A_qk = tril(Q_g Kbar^T)     eqs. eq_gdn2_wy_matrix,
+//                                                     eq_gdn2_chunk_scores
+//   A = (I + T)^{-1}                                  fp32 (App. D.4)
+//   Y = A Ebar,  U = A (W * V)                        eq. eq_gdn2_wy_aux
+//
+// and writes Y, Q_g, A_qk, Ktail^T, U and gamma_C to the workspace in MFMA
+// fragment order (layout in gdr2_kernels.hpp) for the state scan.
+//
+// Precision: T uses one bf16 pass; A enters Y and U as a bf16 operand (the
+// solve itself is fp32) and Y is stored in bf16; A_qk, Q_g, Ktail, Ebar, Z are
+// split hi/lo so their products are fp32-accurate.
+//
+// Decay factors are 2^(G2_r - G2_s) for r >= s, formed relative to the first
+// row p = 16 i of the row block i of r: 2^(G2_r - G2_p) * 2^(G2_p - G2_s); the
+// first factor is <= 1, the second <= 1 outside the diagonal block and bounded
+// by one block's decay inside it.  A diagonal block whose internal decay
+// exceeds e^60 is formed element by element.
+//
+// T and A_qk are computed transposed (rows = keys) so that each lane's four
+// outputs are consecutive keys of one query row: T goes to LDS as float4 rows
+// and A_qk / Y land directly in the permuted fragment order.
+
+#include "gdr2_kernels.hpp"
+#include "gdr2_bf16.hpp"
+
+namespace gdr2 {
+
+template <int DK, int DV>
+struct IntraCfg {
+  static constexpr int NTHR = 256;
+  static constexpr int KS = DK / 32, NCB = DK / 16, NVB = DV / 16;
+  static constexpr int LG = DK + 8;    // G2 fp32 [64][LG]
+  static constexpr int LE = DK + 8;    // Ebar hi/lo bf16 [64][LE] (over G2)
+  static constexpr int LVW = DV + 8;   // v, w bf16 [64][LVW] (over Ebar)
+  static constexpr int LKB = DK + 8;   // k bf16 [64][LKB]
+  static constexpr int LTA = 64 + 4;   // T -> A fp32 [64][LTA]
+  static constexpr int SZ_G = 64 * LG * 4, SZ_E = 2 * 64 * LE * 2, SZ_VW = 2 * 64 * LVW * 2;
+  static constexpr int SZ_X = SZ_G > SZ_E ? (SZ_G > SZ_VW ? SZ_G : SZ_VW) : (SZ_E > SZ_VW ? SZ_E : SZ_VW);
+  static constexpr int OFF_X = 0;
+  static constexpr int OFF_K = SZ_X;
+  static constexpr int OFF_TA = OFF_K + 64 * LKB * 2;
+  static constexpr int OFF_MISC = OFF_TA + 64 * LTA * 4;
+  static constexpr int LDS = OFF_MISC + 16;
+  static_assert(LDS <= 80 * 1024, "two workgroups per CU");
+};
+
+// T / A_qk tiles per wave: (row block i of queries, column block j of keys)
+// encoded as 4 * i + j; -1 marks "no tile".  The A_qk tiles above the
+// diagonal are written as zeros (they share fragment blocks with causal tiles).
+__device__ __forceinline__ int tile_of(int wave, int t) {
+  // w0: (0,0) (1,0) (1,1)   w1: (2,0) (2,1) (2,2)   w2: (3,0) (3,1)   w3: (3,2) (3,3)
+  switch (wave) {
+    case 0: return t == 0 ? 0 : (t == 1 ? 4 : 5);
+    case 1: return 8 + t;
+    case 2: return t < 2 ? 12 + t : -1;
+    default: return t < 2 ? 14 + t : -1;
+  }
+}
+// A_qk tiles above the diagonal that are written as zeros: (0,1) (2,3) (0,2) (0,3) (1,2) (1,3)
+__device__ __forceinline__ int zero_tile(int z) {
+  switch (z) {
+    case 0: return 1;
+    case 1: return 11;
+    case 2: return 2;
+    case 3: return 3;
+    case 4: return 6;
+    default: return 7;
+  }
+}
+
+template <int DK, int DV>
+__global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
+  using C = IntraCfg<DK, DV>;
+  constexpr int KS = C::KS, NCB = C::NCB, NVB = C::NVB;
+  constexpr int LG = C::LG, LE = C::LE, LVW = C::LVW, LKB = C::LKB, LTA = C::LTA;
+
+  extern __shared__ __align__(16) unsigned char smem[];
+  float* sG = reinterpret_cast<float*>(smem + C::OFF_X);
+  __bf16* sEhi = reinterpret_cast<__bf16*>(smem + C::OFF_X);
+  __bf16* sElo = sEhi + 64 * LE;
+  __bf16* sV = reinterpret_cast<__bf16*>(smem + C::OFF_X);
+  __bf16* sW = sV + 64 * LVW;
+  __bf16* sK = reinterpret_cast<__bf16*>(smem + C::OFF_K);
+  float* sTA = reinterpret_cast<float*>(smem + C::OFF_TA);
+  int* unsafe = reinterpret_cast<int*>(smem + C::OFF_MISC);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, r16 = lane & 15;
+  const int n = blockIdx.x, h = blockIdx.y, bb = blockIdx.z;
+  const int T = a.T, H = a.H, NT = a.NT;
+  const size_t ch = ((size_t)bb * H + h) * NT + n;
+
+  const __bf16* Q = reinterpret_cast<const __bf16*>(a.q);
+  const __bf16* K = reinterpret_cast<const __bf16*>(a.k);
+  const __bf16* Vg = reinterpret_cast<const __bf16*>(a.v);
+  const __bf16* Bg = reinterpret_cast<const __bf16*>(a.b);
+  const __bf16* Wg = reinterpret_cast<const __bf16*>(a.w);
+  const size_t row0 = (size_t)bb * T + (size_t)n * CH;
+  auto kofs = [&](int r) -> size_t { return (row0 + r) * ((size_t)H * DK) + (size_t)h * DK; };
+  auto vofs = [&](int r) -> size_t { return (row0 + r) * ((size_t)H * DV) + (size_t)h * DV; };
+
+  // ---- loads: g in scan layout (NG rows of 4 channels per thread), k
+  constexpr int GCG = DK / 4, GSEG = 256 / GCG, NG = 64 / GSEG;
+  constexpr int NKC = DK / 32;  // 16-byte chunks of k per thread
+  const int gcg = tid % GCG, gsg = tid / GCG;
+  float4 gr[NG];
+#pragma unroll
+  for (int m = 0; m < NG; ++m) gr[m] = *reinterpret_cast<const float4*>(a.g + kofs(NG * gsg + m) + 4 * gcg);
+  u4v kst[NKC];
+#pragma unroll
+  for (int m = 0; m < NKC; ++m) {
+    const int e = tid + 256 * m, r = e / (DK / 8), c8 = (e % (DK / 8)) * 8;
+    kst[m] = ldg16(K + kofs(r) + c8);
+  }
+
+  // ---- G2 = log2(e) * cumsum(g): in-register segment scans + segment offsets
+  if (tid < 4) unsafe[tid] = 0;
+  {
+    float4* tot = reinterpret_cast<float4*>(sTA);  // scratch before T exists
+    float4 run = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int m = 0; m < NG; ++m) {
+      run.x += gr[m].x * kLog2e; run.y += gr[m].y * kLog2e;
+      run.z += gr[m].z * kLog2e; run.w += gr[m].w * kLog2e;
+      gr[m] = run;
+    }
+    tot[gsg * GCG + gcg] = run;
+#pragma unroll
+    for (int m = 0; m < NKC; ++m) {
+      const int e = tid + 256 * m, r = e / (DK / 8), c8 = (e % (DK / 8)) * 8;
+      sts16(sK + r * LKB + c8, kst[m]);
+    }
+    __syncthreads();
+    float4 off = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int s = 0; s < gsg; ++s) {
+      const float4 t4 = tot[s * GCG + gcg];
+      off.x += t4.x; off.y += t4.y; off.z += t4.z; off.w += t4.w;
+    }
+#pragma unroll
+    for (int m = 0; m < NG; ++m)
+      *reinterpret_cast<float4*>(sG + (NG * gsg + m) * LG + 4 * gcg) =
+          make_float4(gr[m].x + off.x, gr[m].y + off.y, gr[m].z + off.z, gr[m].w + off.w);
+    __syncthreads();
+  }
+  for (int e = tid; e < 4 * DK; e += 256) {
+    const int i = e / DK, c = e % DK;
+    if (sG[(16 * i) * LG + c] - sG[(16 * i + 15) * LG + c] > kDiagLimit2) unsafe[i] = 1;
+  }
+  for (int c = tid; c < DK; c += 256) a.GC[ch * (WsBf16::gc(DK) / 4) + c] = ex2(sG[(CH - 1) * LG + c]);
+  for (int e = tid; e < 6 * 256; e += 256) {  // upper blocks of T/A (the region held scratch)
+    const int blk = e >> 8, rr = (e & 255) >> 4, cc = e & 15;
+    const int bi = blk < 3 ? 0 : (blk < 5 ? 1 : 2);
+    const int bj = blk < 3 ? blk + 1 : (blk < 5 ? blk - 1 : 3);
+    sTA[(16 * bi + rr) * LTA + 16 * bj + cc] = 0.f;
+  }
+  __syncthreads();
+
+  // ---- Q_g (standard fragments) and Ktail^T (standard fragments, via transposed k)
+  {
+    unsigned char* Qo = a.Qg + ch * WsBf16::qg(DK);
+    for (int blk = wave; blk < 4 * KS; blk += 4) {
+      const int rb = blk / KS, kb = blk % KS;
+      const int r = 16 * rb + r16, c0 = 32 * kb + 8 * g;
+      float Gr[8], qf[8], x[8];
+      ldf8(sG + r * LG + c0, Gr);
+      unpack8(ldg16(Q + kofs(r) + c0), qf);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = qf[e] * ex2(Gr[e]);
+      const Fr f = split8(x);
+      st8(reinterpret_cast<__bf16*>(Qo + blk * 2048 + 16 * lane), f.hi);
+      st8(reinterpret_cast<__bf16*>(Qo + blk * 2048 + 1024 + 16 * lane), f.lo);
+    }
+    unsigned char* Ko = a.KtT + ch * WsBf16::ktt(DK);
+    for (int blk = wave; blk < NCB * 2; blk += 4) {
+      const int cb = blk >> 1, kb = blk & 1;
+      const int c = 16 * cb + r16;
+      float kf[8], x[8];
+      unpack8(ld_tr8(sK, LKB, 32 * kb, 16 * cb, lane), kf);  // k[32 kb + 8 g + e][c]
+      const float GC2 = sG[(CH - 1) * LG + c];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = kf[e] * ex2(GC2 - sG[(32 * kb + 8 * g + e) * LG + c]);
+      const Fr f = split8(x);
+      st8(reinterpret_cast<__bf16*>(Ko + blk * 2048 + 16 * lane), f.hi);
+      st8(reinterpret_cast<__bf16*>(Ko + blk * 2048 + 1024 + 16 * lane), f.lo);
+    }
+  }
+
+  // ---- T^T and A_qk^T tiles: D[s][r] = sum_c RK_s[c] * {LE, LQ}_r[c]
+  {
+    unsigned char* Ao = a.Aqk + ch * WsBf16::aqk();
+#pragma unroll 1
+    for (int t = 0; t < 3; ++t) {
+      const int code = tile_of(wave, t);
+      if (code < 0) continue;
+      const int i = code >> 2, j = code & 3;
+      const int r = 16 * i + r16;  // query row of this lane's outputs
+      f4 accT = f4zero(), accA = f4zero();
+      if (unsafe[i] && i == j) {
+        // element by element: every factor 2^(G2_r - G2_s) with r >= s is <= 1
+#pragma unroll 1
+        for (int u = 0; u < 4; ++u) {
+          const int s = 16 * j + 4 * g + u;
+          float tt = 0.f, ta = 0.f;
+          if (r >= s) {
+#pragma unroll 1
+            for (int c = 0; c < DK; ++c) {
+              const float e = ex2(sG[r * LG + c] - sG[s * LG + c]) * (float)sK[s * LKB + c];
+              tt += (float)Bg[kofs(r) + c] * (float)sK[r * LKB + c] * e;
+              ta += (float)Q[kofs(r) + c] * e;
+            }
+          }
+#pragma unroll
+          for (int uu = 0; uu < 4; ++uu)
+            if (uu == u) {
+              accT[uu] = tt;
+              accA[uu] = ta;
+            }
+        }
+      } else {
+        const int s = 16 * j + r16;  // key row supplied by this lane (A operand)
+#pragma unroll 2
+        for (int p = 0; p < KS; ++p) {
+          const int c0 = 32 * p + 8 * g;
+          float Gs[8], Gr[8], Gp[8], ks[8], kr[8], br[8], qr[8];
+          ldf8(sG + s * LG + c0, Gs);
+          ldf8(sG + r * LG + c0, Gr);
+          ldf8(sG + (16 * i) * LG + c0, Gp);
+          unpack8(ld8(sK + s * LKB + c0), ks);
+          unpack8(ld8(sK + r * LKB + c0), kr);
+          unpack8(ldg16(Bg + kofs(r) + c0), br);
+          unpack8(ldg16(Q + kofs(r) + c0), qr);
+          float rk[8], le[8], lq[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            rk[e] = ks[e] * ex2(Gp[e] - Gs[e]);
+            const float f = ex2(Gr[e] - Gp[e]);
+            le[e] = br[e] * kr[e] * f;
+            lq[e] = qr[e] * f;
+          }
+          const Fr rkf = split8(rk);
+          accT = mma(rkf.hi, round8(le), accT);
+          accA = mma3(rkf, split8(lq), accA);
+        }
+      }
+      // lane holds T[r][s0 + u] and A_qk[r][s0 + u], s0 = 16 j + 4 g
+      const int s0 = 16 * j + 4 * g;
+      float4 tv;
+      tv.x = (r > s0 + 0) ? accT[0] : 0.f;
+      tv.y = (r > s0 + 1) ? accT[1] : 0.f;
+      tv.z = (r > s0 + 2) ? accT[2] : 0.f;
+      tv.w = (r > s0 + 3) ? accT[3] : 0.f;
+      *reinterpret_cast<float4*>(sTA + r * LTA + s0) = tv;
+      f4 av;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) av[u] = (r >= s0 + u) ? accA[u] : 0.f;
+      const size_t off = (size_t)(i * 2 + (j >> 1)) * 2048 + 16 * lane + 8 * (j & 1);
+      st4split(reinterpret_cast<__bf16*>(Ao + off), reinterpret_cast<__bf16*>(Ao + off + 1024), av);
+    }
+    // zero A_qk tiles above the diagonal: (0,1) and (2,3) share fragment blocks
+    // with causal tiles; blocks (0, keys 32..63) and (1, keys 32..63) are all zero
+    {
+      for (int z = wave; z < 6; z += 4) {
+        const int i = zero_tile(z) >> 2, j = zero_tile(z) & 3;
+        const size_t off = (size_t)(i * 2 + (j >> 1)) * 2048 + 16 * lane + 8 * (j & 1);
+        st4split(reinterpret_cast<__bf16*>(Ao + off), reinterpret_cast<__bf16*>(Ao + off + 1024), f4zero());
+      }
+    }
+  }
+  __syncthreads();
+
+  // ---- A = (I + T)^{-1} in place, fp32: diagonal blocks by forward
+  // substitution (lane = column), then the off-diagonal blocks row block by
+  // row block:  A_ij = -A_ii * sum_{j <= k < i} T_ik A_kj
+  if (wave == 0) {
+    const int blk = lane >> 4, cc = lane & 15;
+    float x[16];
+#pragma unroll
+    for (int rr = 0; rr < 16; ++rr) {
+      const float* trow = sTA + (16 * blk + rr) * LTA + 16 * blk;
+      float a0 = (rr == cc) ? 1.f : 0.f, a1 = 0.f;
+#pragma unroll
+      for (int s = 0; s + 1 < rr; s += 2) {
+        a0 -= trow[s] * x[s];
+        a1 -= trow[s + 1] * x[s + 1];
+      }
+      if (rr & 1) a0 -= trow[rr - 1] * x[rr - 1];
+      x[rr] = a0 + a1;
+    }
+#pragma unroll
+    for (int rr = 0; rr < 16; ++rr) sTA[(16 * blk + rr) * LTA + 16 * blk + cc] = x[rr];
+  }
+  // v, w for U = A Z, loaded while the solve runs
+  constexpr int NVC = DV / 32;  // 16-byte chunks of v (and of w) per thread
+  u4v vst[NVC], wst[NVC];
+#pragma unroll
+  for (int m = 0; m < NVC; ++m) {
+    const int e = tid + 256 * m, r = e / (DV / 8), c8 = (e % (DV / 8)) * 8;
+    vst[m] = ldg16(Vg + vofs(r) + c8);
+    wst[m] = ldg16(Wg + vofs(r) + c8);
+  }
+  __syncthreads();
+#pragma unroll 1
+  for (int i = 1; i < 4; ++i) {
+    f4 res = f4zero();
+    if (wave < i) {
+      const int j = wave;
+      f4 M = f4zero();
+      for (int kb = j; kb < i; ++kb) {
+#pragma unroll
+        for (int st = 0; st < 4; ++st) {
+          const int kk = 16 * kb + 4 * st + g;
+          M = mfma_f32(sTA[(16 * i + r16) * LTA + kk], sTA[kk * LTA + 16 * j + r16], M);
+        }
+      }
+#pragma unroll
+      for (int st = 0; st < 4; ++st) {
+        const int src = r16 + 16 * st;
+        const float m0 = __shfl(M[0], src), m1 = __shfl(M[1], src);
+        const float m2 = __shfl(M[2], src), m3 = __shfl(M[3], src);
+        const float mv = g == 0 ? m0 : (g == 1 ? m1 : (g == 2 ? m2 : m3));
+        res = mfma_f32(sTA[(16 * i + r16) * LTA + 16 * i + 4 * st + g], mv, res);
+      }
+    }
+    __syncthreads();
+    if (wave < i) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) sTA[(16 * i + 4 * g + u) * LTA + 16 * wave + r16] = -res[u];
+    }
+    __syncthreads();
+  }
+
+  // ---- Ebar = b * k * gamma (split) over the G2 region
+  {
+    constexpr int NE = DK / 32;  // 8-channel groups per thread
+    float eb[NE][8];
+#pragma unroll
+    for (int m = 0; m < NE; ++m) {
+      const int e = tid + 256 * m, r = e / (DK / 8), c8 = (e % (DK / 8)) * 8;
+      float Gv[8], kf[8], bf[8];
+      ldf8(sG + r * LG + c8, Gv);
+      unpack8(ld8(sK + r * LKB + c8), kf);
+      unpack8(ldg16(Bg + kofs(r) + c8), bf);
+#pragma unroll
+      for (int x = 0; x < 8; ++x) eb[m][x] = bf[x] * kf[x] * ex2(Gv[x]);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int m = 0; m < NE; ++m) {
+      const int e = tid + 256 * m, r = e / (DK / 8), c8 = (e % (DK / 8)) * 8;
+      const Fr f = split8(eb[m]);
+      st8(sEhi + r * LE + c8, f.hi);
+      st8(sElo + r * LE + c8, f.lo);
+    }
+    __syncthreads();
+  }
+
+  // ---- Y^T tiles: D[c][r] = sum_s Ebar[s][c] A[r][s]  -> permuted fragments of Y
+  {
+    unsigned char* Yo = a.Y + ch * WsBf16::y(DK);
+#pragma unroll 1
+    for (int cb = wave; cb < NCB; cb += 4) {
+      Fr ef[2];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        ef[kb].hi = ld_tr8(sEhi, LE, 32 * kb, 16 * cb, lane);
+        ef[kb].lo = ld_tr8(sElo, LE, 32 * kb, 16 * cb, lane);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        f4 acc = f4zero();
+#pragma unroll
+        for (int kb = 0; kb <= (i >> 1); ++kb) {
+          float av[8];
+          ldf8(sTA + (16 * i + r16) * LTA + 32 * kb + 8 * g, av);
+          acc = mma2a(ef[kb], round8(av), acc);
+        }
+        st4(reinterpret_cast<__bf16*>(Yo + (size_t)(i * KS + (cb >> 1)) * 1024 + 16 * lane + 8 * (cb & 1)), acc[0],
+            acc[1], acc[2], acc[3]);
+      }
+    }
+  }
+  __syncthreads();  // Ebar is dead; its region takes v and w
+
+  // ---- U = A (W * V): fp32 accumulator tiles
+#pragma unroll
+  for (int m = 0; m < NVC; ++m) {
+    const int e = tid + 256 * m, r = e / (DV / 8), c8 = (e % (DV / 8)) * 8;
+    sts16(sV + r * LVW + c8, vst[m]);
+    sts16(sW + r * LVW + c8, wst[m]);
+  }
+  __syncthreads();
+  {
+    float* Uo = a.U + ch * (WsBf16::u(DV) / 4);
+    constexpr int VPW = NVB / 4;  // value blocks per wave
+#pragma unroll 1
+    for (int t = 0; t < VPW; ++t) {
+      const int vb = wave * VPW + t;
+      Fr zf[2];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        float vf[8], wf[8], z[8];
+        unpack8(ld_tr8(sV, LVW, 32 * kb, 16 * vb, lane), vf);
+        unpack8(ld_tr8(sW, LVW, 32 * kb, 16 * vb, lane), wf);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) z[e] = vf[e] * wf[e];
+        zf[kb] = split8(z);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        f4 acc = f4zero();
+#pragma unroll
+        for (int kb = 0; kb <= (i >> 1); ++kb) {
+          float av[8];
+          ldf8(sTA + (16 * i + r16) * LTA + 32 * kb + 8 * g, av);
+          acc = mma2b(round8(av), zf[kb], acc);
+        }
+        *reinterpret_cast<f4*>(Uo + ((size_t)(vb * 4 + i) * 64 + lane) * 4) = acc;
+      }
+    }
+  }
+}
+
+template <int DK, int DV>
+hipError_t launch_intra_bf16(const IntraBf16Args& a, hipStream_t st) {
+  using C = IntraCfg<DK, DV>;
+  const void* fn = reinterpret_cast<const void*>(&intra_bf16_kernel<DK, DV>);
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+  if (e != hipSuccess) return e;
+  dim3 grid(a.NT, a.H, a.B);
+  hipLaunchKernelGGL((intra_bf16_kernel<DK, DV>), grid, dim3(C::NTHR), C::LDS, st, a);
+  return hipGetLastError();
+}
+
+template hipError_t launch_intra_bf16<64, 64>(const IntraBf16Args&, hipStream_t);
+template hipError_t launch_intra_bf16<64, 128>(const IntraBf16Args&, hipStream_t);
+template hipError_t launch_intra_bf16<128, 64>(const IntraBf16Args&, hipStream_t);
+template hipError_t launch_intra_bf16<128, 128>(const IntraBf16Args&, hipStream_t);
+
+}  // namespace gdr2

@@ -102,15 +102,54 @@ struct RecurArgs {
   float scale;
 };
 
-// Fused chunkwise scan of the bf16 path: intra-chunk WY products and the
-// inter-chunk state recurrence in one kernel, sequential over chunks.
-struct ScanFwdArgs {
+// ---------------------------------------------------------------------------
+// bf16 path workspace: per chunk-head ch (C = 64 tokens of one head), every
+// tile is stored in MFMA fragment order so that a wave loads a 16 x 32
+// operand block as one contiguous kilobyte (16 bytes per lane):
+//   standard fragment block (row R, key K):  lane l holds R = l % 16,
+//       K = 8 (l / 16) + e, e = 0..7;
+//   permuted fragment block:                 lane l holds R = l % 16,
+//       K = 4 (l / 16) + e (e < 4) and K = 16 + 4 (l / 16) + (e - 4) (e >= 4).
+// Split operands store the hi block and then the lo block (2 KB per block).
+//   Y    (64 x Dk)  bf16, permuted,  blocks [row block 4][key block Dk/32]
+//   Qg   (64 x Dk)  bf16 hi/lo, standard, blocks [4][Dk/32]
+//   Aqk  (64 x 64)  bf16 hi/lo, permuted, blocks [4][2] (causal, zeros above)
+//   KtT  (Dk x 64)  Ktail^T, bf16 hi/lo, standard, blocks [Dk/16][2]
+//   U    (64 x Dv)  fp32 accumulator tiles [Dv/16][4] x (64 lanes x 4):
+//                   lane l holds U[16 i + 4 (l / 16) + u][16 vb + l % 16]
+//   GC   (Dk)       gamma_C, fp32
+struct WsBf16 {
+  static constexpr size_t y(int dk) { return (size_t)4 * (dk / 32) * 1024; }
+  static constexpr size_t qg(int dk) { return (size_t)4 * (dk / 32) * 2048; }
+  static constexpr size_t aqk() { return (size_t)8 * 2048; }
+  static constexpr size_t ktt(int dk) { return (size_t)(dk / 16) * 2 * 2048; }
+  static constexpr size_t u(int dv) { return (size_t)(dv / 16) * 4 * 1024; }
+  static constexpr size_t gc(int dk) { return (size_t)((dk * 4 + 255) / 256) * 256; }
+};
+
+struct IntraBf16Args {
   const bf16_t* q;
   const bf16_t* k;
   const bf16_t* v;
   const float* g;
   const bf16_t* b;
   const bf16_t* w;
+  unsigned char* Y;
+  unsigned char* Qg;
+  unsigned char* Aqk;
+  unsigned char* KtT;
+  float* U;
+  float* GC;
+  int B, T, H, NT;
+};
+
+struct ScanArgs {
+  const unsigned char* Y;
+  const unsigned char* Qg;
+  const unsigned char* Aqk;
+  const unsigned char* KtT;
+  const float* U;
+  const float* GC;
   const float* S0;  // nullable
   float* ST;        // nullable
   bf16_t* o;        // written when the output is fused in
@@ -120,8 +159,10 @@ struct ScanFwdArgs {
   float scale;
 };
 
+template <int DK, int DV>
+hipError_t launch_intra_bf16(const IntraBf16Args& a, hipStream_t st);
 template <int DK, int DV, bool WITH_O, bool STORE_H>
-hipError_t launch_fwd_scan(const ScanFwdArgs& a, hipStream_t st);
+hipError_t launch_scan_bf16(const ScanArgs& a, hipStream_t st);
 
 template <int DK, int DV, typename TIn>
 hipError_t launch_fwd_intra(const IntraArgs<TIn>& a, int B, hipStream_t st);

@@ -1,0 +1,307 @@
+// Inter-chunk state scan of the bf16 path (gfx950): one 8-wave workgroup per
+// (sequence, head, 64-wide value slice) walks the chunks in order:
+//
+//   R  = U - Y S                                     eq. eq_app_residual_matrix
+//   O  = scale * (Q_g S + A_qk R)                    eq. eq_gdn2_chunk_output   [WITH_O]
+//   S <- Diag(gamma_C) S + Ktail^T R                 eq. eq_gdn2_chunk_state
+//
+// reading Y, Q_g, A_qk, Ktail^T, U and gamma_C that the intra-chunk kernel
+// left in fragment order.  The fp32 state slice lives in registers as MFMA
+// accumulators (plus a bf16 hi/lo copy in LDS for the products that read it);
+// the next chunk's operand blocks are fetched into registers while the
+// current chunk computes and copied to LDS at its end.  The two value slices
+// of one head run on the same XCD so that their shared reads hit one L2.
+// With STORE_H the chunk-start states and R are written for the backward.
+//
+// Precision: Y S uses the bf16 part of S (Y itself is bf16); every other
+// product is split hi/lo and fp32-accurate.
+
+#include "gdr2_kernels.hpp"
+#include "gdr2_bf16.hpp"
+
+namespace gdr2 {
+
+template <int DK, int DV>
+struct ScanCfg2 {
+  static constexpr int NTHR = 512;
+  static constexpr int DVS = DV < 64 ? DV : 64;
+  static constexpr int NS = DV / DVS;
+  static constexpr int KS = DK / 32, NCB = DK / 16, NVB = DVS / 16;
+  static constexpr int TPW = NCB * NVB / 8;  // state tiles per wave
+  static constexpr int LSS = DK + 8;         // S hi/lo [DVS][LSS] bf16
+  static constexpr int LR = 64 + 8;          // R hi/lo [DVS][LR] bf16
+  // operand blocks, copied verbatim (contiguous Y | Qg | Aqk | KtT)
+  static constexpr int SZ_Y = (int)WsBf16::y(DK), SZ_Q = (int)WsBf16::qg(DK);
+  static constexpr int SZ_A = (int)WsBf16::aqk(), SZ_K = (int)WsBf16::ktt(DK);
+  static constexpr int SZ_OP = SZ_Y + SZ_Q + SZ_A + SZ_K;
+  static constexpr int NSTG = SZ_OP / (16 * NTHR);  // 16-byte chunks per thread
+  static constexpr int OFF_S = 0;
+  static constexpr int OFF_R = OFF_S + 2 * DVS * LSS * 2;
+  static constexpr int OFF_OP = OFF_R + 2 * DVS * LR * 2;
+  static constexpr int LDS = OFF_OP + SZ_OP;
+  static_assert(SZ_OP % (16 * NTHR) == 0, "operand staging split");
+  static_assert(LDS <= 160 * 1024, "LDS budget");
+  static_assert(TPW >= 1 && NVB % 2 == 0, "wave split");
+};
+
+// B fragment of S for Y S in the permuted key order of Y's fragments:
+// S[c][v] for c = k0 + 4 g + u and k0 + 16 + 4 g + u (stored [v][c]).
+__device__ __forceinline__ bf8 ld_perm8(const __bf16* row, int k0, int g) {
+  const bf4 a = *reinterpret_cast<const bf4*>(row + k0 + 4 * g);
+  const bf4 b = *reinterpret_cast<const bf4*>(row + k0 + 16 + 4 * g);
+  bf8 r;
+  r[0] = a[0]; r[1] = a[1]; r[2] = a[2]; r[3] = a[3];
+  r[4] = b[0]; r[5] = b[1]; r[6] = b[2]; r[7] = b[3];
+  return r;
+}
+
+template <int DK, int DV, bool WITH_O, bool STORE_H>
+__global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
+  using C = ScanCfg2<DK, DV>;
+  constexpr int DVS = C::DVS, NS = C::NS, KS = C::KS, NCB = C::NCB, NVB = C::NVB, TPW = C::TPW;
+  constexpr int LSS = C::LSS, LR = C::LR, NSTG = C::NSTG;
+
+  extern __shared__ __align__(16) unsigned char smem[];
+  __bf16* sShi = reinterpret_cast<__bf16*>(smem + C::OFF_S);
+  __bf16* sSlo = sShi + DVS * LSS;
+  __bf16* sRhi = reinterpret_cast<__bf16*>(smem + C::OFF_R);
+  __bf16* sRlo = sRhi + DVS * LR;
+  unsigned char* sOp = smem + C::OFF_OP;
+  const unsigned char* sY = sOp;
+  const unsigned char* sQ = sY + C::SZ_Y;
+  const unsigned char* sA = sQ + C::SZ_Q;
+  const unsigned char* sK = sA + C::SZ_A;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, r16 = lane & 15;
+  const int T = a.T, H = a.H, NT = a.NT;
+
+  const int nseq = a.B * H;
+  int seq, slice;
+  if (NS > 1 && (nseq & 7) == 0) {
+    const int xcd = blockIdx.x & 7, j = blockIdx.x >> 3;
+    seq = (j / NS) * 8 + xcd;
+    slice = j % NS;
+  } else {
+    seq = blockIdx.x / NS;
+    slice = blockIdx.x % NS;
+  }
+  const int bb = seq / H, h = seq % H;
+  const int v0 = slice * DVS;
+  __bf16* O = reinterpret_cast<__bf16*>(a.o);
+  auto vofs = [&](int n, int r) -> size_t {
+    return ((size_t)bb * T + (size_t)n * CH + r) * ((size_t)H * DV) + (size_t)h * DV + v0;
+  };
+
+  // wave roles
+  const int iO = wave >> 1;                 // row block of the R / O tiles
+  const int vbO = (wave & 1) * (NVB / 2);   // their value blocks (slice-local)
+  const int cs = wave % NCB;                // key block of the state tiles
+  const int sv0 = (wave / NCB) * TPW;       // their value blocks
+
+  // ---- operand staging (global -> registers -> LDS).  Thread t moves bytes
+  // 8192 m + 16 t of the concatenated Y | Qg | Aqk | KtT blocks; every region is
+  // a multiple of 8 KB, so the source region of slice m is known at compile time.
+  constexpr int SLICE = 16 * C::NTHR;
+  constexpr int E_Y = C::SZ_Y / SLICE, E_Q = E_Y + C::SZ_Q / SLICE, E_A = E_Q + C::SZ_A / SLICE;
+  static_assert(C::SZ_Y % SLICE == 0 && C::SZ_Q % SLICE == 0 && C::SZ_A % SLICE == 0 && C::SZ_K % SLICE == 0,
+                "regions are whole staging slices");
+  u4v stg[NSTG];
+  f4 ucur[NVB / 2], unext[NVB / 2];
+  float gcur[4], gnext[4];
+  const size_t chs = (size_t)seq * NT;
+#define GDR2_LOAD_OPS(CHX)                                                                                   \
+  _Pragma("unroll") for (int m = 0; m < NSTG; ++m) {                                                     \
+    const unsigned char* src;                                                                            \
+    if (m < E_Y)                                                                                         \
+      src = a.Y + (CHX) * C::SZ_Y + m * SLICE;                                                           \
+    else if (m < E_Q)                                                                                    \
+      src = a.Qg + (CHX) * C::SZ_Q + (m - E_Y) * SLICE;                                                  \
+    else if (m < E_A)                                                                                    \
+      src = a.Aqk + (CHX) * C::SZ_A + (m - E_Q) * SLICE;                                                 \
+    else                                                                                                 \
+      src = a.KtT + (CHX) * C::SZ_K + (m - E_A) * SLICE;                                                 \
+    stg[m] = ldg16(src + 16 * tid);                                            \
+  }
+#define GDR2_STORE_OPS()                                                                                     \
+  _Pragma("unroll") for (int m = 0; m < NSTG; ++m) sts16(sOp + m * SLICE + 16 * tid, stg[m]);
+  // U tiles (value blocks vbO.., row block iO) and gamma_C rows of the state tiles
+#define GDR2_LOAD_UG(CHX, UARR, GARR)                                                                        \
+  _Pragma("unroll") for (int t = 0; t < NVB / 2; ++t) {                                                  \
+    const int vb_ = v0 / 16 + vbO + t;                                                                   \
+    UARR[t] = *reinterpret_cast<const f4*>(a.U + (CHX) * (WsBf16::u(DV) / 4) +                           \
+                                           ((size_t)(vb_ * 4 + iO) * 64 + lane) * 4);                    \
+  }                                                                                                      \
+  _Pragma("unroll") for (int u2 = 0; u2 < 4; ++u2) GARR[u2] =                                            \
+      a.GC[(CHX) * (WsBf16::gc(DK) / 4) + 16 * cs + 4 * g + u2];
+
+  // ---- state
+  f4 sreg[TPW];
+#pragma unroll
+  for (int t = 0; t < TPW; ++t) {
+    const int vb = sv0 + t;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int c = 16 * cs + 4 * g + u, v = 16 * vb + r16;
+      sreg[t][u] = a.S0 ? a.S0[((size_t)seq * DK + c) * DV + v0 + v] : 0.f;
+    }
+    st4split(sShi + (16 * vb + r16) * LSS + 16 * cs + 4 * g, sSlo + (16 * vb + r16) * LSS + 16 * cs + 4 * g,
+             sreg[t]);
+  }
+  GDR2_LOAD_OPS(chs)
+  GDR2_LOAD_UG(chs, ucur, gcur)
+  GDR2_STORE_OPS()
+  __syncthreads();
+
+  for (int n = 0; n < NT; ++n) {
+    const size_t ch = chs + n;
+    if (n + 1 < NT) {
+      GDR2_LOAD_OPS(ch + 1)
+      GDR2_LOAD_UG(ch + 1, unext, gnext)
+    }
+
+    // ---- R = U - Y S
+    f4 racc[NVB / 2];
+#pragma unroll
+    for (int t = 0; t < NVB / 2; ++t) racc[t] = ucur[t];
+#pragma unroll
+    for (int p = 0; p < KS; ++p) {
+      const bf8 yf = neg8(ld8(reinterpret_cast<const __bf16*>(sY + (iO * KS + p) * 1024 + 16 * lane)));
+#pragma unroll
+      for (int t = 0; t < NVB / 2; ++t) {
+        const int vb = vbO + t;
+        racc[t] = mma(yf, ld_perm8(sShi + (16 * vb + r16) * LSS, 32 * p, g), racc[t]);
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < NVB / 2; ++t) {
+      const int vb = vbO + t;
+      st4split(sRhi + (16 * vb + r16) * LR + 16 * iO + 4 * g, sRlo + (16 * vb + r16) * LR + 16 * iO + 4 * g,
+               racc[t]);
+      if (STORE_H) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) a.Rs[(ch * CH + 16 * iO + 4 * g + u) * DV + v0 + 16 * vb + r16] = racc[t][u];
+      }
+    }
+    __syncthreads();
+
+    // ---- O^T = S^T Q_g^T + R^T A_qk^T  (lane: O[16 iO + r16][16 vb + 4 g + u])
+    if (WITH_O) {
+      f4 accO[NVB / 2];
+#pragma unroll
+      for (int t = 0; t < NVB / 2; ++t) accO[t] = f4zero();
+#pragma unroll
+      for (int p = 0; p < KS; ++p) {
+        Fr qf;
+        qf.hi = ld8(reinterpret_cast<const __bf16*>(sQ + (iO * KS + p) * 2048 + 16 * lane));
+        qf.lo = ld8(reinterpret_cast<const __bf16*>(sQ + (iO * KS + p) * 2048 + 1024 + 16 * lane));
+#pragma unroll
+        for (int t = 0; t < NVB / 2; ++t) {
+          const int vb = vbO + t;
+          Fr sf;
+          sf.hi = ld8(sShi + (16 * vb + r16) * LSS + 32 * p + 8 * g);
+          sf.lo = ld8(sSlo + (16 * vb + r16) * LSS + 32 * p + 8 * g);
+          accO[t] = mma3(sf, qf, accO[t]);
+        }
+      }
+#pragma unroll
+      for (int kb = 0; kb <= (iO >> 1); ++kb) {
+        Fr af;
+        af.hi = ld8(reinterpret_cast<const __bf16*>(sA + (iO * 2 + kb) * 2048 + 16 * lane));
+        af.lo = ld8(reinterpret_cast<const __bf16*>(sA + (iO * 2 + kb) * 2048 + 1024 + 16 * lane));
+#pragma unroll
+        for (int t = 0; t < NVB / 2; ++t) {
+          const int vb = vbO + t;
+          Fr rf;
+          rf.hi = ld_perm8(sRhi + (16 * vb + r16) * LR, 32 * kb, g);
+          rf.lo = ld_perm8(sRlo + (16 * vb + r16) * LR, 32 * kb, g);
+          accO[t] = mma3(rf, af, accO[t]);
+        }
+      }
+      const float sc = a.scale;
+#pragma unroll
+      for (int t = 0; t < NVB / 2; ++t) {
+        const int vb = vbO + t;
+        st4(O + vofs(n, 16 * iO + r16) + 16 * vb + 4 * g, sc * accO[t][0], sc * accO[t][1], sc * accO[t][2],
+            sc * accO[t][3]);
+      }
+    }
+
+    // ---- S <- Diag(gamma_C) S + Ktail^T R
+    if (STORE_H) {
+#pragma unroll
+      for (int t = 0; t < TPW; ++t)
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          a.Hs[(ch * DK + 16 * cs + 4 * g + u) * DV + v0 + 16 * (sv0 + t) + r16] = sreg[t][u];
+    }
+#pragma unroll
+    for (int t = 0; t < TPW; ++t)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) sreg[t][u] *= gcur[u];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      Fr kf;
+      kf.hi = ld8(reinterpret_cast<const __bf16*>(sK + (cs * 2 + kb) * 2048 + 16 * lane));
+      kf.lo = ld8(reinterpret_cast<const __bf16*>(sK + (cs * 2 + kb) * 2048 + 1024 + 16 * lane));
+#pragma unroll
+      for (int t = 0; t < TPW; ++t) {
+        const int vb = sv0 + t;
+        Fr rf;
+        rf.hi = ld8(sRhi + (16 * vb + r16) * LR + 32 * kb + 8 * g);
+        rf.lo = ld8(sRlo + (16 * vb + r16) * LR + 32 * kb + 8 * g);
+        sreg[t] = mma3(kf, rf, sreg[t]);
+      }
+    }
+    __syncthreads();
+
+    // ---- new S and the next chunk's operands to LDS
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) {
+      const int vb = sv0 + t;
+      st4split(sShi + (16 * vb + r16) * LSS + 16 * cs + 4 * g, sSlo + (16 * vb + r16) * LSS + 16 * cs + 4 * g,
+               sreg[t]);
+    }
+    if (n + 1 < NT) {
+      GDR2_STORE_OPS()
+#pragma unroll
+      for (int t = 0; t < NVB / 2; ++t) ucur[t] = unext[t];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) gcur[u] = gnext[u];
+    }
+    __syncthreads();
+  }
+
+#undef GDR2_LOAD_OPS
+#undef GDR2_STORE_OPS
+#undef GDR2_LOAD_UG
+  if (a.ST) {
+#pragma unroll
+    for (int t = 0; t < TPW; ++t)
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        a.ST[((size_t)seq * DK + 16 * cs + 4 * g + u) * DV + v0 + 16 * (sv0 + t) + r16] = sreg[t][u];
+  }
+}
+
+template <int DK, int DV, bool WITH_O, bool STORE_H>
+hipError_t launch_scan_bf16(const ScanArgs& a, hipStream_t st) {
+  using C = ScanCfg2<DK, DV>;
+  const void* fn = reinterpret_cast<const void*>(&scan_bf16_kernel<DK, DV, WITH_O, STORE_H>);
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+  if (e != hipSuccess) return e;
+  dim3 grid(a.B * a.H * C::NS);
+  hipLaunchKernelGGL((scan_bf16_kernel<DK, DV, WITH_O, STORE_H>), grid, dim3(C::NTHR), C::LDS, st, a);
+  return hipGetLastError();
+}
+
+#define GDR2_INST_SCAN2(DK, DV)                                                          \
+  template hipError_t launch_scan_bf16<DK, DV, true, false>(const ScanArgs&, hipStream_t); \
+  template hipError_t launch_scan_bf16<DK, DV, false, true>(const ScanArgs&, hipStream_t);
+
+GDR2_INST_SCAN2(64, 64)
+GDR2_INST_SCAN2(64, 128)
+GDR2_INST_SCAN2(128, 64)
+GDR2_INST_SCAN2(128, 128)
+
+}  // namespace gdr2

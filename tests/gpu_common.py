@@ -69,3 +69,62 @@ def ws_view(ws, lay, name, shape):
     torch = torch_mod()
     off, nf = lay[name]
     return ws[off:off + nf * 4].view(torch.float32).view(*shape)
+
+
+# --------------------------------------------------------------------------- bf16 path workspace
+def bf16_bits_to_f32(u16):
+    """uint16 bfloat16 bit patterns -> float32 (exact)."""
+    return (u16.astype(np.uint32) << 16).view(np.float32)
+
+
+def ws_layout_bf16(B, T, H, Dk, Dv):
+    """Byte offsets / per-chunk-head sizes of the bf16 forward workspace regions
+    (mirrors WsBf16 in the library: fragment-ordered tiles)."""
+    NC = B * H * (T // CH)
+    gc = (Dk * 4 + 255) // 256 * 256
+    sizes = [("Y", 4 * (Dk // 32) * 1024), ("Qg", 4 * (Dk // 32) * 2048), ("Aqk", 8 * 2048),
+             ("KtT", (Dk // 16) * 2 * 2048), ("U", (Dv // 16) * 4 * 1024), ("GC", gc)]
+    off, out = 0, {}
+    for n, per in sizes:
+        out[n] = (off, per)
+        off += (NC * per + 255) // 256 * 256
+    return out, off, NC
+
+
+def _frag_index(permuted):
+    """(lane, e) -> (row, key) inside one 16 x 32 fragment block."""
+    lane = np.arange(64)[:, None]
+    e = np.arange(8)[None, :]
+    row = np.broadcast_to(lane % 16, (64, 8))
+    if permuted:
+        key = np.where(e < 4, 4 * (lane // 16) + e, 16 + 4 * (lane // 16) + (e - 4))
+    else:
+        key = 8 * (lane // 16) + e
+    return row, np.broadcast_to(key, (64, 8))
+
+
+def decode_frag_blocks(raw_u16, nrb, nkb, split, permuted):
+    """raw bf16 bits of one chunk-head region -> dense (16 nrb, 32 nkb) matrix
+    (hi + lo when split)."""
+    planes = 2 if split else 1
+    blocks = raw_u16.reshape(nrb, nkb, planes, 64, 8)
+    vals = bf16_bits_to_f32(blocks).astype(np.float64)
+    vals = vals.sum(axis=2) if split else vals[:, :, 0]
+    row, key = _frag_index(permuted)
+    out = np.zeros((16 * nrb, 32 * nkb))
+    for rb in range(nrb):
+        for kb in range(nkb):
+            out[16 * rb + row, 32 * kb + key] = vals[rb, kb]
+    return out
+
+
+def decode_u_tiles(raw_f32, Dv):
+    """fp32 accumulator tiles [Dv/16][4] x (64 lanes x 4) -> dense (64, Dv)."""
+    t = raw_f32.reshape(Dv // 16, 4, 64, 4)
+    lane = np.arange(64)
+    out = np.zeros((64, Dv))
+    for vb in range(Dv // 16):
+        for i in range(4):
+            for u in range(4):
+                out[16 * i + 4 * (lane // 16) + u, 16 * vb + lane % 16] = t[vb, i, :, u]
+    return out

@@ -140,18 +140,28 @@ def test_recurrent_validation():
         assert _rec(_prob(T=1), ptrs={idx: None}) == g2.GDR2_EINVAL
 
 
-def test_workspace_size_and_check():
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_workspace_size_and_check(dtype):
     p = _prob(B=2, T=256, H=4, Dk=128, Dv=64)
+    p.dtype = g2.GDR2_FP32 if dtype == "fp32" else g2.GDR2_BF16
     fwd = g2.gdr2_chunk_workspace_bytes(p, 0)
     bwd = g2.gdr2_chunk_workspace_bytes(p, 1)
     NC = 2 * 4 * (256 // 64)
-    r = lambda n: (n * 4 + 255) // 256 * 256
-    exp_fwd = r(NC * 64 * 128) + r(NC * 64 * 64) + 2 * r(NC * 64 * 128) + r(NC * 64 * 64) + r(NC * 128)
-    exp_bwd = exp_fwd + 2 * r(NC * 128 * 64) + 2 * r(NC * 64 * 64) + 2 * r(NC * 64 * 64) + r(NC * 64 * 128)
+    r = lambda n: (n * 4 + 255) // 256 * 256      # fp32 tiles, 256-byte aligned regions
+    rb = lambda n: (n + 255) // 256 * 256         # byte regions
+    fwd32 = r(NC * 64 * 128) + r(NC * 64 * 64) + 2 * r(NC * 64 * 128) + r(NC * 64 * 64) + r(NC * 128)
+    exp_bwd = fwd32 + 2 * r(NC * 128 * 64) + 2 * r(NC * 64 * 64) + 2 * r(NC * 64 * 64) + r(NC * 64 * 128)
+    if dtype == "fp32":
+        exp_fwd = fwd32
+    else:
+        # fragment-ordered bf16 tiles: Y, Qg (hi/lo), A_qk (hi/lo), Ktail^T (hi/lo), U (fp32), gamma_C
+        exp_fwd = (rb(NC * 4 * 4 * 1024) + rb(NC * 4 * 4 * 2048) + rb(NC * 8 * 2048) + rb(NC * 8 * 2 * 2048)
+                   + rb(NC * 4 * 4 * 1024) + rb(NC * 512))
     assert fwd == exp_fwd and bwd == exp_bwd
     assert _fwd(p, ws_bytes=fwd - 1) == g2.GDR2_EWORKSPACE
     assert _bwd(p, ws_bytes=bwd - 1) == g2.GDR2_EWORKSPACE
-    assert _bwd(p, ws_bytes=fwd) == g2.GDR2_EWORKSPACE
+    if bwd > fwd:
+        assert _bwd(p, ws_bytes=fwd) == g2.GDR2_EWORKSPACE
 
 
 def test_bf16_round_is_nearest_even():

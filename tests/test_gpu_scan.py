@@ -93,3 +93,52 @@ def test_bf16_state_passing():
     # the split is exact up to fp32 rounding of the hand-over state
     assert rel_l2(np.concatenate([host(o1), host(o2)], axis=1), host(o_all)) < 1e-3
     assert rel_l2(host(S2), host(S_all)) < 1e-5
+
+
+@pytest.mark.parametrize("Dk,Dv", [(64, 128), (128, 128)])
+def test_bf16_workspace_intermediates(Dk, Dv):
+    """Fragment-ordered workspace of the intra-chunk kernel against App. A's chunk
+    algebra: Q_g, Ktail, A_qk, gamma_C are fp32-accurate (split hi/lo); Y and U
+    carry the bf16 solve side of A (and Y its own bf16 storage)."""
+    import torch
+    from oracle.chunkwise import gdr2_chunk_fwd_ref
+    from tests.gpu_common import ws_layout_bf16, decode_frag_blocks, decode_u_tiles, CH
+    B, T, H = 1, 192, 2
+    d = make_inputs(B, T, H, Dk, Dv, seed=79, dtype="bf16", s0_std=0.05)
+    lay, total, NC = ws_layout_bf16(B, T, H, Dk, Dv)
+    ws = torch.full((total,), 0xFF, dtype=torch.uint8, device="cuda")
+    _case(f"bf16 workspace intermediates Dk{Dk} Dv{Dv}")
+    import paper_2605_22791_amd as g2
+    x = dev_inputs(d)
+    g2.gdr2_chunk_fwd(x["q"], x["k"], x["v"], x["log_alpha"], x["b"], x["w"], x["S0"], scale=d["scale"], ws=ws)
+    torch.cuda.synchronize()
+    raw = ws.cpu().numpy()
+    _, _, it = gdr2_chunk_fwd_ref(d["q"], d["k"], d["v"], d["log_alpha"], d["b"], d["w"], d["S0"], d["scale"],
+                                  C=CH, keep=True)
+    NT = T // CH
+    worst = {}
+    for ch in range(NC):
+        bh, n = divmod(ch, NT)
+        bi, hi = divmod(bh, H)
+
+        def region(name):
+            off, per = lay[name]
+            return raw[off + ch * per: off + (ch + 1) * per]
+
+        got = {
+            "Y": decode_frag_blocks(region("Y").view(np.uint16), 4, Dk // 32, False, True),
+            "Qg": decode_frag_blocks(region("Qg").view(np.uint16), 4, Dk // 32, True, False),
+            "Aqk": decode_frag_blocks(region("Aqk").view(np.uint16), 4, 2, True, True),
+            "Kt": decode_frag_blocks(region("KtT").view(np.uint16), Dk // 16, 2, True, False).T,
+            "U": decode_u_tiles(region("U").view(np.float32), Dv),
+            "GC": region("GC").view(np.float32)[:Dk].astype(np.float64),
+        }
+        ref = {"Y": it["Y"][bi, hi, n], "Qg": it["Qg"][bi, hi, n], "Aqk": it["Aqk"][bi, hi, n],
+               "Kt": it["Ktail"][bi, hi, n], "U": it["U"][bi, hi, n], "GC": it["gC"][bi, hi, n]}
+        for k_ in ref:
+            worst[k_] = max(worst.get(k_, 0.0), rel_l2(got[k_], ref[k_]))
+    print({k_: f"{v_:.2e}" for k_, v_ in worst.items()})
+    for k_ in ("Qg", "Aqk", "Kt", "GC"):
+        assert worst[k_] < 1e-4, (k_, worst[k_])
+    for k_ in ("Y", "U"):
+        assert worst[k_] < 1e-2, (k_, worst[k_])
