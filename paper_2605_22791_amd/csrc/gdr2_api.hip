@@ -53,7 +53,12 @@ Layout layout(const gdr2_problem* p, bool bwd) {
   const size_t Dk = p->Dk, Dv = p->Dv;
   Layout L{};
   size_t off = 0;
-  if (p->dtype == GDR2_BF16 && !bwd) {
+  auto take = [&](size_t floats) {
+    const size_t at = off;
+    off += round_up(floats * sizeof(float));
+    return at;
+  };
+  if (p->dtype == GDR2_BF16) {
     auto takeb = [&](size_t bytes) {
       const size_t at = off;
       off += round_up(bytes);
@@ -65,20 +70,14 @@ Layout layout(const gdr2_problem* p, bool bwd) {
     L.bK = takeb(NC * WsBf16::ktt(p->Dk));
     L.bU = takeb(NC * WsBf16::u(p->Dv));
     L.bG = takeb(NC * WsBf16::gc(p->Dk));
-    L.total = off;
-    return L;
+  } else {
+    L.Y = take(NC * CH * Dk);
+    L.U = take(NC * CH * Dv);
+    L.Kt = take(NC * CH * Dk);
+    L.Qg = take(NC * CH * Dk);
+    L.Aqk = take(NC * CH * CH);
+    L.GC = take(NC * Dk);
   }
-  auto take = [&](size_t floats) {
-    const size_t at = off;
-    off += round_up(floats * sizeof(float));
-    return at;
-  };
-  L.Y = take(NC * CH * Dk);
-  L.U = take(NC * CH * Dv);
-  L.Kt = take(NC * CH * Dk);
-  L.Qg = take(NC * CH * Dk);
-  L.Aqk = take(NC * CH * CH);
-  L.GC = take(NC * Dk);
   if (bwd) {
     L.Hs = take(NC * Dk * Dv);
     L.Rs = take(NC * CH * Dv);
@@ -210,6 +209,34 @@ struct BwdRun {
                         float* dg, void* db, void* dw, float* dS0, void* ws, hipStream_t st) {
     const Layout L = layout(p, true);
     const int NT = p->T / CH;
+    if (std::is_same<TIn, bf16_t>::value) {
+      // recompute: intra-chunk tiles, then the forward scan storing the chunk states and R
+      IntraBf16Args ia{static_cast<const bf16_t*>(q), static_cast<const bf16_t*>(k),
+                       static_cast<const bf16_t*>(v), g, static_cast<const bf16_t*>(b),
+                       static_cast<const bf16_t*>(w), at<unsigned char>(ws, L.bY),
+                       at<unsigned char>(ws, L.bQ), at<unsigned char>(ws, L.bA),
+                       at<unsigned char>(ws, L.bK), at<float>(ws, L.bU), at<float>(ws, L.bG),
+                       p->B, p->T, p->H, NT};
+      hipError_t e = timed(GDR2_K_BWD_RECOMPUTE_INTRA, st, [&] { return launch_intra_bf16<DK, DV>(ia, st); });
+      if (e != hipSuccess) return e;
+      ScanArgs sa{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.U, ia.GC, S0, nullptr, nullptr, at<float>(ws, L.Hs),
+                  at<float>(ws, L.Rs), p->B, p->T, p->H, NT, p->scale};
+      e = timed(GDR2_K_BWD_RECOMPUTE_STATE, st, [&] { return launch_scan_bf16<DK, DV, false, true>(sa, st); });
+      if (e != hipSuccess) return e;
+      BScanArgs ba{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.GC, static_cast<const bf16_t*>(dout), dST, dS0,
+                   at<float>(ws, L.DH), at<float>(ws, L.DR), p->B, p->T, p->H, NT, p->scale};
+      e = timed(GDR2_K_BWD_STATE, st, [&] { return launch_bscan_bf16<DK, DV>(ba, st); });
+      if (e != hipSuccess) return e;
+      BwdChunkArgs<TIn> ca{static_cast<const TIn*>(q), static_cast<const TIn*>(k), static_cast<const TIn*>(v), g,
+                           static_cast<const TIn*>(b), static_cast<const TIn*>(w), static_cast<const TIn*>(dout),
+                           at<float>(ws, L.Hs), at<float>(ws, L.DH), at<float>(ws, L.Rs), at<float>(ws, L.DR),
+                           at<float>(ws, L.DAqk), at<float>(ws, L.DT), at<float>(ws, L.DEg), static_cast<TIn*>(dq),
+                           static_cast<TIn*>(dk), static_cast<TIn*>(dv), static_cast<TIn*>(db),
+                           static_cast<TIn*>(dw), dg, p->T, p->H, NT, p->scale};
+      e = timed(GDR2_K_BWD_WY, st, [&] { return launch_bwd_wy<DK, DV, TIn>(ca, p->B, st); });
+      if (e != hipSuccess) return e;
+      return timed(GDR2_K_BWD_INTRA, st, [&] { return launch_bwd_intra<DK, DV, TIn>(ca, p->B, st); });
+    }
     IntraArgs<TIn> ia{static_cast<const TIn*>(q), static_cast<const TIn*>(k),
                       static_cast<const TIn*>(v), g, static_cast<const TIn*>(b),
                       static_cast<const TIn*>(w), at<float>(ws, L.Y), at<float>(ws, L.U),

@@ -146,6 +146,19 @@ __device__ __forceinline__ bf8 ld_tr8(const __bf16* X, int ld, int k0, int n0, i
   return r;
 }
 
+// Transposed fragment from two per-lane addresses: p0 points at the 4
+// consecutive elements (row 8G + i, cols 4q..4q+3) that lane 4i + q of group
+// G contributes for rows 0..3 of its group, p1 at rows 4..7.  Used where the
+// source tile is stored in fragment order rather than row-major.
+__device__ __forceinline__ bf8 ld_tr8p(const __bf16* p0, const __bf16* p1) {
+  const bf4 a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((GDR2_LDS bf4*)(p0));
+  const bf4 b = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((GDR2_LDS bf4*)(p1));
+  bf8 r;
+  r[0] = a[0]; r[1] = a[1]; r[2] = a[2]; r[3] = a[3];
+  r[4] = b[0]; r[5] = b[1]; r[6] = b[2]; r[7] = b[3];
+  return r;
+}
+
 // v_mfma_f32_16x16x4_f32: lane l supplies A[l%16][l/16] and B[l/16][l%16].
 __device__ __forceinline__ f4 mfma_f32(float a, float b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);

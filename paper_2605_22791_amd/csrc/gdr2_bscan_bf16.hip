@@ -1,0 +1,292 @@
+// Reverse inter-chunk scan of the bf16 backward (gfx950), App. B.1: one
+// 8-wave workgroup per (sequence, head, 64-wide value slice) walks the chunks
+// from last to first, carrying dS (the gradient of the chunk's end state):
+//
+//   dR  = scale * A_qk^T dO + Ktail dS
+//   dS <- Diag(gamma_C) dS + scale * Q_g^T dO - Y^T dR
+//
+// writing dS before each update (the gradient of that chunk's end state), dR,
+// and finally dS0.  The operands are the forward's fragment-ordered tiles
+// (gdr2_kernels.hpp): the transposed fragments these products need come out
+// of the same LDS blocks through ds_read_b64_tr_b16 with per-lane addresses,
+// since every 4 consecutive elements of a block row are contiguous.
+//
+// Precision: every product is fp32-accurate (split hi/lo; dO and Y are exact
+// bf16 and keep a single part).
+
+#include "gdr2_kernels.hpp"
+#include "gdr2_bf16.hpp"
+
+namespace gdr2 {
+
+template <int DK, int DV>
+struct BScanCfg {
+  static constexpr int NTHR = 512;
+  static constexpr int DVS = DV < 64 ? DV : 64;
+  static constexpr int NS = DV / DVS;
+  static constexpr int KS = DK / 32, NCB = DK / 16, NVB = DVS / 16;
+  static constexpr int TPW = NCB * NVB / 8;
+  static constexpr int LSD = DK + 8;   // dS hi/lo [DVS][LSD]
+  static constexpr int LDR = 64 + 8;   // dR hi/lo [DVS][LDR]
+  static constexpr int LDO = DVS + 8;  // dO [64][LDO]
+  static constexpr int SZ_Y = (int)WsBf16::y(DK), SZ_Q = (int)WsBf16::qg(DK);
+  static constexpr int SZ_A = (int)WsBf16::aqk(), SZ_K = (int)WsBf16::ktt(DK);
+  static constexpr int SZ_OP = SZ_Y + SZ_Q + SZ_A + SZ_K;
+  static constexpr int SLICE = 16 * NTHR;
+  static constexpr int NSTG = SZ_OP / SLICE;
+  static constexpr int OFF_D = 0;
+  static constexpr int OFF_R = OFF_D + 2 * DVS * LSD * 2;
+  static constexpr int OFF_O = OFF_R + 2 * DVS * LDR * 2;
+  static constexpr int OFF_OP = OFF_O + 64 * LDO * 2;
+  static constexpr int LDS = OFF_OP + SZ_OP;
+  static_assert(SZ_Y % SLICE == 0 && SZ_Q % SLICE == 0 && SZ_A % SLICE == 0 && SZ_K % SLICE == 0,
+                "regions are whole staging slices");
+  static_assert(64 * DVS * 2 == SLICE, "one dO chunk per thread");
+  static_assert(LDS <= 160 * 1024, "LDS budget");
+  static_assert(TPW >= 1 && NVB % 2 == 0, "wave split");
+};
+
+template <int DK, int DV>
+__global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
+  using C = BScanCfg<DK, DV>;
+  constexpr int DVS = C::DVS, NS = C::NS, KS = C::KS, NCB = C::NCB, NVB = C::NVB, TPW = C::TPW;
+  constexpr int LSD = C::LSD, LDR = C::LDR, LDO = C::LDO, NSTG = C::NSTG, SLICE = C::SLICE;
+  constexpr int E_Y = C::SZ_Y / SLICE, E_Q = E_Y + C::SZ_Q / SLICE, E_A = E_Q + C::SZ_A / SLICE;
+
+  extern __shared__ __align__(16) unsigned char smem[];
+  __bf16* sDhi = reinterpret_cast<__bf16*>(smem + C::OFF_D);
+  __bf16* sDlo = sDhi + DVS * LSD;
+  __bf16* sRhi = reinterpret_cast<__bf16*>(smem + C::OFF_R);
+  __bf16* sRlo = sRhi + DVS * LDR;
+  __bf16* sdO = reinterpret_cast<__bf16*>(smem + C::OFF_O);
+  unsigned char* sOp = smem + C::OFF_OP;
+  const unsigned char* sY = sOp;
+  const unsigned char* sQ = sY + C::SZ_Y;
+  const unsigned char* sA = sQ + C::SZ_Q;
+  const unsigned char* sK = sA + C::SZ_A;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, r16 = lane & 15;
+  const int qq = r16 & 3, ii = r16 >> 2;  // transpose-load role of this lane (4 ii + qq)
+  const int T = a.T, H = a.H, NT = a.NT;
+
+  const int nseq = a.B * H;
+  int seq, slice;
+  if (NS > 1 && (nseq & 7) == 0) {
+    const int xcd = blockIdx.x & 7, j = blockIdx.x >> 3;
+    seq = (j / NS) * 8 + xcd;
+    slice = j % NS;
+  } else {
+    seq = blockIdx.x / NS;
+    slice = blockIdx.x % NS;
+  }
+  const int bb = seq / H, h = seq % H;
+  const int v0 = slice * DVS;
+  const __bf16* dO = reinterpret_cast<const __bf16*>(a.dout);
+
+  const int iO = wave >> 1;                // row block of the dR tiles
+  const int vbO = (wave & 1) * (NVB / 2);  // their value blocks
+  const int cs = wave % NCB;               // key block of the dS tiles
+  const int sv0 = (wave / NCB) * TPW;      // their value blocks
+
+  // ---- staging: operand blocks, the dO slice and gamma_C of one chunk
+  u4v stg[NSTG], sto;
+  float gcur[4], gnext[4];
+  const size_t chs = (size_t)seq * NT;
+#define GDR2_LOAD_CHUNK(N_)                                                                               \
+  {                                                                                                    \
+    const size_t chx = chs + (N_);                                                                     \
+    _Pragma("unroll") for (int m = 0; m < NSTG; ++m) {                                                 \
+      const unsigned char* src;                                                                        \
+      if (m < E_Y)                                                                                     \
+        src = a.Y + chx * C::SZ_Y + m * SLICE;                                                         \
+      else if (m < E_Q)                                                                                \
+        src = a.Qg + chx * C::SZ_Q + (m - E_Y) * SLICE;                                                \
+      else if (m < E_A)                                                                                \
+        src = a.Aqk + chx * C::SZ_A + (m - E_Q) * SLICE;                                               \
+      else                                                                                             \
+        src = a.KtT + chx * C::SZ_K + (m - E_A) * SLICE;                                               \
+      stg[m] = ldg16(src + 16 * tid);                                                                  \
+    }                                                                                                  \
+    const int r_ = tid / (DVS / 8), c8_ = (tid % (DVS / 8)) * 8;                                       \
+    sto = ldg16(dO + ((size_t)bb * T + (size_t)(N_) * CH + r_) * ((size_t)H * DV) + (size_t)h * DV + v0 + c8_); \
+    _Pragma("unroll") for (int u2 = 0; u2 < 4; ++u2) gnext[u2] =                                       \
+        a.GC[chx * (WsBf16::gc(DK) / 4) + 16 * cs + 4 * g + u2];                                       \
+  }
+#define GDR2_STORE_CHUNK()                                                                               \
+  {                                                                                                    \
+    _Pragma("unroll") for (int m = 0; m < NSTG; ++m) sts16(sOp + m * SLICE + 16 * tid, stg[m]);        \
+    const int r_ = tid / (DVS / 8), c8_ = (tid % (DVS / 8)) * 8;                                       \
+    sts16(sdO + r_ * LDO + c8_, sto);                                                                  \
+    _Pragma("unroll") for (int u2 = 0; u2 < 4; ++u2) gcur[u2] = gnext[u2];                             \
+  }
+
+  // ---- dS: tiles (key block cs, value blocks sv0..) as fp32 accumulators
+  f4 sreg[TPW];
+#pragma unroll
+  for (int t = 0; t < TPW; ++t) {
+    const int vb = sv0 + t;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int c = 16 * cs + 4 * g + u, v = 16 * vb + r16;
+      sreg[t][u] = a.dST ? a.dST[((size_t)seq * DK + c) * DV + v0 + v] : 0.f;
+    }
+    st4split(sDhi + (16 * vb + r16) * LSD + 16 * cs + 4 * g, sDlo + (16 * vb + r16) * LSD + 16 * cs + 4 * g,
+             sreg[t]);
+  }
+  GDR2_LOAD_CHUNK(NT - 1)
+  GDR2_STORE_CHUNK()
+  __syncthreads();
+
+  for (int n = NT - 1; n >= 0; --n) {
+    const size_t ch = chs + n;
+    if (n > 0) GDR2_LOAD_CHUNK(n - 1)
+    // gradient of this chunk's end state
+#pragma unroll
+    for (int t = 0; t < TPW; ++t)
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        a.DH[(ch * DK + 16 * cs + 4 * g + u) * DV + v0 + 16 * (sv0 + t) + r16] = sreg[t][u];
+
+    // ---- dR = scale * A_qk^T dO + Ktail dS   (tiles: row block iO, value blocks vbO..)
+    f4 racc[NVB / 2], aacc[NVB / 2];
+#pragma unroll
+    for (int t = 0; t < NVB / 2; ++t) {
+      racc[t] = f4zero();
+      aacc[t] = f4zero();
+    }
+#pragma unroll
+    for (int p = 0; p < KS; ++p) {
+      // Ktail[r][c], r = 16 iO + r16, c = 32 p + 8 g + e, from the Ktail^T blocks
+      Fr kf;
+      {
+        const int c0 = 32 * p + 8 * g + ii;
+        const int boff = ((c0 >> 4) * 2 + (iO >> 1)) * 2048 +
+                         ((c0 & 15) + 16 * (2 * (iO & 1) + (qq >> 1))) * 16 + 8 * (qq & 1);
+        const __bf16* p0 = reinterpret_cast<const __bf16*>(sK + boff);
+        kf.hi = ld_tr8p(p0, p0 + 32);  // +4 rows of c = +4 lanes = 64 bytes
+        kf.lo = ld_tr8p(p0 + 512, p0 + 512 + 32);
+      }
+#pragma unroll
+      for (int t = 0; t < NVB / 2; ++t) {
+        const int vb = vbO + t;
+        Fr df;
+        df.hi = ld8(sDhi + (16 * vb + r16) * LSD + 32 * p + 8 * g);
+        df.lo = ld8(sDlo + (16 * vb + r16) * LSD + 32 * p + 8 * g);
+        racc[t] = mma3(kf, df, racc[t]);
+      }
+    }
+#pragma unroll
+    for (int kb = (iO >> 1); kb < 2; ++kb) {
+      // A_qk[i][j], i = 32 kb + 8 g + e (query), j = 16 iO + r16 (key)
+      Fr af;
+      {
+        const int i0 = 32 * kb + 8 * g + ii;
+        const int boff = ((i0 >> 4) * 2 + (iO >> 1)) * 2048 + (16 * qq + (i0 & 15)) * 16 + 8 * (iO & 1);
+        const __bf16* p0 = reinterpret_cast<const __bf16*>(sA + boff);
+        af.hi = ld_tr8p(p0, p0 + 32);  // +4 query rows = +4 lanes
+        af.lo = ld_tr8p(p0 + 512, p0 + 512 + 32);
+      }
+#pragma unroll
+      for (int t = 0; t < NVB / 2; ++t) {
+        const int vb = vbO + t;
+        aacc[t] = mma2a(af, ld_tr8(sdO, LDO, 32 * kb, 16 * vb, lane), aacc[t]);
+      }
+    }
+    const float sc = a.scale;
+#pragma unroll
+    for (int t = 0; t < NVB / 2; ++t) {
+      const int vb = vbO + t;
+      f4 r;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) r[u] = racc[t][u] + sc * aacc[t][u];
+      st4split(sRhi + (16 * vb + r16) * LDR + 16 * iO + 4 * g, sRlo + (16 * vb + r16) * LDR + 16 * iO + 4 * g, r);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) a.DR[(ch * CH + 16 * iO + 4 * g + u) * DV + v0 + 16 * vb + r16] = r[u];
+    }
+    __syncthreads();
+
+    // ---- dS <- Diag(gamma_C) dS + scale * Q_g^T dO - Y^T dR
+    f4 qacc[TPW];
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) qacc[t] = f4zero();
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      // Q_g[r][c], r = 32 kb + 8 g + e, c = 16 cs + r16
+      Fr qf;
+      bf8 yf;
+      {
+        const int r0 = 32 * kb + 8 * g + ii;
+        const int qoff = ((r0 >> 4) * KS + (cs >> 1)) * 2048 + ((r0 & 15) + 16 * (2 * (cs & 1) + (qq >> 1))) * 16 +
+                         8 * (qq & 1);
+        const __bf16* p0 = reinterpret_cast<const __bf16*>(sQ + qoff);
+        qf.hi = ld_tr8p(p0, p0 + 32);  // +4 rows of r = +4 lanes
+        qf.lo = ld_tr8p(p0 + 512, p0 + 512 + 32);
+        const int yoff = ((r0 >> 4) * KS + (cs >> 1)) * 1024 + (16 * qq + (r0 & 15)) * 16 + 8 * (cs & 1);
+        const __bf16* y0 = reinterpret_cast<const __bf16*>(sY + yoff);
+        yf = neg8(ld_tr8p(y0, y0 + 32));
+      }
+#pragma unroll
+      for (int t = 0; t < TPW; ++t) {
+        const int vb = sv0 + t;
+        qacc[t] = mma2a(qf, ld_tr8(sdO, LDO, 32 * kb, 16 * vb, lane), qacc[t]);
+      }
+      if (kb == 0) {
+#pragma unroll
+        for (int t = 0; t < TPW; ++t)
+#pragma unroll
+          for (int u = 0; u < 4; ++u) sreg[t][u] *= gcur[u];
+      }
+#pragma unroll
+      for (int t = 0; t < TPW; ++t) {
+        const int vb = sv0 + t;
+        Fr rf;
+        rf.hi = ld8(sRhi + (16 * vb + r16) * LDR + 32 * kb + 8 * g);
+        rf.lo = ld8(sRlo + (16 * vb + r16) * LDR + 32 * kb + 8 * g);
+        sreg[t] = mma2b(yf, rf, sreg[t]);
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < TPW; ++t)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) sreg[t][u] += sc * qacc[t][u];
+    __syncthreads();
+
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) {
+      const int vb = sv0 + t;
+      st4split(sDhi + (16 * vb + r16) * LSD + 16 * cs + 4 * g, sDlo + (16 * vb + r16) * LSD + 16 * cs + 4 * g,
+               sreg[t]);
+    }
+    if (n > 0) GDR2_STORE_CHUNK()
+    __syncthreads();
+  }
+#undef GDR2_LOAD_CHUNK
+#undef GDR2_STORE_CHUNK
+
+  if (a.dS0) {
+#pragma unroll
+    for (int t = 0; t < TPW; ++t)
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        a.dS0[((size_t)seq * DK + 16 * cs + 4 * g + u) * DV + v0 + 16 * (sv0 + t) + r16] = sreg[t][u];
+  }
+}
+
+template <int DK, int DV>
+hipError_t launch_bscan_bf16(const BScanArgs& a, hipStream_t st) {
+  using C = BScanCfg<DK, DV>;
+  const void* fn = reinterpret_cast<const void*>(&bscan_bf16_kernel<DK, DV>);
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+  if (e != hipSuccess) return e;
+  dim3 grid(a.B * a.H * C::NS);
+  hipLaunchKernelGGL((bscan_bf16_kernel<DK, DV>), grid, dim3(C::NTHR), C::LDS, st, a);
+  return hipGetLastError();
+}
+
+template hipError_t launch_bscan_bf16<64, 64>(const BScanArgs&, hipStream_t);
+template hipError_t launch_bscan_bf16<64, 128>(const BScanArgs&, hipStream_t);
+template hipError_t launch_bscan_bf16<128, 64>(const BScanArgs&, hipStream_t);
+template hipError_t launch_bscan_bf16<128, 128>(const BScanArgs&, hipStream_t);
+
+}  // namespace gdr2

@@ -159,8 +159,25 @@ struct ScanArgs {
   float scale;
 };
 
+struct BScanArgs {
+  const unsigned char* Y;
+  const unsigned char* Qg;
+  const unsigned char* Aqk;
+  const unsigned char* KtT;
+  const float* GC;
+  const bf16_t* dout;
+  const float* dST;  // nullable
+  float* dS0;        // nullable
+  float* DH;         // gradient of each chunk's end state (B,H,NT,Dk,Dv)
+  float* DR;         // dR per chunk (B,H,NT,C,Dv)
+  int B, T, H, NT;
+  float scale;
+};
+
 template <int DK, int DV>
 hipError_t launch_intra_bf16(const IntraBf16Args& a, hipStream_t st);
+template <int DK, int DV>
+hipError_t launch_bscan_bf16(const BScanArgs& a, hipStream_t st);
 template <int DK, int DV, bool WITH_O, bool STORE_H>
 hipError_t launch_scan_bf16(const ScanArgs& a, hipStream_t st);
 

@@ -150,13 +150,14 @@ def test_workspace_size_and_check(dtype):
     r = lambda n: (n * 4 + 255) // 256 * 256      # fp32 tiles, 256-byte aligned regions
     rb = lambda n: (n + 255) // 256 * 256         # byte regions
     fwd32 = r(NC * 64 * 128) + r(NC * 64 * 64) + 2 * r(NC * 64 * 128) + r(NC * 64 * 64) + r(NC * 128)
-    exp_bwd = fwd32 + 2 * r(NC * 128 * 64) + 2 * r(NC * 64 * 64) + 2 * r(NC * 64 * 64) + r(NC * 64 * 128)
+    extras = 2 * r(NC * 128 * 64) + 2 * r(NC * 64 * 64) + 2 * r(NC * 64 * 64) + r(NC * 64 * 128)
     if dtype == "fp32":
         exp_fwd = fwd32
     else:
         # fragment-ordered bf16 tiles: Y, Qg (hi/lo), A_qk (hi/lo), Ktail^T (hi/lo), U (fp32), gamma_C
         exp_fwd = (rb(NC * 4 * 4 * 1024) + rb(NC * 4 * 4 * 2048) + rb(NC * 8 * 2048) + rb(NC * 8 * 2 * 2048)
                    + rb(NC * 4 * 4 * 1024) + rb(NC * 512))
+    exp_bwd = exp_fwd + extras
     assert fwd == exp_fwd and bwd == exp_bwd
     assert _fwd(p, ws_bytes=fwd - 1) == g2.GDR2_EWORKSPACE
     assert _bwd(p, ws_bytes=bwd - 1) == g2.GDR2_EWORKSPACE
