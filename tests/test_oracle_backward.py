@@ -125,3 +125,29 @@ def test_G6_scalar_post_scaling_is_caught():
                                 t["do"], None, t["scale"], C=8)
     for gname in GRADS.values():
         assert rel_l2(bad_t[gname], good_t[gname]) < 1e-12
+
+
+def test_wy_vjp_reduces_to_residual_products():
+    """Since R = A (Z - Ebar S0) (App. A.2, the residual system (I + T) R = Z - Ebar S0),
+    the gate-aware WY VJP of App. B.2 collapses: dA = dR R^T (I + T)^T, hence
+    dT = -tril(A^T dA A^T, -1) = -tril(dZ R^T, -1) and dEbar = A^T dY = -dZ S0^T with
+    dZ = A^T dR.  The bf16 backward kernel uses these forms; this pins them against
+    App. B's equations on random chunks with untied gates."""
+    import oracle.chunkwise as cw
+    from paper_2605_22791_amd.inputs import make_inputs
+    d = make_inputs(1, 64, 1, 32, 24, seed=91, dtype="fp32", s0_std=0.3)
+    q, k, v, g, b, w = [d[n][0, :, 0].astype(np.float64) for n in ("q", "k", "v", "log_alpha", "b", "w")]
+    rng = np.random.default_rng(7)
+    S0 = rng.standard_normal((32, 24))
+    dSC = rng.standard_normal((32, 24))
+    dO = rng.standard_normal((64, 24))
+    c = cw._chunk_prep(q, k, v, g, b, w)
+    A, Z, Ebar, Y, U, T = c["A"], c["Z"], c["Ebar"], c["Y"], c["U"], c["T"]
+    R = U - Y @ S0
+    dR = c["Aqk"].T @ dO + c["Ktail"] @ dSC
+    dY = -dR @ S0.T
+    dA = dR @ Z.T + dY @ Ebar.T
+    dZ = A.T @ dR
+    assert np.allclose(dA, dR @ R.T @ (np.eye(64) + T).T, atol=1e-12)
+    assert np.allclose(-np.tril(A.T @ dA @ A.T, -1), -np.tril(dZ @ R.T, -1), atol=1e-12)
+    assert np.allclose(A.T @ dY, -dZ @ S0.T, atol=1e-12)
