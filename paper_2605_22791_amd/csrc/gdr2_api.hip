@@ -39,12 +39,13 @@ gdr2_status check_problem(const gdr2_problem* p, bool chunked) {
 }
 
 // Workspace regions, chunk-head major: ch = (b*H + h)*NT + n.  The bf16
-// forward uses the fragment-order regions of WsBf16 (gdr2_kernels.hpp); the
-// fp32 path and the backward use fp32 tiles.
+// path uses the fragment-order regions of WsBf16 (gdr2_kernels.hpp) plus fp32
+// chunk states and R for the backward; the fp32 path uses fp32 tiles.
 struct Layout {
   size_t Y, U, Kt, Qg, Aqk, GC;          // fp32 forward tiles
   size_t Hs, Rs, DH, DR, DAqk, DT, DEg;  // backward extras
   size_t bY, bQ, bA, bK, bU, bG;         // bf16 forward (fragment order)
+  size_t bDR, bAm;                       // bf16 backward extras (fragment order)
   size_t total;
 };
 
@@ -82,10 +83,18 @@ Layout layout(const gdr2_problem* p, bool bwd) {
     L.Hs = take(NC * Dk * Dv);
     L.Rs = take(NC * CH * Dv);
     L.DH = take(NC * Dk * Dv);
-    L.DR = take(NC * CH * Dv);
-    L.DAqk = take(NC * CH * CH);
-    L.DT = take(NC * CH * CH);
-    L.DEg = take(NC * CH * Dk);
+    if (p->dtype == GDR2_BF16) {
+      // fragment-ordered dR and A for the chunk-parallel backward
+      L.bDR = off;
+      off += round_up(NC * WsBf16::dr(p->Dv));
+      L.bAm = off;
+      off += round_up(NC * WsBf16::am());
+    } else {
+      L.DR = take(NC * CH * Dv);
+      L.DAqk = take(NC * CH * CH);
+      L.DT = take(NC * CH * CH);
+      L.DEg = take(NC * CH * Dk);
+    }
   }
   L.total = off;
   return L;
@@ -178,7 +187,7 @@ struct FwdRun {
                        static_cast<const bf16_t*>(v), g, static_cast<const bf16_t*>(b),
                        static_cast<const bf16_t*>(w), at<unsigned char>(ws, L.bY),
                        at<unsigned char>(ws, L.bQ), at<unsigned char>(ws, L.bA),
-                       at<unsigned char>(ws, L.bK), at<float>(ws, L.bU), at<float>(ws, L.bG),
+                       at<unsigned char>(ws, L.bK), at<float>(ws, L.bU), at<float>(ws, L.bG), nullptr,
                        p->B, p->T, p->H, p->T / CH};
       hipError_t e = timed(GDR2_K_FWD_INTRA, st, [&] { return launch_intra_bf16<DK, DV>(ia, st); });
       if (e != hipSuccess) return e;
@@ -216,7 +225,7 @@ struct BwdRun {
                        static_cast<const bf16_t*>(w), at<unsigned char>(ws, L.bY),
                        at<unsigned char>(ws, L.bQ), at<unsigned char>(ws, L.bA),
                        at<unsigned char>(ws, L.bK), at<float>(ws, L.bU), at<float>(ws, L.bG),
-                       p->B, p->T, p->H, NT};
+                       at<unsigned char>(ws, L.bAm), p->B, p->T, p->H, NT};
       hipError_t e = timed(GDR2_K_BWD_RECOMPUTE_INTRA, st, [&] { return launch_intra_bf16<DK, DV>(ia, st); });
       if (e != hipSuccess) return e;
       ScanArgs sa{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.U, ia.GC, S0, nullptr, nullptr, at<float>(ws, L.Hs),
@@ -224,18 +233,18 @@ struct BwdRun {
       e = timed(GDR2_K_BWD_RECOMPUTE_STATE, st, [&] { return launch_scan_bf16<DK, DV, false, true>(sa, st); });
       if (e != hipSuccess) return e;
       BScanArgs ba{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.GC, static_cast<const bf16_t*>(dout), dST, dS0,
-                   at<float>(ws, L.DH), at<float>(ws, L.DR), p->B, p->T, p->H, NT, p->scale};
+                   at<float>(ws, L.DH), at<unsigned char>(ws, L.bDR), p->B, p->T, p->H, NT, p->scale};
       e = timed(GDR2_K_BWD_STATE, st, [&] { return launch_bscan_bf16<DK, DV>(ba, st); });
       if (e != hipSuccess) return e;
-      BwdChunkArgs<TIn> ca{static_cast<const TIn*>(q), static_cast<const TIn*>(k), static_cast<const TIn*>(v), g,
-                           static_cast<const TIn*>(b), static_cast<const TIn*>(w), static_cast<const TIn*>(dout),
-                           at<float>(ws, L.Hs), at<float>(ws, L.DH), at<float>(ws, L.Rs), at<float>(ws, L.DR),
-                           at<float>(ws, L.DAqk), at<float>(ws, L.DT), at<float>(ws, L.DEg), static_cast<TIn*>(dq),
-                           static_cast<TIn*>(dk), static_cast<TIn*>(dv), static_cast<TIn*>(db),
-                           static_cast<TIn*>(dw), dg, p->T, p->H, NT, p->scale};
-      e = timed(GDR2_K_BWD_WY, st, [&] { return launch_bwd_wy<DK, DV, TIn>(ca, p->B, st); });
-      if (e != hipSuccess) return e;
-      return timed(GDR2_K_BWD_INTRA, st, [&] { return launch_bwd_intra<DK, DV, TIn>(ca, p->B, st); });
+      // the WY VJP and the intra-chunk VJP in one chunk-parallel kernel
+      BChunkBf16Args ca{static_cast<const bf16_t*>(q), static_cast<const bf16_t*>(k),
+                        static_cast<const bf16_t*>(v), g, static_cast<const bf16_t*>(b),
+                        static_cast<const bf16_t*>(w), static_cast<const bf16_t*>(dout), at<float>(ws, L.Hs),
+                        at<float>(ws, L.DH), at<float>(ws, L.Rs), at<unsigned char>(ws, L.bDR),
+                        at<unsigned char>(ws, L.bAm), static_cast<bf16_t*>(dq), static_cast<bf16_t*>(dk),
+                        static_cast<bf16_t*>(dv), static_cast<bf16_t*>(db), static_cast<bf16_t*>(dw), dg,
+                        p->B, p->T, p->H, NT, p->scale};
+      return timed(GDR2_K_BWD_INTRA, st, [&] { return launch_bchunk_bf16<DK, DV>(ca, st); });
     }
     IntraArgs<TIn> ia{static_cast<const TIn*>(q), static_cast<const TIn*>(k),
                       static_cast<const TIn*>(v), g, static_cast<const TIn*>(b),

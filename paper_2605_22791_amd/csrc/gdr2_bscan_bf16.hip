@@ -5,8 +5,8 @@
 //   dR  = scale * A_qk^T dO + Ktail dS
 //   dS <- Diag(gamma_C) dS + scale * Q_g^T dO - Y^T dR
 //
-// writing dS before each update (the gradient of that chunk's end state), dR,
-// and finally dS0.  The operands are the forward's fragment-ordered tiles
+// writing dS before each update (the gradient of that chunk's end state), dR
+// (split hi/lo, in the fragment order the chunk backward reads), and finally dS0.  The operands are the forward's fragment-ordered tiles
 // (gdr2_kernels.hpp): the transposed fragments these products need come out
 // of the same LDS blocks through ds_read_b64_tr_b16 with per-lane addresses,
 // since every 4 consecutive elements of a block row are contiguous.
@@ -201,8 +201,11 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
 #pragma unroll
       for (int u = 0; u < 4; ++u) r[u] = racc[t][u] + sc * aacc[t][u];
       st4split(sRhi + (16 * vb + r16) * LDR + 16 * iO + 4 * g, sRlo + (16 * vb + r16) * LDR + 16 * iO + 4 * g, r);
-#pragma unroll
-      for (int u = 0; u < 4; ++u) a.DR[(ch * CH + 16 * iO + 4 * g + u) * DV + v0 + 16 * vb + r16] = r[u];
+      // dR as permuted fragment blocks (row = value, K = chunk row): this lane's
+      // four rows 16 iO + 4 g + u are half of its 16-byte slot
+      const size_t doff = ch * WsBf16::dr(DV) + (size_t)((v0 / 16 + vb) * 2 + (iO >> 1)) * 2048 + 16 * lane +
+                          8 * (iO & 1);
+      st4split(reinterpret_cast<__bf16*>(a.DR + doff), reinterpret_cast<__bf16*>(a.DR + doff + 1024), r);
     }
     __syncthreads();
 

@@ -10,7 +10,8 @@
 //   Y = A Ebar,  U = A (W * V)                        eq. eq_gdn2_wy_aux
 //
 // and writes Y, Q_g, A_qk, Ktail^T, U and gamma_C to the workspace in MFMA
-// fragment order (layout in gdr2_kernels.hpp) for the state scan.
+// fragment order (layout in gdr2_kernels.hpp) for the state scan; the
+// backward's recompute also keeps A itself (split hi/lo).
 //
 // Precision: T uses one bf16 pass; A enters Y and U as a bf16 operand (the
 // solve itself is fp32) and Y is stored in bf16; A_qk, Q_g, Ktail, Ebar, Z are
@@ -333,6 +334,23 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
       for (int u = 0; u < 4; ++u) sTA[(16 * i + 4 * g + u) * LTA + 16 * wave + r16] = -res[u];
     }
     __syncthreads();
+  }
+
+  // ---- A for the backward: permuted blocks (row = key s, K = chunk row r)
+  if (a.Am) {
+    unsigned char* Ao = a.Am + ch * WsBf16::am();
+    for (int blk = wave; blk < 8; blk += 4) {
+      const int sb = blk >> 1, kb = blk & 1;
+      float x[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int r = 32 * kb + (e < 4 ? 4 * g + e : 16 + 4 * g + (e - 4));
+        x[e] = sTA[r * LTA + 16 * sb + r16];
+      }
+      const Fr f = split8(x);
+      st8(reinterpret_cast<__bf16*>(Ao + blk * 2048 + 16 * lane), f.hi);
+      st8(reinterpret_cast<__bf16*>(Ao + blk * 2048 + 1024 + 16 * lane), f.lo);
+    }
   }
 
   // ---- Ebar = b * k * gamma (split) over the G2 region

@@ -118,6 +118,11 @@ struct RecurArgs {
 //   U    (64 x Dv)  fp32 accumulator tiles [Dv/16][4] x (64 lanes x 4):
 //                   lane l holds U[16 i + 4 (l / 16) + u][16 vb + l % 16]
 //   GC   (Dk)       gamma_C, fp32
+// and, for the backward:
+//   Am   (64 x 64)  A = (I + T)^{-1}, bf16 hi/lo, permuted blocks [key s block 4][row r block 2]
+//                   (row R = s, permuted K = r): the B operand of A^T-products
+//   DR   (64 x Dv)  dR, bf16 hi/lo, permuted blocks [value block Dv/16][row block 2]
+//                   (row R = value, permuted K = chunk row): the A operand of dR^T A
 struct WsBf16 {
   static constexpr size_t y(int dk) { return (size_t)4 * (dk / 32) * 1024; }
   static constexpr size_t qg(int dk) { return (size_t)4 * (dk / 32) * 2048; }
@@ -125,6 +130,8 @@ struct WsBf16 {
   static constexpr size_t ktt(int dk) { return (size_t)(dk / 16) * 2 * 2048; }
   static constexpr size_t u(int dv) { return (size_t)(dv / 16) * 4 * 1024; }
   static constexpr size_t gc(int dk) { return (size_t)((dk * 4 + 255) / 256) * 256; }
+  static constexpr size_t am() { return (size_t)8 * 2048; }
+  static constexpr size_t dr(int dv) { return (size_t)(dv / 16) * 2 * 2048; }
 };
 
 struct IntraBf16Args {
@@ -140,6 +147,7 @@ struct IntraBf16Args {
   unsigned char* KtT;
   float* U;
   float* GC;
+  unsigned char* Am;  // nullable: A for the backward
   int B, T, H, NT;
 };
 
@@ -169,7 +177,31 @@ struct BScanArgs {
   const float* dST;  // nullable
   float* dS0;        // nullable
   float* DH;         // gradient of each chunk's end state (B,H,NT,Dk,Dv)
-  float* DR;         // dR per chunk (B,H,NT,C,Dv)
+  unsigned char* DR; // dR per chunk, WsBf16 fragment blocks
+  int B, T, H, NT;
+  float scale;
+};
+
+// Chunk-parallel backward of the bf16 path (App. B.2 - B.5).
+struct BChunkBf16Args {
+  const bf16_t* q;
+  const bf16_t* k;
+  const bf16_t* v;
+  const float* g;
+  const bf16_t* b;
+  const bf16_t* w;
+  const bf16_t* dout;
+  const float* Hs;          // chunk-start states (B,H,NT,Dk,Dv)
+  const float* DH;          // gradients of the chunk-end states (B,H,NT,Dk,Dv)
+  const float* Rs;          // R per chunk (B,H,NT,C,Dv)
+  const unsigned char* DR;  // dR, WsBf16 fragment blocks
+  const unsigned char* Am;  // A, WsBf16 fragment blocks
+  bf16_t* dq;
+  bf16_t* dk;
+  bf16_t* dv;
+  bf16_t* db;
+  bf16_t* dw;
+  float* dg;
   int B, T, H, NT;
   float scale;
 };
@@ -180,6 +212,8 @@ template <int DK, int DV>
 hipError_t launch_bscan_bf16(const BScanArgs& a, hipStream_t st);
 template <int DK, int DV, bool WITH_O, bool STORE_H>
 hipError_t launch_scan_bf16(const ScanArgs& a, hipStream_t st);
+template <int DK, int DV>
+hipError_t launch_bchunk_bf16(const BChunkBf16Args& a, hipStream_t st);
 
 template <int DK, int DV, typename TIn>
 hipError_t launch_fwd_intra(const IntraArgs<TIn>& a, int B, hipStream_t st);

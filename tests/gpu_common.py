@@ -77,13 +77,17 @@ def bf16_bits_to_f32(u16):
     return (u16.astype(np.uint32) << 16).view(np.float32)
 
 
-def ws_layout_bf16(B, T, H, Dk, Dv):
-    """Byte offsets / per-chunk-head sizes of the bf16 forward workspace regions
-    (mirrors WsBf16 in the library: fragment-ordered tiles)."""
+def ws_layout_bf16(B, T, H, Dk, Dv, bwd=False):
+    """Byte offsets / per-chunk-head sizes of the bf16 workspace regions
+    (mirrors WsBf16 in the library: fragment-ordered tiles; the backward adds
+    fp32 chunk states Hs, R and dH, then dR and A as fragment blocks)."""
     NC = B * H * (T // CH)
     gc = (Dk * 4 + 255) // 256 * 256
     sizes = [("Y", 4 * (Dk // 32) * 1024), ("Qg", 4 * (Dk // 32) * 2048), ("Aqk", 8 * 2048),
              ("KtT", (Dk // 16) * 2 * 2048), ("U", (Dv // 16) * 4 * 1024), ("GC", gc)]
+    if bwd:
+        sizes += [("Hs", Dk * Dv * 4), ("Rs", CH * Dv * 4), ("DH", Dk * Dv * 4),
+                  ("DR", (Dv // 16) * 2 * 2048), ("Am", 8 * 2048)]
     off, out = 0, {}
     for n, per in sizes:
         out[n] = (off, per)

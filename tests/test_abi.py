@@ -157,7 +157,11 @@ def test_workspace_size_and_check(dtype):
         # fragment-ordered bf16 tiles: Y, Qg (hi/lo), A_qk (hi/lo), Ktail^T (hi/lo), U (fp32), gamma_C
         exp_fwd = (rb(NC * 4 * 4 * 1024) + rb(NC * 4 * 4 * 2048) + rb(NC * 8 * 2048) + rb(NC * 8 * 2 * 2048)
                    + rb(NC * 4 * 4 * 1024) + rb(NC * 512))
-    exp_bwd = exp_fwd + extras
+    if dtype == "fp32":
+        exp_bwd = exp_fwd + extras
+    else:
+        # chunk states, R and dR-gradient states in fp32; dR and A as split bf16 fragment blocks
+        exp_bwd = exp_fwd + 2 * r(NC * 128 * 64) + r(NC * 64 * 64) + rb(NC * (64 // 16) * 2 * 2048) + rb(NC * 8 * 2048)
     assert fwd == exp_fwd and bwd == exp_bwd
     assert _fwd(p, ws_bytes=fwd - 1) == g2.GDR2_EWORKSPACE
     assert _bwd(p, ws_bytes=bwd - 1) == g2.GDR2_EWORKSPACE

@@ -134,3 +134,73 @@ def test_config2_full_size_backward_sampled_heads():
     ref = gdr2_recurrent_bwd(sub["q"], sub["k"], sub["v"], sub["log_alpha"], sub["b"], sub["w"], None,
                              sub["do"], None, d["scale"])
     _compare(got, ref, TOL["bf16"], pairs=pairs)
+
+
+@pytest.mark.parametrize("Dk,Dv", [(64, 64), (64, 128), (128, 64), (128, 128)])
+def test_bf16_backward_head_dims(Dk, Dv):
+    # B*H = 6 chunk-heads of 5 chunks, with S0 and dS_T
+    d = make_inputs(2, 320, 3, Dk, Dv, seed=64 + Dk + Dv, dtype="bf16", s0_std=0.05, with_dST=True)
+    _case(f"bf16 bwd B2 H3 T320 Dk{Dk} Dv{Dv} with S0 and dS_T")
+    _compare(_run_bwd(d), _adjoint(d), TOL["bf16"])
+
+
+def test_bf16_backward_single_chunk_no_state():
+    d = make_inputs(1, 64, 2, 128, 128, seed=65, dtype="bf16")
+    _case("bf16 bwd one chunk, S0 = 0, dS_T = 0")
+    _compare(_run_bwd(d), _adjoint(d), TOL["bf16"])
+
+
+def test_bf16_extreme_decay_backward():
+    """Decay spikes push a block's internal decay past e^60: the diagonal blocks
+    of the decay products are then formed element by element."""
+    d = make_inputs(1, 192, 2, 128, 128, seed=66, dtype="bf16", s0_std=0.1, with_dST=True)
+    la = d["log_alpha"].copy()
+    la[0, 20, 0, :8] = -90.0
+    la[0, 70, 1, 5:40] = -200.0
+    la[0, 75, 1, 30:] = -70.0
+    la[0, 140:150, 0, :] = -9.0
+    d["log_alpha"] = la
+    _case("bf16 bwd extreme decay spikes")
+    _compare(_run_bwd(d), _adjoint(d), TOL["bf16"])
+
+
+@pytest.mark.parametrize("Dk,Dv", [(64, 128), (128, 64)])
+def test_bf16_backward_workspace_intermediates(Dk, Dv):
+    """A and dR in the backward workspace (split bf16 fragment blocks) against
+    the chunk algebra: A = (I + T)^{-1} (App. A.2) and the reverse recursion of
+    App. B.1, dR = scale A_qk^T dO + Ktail dS_C."""
+    import torch
+    from oracle.chunkwise import gdr2_chunk_fwd_ref
+    from tests.gpu_common import ws_layout_bf16, decode_frag_blocks
+    B, T, H = 1, 192, 2
+    d = make_inputs(B, T, H, Dk, Dv, seed=67, dtype="bf16", s0_std=0.05, with_dST=True)
+    lay, total, NC = ws_layout_bf16(B, T, H, Dk, Dv, bwd=True)
+    ws = torch.full((total,), 0xFF, dtype=torch.uint8, device="cuda")
+    _case(f"bf16 bwd workspace intermediates Dk{Dk} Dv{Dv}")
+    _run_bwd(d, ws=ws)
+    torch.cuda.synchronize()
+    raw = ws.cpu().numpy()
+    _, _, it = gdr2_chunk_fwd_ref(d["q"], d["k"], d["v"], d["log_alpha"], d["b"], d["w"], d["S0"],
+                                  d["scale"], C=CH, keep=True)
+    NT = T // CH
+    worst = {"A": 0.0, "dR": 0.0}
+    for bi in range(B):
+        for hi in range(H):
+            dS = d["dST"][bi, hi].astype(np.float64)
+            for n in range(NT - 1, -1, -1):
+                ch = (bi * H + hi) * NT + n
+                dO = d["scale"] * d["do"][bi, n * CH:(n + 1) * CH, hi].astype(np.float64)
+                dR = it["Aqk"][bi, hi, n].T @ dO + it["Ktail"][bi, hi, n] @ dS
+                dS = it["gC"][bi, hi, n][:, None] * dS + it["Qg"][bi, hi, n].T @ dO - it["Y"][bi, hi, n].T @ dR
+
+                def region(name):
+                    off, per = lay[name]
+                    return raw[off + ch * per: off + (ch + 1) * per].view(np.uint16)
+
+                A = decode_frag_blocks(region("Am"), 4, 2, True, True).T
+                dRg = decode_frag_blocks(region("DR"), Dv // 16, 2, True, True).T
+                worst["A"] = max(worst["A"], rel_l2(A, it["A"][bi, hi, n]))
+                worst["dR"] = max(worst["dR"], rel_l2(dRg, dR))
+    print({k_: f"{v_:.2e}" for k_, v_ in worst.items()})
+    # A comes from a Gram matrix formed in one bf16 pass; dR inherits the bf16 Y of the reverse scan
+    assert worst["A"] < 1e-2 and worst["dR"] < 2e-3, worst
