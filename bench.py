@@ -18,43 +18,45 @@ import time
 
 HBM_PEAK_GBS = 8000.0                    # MI355X HBM3E, GB/s
 PEAK_TFLOPS = {"fp32": 157.3, "bf16": 2500.0}
-MFMA_DTYPE = "fp32"                      # the kernels' MFMA operand type (v_mfma_f32_16x16x4_f32)
+MFMA_DTYPE = "bf16"                      # operand type of the path's products (v_mfma_f32_16x16x32_bf16)
 
 
-def kernel_model(B, T, H, Dk, Dv, es):
-    """Algorithmic flops and HBM bytes per launch of each kernel.
+def kernel_model(B, T, H, Dk, Dv):
+    """Algorithmic flops and HBM bytes per launch of each kernel of the bf16 path.
 
-    Per chunk-head (C = 64 tokens of one head), causal triangles counted at
-    half; bytes are each kernel's inputs read once plus outputs written once
-    (es = bytes per element of q/k/v/b/w/o and their gradients; log-decay,
-    states and workspace tiles are fp32).
+    Per chunk-head (C = 64 tokens of one head); a causal C x C x D product
+    counts C^2 D flops (half of the dense 2 C^2 D).  Bytes are each kernel's
+    inputs read once plus its outputs written once, in the dtypes they have:
+    q/k/v/b/w/dO/o and their gradients bf16, log-decay and its gradient fp32,
+    chunk states and R fp32, the fragment-ordered workspace tiles as stored
+    (split tiles hi + lo, Y single bf16, U fp32).
     """
     C = 64
     NC = B * H * (T // C)
-    f = 4
-    tri = C * C * Dk           # a causal C x C x Dk product: C^2/2 * Dk * 2 flops
-    triv = C * C * Dv
-    kin = C * Dk * es          # one (C x Dk) input tile
-    vin = C * Dv * es
-    kf = C * Dk * f            # one (C x Dk) fp32 tile
-    vf = C * Dv * f
-    st = Dk * Dv * f           # one fp32 state
-    aq = C * C * f             # one fp32 C x C tile
+    NT = T // C
+    f, h = 4, 2
+    tri, triv = C * C * Dk, C * C * Dv         # causal products
+    mm = 2 * C * Dk * Dv                      # one dense (C x Dk) x (Dk x Dv) product
     solve = C ** 3 / 3
+    kin, vin = C * Dk * h, C * Dv * h          # bf16 (C x D) tiles
+    kf, vf = C * Dk * f, C * Dv * f            # fp32 (C x D) tiles
+    st = Dk * Dv * f                          # fp32 state
+    ws_y, ws_q, ws_a = C * Dk * h, C * Dk * 2 * h, C * C * 2 * h
+    ws_k, ws_u, ws_g = C * Dk * 2 * h, C * Dv * f, -(-Dk * f // 256) * 256
+    ws_am, ws_dr = C * C * 2 * h, C * Dv * 2 * h
+    seq_state = 2 * st / NT                   # S0 read + S_T write, per sequence
     m = {}
-    m["fwd_intra"] = (tri + tri + solve + tri + triv,
-                      3 * kin + kf + 2 * vin + 3 * kf + vf + aq + Dk * f)
-    m["fwd_state"] = (2 * C * Dk * Dv * 3 + triv,
-                      3 * kf + vf + aq + Dk * f + vin)
-    m["bwd_recompute_intra"] = m["fwd_intra"]
-    m["bwd_recompute_state"] = (2 * C * Dk * Dv * 2,
-                                2 * kf + vf + Dk * f + st + vf)
-    m["bwd_state"] = (triv + 2 * C * Dk * Dv * 3,
-                      3 * kf + aq + Dk * f + vin + st + vf)
-    m["bwd_wy"] = (tri + solve + triv + 2 * C * Dk * Dv + triv + tri + triv + tri + 2 * solve * 2,
-                   2 * kin + kf + 3 * vin + 2 * vf + st + 2 * vin + 2 * aq + kf)
-    m["bwd_intra"] = (tri + tri + 2 * tri + 2 * 2 * C * Dk * Dv + 2 * Dk * Dv,
-                      3 * kin + kf + vin + 2 * st + vf + 2 * aq + kf + 3 * kin + kf)
+    intra_fl = tri + tri + solve + tri + triv
+    intra_by = 3 * kin + kf + 2 * vin + ws_y + ws_q + ws_a + ws_k + ws_u + ws_g
+    m["fwd_intra"] = (intra_fl, intra_by)
+    m["fwd_state"] = (3 * mm + triv, ws_y + ws_q + ws_a + ws_k + ws_u + ws_g + vin + seq_state)
+    m["bwd_recompute_intra"] = (intra_fl, intra_by + ws_am)
+    m["bwd_recompute_state"] = (2 * mm, ws_y + ws_k + ws_u + ws_g + st / NT + st + vf)
+    m["bwd_state"] = (triv + 3 * mm, ws_y + ws_q + ws_a + ws_k + ws_g + vin + seq_state + st + ws_dr)
+    # dZ = A^T dR, dT = -dZ R^T, dA_qk = dO R^T (causal); dZ h^T, dO h^T, R dh^T;
+    # the three decay products with dT / dA_qk (causal)
+    m["bwd_intra"] = (3 * triv + 3 * mm + 4 * tri,
+                      3 * kin + kf + 3 * vin + 2 * st + vf + ws_dr + ws_am + 3 * kin + 2 * vin + kf)
     return {k: (fl * NC, by * NC) for k, (fl, by) in m.items()}
 
 
@@ -191,7 +193,7 @@ def main():
     tokens_per_s = B * T / (ms_step * 1e-3)
     print(f"[bench] {ms_step:.3f} ms/step ({wall / args.steps * 1e3:.3f} ms wall)", file=sys.stderr, flush=True)
 
-    model = kernel_model(B, T, H, Dk, Dv, 2)
+    model = kernel_model(B, T, H, Dk, Dv)
     kern = {}
     for name, (ms, cnt) in per_kernel.items():
         if cnt == 0:

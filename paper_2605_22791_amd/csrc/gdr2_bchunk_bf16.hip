@@ -49,43 +49,57 @@ struct BChunkCfg {
   static constexpr int NTHR = 256;
   static constexpr int NCB = DK / 16, NVB = DV / 16, KV = DV / 32;
   static constexpr int LT = 64 + 8;   // dT^T, dA_qk^T planes, bf16 [64][LT]
-  static constexpr int LGT = 64 + 4;  // G2 columns of a key block, fp32 [16][LGT]
+  static constexpr int LGT = 64 + 4;  // per-key-block fp32 tables [16][LGT]: G2, eL, eR
   static constexpr int LXT = 64 + 8;  // k, b, q columns of a key block, bf16 [16][LXT]
   static constexpr int LH = DV + 8;   // h, dh rows of a key block, bf16 hi/lo [16][LH]
+  // region 1: dR (fragment blocks, prologue) -> dT^T / dA_qk^T planes
+  static constexpr int SZ_DR = (int)WsBf16::dr(DV), SZ_AM = (int)WsBf16::am();
   static constexpr int OFF_T = 0;
-  static constexpr int OFF_G = OFF_T + 4 * 64 * LT * 2;
-  static constexpr int OFF_X = OFF_G + 16 * LGT * 4;
+  static constexpr int SZ_T = 4 * 64 * LT * 2;
+  // region 2: A (fragment blocks, prologue) -> the staged key block
+  static constexpr int OFF_S = OFF_T + SZ_T;
+  static constexpr int OFF_G = OFF_S;
+  static constexpr int OFF_EL = OFF_G + 16 * LGT * 4;
+  static constexpr int OFF_ER = OFF_EL + 16 * LGT * 4;
+  static constexpr int OFF_X = OFF_ER + 16 * LGT * 4;
   static constexpr int OFF_H = OFF_X + 3 * 16 * LXT * 2;
-  static constexpr int OFF_HH = OFF_H + 4 * 16 * LH * 2;  // rowsum(dh * h)      [2][16]
+  static constexpr int OFF_END_S = OFF_H + 4 * 16 * LH * 2;
+  // small exchange arrays
+  static constexpr int OFF_BK = OFF_END_S;              // block totals / first rows [2][4][16]
+  static constexpr int OFF_HH = OFF_BK + 2 * 4 * 16 * 4;  // rowsum(dh * h)      [2][16]
   static constexpr int OFF_BT = OFF_HH + 2 * 16 * 4;      // dG block totals     [2][4][16]
   static constexpr int OFF_TL = OFF_BT + 2 * 4 * 16 * 4;  // tail-key sums       [2][4][16]
-  static constexpr int OFF_GT = OFF_TL + 2 * 4 * 16 * 4;  // G2 wave totals      [4][DK]
-  static constexpr int OFF_U = OFF_GT + 4 * DK * 4;       // unsafe diagonal flags [4]
-  static constexpr int LDS = OFF_U + 16;
+  static constexpr int LDS = OFF_TL + 2 * 4 * 16 * 4;
+  static constexpr int NLD = (SZ_DR + SZ_AM) / (16 * NTHR);  // 16-byte prologue loads per thread
+  static_assert(SZ_DR <= SZ_T && SZ_AM <= OFF_END_S - OFF_S, "prologue operands fit their regions");
+  static_assert((SZ_DR + SZ_AM) % (16 * NTHR) == 0 && SZ_DR % (16 * NTHR) == 0, "whole prologue slices");
   static_assert(LDS <= 80 * 1024, "two workgroups per CU");
   static_assert(16 * DV / 8 <= NTHR, "one 8-value piece of h / dh per thread");
 };
 
-// eight bf16 of a row: elements 0..3 at p, 4..7 at p + 16 (the permuted K order)
-__device__ __forceinline__ bf8 ld_p8(const __bf16* p) {
-  const bf4 x = *reinterpret_cast<const bf4*>(p);
-  const bf4 y = *reinterpret_cast<const bf4*>(p + 16);
+__device__ __forceinline__ bf8 cat8(bf4 x, bf4 y) {
   bf8 r;
   r[0] = x[0]; r[1] = x[1]; r[2] = x[2]; r[3] = x[3];
   r[4] = y[0]; r[5] = y[1]; r[6] = y[2]; r[7] = y[3];
   return r;
 }
-__device__ __forceinline__ bf8 ldg_bf8(const unsigned char* p) { return *reinterpret_cast<const bf8*>(p); }
 __device__ __forceinline__ float4 ldg_f4(const float* p) { return *reinterpret_cast<const float4*>(p); }
 __device__ __forceinline__ Fr split_f44(const float4& x, const float4& y) {
   const float v[8] = {x.x, x.y, x.z, x.w, y.x, y.y, y.z, y.w};
   return split8(v);
 }
+// element j (0..3) of four per-block values, j lane-dependent
+__device__ __forceinline__ float pick4(const float (&x)[4], int j) {
+  return j == 0 ? x[0] : (j == 1 ? x[1] : (j == 2 ? x[2] : x[3]));
+}
+// position, inside its 32-value step, of the four values 32 p + 4 a + (0..3) in
+// the permuted K order (lane group G holds 4 G.. and 16 + 4 G.. as one 8-run)
+__device__ __forceinline__ int perm_pos(int a) { return a < 4 ? 8 * a : 8 * (a - 4) + 4; }
 
 template <int DK, int DV>
 __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   using C = BChunkCfg<DK, DV>;
-  constexpr int NCB = C::NCB, NVB = C::NVB, KV = C::KV;
+  constexpr int NCB = C::NCB, NVB = C::NVB, KV = C::KV, NLD = C::NLD;
   constexpr int LT = C::LT, LGT = C::LGT, LXT = C::LXT, LH = C::LH;
 
   extern __shared__ __align__(16) unsigned char smem[];
@@ -93,19 +107,22 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   __bf16* sTl = sTh + 64 * LT;
   __bf16* sAh = sTl + 64 * LT;  // dA_qk^T [s][r]
   __bf16* sAl = sAh + 64 * LT;
-  float* sG = reinterpret_cast<float*>(smem + C::OFF_G);     // G2 [c][s]
+  const unsigned char* sDR = smem + C::OFF_T;  // prologue: dR fragment blocks
+  const unsigned char* sAm = smem + C::OFF_S;  // prologue: A fragment blocks
+  float* sG = reinterpret_cast<float*>(smem + C::OFF_G);    // in-block cumsum of log2-decay [c][s]
+  float* sEL = reinterpret_cast<float*>(smem + C::OFF_EL);  // 2^(G2_s - G2 at its block's first row)
+  float* sER = reinterpret_cast<float*>(smem + C::OFF_ER);  // 2^(G2 at its block's last row - G2_s)
   __bf16* sKc = reinterpret_cast<__bf16*>(smem + C::OFF_X);  // k [c][s]
   __bf16* sBc = sKc + 16 * LXT;
   __bf16* sQc = sBc + 16 * LXT;
-  __bf16* sHh = reinterpret_cast<__bf16*>(smem + C::OFF_H);  // h [c][v]
+  __bf16* sHh = reinterpret_cast<__bf16*>(smem + C::OFF_H);  // h [c][v], permuted K order
   __bf16* sHl = sHh + 16 * LH;
-  __bf16* sDh = sHl + 16 * LH;  // dh [c][v]
+  __bf16* sDh = sHl + 16 * LH;  // dh [c][v], permuted K order
   __bf16* sDl = sDh + 16 * LH;
+  float* sBK = reinterpret_cast<float*>(smem + C::OFF_BK);  // [0]: block totals, [1]: first rows
   float* sHH = reinterpret_cast<float*>(smem + C::OFF_HH);
   float* sBT = reinterpret_cast<float*>(smem + C::OFF_BT);
   float* sTL = reinterpret_cast<float*>(smem + C::OFF_TL);
-  float* sGT = reinterpret_cast<float*>(smem + C::OFF_GT);
-  int* unsafe = reinterpret_cast<int*>(smem + C::OFF_U);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, r16 = lane & 15;
@@ -113,68 +130,110 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   const int T = a.T, H = a.H, NT = a.NT;
   const size_t ch = ((size_t)bb * H + h) * NT + n;
   const size_t row0 = (size_t)bb * T + (size_t)n * CH;
-  const size_t KST = (size_t)H * DK, VST = (size_t)H * DV;
+  const size_t KST = (size_t)H * DK, VST = (size_t)H * DV;  // token strides
   const size_t kb0 = row0 * KST + (size_t)h * DK, vb0 = row0 * VST + (size_t)h * DV;
   const int i = wave;  // the row block this wave owns
+  const int kbl = i >> 1;
 
-  const __bf16* Qp = reinterpret_cast<const __bf16*>(a.q);
-  const __bf16* Kp = reinterpret_cast<const __bf16*>(a.k);
-  const __bf16* Vp = reinterpret_cast<const __bf16*>(a.v);
-  const __bf16* Bp = reinterpret_cast<const __bf16*>(a.b);
-  const __bf16* Wp = reinterpret_cast<const __bf16*>(a.w);
-  const __bf16* dOp = reinterpret_cast<const __bf16*>(a.dout);
-  __bf16* dQp = reinterpret_cast<__bf16*>(a.dq);
-  __bf16* dKp = reinterpret_cast<__bf16*>(a.dk);
-  __bf16* dVp = reinterpret_cast<__bf16*>(a.dv);
-  __bf16* dBp = reinterpret_cast<__bf16*>(a.db);
-  __bf16* dWp = reinterpret_cast<__bf16*>(a.dw);
+  // per-chunk bases (uniform) and 32-bit lane offsets: KST = H Dk, VST = H Dv
+  const __bf16* Qp = reinterpret_cast<const __bf16*>(a.q) + kb0;
+  const __bf16* Kp = reinterpret_cast<const __bf16*>(a.k) + kb0;
+  const __bf16* Bp = reinterpret_cast<const __bf16*>(a.b) + kb0;
+  const float* Gp0 = a.g + kb0;
+  __bf16* dQp = reinterpret_cast<__bf16*>(a.dq) + kb0;
+  __bf16* dKp = reinterpret_cast<__bf16*>(a.dk) + kb0;
+  __bf16* dBp = reinterpret_cast<__bf16*>(a.db) + kb0;
+  float* dGp = a.dg + kb0;
+  const __bf16* Vp = reinterpret_cast<const __bf16*>(a.v) + vb0;
+  const __bf16* Wp = reinterpret_cast<const __bf16*>(a.w) + vb0;
+  const __bf16* dOp = reinterpret_cast<const __bf16*>(a.dout) + vb0;
+  __bf16* dVp = reinterpret_cast<__bf16*>(a.dv) + vb0;
+  __bf16* dWp = reinterpret_cast<__bf16*>(a.dw) + vb0;
+  const float* Hc = a.Hs + ch * DK * DV;
+  const float* DHc = a.DH + ch * DK * DV;
+  const float* Rc = a.Rs + ch * CH * DV;
+  const int kst = H * DK, vst = H * DV;
 
-  // staging role: chunk row grow, channels 16 cb + 4 cq + (0..3) of key block cb
+  // staging role: chunk row grow (block = wave), channels 16 cb + 4 cq + (0..3)
   const int rl = lane >> 2, cq = lane & 3, grow = 16 * wave + rl;
   // h / dh staging role: row hc of the key block, values hv .. hv + 7
   const int hc = (8 * tid) / DV, hv = (8 * tid) % DV;
   const bool hact = tid < 2 * DV;
+  const int hp0 = (hv & ~31) + perm_pos((hv & 31) >> 2), hp1 = (hv & ~31) + perm_pos(((hv & 31) >> 2) + 1);
 
-  // ---- loads: g (all key blocks) and the staging operands of key block 0
-  float4 G2v[NCB];
+  // ---- loads in flight from the start: dR and A (cooperative), this wave's dO
+  // rows and the operands of key block 0
+  u4v ldv[NLD];
+  {
+    const unsigned char* DRc = a.DR + ch * WsBf16::dr(DV);
+    const unsigned char* Amc = a.Am + ch * WsBf16::am();
 #pragma unroll
-  for (int cb = 0; cb < NCB; ++cb) G2v[cb] = ldg_f4(a.g + kb0 + grow * KST + 16 * cb + 4 * cq);
+    for (int m = 0; m < NLD; ++m) {
+      const int off = 16 * (tid + C::NTHR * m);
+      ldv[m] = off < C::SZ_DR ? ldg16(DRc + off) : ldg16(Amc + (off - C::SZ_DR));
+    }
+  }
+  bf8 dof[KV];
+#pragma unroll
+  for (int p = 0; p < KV; ++p) {
+    const int o = (16 * i + r16) * vst + 32 * p + 4 * g;
+    dof[p] = cat8(*reinterpret_cast<const bf4*>(dOp + o), *reinterpret_cast<const bf4*>(dOp + o + 16));
+  }
+  float4 pg, ph0, ph1, pd0, pd1;
   bf4 pk, pb, pq;
-  float4 ph0, ph1, pd0, pd1;
 #define GDR2_PREFETCH(CB)                                                                  \
   {                                                                                        \
-    const size_t o_ = kb0 + grow * KST + 16 * (CB) + 4 * cq;                               \
+    const int o_ = grow * kst + 16 * (CB) + 4 * cq;                                        \
+    pg = ldg_f4(Gp0 + o_);                                                                 \
     pk = *reinterpret_cast<const bf4*>(Kp + o_);                                           \
     pb = *reinterpret_cast<const bf4*>(Bp + o_);                                           \
     pq = *reinterpret_cast<const bf4*>(Qp + o_);                                           \
     if (hact) {                                                                            \
-      const size_t so_ = (ch * DK + 16 * (CB) + hc) * DV + hv;                             \
-      ph0 = ldg_f4(a.Hs + so_);                                                            \
-      ph1 = ldg_f4(a.Hs + so_ + 4);                                                        \
-      pd0 = ldg_f4(a.DH + so_);                                                            \
-      pd1 = ldg_f4(a.DH + so_ + 4);                                                        \
+      const int so_ = (16 * (CB) + hc) * DV + hv;                                          \
+      ph0 = ldg_f4(Hc + so_);                                                              \
+      ph1 = ldg_f4(Hc + so_ + 4);                                                          \
+      pd0 = ldg_f4(DHc + so_);                                                             \
+      pd1 = ldg_f4(DHc + so_ + 4);                                                         \
     }                                                                                      \
   }
-  // writes the staged operands of key block CB into LDS (rowsum(dh * h) into parity PAR)
-#define GDR2_STAGE(CB, PAR)                                                                \
+  // Writes key block CB's staged operands (parity PAR for the small arrays):
+  // in-block cumulative sums of the log2-decay and their factor tables, the
+  // block totals and first rows, k / b / q columns, h / dh rows, rowsum(dh * h).
+#define GDR2_STAGE(PAR)                                                                    \
   {                                                                                        \
-    float4 gs_ = G2v[0];                                                                   \
-    _Pragma("unroll") for (int m_ = 1; m_ < NCB; ++m_) if (m_ == (CB)) gs_ = G2v[m_];      \
-    sG[(4 * cq + 0) * LGT + grow] = gs_.x;                                                 \
-    sG[(4 * cq + 1) * LGT + grow] = gs_.y;                                                 \
-    sG[(4 * cq + 2) * LGT + grow] = gs_.z;                                                 \
-    sG[(4 * cq + 3) * LGT + grow] = gs_.w;                                                 \
+    float x_[4] = {pg.x * kLog2e, pg.y * kLog2e, pg.z * kLog2e, pg.w * kLog2e};            \
+    _Pragma("unroll") for (int o_ = 4; o_ < 64; o_ <<= 1) {                                \
+      _Pragma("unroll") for (int u_ = 0; u_ < 4; ++u_) {                                   \
+        const float y_ = __shfl_up(x_[u_], o_);                                            \
+        x_[u_] += lane >= o_ ? y_ : 0.f;                                                   \
+      }                                                                                    \
+    }                                                                                      \
     _Pragma("unroll") for (int u_ = 0; u_ < 4; ++u_) {                                     \
+      const float f_ = __shfl(x_[u_], cq), l_ = __shfl(x_[u_], 60 + cq);                   \
+      const int at_ = (4 * cq + u_) * LGT + grow;                                          \
+      sG[at_] = x_[u_];                                                                    \
+      sEL[at_] = ex2(x_[u_] - f_);                                                         \
+      sER[at_] = ex2(l_ - x_[u_]);                                                         \
+      if (rl == 15) sBK[(0 * 4 + wave) * 16 + 4 * cq + u_] = x_[u_];                       \
+      if (rl == 0) sBK[(1 * 4 + wave) * 16 + 4 * cq + u_] = x_[u_];                        \
       sKc[(4 * cq + u_) * LXT + grow] = pk[u_];                                            \
       sBc[(4 * cq + u_) * LXT + grow] = pb[u_];                                            \
       sQc[(4 * cq + u_) * LXT + grow] = pq[u_];                                            \
     }                                                                                      \
     if (hact) {                                                                            \
       const Fr hf_ = split_f44(ph0, ph1), df_ = split_f44(pd0, pd1);                       \
-      st8(sHh + hc * LH + hv, hf_.hi);                                                     \
-      st8(sHl + hc * LH + hv, hf_.lo);                                                     \
-      st8(sDh + hc * LH + hv, df_.hi);                                                     \
-      st8(sDl + hc * LH + hv, df_.lo);                                                     \
+      __bf16* bh_ = sHh + hc * LH;                                                         \
+      *reinterpret_cast<bf4*>(bh_ + hp0) = bf4{hf_.hi[0], hf_.hi[1], hf_.hi[2], hf_.hi[3]}; \
+      *reinterpret_cast<bf4*>(bh_ + hp1) = bf4{hf_.hi[4], hf_.hi[5], hf_.hi[6], hf_.hi[7]}; \
+      bh_ = sHl + hc * LH;                                                                 \
+      *reinterpret_cast<bf4*>(bh_ + hp0) = bf4{hf_.lo[0], hf_.lo[1], hf_.lo[2], hf_.lo[3]}; \
+      *reinterpret_cast<bf4*>(bh_ + hp1) = bf4{hf_.lo[4], hf_.lo[5], hf_.lo[6], hf_.lo[7]}; \
+      bh_ = sDh + hc * LH;                                                                 \
+      *reinterpret_cast<bf4*>(bh_ + hp0) = bf4{df_.hi[0], df_.hi[1], df_.hi[2], df_.hi[3]}; \
+      *reinterpret_cast<bf4*>(bh_ + hp1) = bf4{df_.hi[4], df_.hi[5], df_.hi[6], df_.hi[7]}; \
+      bh_ = sDl + hc * LH;                                                                 \
+      *reinterpret_cast<bf4*>(bh_ + hp0) = bf4{df_.lo[0], df_.lo[1], df_.lo[2], df_.lo[3]}; \
+      *reinterpret_cast<bf4*>(bh_ + hp1) = bf4{df_.lo[4], df_.lo[5], df_.lo[6], df_.lo[7]}; \
       float hh_ = ph0.x * pd0.x + ph0.y * pd0.y + ph0.z * pd0.z + ph0.w * pd0.w +          \
                   ph1.x * pd1.x + ph1.y * pd1.y + ph1.z * pd1.z + ph1.w * pd1.w;           \
       _Pragma("unroll") for (int o_ = DV / 16; o_ >= 1; o_ >>= 1) hh_ += __shfl_xor(hh_, o_); \
@@ -183,18 +242,41 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   }
   GDR2_PREFETCH(0)
 
+  // ---- dR and A into LDS (regions that later hold dT / dA_qk and the staged key block)
+#pragma unroll
+  for (int m = 0; m < NLD; ++m) {
+    const int off = 16 * (tid + C::NTHR * m);
+    if (off < C::SZ_DR)
+      sts16(smem + C::OFF_T + off, ldv[m]);
+    else
+      sts16(smem + C::OFF_S + (off - C::SZ_DR), ldv[m]);
+  }
+  // this wave's R rows (permuted K) and v, w for dv / dw, in flight across the barrier
+  float4 rraw[2 * KV];
+#pragma unroll
+  for (int p = 0; p < KV; ++p) {
+    const float* rp = Rc + (16 * i + r16) * DV + 32 * p + 4 * g;
+    rraw[2 * p] = ldg_f4(rp);
+    rraw[2 * p + 1] = ldg_f4(rp + 16);
+  }
+  bf4 vvr[NVB], wwr[NVB];
+#pragma unroll
+  for (int vb = 0; vb < NVB; ++vb) {
+    const int o = (16 * i + r16) * vst + 16 * vb + 4 * g;
+    vvr[vb] = *reinterpret_cast<const bf4*>(Vp + o);
+    wwr[vb] = *reinterpret_cast<const bf4*>(Wp + o);
+  }
+  __syncthreads();
+
   // ---- dZ^T = dR^T A for the key rows s of block i: lane gets
-  //      dZ[s = 16 i + r16][v = 16 vb + 4 g + u]
-  const int kbl = i >> 1;  // first 32-row block of r with A[r][s] != 0
+  //      dZ[s = 16 i + r16][v = 16 vb + 4 g + u];  dv = dZ * w, dw = dZ * v
   f4 zacc[NVB];
   {
-    const unsigned char* Ab = a.Am + ch * WsBf16::am();
-    const unsigned char* Rb = a.DR + ch * WsBf16::dr(DV);
     Fr af[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
-      af[kb].hi = ldg_bf8(Ab + (2 * i + kb) * 2048 + 16 * lane);
-      af[kb].lo = ldg_bf8(Ab + (2 * i + kb) * 2048 + 1024 + 16 * lane);
+      af[kb].hi = ld8(reinterpret_cast<const __bf16*>(sAm + (2 * i + kb) * 2048 + 16 * lane));
+      af[kb].lo = ld8(reinterpret_cast<const __bf16*>(sAm + (2 * i + kb) * 2048 + 1024 + 16 * lane));
     }
 #pragma unroll
     for (int vb = 0; vb < NVB; ++vb) {
@@ -203,50 +285,39 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       for (int kb = 0; kb < 2; ++kb) {
         if (kb < kbl) continue;
         Fr rf;
-        rf.hi = ldg_bf8(Rb + (2 * vb + kb) * 2048 + 16 * lane);
-        rf.lo = ldg_bf8(Rb + (2 * vb + kb) * 2048 + 1024 + 16 * lane);
+        rf.hi = ld8(reinterpret_cast<const __bf16*>(sDR + (2 * vb + kb) * 2048 + 16 * lane));
+        rf.lo = ld8(reinterpret_cast<const __bf16*>(sDR + (2 * vb + kb) * 2048 + 1024 + 16 * lane));
         zacc[vb] = mma3(rf, af[kb], zacc[vb]);
       }
     }
   }
-  // dv = dZ * w, dw = dZ * v
-  {
-    const int s = 16 * i + r16;
 #pragma unroll
-    for (int vb = 0; vb < NVB; ++vb) {
-      const size_t o = vb0 + (size_t)s * VST + 16 * vb + 4 * g;
-      const bf4 vv = *reinterpret_cast<const bf4*>(Vp + o);
-      const bf4 ww = *reinterpret_cast<const bf4*>(Wp + o);
-      bf4 odv, odw;
+  for (int vb = 0; vb < NVB; ++vb) {
+    const int o = (16 * i + r16) * vst + 16 * vb + 4 * g;
+    bf4 odv, odw;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        odv[u] = (__bf16)(zacc[vb][u] * (float)ww[u]);
-        odw[u] = (__bf16)(zacc[vb][u] * (float)vv[u]);
-      }
-      *reinterpret_cast<bf4*>(dVp + o) = odv;
-      *reinterpret_cast<bf4*>(dWp + o) = odw;
+    for (int u = 0; u < 4; ++u) {
+      odv[u] = (__bf16)(zacc[vb][u] * (float)wwr[vb][u]);
+      odw[u] = (__bf16)(zacc[vb][u] * (float)vvr[vb][u]);
     }
+    *reinterpret_cast<bf4*>(dVp + o) = odv;
+    *reinterpret_cast<bf4*>(dWp + o) = odw;
   }
   // dZ, dO and R rows of block i as A operands over the values, permuted K:
   // K-step p holds values 32 p + 4 g + (0..3) and 32 p + 16 + 4 g + (0..3)
   Fr zf[KV], rfr[KV];
-  bf8 dof[KV];
-  {
-    const int r = 16 * i + r16;
 #pragma unroll
-    for (int p = 0; p < KV; ++p) {
-      float x[8];
+  for (int p = 0; p < KV; ++p) {
+    float x[8];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        x[u] = zacc[2 * p][u];
-        x[4 + u] = zacc[2 * p + 1][u];
-      }
-      zf[p] = split8(x);
-      dof[p] = ld_p8(dOp + vb0 + (size_t)r * VST + 32 * p + 4 * g);
-      const float* rp = a.Rs + (ch * CH + r) * DV + 32 * p + 4 * g;
-      rfr[p] = split_f44(ldg_f4(rp), ldg_f4(rp + 16));
+    for (int u = 0; u < 4; ++u) {
+      x[u] = zacc[2 * p][u];
+      x[4 + u] = zacc[2 * p + 1][u];
     }
+    zf[p] = split8(x);
+    rfr[p] = split_f44(rraw[2 * p], rraw[2 * p + 1]);
   }
+  __syncthreads();  // dR and A are dead
 
   // ---- dT = -tril(dZ R^T, -1) and dA_qk = tril(scale dO R^T), tiles (i, j <= i),
   //      stored transposed: plane[s][r]
@@ -256,8 +327,13 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     f4 ta = f4zero(), aa = f4zero();
 #pragma unroll
     for (int p = 0; p < KV; ++p) {
-      const float* rp = a.Rs + (ch * CH + s) * DV + 32 * p + 4 * g;
-      const Fr rj = split_f44(ldg_f4(rp), ldg_f4(rp + 16));
+      Fr rj;
+      if (j == i) {
+        rj = rfr[p];
+      } else {
+        const float* rp = Rc + s * DV + 32 * p + 4 * g;
+        rj = split_f44(ldg_f4(rp), ldg_f4(rp + 16));
+      }
       ta = mma3(zf[p], rj, ta);
       aa = mma2b(dof[p], rj, aa);
     }
@@ -277,51 +353,7 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     st4split(sTh + s * LT + rr, sTl + s * LT + rr, f4zero());
     st4split(sAh + s * LT + rr, sAl + s * LT + rr, f4zero());
   }
-
-  // ---- G2 = log2(e) cumsum(g): scan over the wave's 16 rows, then wave offsets
-  {
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) {
-      G2v[cb].x *= kLog2e; G2v[cb].y *= kLog2e; G2v[cb].z *= kLog2e; G2v[cb].w *= kLog2e;
-    }
-#pragma unroll
-    for (int off = 4; off < 64; off <<= 1) {
-#pragma unroll
-      for (int cb = 0; cb < NCB; ++cb) {
-        const float x0 = __shfl_up(G2v[cb].x, off), x1 = __shfl_up(G2v[cb].y, off);
-        const float x2 = __shfl_up(G2v[cb].z, off), x3 = __shfl_up(G2v[cb].w, off);
-        if (lane >= off) {
-          G2v[cb].x += x0; G2v[cb].y += x1; G2v[cb].z += x2; G2v[cb].w += x3;
-        }
-      }
-    }
-    // block i's internal decay G2[16 i] - G2[16 i + 15] (offsets cancel)
-    bool bad = false;
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) {
-      const float y0 = __shfl(G2v[cb].x, cq), y1 = __shfl(G2v[cb].y, cq);
-      const float y2 = __shfl(G2v[cb].z, cq), y3 = __shfl(G2v[cb].w, cq);
-      if (rl == 15)
-        bad = bad || (y0 - G2v[cb].x > kDiagLimit2) || (y1 - G2v[cb].y > kDiagLimit2) ||
-              (y2 - G2v[cb].z > kDiagLimit2) || (y3 - G2v[cb].w > kDiagLimit2);
-    }
-    const unsigned long long m = __ballot(bad);
-    if (lane == 0) unsafe[wave] = (m != 0ull) ? 1 : 0;
-    if (rl == 15) {
-#pragma unroll
-      for (int cb = 0; cb < NCB; ++cb) *reinterpret_cast<float4*>(sGT + wave * DK + 16 * cb + 4 * cq) = G2v[cb];
-    }
-  }
-  __syncthreads();
-  for (int w2 = 0; w2 < wave; ++w2) {
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) {
-      const float4 t4 = *reinterpret_cast<const float4*>(sGT + w2 * DK + 16 * cb + 4 * cq);
-      G2v[cb].x += t4.x; G2v[cb].y += t4.y; G2v[cb].z += t4.z; G2v[cb].w += t4.w;
-    }
-  }
-  const bool uns = unsafe[i] != 0;
-  GDR2_STAGE(0, 0)
+  GDR2_STAGE(0)
   __syncthreads();
 
   const float scale = a.scale;
@@ -336,33 +368,47 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
 #pragma unroll
     for (int p = 0; p < KV; ++p) {
       Fr hf, df;
-      hf.hi = ld_p8(sHh + r16 * LH + 32 * p + 4 * g);
-      hf.lo = ld_p8(sHl + r16 * LH + 32 * p + 4 * g);
-      df.hi = ld_p8(sDh + r16 * LH + 32 * p + 4 * g);
-      df.lo = ld_p8(sDl + r16 * LH + 32 * p + 4 * g);
+      hf.hi = ld8(sHh + r16 * LH + 32 * p + 8 * g);
+      hf.lo = ld8(sHl + r16 * LH + 32 * p + 8 * g);
+      df.hi = ld8(sDh + r16 * LH + 32 * p + 8 * g);
+      df.lo = ld8(sDl + r16 * LH + 32 * p + 8 * g);
       x1 = mma3(zf[p], hf, x1);
       x2 = mma2b(dof[p], hf, x2);
       x3 = mma3(rfr[p], df, x3);
+      __builtin_amdgcn_sched_barrier(0);  // keep one K-step of operands live at a time
     }
 
-    const float* gcol = sG + r16 * LGT;
-    const float Gp = gcol[16 * i], Ge = gcol[16 * i + 15], GCl = gcol[CH - 1];
+    // G2 at the first (G2f) and last (G2l) row of every 16-row block, channel c
+    float G2f[4], G2l[4];
+    {
+      float run = 0.f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        G2f[j] = run + sBK[(4 + j) * 16 + r16];
+        run += sBK[j * 16 + r16];
+        G2l[j] = run;
+      }
+    }
+    const float G2fi = pick4(G2f, i), G2li = pick4(G2l, i);
+    // a diagonal block whose decay exceeds e^60 anywhere in this key block is formed element by element
+    const bool uns = __ballot(G2fi - G2li > kDiagLimit2) != 0ull;
+    const float* elc = sEL + r16 * LGT;
+    const float* erc = sER + r16 * LGT;
 
-    // P1 = dT (k 2^(G2_p - G2_s)),  P2 = dA_qk (k 2^(G2_p - G2_s)),  s <= 16 i + 15
+    // P1 = dT (k 2^(G2_p - G2_s)),  P2 = dA_qk (k 2^(G2_p - G2_s)),  p = 16 i, s <= 16 i + 15;
+    // for s in block j the factor is eR_s * 2^(G2f_i - G2l_j)
     f4 p1 = f4zero(), p2 = f4zero();
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       if (kb > kbl) break;
-      const int s0 = 32 * kb + 8 * g;
-      float Gs[8], ks[8], x[8];
-      ldf8(gcol + s0, Gs);
+      const int s0 = 32 * kb + 8 * g, j = 2 * kb + (g >> 1);
+      const bool inc = j < i || (j == i && !uns);
+      const float br = inc ? ex2(G2fi - pick4(G2l, j)) : 0.f;
+      float er[8], ks[8], x[8];
+      ldf8(erc + s0, er);
       unpack8(ld8(sKc + r16 * LXT + s0), ks);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int s = s0 + e;
-        const bool ok = (s < 16 * i + 16) && !(uns && s >= 16 * i);
-        x[e] = ok ? ks[e] * ex2(Gp - Gs[e]) : 0.f;
-      }
+      for (int e = 0; e < 8; ++e) x[e] = ks[e] * er[e] * br;
       const Fr kf = split8(x);
       Fr tf, af;
       tf.hi = ld_tr8(sTh, LT, 32 * kb, 16 * i, lane);
@@ -371,25 +417,27 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       af.lo = ld_tr8(sAl, LT, 32 * kb, 16 * i, lane);
       p1 = mma3(tf, kf, p1);
       p2 = mma3(af, kf, p2);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    // P3 = dT^T ((b k) 2^(G2_r - G2_e)) + dA_qk^T (q 2^(G2_r - G2_e)),  r >= 16 i
+    // P3 = dT^T ((b k) 2^(G2_r - G2_e)) + dA_qk^T (q 2^(G2_r - G2_e)),  e = 16 i + 15, r >= 16 i;
+    // for r in block j the factor is eL_r * 2^(G2f_j - G2l_i)
     f4 p3 = f4zero();
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       if (kb < kbl) continue;
-      const int r0 = 32 * kb + 8 * g;
-      float Gr[8], kr[8], br[8], qr[8], lb[8], lq[8];
-      ldf8(gcol + r0, Gr);
+      const int r0 = 32 * kb + 8 * g, j = 2 * kb + (g >> 1);
+      const bool inc = j > i || (j == i && !uns);
+      const float br = inc ? ex2(pick4(G2f, j) - G2li) : 0.f;
+      float el[8], kr[8], bv[8], qv[8], lb[8], lq[8];
+      ldf8(elc + r0, el);
       unpack8(ld8(sKc + r16 * LXT + r0), kr);
-      unpack8(ld8(sBc + r16 * LXT + r0), br);
-      unpack8(ld8(sQc + r16 * LXT + r0), qr);
+      unpack8(ld8(sBc + r16 * LXT + r0), bv);
+      unpack8(ld8(sQc + r16 * LXT + r0), qv);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const int r = r0 + e;
-        const bool ok = (r >= 16 * i) && !(uns && r < 16 * i + 16);
-        const float f = ex2(Gr[e] - Ge);
-        lb[e] = ok ? br[e] * kr[e] * f : 0.f;
-        lq[e] = ok ? qr[e] * f : 0.f;
+        const float f = el[e] * br;
+        lb[e] = bv[e] * kr[e] * f;
+        lq[e] = qv[e] * f;
       }
       Fr tf, af;
       tf.hi = ld8(sTh + (16 * i + r16) * LT + r0);
@@ -398,33 +446,35 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       af.lo = ld8(sAl + (16 * i + r16) * LT + r0);
       p3 = mma3(tf, split8(lb), p3);
       p3 = mma3(af, split8(lq), p3);
+      __builtin_amdgcn_sched_barrier(0);
     }
 
-    // ---- elementwise chain (App. B.4) on rows rb + u, key c
+    // ---- elementwise chain (App. B.4) on rows rb + u, key c:
+    // gamma_r = eL_r 2^(G2f_i),  tail_r = eR_r 2^(G2_{C-1} - G2l_i)
     const int rb = 16 * i + 4 * g;
-    float Gr4[4];
-    {
-      const float4 t4 = *reinterpret_cast<const float4*>(gcol + rb);
-      Gr4[0] = t4.x; Gr4[1] = t4.y; Gr4[2] = t4.z; Gr4[3] = t4.w;
-    }
+    const float4 eL4 = *reinterpret_cast<const float4*>(elc + rb);
+    const float4 eR4 = *reinterpret_cast<const float4*>(erc + rb);
+    const float elv[4] = {eL4.x, eL4.y, eL4.z, eL4.w}, erv[4] = {eR4.x, eR4.y, eR4.z, eR4.w};
     const bf4 k4 = *reinterpret_cast<const bf4*>(sKc + r16 * LXT + rb);
     const bf4 b4 = *reinterpret_cast<const bf4*>(sBc + r16 * LXT + rb);
     const bf4 q4 = *reinterpret_cast<const bf4*>(sQc + r16 * LXT + rb);
+    const float gam0 = ex2(G2fi), tb = ex2(G2l[3] - G2li);
     float dgl[4], tailp = 0.f;
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const float G = Gr4[u];
-      const float gam = ex2(G), lf = ex2(G - Gp), rf = ex2(Ge - G), tl = ex2(GCl - G);
+      const float lf = elv[u], rf = erv[u], gam = lf * gam0, tl = rf * tb;
       const float kv = (float)k4[u], bv = (float)b4[u], qv = (float)q4[u];
       float dEg = lf * p1[u] - gam * x1[u];
       float dq = scale * gam * x2[u] + lf * p2[u];
       float dKg = rf * p3[u] + tl * x3[u];
       if (uns) {
-        // diagonal block element by element: every factor has exponent <= 0
+        // diagonal block element by element (in-block sums of the log2-decay):
+        // every factor has exponent <= 0
         const int r = rb + u;
+        const float G = sG[r16 * LGT + r];
 #pragma unroll 1
         for (int s = 16 * i; s < 16 * i + 16; ++s) {
-          const float Gs = gcol[s];
+          const float Gs = sG[r16 * LGT + s];
           const float ks = (float)sKc[r16 * LXT + s];
           if (s <= r) {
             const float e = ex2(G - Gs);
@@ -441,7 +491,7 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
           }
         }
       }
-      const size_t o = kb0 + (size_t)(rb + u) * KST + c;
+      const int o = (rb + u) * kst + c;
       dQp[o] = (__bf16)dq;
       dKp[o] = (__bf16)(dEg * bv + dKg);
       dBp[o] = (__bf16)(dEg * kv);
@@ -453,9 +503,9 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     float y = s0;
     {
       const float t1 = __shfl_down(y, 16);
-      if (g < 3) y += t1;
+      y += g < 3 ? t1 : 0.f;
       const float t2 = __shfl_down(y, 32);
-      if (g < 2) y += t2;
+      y += g < 2 ? t2 : 0.f;
     }
     float tp = tailp;
     tp += __shfl_xor(tp, 16);
@@ -464,7 +514,7 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       sBT[(par * 4 + i) * 16 + r16] = y;
       sTL[(par * 4 + i) * 16 + r16] = tp;
     }
-    const float gamC = ex2(GCl);
+    const float gamC = ex2(G2l[3]);
     __syncthreads();
     // gamma_C d gamma_C joins row C - 1, hence every row's suffix sum
     float off = gamC * sHH[par * 16 + r16] + (y - s0);
@@ -473,11 +523,11 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       off += sTL[(par * 4 + i2) * 16 + r16];
       if (i2 > i) off += sBT[(par * 4 + i2) * 16 + r16];
     }
-    a.dg[kb0 + (size_t)(rb + 0) * KST + c] = s0 + off;
-    a.dg[kb0 + (size_t)(rb + 1) * KST + c] = s1 + off;
-    a.dg[kb0 + (size_t)(rb + 2) * KST + c] = s2 + off;
-    a.dg[kb0 + (size_t)(rb + 3) * KST + c] = s3 + off;
-    if (cb + 1 < NCB) GDR2_STAGE(cb + 1, par ^ 1)
+    dGp[(rb + 0) * kst + c] = s0 + off;
+    dGp[(rb + 1) * kst + c] = s1 + off;
+    dGp[(rb + 2) * kst + c] = s2 + off;
+    dGp[(rb + 3) * kst + c] = s3 + off;
+    if (cb + 1 < NCB) GDR2_STAGE(par ^ 1)
     __syncthreads();
   }
 #undef GDR2_PREFETCH
