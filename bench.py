@@ -1,10 +1,15 @@
 """Throughput of the chunkwise GDR-2 operator (forward + gate-aware backward) on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-decode]
+                    [--path stored|recompute]
 
-One step = gdr2_chunk_fwd + gdr2_chunk_bwd over one batch of the 1.3B-layer
+One step = the forward + gate-aware backward over one batch of the 1.3B-layer
 training shape (B=8, H=16, T=4096, d_k=d_v=128, bf16 inputs, fp32 log-decay
-and state), inputs resident in HBM before the timed region.  Prints one JSON
+and state), inputs resident in HBM before the timed region.  The default
+training path keeps the forward's A, chunk states and R for the backward
+(gdr2_chunk_fwd_save + gdr2_chunk_bwd_saved); the memory-saving path, where
+the backward recomputes them (gdr2_chunk_fwd + gdr2_chunk_bwd), is timed beside
+it over the same number of steps.  Prints one JSON
 line with tokens/s (B*T per step over the K timed steps), the roofline of the
 dominant kernel (per-kernel durations from hipEvents recorded on the launch
 stream during the timed steps) and the CPU oracle timed on a bounded sample.
@@ -21,8 +26,11 @@ PEAK_TFLOPS = {"fp32": 157.3, "bf16": 2500.0}
 MFMA_DTYPE = "bf16"                      # operand type of the path's products (v_mfma_f32_16x16x32_bf16)
 
 
-def kernel_model(B, T, H, Dk, Dv):
+def kernel_model(B, T, H, Dk, Dv, stored=True):
     """Algorithmic flops and HBM bytes per launch of each kernel of the bf16 path.
+
+    stored: the forward also writes A, the chunk-start states and R for the
+    backward (the saved training path); otherwise the backward recomputes them.
 
     Per chunk-head (C = 64 tokens of one head); a causal C x C x D product
     counts C^2 D flops (half of the dense 2 C^2 D).  Bytes are each kernel's
@@ -48,8 +56,9 @@ def kernel_model(B, T, H, Dk, Dv):
     m = {}
     intra_fl = tri + tri + solve + tri + triv
     intra_by = 3 * kin + kf + 2 * vin + ws_y + ws_q + ws_a + ws_k + ws_u + ws_g
-    m["fwd_intra"] = (intra_fl, intra_by)
-    m["fwd_state"] = (3 * mm + triv, ws_y + ws_q + ws_a + ws_k + ws_u + ws_g + vin + seq_state)
+    m["fwd_intra"] = (intra_fl, intra_by + (ws_am if stored else 0))
+    m["fwd_state"] = (3 * mm + triv, ws_y + ws_q + ws_a + ws_k + ws_u + ws_g + vin + seq_state
+                      + (st + vf if stored else 0))
     m["bwd_recompute_intra"] = (intra_fl, intra_by + ws_am)
     m["bwd_recompute_state"] = (2 * mm, ws_y + ws_k + ws_u + ws_g + st / NT + st + vf)
     m["bwd_state"] = (triv + 3 * mm, ws_y + ws_q + ws_a + ws_k + ws_g + vin + seq_state + st + ws_dr)
@@ -141,6 +150,13 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--cpu-heads", type=int, default=16)
+    ap.add_argument("--path", choices=("stored", "recompute"), default="stored",
+                    help="training path of the timed step: the forward keeps A, h and R for the backward "
+                         "(stored) or the backward recomputes them (recompute, the memory-saving path); "
+                         "the other path is timed too and reported beside")
+    ap.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
+                    help="run one copy-like elementwise kernel (torch.neg) over MIB MiB of fp32 before the "
+                         "timed steps: the reference that scales rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
@@ -166,9 +182,26 @@ def main():
     prob = g2.Gdr2Problem(B, T, H, Dk, Dv, 64, d["scale"], g2.GDR2_BF16)
     ws = torch.empty(g2.gdr2_chunk_workspace_bytes(prob, 1), dtype=torch.uint8, device=dev)
 
-    def step():
-        g2.gdr2_chunk_fwd(q, k, v, la, b, w, None, scale=d["scale"], o=o, S_T=ST, ws=ws)
-        g2.gdr2_chunk_bwd(q, k, v, la, b, w, None, do, None, scale=d["scale"], grads=grads, ws=ws)
+    def make_step(stored):
+        def step():
+            g2.gdr2_chunk_fwd(q, k, v, la, b, w, None, scale=d["scale"], o=o, S_T=ST, ws=ws, save=stored)
+            g2.gdr2_chunk_bwd(q, k, v, la, b, w, None, do, None, scale=d["scale"], grads=grads, ws=ws,
+                              saved=stored)
+        return step
+
+    stored = args.path == "stored"
+    step = make_step(stored)
+
+    if args.calib_copy > 0:
+        n = args.calib_copy * (1 << 20) // 4
+        src_c = torch.ones(n, device=dev)
+        dst_c = torch.empty_like(src_c)
+        torch.cuda.synchronize()
+        torch.neg(src_c, out=dst_c)               # one elementwise kernel: n*4 bytes in, n*4 out
+        torch.cuda.synchronize()
+        print(f"[bench] calibration copy: {args.calib_copy} MiB read + {args.calib_copy} MiB written",
+              file=sys.stderr, flush=True)
+        del src_c, dst_c
 
     print("[bench] warmup", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
@@ -193,7 +226,7 @@ def main():
     tokens_per_s = B * T / (ms_step * 1e-3)
     print(f"[bench] {ms_step:.3f} ms/step ({wall / args.steps * 1e3:.3f} ms wall)", file=sys.stderr, flush=True)
 
-    model = kernel_model(B, T, H, Dk, Dv)
+    model = kernel_model(B, T, H, Dk, Dv, stored)
     kern = {}
     for name, (ms, cnt) in per_kernel.items():
         if cnt == 0:
@@ -216,8 +249,22 @@ def main():
     roof.update({"kernel": dom, "avg_us": kd["avg_us"], "traffic": None,
                  "mfma_dtype": MFMA_DTYPE, "arith_intensity": ai, "ridge": ridge})
 
+    # the other training path, same number of steps, no per-kernel events
+    other = make_step(not stored)
+    for _ in range(args.warmup):
+        other()
+    torch.cuda.synchronize()
+    f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    f0.record()
+    for _ in range(args.steps):
+        other()
+    f1.record()
+    torch.cuda.synchronize()
+    other_ms = f0.elapsed_time(f1) / args.steps
+    print(f"[bench] {'recompute' if stored else 'stored'} path: {other_ms:.3f} ms/step", file=sys.stderr, flush=True)
+
     fwd_flops = sum(model[n][0] for n in ("fwd_intra", "fwd_state"))
-    step_flops = sum(model[n][0] for n in model)
+    step_flops = sum(model[n][0] for n in model if n in kern)
     out = {
         "metric": "tokens/s fwd+bwd GDR-2 chunked op (H=16,d=128,T=4096,bf16); % MFMA peak",
         "value": tokens_per_s, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
@@ -225,7 +272,8 @@ def main():
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "GDR-2 chunkwise fwd+bwd, 1.3B-layer training shape",
                    "B": B, "H": H, "T": T, "d_k": Dk, "d_v": Dv, "chunk": 64, "io": "bf16",
-                   "log_alpha": "fp32", "state": "fp32", "global_batch": B, "seq_len": T},
+                   "log_alpha": "fp32", "state": "fp32", "global_batch": B, "seq_len": T,
+                   "training_path": args.path},
         "mfma_pct_of_bf16_peak": 100.0 * step_flops / (ms_step * 1e-3) / 1e12 / PEAK_TFLOPS["bf16"],
         "roofline": roof,
         "kernels": {n: {kk: (round(vv, 3) if isinstance(vv, float) else vv) for kk, vv in kv.items()}
@@ -233,6 +281,8 @@ def main():
         "fwd_ms": sum(kern[n]["avg_us"] for n in ("fwd_intra", "fwd_state") if n in kern) / 1e3,
         "bwd_ms": sum(kern[n]["avg_us"] for n in kern if n.startswith("bwd")) / 1e3,
         "alg_tflops_per_step": step_flops / 1e12, "fwd_alg_tflops": fwd_flops / 1e12,
+        "other_path": {"training_path": "recompute" if stored else "stored", "ms_per_step": other_ms,
+                       "tokens_per_s": B * T / (other_ms * 1e-3)},
     }
     if not args.no_decode:
         print("[bench] decode", file=sys.stderr, flush=True)

@@ -113,6 +113,30 @@ gdr2_status gdr2_chunk_bwd(const gdr2_problem* problem, const void* q, const voi
                            float* dlog_alpha, void* db, void* dw, float* dS0, void* ws,
                            size_t ws_bytes, hipStream_t stream);
 
+/* Training path that keeps the forward's intermediates instead of recomputing
+ * them (App. D.3 names recomputation as the memory-saving path; a8 of the
+ * backward then reads h_n, R and A as stored).  gdr2_chunk_fwd_save computes
+ * exactly what gdr2_chunk_fwd computes and additionally leaves in ws the
+ * intra-chunk tiles, A = (I + T)^{-1}, the chunk-start states h_n and R_n;
+ * gdr2_chunk_bwd_saved returns exactly what gdr2_chunk_bwd returns but reads
+ * those instead of recomputing them (it skips the two recompute kernels).
+ *   * ws must hold at least gdr2_chunk_workspace_bytes(p, 1) bytes for both
+ *     calls, and must not be written between them.
+ *   * The two calls must get the same problem, q, k, v, log_alpha, b, w and
+ *     S0 (the saved states already contain S0); otherwise the gradients are
+ *     undefined.  Other arguments, errors and ownership as in gdr2_chunk_fwd /
+ *     gdr2_chunk_bwd. */
+gdr2_status gdr2_chunk_fwd_save(const gdr2_problem* problem, const void* q, const void* k,
+                                const void* v, const float* log_alpha, const void* b,
+                                const void* w, const float* S0, void* o, float* S_T, void* ws,
+                                size_t ws_bytes, hipStream_t stream);
+gdr2_status gdr2_chunk_bwd_saved(const gdr2_problem* problem, const void* q, const void* k,
+                                 const void* v, const float* log_alpha, const void* b,
+                                 const void* w, const float* S0, const void* dout,
+                                 const float* dS_T, void* dq, void* dk, void* dv,
+                                 float* dlog_alpha, void* db, void* dw, float* dS0, void* ws,
+                                 size_t ws_bytes, hipStream_t stream);
+
 /* Recurrent (token-by-token) forward for decoding (App. C.5): applies the
  * update to problem->T >= 1 consecutive tokens (T = 1 for one decode step),
  * keeping S in fp32 and updating it in place; o (B,T,H,Dv) in problem->dtype.
@@ -132,8 +156,9 @@ typedef enum gdr2_kernel_id {
   GDR2_K_BWD_RECOMPUTE_INTRA = 2, /* backward: intra-chunk recompute              */
   GDR2_K_BWD_RECOMPUTE_STATE = 3, /* backward: chunk-state recompute              */
   GDR2_K_BWD_STATE = 4,           /* backward: reverse state scan                 */
-  GDR2_K_BWD_WY = 5,              /* backward: gate-aware WY VJP                  */
-  GDR2_K_BWD_INTRA = 6,           /* backward: intra-chunk VJP + decay chain      */
+  GDR2_K_BWD_WY = 5,              /* backward: gate-aware WY VJP (fp32 problems)  */
+  GDR2_K_BWD_INTRA = 6,           /* backward: intra-chunk VJP + decay chain (bf16
+                                     problems: with the WY VJP, one kernel)      */
   GDR2_K_RECURRENT = 7,           /* recurrent / decode                           */
   GDR2_NUM_KERNELS = 8
 } gdr2_kernel_id;

@@ -15,7 +15,8 @@ import os
 __all__ = [
     "GDR2_OK", "GDR2_EINVAL", "GDR2_EUNSUPPORTED", "GDR2_EWORKSPACE", "GDR2_EHIP",
     "GDR2_BF16", "GDR2_FP32", "Gdr2Problem", "Gdr2Error", "lib", "lib_path",
-    "gdr2_chunk_workspace_bytes", "gdr2_chunk_fwd", "gdr2_chunk_bwd",
+    "gdr2_chunk_workspace_bytes", "gdr2_chunk_fwd", "gdr2_chunk_bwd", "gdr2_chunk_fwd_save",
+    "gdr2_chunk_bwd_saved",
     "gdr2_recurrent_step", "gdr2_status_str", "CHUNK", "KERNEL_NAMES",
     "gdr2_profile_enable", "gdr2_profile_collect",
 ]
@@ -66,6 +67,10 @@ def lib():
         L.gdr2_chunk_fwd.restype = ctypes.c_int
         L.gdr2_chunk_bwd.argtypes = [P] + [vp] * 17 + [ctypes.c_size_t, vp]
         L.gdr2_chunk_bwd.restype = ctypes.c_int
+        L.gdr2_chunk_fwd_save.argtypes = L.gdr2_chunk_fwd.argtypes
+        L.gdr2_chunk_fwd_save.restype = ctypes.c_int
+        L.gdr2_chunk_bwd_saved.argtypes = L.gdr2_chunk_bwd.argtypes
+        L.gdr2_chunk_bwd_saved.restype = ctypes.c_int
         L.gdr2_recurrent_step.argtypes = [P] + [vp] * 8 + [vp]
         L.gdr2_recurrent_step.restype = ctypes.c_int
         L.gdr2_profile_enable.argtypes = [ctypes.c_int]
@@ -149,8 +154,11 @@ def gdr2_chunk_workspace_bytes(problem, for_backward):
 
 
 def gdr2_chunk_fwd(q, k, v, log_alpha, b, w, S0=None, *, scale=None, o=None, S_T=None,
-                   want_state=True, ws=None):
-    """Chunkwise GDR-2 forward.  Returns (o, S_T) (S_T None unless wanted)."""
+                   want_state=True, ws=None, save=False):
+    """Chunkwise GDR-2 forward.  Returns (o, S_T) (S_T None unless wanted).
+
+    save=True calls gdr2_chunk_fwd_save: ws (backward-sized, required) then
+    holds the intermediates that gdr2_chunk_bwd(..., saved=True) reads."""
     torch = _torch()
     B, T, H, Dk, Dv = _validate(q, k, v, log_alpha, b, w)
     _require("S0", S0, (B, H, Dk, Dv), torch.float32)
@@ -161,18 +169,23 @@ def gdr2_chunk_fwd(q, k, v, log_alpha, b, w, S0=None, *, scale=None, o=None, S_T
     if S_T is None and want_state:
         S_T = torch.empty((B, H, Dk, Dv), dtype=torch.float32, device=q.device)
     _require("S_T", S_T, (B, H, Dk, Dv), torch.float32)
-    need = gdr2_chunk_workspace_bytes(prob, 0)
+    need = gdr2_chunk_workspace_bytes(prob, 1 if save else 0)
     if ws is None:
+        if save:
+            raise ValueError("save=True needs the workspace that the backward will read")
         ws = torch.empty(need, dtype=torch.uint8, device=q.device)
-    st = lib().gdr2_chunk_fwd(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(b),
+    fn = lib().gdr2_chunk_fwd_save if save else lib().gdr2_chunk_fwd
+    st = fn(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(b),
                               _ptr(w), _ptr(S0), _ptr(o), _ptr(S_T), _ptr(ws), ws.numel(), _stream())
-    _check(st, "gdr2_chunk_fwd")
+    _check(st, "gdr2_chunk_fwd_save" if save else "gdr2_chunk_fwd")
     return o, S_T
 
 
 def gdr2_chunk_bwd(q, k, v, log_alpha, b, w, S0, dout, dS_T=None, *, scale=None, grads=None,
-                   want_dS0=True, ws=None):
-    """Gate-aware chunkwise backward.  Returns dict dq, dk, dv, dlog_alpha, db, dw, dS0."""
+                   want_dS0=True, ws=None, saved=False):
+    """Gate-aware chunkwise backward.  Returns dict dq, dk, dv, dlog_alpha, db, dw, dS0.
+
+    saved=True calls gdr2_chunk_bwd_saved on the ws a save=True forward filled."""
     torch = _torch()
     B, T, H, Dk, Dv = _validate(q, k, v, log_alpha, b, w)
     _require("S0", S0, (B, H, Dk, Dv), torch.float32)
@@ -193,12 +206,15 @@ def gdr2_chunk_bwd(q, k, v, log_alpha, b, w, S0, dout, dS_T=None, *, scale=None,
         g.setdefault("dS0", None)
     need = gdr2_chunk_workspace_bytes(prob, 1)
     if ws is None:
+        if saved:
+            raise ValueError("saved=True needs the workspace of the saving forward")
         ws = torch.empty(need, dtype=torch.uint8, device=dev)
-    st = lib().gdr2_chunk_bwd(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(b),
+    fn = lib().gdr2_chunk_bwd_saved if saved else lib().gdr2_chunk_bwd
+    st = fn(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(b),
                               _ptr(w), _ptr(S0), _ptr(dout), _ptr(dS_T), _ptr(g["dq"]), _ptr(g["dk"]),
                               _ptr(g["dv"]), _ptr(g["dlog_alpha"]), _ptr(g["db"]), _ptr(g["dw"]),
                               _ptr(g["dS0"]), _ptr(ws), ws.numel(), _stream())
-    _check(st, "gdr2_chunk_bwd")
+    _check(st, "gdr2_chunk_bwd_saved" if saved else "gdr2_chunk_bwd")
     return g
 
 

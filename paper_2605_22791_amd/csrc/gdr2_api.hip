@@ -177,61 +177,72 @@ hipError_t dispatch(int Dk, int Dv, A&&... args) {
 
 template <int DK, int DV, typename TIn>
 struct FwdRun {
+  // save: also leave A, the chunk-start states and R in the workspace (backward layout)
   static hipError_t run(const gdr2_problem* p, const void* q, const void* k, const void* v,
                         const float* g, const void* b, const void* w, const float* S0, void* o,
-                        float* ST, void* ws, hipStream_t st) {
+                        float* ST, void* ws, bool save, hipStream_t st) {
+    const Layout L = layout(p, save);
+    const int NT = p->T / CH;
     if (std::is_same<TIn, bf16_t>::value) {
       // bf16: chunk-parallel intra-chunk kernel, then the state scan with the output
-      const Layout L = layout(p, false);
       IntraBf16Args ia{static_cast<const bf16_t*>(q), static_cast<const bf16_t*>(k),
                        static_cast<const bf16_t*>(v), g, static_cast<const bf16_t*>(b),
                        static_cast<const bf16_t*>(w), at<unsigned char>(ws, L.bY),
                        at<unsigned char>(ws, L.bQ), at<unsigned char>(ws, L.bA),
-                       at<unsigned char>(ws, L.bK), at<float>(ws, L.bU), at<float>(ws, L.bG), nullptr,
-                       p->B, p->T, p->H, p->T / CH};
+                       at<unsigned char>(ws, L.bK), at<float>(ws, L.bU), at<float>(ws, L.bG),
+                       save ? at<unsigned char>(ws, L.bAm) : nullptr, p->B, p->T, p->H, NT};
       hipError_t e = timed(GDR2_K_FWD_INTRA, st, [&] { return launch_intra_bf16<DK, DV>(ia, st); });
       if (e != hipSuccess) return e;
-      ScanArgs sa{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.U, ia.GC, S0, ST, static_cast<bf16_t*>(o), nullptr, nullptr,
-                  p->B, p->T, p->H, p->T / CH, p->scale};
-      return timed(GDR2_K_FWD_STATE, st, [&] { return launch_scan_bf16<DK, DV, true, false>(sa, st); });
+      ScanArgs sa{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.U, ia.GC, S0, ST, static_cast<bf16_t*>(o),
+                  save ? at<float>(ws, L.Hs) : nullptr, save ? at<float>(ws, L.Rs) : nullptr,
+                  p->B, p->T, p->H, NT, p->scale};
+      return timed(GDR2_K_FWD_STATE, st, [&] {
+        return save ? launch_scan_bf16<DK, DV, true, true>(sa, st) : launch_scan_bf16<DK, DV, true, false>(sa, st);
+      });
     }
-    const Layout L = layout(p, false);
     IntraArgs<TIn> ia{static_cast<const TIn*>(q), static_cast<const TIn*>(k),
                       static_cast<const TIn*>(v), g, static_cast<const TIn*>(b),
                       static_cast<const TIn*>(w), at<float>(ws, L.Y), at<float>(ws, L.U),
                       at<float>(ws, L.Kt), at<float>(ws, L.Qg), at<float>(ws, L.Aqk),
-                      at<float>(ws, L.GC), p->T, p->H, p->T / CH};
+                      at<float>(ws, L.GC), p->T, p->H, NT};
     hipError_t e = timed(GDR2_K_FWD_INTRA, st, [&] { return launch_fwd_intra<DK, DV, TIn>(ia, p->B, st); });
     if (e != hipSuccess) return e;
     StateArgs<TIn> sa{ia.Y, ia.U, ia.Kt, ia.Qg, ia.Aqk, ia.GC, S0, ST, static_cast<TIn*>(o),
-                      nullptr, nullptr, p->T, p->H, p->T / CH, p->scale};
-    return timed(GDR2_K_FWD_STATE, st,
-                 [&] { return launch_fwd_state<DK, DV, TIn, true, false>(sa, p->B, st); });
+                      save ? at<float>(ws, L.Hs) : nullptr, save ? at<float>(ws, L.Rs) : nullptr,
+                      p->T, p->H, NT, p->scale};
+    return timed(GDR2_K_FWD_STATE, st, [&] {
+      return save ? launch_fwd_state<DK, DV, TIn, true, true>(sa, p->B, st)
+                  : launch_fwd_state<DK, DV, TIn, true, false>(sa, p->B, st);
+    });
   }
 };
 
 template <int DK, int DV, typename TIn>
 struct BwdRun {
+  // saved: the workspace holds what a saving forward left there; skip the recompute
   static hipError_t run(const gdr2_problem* p, const void* q, const void* k, const void* v,
                         const float* g, const void* b, const void* w, const float* S0,
                         const void* dout, const float* dST, void* dq, void* dk, void* dv,
-                        float* dg, void* db, void* dw, float* dS0, void* ws, hipStream_t st) {
+                        float* dg, void* db, void* dw, float* dS0, void* ws, bool saved, hipStream_t st) {
     const Layout L = layout(p, true);
     const int NT = p->T / CH;
+    hipError_t e = hipSuccess;
     if (std::is_same<TIn, bf16_t>::value) {
-      // recompute: intra-chunk tiles, then the forward scan storing the chunk states and R
       IntraBf16Args ia{static_cast<const bf16_t*>(q), static_cast<const bf16_t*>(k),
                        static_cast<const bf16_t*>(v), g, static_cast<const bf16_t*>(b),
                        static_cast<const bf16_t*>(w), at<unsigned char>(ws, L.bY),
                        at<unsigned char>(ws, L.bQ), at<unsigned char>(ws, L.bA),
                        at<unsigned char>(ws, L.bK), at<float>(ws, L.bU), at<float>(ws, L.bG),
                        at<unsigned char>(ws, L.bAm), p->B, p->T, p->H, NT};
-      hipError_t e = timed(GDR2_K_BWD_RECOMPUTE_INTRA, st, [&] { return launch_intra_bf16<DK, DV>(ia, st); });
-      if (e != hipSuccess) return e;
-      ScanArgs sa{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.U, ia.GC, S0, nullptr, nullptr, at<float>(ws, L.Hs),
-                  at<float>(ws, L.Rs), p->B, p->T, p->H, NT, p->scale};
-      e = timed(GDR2_K_BWD_RECOMPUTE_STATE, st, [&] { return launch_scan_bf16<DK, DV, false, true>(sa, st); });
-      if (e != hipSuccess) return e;
+      if (!saved) {
+        // recompute: intra-chunk tiles (with A), then the forward scan storing the chunk states and R
+        e = timed(GDR2_K_BWD_RECOMPUTE_INTRA, st, [&] { return launch_intra_bf16<DK, DV>(ia, st); });
+        if (e != hipSuccess) return e;
+        ScanArgs sa{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.U, ia.GC, S0, nullptr, nullptr, at<float>(ws, L.Hs),
+                    at<float>(ws, L.Rs), p->B, p->T, p->H, NT, p->scale};
+        e = timed(GDR2_K_BWD_RECOMPUTE_STATE, st, [&] { return launch_scan_bf16<DK, DV, false, true>(sa, st); });
+        if (e != hipSuccess) return e;
+      }
       BScanArgs ba{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.GC, static_cast<const bf16_t*>(dout), dST, dS0,
                    at<float>(ws, L.DH), at<unsigned char>(ws, L.bDR), p->B, p->T, p->H, NT, p->scale};
       e = timed(GDR2_K_BWD_STATE, st, [&] { return launch_bscan_bf16<DK, DV>(ba, st); });
@@ -251,14 +262,15 @@ struct BwdRun {
                       static_cast<const TIn*>(w), at<float>(ws, L.Y), at<float>(ws, L.U),
                       at<float>(ws, L.Kt), at<float>(ws, L.Qg), at<float>(ws, L.Aqk),
                       at<float>(ws, L.GC), p->T, p->H, NT};
-    hipError_t e = timed(GDR2_K_BWD_RECOMPUTE_INTRA, st,
-                         [&] { return launch_fwd_intra<DK, DV, TIn>(ia, p->B, st); });
-    if (e != hipSuccess) return e;
     StateArgs<TIn> sa{ia.Y, ia.U, ia.Kt, ia.Qg, ia.Aqk, ia.GC, S0, nullptr, nullptr,
                       at<float>(ws, L.Hs), at<float>(ws, L.Rs), p->T, p->H, NT, p->scale};
-    e = timed(GDR2_K_BWD_RECOMPUTE_STATE, st,
-              [&] { return launch_fwd_state<DK, DV, TIn, false, true>(sa, p->B, st); });
-    if (e != hipSuccess) return e;
+    if (!saved) {
+      e = timed(GDR2_K_BWD_RECOMPUTE_INTRA, st, [&] { return launch_fwd_intra<DK, DV, TIn>(ia, p->B, st); });
+      if (e != hipSuccess) return e;
+      e = timed(GDR2_K_BWD_RECOMPUTE_STATE, st,
+                [&] { return launch_fwd_state<DK, DV, TIn, false, true>(sa, p->B, st); });
+      if (e != hipSuccess) return e;
+    }
     BwdStateArgs<TIn> ba{ia.Qg, ia.Kt, ia.Y, ia.Aqk, ia.GC, static_cast<const TIn*>(dout), dST,
                          dS0, at<float>(ws, L.DH), at<float>(ws, L.DR), p->T, p->H, NT, p->scale};
     e = timed(GDR2_K_BWD_STATE, st, [&] { return launch_bwd_state<DK, DV, TIn>(ba, p->B, st); });
@@ -312,26 +324,28 @@ gdr2_status gdr2_chunk_workspace_bytes(const gdr2_problem* p, int for_backward, 
   return GDR2_OK;
 }
 
-gdr2_status gdr2_chunk_fwd(const gdr2_problem* p, const void* q, const void* k, const void* v,
-                           const float* log_alpha, const void* b, const void* w, const float* S0,
-                           void* o, float* S_T, void* ws, size_t ws_bytes, hipStream_t stream) {
+namespace {
+
+gdr2_status chunk_fwd(const gdr2_problem* p, const void* q, const void* k, const void* v,
+                      const float* log_alpha, const void* b, const void* w, const float* S0, void* o,
+                      float* S_T, void* ws, size_t ws_bytes, bool save, hipStream_t stream) {
   gdr2_status s = check_problem(p, true);
   if (s != GDR2_OK) return s;
   if (!all_ok({q, k, v, log_alpha, b, w, o, ws}) || !opt_ok({S0, S_T})) return GDR2_EINVAL;
-  if (ws_bytes < layout(p, false).total) return GDR2_EWORKSPACE;
+  if (ws_bytes < layout(p, save).total) return GDR2_EWORKSPACE;
   hipError_t e;
   if (p->dtype == GDR2_BF16)
-    e = dispatch<FwdRun, bf16_t>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S0, o, S_T, ws, stream);
+    e = dispatch<FwdRun, bf16_t>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S0, o, S_T, ws, save, stream);
   else
-    e = dispatch<FwdRun, float>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S0, o, S_T, ws, stream);
+    e = dispatch<FwdRun, float>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S0, o, S_T, ws, save, stream);
   return hip_status(e, stream);
 }
 
-gdr2_status gdr2_chunk_bwd(const gdr2_problem* p, const void* q, const void* k, const void* v,
-                           const float* log_alpha, const void* b, const void* w, const float* S0,
-                           const void* dout, const float* dS_T, void* dq, void* dk, void* dv,
-                           float* dlog_alpha, void* db, void* dw, float* dS0, void* ws,
-                           size_t ws_bytes, hipStream_t stream) {
+gdr2_status chunk_bwd(const gdr2_problem* p, const void* q, const void* k, const void* v,
+                      const float* log_alpha, const void* b, const void* w, const float* S0,
+                      const void* dout, const float* dS_T, void* dq, void* dk, void* dv,
+                      float* dlog_alpha, void* db, void* dw, float* dS0, void* ws, size_t ws_bytes,
+                      bool saved, hipStream_t stream) {
   gdr2_status s = check_problem(p, true);
   if (s != GDR2_OK) return s;
   if (!all_ok({q, k, v, log_alpha, b, w, dout, dq, dk, dv, dlog_alpha, db, dw, ws}) ||
@@ -341,11 +355,43 @@ gdr2_status gdr2_chunk_bwd(const gdr2_problem* p, const void* q, const void* k, 
   hipError_t e;
   if (p->dtype == GDR2_BF16)
     e = dispatch<BwdRun, bf16_t>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S0, dout, dS_T, dq,
-                                 dk, dv, dlog_alpha, db, dw, dS0, ws, stream);
+                                 dk, dv, dlog_alpha, db, dw, dS0, ws, saved, stream);
   else
     e = dispatch<BwdRun, float>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S0, dout, dS_T, dq,
-                                dk, dv, dlog_alpha, db, dw, dS0, ws, stream);
+                                dk, dv, dlog_alpha, db, dw, dS0, ws, saved, stream);
   return hip_status(e, stream);
+}
+
+}  // namespace
+
+gdr2_status gdr2_chunk_fwd(const gdr2_problem* p, const void* q, const void* k, const void* v,
+                           const float* log_alpha, const void* b, const void* w, const float* S0,
+                           void* o, float* S_T, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return chunk_fwd(p, q, k, v, log_alpha, b, w, S0, o, S_T, ws, ws_bytes, false, stream);
+}
+
+gdr2_status gdr2_chunk_fwd_save(const gdr2_problem* p, const void* q, const void* k, const void* v,
+                                const float* log_alpha, const void* b, const void* w, const float* S0,
+                                void* o, float* S_T, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return chunk_fwd(p, q, k, v, log_alpha, b, w, S0, o, S_T, ws, ws_bytes, true, stream);
+}
+
+gdr2_status gdr2_chunk_bwd(const gdr2_problem* p, const void* q, const void* k, const void* v,
+                           const float* log_alpha, const void* b, const void* w, const float* S0,
+                           const void* dout, const float* dS_T, void* dq, void* dk, void* dv,
+                           float* dlog_alpha, void* db, void* dw, float* dS0, void* ws,
+                           size_t ws_bytes, hipStream_t stream) {
+  return chunk_bwd(p, q, k, v, log_alpha, b, w, S0, dout, dS_T, dq, dk, dv, dlog_alpha, db, dw, dS0, ws,
+                   ws_bytes, false, stream);
+}
+
+gdr2_status gdr2_chunk_bwd_saved(const gdr2_problem* p, const void* q, const void* k, const void* v,
+                                 const float* log_alpha, const void* b, const void* w, const float* S0,
+                                 const void* dout, const float* dS_T, void* dq, void* dk, void* dv,
+                                 float* dlog_alpha, void* db, void* dw, float* dS0, void* ws,
+                                 size_t ws_bytes, hipStream_t stream) {
+  return chunk_bwd(p, q, k, v, log_alpha, b, w, S0, dout, dS_T, dq, dk, dv, dlog_alpha, db, dw, dS0, ws,
+                   ws_bytes, true, stream);
 }
 
 gdr2_status gdr2_recurrent_step(const gdr2_problem* p, const void* q, const void* k, const void* v,

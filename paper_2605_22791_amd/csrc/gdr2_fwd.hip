@@ -353,7 +353,9 @@ hipError_t launch_fwd_state(const StateArgs<TIn>& a, int B, hipStream_t st) {
   template hipError_t launch_fwd_state<DK, DV, TIN, true, false>(const StateArgs<TIN>&, int,  \
                                                                  hipStream_t);               \
   template hipError_t launch_fwd_state<DK, DV, TIN, false, true>(const StateArgs<TIN>&, int,  \
-                                                                 hipStream_t);
+                                                                 hipStream_t);               \
+  template hipError_t launch_fwd_state<DK, DV, TIN, true, true>(const StateArgs<TIN>&, int,   \
+                                                                hipStream_t);
 
 GDR2_INST_FWD(64, 64, float)
 GDR2_INST_FWD(64, 128, float)

@@ -11,7 +11,8 @@
 // the next chunk's operand blocks are fetched into registers while the
 // current chunk computes and copied to LDS at its end.  The two value slices
 // of one head run on the same XCD so that their shared reads hit one L2.
-// With STORE_H the chunk-start states and R are written for the backward.
+// With STORE_H the chunk-start states and R are written for the backward
+// (alone in the backward's recompute, or with the output when the forward keeps them).
 //
 // Precision: Y S uses the bf16 part of S (Y itself is bf16); every other
 // product is split hi/lo and fp32-accurate.
@@ -297,7 +298,8 @@ hipError_t launch_scan_bf16(const ScanArgs& a, hipStream_t st) {
 
 #define GDR2_INST_SCAN2(DK, DV)                                                          \
   template hipError_t launch_scan_bf16<DK, DV, true, false>(const ScanArgs&, hipStream_t); \
-  template hipError_t launch_scan_bf16<DK, DV, false, true>(const ScanArgs&, hipStream_t);
+  template hipError_t launch_scan_bf16<DK, DV, false, true>(const ScanArgs&, hipStream_t); \
+  template hipError_t launch_scan_bf16<DK, DV, true, true>(const ScanArgs&, hipStream_t);
 
 GDR2_INST_SCAN2(64, 64)
 GDR2_INST_SCAN2(64, 128)

@@ -30,7 +30,8 @@ def _declared_symbols():
 
 def test_header_declares_the_entry_points():
     assert _declared_symbols() == sorted(["gdr2_chunk_workspace_bytes", "gdr2_chunk_fwd",
-                                          "gdr2_chunk_bwd", "gdr2_recurrent_step",
+                                          "gdr2_chunk_bwd", "gdr2_chunk_fwd_save",
+                                          "gdr2_chunk_bwd_saved", "gdr2_recurrent_step",
                                           "gdr2_status_str", "gdr2_profile_enable",
                                           "gdr2_profile_collect"])
 
@@ -191,3 +192,27 @@ def test_input_recipes():
     assert np.all(d1["log_alpha"] == d1["log_alpha"][..., :1])
     assert np.all((d1["q"].view(np.uint32) & 0xFFFF) == 0)
     assert set(CONFIGS) == {0, 1, 2, 3, 4}
+
+
+def test_saved_training_path_validation():
+    """gdr2_chunk_fwd_save needs the backward-sized workspace; both saved-path calls
+    validate like their plain counterparts before any launch."""
+    L = g2.lib()
+    p = _prob(B=2, T=256, H=4, Dk=128, Dv=64)
+    fwd = g2.gdr2_chunk_workspace_bytes(p, 0)
+    bwd = g2.gdr2_chunk_workspace_bytes(p, 1)
+    assert bwd > fwd
+    vp = lambda xs: [ctypes.c_void_p(x) if x else None for x in xs]
+    fargs = [FAKE] * 6 + [None, FAKE, None, FAKE]
+    assert L.gdr2_chunk_fwd_save(ctypes.byref(p), *vp(fargs), fwd, None) == g2.GDR2_EWORKSPACE
+    assert L.gdr2_chunk_fwd_save(ctypes.byref(p), *vp(fargs), bwd - 1, None) == g2.GDR2_EWORKSPACE
+    bad = list(fargs)
+    bad[0] = None
+    assert L.gdr2_chunk_fwd_save(ctypes.byref(p), *vp(bad), bwd, None) == g2.GDR2_EINVAL
+    bargs = [FAKE] * 6 + [None, FAKE, None] + [FAKE] * 6 + [None, FAKE]
+    assert L.gdr2_chunk_bwd_saved(ctypes.byref(p), *vp(bargs), bwd - 1, None) == g2.GDR2_EWORKSPACE
+    bad = list(bargs)
+    bad[7] = None                      # dout
+    assert L.gdr2_chunk_bwd_saved(ctypes.byref(p), *vp(bad), bwd, None) == g2.GDR2_EINVAL
+    q = _prob(Dk=96)
+    assert L.gdr2_chunk_bwd_saved(ctypes.byref(q), *vp(bargs), 1 << 40, None) == g2.GDR2_EUNSUPPORTED

@@ -204,3 +204,27 @@ def test_bf16_backward_workspace_intermediates(Dk, Dv):
     print({k_: f"{v_:.2e}" for k_, v_ in worst.items()})
     # A comes from a Gram matrix formed in one bf16 pass; dR inherits the bf16 Y of the reverse scan
     assert worst["A"] < 1e-2 and worst["dR"] < 2e-3, worst
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_saved_training_path_matches_recompute(dtype):
+    """gdr2_chunk_fwd_save / gdr2_chunk_bwd_saved run the same kernels on the same
+    inputs as the recomputing backward, so o, S_T and every gradient must be
+    bit-identical to it (and therefore within the bound of the adjoint)."""
+    import torch
+    import paper_2605_22791_amd as g2
+    d = make_inputs(2, 256, 3, 128, 64, seed=68, dtype=dtype, s0_std=0.05, with_dST=True)
+    _case(f"{dtype} saved training path B2 H3 T256 Dk128 Dv64")
+    x = dev_inputs(d)
+    args = [x[n] for n in ("q", "k", "v", "log_alpha", "b", "w")]
+    prob = g2._problem(x["q"], x["v"], d["scale"])
+    ws = torch.full((g2.gdr2_chunk_workspace_bytes(prob, 1),), 0xFF, dtype=torch.uint8, device="cuda")
+    o_s, S_s = g2.gdr2_chunk_fwd(*args, x["S0"], scale=d["scale"], ws=ws, save=True)
+    g_s = g2.gdr2_chunk_bwd(*args, x["S0"], x["do"], x["dST"], scale=d["scale"], ws=ws, saved=True)
+    o_r, S_r = g2.gdr2_chunk_fwd(*args, x["S0"], scale=d["scale"])
+    g_r = g2.gdr2_chunk_bwd(*args, x["S0"], x["do"], x["dST"], scale=d["scale"])
+    torch.cuda.synchronize()
+    assert torch.equal(o_s, o_r) and torch.equal(S_s, S_r)
+    for n in g_r:
+        assert torch.equal(g_s[n], g_r[n]), n
+    _compare({n: host(t) for n, t in g_s.items()}, _adjoint(d), TOL[dtype])
