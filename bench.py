@@ -69,6 +69,37 @@ def kernel_model(B, T, H, Dk, Dv, stored=True):
     return {k: (fl * NC, by * NC) for k, (fl, by) in m.items()}
 
 
+KERNEL_SOURCES = {"fwd_intra": "gdr2_intra_bf16.hip", "bwd_recompute_intra": "gdr2_intra_bf16.hip",
+                  "fwd_state": "gdr2_scan_bf16.hip", "bwd_recompute_state": "gdr2_scan_bf16.hip",
+                  "bwd_state": "gdr2_bscan_bf16.hip", "bwd_intra": "gdr2_bchunk_bf16.hip"}
+SHARED_HEADERS = ("gdr2_bf16.hpp", "gdr2_kernels.hpp", "gdr2_device.hpp")
+
+
+def measured_traffic(kernel_id, table="hbm_traffic_B8H16T4096.txt"):
+    """HBM bytes per launch of `kernel_id` from the committed rocprofv3 FETCH_SIZE /
+    WRITE_SIZE summary, or None when there is none or the kernel's source (with the
+    shared headers) has changed since the counters were taken."""
+    import hashlib
+    here = os.path.dirname(os.path.abspath(__file__))
+    path = os.path.join(here, "profiles", table)
+    src = KERNEL_SOURCES.get(kernel_id)
+    if src is None or not os.path.exists(path):
+        return None
+    h = hashlib.sha256()
+    for f in (src,) + SHARED_HEADERS:
+        with open(os.path.join(here, "paper_2605_22791_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    digest = h.hexdigest()[:12]
+    with open(path) as fh:
+        for line in fh:
+            parts = line.split()
+            if not parts or parts[0].startswith("#") or parts[0] != kernel_id:
+                continue
+            fetch, write, sha = int(parts[-3]), int(parts[-2]), parts[-1]
+            return fetch + write if sha == digest else None
+    return None
+
+
 def _cpu_worker(args):
     """Oracle forward + adjoint on one head (runs in a spawned process)."""
     import numpy as np
@@ -246,7 +277,9 @@ def main():
     else:
         roof = {"bound": "hbm", "achieved": kd["GBs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": kd["GBs"] / HBM_PEAK_GBS}
-    roof.update({"kernel": dom, "avg_us": kd["avg_us"], "traffic": None,
+    traffic = measured_traffic(dom)
+    roof.update({"traffic": traffic, "kernel": dom, "avg_us": kd["avg_us"],
+                 "alg_bytes": kd["alg_bytes"], "traffic_over_alg": None if traffic is None else traffic / kd["alg_bytes"],
                  "mfma_dtype": MFMA_DTYPE, "arith_intensity": ai, "ridge": ridge})
 
     # the other training path, same number of steps, no per-kernel events
