@@ -4,9 +4,12 @@ This module only draws random numbers and shapes them the way the paper's layer
 produces them; it computes nothing of the recurrence.  The tests, the bench and
 the CPU oracle all consume what it returns, so both sides see identical values.
 
-Recipe (one numpy PCG64 generator per call, ``default_rng(seed)``):
+Recipe (numpy PCG64 streams from ``SeedSequence(seed)``):
   * draws are float32 normals, in the fixed order q, k, v, log_alpha, the
-    gates (b then w, or one tied beta), S0, do;
+    gates (b then w, or one tied beta), S0, do, dS_T; draw i uses child i of
+    the seed's SeedSequence, and a draw of n values is cut into fixed pieces of
+    2^21 values (whole rows), piece j drawn from child j of the draw's
+    sequence, so the values do not depend on how many threads fill them;
   * q and k are L2-normalised per (batch, token, head) in float32, as the layer
     does before the recurrence (App. D.2);
   * log_alpha = -softplus(N(0,1) + shift) in float32: the paper's
@@ -18,17 +21,51 @@ Recipe (one numpy PCG64 generator per call, ``default_rng(seed)``):
     log_alpha and the states stay float32.
 """
 
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 
 __all__ = ["bf16_round", "make_inputs", "config", "CONFIGS", "decode_inputs"]
 
 
 def bf16_round(x):
-    """Round float32 values to the nearest bfloat16 (ties to even); float32 out."""
+    """Round float32 values to the nearest bfloat16 (ties to even); float32 out.
+    (Finite inputs: the 32-bit sum cannot overflow below the NaN range.)"""
     x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32).astype(np.uint64)
-    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
-    return u.astype(np.uint32).view(np.float32)
+    u = x.view(np.uint32)
+    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) & np.uint32(0xFFFF0000)
+    return r.view(np.float32)
+
+
+_PIECE = 1 << 21
+_WORKERS = max(1, min(16, len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else 4))
+
+
+def _draw(ss, shape, post=None):
+    """float32 normals of `shape` from SeedSequence `ss`, in fixed pieces of
+    _PIECE values (whole rows of the last axis), each piece from its own child
+    stream; `post` maps a piece (rows x last axis) to its final values."""
+    n = int(np.prod(shape))
+    last = shape[-1]
+    piece = max(last, (_PIECE // last) * last)
+    nb = -(-n // piece)
+    kids = ss.spawn(nb)
+    out = np.empty(n, dtype=np.float32)
+
+    def work(j):
+        lo, hi = j * piece, min(n, (j + 1) * piece)
+        x = np.random.default_rng(kids[j]).standard_normal(hi - lo, dtype=np.float32)
+        if post is not None:
+            x = post(x.reshape(-1, last)).reshape(-1)
+        out[lo:hi] = x
+
+    if nb == 1:
+        work(0)
+    else:
+        with ThreadPoolExecutor(min(_WORKERS, nb)) as ex:
+            list(ex.map(work, range(nb)))
+    return out.reshape(shape)
 
 
 def _softplus(x):
@@ -40,7 +77,7 @@ def _sigmoid(x):
 
 
 def _l2n(x):
-    n = np.sqrt(np.sum(x * x, axis=-1, keepdims=True, dtype=np.float32))
+    n = np.sqrt(np.einsum("...d,...d->...", x, x, dtype=np.float32))[..., None]
     return (x / n).astype(np.float32)
 
 
@@ -52,38 +89,34 @@ def make_inputs(B, T, H, Dk, Dv, seed, dtype="bf16", decay_shift=0.0,
     decay: "channel" (per key channel) or "scalar" (one value per token-head,
            broadcast over Dk);  gates: "channel" or "tied".
     """
-    rng = np.random.default_rng(seed)
     f32 = np.float32
-    q = _l2n(rng.standard_normal((B, T, H, Dk), dtype=f32))
-    k = _l2n(rng.standard_normal((B, T, H, Dk), dtype=f32))
-    v = rng.standard_normal((B, T, H, Dv), dtype=f32)
+    kids = np.random.SeedSequence(seed).spawn(9)
+    rnd = (lambda x: bf16_round(x)) if dtype == "bf16" else (lambda x: x)
+    shift = f32(decay_shift)
+    q = _draw(kids[0], (B, T, H, Dk), lambda x: rnd(_l2n(x)))
+    k = _draw(kids[1], (B, T, H, Dk), lambda x: rnd(_l2n(x)))
+    v = _draw(kids[2], (B, T, H, Dv), rnd)
     if decay == "channel":
-        la = -_softplus(rng.standard_normal((B, T, H, Dk), dtype=f32) + f32(decay_shift))
+        la = _draw(kids[3], (B, T, H, Dk), lambda x: -_softplus(x + shift))
     elif decay == "scalar":
-        la1 = -_softplus(rng.standard_normal((B, T, H, 1), dtype=f32) + f32(decay_shift))
+        la1 = _draw(kids[3], (B, T, H, 1), lambda x: -_softplus(x + shift))
         la = np.ascontiguousarray(np.broadcast_to(la1, (B, T, H, Dk)))
     else:
         raise ValueError(decay)
     if gates == "channel":
-        b = _sigmoid(rng.standard_normal((B, T, H, Dk), dtype=f32))
-        w = _sigmoid(rng.standard_normal((B, T, H, Dv), dtype=f32))
+        b = _draw(kids[4], (B, T, H, Dk), lambda x: rnd(_sigmoid(x)))
+        w = _draw(kids[5], (B, T, H, Dv), lambda x: rnd(_sigmoid(x)))
         beta = None
     elif gates == "tied":
-        beta = _sigmoid(rng.standard_normal((B, T, H, 1), dtype=f32))
-        if dtype == "bf16":
-            beta = bf16_round(beta)
+        beta = _draw(kids[4], (B, T, H, 1), lambda x: rnd(_sigmoid(x)))
         b = np.ascontiguousarray(np.broadcast_to(beta, (B, T, H, Dk)))
         w = np.ascontiguousarray(np.broadcast_to(beta, (B, T, H, Dv)))
         beta = beta[..., 0]
     else:
         raise ValueError(gates)
-    S0 = (s0_std * rng.standard_normal((B, H, Dk, Dv), dtype=f32)).astype(f32) if s0_std > 0 else None
-    do = rng.standard_normal((B, T, H, Dv), dtype=f32) if with_do else None
-    dST = rng.standard_normal((B, H, Dk, Dv), dtype=f32) if with_dST else None
-    if dtype == "bf16":
-        q, k, v, b, w = (bf16_round(x) for x in (q, k, v, b, w))
-        if do is not None:
-            do = bf16_round(do)
+    S0 = _draw(kids[6], (B, H, Dk, Dv), lambda x: (s0_std * x).astype(f32)) if s0_std > 0 else None
+    do = _draw(kids[7], (B, T, H, Dv), rnd) if with_do else None
+    dST = _draw(kids[8], (B, H, Dk, Dv)) if with_dST else None
     out = dict(q=q, k=k, v=v, log_alpha=la.astype(f32), b=b, w=w, S0=S0, do=do, dST=dST,
                beta=beta, scale=float(1.0 / np.sqrt(Dk)), dtype=dtype,
                B=B, T=T, H=H, Dk=Dk, Dv=Dv)

@@ -228,3 +228,23 @@ def test_saved_training_path_matches_recompute(dtype):
     for n in g_r:
         assert torch.equal(g_s[n], g_r[n]), n
     _compare({n: host(t) for n, t in g_s.items()}, _adjoint(d), TOL[dtype])
+
+
+def test_config3_long_context_backward_sampled_head():
+    """B=1 H=16 T=65536 (1024 chunks per head, slow-forgetting decay, S0 != 0):
+    the reverse scan carries dS across every chunk; adjoint on one head."""
+    d = config(3)
+    d["dST"] = None
+    pairs = [(0, 11)]
+    _case("config3 bwd B1 H16 T65536 d128 bf16; adjoint on 1 head")
+    import paper_2605_22791_amd as g2
+    x = dev_inputs(d)
+    g = g2.gdr2_chunk_bwd(x["q"], x["k"], x["v"], x["log_alpha"], x["b"], x["w"], x["S0"], x["do"], None,
+                          scale=d["scale"])
+    got = {n: host(t) for n, t in g.items()}
+    for n, t in got.items():
+        assert np.all(np.isfinite(t)), n
+    sub = heads(d, pairs)
+    ref = gdr2_recurrent_bwd(sub["q"], sub["k"], sub["v"], sub["log_alpha"], sub["b"], sub["w"], sub["S0"],
+                             sub["do"], None, d["scale"])
+    _compare(got, ref, TOL["bf16"], pairs=pairs)
