@@ -179,6 +179,16 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     const int o = (16 * i + r16) * vst + 32 * p + 4 * g;
     dof[p] = cat8(*reinterpret_cast<const bf4*>(dOp + o), *reinterpret_cast<const bf4*>(dOp + o + 16));
   }
+  // R rows of block 0 (permuted K) for the first dT / dA_qk tile of waves 1..3
+  float4 rblk[2 * KV];
+  if (i > 0) {
+#pragma unroll
+    for (int p = 0; p < KV; ++p) {
+      const float* rp = Rc + r16 * DV + 32 * p + 4 * g;
+      rblk[2 * p] = ldg_f4(rp);
+      rblk[2 * p + 1] = ldg_f4(rp + 16);
+    }
+  }
   float4 pg, ph0, ph1, pd0, pd1;
   bf4 pk, pb, pq;
 #define GDR2_PREFETCH(CB)                                                                  \
@@ -320,22 +330,31 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   __syncthreads();  // dR and A are dead
 
   // ---- dT = -tril(dZ R^T, -1) and dA_qk = tril(scale dO R^T), tiles (i, j <= i),
-  //      stored transposed: plane[s][r]
-#pragma unroll 1
-  for (int j = 0; j <= i; ++j) {
+  //      stored transposed: plane[s][r].  The R rows of block j + 1 are in flight
+  //      while tile j computes (those of block 0 since the kernel start).
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    if (j > i) break;
     const int s = 16 * j + r16;
+    float4 rnext[2 * KV];
+    if (j + 1 < i) {
+#pragma unroll
+      for (int p = 0; p < KV; ++p) {
+        const float* rp = Rc + (s + 16) * DV + 32 * p + 4 * g;
+        rnext[2 * p] = ldg_f4(rp);
+        rnext[2 * p + 1] = ldg_f4(rp + 16);
+      }
+    }
     f4 ta = f4zero(), aa = f4zero();
 #pragma unroll
     for (int p = 0; p < KV; ++p) {
-      Fr rj;
-      if (j == i) {
-        rj = rfr[p];
-      } else {
-        const float* rp = Rc + s * DV + 32 * p + 4 * g;
-        rj = split_f44(ldg_f4(rp), ldg_f4(rp + 16));
-      }
+      const Fr rj = (j == i) ? rfr[p] : split_f44(rblk[2 * p], rblk[2 * p + 1]);
       ta = mma3(zf[p], rj, ta);
       aa = mma2b(dof[p], rj, aa);
+    }
+    if (j + 1 < i) {
+#pragma unroll
+      for (int p = 0; p < 2 * KV; ++p) rblk[p] = rnext[p];
     }
     const int rr = 16 * i + 4 * g;
     f4 tv, av;
