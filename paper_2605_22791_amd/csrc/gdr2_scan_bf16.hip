@@ -9,7 +9,7 @@
 // left in fragment order.  The fp32 state slice lives in registers as MFMA
 // accumulators (plus a bf16 hi/lo copy in LDS for the products that read it);
 // the next chunk's operand blocks are fetched into registers while the
-// current chunk computes and copied to LDS at its end.  The two value slices
+// current chunk computes (from R onwards) and copied to LDS at its end.  The two value slices
 // of one head run on the same XCD so that their shared reads hit one L2.
 // With STORE_H the chunk-start states and R are written for the backward
 // (alone in the backward's recompute, or with the output when the forward keeps them).
@@ -156,10 +156,6 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
 
   for (int n = 0; n < NT; ++n) {
     const size_t ch = chs + n;
-    if (n + 1 < NT) {
-      GDR2_LOAD_OPS(ch + 1)
-      GDR2_LOAD_UG(ch + 1, unext, gnext)
-    }
 
     // ---- R = U - Y S
     f4 racc[NVB / 2];
@@ -184,41 +180,57 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
         for (int u = 0; u < 4; ++u) a.Rs[(ch * CH + 16 * iO + 4 * g + u) * DV + v0 + 16 * vb + r16] = racc[t][u];
       }
     }
+    // the next chunk's operands are fetched only now: a fetch issued before R
+    // would be drained by the wait that frees the registers of the previous
+    // chunk's stores (one vmcnt counts loads and stores alike)
+    if (n + 1 < NT) {
+      GDR2_LOAD_OPS(ch + 1)
+      GDR2_LOAD_UG(ch + 1, unext, gnext)
+    }
     __syncthreads();
 
-    // ---- O^T = S^T Q_g^T + R^T A_qk^T  (lane: O[16 iO + r16][16 vb + 4 g + u])
+    // ---- O^T = S^T Q_g^T + R^T A_qk^T  (lane: O[16 iO + r16][16 vb + 4 g + u]);
+    //      each K-step's fragments are read from LDS one step ahead
     if (WITH_O) {
       f4 accO[NVB / 2];
 #pragma unroll
       for (int t = 0; t < NVB / 2; ++t) accO[t] = f4zero();
+      constexpr int NKO = KS + 2;  // K-steps: KS over keys (S^T Q_g^T), then 2 over rows (R^T A_qk^T)
+      Fr fa[2], fb[2][NVB / 2];
+#define GDR2_O_FRAGS(P_, BUF_)                                                                            \
+  {                                                                                                       \
+    if ((P_) < KS) {                                                                                      \
+      fa[BUF_].hi = ld8(reinterpret_cast<const __bf16*>(sQ + (iO * KS + (P_)) * 2048 + 16 * lane));      \
+      fa[BUF_].lo = ld8(reinterpret_cast<const __bf16*>(sQ + (iO * KS + (P_)) * 2048 + 1024 + 16 * lane)); \
+      _Pragma("unroll") for (int t = 0; t < NVB / 2; ++t) {                                               \
+        const int vb = vbO + t;                                                                           \
+        fb[BUF_][t].hi = ld8(sShi + (16 * vb + r16) * LSS + 32 * (P_) + 8 * g);                          \
+        fb[BUF_][t].lo = ld8(sSlo + (16 * vb + r16) * LSS + 32 * (P_) + 8 * g);                          \
+      }                                                                                                   \
+    } else {                                                                                              \
+      const int kb_ = (P_) - KS;                                                                          \
+      fa[BUF_].hi = ld8(reinterpret_cast<const __bf16*>(sA + (iO * 2 + kb_) * 2048 + 16 * lane));        \
+      fa[BUF_].lo = ld8(reinterpret_cast<const __bf16*>(sA + (iO * 2 + kb_) * 2048 + 1024 + 16 * lane)); \
+      _Pragma("unroll") for (int t = 0; t < NVB / 2; ++t) {                                               \
+        const int vb = vbO + t;                                                                           \
+        fb[BUF_][t].hi = ld_perm8(sRhi + (16 * vb + r16) * LR, 32 * kb_, g);                             \
+        fb[BUF_][t].lo = ld_perm8(sRlo + (16 * vb + r16) * LR, 32 * kb_, g);                             \
+      }                                                                                                   \
+    }                                                                                                     \
+  }
+      GDR2_O_FRAGS(0, 0)
 #pragma unroll
-      for (int p = 0; p < KS; ++p) {
-        Fr qf;
-        qf.hi = ld8(reinterpret_cast<const __bf16*>(sQ + (iO * KS + p) * 2048 + 16 * lane));
-        qf.lo = ld8(reinterpret_cast<const __bf16*>(sQ + (iO * KS + p) * 2048 + 1024 + 16 * lane));
+      for (int p = 0; p < NKO; ++p) {
+        // K-steps over rows r < 16 iO of A_qk^T are zero (causal): skip them
+        const bool live = p < KS || (p - KS) <= (iO >> 1);
+        const bool next = p + 1 < NKO && (p + 1 < KS || (p + 1 - KS) <= (iO >> 1));
+        if (next) GDR2_O_FRAGS(p + 1, (p + 1) & 1)
+        if (live) {
 #pragma unroll
-        for (int t = 0; t < NVB / 2; ++t) {
-          const int vb = vbO + t;
-          Fr sf;
-          sf.hi = ld8(sShi + (16 * vb + r16) * LSS + 32 * p + 8 * g);
-          sf.lo = ld8(sSlo + (16 * vb + r16) * LSS + 32 * p + 8 * g);
-          accO[t] = mma3(sf, qf, accO[t]);
+          for (int t = 0; t < NVB / 2; ++t) accO[t] = mma3(fb[p & 1][t], fa[p & 1], accO[t]);
         }
       }
-#pragma unroll
-      for (int kb = 0; kb <= (iO >> 1); ++kb) {
-        Fr af;
-        af.hi = ld8(reinterpret_cast<const __bf16*>(sA + (iO * 2 + kb) * 2048 + 16 * lane));
-        af.lo = ld8(reinterpret_cast<const __bf16*>(sA + (iO * 2 + kb) * 2048 + 1024 + 16 * lane));
-#pragma unroll
-        for (int t = 0; t < NVB / 2; ++t) {
-          const int vb = vbO + t;
-          Fr rf;
-          rf.hi = ld_perm8(sRhi + (16 * vb + r16) * LR, 32 * kb, g);
-          rf.lo = ld_perm8(sRlo + (16 * vb + r16) * LR, 32 * kb, g);
-          accO[t] = mma3(rf, af, accO[t]);
-        }
-      }
+#undef GDR2_O_FRAGS
       const float sc = a.scale;
 #pragma unroll
       for (int t = 0; t < NVB / 2; ++t) {
@@ -230,29 +242,37 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
 
     // ---- S <- Diag(gamma_C) S + Ktail^T R
     if (STORE_H) {
+      // from a copy: the state registers change right below
+      f4 hcopy[TPW];
+#pragma unroll
+      for (int t = 0; t < TPW; ++t) hcopy[t] = sreg[t];
 #pragma unroll
       for (int t = 0; t < TPW; ++t)
 #pragma unroll
         for (int u = 0; u < 4; ++u)
-          a.Hs[(ch * DK + 16 * cs + 4 * g + u) * DV + v0 + 16 * (sv0 + t) + r16] = sreg[t][u];
+          a.Hs[(ch * DK + 16 * cs + 4 * g + u) * DV + v0 + 16 * (sv0 + t) + r16] = hcopy[t][u];
     }
+    {
+      Fr kf[2], rfs[2][TPW];
 #pragma unroll
-    for (int t = 0; t < TPW; ++t)
+      for (int kb = 0; kb < 2; ++kb) {
+        kf[kb].hi = ld8(reinterpret_cast<const __bf16*>(sK + (cs * 2 + kb) * 2048 + 16 * lane));
+        kf[kb].lo = ld8(reinterpret_cast<const __bf16*>(sK + (cs * 2 + kb) * 2048 + 1024 + 16 * lane));
 #pragma unroll
-      for (int u = 0; u < 4; ++u) sreg[t][u] *= gcur[u];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      Fr kf;
-      kf.hi = ld8(reinterpret_cast<const __bf16*>(sK + (cs * 2 + kb) * 2048 + 16 * lane));
-      kf.lo = ld8(reinterpret_cast<const __bf16*>(sK + (cs * 2 + kb) * 2048 + 1024 + 16 * lane));
-#pragma unroll
-      for (int t = 0; t < TPW; ++t) {
-        const int vb = sv0 + t;
-        Fr rf;
-        rf.hi = ld8(sRhi + (16 * vb + r16) * LR + 32 * kb + 8 * g);
-        rf.lo = ld8(sRlo + (16 * vb + r16) * LR + 32 * kb + 8 * g);
-        sreg[t] = mma3(kf, rf, sreg[t]);
+        for (int t = 0; t < TPW; ++t) {
+          const int vb = sv0 + t;
+          rfs[kb][t].hi = ld8(sRhi + (16 * vb + r16) * LR + 32 * kb + 8 * g);
+          rfs[kb][t].lo = ld8(sRlo + (16 * vb + r16) * LR + 32 * kb + 8 * g);
+        }
       }
+#pragma unroll
+      for (int t = 0; t < TPW; ++t)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) sreg[t][u] *= gcur[u];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int t = 0; t < TPW; ++t) sreg[t] = mma3(kf[kb], rfs[kb][t], sreg[t]);
     }
     __syncthreads();
 
