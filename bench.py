@@ -101,13 +101,15 @@ def measured_traffic(kernel_id, table="hbm_traffic_B8H16T4096.txt"):
 
 
 def _cpu_worker(args):
-    """Oracle forward + adjoint on one head (runs in a spawned process)."""
-    import numpy as np
+    """Oracle forward + adjoint on one head (runs in a spawned process); returns
+    the two durations in seconds."""
     from oracle import gdr2_recurrent_fwd, gdr2_recurrent_bwd
     q, k, v, la, b, w, do, scale = args
+    t0 = time.perf_counter()
     gdr2_recurrent_fwd(q, k, v, la, b, w, None, scale)
+    t1 = time.perf_counter()
     gdr2_recurrent_bwd(q, k, v, la, b, w, None, do, None, scale)
-    return True
+    return t1 - t0, time.perf_counter() - t1
 
 
 def cpu_baseline(d, heads_sample):
@@ -128,7 +130,7 @@ def cpu_baseline(d, heads_sample):
     with ctx.Pool(workers) as pool:
         pool.map(_cpu_worker, jobs[:1])           # warm the workers' imports
         t0 = time.perf_counter()
-        pool.map(_cpu_worker, jobs, chunksize=1)
+        parts = pool.map(_cpu_worker, jobs, chunksize=1)
         wall = time.perf_counter() - t0
     for k, v in env_keep.items():
         if v is None:
@@ -137,33 +139,37 @@ def cpu_baseline(d, heads_sample):
             os.environ[k] = v
     H = d["H"]
     tokens = d["T"] * heads_sample / H           # token = one (b, t) position across all H heads
+    fwd_share = sum(p[0] for p in parts) / max(1e-12, sum(p[0] + p[1] for p in parts))
     return {"value": tokens / wall, "unit": "tokens/s", "cores": workers, "kind": "oracle",
             "sample": f"fp64 numpy token recurrence + adjoint, batch row 0, {heads_sample} of {H} heads, "
                       f"T={d['T']} (= {tokens:.0f} tokens of the workload), {workers} single-threaded workers",
-            "wall_s": wall}
+            "wall_s": wall, "fwd_value": tokens / (wall * fwd_share)}
 
 
-def decode_bench(steps, B=256, H=16, D=128):
-    """Decode: one-token recurrent calls on a 256 MiB fp32 state (synthetic inputs drawn on the GPU)."""
+def decode_bench(steps, B=256, H=16, D=128, distinct=64):
+    """Decode: `steps` one-token recurrent calls on a 256 MiB fp32 state; the
+    synthetic token inputs (drawn on the GPU) cycle through `distinct` sets."""
     import torch
     import paper_2605_22791_amd as g2
     gen = torch.Generator(device="cuda").manual_seed(4)
+    m = min(steps, distinct)
     n = lambda *s: torch.randn(*s, device="cuda", generator=gen)
-    q = torch.nn.functional.normalize(n(steps, B, 1, H, D), dim=-1).bfloat16()
-    k = torch.nn.functional.normalize(n(steps, B, 1, H, D), dim=-1).bfloat16()
-    v = n(steps, B, 1, H, D).bfloat16()
-    la = -torch.nn.functional.softplus(n(steps, B, 1, H, D) - 2.0)
-    b = torch.sigmoid(n(steps, B, 1, H, D)).bfloat16()
-    w = torch.sigmoid(n(steps, B, 1, H, D)).bfloat16()
+    q = torch.nn.functional.normalize(n(m, B, 1, H, D), dim=-1).bfloat16()
+    k = torch.nn.functional.normalize(n(m, B, 1, H, D), dim=-1).bfloat16()
+    v = n(m, B, 1, H, D).bfloat16()
+    la = -torch.nn.functional.softplus(n(m, B, 1, H, D) - 2.0)
+    b = torch.sigmoid(n(m, B, 1, H, D)).bfloat16()
+    w = torch.sigmoid(n(m, B, 1, H, D)).bfloat16()
     S = torch.zeros(B, H, D, D, device="cuda")
     o = torch.empty(B, 1, H, D, device="cuda", dtype=torch.bfloat16)
-    for t in range(min(8, steps)):
+    for t in range(min(8, m)):
         g2.gdr2_recurrent_step(q[t], k[t], v[t], la[t], b[t], w[t], S, o=o)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for t in range(steps):
-        g2.gdr2_recurrent_step(q[t], k[t], v[t], la[t], b[t], w[t], S, o=o)
+        j = t % m
+        g2.gdr2_recurrent_step(q[j], k[j], v[j], la[j], b[j], w[j], S, o=o)
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
@@ -173,6 +179,69 @@ def decode_bench(steps, B=256, H=16, D=128):
             "config": {"B": B, "H": H, "d": D, "steps": steps}}
 
 
+def copy_bandwidth(mib=2048, reps=5):
+    """Measured device copy bandwidth (read + write bytes / time) of a plain
+    torch copy, reported beside the 8 TB/s spec peak."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del src, dst
+    return 2 * n * 4 / (ms * 1e-3) / 1e9
+
+
+def config3_bench(steps=3, stored=True):
+    """Long-context workload (B=1, H=16, T=65536, d=128, S0 != 0): fwd+bwd step
+    time, per-kernel times and the state scans' HBM fraction."""
+    import torch
+    import paper_2605_22791_amd as g2
+    from paper_2605_22791_amd.inputs import config
+    d = config(3)
+    B, T, H, Dk, Dv = d["B"], d["T"], d["H"], d["Dk"], d["Dv"]
+    tb = lambda x: torch.from_numpy(x).cuda().to(torch.bfloat16).contiguous()
+    q, k, v, b, w, do = (tb(d[n]) for n in ("q", "k", "v", "b", "w", "do"))
+    la = torch.from_numpy(d["log_alpha"]).cuda().contiguous()
+    S0 = torch.from_numpy(d["S0"]).cuda().contiguous()
+    del d
+    prob = g2.Gdr2Problem(B, T, H, Dk, Dv, 64, Dk ** -0.5, g2.GDR2_BF16)
+    ws = torch.empty(g2.gdr2_chunk_workspace_bytes(prob, 1), dtype=torch.uint8, device="cuda")
+
+    def step():
+        g2.gdr2_chunk_fwd(q, k, v, la, b, w, S0, ws=ws, save=stored)
+        g2.gdr2_chunk_bwd(q, k, v, la, b, w, S0, do, None, ws=ws, saved=stored)
+
+    step()
+    torch.cuda.synchronize()
+    g2.gdr2_profile_enable(True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    per_kernel = g2.gdr2_profile_collect()
+    g2.gdr2_profile_enable(False)
+    ms = e0.elapsed_time(e1) / steps
+    model = kernel_model(B, T, H, Dk, Dv, stored)
+    kern = {}
+    for name, (kms, cnt) in per_kernel.items():
+        if cnt:
+            avg = kms / cnt
+            kern[name] = {"avg_us": round(avg * 1e3, 1),
+                          "hbm_frac": round(model[name][1] / (avg * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    return {"workload": "B1 H16 T65536 d128 bf16, S0 != 0", "training_path": "stored" if stored else "recompute",
+            "ms_per_step": ms, "tokens_per_s": B * T / (ms * 1e-3), "kernels": kern}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -180,6 +249,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the copy-bandwidth, long-context (config 3) and decode side measurements")
     ap.add_argument("--cpu-heads", type=int, default=16)
     ap.add_argument("--path", choices=("stored", "recompute"), default="stored",
                     help="training path of the timed step: the forward keeps A, h and R for the backward "
@@ -317,9 +388,15 @@ def main():
         "other_path": {"training_path": "recompute" if stored else "stored", "ms_per_step": other_ms,
                        "tokens_per_s": B * T / (other_ms * 1e-3)},
     }
-    if not args.no_decode:
-        print("[bench] decode", file=sys.stderr, flush=True)
-        out["decode"] = decode_bench(64)
+    if not args.no_extra:
+        print("[bench] copy bandwidth", file=sys.stderr, flush=True)
+        out["copy_GBs"] = copy_bandwidth()
+    if not args.no_decode and not args.no_extra:
+        print("[bench] decode (1024 one-token calls, B=256)", file=sys.stderr, flush=True)
+        out["decode"] = decode_bench(1024)
+    if not args.no_extra:
+        print("[bench] long context (config 3)", file=sys.stderr, flush=True)
+        out["long_context"] = config3_bench(stored=stored)
     if not args.no_cpu:
         print("[bench] cpu oracle baseline", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(d, args.cpu_heads)
