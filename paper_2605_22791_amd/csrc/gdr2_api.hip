@@ -46,8 +46,36 @@ struct Layout {
   size_t Hs, Rs, DH, DR, DAqk, DT, DEg;  // backward extras
   size_t bY, bQ, bA, bK, bU, bG;         // bf16 forward (fragment order)
   size_t bDR, bAm;                       // bf16 backward extras (fragment order)
+  size_t sM, sN, sX;                     // segment maps and entry states (sequence-parallel scans)
+  int nseg, seg_len;
   size_t total;
 };
+
+// Sequence-parallel scans (bf16 path).  The state scans run one workgroup per
+// (sequence, 64-wide value slice); when there are too few of those to occupy
+// the chip and the sequences are long, every sequence is cut into segments
+// that are scanned side by side (segment maps, then a short chain over the
+// segments, then the segments again from their true start states).  Segments
+// are doubled while the scan grid stays within one workgroup per compute unit
+// and a segment keeps at least 8 chunks.  GDR2_SCAN_SEGMENTS=<n> overrides the
+// count (1 turns the mode off).
+void scan_segments(const gdr2_problem* p, int& nseg, int& seg_len) {
+  const int NT = p->T / CH;
+  const long long slices = (long long)p->B * p->H * (p->Dv / 64);
+  static const int forced = [] {
+    const char* e = std::getenv("GDR2_SCAN_SEGMENTS");
+    return e != nullptr ? std::atoi(e) : 0;
+  }();
+  int n = 1;
+  if (forced > 0) {
+    n = forced < NT ? forced : NT;
+  } else if (p->dtype == GDR2_BF16 && slices < 128 && NT >= 16) {
+    while (slices * n * 2 <= 256 && n * 2 * 8 <= NT) n *= 2;
+  }
+  if (p->dtype != GDR2_BF16 || n < 1) n = 1;
+  seg_len = (NT + n - 1) / n;
+  nseg = (NT + seg_len - 1) / seg_len;
+}
 
 Layout layout(const gdr2_problem* p, bool bwd) {
   const size_t NC = (size_t)p->B * p->H * (size_t)(p->T / CH);
@@ -95,6 +123,13 @@ Layout layout(const gdr2_problem* p, bool bwd) {
       L.DT = take(NC * CH * CH);
       L.DEg = take(NC * CH * Dk);
     }
+  }
+  scan_segments(p, L.nseg, L.seg_len);
+  if (L.nseg > 1) {
+    const size_t nvs = (size_t)p->B * p->H * L.nseg;
+    L.sM = take(nvs * Dk * Dk);
+    L.sN = take(nvs * Dk * Dv);
+    L.sX = take(nvs * Dk * Dv);
   }
   L.total = off;
   return L;
@@ -166,6 +201,72 @@ hipError_t timed(int id, hipStream_t st, F&& launch) {
   return hipSuccess;
 }
 
+// ---- state scans of the bf16 path, sequential or sequence-parallel ---------
+// Forward: segment maps N (zero start) and M (identity start, no input), the
+// chain X_k entering every segment, then `last` scans every segment from X_k
+// (it writes the output and, if asked, the chunk states, R and S_T).
+template <int DK, int DV, class Last>
+hipError_t scan_fwd_bf16(const ScanArgs& sa, const Layout& L, void* ws, Last&& last, hipStream_t st) {
+  if (L.nseg == 1) return last(sa);
+  ScanArgs pn = sa;
+  pn.S0 = nullptr;
+  pn.ST = nullptr;
+  pn.o = nullptr;
+  pn.Hs = pn.Rs = nullptr;
+  pn.nseg = L.nseg;
+  pn.seg_len = L.seg_len;
+  pn.STseg = at<float>(ws, L.sN);
+  hipError_t e = launch_scan_bf16<DK, DV, false, false>(pn, st);
+  if (e != hipSuccess) return e;
+  ScanArgs pm = pn;
+  pm.U = nullptr;
+  pm.flags = kScanNoInput | kScanEye;
+  pm.STseg = at<float>(ws, L.sM);
+  e = launch_scan_bf16<DK, DK, false, false>(pm, st);
+  if (e != hipSuccess) return e;
+  const SegCombineArgs ca{at<float>(ws, L.sM), at<float>(ws, L.sN), sa.S0, at<float>(ws, L.sX),
+                          sa.B * sa.H, L.nseg, 0};
+  e = launch_segcombine<DK, DV>(ca, st);
+  if (e != hipSuccess) return e;
+  ScanArgs p3 = sa;
+  p3.nseg = L.nseg;
+  p3.seg_len = L.seg_len;
+  p3.S0seg = at<float>(ws, L.sX);
+  return last(p3);
+}
+
+// Reverse: the same three steps from the segment ends, then every segment
+// again from the gradient at its end (writing dH, dR and dS0).
+template <int DK, int DV>
+hipError_t scan_bwd_bf16(const BScanArgs& ba, const Layout& L, void* ws, hipStream_t st) {
+  if (L.nseg == 1) return launch_bscan_bf16<DK, DV>(ba, st);
+  BScanArgs pn = ba;
+  pn.dST = nullptr;
+  pn.dS0 = nullptr;
+  pn.DH = nullptr;
+  pn.DR = nullptr;
+  pn.nseg = L.nseg;
+  pn.seg_len = L.seg_len;
+  pn.dSseg_out = at<float>(ws, L.sN);
+  hipError_t e = launch_bscan_bf16<DK, DV>(pn, st);
+  if (e != hipSuccess) return e;
+  BScanArgs pm = pn;
+  pm.dout = nullptr;
+  pm.flags = kScanNoInput | kScanEye;
+  pm.dSseg_out = at<float>(ws, L.sM);
+  e = launch_bscan_bf16<DK, DK>(pm, st);
+  if (e != hipSuccess) return e;
+  const SegCombineArgs ca{at<float>(ws, L.sM), at<float>(ws, L.sN), ba.dST, at<float>(ws, L.sX),
+                          ba.B * ba.H, L.nseg, 1};
+  e = launch_segcombine<DK, DV>(ca, st);
+  if (e != hipSuccess) return e;
+  BScanArgs p3 = ba;
+  p3.nseg = L.nseg;
+  p3.seg_len = L.seg_len;
+  p3.dSseg_in = at<float>(ws, L.sX);
+  return launch_bscan_bf16<DK, DV>(p3, st);
+}
+
 // ---- dispatch over (Dk, Dv) ------------------------------------------------
 template <template <int, int, typename> class F, typename TIn, typename... A>
 hipError_t dispatch(int Dk, int Dv, A&&... args) {
@@ -197,7 +298,9 @@ struct FwdRun {
                   save ? at<float>(ws, L.Hs) : nullptr, save ? at<float>(ws, L.Rs) : nullptr,
                   p->B, p->T, p->H, NT, p->scale};
       return timed(GDR2_K_FWD_STATE, st, [&] {
-        return save ? launch_scan_bf16<DK, DV, true, true>(sa, st) : launch_scan_bf16<DK, DV, true, false>(sa, st);
+        return scan_fwd_bf16<DK, DV>(sa, L, ws, [&](const ScanArgs& x) {
+          return save ? launch_scan_bf16<DK, DV, true, true>(x, st) : launch_scan_bf16<DK, DV, true, false>(x, st);
+        }, st);
       });
     }
     IntraArgs<TIn> ia{static_cast<const TIn*>(q), static_cast<const TIn*>(k),
@@ -240,12 +343,16 @@ struct BwdRun {
         if (e != hipSuccess) return e;
         ScanArgs sa{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.U, ia.GC, S0, nullptr, nullptr, at<float>(ws, L.Hs),
                     at<float>(ws, L.Rs), p->B, p->T, p->H, NT, p->scale};
-        e = timed(GDR2_K_BWD_RECOMPUTE_STATE, st, [&] { return launch_scan_bf16<DK, DV, false, true>(sa, st); });
+        e = timed(GDR2_K_BWD_RECOMPUTE_STATE, st, [&] {
+          return scan_fwd_bf16<DK, DV>(sa, L, ws, [&](const ScanArgs& x) {
+            return launch_scan_bf16<DK, DV, false, true>(x, st);
+          }, st);
+        });
         if (e != hipSuccess) return e;
       }
       BScanArgs ba{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.GC, static_cast<const bf16_t*>(dout), dST, dS0,
                    at<float>(ws, L.DH), at<unsigned char>(ws, L.bDR), p->B, p->T, p->H, NT, p->scale};
-      e = timed(GDR2_K_BWD_STATE, st, [&] { return launch_bscan_bf16<DK, DV>(ba, st); });
+      e = timed(GDR2_K_BWD_STATE, st, [&] { return scan_bwd_bf16<DK, DV>(ba, L, ws, st); });
       if (e != hipSuccess) return e;
       // the WY VJP and the intra-chunk VJP in one chunk-parallel kernel
       BChunkBf16Args ca{static_cast<const bf16_t*>(q), static_cast<const bf16_t*>(k),

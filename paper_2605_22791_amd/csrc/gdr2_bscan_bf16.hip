@@ -6,7 +6,9 @@
 //   dS <- Diag(gamma_C) dS + scale * Q_g^T dO - Y^T dR
 //
 // writing dS before each update (the gradient of that chunk's end state), dR
-// (split hi/lo, in the fragment order the chunk backward reads), and finally dS0.  The operands are the forward's fragment-ordered tiles
+// (split hi/lo, in the fragment order the chunk backward reads), and finally dS0.
+// With nseg > 1 each workgroup runs one segment of a sequence, from the
+// gradient at the segment's end to the one at its start (BScanArgs).  The operands are the forward's fragment-ordered tiles
 // (gdr2_kernels.hpp): the transposed fragments these products need come out
 // of the same LDS blocks through ds_read_b64_tr_b16 with per-lane addresses,
 // since every 4 consecutive elements of a block row are contiguous.
@@ -70,16 +72,21 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
   const int qq = r16 & 3, ii = r16 >> 2;  // transpose-load role of this lane (4 ii + qq)
   const int T = a.T, H = a.H, NT = a.NT;
 
-  const int nseq = a.B * H;
-  int seq, slice;
-  if (NS > 1 && (nseq & 7) == 0) {
+  // independent scans: (sequence, segment) pairs, vs = seq * nseg + seg
+  const int nseg = a.nseg, nvirt = a.B * H * nseg;
+  int vs, slice;
+  if (NS > 1 && (nvirt & 7) == 0) {
     const int xcd = blockIdx.x & 7, j = blockIdx.x >> 3;
-    seq = (j / NS) * 8 + xcd;
+    vs = (j / NS) * 8 + xcd;
     slice = j % NS;
   } else {
-    seq = blockIdx.x / NS;
+    vs = blockIdx.x / NS;
     slice = blockIdx.x % NS;
   }
+  const int seq = vs / nseg, seg = vs % nseg;
+  const int seg_len = a.seg_len > 0 ? a.seg_len : NT;
+  const int n0 = seg * seg_len, n1 = min(NT, n0 + seg_len);
+  const bool no_input = (a.flags & kScanNoInput) != 0;
   const int bb = seq / H, h = seq % H;
   const int v0 = slice * DVS;
   const __bf16* dO = reinterpret_cast<const __bf16*>(a.dout);
@@ -109,7 +116,9 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
       stg[m] = ldg16(src + 16 * tid);                                                                  \
     }                                                                                                  \
     const int r_ = tid / (DVS / 8), c8_ = (tid % (DVS / 8)) * 8;                                       \
-    sto = ldg16(dO + ((size_t)bb * T + (size_t)(N_) * CH + r_) * ((size_t)H * DV) + (size_t)h * DV + v0 + c8_); \
+    sto = no_input ? u4v{0u, 0u, 0u, 0u}                                                              \
+                   : ldg16(dO + ((size_t)bb * T + (size_t)(N_) * CH + r_) * ((size_t)H * DV) + (size_t)h * DV + \
+                           v0 + c8_);                                                                  \
     _Pragma("unroll") for (int u2 = 0; u2 < 4; ++u2) gnext[u2] =                                       \
         a.GC[chx * (WsBf16::gc(DK) / 4) + 16 * cs + 4 * g + u2];                                       \
   }
@@ -129,24 +138,35 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int c = 16 * cs + 4 * g + u, v = 16 * vb + r16;
-      sreg[t][u] = a.dST ? a.dST[((size_t)seq * DK + c) * DV + v0 + v] : 0.f;
+      float x0 = 0.f;
+      if (a.flags & kScanEye)
+        x0 = (c == v0 + v) ? 1.f : 0.f;  // identity columns (DV == DK)
+      else if (a.dSseg_in)
+        x0 = a.dSseg_in[((size_t)vs * DK + c) * DV + v0 + v];
+      else if (a.dST && seg == nseg - 1)
+        x0 = a.dST[((size_t)seq * DK + c) * DV + v0 + v];
+      sreg[t][u] = x0;
     }
     st4split(sDhi + (16 * vb + r16) * LSD + 16 * cs + 4 * g, sDlo + (16 * vb + r16) * LSD + 16 * cs + 4 * g,
              sreg[t]);
   }
-  GDR2_LOAD_CHUNK(NT - 1)
-  GDR2_STORE_CHUNK()
+  if (n0 < n1) {
+    GDR2_LOAD_CHUNK(n1 - 1)
+    GDR2_STORE_CHUNK()
+  }
   __syncthreads();
 
-  for (int n = NT - 1; n >= 0; --n) {
+  for (int n = n1 - 1; n >= n0; --n) {
     const size_t ch = chs + n;
-    if (n > 0) GDR2_LOAD_CHUNK(n - 1)
+    if (n > n0) GDR2_LOAD_CHUNK(n - 1)
     // gradient of this chunk's end state
+    if (a.DH) {
 #pragma unroll
-    for (int t = 0; t < TPW; ++t)
+      for (int t = 0; t < TPW; ++t)
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-        a.DH[(ch * DK + 16 * cs + 4 * g + u) * DV + v0 + 16 * (sv0 + t) + r16] = sreg[t][u];
+        for (int u = 0; u < 4; ++u)
+          a.DH[(ch * DK + 16 * cs + 4 * g + u) * DV + v0 + 16 * (sv0 + t) + r16] = sreg[t][u];
+    }
 
     // ---- dR = scale * A_qk^T dO + Ktail dS   (tiles: row block iO, value blocks vbO..)
     f4 racc[NVB / 2], aacc[NVB / 2];
@@ -203,9 +223,11 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
       st4split(sRhi + (16 * vb + r16) * LDR + 16 * iO + 4 * g, sRlo + (16 * vb + r16) * LDR + 16 * iO + 4 * g, r);
       // dR as permuted fragment blocks (row = value, K = chunk row): this lane's
       // four rows 16 iO + 4 g + u are half of its 16-byte slot
-      const size_t doff = ch * WsBf16::dr(DV) + (size_t)((v0 / 16 + vb) * 2 + (iO >> 1)) * 2048 + 16 * lane +
-                          8 * (iO & 1);
-      st4split(reinterpret_cast<__bf16*>(a.DR + doff), reinterpret_cast<__bf16*>(a.DR + doff + 1024), r);
+      if (a.DR) {
+        const size_t doff = ch * WsBf16::dr(DV) + (size_t)((v0 / 16 + vb) * 2 + (iO >> 1)) * 2048 + 16 * lane +
+                            8 * (iO & 1);
+        st4split(reinterpret_cast<__bf16*>(a.DR + doff), reinterpret_cast<__bf16*>(a.DR + doff + 1024), r);
+      }
     }
     __syncthreads();
 
@@ -261,18 +283,20 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
       st4split(sDhi + (16 * vb + r16) * LSD + 16 * cs + 4 * g, sDlo + (16 * vb + r16) * LSD + 16 * cs + 4 * g,
                sreg[t]);
     }
-    if (n > 0) GDR2_STORE_CHUNK()
+    if (n > n0) GDR2_STORE_CHUNK()
     __syncthreads();
   }
 #undef GDR2_LOAD_CHUNK
 #undef GDR2_STORE_CHUNK
 
-  if (a.dS0) {
+  float* dstart = a.dSseg_out ? a.dSseg_out + (size_t)vs * DK * DV
+                              : ((a.dS0 && seg == 0) ? a.dS0 + (size_t)seq * DK * DV : nullptr);
+  if (dstart) {
 #pragma unroll
     for (int t = 0; t < TPW; ++t)
 #pragma unroll
       for (int u = 0; u < 4; ++u)
-        a.dS0[((size_t)seq * DK + 16 * cs + 4 * g + u) * DV + v0 + 16 * (sv0 + t) + r16] = sreg[t][u];
+        dstart[(size_t)(16 * cs + 4 * g + u) * DV + v0 + 16 * (sv0 + t) + r16] = sreg[t][u];
   }
 }
 
@@ -282,7 +306,7 @@ hipError_t launch_bscan_bf16(const BScanArgs& a, hipStream_t st) {
   const void* fn = reinterpret_cast<const void*>(&bscan_bf16_kernel<DK, DV>);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
   if (e != hipSuccess) return e;
-  dim3 grid(a.B * a.H * C::NS);
+  dim3 grid(a.B * a.H * a.nseg * C::NS);
   hipLaunchKernelGGL((bscan_bf16_kernel<DK, DV>), grid, dim3(C::NTHR), C::LDS, st, a);
   return hipGetLastError();
 }

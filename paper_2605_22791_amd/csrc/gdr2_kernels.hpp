@@ -151,6 +151,13 @@ struct IntraBf16Args {
   int B, T, H, NT;
 };
 
+// Sequence-parallel scans: with nseg > 1 every sequence is cut into nseg
+// segments of seg_len chunks and each workgroup scans one segment of one
+// sequence alone, from a given start state.  A pass with kScanNoInput (U = 0,
+// resp. dO = 0) and kScanEye (identity start columns) yields a segment's
+// transition matrix; the segment-combine kernel then chains the segments.
+enum ScanFlags : int { kScanNoInput = 1, kScanEye = 2 };
+
 struct ScanArgs {
   const unsigned char* Y;
   const unsigned char* Qg;
@@ -165,6 +172,10 @@ struct ScanArgs {
   float* Rs;        // R per chunk (backward recompute)
   int B, T, H, NT;
   float scale;
+  int nseg = 1, seg_len = 0;     // segments per sequence and their length in chunks (0: NT)
+  const float* S0seg = nullptr;  // nullable: start state of every segment (B*H*nseg, Dk, DV)
+  float* STseg = nullptr;        // nullable: end state of every segment (B*H*nseg, Dk, DV)
+  int flags = 0;                 // ScanFlags
 };
 
 struct BScanArgs {
@@ -176,10 +187,27 @@ struct BScanArgs {
   const bf16_t* dout;
   const float* dST;  // nullable
   float* dS0;        // nullable
-  float* DH;         // gradient of each chunk's end state (B,H,NT,Dk,Dv)
-  unsigned char* DR; // dR per chunk, WsBf16 fragment blocks
+  float* DH;         // nullable: gradient of each chunk's end state (B,H,NT,Dk,Dv)
+  unsigned char* DR; // nullable: dR per chunk, WsBf16 fragment blocks
   int B, T, H, NT;
   float scale;
+  int nseg = 1, seg_len = 0;       // as in ScanArgs; the scan runs from a segment's end to its start
+  const float* dSseg_in = nullptr; // nullable: gradient at the end of every segment (B*H*nseg, Dk, DV)
+  float* dSseg_out = nullptr;      // nullable: gradient at the start of every segment
+  int flags = 0;                   // ScanFlags (kScanNoInput: dO = 0)
+};
+
+// Chaining of segment maps: X <- M_k X + N_k over the segments of each sequence
+// (forward: k = 0, 1, ..., Xs[0] = X0; reverse: k = nseg-1, ..., Xs[nseg-1] = X0).
+// Xs[k] receives the value entering segment k.  M: (nseq*nseg, Dk, Dk),
+// N, Xs: (nseq*nseg, Dk, DV), X0: (nseq, Dk, DV) or null (zero); fp32.
+struct SegCombineArgs {
+  const float* M;
+  const float* N;
+  const float* X0;
+  float* Xs;
+  int nseq, nseg;
+  int reverse;
 };
 
 // Chunk-parallel backward of the bf16 path (App. B.2 - B.5).
@@ -214,6 +242,8 @@ template <int DK, int DV, bool WITH_O, bool STORE_H>
 hipError_t launch_scan_bf16(const ScanArgs& a, hipStream_t st);
 template <int DK, int DV>
 hipError_t launch_bchunk_bf16(const BChunkBf16Args& a, hipStream_t st);
+template <int DK, int DV>
+hipError_t launch_segcombine(const SegCombineArgs& a, hipStream_t st);
 
 template <int DK, int DV, typename TIn>
 hipError_t launch_fwd_intra(const IntraArgs<TIn>& a, int B, hipStream_t st);

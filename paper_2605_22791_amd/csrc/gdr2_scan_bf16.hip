@@ -13,6 +13,8 @@
 // of one head run on the same XCD so that their shared reads hit one L2.
 // With STORE_H the chunk-start states and R are written for the backward
 // (alone in the backward's recompute, or with the output when the forward keeps them).
+// With nseg > 1 each workgroup scans one segment of a sequence from a given
+// start state (ScanArgs), which the sequence-parallel mode builds on.
 //
 // Precision: Y S uses the bf16 part of S (Y itself is bf16); every other
 // product is split hi/lo and fp32-accurate.
@@ -77,16 +79,21 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
   const int g = lane >> 4, r16 = lane & 15;
   const int T = a.T, H = a.H, NT = a.NT;
 
-  const int nseq = a.B * H;
-  int seq, slice;
-  if (NS > 1 && (nseq & 7) == 0) {
+  // independent scans: (sequence, segment) pairs, vs = seq * nseg + seg
+  const int nseg = a.nseg, nvirt = a.B * H * nseg;
+  int vs, slice;
+  if (NS > 1 && (nvirt & 7) == 0) {
     const int xcd = blockIdx.x & 7, j = blockIdx.x >> 3;
-    seq = (j / NS) * 8 + xcd;
+    vs = (j / NS) * 8 + xcd;
     slice = j % NS;
   } else {
-    seq = blockIdx.x / NS;
+    vs = blockIdx.x / NS;
     slice = blockIdx.x % NS;
   }
+  const int seq = vs / nseg, seg = vs % nseg;
+  const int seg_len = a.seg_len > 0 ? a.seg_len : NT;
+  const int n0 = seg * seg_len, n1 = min(NT, n0 + seg_len);
+  const bool no_input = (a.flags & kScanNoInput) != 0;
   const int bb = seq / H, h = seq % H;
   const int v0 = slice * DVS;
   __bf16* O = reinterpret_cast<__bf16*>(a.o);
@@ -130,8 +137,9 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
 #define GDR2_LOAD_UG(CHX, UARR, GARR)                                                                        \
   _Pragma("unroll") for (int t = 0; t < NVB / 2; ++t) {                                                  \
     const int vb_ = v0 / 16 + vbO + t;                                                                   \
-    UARR[t] = *reinterpret_cast<const f4*>(a.U + (CHX) * (WsBf16::u(DV) / 4) +                           \
-                                           ((size_t)(vb_ * 4 + iO) * 64 + lane) * 4);                    \
+    UARR[t] = no_input ? f4zero()                                                                        \
+                       : *reinterpret_cast<const f4*>(a.U + (CHX) * (WsBf16::u(DV) / 4) +                \
+                                                      ((size_t)(vb_ * 4 + iO) * 64 + lane) * 4);         \
   }                                                                                                      \
   _Pragma("unroll") for (int u2 = 0; u2 < 4; ++u2) GARR[u2] =                                            \
       a.GC[(CHX) * (WsBf16::gc(DK) / 4) + 16 * cs + 4 * g + u2];
@@ -144,17 +152,26 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int c = 16 * cs + 4 * g + u, v = 16 * vb + r16;
-      sreg[t][u] = a.S0 ? a.S0[((size_t)seq * DK + c) * DV + v0 + v] : 0.f;
+      float x0 = 0.f;
+      if (a.flags & kScanEye)
+        x0 = (c == v0 + v) ? 1.f : 0.f;  // identity columns (DV == DK)
+      else if (a.S0seg)
+        x0 = a.S0seg[((size_t)vs * DK + c) * DV + v0 + v];
+      else if (a.S0 && seg == 0)
+        x0 = a.S0[((size_t)seq * DK + c) * DV + v0 + v];
+      sreg[t][u] = x0;
     }
     st4split(sShi + (16 * vb + r16) * LSS + 16 * cs + 4 * g, sSlo + (16 * vb + r16) * LSS + 16 * cs + 4 * g,
              sreg[t]);
   }
-  GDR2_LOAD_OPS(chs)
-  GDR2_LOAD_UG(chs, ucur, gcur)
-  GDR2_STORE_OPS()
+  if (n0 < n1) {
+    GDR2_LOAD_OPS(chs + n0)
+    GDR2_LOAD_UG(chs + n0, ucur, gcur)
+    GDR2_STORE_OPS()
+  }
   __syncthreads();
 
-  for (int n = 0; n < NT; ++n) {
+  for (int n = n0; n < n1; ++n) {
     const size_t ch = chs + n;
 
     // ---- R = U - Y S
@@ -183,7 +200,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
     // the next chunk's operands are fetched only now: a fetch issued before R
     // would be drained by the wait that frees the registers of the previous
     // chunk's stores (one vmcnt counts loads and stores alike)
-    if (n + 1 < NT) {
+    if (n + 1 < n1) {
       GDR2_LOAD_OPS(ch + 1)
       GDR2_LOAD_UG(ch + 1, unext, gnext)
     }
@@ -283,7 +300,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
       st4split(sShi + (16 * vb + r16) * LSS + 16 * cs + 4 * g, sSlo + (16 * vb + r16) * LSS + 16 * cs + 4 * g,
                sreg[t]);
     }
-    if (n + 1 < NT) {
+    if (n + 1 < n1) {
       GDR2_STORE_OPS()
 #pragma unroll
       for (int t = 0; t < NVB / 2; ++t) ucur[t] = unext[t];
@@ -296,12 +313,13 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
 #undef GDR2_LOAD_OPS
 #undef GDR2_STORE_OPS
 #undef GDR2_LOAD_UG
-  if (a.ST) {
+  float* send = a.STseg ? a.STseg + (size_t)vs * DK * DV
+                        : ((a.ST && seg == nseg - 1) ? a.ST + (size_t)seq * DK * DV : nullptr);
+  if (send) {
 #pragma unroll
     for (int t = 0; t < TPW; ++t)
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-        a.ST[((size_t)seq * DK + 16 * cs + 4 * g + u) * DV + v0 + 16 * (sv0 + t) + r16] = sreg[t][u];
+      for (int u = 0; u < 4; ++u) send[(size_t)(16 * cs + 4 * g + u) * DV + v0 + 16 * (sv0 + t) + r16] = sreg[t][u];
   }
 }
 
@@ -311,7 +329,7 @@ hipError_t launch_scan_bf16(const ScanArgs& a, hipStream_t st) {
   const void* fn = reinterpret_cast<const void*>(&scan_bf16_kernel<DK, DV, WITH_O, STORE_H>);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
   if (e != hipSuccess) return e;
-  dim3 grid(a.B * a.H * C::NS);
+  dim3 grid(a.B * a.H * a.nseg * C::NS);
   hipLaunchKernelGGL((scan_bf16_kernel<DK, DV, WITH_O, STORE_H>), grid, dim3(C::NTHR), C::LDS, st, a);
   return hipGetLastError();
 }
@@ -320,6 +338,12 @@ hipError_t launch_scan_bf16(const ScanArgs& a, hipStream_t st) {
   template hipError_t launch_scan_bf16<DK, DV, true, false>(const ScanArgs&, hipStream_t); \
   template hipError_t launch_scan_bf16<DK, DV, false, true>(const ScanArgs&, hipStream_t); \
   template hipError_t launch_scan_bf16<DK, DV, true, true>(const ScanArgs&, hipStream_t);
+
+// transition-matrix passes of the sequence-parallel scan (value width = Dk)
+template hipError_t launch_scan_bf16<64, 64, false, false>(const ScanArgs&, hipStream_t);
+template hipError_t launch_scan_bf16<128, 128, false, false>(const ScanArgs&, hipStream_t);
+template hipError_t launch_scan_bf16<64, 128, false, false>(const ScanArgs&, hipStream_t);
+template hipError_t launch_scan_bf16<128, 64, false, false>(const ScanArgs&, hipStream_t);
 
 GDR2_INST_SCAN2(64, 64)
 GDR2_INST_SCAN2(64, 128)

@@ -132,3 +132,29 @@ def decode_u_tiles(raw_f32, Dv):
             for u in range(4):
                 out[16 * i + 4 * (lane // 16) + u, 16 * vb + lane % 16] = t[vb, i, :, u]
     return out
+
+
+# --------------------------------------------------------------------------- sequence-parallel scans
+def scan_segments(B, T, H, Dv, dtype="bf16"):
+    """(nseg, seg_len) the library picks for its state scans (mirrors its rule:
+    bf16 problems with fewer than 128 (sequence, 64-wide value slice) scans and
+    at least 16 chunks double the segments while the grid stays within 256
+    workgroups and a segment keeps 8 chunks or more)."""
+    NT = T // CH
+    slices = B * H * (Dv // 64)
+    n = 1
+    if dtype == "bf16" and slices < 128 and NT >= 16:
+        while slices * n * 2 <= 256 and n * 2 * 8 <= NT:
+            n *= 2
+    seg_len = -(-NT // n)
+    return -(-NT // seg_len), seg_len
+
+
+def seg_buffer_bytes(B, T, H, Dk, Dv, dtype="bf16"):
+    """Workspace bytes of the segment maps M, N and entry states X (0 if unsegmented)."""
+    nseg, _ = scan_segments(B, T, H, Dv, dtype)
+    if nseg == 1:
+        return 0
+    r = lambda n: (n * 4 + 255) // 256 * 256
+    nvs = B * H * nseg
+    return r(nvs * Dk * Dk) + 2 * r(nvs * Dk * Dv)

@@ -216,3 +216,23 @@ def test_saved_training_path_validation():
     assert L.gdr2_chunk_bwd_saved(ctypes.byref(p), *vp(bad), bwd, None) == g2.GDR2_EINVAL
     q = _prob(Dk=96)
     assert L.gdr2_chunk_bwd_saved(ctypes.byref(q), *vp(bargs), 1 << 40, None) == g2.GDR2_EUNSUPPORTED
+
+
+def test_workspace_segment_buffers():
+    """bf16 problems with few scans and long sequences get the segment maps of
+    the sequence-parallel scans appended to the workspace; others do not."""
+    from tests.gpu_common import ws_layout_bf16, seg_buffer_bytes, scan_segments
+    assert scan_segments(1, 65536, 16, 128) == (8, 128)
+    assert scan_segments(8, 4096, 16, 128) == (1, 64)
+    assert scan_segments(1, 640, 2, 128) == (1, 10)
+    assert scan_segments(1, 3200, 2, 64) == (4, 13)
+    for (B, T, H, Dk, Dv) in [(1, 3200, 2, 128, 64), (1, 4096, 4, 64, 128), (2, 1024, 4, 128, 128),
+                              (8, 4096, 16, 128, 128), (1, 640, 2, 64, 64)]:
+        p = _prob(B=B, T=T, H=H, Dk=Dk, Dv=Dv)
+        p.dtype = g2.GDR2_BF16
+        extra = seg_buffer_bytes(B, T, H, Dk, Dv)
+        for bwd in (0, 1):
+            _, base, _ = ws_layout_bf16(B, T, H, Dk, Dv, bwd=bool(bwd))
+            assert g2.gdr2_chunk_workspace_bytes(p, bwd) == base + extra, (B, T, H, Dk, Dv, bwd)
+        p.dtype = g2.GDR2_FP32
+        assert seg_buffer_bytes(B, T, H, Dk, Dv, "fp32") == 0
