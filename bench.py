@@ -259,11 +259,17 @@ def main():
     ap.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
                     help="run one copy-like elementwise kernel (torch.neg) over MIB MiB of fp32 before the "
                          "timed steps: the reference that scales rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes")
+    ap.add_argument("--long-context-only", action="store_true",
+                    help="time only the long-context step (B=1, H=16, T=65536) for --steps steps and print "
+                         "its figures (not the benchmark line)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
               file=sys.stderr)
         sys.exit(2)
+    if args.long_context_only:
+        print(json.dumps(config3_bench(steps=args.steps, stored=args.path == "stored")), flush=True)
+        return
 
     import torch
     import paper_2605_22791_amd as g2
