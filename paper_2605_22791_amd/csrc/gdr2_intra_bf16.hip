@@ -119,6 +119,27 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
     const int e = tid + 256 * m, r = e / (DK / 8), c8 = (e % (DK / 8)) * 8;
     kst[m] = ldg16(K + kofs(r) + c8);
   }
+  // q and b rows of the row blocks whose T / A_qk tiles this wave forms (wave 0:
+  // blocks 0 and 1, wave 1: block 2, waves 2 and 3: block 3), as K-step
+  // fragments (row 16 rb + r16, channels 32 p + 8 g ..): the same registers
+  // feed Q_g and Ebar, so each row of q and b is fetched once per wave that needs it
+  const int rbA = wave == 0 ? 0 : (wave == 1 ? 2 : 3);
+  u4v qreg[2][KS], breg[2][KS];
+#pragma unroll
+  for (int p = 0; p < KS; ++p) {
+    qreg[0][p] = ldg16(Q + kofs(16 * rbA + r16) + 32 * p + 8 * g);
+    breg[0][p] = ldg16(Bg + kofs(16 * rbA + r16) + 32 * p + 8 * g);
+  }
+  if (wave == 0) {
+#pragma unroll
+    for (int p = 0; p < KS; ++p) {
+      qreg[1][p] = ldg16(Q + kofs(16 + r16) + 32 * p + 8 * g);
+      breg[1][p] = ldg16(Bg + kofs(16 + r16) + 32 * p + 8 * g);
+    }
+  } else {
+#pragma unroll
+    for (int p = 0; p < KS; ++p) qreg[1][p] = breg[1][p] = u4v{0u, 0u, 0u, 0u};
+  }
 
   // ---- G2 = log2(e) * cumsum(g): in-register segment scans + segment offsets
   if (tid < 4) unsafe[tid] = 0;
@@ -165,17 +186,23 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
   // ---- Q_g (standard fragments) and Ktail^T (standard fragments, via transposed k)
   {
     unsigned char* Qo = a.Qg + ch * WsBf16::qg(DK);
-    for (int blk = wave; blk < 4 * KS; blk += 4) {
-      const int rb = blk / KS, kb = blk % KS;
-      const int r = 16 * rb + r16, c0 = 32 * kb + 8 * g;
-      float Gr[8], qf[8], x[8];
-      ldf8(sG + r * LG + c0, Gr);
-      unpack8(ldg16(Q + kofs(r) + c0), qf);
+    // row block rb (K-steps kb) from the q fragments; wave 3 holds a copy of block 3
 #pragma unroll
-      for (int e = 0; e < 8; ++e) x[e] = qf[e] * ex2(Gr[e]);
-      const Fr f = split8(x);
-      st8(reinterpret_cast<__bf16*>(Qo + blk * 2048 + 16 * lane), f.hi);
-      st8(reinterpret_cast<__bf16*>(Qo + blk * 2048 + 1024 + 16 * lane), f.lo);
+    for (int sl = 0; sl < 2; ++sl) {
+      if (sl == 0 ? wave == 3 : wave != 0) continue;
+      const int rb = sl == 0 ? rbA : 1;
+#pragma unroll
+      for (int kb = 0; kb < KS; ++kb) {
+        const int r = 16 * rb + r16, c0 = 32 * kb + 8 * g, blk = rb * KS + kb;
+        float Gr[8], qf[8], x[8];
+        ldf8(sG + r * LG + c0, Gr);
+        unpack8(qreg[sl][kb], qf);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[e] = qf[e] * ex2(Gr[e]);
+        const Fr f = split8(x);
+        st8(reinterpret_cast<__bf16*>(Qo + blk * 2048 + 16 * lane), f.hi);
+        st8(reinterpret_cast<__bf16*>(Qo + blk * 2048 + 1024 + 16 * lane), f.lo);
+      }
     }
     unsigned char* Ko = a.KtT + ch * WsBf16::ktt(DK);
     for (int blk = wave; blk < NCB * 2; blk += 4) {
@@ -225,7 +252,8 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
         }
       } else {
         const int s = 16 * j + r16;  // key row supplied by this lane (A operand)
-#pragma unroll 2
+        const bool sec = i == 1;        // wave 0's second row block
+#pragma unroll
         for (int p = 0; p < KS; ++p) {
           const int c0 = 32 * p + 8 * g;
           float Gs[8], Gr[8], Gp[8], ks[8], kr[8], br[8], qr[8];
@@ -234,8 +262,8 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
           ldf8(sG + (16 * i) * LG + c0, Gp);
           unpack8(ld8(sK + s * LKB + c0), ks);
           unpack8(ld8(sK + r * LKB + c0), kr);
-          unpack8(ldg16(Bg + kofs(r) + c0), br);
-          unpack8(ldg16(Q + kofs(r) + c0), qr);
+          unpack8(sec ? breg[1][p] : breg[0][p], br);
+          unpack8(sec ? qreg[1][p] : qreg[0][p], qr);
           float rk[8], le[8], lq[8];
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
@@ -354,26 +382,35 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
   }
 
   // ---- Ebar = b * k * gamma (split) over the G2 region
+  // (rows of the wave's row blocks, from the b fragments; wave 3 has none of its own)
   {
-    constexpr int NE = DK / 32;  // 8-channel groups per thread
-    float eb[NE][8];
+    Fr ef[2][KS];
 #pragma unroll
-    for (int m = 0; m < NE; ++m) {
-      const int e = tid + 256 * m, r = e / (DK / 8), c8 = (e % (DK / 8)) * 8;
-      float Gv[8], kf[8], bf[8];
-      ldf8(sG + r * LG + c8, Gv);
-      unpack8(ld8(sK + r * LKB + c8), kf);
-      unpack8(ldg16(Bg + kofs(r) + c8), bf);
+    for (int sl = 0; sl < 2; ++sl) {
+      if (sl == 0 ? wave == 3 : wave != 0) continue;
+      const int r = 16 * (sl == 0 ? rbA : 1) + r16;
 #pragma unroll
-      for (int x = 0; x < 8; ++x) eb[m][x] = bf[x] * kf[x] * ex2(Gv[x]);
+      for (int p = 0; p < KS; ++p) {
+        const int c0 = 32 * p + 8 * g;
+        float Gv[8], kf[8], bf[8], x[8];
+        ldf8(sG + r * LG + c0, Gv);
+        unpack8(ld8(sK + r * LKB + c0), kf);
+        unpack8(breg[sl][p], bf);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[e] = bf[e] * kf[e] * ex2(Gv[e]);
+        ef[sl][p] = split8(x);
+      }
     }
     __syncthreads();
 #pragma unroll
-    for (int m = 0; m < NE; ++m) {
-      const int e = tid + 256 * m, r = e / (DK / 8), c8 = (e % (DK / 8)) * 8;
-      const Fr f = split8(eb[m]);
-      st8(sEhi + r * LE + c8, f.hi);
-      st8(sElo + r * LE + c8, f.lo);
+    for (int sl = 0; sl < 2; ++sl) {
+      if (sl == 0 ? wave == 3 : wave != 0) continue;
+      const int r = 16 * (sl == 0 ? rbA : 1) + r16;
+#pragma unroll
+      for (int p = 0; p < KS; ++p) {
+        st8(sEhi + r * LE + 32 * p + 8 * g, ef[sl][p].hi);
+        st8(sElo + r * LE + 32 * p + 8 * g, ef[sl][p].lo);
+      }
     }
     __syncthreads();
   }
