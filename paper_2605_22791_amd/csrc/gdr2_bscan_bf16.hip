@@ -130,23 +130,27 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
     _Pragma("unroll") for (int u2 = 0; u2 < 4; ++u2) gcur[u2] = gnext[u2];                             \
   }
 
-  // ---- dS: tiles (key block cs, value blocks sv0..) as fp32 accumulators
+  // ---- dS: tiles (key block cs, value blocks sv0..) as fp32 accumulators, starting
+  // from identity columns, the given segment end, dS_T (last segment) or zero
+  const bool eye = (a.flags & kScanEye) != 0;  // (DV == DK)
+  const float* init = eye ? nullptr
+                          : (a.dSseg_in ? a.dSseg_in + (size_t)vs * DK * DV
+                                        : ((a.dST && seg == nseg - 1) ? a.dST + (size_t)seq * DK * DV : nullptr));
   f4 sreg[TPW];
+  if (init) {
+#pragma unroll
+    for (int t = 0; t < TPW; ++t)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) sreg[t][u] = init[(size_t)(16 * cs + 4 * g + u) * DV + v0 + 16 * (sv0 + t) + r16];
+  } else {
+#pragma unroll
+    for (int t = 0; t < TPW; ++t)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) sreg[t][u] = (eye && 16 * cs + 4 * g + u == v0 + 16 * (sv0 + t) + r16) ? 1.f : 0.f;
+  }
 #pragma unroll
   for (int t = 0; t < TPW; ++t) {
     const int vb = sv0 + t;
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int c = 16 * cs + 4 * g + u, v = 16 * vb + r16;
-      float x0 = 0.f;
-      if (a.flags & kScanEye)
-        x0 = (c == v0 + v) ? 1.f : 0.f;  // identity columns (DV == DK)
-      else if (a.dSseg_in)
-        x0 = a.dSseg_in[((size_t)vs * DK + c) * DV + v0 + v];
-      else if (a.dST && seg == nseg - 1)
-        x0 = a.dST[((size_t)seq * DK + c) * DV + v0 + v];
-      sreg[t][u] = x0;
-    }
     st4split(sDhi + (16 * vb + r16) * LSD + 16 * cs + 4 * g, sDlo + (16 * vb + r16) * LSD + 16 * cs + 4 * g,
              sreg[t]);
   }

@@ -144,23 +144,26 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
   _Pragma("unroll") for (int u2 = 0; u2 < 4; ++u2) GARR[u2] =                                            \
       a.GC[(CHX) * (WsBf16::gc(DK) / 4) + 16 * cs + 4 * g + u2];
 
-  // ---- state
+  // ---- state: identity columns, the given segment start, S0 (first segment) or zero
+  const bool eye = (a.flags & kScanEye) != 0;  // (DV == DK)
+  const float* init = eye ? nullptr
+                          : (a.S0seg ? a.S0seg + (size_t)vs * DK * DV
+                                     : ((a.S0 && seg == 0) ? a.S0 + (size_t)seq * DK * DV : nullptr));
   f4 sreg[TPW];
+  if (init) {
+#pragma unroll
+    for (int t = 0; t < TPW; ++t)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) sreg[t][u] = init[(size_t)(16 * cs + 4 * g + u) * DV + v0 + 16 * (sv0 + t) + r16];
+  } else {
+#pragma unroll
+    for (int t = 0; t < TPW; ++t)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) sreg[t][u] = (eye && 16 * cs + 4 * g + u == v0 + 16 * (sv0 + t) + r16) ? 1.f : 0.f;
+  }
 #pragma unroll
   for (int t = 0; t < TPW; ++t) {
     const int vb = sv0 + t;
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int c = 16 * cs + 4 * g + u, v = 16 * vb + r16;
-      float x0 = 0.f;
-      if (a.flags & kScanEye)
-        x0 = (c == v0 + v) ? 1.f : 0.f;  // identity columns (DV == DK)
-      else if (a.S0seg)
-        x0 = a.S0seg[((size_t)vs * DK + c) * DV + v0 + v];
-      else if (a.S0 && seg == 0)
-        x0 = a.S0[((size_t)seq * DK + c) * DV + v0 + v];
-      sreg[t][u] = x0;
-    }
     st4split(sShi + (16 * vb + r16) * LSS + 16 * cs + 4 * g, sSlo + (16 * vb + r16) * LSS + 16 * cs + 4 * g,
              sreg[t]);
   }
