@@ -16,6 +16,9 @@
  * notation is scale = 1).  q and k are consumed as given: L2 normalisation,
  * when wanted (App. D.2), is the caller's.
  *
+ * T need not be a multiple of the chunk length: the last chunk of every
+ * sequence may be partial.
+ *
  * Layout and dtypes (all tensors contiguous, row-major, device memory):
  *     q, k, b, log_alpha           (B, T, H, Dk)
  *     v, w, o                      (B, T, H, Dv)
@@ -37,11 +40,13 @@
  *     gdr2_recurrent_step, which is updated in place).
  *   * Every argument is validated before any HIP call; on error nothing is
  *     launched and the status says why:
- *       GDR2_EINVAL        null required pointer, pointer not 16-byte aligned,
- *                          a dimension <= 0, non-finite scale, unknown dtype;
- *       GDR2_EUNSUPPORTED  Dk or Dv not in {64, 128}, chunk != 64, T not a
- *                          multiple of 64 (chunk calls), sizes beyond 2^31
- *                          elements per tensor;
+ *       GDR2_EINVAL        null required pointer, pointer not 16-byte aligned
+ *                          (cu_seqlens: 4-byte aligned), a dimension <= 0,
+ *                          non-finite scale, unknown dtype, n_seqs <= 0 or
+ *                          B != 1 in a packed call;
+ *       GDR2_EUNSUPPORTED  Dk or Dv not in {64, 128}, chunk != 64, sizes
+ *                          beyond 2^31 elements per tensor, more than 2^24
+ *                          sequences in a packed call;
  *       GDR2_EWORKSPACE    ws_bytes below gdr2_chunk_workspace_bytes();
  *       GDR2_EHIP          a launch reported an error (hipGetLastError).
  *   * No C++ exception crosses this interface.
@@ -144,6 +149,50 @@ gdr2_status gdr2_chunk_bwd_saved(const gdr2_problem* problem, const void* q, con
 gdr2_status gdr2_recurrent_step(const gdr2_problem* problem, const void* q, const void* k,
                                 const void* v, const float* log_alpha, const void* b,
                                 const void* w, float* S, void* o, hipStream_t stream);
+
+/* ---- packed variable-length sequences (App. C.6) -------------------------
+ * A packed batch holds n_seqs sequences end to end along T: problem->B must be
+ * 1, problem->T is the total token count, and sequence s owns tokens
+ * cu_seqlens[s] .. cu_seqlens[s+1) of q, k, v, log_alpha, b, w, o, dout and
+ * of every token gradient.  cu_seqlens is a device array of n_seqs + 1 int32
+ * offsets with 0 = cu[0] <= cu[1] <= ... <= cu[n_seqs] = T (empty sequences
+ * allowed).  Each sequence is chunked on its own (its last chunk may be
+ * partial), so the state restarts at every sequence boundary: the result for
+ * sequence s equals a separate call on its tokens alone.  The states S0, S_T,
+ * dS_T, dS0 and S (recurrent) are (n_seqs, H, Dk, Dv) fp32.
+ * The offsets are read on the device and not checked on the host: the
+ * kernels clamp them into [0, T], so malformed offsets cannot cause accesses
+ * outside the tensors or the workspace, but the results are then undefined.
+ * Errors, ownership and streams as for the fixed-length calls. */
+
+/* Workspace bytes of a packed chunk call (for_backward as in
+ * gdr2_chunk_workspace_bytes). */
+gdr2_status gdr2_varlen_workspace_bytes(const gdr2_problem* problem, int32_t n_seqs, int for_backward,
+                                        size_t* bytes);
+
+/* Chunk forward of a packed batch.  save = 0 is gdr2_chunk_fwd (workspace of
+ * gdr2_varlen_workspace_bytes(p, n, 0)), save = 1 is gdr2_chunk_fwd_save
+ * (workspace of gdr2_varlen_workspace_bytes(p, n, 1)). */
+gdr2_status gdr2_chunk_fwd_varlen(const gdr2_problem* problem, const int32_t* cu_seqlens, int32_t n_seqs,
+                                  const void* q, const void* k, const void* v, const float* log_alpha,
+                                  const void* b, const void* w, const float* S0, void* o, float* S_T,
+                                  void* ws, size_t ws_bytes, int save, hipStream_t stream);
+
+/* Chunk backward of a packed batch.  saved = 0 recomputes the forward's
+ * intermediates (gdr2_chunk_bwd), saved = 1 reads those a save = 1 forward
+ * left in ws (gdr2_chunk_bwd_saved; same problem, cu_seqlens and inputs). */
+gdr2_status gdr2_chunk_bwd_varlen(const gdr2_problem* problem, const int32_t* cu_seqlens, int32_t n_seqs,
+                                  const void* q, const void* k, const void* v, const float* log_alpha,
+                                  const void* b, const void* w, const float* S0, const void* dout,
+                                  const float* dS_T, void* dq, void* dk, void* dv, float* dlog_alpha,
+                                  void* db, void* dw, float* dS0, void* ws, size_t ws_bytes, int saved,
+                                  hipStream_t stream);
+
+/* Recurrent forward of a packed batch (App. C.5 / C.6): every sequence's
+ * tokens in order, its state S[s] updated in place. */
+gdr2_status gdr2_recurrent_varlen(const gdr2_problem* problem, const int32_t* cu_seqlens, int32_t n_seqs,
+                                  const void* q, const void* k, const void* v, const float* log_alpha,
+                                  const void* b, const void* w, float* S, void* o, hipStream_t stream);
 
 /* Static, human-readable name of a status code. */
 const char* gdr2_status_str(gdr2_status status);

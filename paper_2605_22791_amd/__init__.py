@@ -16,7 +16,8 @@ __all__ = [
     "GDR2_OK", "GDR2_EINVAL", "GDR2_EUNSUPPORTED", "GDR2_EWORKSPACE", "GDR2_EHIP",
     "GDR2_BF16", "GDR2_FP32", "Gdr2Problem", "Gdr2Error", "lib", "lib_path",
     "gdr2_chunk_workspace_bytes", "gdr2_chunk_fwd", "gdr2_chunk_bwd", "gdr2_chunk_fwd_save",
-    "gdr2_chunk_bwd_saved",
+    "gdr2_chunk_bwd_saved", "gdr2_varlen_workspace_bytes", "gdr2_chunk_fwd_varlen", "gdr2_chunk_bwd_varlen",
+    "gdr2_recurrent_varlen",
     "gdr2_recurrent_step", "gdr2_status_str", "CHUNK", "KERNEL_NAMES",
     "gdr2_profile_enable", "gdr2_profile_collect",
 ]
@@ -73,6 +74,15 @@ def lib():
         L.gdr2_chunk_bwd_saved.restype = ctypes.c_int
         L.gdr2_recurrent_step.argtypes = [P] + [vp] * 8 + [vp]
         L.gdr2_recurrent_step.restype = ctypes.c_int
+        i32 = ctypes.c_int32
+        L.gdr2_varlen_workspace_bytes.argtypes = [P, i32, ctypes.c_int, ctypes.POINTER(ctypes.c_size_t)]
+        L.gdr2_varlen_workspace_bytes.restype = ctypes.c_int
+        L.gdr2_chunk_fwd_varlen.argtypes = [P, vp, i32] + [vp] * 10 + [ctypes.c_size_t, ctypes.c_int, vp]
+        L.gdr2_chunk_fwd_varlen.restype = ctypes.c_int
+        L.gdr2_chunk_bwd_varlen.argtypes = [P, vp, i32] + [vp] * 17 + [ctypes.c_size_t, ctypes.c_int, vp]
+        L.gdr2_chunk_bwd_varlen.restype = ctypes.c_int
+        L.gdr2_recurrent_varlen.argtypes = [P, vp, i32] + [vp] * 8 + [vp]
+        L.gdr2_recurrent_varlen.restype = ctypes.c_int
         L.gdr2_profile_enable.argtypes = [ctypes.c_int]
         L.gdr2_profile_enable.restype = ctypes.c_int
         L.gdr2_profile_collect.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_longlong),
@@ -229,6 +239,97 @@ def gdr2_recurrent_step(q, k, v, log_alpha, b, w, S, *, scale=None, o=None):
     st = lib().gdr2_recurrent_step(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha),
                                    _ptr(b), _ptr(w), _ptr(S), _ptr(o), _stream())
     _check(st, "gdr2_recurrent_step")
+    return o
+
+
+# --------------------------------------------------------------------------- packed sequences
+def _cu(cu_seqlens, T):
+    torch = _torch()
+    if cu_seqlens.dim() != 1 or cu_seqlens.numel() < 2:
+        raise ValueError("cu_seqlens: expected a 1-D tensor of n_seqs + 1 offsets")
+    _require("cu_seqlens", cu_seqlens, (cu_seqlens.numel(),), torch.int32)
+    return cu_seqlens.numel() - 1
+
+
+def gdr2_varlen_workspace_bytes(problem, n_seqs, for_backward):
+    """Bytes of workspace of a packed call of n_seqs sequences."""
+    n = ctypes.c_size_t(0)
+    _check(lib().gdr2_varlen_workspace_bytes(ctypes.byref(problem), int(n_seqs), int(for_backward),
+                                             ctypes.byref(n)), "gdr2_varlen_workspace_bytes")
+    return n.value
+
+
+def gdr2_chunk_fwd_varlen(q, k, v, log_alpha, b, w, cu_seqlens, S0=None, *, scale=None, o=None, S_T=None,
+                          want_state=True, ws=None, save=False):
+    """Chunk forward of a packed batch: q.. of shape (1, T, H, D), sequence s owns
+    tokens cu_seqlens[s] .. cu_seqlens[s+1) (int32 device tensor).  States are
+    (n_seqs, H, Dk, Dv).  Returns (o, S_T); save=True as in gdr2_chunk_fwd."""
+    torch = _torch()
+    B, T, H, Dk, Dv = _validate(q, k, v, log_alpha, b, w)
+    N = _cu(cu_seqlens, T)
+    _require("S0", S0, (N, H, Dk, Dv), torch.float32)
+    prob = _problem(q, v, scale)
+    if o is None:
+        o = torch.empty((B, T, H, Dv), dtype=q.dtype, device=q.device)
+    _require("o", o, (B, T, H, Dv), q.dtype)
+    if S_T is None and want_state:
+        S_T = torch.empty((N, H, Dk, Dv), dtype=torch.float32, device=q.device)
+    _require("S_T", S_T, (N, H, Dk, Dv), torch.float32)
+    need = gdr2_varlen_workspace_bytes(prob, N, 1 if save else 0)
+    if ws is None:
+        if save:
+            raise ValueError("save=True needs the workspace that the backward will read")
+        ws = torch.empty(need, dtype=torch.uint8, device=q.device)
+    st = lib().gdr2_chunk_fwd_varlen(ctypes.byref(prob), _ptr(cu_seqlens), N, _ptr(q), _ptr(k), _ptr(v),
+                                     _ptr(log_alpha), _ptr(b), _ptr(w), _ptr(S0), _ptr(o), _ptr(S_T), _ptr(ws),
+                                     ws.numel(), 1 if save else 0, _stream())
+    _check(st, "gdr2_chunk_fwd_varlen")
+    return o, S_T
+
+
+def gdr2_chunk_bwd_varlen(q, k, v, log_alpha, b, w, cu_seqlens, S0, dout, dS_T=None, *, scale=None,
+                          grads=None, want_dS0=True, ws=None, saved=False):
+    """Backward of a packed batch; returns dict dq, dk, dv, dlog_alpha, db, dw, dS0."""
+    torch = _torch()
+    B, T, H, Dk, Dv = _validate(q, k, v, log_alpha, b, w)
+    N = _cu(cu_seqlens, T)
+    _require("S0", S0, (N, H, Dk, Dv), torch.float32)
+    _require("dout", dout, (B, T, H, Dv), q.dtype)
+    _require("dS_T", dS_T, (N, H, Dk, Dv), torch.float32)
+    prob = _problem(q, v, scale)
+    g = dict(grads or {})
+    for n, like in (("dq", q), ("dk", k), ("dv", v), ("dlog_alpha", log_alpha), ("db", b), ("dw", w)):
+        g.setdefault(n, torch.empty_like(like))
+    if want_dS0:
+        g.setdefault("dS0", torch.empty((N, H, Dk, Dv), dtype=torch.float32, device=q.device))
+    else:
+        g.setdefault("dS0", None)
+    need = gdr2_varlen_workspace_bytes(prob, N, 1)
+    if ws is None:
+        if saved:
+            raise ValueError("saved=True needs the workspace of the saving forward")
+        ws = torch.empty(need, dtype=torch.uint8, device=q.device)
+    st = lib().gdr2_chunk_bwd_varlen(ctypes.byref(prob), _ptr(cu_seqlens), N, _ptr(q), _ptr(k), _ptr(v),
+                                     _ptr(log_alpha), _ptr(b), _ptr(w), _ptr(S0), _ptr(dout), _ptr(dS_T),
+                                     _ptr(g["dq"]), _ptr(g["dk"]), _ptr(g["dv"]), _ptr(g["dlog_alpha"]),
+                                     _ptr(g["db"]), _ptr(g["dw"]), _ptr(g["dS0"]), _ptr(ws), ws.numel(),
+                                     1 if saved else 0, _stream())
+    _check(st, "gdr2_chunk_bwd_varlen")
+    return g
+
+
+def gdr2_recurrent_varlen(q, k, v, log_alpha, b, w, cu_seqlens, S, *, scale=None, o=None):
+    """Token-by-token forward of a packed batch; S (n_seqs, H, Dk, Dv) updated in place.  Returns o."""
+    torch = _torch()
+    B, T, H, Dk, Dv = _validate(q, k, v, log_alpha, b, w)
+    N = _cu(cu_seqlens, T)
+    _require("S", S, (N, H, Dk, Dv), torch.float32)
+    prob = _problem(q, v, scale)
+    if o is None:
+        o = torch.empty((B, T, H, Dv), dtype=q.dtype, device=q.device)
+    st = lib().gdr2_recurrent_varlen(ctypes.byref(prob), _ptr(cu_seqlens), N, _ptr(q), _ptr(k), _ptr(v),
+                                     _ptr(log_alpha), _ptr(b), _ptr(w), _ptr(S), _ptr(o), _stream())
+    _check(st, "gdr2_recurrent_varlen")
     return o
 
 

@@ -21,24 +21,33 @@ size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-gdr2_status check_problem(const gdr2_problem* p, bool chunked) {
+constexpr int kMaxSeqs = 1 << 24;  // sequences of one packed call
+
+// nseq > 0: a packed variable-length call of nseq sequences (B must be 1).
+gdr2_status check_problem(const gdr2_problem* p, bool chunked, int nseq = 0) {
   if (p == nullptr) return GDR2_EINVAL;
   if (p->B <= 0 || p->T <= 0 || p->H <= 0 || p->Dk <= 0 || p->Dv <= 0) return GDR2_EINVAL;
   if (!std::isfinite(p->scale)) return GDR2_EINVAL;
   if (p->dtype != GDR2_BF16 && p->dtype != GDR2_FP32) return GDR2_EINVAL;
+  if (nseq < 0 || (nseq > 0 && p->B != 1)) return GDR2_EINVAL;
   if ((p->Dk != 64 && p->Dk != 128) || (p->Dv != 64 && p->Dv != 128)) return GDR2_EUNSUPPORTED;
-  if (chunked) {
-    if (p->chunk != CH) return GDR2_EUNSUPPORTED;
-    if (p->T % CH != 0) return GDR2_EUNSUPPORTED;
-  }
+  if (chunked && p->chunk != CH) return GDR2_EUNSUPPORTED;
+  if (nseq > kMaxSeqs) return GDR2_EUNSUPPORTED;
   const double rows = (double)p->B * (double)p->T * (double)p->H;
   const int dmax = p->Dk > p->Dv ? p->Dk : p->Dv;
   if (rows * dmax >= 2147483648.0) return GDR2_EUNSUPPORTED;
-  if ((double)p->B * p->H * (double)p->Dk * p->Dv >= 2147483648.0) return GDR2_EUNSUPPORTED;
+  const double states = nseq > 0 ? (double)nseq : (double)p->B;
+  if (states * p->H * (double)p->Dk * p->Dv >= 2147483648.0) return GDR2_EUNSUPPORTED;
   return GDR2_OK;
 }
 
-// Workspace regions, chunk-head major: ch = (b*H + h)*NT + n.  The bf16
+// Chunks per sequence of a fixed-length call (the last one partial when 64 does not divide T).
+int chunks_per_seq(const gdr2_problem* p) { return (p->T + CH - 1) / CH; }
+// Chunk slots of a packed call: sum_s ceil(L_s / 64) <= floor(T / 64) + nseq.
+int varlen_slots(const gdr2_problem* p, int nseq) { return p->T / CH + nseq; }
+
+// Workspace regions, chunk-head major: ch = (b*H + h)*NT + n (fixed length) or
+// h*slots + c (packed; see Varlen in gdr2_kernels.hpp).  The bf16
 // path uses the fragment-order regions of WsBf16 (gdr2_kernels.hpp) plus fp32
 // chunk states and R for the backward; the fp32 path uses fp32 tiles.
 struct Layout {
@@ -48,6 +57,7 @@ struct Layout {
   size_t bDR, bAm;                       // bf16 backward extras (fragment order)
   size_t sM, sN, sX;                     // segment maps and entry states (sequence-parallel scans)
   int nseg, seg_len;
+  size_t vcoff, vct0, vclen;             // chunk table of a packed call (int32)
   size_t total;
 };
 
@@ -60,7 +70,7 @@ struct Layout {
 // and a segment keeps at least 8 chunks.  GDR2_SCAN_SEGMENTS=<n> overrides the
 // count (1 turns the mode off).
 void scan_segments(const gdr2_problem* p, int& nseg, int& seg_len) {
-  const int NT = p->T / CH;
+  const int NT = chunks_per_seq(p);
   const long long slices = (long long)p->B * p->H * (p->Dv / 64);
   static const int forced = [] {
     const char* e = std::getenv("GDR2_SCAN_SEGMENTS");
@@ -77,8 +87,8 @@ void scan_segments(const gdr2_problem* p, int& nseg, int& seg_len) {
   nseg = (NT + seg_len - 1) / seg_len;
 }
 
-Layout layout(const gdr2_problem* p, bool bwd) {
-  const size_t NC = (size_t)p->B * p->H * (size_t)(p->T / CH);
+Layout layout(const gdr2_problem* p, bool bwd, int nseq = 0) {
+  const size_t NC = nseq > 0 ? (size_t)p->H * varlen_slots(p, nseq) : (size_t)p->B * p->H * chunks_per_seq(p);
   const size_t Dk = p->Dk, Dv = p->Dv;
   Layout L{};
   size_t off = 0;
@@ -124,7 +134,17 @@ Layout layout(const gdr2_problem* p, bool bwd) {
       L.DEg = take(NC * CH * Dk);
     }
   }
-  scan_segments(p, L.nseg, L.seg_len);
+  if (nseq > 0) {
+    // packed calls scan every sequence whole (their lengths differ)
+    L.nseg = 1;
+    L.seg_len = 0;
+    const size_t slots = (size_t)varlen_slots(p, nseq);
+    L.vcoff = take((size_t)nseq + 1);
+    L.vct0 = take(slots);
+    L.vclen = take(slots);
+  } else {
+    scan_segments(p, L.nseg, L.seg_len);
+  }
   if (L.nseg > 1) {
     const size_t nvs = (size_t)p->B * p->H * L.nseg;
     L.sM = take(nvs * Dk * Dk);
@@ -138,6 +158,42 @@ Layout layout(const gdr2_problem* p, bool bwd) {
 template <typename T>
 T* at(void* ws, size_t off) {
   return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
+}
+
+// Everything a run needs about the chunking: the workspace layout, chunks per
+// sequence (fixed length) or chunk slots (packed), the number of scanned
+// sequences and, for packed calls, the device chunk table.
+struct Geo {
+  Layout L;
+  int NT;
+  int nscan;
+  Varlen vl;
+};
+
+Geo make_geo(const gdr2_problem* p, bool bwd, int nseq, const int* cu, void* ws) {
+  Geo G{};
+  G.L = layout(p, bwd, nseq);
+  if (nseq > 0) {
+    G.NT = varlen_slots(p, nseq);
+    G.nscan = nseq;
+    G.vl.cu = cu;
+    G.vl.coff = at<int>(ws, G.L.vcoff);
+    G.vl.ct0 = at<int>(ws, G.L.vct0);
+    G.vl.clen = at<int>(ws, G.L.vclen);
+    G.vl.nseq = nseq;
+    G.vl.ncmax = G.NT;
+  } else {
+    G.NT = chunks_per_seq(p);
+    G.nscan = p->B;
+  }
+  return G;
+}
+
+// Builds the chunk table of a packed call in the workspace (no-op otherwise).
+hipError_t build_table(const gdr2_problem* p, const Geo& G, hipStream_t st) {
+  if (G.vl.cu == nullptr) return hipSuccess;
+  return launch_varlen_table(G.vl.cu, G.vl.nseq, p->T, G.vl.ncmax, const_cast<int*>(G.vl.coff),
+                             const_cast<int*>(G.vl.ct0), const_cast<int*>(G.vl.clen), st);
 }
 
 bool debug_sync() {
@@ -281,9 +337,9 @@ struct FwdRun {
   // save: also leave A, the chunk-start states and R in the workspace (backward layout)
   static hipError_t run(const gdr2_problem* p, const void* q, const void* k, const void* v,
                         const float* g, const void* b, const void* w, const float* S0, void* o,
-                        float* ST, void* ws, bool save, hipStream_t st) {
-    const Layout L = layout(p, save);
-    const int NT = p->T / CH;
+                        float* ST, void* ws, bool save, const Geo& G, hipStream_t st) {
+    const Layout& L = G.L;
+    const int NT = G.NT;
     if (std::is_same<TIn, bf16_t>::value) {
       // bf16: chunk-parallel intra-chunk kernel, then the state scan with the output
       IntraBf16Args ia{static_cast<const bf16_t*>(q), static_cast<const bf16_t*>(k),
@@ -292,11 +348,13 @@ struct FwdRun {
                        at<unsigned char>(ws, L.bQ), at<unsigned char>(ws, L.bA),
                        at<unsigned char>(ws, L.bK), at<float>(ws, L.bU), at<float>(ws, L.bG),
                        save ? at<unsigned char>(ws, L.bAm) : nullptr, p->B, p->T, p->H, NT};
+      ia.vl = G.vl;
       hipError_t e = timed(GDR2_K_FWD_INTRA, st, [&] { return launch_intra_bf16<DK, DV>(ia, st); });
       if (e != hipSuccess) return e;
       ScanArgs sa{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.U, ia.GC, S0, ST, static_cast<bf16_t*>(o),
                   save ? at<float>(ws, L.Hs) : nullptr, save ? at<float>(ws, L.Rs) : nullptr,
-                  p->B, p->T, p->H, NT, p->scale};
+                  G.nscan, p->T, p->H, NT, p->scale};
+      sa.vl = G.vl;
       return timed(GDR2_K_FWD_STATE, st, [&] {
         return scan_fwd_bf16<DK, DV>(sa, L, ws, [&](const ScanArgs& x) {
           return save ? launch_scan_bf16<DK, DV, true, true>(x, st) : launch_scan_bf16<DK, DV, true, false>(x, st);
@@ -308,14 +366,16 @@ struct FwdRun {
                       static_cast<const TIn*>(w), at<float>(ws, L.Y), at<float>(ws, L.U),
                       at<float>(ws, L.Kt), at<float>(ws, L.Qg), at<float>(ws, L.Aqk),
                       at<float>(ws, L.GC), p->T, p->H, NT};
+    ia.vl = G.vl;
     hipError_t e = timed(GDR2_K_FWD_INTRA, st, [&] { return launch_fwd_intra<DK, DV, TIn>(ia, p->B, st); });
     if (e != hipSuccess) return e;
     StateArgs<TIn> sa{ia.Y, ia.U, ia.Kt, ia.Qg, ia.Aqk, ia.GC, S0, ST, static_cast<TIn*>(o),
                       save ? at<float>(ws, L.Hs) : nullptr, save ? at<float>(ws, L.Rs) : nullptr,
                       p->T, p->H, NT, p->scale};
+    sa.vl = G.vl;
     return timed(GDR2_K_FWD_STATE, st, [&] {
-      return save ? launch_fwd_state<DK, DV, TIn, true, true>(sa, p->B, st)
-                  : launch_fwd_state<DK, DV, TIn, true, false>(sa, p->B, st);
+      return save ? launch_fwd_state<DK, DV, TIn, true, true>(sa, G.nscan, st)
+                  : launch_fwd_state<DK, DV, TIn, true, false>(sa, G.nscan, st);
     });
   }
 };
@@ -326,9 +386,10 @@ struct BwdRun {
   static hipError_t run(const gdr2_problem* p, const void* q, const void* k, const void* v,
                         const float* g, const void* b, const void* w, const float* S0,
                         const void* dout, const float* dST, void* dq, void* dk, void* dv,
-                        float* dg, void* db, void* dw, float* dS0, void* ws, bool saved, hipStream_t st) {
-    const Layout L = layout(p, true);
-    const int NT = p->T / CH;
+                        float* dg, void* db, void* dw, float* dS0, void* ws, bool saved, const Geo& G,
+                        hipStream_t st) {
+    const Layout& L = G.L;
+    const int NT = G.NT;
     hipError_t e = hipSuccess;
     if (std::is_same<TIn, bf16_t>::value) {
       IntraBf16Args ia{static_cast<const bf16_t*>(q), static_cast<const bf16_t*>(k),
@@ -337,12 +398,14 @@ struct BwdRun {
                        at<unsigned char>(ws, L.bQ), at<unsigned char>(ws, L.bA),
                        at<unsigned char>(ws, L.bK), at<float>(ws, L.bU), at<float>(ws, L.bG),
                        at<unsigned char>(ws, L.bAm), p->B, p->T, p->H, NT};
+      ia.vl = G.vl;
       if (!saved) {
         // recompute: intra-chunk tiles (with A), then the forward scan storing the chunk states and R
         e = timed(GDR2_K_BWD_RECOMPUTE_INTRA, st, [&] { return launch_intra_bf16<DK, DV>(ia, st); });
         if (e != hipSuccess) return e;
         ScanArgs sa{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.U, ia.GC, S0, nullptr, nullptr, at<float>(ws, L.Hs),
-                    at<float>(ws, L.Rs), p->B, p->T, p->H, NT, p->scale};
+                    at<float>(ws, L.Rs), G.nscan, p->T, p->H, NT, p->scale};
+        sa.vl = G.vl;
         e = timed(GDR2_K_BWD_RECOMPUTE_STATE, st, [&] {
           return scan_fwd_bf16<DK, DV>(sa, L, ws, [&](const ScanArgs& x) {
             return launch_scan_bf16<DK, DV, false, true>(x, st);
@@ -351,7 +414,8 @@ struct BwdRun {
         if (e != hipSuccess) return e;
       }
       BScanArgs ba{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.GC, static_cast<const bf16_t*>(dout), dST, dS0,
-                   at<float>(ws, L.DH), at<unsigned char>(ws, L.bDR), p->B, p->T, p->H, NT, p->scale};
+                   at<float>(ws, L.DH), at<unsigned char>(ws, L.bDR), G.nscan, p->T, p->H, NT, p->scale};
+      ba.vl = G.vl;
       e = timed(GDR2_K_BWD_STATE, st, [&] { return scan_bwd_bf16<DK, DV>(ba, L, ws, st); });
       if (e != hipSuccess) return e;
       // the WY VJP and the intra-chunk VJP in one chunk-parallel kernel
@@ -362,6 +426,7 @@ struct BwdRun {
                         at<unsigned char>(ws, L.bAm), static_cast<bf16_t*>(dq), static_cast<bf16_t*>(dk),
                         static_cast<bf16_t*>(dv), static_cast<bf16_t*>(db), static_cast<bf16_t*>(dw), dg,
                         p->B, p->T, p->H, NT, p->scale};
+      ca.vl = G.vl;
       return timed(GDR2_K_BWD_INTRA, st, [&] { return launch_bchunk_bf16<DK, DV>(ca, st); });
     }
     IntraArgs<TIn> ia{static_cast<const TIn*>(q), static_cast<const TIn*>(k),
@@ -369,18 +434,21 @@ struct BwdRun {
                       static_cast<const TIn*>(w), at<float>(ws, L.Y), at<float>(ws, L.U),
                       at<float>(ws, L.Kt), at<float>(ws, L.Qg), at<float>(ws, L.Aqk),
                       at<float>(ws, L.GC), p->T, p->H, NT};
+    ia.vl = G.vl;
     StateArgs<TIn> sa{ia.Y, ia.U, ia.Kt, ia.Qg, ia.Aqk, ia.GC, S0, nullptr, nullptr,
                       at<float>(ws, L.Hs), at<float>(ws, L.Rs), p->T, p->H, NT, p->scale};
+    sa.vl = G.vl;
     if (!saved) {
       e = timed(GDR2_K_BWD_RECOMPUTE_INTRA, st, [&] { return launch_fwd_intra<DK, DV, TIn>(ia, p->B, st); });
       if (e != hipSuccess) return e;
       e = timed(GDR2_K_BWD_RECOMPUTE_STATE, st,
-                [&] { return launch_fwd_state<DK, DV, TIn, false, true>(sa, p->B, st); });
+                [&] { return launch_fwd_state<DK, DV, TIn, false, true>(sa, G.nscan, st); });
       if (e != hipSuccess) return e;
     }
     BwdStateArgs<TIn> ba{ia.Qg, ia.Kt, ia.Y, ia.Aqk, ia.GC, static_cast<const TIn*>(dout), dST,
                          dS0, at<float>(ws, L.DH), at<float>(ws, L.DR), p->T, p->H, NT, p->scale};
-    e = timed(GDR2_K_BWD_STATE, st, [&] { return launch_bwd_state<DK, DV, TIn>(ba, p->B, st); });
+    ba.vl = G.vl;
+    e = timed(GDR2_K_BWD_STATE, st, [&] { return launch_bwd_state<DK, DV, TIn>(ba, G.nscan, st); });
     if (e != hipSuccess) return e;
     BwdChunkArgs<TIn> ca{static_cast<const TIn*>(q), static_cast<const TIn*>(k),
                          static_cast<const TIn*>(v), g, static_cast<const TIn*>(b),
@@ -389,6 +457,7 @@ struct BwdRun {
                          at<float>(ws, L.DEg), static_cast<TIn*>(dq), static_cast<TIn*>(dk),
                          static_cast<TIn*>(dv), static_cast<TIn*>(db), static_cast<TIn*>(dw), dg,
                          p->T, p->H, NT, p->scale};
+    ca.vl = G.vl;
     e = timed(GDR2_K_BWD_WY, st, [&] { return launch_bwd_wy<DK, DV, TIn>(ca, p->B, st); });
     if (e != hipSuccess) return e;
     return timed(GDR2_K_BWD_INTRA, st, [&] { return launch_bwd_intra<DK, DV, TIn>(ca, p->B, st); });
@@ -398,12 +467,14 @@ struct BwdRun {
 template <int DK, int DV, typename TIn>
 struct RecRun {
   static hipError_t run(const gdr2_problem* p, const void* q, const void* k, const void* v,
-                        const float* g, const void* b, const void* w, float* S, void* o,
-                        hipStream_t st) {
+                        const float* g, const void* b, const void* w, float* S, void* o, const int* cu,
+                        int nseq, hipStream_t st) {
     RecurArgs<TIn> ra{static_cast<const TIn*>(q), static_cast<const TIn*>(k),
                       static_cast<const TIn*>(v), g, static_cast<const TIn*>(b),
                       static_cast<const TIn*>(w), S, static_cast<TIn*>(o), p->T, p->H, p->scale};
-    return timed(GDR2_K_RECURRENT, st, [&] { return launch_recurrent<DK, DV, TIn>(ra, p->B, st); });
+    ra.cu = cu;
+    const int nb = cu != nullptr ? nseq : p->B;
+    return timed(GDR2_K_RECURRENT, st, [&] { return launch_recurrent<DK, DV, TIn>(ra, nb, st); });
   }
 };
 
@@ -419,6 +490,8 @@ bool opt_ok(std::initializer_list<const void*> opt) {
   return true;
 }
 
+bool cu_ok(const int32_t* cu) { return cu != nullptr && (reinterpret_cast<uintptr_t>(cu) & 3u) == 0; }
+
 }  // namespace
 
 extern "C" {
@@ -433,39 +506,61 @@ gdr2_status gdr2_chunk_workspace_bytes(const gdr2_problem* p, int for_backward, 
 
 namespace {
 
-gdr2_status chunk_fwd(const gdr2_problem* p, const void* q, const void* k, const void* v,
-                      const float* log_alpha, const void* b, const void* w, const float* S0, void* o,
-                      float* S_T, void* ws, size_t ws_bytes, bool save, hipStream_t stream) {
-  gdr2_status s = check_problem(p, true);
+// nseq > 0 (with cu): packed variable-length call
+gdr2_status chunk_fwd(const gdr2_problem* p, const int32_t* cu, int nseq, const void* q, const void* k,
+                      const void* v, const float* log_alpha, const void* b, const void* w, const float* S0,
+                      void* o, float* S_T, void* ws, size_t ws_bytes, bool save, hipStream_t stream) {
+  gdr2_status s = check_problem(p, true, nseq);
   if (s != GDR2_OK) return s;
   if (!all_ok({q, k, v, log_alpha, b, w, o, ws}) || !opt_ok({S0, S_T})) return GDR2_EINVAL;
-  if (ws_bytes < layout(p, save).total) return GDR2_EWORKSPACE;
-  hipError_t e;
+  if (nseq > 0 && !cu_ok(cu)) return GDR2_EINVAL;
+  const Geo G = make_geo(p, save, nseq, cu, ws);
+  if (ws_bytes < G.L.total) return GDR2_EWORKSPACE;
+  hipError_t e = build_table(p, G, stream);
+  if (e != hipSuccess) return GDR2_EHIP;
   if (p->dtype == GDR2_BF16)
-    e = dispatch<FwdRun, bf16_t>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S0, o, S_T, ws, save, stream);
+    e = dispatch<FwdRun, bf16_t>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S0, o, S_T, ws, save, G, stream);
   else
-    e = dispatch<FwdRun, float>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S0, o, S_T, ws, save, stream);
+    e = dispatch<FwdRun, float>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S0, o, S_T, ws, save, G, stream);
   return hip_status(e, stream);
 }
 
-gdr2_status chunk_bwd(const gdr2_problem* p, const void* q, const void* k, const void* v,
-                      const float* log_alpha, const void* b, const void* w, const float* S0,
+gdr2_status chunk_bwd(const gdr2_problem* p, const int32_t* cu, int nseq, const void* q, const void* k,
+                      const void* v, const float* log_alpha, const void* b, const void* w, const float* S0,
                       const void* dout, const float* dS_T, void* dq, void* dk, void* dv,
                       float* dlog_alpha, void* db, void* dw, float* dS0, void* ws, size_t ws_bytes,
                       bool saved, hipStream_t stream) {
-  gdr2_status s = check_problem(p, true);
+  gdr2_status s = check_problem(p, true, nseq);
   if (s != GDR2_OK) return s;
   if (!all_ok({q, k, v, log_alpha, b, w, dout, dq, dk, dv, dlog_alpha, db, dw, ws}) ||
       !opt_ok({S0, dS_T, dS0}))
     return GDR2_EINVAL;
-  if (ws_bytes < layout(p, true).total) return GDR2_EWORKSPACE;
-  hipError_t e;
+  if (nseq > 0 && !cu_ok(cu)) return GDR2_EINVAL;
+  const Geo G = make_geo(p, true, nseq, cu, ws);
+  if (ws_bytes < G.L.total) return GDR2_EWORKSPACE;
+  hipError_t e = build_table(p, G, stream);
+  if (e != hipSuccess) return GDR2_EHIP;
   if (p->dtype == GDR2_BF16)
     e = dispatch<BwdRun, bf16_t>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S0, dout, dS_T, dq,
-                                 dk, dv, dlog_alpha, db, dw, dS0, ws, saved, stream);
+                                 dk, dv, dlog_alpha, db, dw, dS0, ws, saved, G, stream);
   else
     e = dispatch<BwdRun, float>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S0, dout, dS_T, dq,
-                                dk, dv, dlog_alpha, db, dw, dS0, ws, saved, stream);
+                                dk, dv, dlog_alpha, db, dw, dS0, ws, saved, G, stream);
+  return hip_status(e, stream);
+}
+
+gdr2_status recurrent(const gdr2_problem* p, const int32_t* cu, int nseq, const void* q, const void* k,
+                      const void* v, const float* log_alpha, const void* b, const void* w, float* S, void* o,
+                      hipStream_t stream) {
+  gdr2_status s = check_problem(p, false, nseq);
+  if (s != GDR2_OK) return s;
+  if (!all_ok({q, k, v, log_alpha, b, w, S, o})) return GDR2_EINVAL;
+  if (nseq > 0 && !cu_ok(cu)) return GDR2_EINVAL;
+  hipError_t e;
+  if (p->dtype == GDR2_BF16)
+    e = dispatch<RecRun, bf16_t>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S, o, cu, nseq, stream);
+  else
+    e = dispatch<RecRun, float>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S, o, cu, nseq, stream);
   return hip_status(e, stream);
 }
 
@@ -474,13 +569,13 @@ gdr2_status chunk_bwd(const gdr2_problem* p, const void* q, const void* k, const
 gdr2_status gdr2_chunk_fwd(const gdr2_problem* p, const void* q, const void* k, const void* v,
                            const float* log_alpha, const void* b, const void* w, const float* S0,
                            void* o, float* S_T, void* ws, size_t ws_bytes, hipStream_t stream) {
-  return chunk_fwd(p, q, k, v, log_alpha, b, w, S0, o, S_T, ws, ws_bytes, false, stream);
+  return chunk_fwd(p, nullptr, 0, q, k, v, log_alpha, b, w, S0, o, S_T, ws, ws_bytes, false, stream);
 }
 
 gdr2_status gdr2_chunk_fwd_save(const gdr2_problem* p, const void* q, const void* k, const void* v,
                                 const float* log_alpha, const void* b, const void* w, const float* S0,
                                 void* o, float* S_T, void* ws, size_t ws_bytes, hipStream_t stream) {
-  return chunk_fwd(p, q, k, v, log_alpha, b, w, S0, o, S_T, ws, ws_bytes, true, stream);
+  return chunk_fwd(p, nullptr, 0, q, k, v, log_alpha, b, w, S0, o, S_T, ws, ws_bytes, true, stream);
 }
 
 gdr2_status gdr2_chunk_bwd(const gdr2_problem* p, const void* q, const void* k, const void* v,
@@ -488,8 +583,8 @@ gdr2_status gdr2_chunk_bwd(const gdr2_problem* p, const void* q, const void* k, 
                            const void* dout, const float* dS_T, void* dq, void* dk, void* dv,
                            float* dlog_alpha, void* db, void* dw, float* dS0, void* ws,
                            size_t ws_bytes, hipStream_t stream) {
-  return chunk_bwd(p, q, k, v, log_alpha, b, w, S0, dout, dS_T, dq, dk, dv, dlog_alpha, db, dw, dS0, ws,
-                   ws_bytes, false, stream);
+  return chunk_bwd(p, nullptr, 0, q, k, v, log_alpha, b, w, S0, dout, dS_T, dq, dk, dv, dlog_alpha, db, dw,
+                   dS0, ws, ws_bytes, false, stream);
 }
 
 gdr2_status gdr2_chunk_bwd_saved(const gdr2_problem* p, const void* q, const void* k, const void* v,
@@ -497,22 +592,50 @@ gdr2_status gdr2_chunk_bwd_saved(const gdr2_problem* p, const void* q, const voi
                                  const void* dout, const float* dS_T, void* dq, void* dk, void* dv,
                                  float* dlog_alpha, void* db, void* dw, float* dS0, void* ws,
                                  size_t ws_bytes, hipStream_t stream) {
-  return chunk_bwd(p, q, k, v, log_alpha, b, w, S0, dout, dS_T, dq, dk, dv, dlog_alpha, db, dw, dS0, ws,
-                   ws_bytes, true, stream);
+  return chunk_bwd(p, nullptr, 0, q, k, v, log_alpha, b, w, S0, dout, dS_T, dq, dk, dv, dlog_alpha, db, dw,
+                   dS0, ws, ws_bytes, true, stream);
 }
 
 gdr2_status gdr2_recurrent_step(const gdr2_problem* p, const void* q, const void* k, const void* v,
                                 const float* log_alpha, const void* b, const void* w, float* S,
                                 void* o, hipStream_t stream) {
-  gdr2_status s = check_problem(p, false);
+  return recurrent(p, nullptr, 0, q, k, v, log_alpha, b, w, S, o, stream);
+}
+
+gdr2_status gdr2_varlen_workspace_bytes(const gdr2_problem* p, int32_t n_seqs, int for_backward,
+                                        size_t* bytes) {
+  if (bytes == nullptr || n_seqs <= 0) return GDR2_EINVAL;
+  const gdr2_status s = check_problem(p, true, n_seqs);
   if (s != GDR2_OK) return s;
-  if (!all_ok({q, k, v, log_alpha, b, w, S, o})) return GDR2_EINVAL;
-  hipError_t e;
-  if (p->dtype == GDR2_BF16)
-    e = dispatch<RecRun, bf16_t>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S, o, stream);
-  else
-    e = dispatch<RecRun, float>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S, o, stream);
-  return hip_status(e, stream);
+  *bytes = layout(p, for_backward != 0, n_seqs).total;
+  return GDR2_OK;
+}
+
+gdr2_status gdr2_chunk_fwd_varlen(const gdr2_problem* p, const int32_t* cu_seqlens, int32_t n_seqs,
+                                  const void* q, const void* k, const void* v, const float* log_alpha,
+                                  const void* b, const void* w, const float* S0, void* o, float* S_T, void* ws,
+                                  size_t ws_bytes, int save, hipStream_t stream) {
+  if (n_seqs <= 0) return GDR2_EINVAL;
+  return chunk_fwd(p, cu_seqlens, n_seqs, q, k, v, log_alpha, b, w, S0, o, S_T, ws, ws_bytes, save != 0,
+                   stream);
+}
+
+gdr2_status gdr2_chunk_bwd_varlen(const gdr2_problem* p, const int32_t* cu_seqlens, int32_t n_seqs,
+                                  const void* q, const void* k, const void* v, const float* log_alpha,
+                                  const void* b, const void* w, const float* S0, const void* dout,
+                                  const float* dS_T, void* dq, void* dk, void* dv, float* dlog_alpha, void* db,
+                                  void* dw, float* dS0, void* ws, size_t ws_bytes, int saved,
+                                  hipStream_t stream) {
+  if (n_seqs <= 0) return GDR2_EINVAL;
+  return chunk_bwd(p, cu_seqlens, n_seqs, q, k, v, log_alpha, b, w, S0, dout, dS_T, dq, dk, dv, dlog_alpha, db,
+                   dw, dS0, ws, ws_bytes, saved != 0, stream);
+}
+
+gdr2_status gdr2_recurrent_varlen(const gdr2_problem* p, const int32_t* cu_seqlens, int32_t n_seqs,
+                                  const void* q, const void* k, const void* v, const float* log_alpha,
+                                  const void* b, const void* w, float* S, void* o, hipStream_t stream) {
+  if (n_seqs <= 0) return GDR2_EINVAL;
+  return recurrent(p, cu_seqlens, n_seqs, q, k, v, log_alpha, b, w, S, o, stream);
 }
 
 gdr2_status gdr2_profile_enable(int on) {

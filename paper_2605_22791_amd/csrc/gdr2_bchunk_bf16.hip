@@ -126,10 +126,15 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, r16 = lane & 15;
-  const int n = blockIdx.x, h = blockIdx.y, bb = blockIdx.z;
-  const int T = a.T, H = a.H, NT = a.NT;
-  const size_t ch = ((size_t)bb * H + h) * NT + n;
-  const size_t row0 = (size_t)bb * T + (size_t)n * CH;
+  ChunkPos cp;
+  if (!chunk_pos(a.vl, blockIdx.x, blockIdx.y, blockIdx.z, a.T, a.H, a.NT, cp)) return;
+  const int h = blockIdx.y, H = a.H;
+  const size_t ch = cp.ch, row0 = cp.row0;
+  // Rows in use.  Loads read in-range rows only (rows past a partial chunk's
+  // end re-read its last row); g, k and dO of those rows are then taken as
+  // zero, which makes every term they could add to a valid row vanish (their
+  // dT, dA_qk, dR and dG are zero), and their outputs are not written.
+  const int len = cp.len;
   const size_t KST = (size_t)H * DK, VST = (size_t)H * DV;  // token strides
   const size_t kb0 = row0 * KST + (size_t)h * DK, vb0 = row0 * VST + (size_t)h * DV;
   const int i = wave;  // the row block this wave owns
@@ -156,6 +161,8 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
 
   // staging role: chunk row grow (block = wave), channels 16 cb + 4 cq + (0..3)
   const int rl = lane >> 2, cq = lane & 3, grow = 16 * wave + rl;
+  const bool grin = grow < len;
+  const int growc = min(grow, len - 1);
   // h / dh staging role: row hc of the key block, values hv .. hv + 7
   const int hc = (8 * tid) / DV, hv = (8 * tid) % DV;
   const bool hact = tid < 2 * DV;
@@ -176,7 +183,7 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   bf8 dof[KV];
 #pragma unroll
   for (int p = 0; p < KV; ++p) {
-    const int o = (16 * i + r16) * vst + 32 * p + 4 * g;
+    const int o = (min(16 * i + r16, len - 1)) * vst + 32 * p + 4 * g;
     dof[p] = cat8(*reinterpret_cast<const bf4*>(dOp + o), *reinterpret_cast<const bf4*>(dOp + o + 16));
   }
   // R rows of block 0 (permuted K) for the first dT / dA_qk tile of waves 1..3
@@ -193,7 +200,7 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   bf4 pk, pb, pq;
 #define GDR2_PREFETCH(CB)                                                                  \
   {                                                                                        \
-    const int o_ = grow * kst + 16 * (CB) + 4 * cq;                                        \
+    const int o_ = growc * kst + 16 * (CB) + 4 * cq;                                       \
     pg = ldg_f4(Gp0 + o_);                                                                 \
     pk = *reinterpret_cast<const bf4*>(Kp + o_);                                           \
     pb = *reinterpret_cast<const bf4*>(Bp + o_);                                           \
@@ -211,6 +218,10 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   // block totals and first rows, k / b / q columns, h / dh rows, rowsum(dh * h).
 #define GDR2_STAGE(PAR)                                                                    \
   {                                                                                        \
+    if (!grin) {                                                                           \
+      pg = make_float4(0.f, 0.f, 0.f, 0.f);                                                \
+      pk = bf4{};                                                                          \
+    }                                                                                      \
     float x_[4] = {pg.x * kLog2e, pg.y * kLog2e, pg.z * kLog2e, pg.w * kLog2e};            \
     _Pragma("unroll") for (int o_ = 4; o_ < 64; o_ <<= 1) {                                \
       _Pragma("unroll") for (int u_ = 0; u_ < 4; ++u_) {                                   \
@@ -272,7 +283,7 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   bf4 vvr[NVB], wwr[NVB];
 #pragma unroll
   for (int vb = 0; vb < NVB; ++vb) {
-    const int o = (16 * i + r16) * vst + 16 * vb + 4 * g;
+    const int o = min(16 * i + r16, len - 1) * vst + 16 * vb + 4 * g;
     vvr[vb] = *reinterpret_cast<const bf4*>(Vp + o);
     wwr[vb] = *reinterpret_cast<const bf4*>(Wp + o);
   }
@@ -310,8 +321,10 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       odv[u] = (__bf16)(zacc[vb][u] * (float)wwr[vb][u]);
       odw[u] = (__bf16)(zacc[vb][u] * (float)vvr[vb][u]);
     }
-    *reinterpret_cast<bf4*>(dVp + o) = odv;
-    *reinterpret_cast<bf4*>(dWp + o) = odw;
+    if (16 * i + r16 < len) {
+      *reinterpret_cast<bf4*>(dVp + o) = odv;
+      *reinterpret_cast<bf4*>(dWp + o) = odw;
+    }
   }
   // dZ, dO and R rows of block i as A operands over the values, permuted K:
   // K-step p holds values 32 p + 4 g + (0..3) and 32 p + 16 + 4 g + (0..3)
@@ -328,6 +341,10 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     rfr[p] = split_f44(rraw[2 * p], rraw[2 * p + 1]);
   }
   __syncthreads();  // dR and A are dead
+  if (16 * i + r16 >= len) {
+#pragma unroll
+    for (int p = 0; p < KV; ++p) dof[p] = bf8{};
+  }
 
   // ---- dT = -tril(dZ R^T, -1) and dA_qk = tril(scale dO R^T), tiles (i, j <= i),
   //      stored transposed: plane[s][r].  The R rows of block j + 1 are in flight
@@ -511,9 +528,11 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
         }
       }
       const int o = (rb + u) * kst + c;
-      dQp[o] = (__bf16)dq;
-      dKp[o] = (__bf16)(dEg * bv + dKg);
-      dBp[o] = (__bf16)(dEg * kv);
+      if (rb + u < len) {
+        dQp[o] = (__bf16)dq;
+        dKp[o] = (__bf16)(dEg * bv + dKg);
+        dBp[o] = (__bf16)(dEg * kv);
+      }
       dgl[u] = dq * qv - dKg * kv + dEg * bv * kv;
       tailp += x3[u] * kv * tl;
     }
@@ -542,10 +561,10 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       off += sTL[(par * 4 + i2) * 16 + r16];
       if (i2 > i) off += sBT[(par * 4 + i2) * 16 + r16];
     }
-    dGp[(rb + 0) * kst + c] = s0 + off;
-    dGp[(rb + 1) * kst + c] = s1 + off;
-    dGp[(rb + 2) * kst + c] = s2 + off;
-    dGp[(rb + 3) * kst + c] = s3 + off;
+    if (rb + 0 < len) dGp[(rb + 0) * kst + c] = s0 + off;
+    if (rb + 1 < len) dGp[(rb + 1) * kst + c] = s1 + off;
+    if (rb + 2 < len) dGp[(rb + 2) * kst + c] = s2 + off;
+    if (rb + 3 < len) dGp[(rb + 3) * kst + c] = s3 + off;
     if (cb + 1 < NCB) GDR2_STAGE(par ^ 1)
     __syncthreads();
   }
@@ -559,7 +578,7 @@ hipError_t launch_bchunk_bf16(const BChunkBf16Args& a, hipStream_t st) {
   const void* fn = reinterpret_cast<const void*>(&bchunk_bf16_kernel<DK, DV>);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
   if (e != hipSuccess) return e;
-  dim3 grid(a.NT, a.H, a.B);
+  dim3 grid(a.vl.ct0 ? a.vl.ncmax : a.NT, a.H, a.vl.ct0 ? 1 : a.B);
   hipLaunchKernelGGL((bchunk_bf16_kernel<DK, DV>), grid, dim3(C::NTHR), C::LDS, st, a);
   return hipGetLastError();
 }

@@ -83,11 +83,12 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
     vs = blockIdx.x / NS;
     slice = blockIdx.x % NS;
   }
-  const int seq = vs / nseg, seg = vs % nseg;
-  const int seg_len = a.seg_len > 0 ? a.seg_len : NT;
-  const int n0 = seg * seg_len, n1 = min(NT, n0 + seg_len);
+  const int seq = vs / nseg, seg = vs % nseg;  // seq = (sequence, head) pair, sequence-major
+  const ScanRange rng = scan_range(a.vl, seq, H, NT);
+  const int seg_len = a.seg_len > 0 ? a.seg_len : rng.c1 - rng.c0;
+  const int n0 = rng.c0 + seg * seg_len, n1 = min(rng.c1, n0 + seg_len);
   const bool no_input = (a.flags & kScanNoInput) != 0;
-  const int bb = seq / H, h = seq % H;
+  const int h = seq % H;
   const int v0 = slice * DVS;
   const __bf16* dO = reinterpret_cast<const __bf16*>(a.dout);
 
@@ -99,7 +100,7 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
   // ---- staging: operand blocks, the dO slice and gamma_C of one chunk
   u4v stg[NSTG], sto;
   float gcur[4], gnext[4];
-  const size_t chs = (size_t)seq * NT;
+  const size_t chs = rng.chs;
 #define GDR2_LOAD_CHUNK(N_)                                                                               \
   {                                                                                                    \
     const size_t chx = chs + (N_);                                                                     \
@@ -116,9 +117,12 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
       stg[m] = ldg16(src + 16 * tid);                                                                  \
     }                                                                                                  \
     const int r_ = tid / (DVS / 8), c8_ = (tid % (DVS / 8)) * 8;                                       \
-    sto = no_input ? u4v{0u, 0u, 0u, 0u}                                                              \
-                   : ldg16(dO + ((size_t)bb * T + (size_t)(N_) * CH + r_) * ((size_t)H * DV) + (size_t)h * DV + \
-                           v0 + c8_);                                                                  \
+    size_t orow_;                                                                                      \
+    int olen_;                                                                                         \
+    scan_rows(a.vl, seq, H, T, (N_), orow_, olen_);                                                    \
+    sto = (no_input || r_ >= olen_)                                                                    \
+              ? u4v{0u, 0u, 0u, 0u}                                                                    \
+              : ldg16(dO + (orow_ + r_) * ((size_t)H * DV) + (size_t)h * DV + v0 + c8_);               \
     _Pragma("unroll") for (int u2 = 0; u2 < 4; ++u2) gnext[u2] =                                       \
         a.GC[chx * (WsBf16::gc(DK) / 4) + 16 * cs + 4 * g + u2];                                       \
   }

@@ -35,7 +35,8 @@ __global__ __launch_bounds__(256) void bwd_state_kernel(BwdStateArgs<TIn> a) {
   const int lr = lane & 15, lg = lane >> 4;
   const int T = a.T, H = a.H, NT = a.NT;
   const int v0 = vs * DVS;
-  const size_t seq = (size_t)bb * H + h;
+  const size_t seq = (size_t)bb * H + h;  // (sequence, head) pair
+  const ScanRange rng = scan_range(a.vl, (int)seq, H, NT);
 
   __shared__ float sdS[DK * LSS];
   __shared__ float sdO[CH * LSS];
@@ -47,18 +48,20 @@ __global__ __launch_bounds__(256) void bwd_state_kernel(BwdStateArgs<TIn> a) {
   }
   __syncthreads();
 
-  for (int n = NT - 1; n >= 0; --n) {
-    const size_t ch = seq * NT + n;
+  for (int n = rng.c1 - 1; n >= rng.c0; --n) {
+    const size_t ch = rng.chs + n;
     const float* Qg = a.Qg + ch * CH * DK;
     const float* Kt = a.Kt + ch * CH * DK;
     const float* Y = a.Y + ch * CH * DK;
     const float* Aqk = a.Aqk + ch * CH * CH;
     const float* GC = a.GC + ch * DK;
-    const size_t orow0 = (size_t)bb * T + (size_t)n * CH;
+    size_t orow0;
+    int olen;
+    scan_rows(a.vl, (int)seq, H, T, n, orow0, olen);
 
     for (int e = tid; e < CH * DVS; e += NTHR) {
       const int r = e / DVS, v = e % DVS;
-      sdO[r * LSS + v] = a.scale * to_f(a.dout[((orow0 + r) * H + h) * DV + v0 + v]);
+      sdO[r * LSS + v] = a.scale * to_fz(a.dout + ((orow0 + r) * H + h) * DV + v0 + v, r < olen);
     }
     {
       float* DHn = a.DH + ch * DK * DV;
@@ -156,15 +159,18 @@ template <int DK, int DV, typename TIn>
 __global__ __launch_bounds__(512) void bwd_wy_kernel(BwdChunkArgs<TIn> a) {
   constexpr int NTHR = 512, NW = 8;
   constexpr int LS = DK + 4;
-  const int n = blockIdx.x, h = blockIdx.y, bb = blockIdx.z;
+  ChunkPos cp;
+  if (!chunk_pos(a.vl, blockIdx.x, blockIdx.y, blockIdx.z, a.T, a.H, a.NT, cp)) return;
+  const int h = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
-  const int T = a.T, H = a.H, NT = a.NT;
+  const int H = a.H;
   const size_t rs = (size_t)H * DK, rsv = (size_t)H * DV;
-  const size_t row0 = (size_t)bb * T + (size_t)n * CH;
+  const size_t row0 = cp.row0;
+  const int len = cp.len;  // rows in use: the rest read as zero and are not written
   const size_t kbase = row0 * rs + (size_t)h * DK;
   const size_t vbase = row0 * rsv + (size_t)h * DV;
-  const size_t ch = ((size_t)bb * H + h) * NT + n;
+  const size_t ch = cp.ch;
 
   extern __shared__ float smem[];
   float* sR0 = smem;                // G, later X = A^T dA (LD64)
@@ -188,12 +194,12 @@ __global__ __launch_bounds__(512) void bwd_wy_kernel(BwdChunkArgs<TIn> a) {
   float* DEg = a.DEg + ch * CH * DK;
 
   if (tid < 4) unsafe[tid] = 0;
-  chunk_cumsum<DK, NTHR>(a.g + kbase, rs, sG, tid);
+  chunk_cumsum<DK, NTHR>(a.g + kbase, rs, sG, tid, len);
   chunk_refs<DK, NTHR>(sG, eP, brg, eGC, unsafe, tid);
   for (int e = tid; e < CH * DK / 4; e += NTHR) {
     const int r = e / (DK / 4), c4 = (e % (DK / 4)) * 4, i = r >> 4;
-    const float4 kk = ld4(a.k + kbase + r * rs + c4);
-    const float4 bv = ld4(a.b + kbase + r * rs + c4);
+    const float4 kk = ld4z(a.k + kbase + r * rs + c4, r < len);
+    const float4 bv = ld4z(a.b + kbase + r * rs + c4, r < len);
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int c = c4 + u;
@@ -212,7 +218,7 @@ __global__ __launch_bounds__(512) void bwd_wy_kernel(BwdChunkArgs<TIn> a) {
       pair_of(it, i, j);
       const f4 acc = (i == j && unsafe[i])
                          ? diag_tile_direct<DK, TIn>(a.b + kbase, a.k + kbase, a.k + kbase,
-                                                     a.g + kbase, rs, i, lane, true)
+                                                     a.g + kbase, rs, i, lane, true, len)
                          : gram_tile<DK>(sLe, sRk, brg + pair_index(i, j) * DK, i, j, lane);
       const int s = 16 * j + lr;
 #pragma unroll
@@ -225,9 +231,10 @@ __global__ __launch_bounds__(512) void bwd_wy_kernel(BwdChunkArgs<TIn> a) {
       f4 acc = {0.f, 0.f, 0.f, 0.f};
       if (j <= i) {
         const TIn* pd = a.dout + vbase + (16 * i + lr) * rsv + 4 * lg;
+        const bool pdin = 16 * i + lr < len;
         const float* pr = Rn + (16 * j + lr) * DV + 4 * lg;
         for (int kk = 0; kk < DV; kk += 16) {
-          const float4 dv4 = ld4(pd + kk), r4 = ld4(pr + kk);
+          const float4 dv4 = ld4z(pd + kk, pdin), r4 = ld4(pr + kk);
           acc = mfma4(dv4.x, r4.x, acc);
           acc = mfma4(dv4.y, r4.y, acc);
           acc = mfma4(dv4.z, r4.z, acc);
@@ -283,8 +290,10 @@ __global__ __launch_bounds__(512) void bwd_wy_kernel(BwdChunkArgs<TIn> a) {
       const int s = 16 * i + 4 * lg + u;
       if (isZ) {
         const size_t off = vbase + s * rsv + col;
-        put(a.dw + off, acc[u] * to_f(a.v[off]));
-        put(a.dv + off, acc[u] * to_f(a.w[off]));
+        if (s < len) {
+          put(a.dw + off, acc[u] * to_f(a.v[off]));
+          put(a.dv + off, acc[u] * to_f(a.w[off]));
+        }
       } else {
         DEg[s * DK + col] = acc[u] * expf(sG[s * LS + col]);
       }
@@ -300,8 +309,9 @@ __global__ __launch_bounds__(512) void bwd_wy_kernel(BwdChunkArgs<TIn> a) {
       const float* pa = DRn + (16 * i + lr) * DV + 4 * lg;
       const TIn* pw = a.w + vbase + (16 * j + lr) * rsv + 4 * lg;
       const TIn* pv = a.v + vbase + (16 * j + lr) * rsv + 4 * lg;
+      const bool jin = 16 * j + lr < len;
       for (int kk = 0; kk < DV; kk += 16) {
-        const float4 x = ld4(pa + kk), w4 = ld4(pw + kk), v4 = ld4(pv + kk);
+        const float4 x = ld4(pa + kk), w4 = ld4z(pw + kk, jin), v4 = ld4z(pv + kk, jin);
         acc = mfma4(x.x, w4.x * v4.x, acc);
         acc = mfma4(x.y, w4.y * v4.y, acc);
         acc = mfma4(x.z, w4.z * v4.z, acc);
@@ -375,15 +385,18 @@ __global__ __launch_bounds__(512) void bwd_intra_kernel(BwdChunkArgs<TIn> a) {
   constexpr int IPW = NITEM / NW;
   constexpr int NSPLIT = NTHR / DK;
   static_assert(NITEM % NW == 0, "items per wave");
-  const int n = blockIdx.x, h = blockIdx.y, bb = blockIdx.z;
+  ChunkPos cp;
+  if (!chunk_pos(a.vl, blockIdx.x, blockIdx.y, blockIdx.z, a.T, a.H, a.NT, cp)) return;
+  const int h = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
-  const int T = a.T, H = a.H, NT = a.NT;
+  const int H = a.H;
   const size_t rs = (size_t)H * DK, rsv = (size_t)H * DV;
-  const size_t row0 = (size_t)bb * T + (size_t)n * CH;
+  const size_t row0 = cp.row0;
+  const int len = cp.len;  // rows in use: the rest read as zero and are not written
   const size_t kbase = row0 * rs + (size_t)h * DK;
   const size_t vbase = row0 * rsv + (size_t)h * DV;
-  const size_t ch = ((size_t)bb * H + h) * NT + n;
+  const size_t ch = cp.ch;
 
   extern __shared__ float smem[];
   float* sG = smem;
@@ -406,13 +419,13 @@ __global__ __launch_bounds__(512) void bwd_intra_kernel(BwdChunkArgs<TIn> a) {
   const float* DEg = a.DEg + ch * CH * DK;
 
   if (tid < 4) unsafe[tid] = 0;
-  chunk_cumsum<DK, NTHR>(a.g + kbase, rs, sG, tid);
+  chunk_cumsum<DK, NTHR>(a.g + kbase, rs, sG, tid, len);
   chunk_refs<DK, NTHR>(sG, eP, brg, eGC, unsafe, tid);
   for (int e = tid; e < CH * DK / 4; e += NTHR) {
     const int r = e / (DK / 4), c4 = (e % (DK / 4)) * 4, i = r >> 4;
-    const float4 kk = ld4(a.k + kbase + r * rs + c4);
-    const float4 bv = ld4(a.b + kbase + r * rs + c4);
-    const float4 qq = ld4(a.q + kbase + r * rs + c4);
+    const float4 kk = ld4z(a.k + kbase + r * rs + c4, r < len);
+    const float4 bv = ld4z(a.b + kbase + r * rs + c4, r < len);
+    const float4 qq = ld4z(a.q + kbase + r * rs + c4, r < len);
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int c = c4 + u;
@@ -470,11 +483,12 @@ __global__ __launch_bounds__(512) void bwd_intra_kernel(BwdChunkArgs<TIn> a) {
     // dQs = dO S0^T and dKt = R dS_C^T
     {
       const TIn* pd = a.dout + vbase + (16 * i + lr) * rsv + 4 * lg;
+      const bool pdin = 16 * i + lr < len;
       const float* pr = Rn + (16 * i + lr) * DV + 4 * lg;
       const float* ph = Hn + (16 * cb + lr) * DV + 4 * lg;
       const float* pdh = DHn + (16 * cb + lr) * DV + 4 * lg;
       for (int kk = 0; kk < DV; kk += 16) {
-        const float4 x = ld4(pd + kk), y = ld4(ph + kk);
+        const float4 x = ld4z(pd + kk, pdin), y = ld4(ph + kk);
         const float4 rr = ld4(pr + kk), z = ld4(pdh + kk);
         dQs = mfma4(x.x, y.x, dQs);
         dQs = mfma4(x.y, y.y, dQs);
@@ -496,7 +510,8 @@ __global__ __launch_bounds__(512) void bwd_intra_kernel(BwdChunkArgs<TIn> a) {
       const float gam = expf(G);
       const float tail = expf(sG[(CH - 1) * LS + c] - G);
       const size_t off = kbase + r * rs + c;
-      const float kv = to_f(a.k[off]), bv = to_f(a.b[off]), qv = to_f(a.q[off]);
+      const bool rin = r < len;
+      const float kv = to_fz(a.k + off, rin), bv = to_fz(a.b + off, rin), qv = to_fz(a.q + off, rin);
       float dEg = DEg[r * DK + c] + lf * P1[u];
       float dq = a.scale * gam * dQs[u] + lf * P2[u];
       float dKg = rf * P3[u] + tail * dKt[u];
@@ -506,20 +521,22 @@ __global__ __launch_bounds__(512) void bwd_intra_kernel(BwdChunkArgs<TIn> a) {
           const float Gs = sG[s * LS + c];
           if (s <= r) {
             const float e = expf(G - Gs);   // r >= s: <= 1
-            const float ks = to_f(a.k[so]);
+            const float ks = to_fz(a.k + so, s < len);
             if (s < r) dEg += DT[r * CH + s] * ks * e;
             dq += DAqk[r * CH + s] * ks * e;
           }
           if (s >= r) {
             const float e = expf(Gs - G);   // s >= r: <= 1
-            if (s > r) dKg += DT[s * CH + r] * to_f(a.b[so]) * to_f(a.k[so]) * e;
-            dKg += DAqk[s * CH + r] * to_f(a.q[so]) * e;
+            if (s > r) dKg += DT[s * CH + r] * to_fz(a.b + so, s < len) * to_fz(a.k + so, s < len) * e;
+            dKg += DAqk[s * CH + r] * to_fz(a.q + so, s < len) * e;
           }
         }
       }
-      put(a.db + off, dEg * kv);
-      put(a.dk + off, dEg * bv + dKg);
-      put(a.dq + off, dq);
+      if (rin) {
+        put(a.db + off, dEg * kv);
+        put(a.dk + off, dEg * bv + dKg);
+        put(a.dq + off, dq);
+      }
       keep[q][u] = dq * qv - dKg * kv + dEg * bv * kv;
       tailpart += dKt[u] * kv * tail;
     }
@@ -559,7 +576,7 @@ __global__ __launch_bounds__(512) void bwd_intra_kernel(BwdChunkArgs<TIn> a) {
     for (int s = seg + 1; s < NSEG; ++s) off += sdG[(s * RPS) * LS + c];
     __syncthreads();
     for (int r = seg * RPS; r < (seg + 1) * RPS; ++r)
-      a.dg[kbase + r * rs + c] = sdG[r * LS + c] + off;
+      if (r < len) a.dg[kbase + r * rs + c] = sdG[r * LS + c] + off;
   }
 }
 
@@ -578,7 +595,7 @@ hipError_t launch_bwd_wy(const BwdChunkArgs<TIn>& a, int B, hipStream_t st) {
   hipError_t e = hipFuncSetAttribute((const void*)bwd_wy_kernel<DK, DV, TIn>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  dim3 grid(a.NT, a.H, B);
+  dim3 grid(a.vl.ct0 ? a.vl.ncmax : a.NT, a.H, a.vl.ct0 ? 1 : B);
   hipLaunchKernelGGL((bwd_wy_kernel<DK, DV, TIn>), grid, dim3(512), lds, st, a);
   return hipGetLastError();
 }
@@ -590,7 +607,7 @@ hipError_t launch_bwd_intra(const BwdChunkArgs<TIn>& a, int B, hipStream_t st) {
   hipError_t e = hipFuncSetAttribute((const void*)bwd_intra_kernel<DK, DV, TIn>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  dim3 grid(a.NT, a.H, B);
+  dim3 grid(a.vl.ct0 ? a.vl.ncmax : a.NT, a.H, a.vl.ct0 ? 1 : B);
   hipLaunchKernelGGL((bwd_intra_kernel<DK, DV, TIn>), grid, dim3(512), lds, st, a);
   return hipGetLastError();
 }

@@ -64,6 +64,15 @@ __device__ __forceinline__ float4 ld4(const bf16_t* p) {
   return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
                      __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
 }
+// ld4 / to_f of a token row that may lie past a partial chunk's end (then 0)
+template <typename T>
+__device__ __forceinline__ float4 ld4z(const T* p, bool ok) {
+  return ok ? ld4(p) : make_float4(0.f, 0.f, 0.f, 0.f);
+}
+template <typename T>
+__device__ __forceinline__ float to_fz(const T* p, bool ok) {
+  return ok ? to_f(*p) : 0.f;
+}
 __device__ __forceinline__ float f4at(const float4& v, int u) {
   return u == 0 ? v.x : (u == 1 ? v.y : (u == 2 ? v.z : v.w));
 }
@@ -78,13 +87,14 @@ __device__ __forceinline__ void pair_of(int p, int& i, int& j) {
 // Chunk-local cumulative log-decay G_r = sum_{i<=r} g_i (eq. eq_gdn2_gamma),
 // computed in fp32 from the fp32 log-decay (App. D.1).  g points at row 0,
 // channel 0 of the chunk for one head; rs is the row stride in elements.
-// Result in sG[r * (DK+4) + c].  All threads of the block must call it.
+// Result in sG[r * (DK+4) + c]; rows r >= len (past a partial chunk's end)
+// count as g = 0.  All threads of the block must call it.
 template <int DK, int NTHR>
-__device__ void chunk_cumsum(const float* __restrict__ g, size_t rs, float* sG, int tid) {
+__device__ void chunk_cumsum(const float* __restrict__ g, size_t rs, float* sG, int tid, int len) {
   constexpr int LG = DK + 4;
   for (int e = tid; e < CH * DK / 4; e += NTHR) {
     const int r = e / (DK / 4), c4 = (e % (DK / 4)) * 4;
-    const float4 x = ld4(g + r * rs + c4);
+    const float4 x = ld4z(g + r * rs + c4, r < len);
     float* d = sG + r * LG + c4;
     d[0] = x.x; d[1] = x.y; d[2] = x.z; d[3] = x.w;
   }
@@ -157,31 +167,31 @@ __device__ __forceinline__ f4 gram_tile(const float* L, const float* R, const fl
 // block): out[m][n] = sum_c X[r][c] * k[s][c] * exp(G_r - G_s), r = 16i+m,
 // s = 16i+n, for r >= s (strict when `strict`), else 0.  X = b*k (Gram T) or
 // q (scores).  Reads the raw inputs; G differences are accumulated locally
-// from g so they never leave the block.
+// from g so they never leave the block.  Rows >= len read as zero.
 template <int DK, typename TIn>
 __device__ f4 diag_tile_direct(const TIn* __restrict__ x1, const TIn* __restrict__ x2,
                                const TIn* __restrict__ k, const float* __restrict__ g,
-                               size_t rs, int i, int lane, bool strict) {
+                               size_t rs, int i, int lane, bool strict, int len) {
   f4 acc = {0.f, 0.f, 0.f, 0.f};
   const int n = lane & 15, mb = 4 * (lane >> 4);
   const int s = 16 * i + n;
   for (int c = 0; c < DK; ++c) {
     float run = 0.f, Gs = 0.f, Gr[4] = {0.f, 0.f, 0.f, 0.f};
     for (int t = 0; t < 16; ++t) {
-      run += g[(16 * i + t) * rs + c];
+      run += to_fz(g + (16 * i + t) * rs + c, 16 * i + t < len);
       if (t == n) Gs = run;
 #pragma unroll
       for (int u = 0; u < 4; ++u)
         if (t == mb + u) Gr[u] = run;
     }
-    const float ks = to_f(k[s * rs + c]);
+    const float ks = to_fz(k + s * rs + c, s < len);
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int m = mb + u;
       if (m > n || (!strict && m == n)) {
         const int r = 16 * i + m;
-        float xv = to_f(x1[r * rs + c]);
-        if (x2) xv *= to_f(x2[r * rs + c]);
+        float xv = to_fz(x1 + r * rs + c, r < len);
+        if (x2) xv *= to_fz(x2 + r * rs + c, r < len);
         acc[u] += xv * ks * expf(Gr[u] - Gs);
       }
     }

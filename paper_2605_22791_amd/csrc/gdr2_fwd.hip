@@ -27,14 +27,17 @@ template <int DK, int DV, typename TIn>
 __global__ __launch_bounds__(512) void fwd_intra_kernel(IntraArgs<TIn> a) {
   constexpr int NTHR = 512;
   constexpr int LS = DK + 4;
-  const int n = blockIdx.x, h = blockIdx.y, bb = blockIdx.z;
+  ChunkPos cp;
+  if (!chunk_pos(a.vl, blockIdx.x, blockIdx.y, blockIdx.z, a.T, a.H, a.NT, cp)) return;
+  const int h = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int T = a.T, H = a.H, NT = a.NT;
+  const int H = a.H;
   const size_t rs = (size_t)H * DK, rsv = (size_t)H * DV;
-  const size_t row0 = (size_t)bb * T + (size_t)n * CH;
+  const size_t row0 = cp.row0;
+  const int len = cp.len;  // rows in use: the rest read as zero and are not written
   const size_t kbase = row0 * rs + (size_t)h * DK;
   const size_t vbase = row0 * rsv + (size_t)h * DV;
-  const size_t ch = ((size_t)bb * H + h) * NT + n;
+  const size_t ch = cp.ch;
 
   extern __shared__ float smem[];
   float* sR0 = smem;                      // G (64 x LS), later T (64 x LD64)
@@ -50,7 +53,7 @@ __global__ __launch_bounds__(512) void fwd_intra_kernel(IntraArgs<TIn> a) {
   float* sT = sR0;
 
   if (tid < 4) unsafe[tid] = 0;
-  chunk_cumsum<DK, NTHR>(a.g + kbase, rs, sG, tid);
+  chunk_cumsum<DK, NTHR>(a.g + kbase, rs, sG, tid, len);
   chunk_refs<DK, NTHR>(sG, eP, brg, eGC, unsafe, tid);
 
   // gate-absorbed tiles; Qg and Ktail go straight to the workspace
@@ -58,9 +61,9 @@ __global__ __launch_bounds__(512) void fwd_intra_kernel(IntraArgs<TIn> a) {
   float* Kt = a.Kt + ch * CH * DK;
   for (int e = tid; e < CH * DK / 4; e += NTHR) {
     const int r = e / (DK / 4), c4 = (e % (DK / 4)) * 4, i = r >> 4;
-    const float4 kk = ld4(a.k + kbase + r * rs + c4);
-    const float4 bv = ld4(a.b + kbase + r * rs + c4);
-    const float4 qq = ld4(a.q + kbase + r * rs + c4);
+    const float4 kk = ld4z(a.k + kbase + r * rs + c4, r < len);
+    const float4 bv = ld4z(a.b + kbase + r * rs + c4, r < len);
+    const float4 qq = ld4z(a.q + kbase + r * rs + c4, r < len);
     float4 qg, kt;
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
@@ -92,8 +95,8 @@ __global__ __launch_bounds__(512) void fwd_intra_kernel(IntraArgs<TIn> a) {
     pair_of(isT ? it : it - 10, i, j);
     f4 acc;
     if (i == j && unsafe[i]) {
-      acc = isT ? diag_tile_direct<DK, TIn>(a.b + kbase, a.k + kbase, a.k + kbase, a.g + kbase, rs, i, lane, true)
-                : diag_tile_direct<DK, TIn>(a.q + kbase, nullptr, a.k + kbase, a.g + kbase, rs, i, lane, false);
+      acc = isT ? diag_tile_direct<DK, TIn>(a.b + kbase, a.k + kbase, a.k + kbase, a.g + kbase, rs, i, lane, true, len)
+                : diag_tile_direct<DK, TIn>(a.q + kbase, nullptr, a.k + kbase, a.g + kbase, rs, i, lane, false, len);
     } else {
       acc = gram_tile<DK>(isT ? sLe : sLq, sRk, brg + pair_index(i, j) * DK, i, j, lane);
     }
@@ -122,8 +125,8 @@ __global__ __launch_bounds__(512) void fwd_intra_kernel(IntraArgs<TIn> a) {
   constexpr int LZ = DV + 4;
   for (int e = tid; e < CH * DV / 4; e += NTHR) {
     const int r = e / (DV / 4), c4 = (e % (DV / 4)) * 4;
-    const float4 wv = ld4(a.w + vbase + r * rsv + c4);
-    const float4 vv = ld4(a.v + vbase + r * rsv + c4);
+    const float4 wv = ld4z(a.w + vbase + r * rsv + c4, r < len);
+    const float4 vv = ld4z(a.v + vbase + r * rsv + c4, r < len);
     float* d = sZ + r * LZ + c4;
     d[0] = wv.x * vv.x; d[1] = wv.y * vv.y; d[2] = wv.z * vv.z; d[3] = wv.w * vv.w;
   }
@@ -184,7 +187,8 @@ __global__ __launch_bounds__(256) void fwd_state_kernel(StateArgs<TIn> a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int T = a.T, H = a.H, NT = a.NT;
   const int v0 = vs * DVS;
-  const size_t seq = (size_t)bb * H + h;
+  const size_t seq = (size_t)bb * H + h;  // (sequence, head) pair
+  const ScanRange rng = scan_range(a.vl, (int)seq, H, NT);
 
   __shared__ float sS[DK * LSS];
   __shared__ float sR[CH * LSS];
@@ -196,8 +200,8 @@ __global__ __launch_bounds__(256) void fwd_state_kernel(StateArgs<TIn> a) {
   __syncthreads();
 
   const int lr = lane & 15, lg = lane >> 4;
-  for (int n = 0; n < NT; ++n) {
-    const size_t ch = seq * NT + n;
+  for (int n = rng.c0; n < rng.c1; ++n) {
+    const size_t ch = rng.chs + n;
     const float* Y = a.Y + ch * CH * DK;
     const float* U = a.U + ch * CH * DV;
     const float* Kt = a.Kt + ch * CH * DK;
@@ -273,13 +277,15 @@ __global__ __launch_bounds__(256) void fwd_state_kernel(StateArgs<TIn> a) {
           acc[vb] = mfma4(av.w, sR[(s0 + 3) * LSS + 16 * vb + lr], acc[vb]);
         }
       }
-      const size_t orow0 = (size_t)bb * T + (size_t)n * CH;
+      size_t orow0;
+      int olen;
+      scan_rows(a.vl, (int)seq, H, T, n, orow0, olen);
 #pragma unroll
       for (int vb = 0; vb < NVB; ++vb)
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const int r = 16 * i + 4 * lg + u;
-          put(a.o + ((orow0 + r) * H + h) * DV + v0 + 16 * vb + lr, a.scale * acc[vb][u]);
+          if (r < olen) put(a.o + ((orow0 + r) * H + h) * DV + v0 + 16 * vb + lr, a.scale * acc[vb][u]);
         }
     }
 
@@ -335,7 +341,7 @@ hipError_t launch_fwd_intra(const IntraArgs<TIn>& a, int B, hipStream_t st) {
   hipError_t e = hipFuncSetAttribute((const void*)fwd_intra_kernel<DK, DV, TIn>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  dim3 grid(a.NT, a.H, B);
+  dim3 grid(a.vl.ct0 ? a.vl.ncmax : a.NT, a.H, a.vl.ct0 ? 1 : B);
   hipLaunchKernelGGL((fwd_intra_kernel<DK, DV, TIn>), grid, dim3(512), lds, st, a);
   return hipGetLastError();
 }

@@ -93,18 +93,26 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, r16 = lane & 15;
-  const int n = blockIdx.x, h = blockIdx.y, bb = blockIdx.z;
-  const int T = a.T, H = a.H, NT = a.NT;
-  const size_t ch = ((size_t)bb * H + h) * NT + n;
+  ChunkPos cp;
+  if (!chunk_pos(a.vl, blockIdx.x, blockIdx.y, blockIdx.z, a.T, a.H, a.NT, cp)) return;
+  const int h = blockIdx.y, H = a.H;
+  const size_t ch = cp.ch;
+  // Rows in use.  Every load below reads an in-range row (rows past a partial
+  // chunk's end re-read its last row); g, k and v of those rows are then taken
+  // as zero, which makes their T / A_qk entries, Ebar, Z, Ktail and decay
+  // vanish, so they add nothing to the valid rows or the state.  Their q, b and
+  // w only reach outputs of those rows, which nobody reads.
+  const int len = cp.len;
+  const u4v z16 = {0u, 0u, 0u, 0u};
 
   const __bf16* Q = reinterpret_cast<const __bf16*>(a.q);
   const __bf16* K = reinterpret_cast<const __bf16*>(a.k);
   const __bf16* Vg = reinterpret_cast<const __bf16*>(a.v);
   const __bf16* Bg = reinterpret_cast<const __bf16*>(a.b);
   const __bf16* Wg = reinterpret_cast<const __bf16*>(a.w);
-  const size_t row0 = (size_t)bb * T + (size_t)n * CH;
-  auto kofs = [&](int r) -> size_t { return (row0 + r) * ((size_t)H * DK) + (size_t)h * DK; };
-  auto vofs = [&](int r) -> size_t { return (row0 + r) * ((size_t)H * DV) + (size_t)h * DV; };
+  const size_t row0 = cp.row0;
+  auto kofs = [&](int r) -> size_t { return (row0 + min(r, len - 1)) * ((size_t)H * DK) + (size_t)h * DK; };
+  auto vofs = [&](int r) -> size_t { return (row0 + min(r, len - 1)) * ((size_t)H * DV) + (size_t)h * DV; };
 
   // ---- loads: g in scan layout (NG rows of 4 channels per thread), k
   constexpr int GCG = DK / 4, GSEG = 256 / GCG, NG = 64 / GSEG;
@@ -148,6 +156,7 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
     float4 run = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
     for (int m = 0; m < NG; ++m) {
+      if (NG * gsg + m >= len) gr[m] = make_float4(0.f, 0.f, 0.f, 0.f);
       run.x += gr[m].x * kLog2e; run.y += gr[m].y * kLog2e;
       run.z += gr[m].z * kLog2e; run.w += gr[m].w * kLog2e;
       gr[m] = run;
@@ -156,7 +165,7 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
 #pragma unroll
     for (int m = 0; m < NKC; ++m) {
       const int e = tid + 256 * m, r = e / (DK / 8), c8 = (e % (DK / 8)) * 8;
-      sts16(sK + r * LKB + c8, kst[m]);
+      sts16(sK + r * LKB + c8, r < len ? kst[m] : z16);
     }
     __syncthreads();
     float4 off = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -446,7 +455,7 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
 #pragma unroll
   for (int m = 0; m < NVC; ++m) {
     const int e = tid + 256 * m, r = e / (DV / 8), c8 = (e % (DV / 8)) * 8;
-    sts16(sV + r * LVW + c8, vst[m]);
+    sts16(sV + r * LVW + c8, r < len ? vst[m] : u4v{0u, 0u, 0u, 0u});
     sts16(sW + r * LVW + c8, wst[m]);
   }
   __syncthreads();
@@ -487,7 +496,7 @@ hipError_t launch_intra_bf16(const IntraBf16Args& a, hipStream_t st) {
   const void* fn = reinterpret_cast<const void*>(&intra_bf16_kernel<DK, DV>);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
   if (e != hipSuccess) return e;
-  dim3 grid(a.NT, a.H, a.B);
+  dim3 grid(a.vl.ct0 ? a.vl.ncmax : a.NT, a.H, a.vl.ct0 ? 1 : a.B);
   hipLaunchKernelGGL((intra_bf16_kernel<DK, DV>), grid, dim3(C::NTHR), C::LDS, st, a);
   return hipGetLastError();
 }

@@ -5,6 +5,66 @@
 
 namespace gdr2 {
 
+// Token placement of the chunks.  Fixed-length calls: sequence bb holds T
+// tokens in NT = ceil(T / C) chunks (the last one partial when C does not
+// divide T) and chunk-head ch = (bb * H + h) * NT + n.  Packed variable-length
+// calls (App. C.6): B = 1, sequence s holds tokens cu[s] .. cu[s+1) and its
+// chunks are entries coff[s] .. coff[s+1) of a table built on the device from
+// cu_seqlens (first token ct0, rows clen <= C); ch = h * ncmax + c.  Rows of a
+// partial chunk past its length read as zero (log-decay 0) and are never
+// written: they add nothing to the chunk's products, its decay or the state.
+struct Varlen {
+  const int* cu = nullptr;    // cu_seqlens (nseq + 1); null: fixed-length call
+  const int* coff = nullptr;  // first chunk of every sequence; coff[nseq] = chunks in use
+  const int* ct0 = nullptr;   // first token of every chunk
+  const int* clen = nullptr;  // rows of every chunk (1 .. C)
+  int nseq = 0, ncmax = 0;    // sequences; chunk slots (grid and workspace extent)
+};
+
+struct ChunkPos {
+  size_t row0;  // token row of the chunk's first row (row = b * T + t)
+  int len;      // rows in use
+  size_t ch;    // chunk-head index
+};
+
+// Chunk x of a chunk-parallel grid (x < NT resp. ncmax, y = h, z = bb);
+// false for the unused tail of a packed grid (uniform per workgroup).
+__device__ __forceinline__ bool chunk_pos(const Varlen& vl, int x, int h, int bb, int T, int H, int NT,
+                                          ChunkPos& p) {
+  if (vl.ct0 != nullptr) {
+    if (x >= vl.coff[vl.nseq]) return false;
+    p.row0 = (size_t)vl.ct0[x];
+    p.len = vl.clen[x];
+    p.ch = (size_t)h * vl.ncmax + x;
+  } else {
+    p.row0 = (size_t)bb * T + (size_t)x * CH;
+    p.len = min(CH, T - x * CH);
+    p.ch = ((size_t)bb * H + h) * NT + x;
+  }
+  return true;
+}
+
+// Chunks of the scanned pair q = s * H + h (sequence s, head h): ch = chs + c
+// for c in [c0, c1).
+struct ScanRange {
+  size_t chs;
+  int c0, c1;
+};
+__device__ __forceinline__ ScanRange scan_range(const Varlen& vl, int q, int H, int NT) {
+  if (vl.coff != nullptr) return {(size_t)(q % H) * vl.ncmax, vl.coff[q / H], vl.coff[q / H + 1]};
+  return {(size_t)q * NT, 0, NT};
+}
+// First token row and rows in use of chunk c of the scanned pair q.
+__device__ __forceinline__ void scan_rows(const Varlen& vl, int q, int H, int T, int c, size_t& row0, int& len) {
+  if (vl.ct0 != nullptr) {
+    row0 = (size_t)vl.ct0[c];
+    len = vl.clen[c];
+  } else {
+    row0 = (size_t)(q / H) * T + (size_t)c * CH;
+    len = min(CH, T - c * CH);
+  }
+}
+
 // Arguments of the intra-chunk forward kernel.  Inputs use the operator's
 // token-major layouts; outputs are per-chunk-head workspace tiles, chunk-head
 // index ch = (b * H + h) * NT + n.
@@ -23,6 +83,7 @@ struct IntraArgs {
   float* Aqk;
   float* GC;
   int T, H, NT;
+  Varlen vl{};
 };
 
 // Arguments of the sequential forward state kernel.
@@ -41,6 +102,7 @@ struct StateArgs {
   float* Rs;        // R per chunk (backward recompute)
   int T, H, NT;
   float scale;
+  Varlen vl{};
 };
 
 // Reverse state scan of the backward (App. B.1).
@@ -58,6 +120,7 @@ struct BwdStateArgs {
   float* DR;         // dR per chunk
   int T, H, NT;
   float scale;
+  Varlen vl{};
 };
 
 // Chunk-parallel backward kernels (App. B.2 - B.5).
@@ -85,6 +148,7 @@ struct BwdChunkArgs {
   float* dg;
   int T, H, NT;
   float scale;
+  Varlen vl{};
 };
 
 // One recurrent (decode) call over T tokens, state updated in place.
@@ -100,6 +164,7 @@ struct RecurArgs {
   TIn* o;
   int T, H;
   float scale;
+  const int* cu = nullptr;  // packed sequences: tokens cu[s] .. cu[s+1) of sequence s (B = 1)
 };
 
 // ---------------------------------------------------------------------------
@@ -149,6 +214,7 @@ struct IntraBf16Args {
   float* GC;
   unsigned char* Am;  // nullable: A for the backward
   int B, T, H, NT;
+  Varlen vl{};
 };
 
 // Sequence-parallel scans: with nseg > 1 every sequence is cut into nseg
@@ -176,6 +242,7 @@ struct ScanArgs {
   const float* S0seg = nullptr;  // nullable: start state of every segment (B*H*nseg, Dk, DV)
   float* STseg = nullptr;        // nullable: end state of every segment (B*H*nseg, Dk, DV)
   int flags = 0;                 // ScanFlags
+  Varlen vl{};
 };
 
 struct BScanArgs {
@@ -195,6 +262,7 @@ struct BScanArgs {
   const float* dSseg_in = nullptr; // nullable: gradient at the end of every segment (B*H*nseg, Dk, DV)
   float* dSseg_out = nullptr;      // nullable: gradient at the start of every segment
   int flags = 0;                   // ScanFlags (kScanNoInput: dO = 0)
+  Varlen vl{};
 };
 
 // Chaining of segment maps: X <- M_k X + N_k over the segments of each sequence
@@ -232,6 +300,7 @@ struct BChunkBf16Args {
   float* dg;
   int B, T, H, NT;
   float scale;
+  Varlen vl{};
 };
 
 template <int DK, int DV>
@@ -257,5 +326,11 @@ template <int DK, int DV, typename TIn>
 hipError_t launch_bwd_intra(const BwdChunkArgs<TIn>& a, int B, hipStream_t st);
 template <int DK, int DV, typename TIn>
 hipError_t launch_recurrent(const RecurArgs<TIn>& a, int B, hipStream_t st);
+
+// Builds the chunk table of a packed call (Varlen) from cu_seqlens: lengths
+// are clamped into [0, T] and the chunk count to ncmax, so malformed offsets
+// cannot lead to accesses outside the tensors or the workspace.
+hipError_t launch_varlen_table(const int* cu, int nseq, int T, int ncmax, int* coff, int* ct0, int* clen,
+                               hipStream_t st);
 
 }  // namespace gdr2

@@ -1,6 +1,7 @@
 // Recurrent (token-by-token) GDR-2 forward for decoding, App. C.5.
 //
-// One workgroup per (batch, head).  The fp32 state (DK x DV) stays in registers
+// One workgroup per (batch, head), or per (sequence, head) of a packed batch
+// (App. C.6: the same cumulative-length layout as the chunk kernels).  The fp32 state (DK x DV) stays in registers
 // for all T tokens of the call: each thread owns RPG rows x 4 columns.  Per token
 //     Sbar = Diag(exp g) S,  r = Sbar^T (b*k),  S = Sbar + k (w*v - r)^T,
 //     o    = scale * S^T q = scale * (Sbar^T q + (w*v - r) (k . q)),
@@ -33,8 +34,16 @@ __global__ __launch_bounds__(256) void recurrent_kernel(RecurArgs<TIn> a) {
 #pragma unroll
   for (int i = 0; i < RPG; ++i) S[i] = ld4(Sg + (rg * RPG + i) * DV + 4 * cg);
 
-  for (int t = 0; t < T; ++t) {
-    const size_t row = ((size_t)bb * T + t) * H + h;
+  // tokens of this sequence: bb's T tokens, or cu[bb] .. cu[bb+1) of a packed batch (clamped into [0, T])
+  int t0 = 0, t1 = T;
+  size_t rbase = (size_t)bb * T;
+  if (a.cu != nullptr) {
+    t0 = min(max(a.cu[bb], 0), T);
+    t1 = min(max(a.cu[bb + 1], t0), T);
+    rbase = 0;
+  }
+  for (int t = t0; t < t1; ++t) {
+    const size_t row = (rbase + t) * H + h;
     float kq = 0.f;
     for (int c = tid; c < DK; c += NTHR) {
       const float kv = to_f(a.k[row * DK + c]), qv = to_f(a.q[row * DK + c]);

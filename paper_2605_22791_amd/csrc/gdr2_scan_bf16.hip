@@ -90,16 +90,14 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
     vs = blockIdx.x / NS;
     slice = blockIdx.x % NS;
   }
-  const int seq = vs / nseg, seg = vs % nseg;
-  const int seg_len = a.seg_len > 0 ? a.seg_len : NT;
-  const int n0 = seg * seg_len, n1 = min(NT, n0 + seg_len);
+  const int seq = vs / nseg, seg = vs % nseg;  // seq = (sequence, head) pair, sequence-major
+  const ScanRange rng = scan_range(a.vl, seq, H, NT);
+  const int seg_len = a.seg_len > 0 ? a.seg_len : rng.c1 - rng.c0;
+  const int n0 = rng.c0 + seg * seg_len, n1 = min(rng.c1, n0 + seg_len);
   const bool no_input = (a.flags & kScanNoInput) != 0;
-  const int bb = seq / H, h = seq % H;
+  const int h = seq % H;
   const int v0 = slice * DVS;
   __bf16* O = reinterpret_cast<__bf16*>(a.o);
-  auto vofs = [&](int n, int r) -> size_t {
-    return ((size_t)bb * T + (size_t)n * CH + r) * ((size_t)H * DV) + (size_t)h * DV + v0;
-  };
 
   // wave roles
   const int iO = wave >> 1;                 // row block of the R / O tiles
@@ -117,7 +115,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
   u4v stg[NSTG];
   f4 ucur[NVB / 2], unext[NVB / 2];
   float gcur[4], gnext[4];
-  const size_t chs = (size_t)seq * NT;
+  const size_t chs = rng.chs;
 #define GDR2_LOAD_OPS(CHX)                                                                                   \
   _Pragma("unroll") for (int m = 0; m < NSTG; ++m) {                                                     \
     const unsigned char* src;                                                                            \
@@ -252,11 +250,14 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
       }
 #undef GDR2_O_FRAGS
       const float sc = a.scale;
+      size_t orow;
+      int olen;
+      scan_rows(a.vl, seq, H, T, n, orow, olen);
+      if (16 * iO + r16 < olen) {
+        __bf16* orp = O + (orow + 16 * iO + r16) * ((size_t)H * DV) + (size_t)h * DV + v0;
 #pragma unroll
-      for (int t = 0; t < NVB / 2; ++t) {
-        const int vb = vbO + t;
-        st4(O + vofs(n, 16 * iO + r16) + 16 * vb + 4 * g, sc * accO[t][0], sc * accO[t][1], sc * accO[t][2],
-            sc * accO[t][3]);
+        for (int t = 0; t < NVB / 2; ++t)
+          st4(orp + 16 * (vbO + t) + 4 * g, sc * accO[t][0], sc * accO[t][1], sc * accO[t][2], sc * accO[t][3]);
       }
     }
 

@@ -140,6 +140,26 @@ CONFIGS = {
 }
 
 
+def make_packed(lengths, H, Dk, Dv, seed, dtype="bf16", decay_shift=0.0, s0_std=0.0, with_dST=False):
+    """A packed variable-length batch (App. C.6): sequences of the given lengths
+    laid end to end along T (B = 1), drawn like make_inputs, with their offsets
+    ``cu_seqlens`` (int32, len(lengths) + 1) and per-sequence start states /
+    final-state gradients of shape (n_seqs, H, Dk, Dv)."""
+    lengths = [int(x) for x in lengths]
+    T = sum(lengths)
+    if T <= 0:
+        raise ValueError("a packed batch needs at least one token")
+    d = make_inputs(1, T, H, Dk, Dv, seed, dtype=dtype, decay_shift=decay_shift)
+    N = len(lengths)
+    rng = np.random.default_rng(np.random.SeedSequence([seed, 0x9ac4ed]))
+    f32 = np.float32
+    d["S0"] = (s0_std * rng.standard_normal((N, H, Dk, Dv))).astype(f32) if s0_std > 0 else None
+    d["dST"] = rng.standard_normal((N, H, Dk, Dv)).astype(f32) if with_dST else None
+    d["cu_seqlens"] = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int32)
+    d["lengths"] = lengths
+    return d
+
+
 def config(idx, decay="channel", **overrides):
     """Inputs of workload ``idx`` (config 1 takes decay="channel" or "scalar")."""
     c = dict(CONFIGS[idx])

@@ -32,6 +32,8 @@ def test_header_declares_the_entry_points():
     assert _declared_symbols() == sorted(["gdr2_chunk_workspace_bytes", "gdr2_chunk_fwd",
                                           "gdr2_chunk_bwd", "gdr2_chunk_fwd_save",
                                           "gdr2_chunk_bwd_saved", "gdr2_recurrent_step",
+                                          "gdr2_varlen_workspace_bytes", "gdr2_chunk_fwd_varlen",
+                                          "gdr2_chunk_bwd_varlen", "gdr2_recurrent_varlen",
                                           "gdr2_status_str", "gdr2_profile_enable",
                                           "gdr2_profile_collect"])
 
@@ -101,7 +103,7 @@ def _rec(prob, ptrs=None):
     (dict(Dk=0), g2.GDR2_EINVAL), (dict(scale=float("nan")), g2.GDR2_EINVAL),
     (dict(scale=float("inf")), g2.GDR2_EINVAL), (dict(dtype=7), g2.GDR2_EINVAL),
     (dict(Dk=96), g2.GDR2_EUNSUPPORTED), (dict(Dv=256), g2.GDR2_EUNSUPPORTED),
-    (dict(chunk=32), g2.GDR2_EUNSUPPORTED), (dict(T=100), g2.GDR2_EUNSUPPORTED),
+    (dict(chunk=32), g2.GDR2_EUNSUPPORTED),
     (dict(B=1 << 20, T=1 << 16), g2.GDR2_EUNSUPPORTED),
 ])
 def test_problem_validation(kw, code):
@@ -236,3 +238,69 @@ def test_workspace_segment_buffers():
             assert g2.gdr2_chunk_workspace_bytes(p, bwd) == base + extra, (B, T, H, Dk, Dv, bwd)
         p.dtype = g2.GDR2_FP32
         assert seg_buffer_bytes(B, T, H, Dk, Dv, "fp32") == 0
+
+
+def test_partial_last_chunk_workspace():
+    """T need not be a multiple of 64: a sequence of T tokens takes ceil(T/64)
+    chunks (the last one partial), so the workspace equals that of the next multiple."""
+    for dtype in (g2.GDR2_BF16, g2.GDR2_FP32):
+        for bwd in (0, 1):
+            a = _prob(B=2, T=100, dtype=dtype)
+            b = _prob(B=2, T=128, dtype=dtype)
+            assert g2.gdr2_chunk_workspace_bytes(a, bwd) == g2.gdr2_chunk_workspace_bytes(b, bwd)
+            assert g2.gdr2_chunk_workspace_bytes(_prob(T=65, dtype=dtype), bwd) == \
+                g2.gdr2_chunk_workspace_bytes(_prob(T=128, dtype=dtype), bwd)
+
+
+def _vfwd(prob, cu=FAKE, n=3, ws_bytes=1 << 40, save=0):
+    L = g2.lib()
+    p = [FAKE] * 6 + [None, FAKE, None, FAKE]
+    return L.gdr2_chunk_fwd_varlen(ctypes.byref(prob), ctypes.c_void_p(cu) if cu else None, n,
+                                   *[ctypes.c_void_p(x) if x else None for x in p], ws_bytes, save, None)
+
+
+def _vbwd(prob, cu=FAKE, n=3, ws_bytes=1 << 40, saved=0):
+    L = g2.lib()
+    p = [FAKE] * 6 + [None, FAKE, None] + [FAKE] * 6 + [None, FAKE]
+    return L.gdr2_chunk_bwd_varlen(ctypes.byref(prob), ctypes.c_void_p(cu) if cu else None, n,
+                                   *[ctypes.c_void_p(x) if x else None for x in p], ws_bytes, saved, None)
+
+
+def test_varlen_validation():
+    """Packed calls: B must be 1, n_seqs >= 1 (at most 2^24), cu_seqlens non-null and
+    4-byte aligned, and the workspace large enough -- all checked before any launch."""
+    L = g2.lib()
+    p1 = _prob(B=1, T=1000)
+    n = ctypes.c_size_t(0)
+    assert L.gdr2_varlen_workspace_bytes(ctypes.byref(p1), 0, 0, ctypes.byref(n)) == g2.GDR2_EINVAL
+    assert L.gdr2_varlen_workspace_bytes(ctypes.byref(_prob(B=2)), 3, 0, ctypes.byref(n)) == g2.GDR2_EINVAL
+    assert L.gdr2_varlen_workspace_bytes(ctypes.byref(p1), (1 << 24) + 1, 0, ctypes.byref(n)) == \
+        g2.GDR2_EUNSUPPORTED
+    assert L.gdr2_varlen_workspace_bytes(ctypes.byref(p1), 3, 0, None) == g2.GDR2_EINVAL
+    for call in (_vfwd, _vbwd):
+        assert call(_prob(B=2, T=1000)) == g2.GDR2_EINVAL
+        assert call(p1, cu=None) == g2.GDR2_EINVAL
+        assert call(p1, cu=FAKE + 2) == g2.GDR2_EINVAL
+        assert call(p1, n=0) == g2.GDR2_EINVAL
+        assert call(_prob(B=1, T=1000, Dk=96)) == g2.GDR2_EUNSUPPORTED
+    fwd = g2.gdr2_varlen_workspace_bytes(p1, 3, 0)
+    bwd = g2.gdr2_varlen_workspace_bytes(p1, 3, 1)
+    assert _vfwd(p1, ws_bytes=fwd - 1) == g2.GDR2_EWORKSPACE
+    assert _vfwd(p1, ws_bytes=fwd, save=1) == g2.GDR2_EWORKSPACE
+    assert _vbwd(p1, ws_bytes=bwd - 1) == g2.GDR2_EWORKSPACE
+    vp = lambda xs: [ctypes.c_void_p(x) if x else None for x in xs]
+    assert L.gdr2_recurrent_varlen(ctypes.byref(p1), None, 3, *vp([FAKE] * 8), None) == g2.GDR2_EINVAL
+    assert L.gdr2_recurrent_varlen(ctypes.byref(p1), ctypes.c_void_p(FAKE), 0, *vp([FAKE] * 8), None) == \
+        g2.GDR2_EINVAL
+
+
+def test_varlen_workspace_size():
+    """A packed call of N sequences and T tokens reserves floor(T/64) + N chunk
+    slots per head (an upper bound of sum ceil(L_s/64)) plus the chunk table."""
+    from tests.gpu_common import ws_layout_bf16
+    for (T, N, H, Dk, Dv) in [(1000, 3, 4, 128, 64), (64, 1, 2, 64, 64), (4096, 37, 16, 128, 128)]:
+        p = _prob(B=1, T=T, H=H, Dk=Dk, Dv=Dv)
+        for bwd in (0, 1):
+            _, total, NC = ws_layout_bf16(1, T, H, Dk, Dv, bwd=bool(bwd), nseq=N)
+            assert NC == H * (T // 64 + N)
+            assert g2.gdr2_varlen_workspace_bytes(p, N, bwd) == total, (T, N, bwd)
