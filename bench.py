@@ -242,6 +242,65 @@ def config3_bench(steps=3, stored=True):
             "ms_per_step": ms, "tokens_per_s": B * T / (ms * 1e-3), "kernels": kern}
 
 
+def packed_lengths(total, seed=2024, lo=64, hi=4096):
+    """Sequence lengths of a packed batch: log-uniform in [lo, hi] (documents up
+    to the 4K training context), drawn until `total` tokens are used (the last
+    one takes the remainder)."""
+    import numpy as np
+    rng = np.random.default_rng(seed)
+    out, used = [], 0
+    while used < total:
+        L = int(np.exp(rng.uniform(np.log(lo), np.log(hi + 1))))
+        L = min(L, total - used)
+        out.append(L)
+        used += L
+    return out
+
+
+def varlen_bench(steps=10, stored=True):
+    """Packed variable-length batch with the tokens of the headline step
+    (32768 tokens x 16 heads, d = 128, bf16): documents of log-uniform length in
+    [64, 4096] (the 4K training context), so most end in a partial chunk.
+    fwd+bwd step time and per-kernel averages."""
+    import numpy as np
+    import torch
+    import paper_2605_22791_amd as g2
+    from paper_2605_22791_amd.inputs import make_packed
+    lengths = packed_lengths(8 * 4096)
+    d = make_packed(lengths, 16, 128, 128, seed=31, dtype="bf16", decay_shift=-2.0)
+    tb = lambda x: torch.from_numpy(x).cuda().to(torch.bfloat16).contiguous()
+    q, k, v, b, w, do = (tb(d[n]) for n in ("q", "k", "v", "b", "w", "do"))
+    la = torch.from_numpy(d["log_alpha"]).cuda().contiguous()
+    cu = torch.from_numpy(d["cu_seqlens"]).cuda()
+    N, T = len(lengths), sum(lengths)
+    prob = g2.Gdr2Problem(1, T, 16, 128, 128, 64, d["scale"], g2.GDR2_BF16)
+    ws = torch.empty(g2.gdr2_varlen_workspace_bytes(prob, N, 1), dtype=torch.uint8, device="cuda")
+
+    def step():
+        g2.gdr2_chunk_fwd_varlen(q, k, v, la, b, w, cu, None, scale=d["scale"], ws=ws, save=stored)
+        g2.gdr2_chunk_bwd_varlen(q, k, v, la, b, w, cu, None, do, None, scale=d["scale"], ws=ws, saved=stored)
+
+    for _ in range(2):
+        step()
+    torch.cuda.synchronize()
+    g2.gdr2_profile_enable(True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    per_kernel = g2.gdr2_profile_collect()
+    g2.gdr2_profile_enable(False)
+    ms = e0.elapsed_time(e1) / steps
+    chunks = int(sum(-(-L // 64) for L in lengths))
+    kern = {n: round(kms / cnt * 1e3, 1) for n, (kms, cnt) in per_kernel.items() if cnt}
+    return {"workload": f"packed batch, {N} sequences (log-uniform 64..4096 tokens), T = {T}, H16 d128 bf16",
+            "training_path": "stored" if stored else "recompute", "n_seqs": N, "chunks_per_head": chunks,
+            "partial_chunks_per_head": int(sum(1 for L in lengths if L % 64)),
+            "ms_per_step": ms, "tokens_per_s": T / (ms * 1e-3), "kernels_avg_us": kern}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -259,6 +318,8 @@ def main():
     ap.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
                     help="run one copy-like elementwise kernel (torch.neg) over MIB MiB of fp32 before the "
                          "timed steps: the reference that scales rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes")
+    ap.add_argument("--varlen-only", action="store_true",
+                    help="time only the packed variable-length batch (32768 tokens, H=16) and print its figures")
     ap.add_argument("--long-context-only", action="store_true",
                     help="time only the long-context step (B=1, H=16, T=65536) for --steps steps and print "
                          "its figures (not the benchmark line)")
@@ -269,6 +330,9 @@ def main():
         sys.exit(2)
     if args.long_context_only:
         print(json.dumps(config3_bench(steps=args.steps, stored=args.path == "stored")), flush=True)
+        return
+    if args.varlen_only:
+        print(json.dumps(varlen_bench(steps=args.steps, stored=args.path == "stored")), flush=True)
         return
 
     import torch
@@ -403,6 +467,8 @@ def main():
     if not args.no_extra:
         print("[bench] long context (config 3)", file=sys.stderr, flush=True)
         out["long_context"] = config3_bench(stored=stored)
+        print("[bench] packed variable-length batch", file=sys.stderr, flush=True)
+        out["varlen"] = varlen_bench(stored=stored)
     if not args.no_cpu:
         print("[bench] cpu oracle baseline", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(d, args.cpu_heads)

@@ -30,7 +30,8 @@ Layouts follow the operator: q, k, b, g are (B, T, H, Dk); v, w, o are
 
 import numpy as np
 
-__all__ = ["gdr2_recurrent_fwd", "gdr2_recurrent_bwd", "gdr2_step_states"]
+__all__ = ["gdr2_recurrent_fwd", "gdr2_recurrent_bwd", "gdr2_step_states", "gdr2_packed_fwd",
+           "gdr2_packed_bwd"]
 
 
 def _f64(*xs):
@@ -153,3 +154,48 @@ def gdr2_recurrent_bwd(q, k, v, g, b, w, S0, do, dS_T=None, scale=1.0, ckpt=64):
             dg[:, t] = a * np.einsum("bhkv,bhkv->bhk", dSbar, S_prev)
             dS = a[..., :, None] * dSbar
     return dict(dq=dq, dk=dk, dv=dv, dg=dg, db=db, dw=dw, dS0=dS)
+
+
+# ---------------------------------------------------------------------------
+# Packed variable-length batches (App. C.6): B = 1 and sequence s owns tokens
+# cu[s] .. cu[s+1) of the (1, T, H, D) tensors.  The state restarts at every
+# boundary, so a packed batch is nothing but its sequences run one by one from
+# their own start states (S0 / dS_T of shape (n_seqs, H, Dk, Dv)).
+
+def gdr2_packed_fwd(q, k, v, g, b, w, cu_seqlens, S0=None, scale=1.0):
+    """Forward of a packed batch.  Returns (o (1, T, H, Dv), S_T (n_seqs, H, Dk, Dv))."""
+    q, k, v, g, b, w = _f64(q, k, v, g, b, w)
+    _, T, H, Dk, Dv = _shapes(k, v)
+    cu = [int(x) for x in cu_seqlens]
+    N = len(cu) - 1
+    S0 = np.zeros((N, H, Dk, Dv)) if S0 is None else np.asarray(S0, dtype=np.float64)
+    o = np.zeros((1, T, H, Dv))
+    ST = np.array(S0, dtype=np.float64)
+    for s in range(N):
+        a, e = cu[s], cu[s + 1]
+        if e > a:
+            sl = [x[:, a:e] for x in (q, k, v, g, b, w)]
+            o[:, a:e], S = gdr2_recurrent_fwd(*sl, S0[s:s + 1], scale)
+            ST[s] = S[0]
+    return o, ST
+
+
+def gdr2_packed_bwd(q, k, v, g, b, w, cu_seqlens, S0, do, dS_T=None, scale=1.0):
+    """Adjoint of gdr2_packed_fwd: dict dq, dk, dv, dg, db, dw (1, T, H, .) and dS0 (n_seqs, H, Dk, Dv)."""
+    q, k, v, g, b, w, do = _f64(q, k, v, g, b, w, do)
+    _, T, H, Dk, Dv = _shapes(k, v)
+    cu = [int(x) for x in cu_seqlens]
+    N = len(cu) - 1
+    S0 = np.zeros((N, H, Dk, Dv)) if S0 is None else np.asarray(S0, dtype=np.float64)
+    dS_T = np.zeros((N, H, Dk, Dv)) if dS_T is None else np.asarray(dS_T, dtype=np.float64)
+    out = {n: np.zeros_like(x) for n, x in (("dq", q), ("dk", k), ("dv", v), ("dg", g), ("db", b), ("dw", w))}
+    out["dS0"] = np.array(dS_T, dtype=np.float64)
+    for s in range(N):
+        a, e = cu[s], cu[s + 1]
+        if e > a:
+            sl = [x[:, a:e] for x in (q, k, v, g, b, w)]
+            r = gdr2_recurrent_bwd(*sl, S0[s:s + 1], do[:, a:e], dS_T[s:s + 1], scale)
+            for n in ("dq", "dk", "dv", "dg", "db", "dw"):
+                out[n][:, a:e] = r[n]
+            out["dS0"][s] = r["dS0"][0]
+    return out

@@ -57,7 +57,7 @@ struct Layout {
   size_t bDR, bAm;                       // bf16 backward extras (fragment order)
   size_t sM, sN, sX;                     // segment maps and entry states (sequence-parallel scans)
   int nseg, seg_len;
-  size_t vcoff, vct0, vclen;             // chunk table of a packed call (int32)
+  size_t vcoff, vct0, vclen, vsord;      // chunk table and scan order of a packed call (int32)
   size_t total;
 };
 
@@ -142,6 +142,7 @@ Layout layout(const gdr2_problem* p, bool bwd, int nseq = 0) {
     L.vcoff = take((size_t)nseq + 1);
     L.vct0 = take(slots);
     L.vclen = take(slots);
+    L.vsord = take((size_t)nseq);
   } else {
     scan_segments(p, L.nseg, L.seg_len);
   }
@@ -180,6 +181,7 @@ Geo make_geo(const gdr2_problem* p, bool bwd, int nseq, const int* cu, void* ws)
     G.vl.coff = at<int>(ws, G.L.vcoff);
     G.vl.ct0 = at<int>(ws, G.L.vct0);
     G.vl.clen = at<int>(ws, G.L.vclen);
+    G.vl.sorder = at<int>(ws, G.L.vsord);
     G.vl.nseq = nseq;
     G.vl.ncmax = G.NT;
   } else {
@@ -193,7 +195,8 @@ Geo make_geo(const gdr2_problem* p, bool bwd, int nseq, const int* cu, void* ws)
 hipError_t build_table(const gdr2_problem* p, const Geo& G, hipStream_t st) {
   if (G.vl.cu == nullptr) return hipSuccess;
   return launch_varlen_table(G.vl.cu, G.vl.nseq, p->T, G.vl.ncmax, const_cast<int*>(G.vl.coff),
-                             const_cast<int*>(G.vl.ct0), const_cast<int*>(G.vl.clen), st);
+                             const_cast<int*>(G.vl.ct0), const_cast<int*>(G.vl.clen),
+                             const_cast<int*>(G.vl.sorder), st);
 }
 
 bool debug_sync() {

@@ -35,7 +35,7 @@ __global__ __launch_bounds__(256) void bwd_state_kernel(BwdStateArgs<TIn> a) {
   const int lr = lane & 15, lg = lane >> 4;
   const int T = a.T, H = a.H, NT = a.NT;
   const int v0 = vs * DVS;
-  const size_t seq = (size_t)bb * H + h;  // (sequence, head) pair
+  const size_t seq = (size_t)scan_pair(a.vl, bb * H + h, H);  // (sequence, head) pair
   const ScanRange rng = scan_range(a.vl, (int)seq, H, NT);
 
   __shared__ float sdS[DK * LSS];

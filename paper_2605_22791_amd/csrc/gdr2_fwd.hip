@@ -187,7 +187,7 @@ __global__ __launch_bounds__(256) void fwd_state_kernel(StateArgs<TIn> a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int T = a.T, H = a.H, NT = a.NT;
   const int v0 = vs * DVS;
-  const size_t seq = (size_t)bb * H + h;  // (sequence, head) pair
+  const size_t seq = (size_t)scan_pair(a.vl, bb * H + h, H);  // (sequence, head) pair
   const ScanRange rng = scan_range(a.vl, (int)seq, H, NT);
 
   __shared__ float sS[DK * LSS];

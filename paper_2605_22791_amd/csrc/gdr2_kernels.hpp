@@ -18,8 +18,16 @@ struct Varlen {
   const int* coff = nullptr;  // first chunk of every sequence; coff[nseq] = chunks in use
   const int* ct0 = nullptr;   // first token of every chunk
   const int* clen = nullptr;  // rows of every chunk (1 .. C)
+  const int* sorder = nullptr;  // sequences by decreasing chunk count: the order the scans take them in
   int nseq = 0, ncmax = 0;    // sequences; chunk slots (grid and workspace extent)
 };
+
+// Scanned pair (sequence, head) of a scan workgroup's index q: for packed
+// calls the sequences are taken longest first, so that the longest scans start
+// with the grid and the short ones fill in behind them.
+__device__ __forceinline__ int scan_pair(const Varlen& vl, int q, int H) {
+  return vl.sorder != nullptr ? vl.sorder[q / H] * H + q % H : q;
+}
 
 struct ChunkPos {
   size_t row0;  // token row of the chunk's first row (row = b * T + t)
@@ -329,8 +337,9 @@ hipError_t launch_recurrent(const RecurArgs<TIn>& a, int B, hipStream_t st);
 
 // Builds the chunk table of a packed call (Varlen) from cu_seqlens: lengths
 // are clamped into [0, T] and the chunk count to ncmax, so malformed offsets
-// cannot lead to accesses outside the tensors or the workspace.
+// cannot lead to accesses outside the tensors or the workspace; and the scan
+// order of the sequences (decreasing chunk count).
 hipError_t launch_varlen_table(const int* cu, int nseq, int T, int ncmax, int* coff, int* ct0, int* clen,
-                               hipStream_t st);
+                               int* sorder, hipStream_t st);
 
 }  // namespace gdr2

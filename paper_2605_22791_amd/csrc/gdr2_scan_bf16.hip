@@ -90,7 +90,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
     vs = blockIdx.x / NS;
     slice = blockIdx.x % NS;
   }
-  const int seq = vs / nseg, seg = vs % nseg;  // seq = (sequence, head) pair, sequence-major
+  const int seq = scan_pair(a.vl, vs / nseg, H), seg = vs % nseg;  // (sequence, head) pair
   const ScanRange rng = scan_range(a.vl, seq, H, NT);
   const int seg_len = a.seg_len > 0 ? a.seg_len : rng.c1 - rng.c0;
   const int n0 = rng.c0 + seg * seg_len, n1 = min(rng.c1, n0 + seg_len);

@@ -82,7 +82,7 @@ def ws_layout_bf16(B, T, H, Dk, Dv, bwd=False, nseq=0):
     (mirrors WsBf16 in the library: fragment-ordered tiles; the backward adds
     fp32 chunk states Hs, R and dH, then dR and A as fragment blocks).  A
     packed call (nseq > 0) has H * (T // 64 + nseq) chunk-heads and appends
-    its chunk table (int32: nseq + 1 offsets, then two slot arrays)."""
+    its chunk table (int32: nseq + 1 offsets, two slot arrays, the scan order)."""
     NC = H * (T // CH + nseq) if nseq > 0 else B * H * (-(-T // CH))
     gc = (Dk * 4 + 255) // 256 * 256
     sizes = [("Y", 4 * (Dk // 32) * 1024), ("Qg", 4 * (Dk // 32) * 2048), ("Aqk", 8 * 2048),
@@ -96,7 +96,7 @@ def ws_layout_bf16(B, T, H, Dk, Dv, bwd=False, nseq=0):
         off += (NC * per + 255) // 256 * 256
     if nseq > 0:
         slots = T // CH + nseq
-        for n, cnt in (("coff", nseq + 1), ("ct0", slots), ("clen", slots)):
+        for n, cnt in (("coff", nseq + 1), ("ct0", slots), ("clen", slots), ("sorder", nseq)):
             out[n] = (off, cnt * 4)
             off += (cnt * 4 + 255) // 256 * 256
     return out, off, NC

@@ -11,7 +11,7 @@ the chunk and ragged tails.  Tolerances as elsewhere (rel-L2 2e-3 bf16, 1e-5 fp3
 import numpy as np
 import pytest
 
-from oracle import gdr2_recurrent_bwd, gdr2_recurrent_fwd
+from oracle import gdr2_packed_bwd, gdr2_packed_fwd, gdr2_recurrent_bwd, gdr2_recurrent_fwd
 from paper_2605_22791_amd.inputs import make_inputs, make_packed
 from tests.helpers import rel_l2
 from tests.gpu_common import dev_inputs, host, ws_layout_bf16
@@ -27,34 +27,15 @@ def _case(msg):
     print(f"\n[gpu case] {msg}", flush=True)
 
 
-def _seq(d, name, a, b):
-    return d[name][:, a:b]
-
-
 def oracle_packed(d, backward=True):
-    """Per-sequence fp64 recurrence (and adjoint) of a packed batch."""
-    cu, T = d["cu_seqlens"], d["q"].shape[1]
-    H, Dk, Dv = d["q"].shape[2], d["q"].shape[3], d["v"].shape[3]
-    N = len(cu) - 1
-    S0 = d["S0"] if d["S0"] is not None else np.zeros((N, H, Dk, Dv), np.float32)
-    dST = d["dST"] if d.get("dST") is not None else np.zeros((N, H, Dk, Dv), np.float32)
-    out = {"o": np.zeros((1, T, H, Dv)), "S_T": np.zeros((N, H, Dk, Dv)), "dS0": np.zeros((N, H, Dk, Dv))}
-    for n in GRADS:
-        out[n] = np.zeros(d["v"].shape if n in ("dv", "dw") else d["q"].shape)
-    for s in range(N):
-        a, b = int(cu[s]), int(cu[s + 1])
-        if a == b:  # no tokens: the state passes through
-            out["S_T"][s] = S0[s]
-            out["dS0"][s] = dST[s]
-            continue
-        args = [_seq(d, n, a, b) for n in ("q", "k", "v", "log_alpha", "b", "w")]
-        o, ST = gdr2_recurrent_fwd(*args, S0[s:s + 1], d["scale"])
-        out["o"][:, a:b], out["S_T"][s] = o, ST[0]
-        if backward:
-            g = gdr2_recurrent_bwd(*args, S0[s:s + 1], _seq(d, "do", a, b), dST[s:s + 1], d["scale"])
-            for n in GRADS:
-                out[n][:, a:b] = g[REF.get(n, n)]
-            out["dS0"][s] = g["dS0"][0]
+    """The oracle's packed batch (App. C.6): the fp64 recurrence and adjoint per sequence."""
+    args = [d[n] for n in ("q", "k", "v", "log_alpha", "b", "w")]
+    o, ST = gdr2_packed_fwd(*args, d["cu_seqlens"], d["S0"], d["scale"])
+    out = {"o": o, "S_T": ST}
+    if backward:
+        g = gdr2_packed_bwd(*args, d["cu_seqlens"], d["S0"], d["do"], d.get("dST"), d["scale"])
+        out.update({n: g[REF.get(n, n)] for n in GRADS})
+        out["dS0"] = g["dS0"]
     return out
 
 
@@ -177,7 +158,8 @@ def test_recurrent_varlen_matches_oracle():
 
 def test_chunk_table_in_workspace():
     """The device chunk table: every sequence cut into ceil(L/64) chunks from its
-    own first token, the last one holding the remainder; empty sequences none."""
+    own first token, the last one holding the remainder; empty sequences none;
+    the scans take the sequences longest first."""
     import torch
     import paper_2605_22791_amd as g2
     lengths = [100, 0, 64, 1, 129]
@@ -204,3 +186,8 @@ def test_chunk_table_in_workspace():
         exp_off.append(len(exp_t0))
     assert list(coff) == exp_off
     assert list(ct0[:len(exp_t0)]) == exp_t0 and list(clen[:len(exp_len)]) == exp_len
+    # scan order: a permutation of the sequences by non-increasing chunk count
+    order = list(region("sorder"))
+    counts = [exp_off[s + 1] - exp_off[s] for s in range(N)]
+    assert sorted(order) == list(range(N))
+    assert all(counts[order[i]] >= counts[order[i + 1]] for i in range(N - 1))

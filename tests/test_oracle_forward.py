@@ -193,3 +193,33 @@ def test_chunk_internals_wy_identities():
     for r in range(1, C + 1):  # eq. eq_app_prefix_state: Shat_r = S0 + Kbar_{<=r}^T R_{<=r}
         Shat = S0 + Kbar[:r].T @ R[:r]
         assert rel_l2(gam[r - 1][:, None] * Shat, S_all[r][0, 0]) < 1e-11
+
+
+def test_P11_packed_batch_restarts_at_boundaries():
+    """App. C.6: a packed batch resets the state at every sequence boundary.
+    Each sequence's outputs equal the dense transition-product form run on its
+    tokens alone (brute force, an independent path), changing one sequence's
+    tokens leaves the others untouched, and an empty sequence passes S0 through."""
+    from oracle import gdr2_packed_fwd
+    lengths = [7, 0, 12, 1]
+    cu = np.concatenate([[0], np.cumsum(lengths)])
+    d = small_problem(1, int(cu[-1]), 2, 5, 4, seed=19)
+    rng = np.random.default_rng(3)
+    S0 = rng.standard_normal((len(lengths), 2, 5, 4))
+    args = lambda dd: (dd["q"], dd["k"], dd["v"], dd["log_alpha"], dd["b"], dd["w"])
+    o, ST = gdr2_packed_fwd(*args(d), cu, S0, d["scale"])
+    for s, L in enumerate(lengths):
+        a, e = int(cu[s]), int(cu[s + 1])
+        if L == 0:
+            assert np.array_equal(ST[s], S0[s])
+            continue
+        sl = [x[:, a:e] for x in args(d)]
+        ob, Sb = brute.gdr2_brute_fwd(*sl, S0[s:s + 1], d["scale"])
+        assert rel_l2(o[:, a:e], ob) < 1e-12 and rel_l2(ST[s], Sb[0]) < 1e-12
+    d2 = {n: np.array(x, copy=True) for n, x in d.items() if isinstance(x, np.ndarray)}
+    d2.update(scale=d["scale"])
+    for n in ("q", "k", "v", "log_alpha", "b", "w"):
+        d2[n][:, :7] = rng.standard_normal(d2[n][:, :7].shape) * 0.3 - (0.5 if n == "log_alpha" else 0.0)
+    o2, ST2 = gdr2_packed_fwd(*args(d2), cu, S0, d["scale"])
+    assert not np.allclose(o2[:, :7], o[:, :7])
+    assert np.array_equal(o2[:, 7:], o[:, 7:]) and np.array_equal(ST2[1:], ST[1:])
