@@ -248,3 +248,40 @@ def test_config3_long_context_backward_sampled_head():
     ref = gdr2_recurrent_bwd(sub["q"], sub["k"], sub["v"], sub["log_alpha"], sub["b"], sub["w"], sub["S0"],
                              sub["do"], None, d["scale"])
     _compare(got, ref, TOL["bf16"], pairs=pairs)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_negative_eigenvalue_backward(dtype):
+    """b in [0, 2] (negative-eigenvalue variant, Sec. 3.1; NEXT-4): the same
+    operator on a wider erase range, forward and every gradient against the
+    adjoint, with a partial last chunk (T = 300)."""
+    d = make_inputs(1, 300, 2, 128, 128, seed=69, dtype=dtype, s0_std=0.05, with_dST=True)
+    d["b"] = 2.0 * d["b"]   # exact in bf16
+    _case(f"{dtype} bwd, erase gate in [0, 2], T300")
+    _compare(_run_bwd(d), _adjoint(d), TOL[dtype])
+
+
+def test_negative_eigenvalue_reflections_keep_the_state_norm():
+    """b = 2 with unit keys, no decay and no write: 4096 Householder reflections
+    per head; the bf16 path's fp32 state keeps its Frobenius norm to 2e-4 (the
+    drift is the rounding of the one bf16 product on the state path, Y S with
+    the bf16 part of S; 6.7e-5 measured).  The keys are +-1/2 on four random
+    channels, unit vectors exactly in bf16."""
+    import paper_2605_22791_amd as g2
+    d = make_inputs(1, 4096, 2, 128, 128, seed=70, dtype="bf16", s0_std=0.05)
+    rng = np.random.default_rng(70)
+    k = np.zeros_like(d["k"])
+    for t in range(k.shape[1]):
+        for h in range(k.shape[2]):
+            k[0, t, h, rng.choice(128, 4, replace=False)] = rng.choice([-0.5, 0.5], 4)
+    d["k"] = k
+    d["b"] = np.full_like(d["b"], 2.0)
+    d["log_alpha"] = np.zeros_like(d["log_alpha"])
+    d["w"] = np.zeros_like(d["w"])
+    _case("bf16 fwd, 4096 reflections")
+    x = dev_inputs(d)
+    _, ST = g2.gdr2_chunk_fwd(*[x[n] for n in ("q", "k", "v", "log_alpha", "b", "w")], x["S0"], scale=d["scale"])
+    n0 = np.linalg.norm(d["S0"].astype(np.float64), axis=(-2, -1))
+    n1 = np.linalg.norm(host(ST), axis=(-2, -1))
+    print("norm ratio", n1 / n0)
+    assert np.allclose(n1, n0, rtol=2e-4)

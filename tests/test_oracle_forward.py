@@ -223,3 +223,23 @@ def test_P11_packed_batch_restarts_at_boundaries():
     o2, ST2 = gdr2_packed_fwd(*args(d2), cu, S0, d["scale"])
     assert not np.allclose(o2[:, :7], o[:, :7])
     assert np.array_equal(o2[:, 7:], o[:, 7:]) and np.array_equal(ST2[1:], ST[1:])
+
+
+def test_P12_negative_eigenvalue_reflection_preserves_the_state_norm():
+    """Sec. 3.1, negative-eigenvalue range b in [0, 2]: with b = 2, unit keys, no
+    decay (g = 0) and no write (w = 0) every step applies I - 2 k k^T, a Householder
+    reflection, so the Frobenius norm of the state is preserved exactly and two
+    equal consecutive keys undo each other."""
+    d = small_problem(1, 40, 2, 6, 5, seed=29)
+    k = d["k"].astype(np.float64)
+    d["k"] = k / np.linalg.norm(k, axis=-1, keepdims=True)   # unit in fp64
+    d["b"] = np.full_like(d["b"], 2.0)
+    d["log_alpha"] = np.zeros_like(d["log_alpha"])
+    d["w"] = np.zeros_like(d["w"])
+    S0 = d["S0"].astype(np.float64)
+    _, S = _fwd(d)
+    assert np.allclose(np.linalg.norm(S, axis=(-2, -1)), np.linalg.norm(S0, axis=(-2, -1)), rtol=1e-12)
+    d["k"][:, 1] = d["k"][:, 0]
+    d2 = {n: (x[:, :2] if isinstance(x, np.ndarray) and x.ndim == 4 and x.shape[1] == 40 else x) for n, x in d.items()}
+    _, S2 = _fwd(d2)
+    assert rel_l2(S2, S0) < 1e-12
