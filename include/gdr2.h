@@ -19,10 +19,11 @@
  * T need not be a multiple of the chunk length: the last chunk of every
  * sequence may be partial.
  *
- * Layout and dtypes (all tensors contiguous, row-major, device memory):
+ * Layout and dtypes (all tensors contiguous, row-major, device memory; Hv =
+ * H unless grouped value heads are asked for, see gdr2_problem):
  *     q, k, b, log_alpha           (B, T, H, Dk)
- *     v, w, o                      (B, T, H, Dv)
- *     S0, S_T, S, dS_T, dS0        (B, H, Dk, Dv)   always fp32
+ *     v, w, o                      (B, T, Hv, Dv)
+ *     S0, S_T, S, dS_T, dS0        (B, Hv, Dk, Dv)  always fp32
  *     log_alpha, dlog_alpha        always fp32 (the decay is formed in fp32,
  *                                  App. C.1 / App. D.1)
  *     q, k, v, b, w, o, dout, dq, dk, dv, db, dw
@@ -42,8 +43,9 @@
  *     launched and the status says why:
  *       GDR2_EINVAL        null required pointer, pointer not 16-byte aligned
  *                          (cu_seqlens: 4-byte aligned), a dimension <= 0,
- *                          non-finite scale, unknown dtype, n_seqs <= 0 or
- *                          B != 1 in a packed call;
+ *                          non-finite scale, unknown dtype, Hv not a
+ *                          multiple of H, n_seqs <= 0 or B != 1 in a
+ *                          packed call;
  *       GDR2_EUNSUPPORTED  Dk or Dv not in {64, 128}, chunk != 64, sizes
  *                          beyond 2^31 elements per tensor, more than 2^24
  *                          sequences in a packed call;
@@ -75,12 +77,18 @@ typedef enum gdr2_status {
 typedef enum gdr2_dtype { GDR2_BF16 = 0, GDR2_FP32 = 1 } gdr2_dtype;
 
 /* Problem description shared by every call.  `chunk` must be 64 (the chunk
- * length C of Sec. 3.3; App. C.2 fixes C = 64). */
+ * length C of Sec. 3.3; App. C.2 fixes C = 64).  Hv: value heads (0 means
+ * Hv = H); grouped value heads (Sec. 3.5, App. C.1) have Hv = G * H: value
+ * head j uses key head j / G, i.e. q, k, log_alpha and b (H heads) are
+ * repeated across each group of G consecutive value heads, while v, w, o,
+ * dout and every state live on the Hv value heads.  dq, dk, db and
+ * dlog_alpha are then the sums over the group. */
 typedef struct gdr2_problem {
   int32_t B, T, H, Dk, Dv;
   int32_t chunk;
   float scale;
   int32_t dtype; /* gdr2_dtype */
+  int32_t Hv;    /* value heads, a multiple of H; 0: Hv = H */
 } gdr2_problem;
 
 /* Bytes of device workspace a chunk call needs (for_backward = 0: forward,
@@ -94,7 +102,7 @@ gdr2_status gdr2_chunk_workspace_bytes(const gdr2_problem* problem, int for_back
  * state kernel then carries S across chunks (eq. eq_gdn2_chunk_state) and
  * writes O (eq. eq_gdn2_chunk_output).
  *   S0   may be NULL (zero start state).
- *   o    receives (B,T,H,Dv) in problem->dtype.
+ *   o    receives (B,T,Hv,Dv) in problem->dtype.
  *   S_T  may be NULL; otherwise receives the final state (fp32).
  *   ws   device workspace of at least gdr2_chunk_workspace_bytes(p, 0). */
 gdr2_status gdr2_chunk_fwd(const gdr2_problem* problem, const void* q, const void* k,
@@ -108,8 +116,8 @@ gdr2_status gdr2_chunk_fwd(const gdr2_problem* problem, const void* q, const voi
  * the inputs (the memory-saving path of App. D.3), so the call takes exactly
  * the forward's inputs plus the upstream gradients.
  *   S0, dS_T   may be NULL (zero).
- *   dq, dk, db (B,T,H,Dk) and dv, dw (B,T,H,Dv) in problem->dtype;
- *   dlog_alpha (B,T,H,Dk) fp32; dS0 (B,H,Dk,Dv) fp32 or NULL (not wanted).
+ *   dq, dk, db (B,T,H,Dk) and dv, dw (B,T,Hv,Dv) in problem->dtype;
+ *   dlog_alpha (B,T,H,Dk) fp32; dS0 (B,Hv,Dk,Dv) fp32 or NULL (not wanted).
  *   ws   device workspace of at least gdr2_chunk_workspace_bytes(p, 1). */
 gdr2_status gdr2_chunk_bwd(const gdr2_problem* problem, const void* q, const void* k,
                            const void* v, const float* log_alpha, const void* b,
@@ -159,7 +167,7 @@ gdr2_status gdr2_recurrent_step(const gdr2_problem* problem, const void* q, cons
  * allowed).  Each sequence is chunked on its own (its last chunk may be
  * partial), so the state restarts at every sequence boundary: the result for
  * sequence s equals a separate call on its tokens alone.  The states S0, S_T,
- * dS_T, dS0 and S (recurrent) are (n_seqs, H, Dk, Dv) fp32.
+ * dS_T, dS0 and S (recurrent) are (n_seqs, Hv, Dk, Dv) fp32.
  * The offsets are read on the device and not checked on the host: the
  * kernels clamp them into [0, T], so malformed offsets cannot cause accesses
  * outside the tensors or the workspace, but the results are then undefined.

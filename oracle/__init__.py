@@ -18,7 +18,8 @@ Modules:
                 eq_gdn2_residual, eq_gdn2_recurrence) and its hand-derived
                 reverse-time adjoint (the definition the method reaches);
                 packed variable-length batches (App. C.6) as their sequences
-                run one by one.
+                run one by one; grouped value heads (Sec. 3.5) as the key-side
+                tensors repeated over each group.
   chunkwise  -- the chunk algebra of App. A (WY form) and App. B (backward),
                 exposing every intermediate for per-kernel debugging.
   limits     -- independent textbook recurrences the paper reduces to:
@@ -31,6 +32,6 @@ itself: closed forms, tied-gate reductions, brute force and finite differences.
 """
 
 from .recurrent import gdr2_recurrent_fwd, gdr2_recurrent_bwd, gdr2_step_states  # noqa: F401
-from .recurrent import gdr2_packed_fwd, gdr2_packed_bwd  # noqa: F401
+from .recurrent import gdr2_packed_fwd, gdr2_packed_bwd, gdr2_grouped_fwd, gdr2_grouped_bwd  # noqa: F401
 from .chunkwise import gdr2_chunk_fwd_ref, gdr2_chunk_bwd_ref  # noqa: F401
 from . import limits, brute, fd  # noqa: F401

@@ -31,7 +31,7 @@ Layouts follow the operator: q, k, b, g are (B, T, H, Dk); v, w, o are
 import numpy as np
 
 __all__ = ["gdr2_recurrent_fwd", "gdr2_recurrent_bwd", "gdr2_step_states", "gdr2_packed_fwd",
-           "gdr2_packed_bwd"]
+           "gdr2_packed_bwd", "gdr2_grouped_fwd", "gdr2_grouped_bwd"]
 
 
 def _f64(*xs):
@@ -199,3 +199,34 @@ def gdr2_packed_bwd(q, k, v, g, b, w, cu_seqlens, S0, do, dS_T=None, scale=1.0):
                 out[n][:, a:e] = r[n]
             out["dS0"][s] = r["dS0"][0]
     return out
+
+
+# ---------------------------------------------------------------------------
+# Grouped value heads (Sec. 3.5, App. C.1): with Hv = G * H value heads, q, k,
+# the log-decay and b (H heads) are repeated across each group of G
+# consecutive value heads (value head j uses key head j // G), while v, w, the
+# outputs and the states live on the value heads.  The key-side gradients are
+# therefore the sums over the group (the adjoint of the repetition).
+
+def _repeat_keys(G, *xs):
+    return [np.repeat(np.asarray(x, dtype=np.float64), G, axis=2) for x in xs]
+
+
+def gdr2_grouped_fwd(q, k, v, g, b, w, S0=None, scale=1.0):
+    """Forward with Hv = v.shape[2] value heads over H = q.shape[2] key heads."""
+    G = np.shape(v)[2] // np.shape(q)[2]
+    qe, ke, ge, be = _repeat_keys(G, q, k, g, b)
+    return gdr2_recurrent_fwd(qe, ke, v, ge, be, w, S0, scale)
+
+
+def gdr2_grouped_bwd(q, k, v, g, b, w, S0, do, dS_T=None, scale=1.0):
+    """Adjoint of gdr2_grouped_fwd: dq, dk, dg, db on the key heads (group sums),
+    dv, dw and dS0 on the value heads."""
+    H, Hv = np.shape(q)[2], np.shape(v)[2]
+    G = Hv // H
+    qe, ke, ge, be = _repeat_keys(G, q, k, g, b)
+    r = gdr2_recurrent_bwd(qe, ke, v, ge, be, w, S0, do, dS_T, scale)
+    for n in ("dq", "dk", "dg", "db"):
+        x = r[n]
+        r[n] = x.reshape(x.shape[0], x.shape[1], H, G, x.shape[3]).sum(axis=3)
+    return r

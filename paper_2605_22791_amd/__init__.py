@@ -39,7 +39,7 @@ def lib_path():
 class Gdr2Problem(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int32), ("T", ctypes.c_int32), ("H", ctypes.c_int32),
                 ("Dk", ctypes.c_int32), ("Dv", ctypes.c_int32), ("chunk", ctypes.c_int32),
-                ("scale", ctypes.c_float), ("dtype", ctypes.c_int32)]
+                ("scale", ctypes.c_float), ("dtype", ctypes.c_int32), ("Hv", ctypes.c_int32)]
 
 
 class Gdr2Error(RuntimeError):
@@ -128,10 +128,10 @@ def _stream():
 
 def _problem(q, v, scale, chunk=CHUNK):
     B, T, H, Dk = q.shape
-    Dv = v.shape[-1]
+    Hv, Dv = v.shape[2], v.shape[-1]
     if scale is None:
         scale = Dk ** -0.5
-    return Gdr2Problem(B, T, H, Dk, Dv, chunk, float(scale), _dtype_code(q))
+    return Gdr2Problem(B, T, H, Dk, Dv, chunk, float(scale), _dtype_code(q), Hv)
 
 
 def _require(name, t, shape, dtype):
@@ -143,15 +143,20 @@ def _require(name, t, shape, dtype):
 
 
 def _validate(q, k, v, log_alpha, b, w):
+    """Shapes: q, k, b, log_alpha (B, T, H, Dk); v, w (B, T, Hv, Dv) with Hv a
+    multiple of H (grouped value heads when Hv > H).  Returns B, T, Hv, Dk, Dv:
+    outputs and states live on the value heads."""
     torch = _torch()
     B, T, H, Dk = q.shape
-    Dv = v.shape[-1]
+    Hv, Dv = v.shape[2], v.shape[-1]
+    if Hv % H != 0:
+        raise ValueError(f"value heads ({Hv}) must be a multiple of key heads ({H})")
     for n, t in (("q", q), ("k", k), ("b", b)):
         _require(n, t, (B, T, H, Dk), q.dtype)
     for n, t in (("v", v), ("w", w)):
-        _require(n, t, (B, T, H, Dv), q.dtype)
+        _require(n, t, (B, T, Hv, Dv), q.dtype)
     _require("log_alpha", log_alpha, (B, T, H, Dk), torch.float32)
-    return B, T, H, Dk, Dv
+    return B, T, Hv, Dk, Dv
 
 
 # --------------------------------------------------------------------------- public calls

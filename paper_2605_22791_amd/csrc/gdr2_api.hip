@@ -30,16 +30,28 @@ gdr2_status check_problem(const gdr2_problem* p, bool chunked, int nseq = 0) {
   if (!std::isfinite(p->scale)) return GDR2_EINVAL;
   if (p->dtype != GDR2_BF16 && p->dtype != GDR2_FP32) return GDR2_EINVAL;
   if (nseq < 0 || (nseq > 0 && p->B != 1)) return GDR2_EINVAL;
+  if (p->Hv < 0 || (p->Hv > 0 && p->Hv % p->H != 0)) return GDR2_EINVAL;
   if ((p->Dk != 64 && p->Dk != 128) || (p->Dv != 64 && p->Dv != 128)) return GDR2_EUNSUPPORTED;
   if (chunked && p->chunk != CH) return GDR2_EUNSUPPORTED;
   if (nseq > kMaxSeqs) return GDR2_EUNSUPPORTED;
-  const double rows = (double)p->B * (double)p->T * (double)p->H;
+  const double Hv = p->Hv > 0 ? p->Hv : p->H;
+  const double rows = (double)p->B * (double)p->T * Hv;
   const int dmax = p->Dk > p->Dv ? p->Dk : p->Dv;
   if (rows * dmax >= 2147483648.0) return GDR2_EUNSUPPORTED;
   const double states = nseq > 0 ? (double)nseq : (double)p->B;
-  if (states * p->H * (double)p->Dk * p->Dv >= 2147483648.0) return GDR2_EUNSUPPORTED;
+  if (states * Hv * (double)p->Dk * p->Dv >= 2147483648.0) return GDR2_EUNSUPPORTED;
   return GDR2_OK;
 }
+
+// The problem seen from the value heads: every kernel runs per value head
+// (H := Hv) and reads the key-side tensors q, k, g, b at key head h / G.
+gdr2_problem value_view(const gdr2_problem* p) {
+  gdr2_problem v = *p;
+  v.H = p->Hv > 0 ? p->Hv : p->H;
+  v.Hv = 0;
+  return v;
+}
+int group_of(const gdr2_problem* p) { return p->Hv > 0 ? p->Hv / p->H : 1; }
 
 // Chunks per sequence of a fixed-length call (the last one partial when 64 does not divide T).
 int chunks_per_seq(const gdr2_problem* p) { return (p->T + CH - 1) / CH; }
@@ -58,6 +70,7 @@ struct Layout {
   size_t sM, sN, sX;                     // segment maps and entry states (sequence-parallel scans)
   int nseg, seg_len;
   size_t vcoff, vct0, vclen, vsord;      // chunk table and scan order of a packed call (int32)
+  size_t pQ, pK, pB, pG;                 // grouped value heads: fp32 key-side gradient partials
   size_t total;
 };
 
@@ -87,7 +100,8 @@ void scan_segments(const gdr2_problem* p, int& nseg, int& seg_len) {
   nseg = (NT + seg_len - 1) / seg_len;
 }
 
-Layout layout(const gdr2_problem* p, bool bwd, int nseq = 0) {
+// p: the value view (value_view); G > 1 adds the backward's group partials.
+Layout layout(const gdr2_problem* p, bool bwd, int nseq = 0, int G = 1) {
   const size_t NC = nseq > 0 ? (size_t)p->H * varlen_slots(p, nseq) : (size_t)p->B * p->H * chunks_per_seq(p);
   const size_t Dk = p->Dk, Dv = p->Dv;
   Layout L{};
@@ -146,6 +160,13 @@ Layout layout(const gdr2_problem* p, bool bwd, int nseq = 0) {
   } else {
     scan_segments(p, L.nseg, L.seg_len);
   }
+  if (bwd && G > 1) {
+    const size_t n = (size_t)p->B * p->T * p->H * Dk;
+    L.pQ = take(n);
+    L.pK = take(n);
+    L.pB = take(n);
+    L.pG = take(n);
+  }
   if (L.nseg > 1) {
     const size_t nvs = (size_t)p->B * p->H * L.nseg;
     L.sM = take(nvs * Dk * Dk);
@@ -169,11 +190,14 @@ struct Geo {
   int NT;
   int nscan;
   Varlen vl;
+  int G;  // value heads per key head
 };
 
-Geo make_geo(const gdr2_problem* p, bool bwd, int nseq, const int* cu, void* ws) {
+// p: the value view; G: value heads per key head
+Geo make_geo(const gdr2_problem* p, bool bwd, int nseq, const int* cu, void* ws, int grp = 1) {
   Geo G{};
-  G.L = layout(p, bwd, nseq);
+  G.G = grp;
+  G.L = layout(p, bwd, nseq, grp);
   if (nseq > 0) {
     G.NT = varlen_slots(p, nseq);
     G.nscan = nseq;
@@ -258,6 +282,20 @@ hipError_t timed(int id, hipStream_t st, F&& launch) {
   if (e != hipSuccess) return e;
   g_prof.pending.push_back({id, a, b});
   return hipSuccess;
+}
+
+// ---- grouped value heads: sum each key head's G partials into dq, dk, db, dlog_alpha
+// (p: the value view, so the key heads are p->H / G)
+template <typename TIn>
+hipError_t group_reduce(const gdr2_problem* p, const Geo& G, const Layout& L, void* ws, void* dq, void* dk,
+                        void* db, float* dg, hipStream_t st) {
+  const size_t rows = (size_t)p->B * p->T;
+  const int Hk = p->H / G.G;
+  hipError_t e = launch_group_reduce<TIn>(at<float>(ws, L.pQ), static_cast<TIn*>(dq), rows, Hk, G.G, p->Dk, st);
+  if (e == hipSuccess) e = launch_group_reduce<TIn>(at<float>(ws, L.pK), static_cast<TIn*>(dk), rows, Hk, G.G, p->Dk, st);
+  if (e == hipSuccess) e = launch_group_reduce<TIn>(at<float>(ws, L.pB), static_cast<TIn*>(db), rows, Hk, G.G, p->Dk, st);
+  if (e == hipSuccess) e = launch_group_reduce<float>(at<float>(ws, L.pG), dg, rows, Hk, G.G, p->Dk, st);
+  return e;
 }
 
 // ---- state scans of the bf16 path, sequential or sequence-parallel ---------
@@ -352,6 +390,7 @@ struct FwdRun {
                        at<unsigned char>(ws, L.bK), at<float>(ws, L.bU), at<float>(ws, L.bG),
                        save ? at<unsigned char>(ws, L.bAm) : nullptr, p->B, p->T, p->H, NT};
       ia.vl = G.vl;
+      ia.G = G.G;
       hipError_t e = timed(GDR2_K_FWD_INTRA, st, [&] { return launch_intra_bf16<DK, DV>(ia, st); });
       if (e != hipSuccess) return e;
       ScanArgs sa{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.U, ia.GC, S0, ST, static_cast<bf16_t*>(o),
@@ -370,6 +409,7 @@ struct FwdRun {
                       at<float>(ws, L.Kt), at<float>(ws, L.Qg), at<float>(ws, L.Aqk),
                       at<float>(ws, L.GC), p->T, p->H, NT};
     ia.vl = G.vl;
+    ia.G = G.G;
     hipError_t e = timed(GDR2_K_FWD_INTRA, st, [&] { return launch_fwd_intra<DK, DV, TIn>(ia, p->B, st); });
     if (e != hipSuccess) return e;
     StateArgs<TIn> sa{ia.Y, ia.U, ia.Kt, ia.Qg, ia.Aqk, ia.GC, S0, ST, static_cast<TIn*>(o),
@@ -402,6 +442,7 @@ struct BwdRun {
                        at<unsigned char>(ws, L.bK), at<float>(ws, L.bU), at<float>(ws, L.bG),
                        at<unsigned char>(ws, L.bAm), p->B, p->T, p->H, NT};
       ia.vl = G.vl;
+      ia.G = G.G;
       if (!saved) {
         // recompute: intra-chunk tiles (with A), then the forward scan storing the chunk states and R
         e = timed(GDR2_K_BWD_RECOMPUTE_INTRA, st, [&] { return launch_intra_bf16<DK, DV>(ia, st); });
@@ -430,7 +471,18 @@ struct BwdRun {
                         static_cast<bf16_t*>(dv), static_cast<bf16_t*>(db), static_cast<bf16_t*>(dw), dg,
                         p->B, p->T, p->H, NT, p->scale};
       ca.vl = G.vl;
-      return timed(GDR2_K_BWD_INTRA, st, [&] { return launch_bchunk_bf16<DK, DV>(ca, st); });
+      ca.G = G.G;
+      if (G.G > 1) {
+        ca.Pq = at<float>(ws, L.pQ);
+        ca.Pk = at<float>(ws, L.pK);
+        ca.Pb = at<float>(ws, L.pB);
+        ca.dg = at<float>(ws, L.pG);
+      }
+      return timed(GDR2_K_BWD_INTRA, st, [&] {
+        hipError_t r = launch_bchunk_bf16<DK, DV>(ca, st);
+        if (r == hipSuccess && G.G > 1) r = group_reduce<bf16_t>(p, G, L, ws, dq, dk, db, dg, st);
+        return r;
+      });
     }
     IntraArgs<TIn> ia{static_cast<const TIn*>(q), static_cast<const TIn*>(k),
                       static_cast<const TIn*>(v), g, static_cast<const TIn*>(b),
@@ -438,6 +490,7 @@ struct BwdRun {
                       at<float>(ws, L.Kt), at<float>(ws, L.Qg), at<float>(ws, L.Aqk),
                       at<float>(ws, L.GC), p->T, p->H, NT};
     ia.vl = G.vl;
+    ia.G = G.G;
     StateArgs<TIn> sa{ia.Y, ia.U, ia.Kt, ia.Qg, ia.Aqk, ia.GC, S0, nullptr, nullptr,
                       at<float>(ws, L.Hs), at<float>(ws, L.Rs), p->T, p->H, NT, p->scale};
     sa.vl = G.vl;
@@ -461,9 +514,20 @@ struct BwdRun {
                          static_cast<TIn*>(dv), static_cast<TIn*>(db), static_cast<TIn*>(dw), dg,
                          p->T, p->H, NT, p->scale};
     ca.vl = G.vl;
+    ca.G = G.G;
     e = timed(GDR2_K_BWD_WY, st, [&] { return launch_bwd_wy<DK, DV, TIn>(ca, p->B, st); });
     if (e != hipSuccess) return e;
-    return timed(GDR2_K_BWD_INTRA, st, [&] { return launch_bwd_intra<DK, DV, TIn>(ca, p->B, st); });
+    if (G.G > 1) {  // the key-side gradients of each value head go to the fp32 partials
+      ca.dq = reinterpret_cast<TIn*>(at<float>(ws, L.pQ));
+      ca.dk = reinterpret_cast<TIn*>(at<float>(ws, L.pK));
+      ca.db = reinterpret_cast<TIn*>(at<float>(ws, L.pB));
+      ca.dg = at<float>(ws, L.pG);
+    }
+    return timed(GDR2_K_BWD_INTRA, st, [&] {
+      hipError_t r = launch_bwd_intra<DK, DV, TIn>(ca, p->B, st);
+      if (r == hipSuccess && G.G > 1) r = group_reduce<TIn>(p, G, L, ws, dq, dk, db, dg, st);
+      return r;
+    });
   }
 };
 
@@ -471,11 +535,12 @@ template <int DK, int DV, typename TIn>
 struct RecRun {
   static hipError_t run(const gdr2_problem* p, const void* q, const void* k, const void* v,
                         const float* g, const void* b, const void* w, float* S, void* o, const int* cu,
-                        int nseq, hipStream_t st) {
+                        int nseq, int grp, hipStream_t st) {
     RecurArgs<TIn> ra{static_cast<const TIn*>(q), static_cast<const TIn*>(k),
                       static_cast<const TIn*>(v), g, static_cast<const TIn*>(b),
                       static_cast<const TIn*>(w), S, static_cast<TIn*>(o), p->T, p->H, p->scale};
     ra.cu = cu;
+    ra.G = grp;
     const int nb = cu != nullptr ? nseq : p->B;
     return timed(GDR2_K_RECURRENT, st, [&] { return launch_recurrent<DK, DV, TIn>(ra, nb, st); });
   }
@@ -503,7 +568,8 @@ gdr2_status gdr2_chunk_workspace_bytes(const gdr2_problem* p, int for_backward, 
   if (bytes == nullptr) return GDR2_EINVAL;
   const gdr2_status s = check_problem(p, true);
   if (s != GDR2_OK) return s;
-  *bytes = layout(p, for_backward != 0).total;
+  const gdr2_problem pv = value_view(p);
+  *bytes = layout(&pv, for_backward != 0, 0, group_of(p)).total;
   return GDR2_OK;
 }
 
@@ -517,14 +583,15 @@ gdr2_status chunk_fwd(const gdr2_problem* p, const int32_t* cu, int nseq, const 
   if (s != GDR2_OK) return s;
   if (!all_ok({q, k, v, log_alpha, b, w, o, ws}) || !opt_ok({S0, S_T})) return GDR2_EINVAL;
   if (nseq > 0 && !cu_ok(cu)) return GDR2_EINVAL;
-  const Geo G = make_geo(p, save, nseq, cu, ws);
+  const gdr2_problem pv = value_view(p);
+  const Geo G = make_geo(&pv, save, nseq, cu, ws, group_of(p));
   if (ws_bytes < G.L.total) return GDR2_EWORKSPACE;
-  hipError_t e = build_table(p, G, stream);
+  hipError_t e = build_table(&pv, G, stream);
   if (e != hipSuccess) return GDR2_EHIP;
   if (p->dtype == GDR2_BF16)
-    e = dispatch<FwdRun, bf16_t>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S0, o, S_T, ws, save, G, stream);
+    e = dispatch<FwdRun, bf16_t>(p->Dk, p->Dv, &pv, q, k, v, log_alpha, b, w, S0, o, S_T, ws, save, G, stream);
   else
-    e = dispatch<FwdRun, float>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S0, o, S_T, ws, save, G, stream);
+    e = dispatch<FwdRun, float>(p->Dk, p->Dv, &pv, q, k, v, log_alpha, b, w, S0, o, S_T, ws, save, G, stream);
   return hip_status(e, stream);
 }
 
@@ -539,15 +606,16 @@ gdr2_status chunk_bwd(const gdr2_problem* p, const int32_t* cu, int nseq, const 
       !opt_ok({S0, dS_T, dS0}))
     return GDR2_EINVAL;
   if (nseq > 0 && !cu_ok(cu)) return GDR2_EINVAL;
-  const Geo G = make_geo(p, true, nseq, cu, ws);
+  const gdr2_problem pv = value_view(p);
+  const Geo G = make_geo(&pv, true, nseq, cu, ws, group_of(p));
   if (ws_bytes < G.L.total) return GDR2_EWORKSPACE;
-  hipError_t e = build_table(p, G, stream);
+  hipError_t e = build_table(&pv, G, stream);
   if (e != hipSuccess) return GDR2_EHIP;
   if (p->dtype == GDR2_BF16)
-    e = dispatch<BwdRun, bf16_t>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S0, dout, dS_T, dq,
+    e = dispatch<BwdRun, bf16_t>(p->Dk, p->Dv, &pv, q, k, v, log_alpha, b, w, S0, dout, dS_T, dq,
                                  dk, dv, dlog_alpha, db, dw, dS0, ws, saved, G, stream);
   else
-    e = dispatch<BwdRun, float>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S0, dout, dS_T, dq,
+    e = dispatch<BwdRun, float>(p->Dk, p->Dv, &pv, q, k, v, log_alpha, b, w, S0, dout, dS_T, dq,
                                 dk, dv, dlog_alpha, db, dw, dS0, ws, saved, G, stream);
   return hip_status(e, stream);
 }
@@ -560,10 +628,11 @@ gdr2_status recurrent(const gdr2_problem* p, const int32_t* cu, int nseq, const 
   if (!all_ok({q, k, v, log_alpha, b, w, S, o})) return GDR2_EINVAL;
   if (nseq > 0 && !cu_ok(cu)) return GDR2_EINVAL;
   hipError_t e;
+  const gdr2_problem pv = value_view(p);
   if (p->dtype == GDR2_BF16)
-    e = dispatch<RecRun, bf16_t>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S, o, cu, nseq, stream);
+    e = dispatch<RecRun, bf16_t>(p->Dk, p->Dv, &pv, q, k, v, log_alpha, b, w, S, o, cu, nseq, group_of(p), stream);
   else
-    e = dispatch<RecRun, float>(p->Dk, p->Dv, p, q, k, v, log_alpha, b, w, S, o, cu, nseq, stream);
+    e = dispatch<RecRun, float>(p->Dk, p->Dv, &pv, q, k, v, log_alpha, b, w, S, o, cu, nseq, group_of(p), stream);
   return hip_status(e, stream);
 }
 
@@ -610,7 +679,8 @@ gdr2_status gdr2_varlen_workspace_bytes(const gdr2_problem* p, int32_t n_seqs, i
   if (bytes == nullptr || n_seqs <= 0) return GDR2_EINVAL;
   const gdr2_status s = check_problem(p, true, n_seqs);
   if (s != GDR2_OK) return s;
-  *bytes = layout(p, for_backward != 0, n_seqs).total;
+  const gdr2_problem pv = value_view(p);
+  *bytes = layout(&pv, for_backward != 0, n_seqs, group_of(p)).total;
   return GDR2_OK;
 }
 

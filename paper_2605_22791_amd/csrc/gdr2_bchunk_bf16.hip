@@ -135,20 +135,29 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   // zero, which makes every term they could add to a valid row vanish (their
   // dT, dA_qk, dR and dG are zero), and their outputs are not written.
   const int len = cp.len;
-  const size_t KST = (size_t)H * DK, VST = (size_t)H * DV;  // token strides
-  const size_t kb0 = row0 * KST + (size_t)h * DK, vb0 = row0 * VST + (size_t)h * DV;
+  // key-side inputs (q, k, g, b) live on the H / G key heads (value head h reads
+  // key head h / G); with G > 1 (part) the key-side gradients of this value head
+  // go to fp32 partials on the value-head axis, which the group reduction sums
+  const int HK = H / a.G, hk = h / a.G;
+  const bool part = a.Pq != nullptr;
+  const size_t KST = (size_t)HK * DK, VST = (size_t)H * DV;  // token strides
+  const size_t kb0 = row0 * KST + (size_t)hk * DK, vb0 = row0 * VST + (size_t)h * DV;
+  const size_t ko0 = part ? row0 * ((size_t)H * DK) + (size_t)h * DK : kb0;  // key-side outputs
   const int i = wave;  // the row block this wave owns
   const int kbl = i >> 1;
 
-  // per-chunk bases (uniform) and 32-bit lane offsets: KST = H Dk, VST = H Dv
+  // per-chunk bases (uniform) and 32-bit lane offsets: KST = (H / G) Dk, VST = H Dv
   const __bf16* Qp = reinterpret_cast<const __bf16*>(a.q) + kb0;
   const __bf16* Kp = reinterpret_cast<const __bf16*>(a.k) + kb0;
   const __bf16* Bp = reinterpret_cast<const __bf16*>(a.b) + kb0;
   const float* Gp0 = a.g + kb0;
-  __bf16* dQp = reinterpret_cast<__bf16*>(a.dq) + kb0;
-  __bf16* dKp = reinterpret_cast<__bf16*>(a.dk) + kb0;
-  __bf16* dBp = reinterpret_cast<__bf16*>(a.db) + kb0;
-  float* dGp = a.dg + kb0;
+  __bf16* dQp = reinterpret_cast<__bf16*>(a.dq) + ko0;
+  __bf16* dKp = reinterpret_cast<__bf16*>(a.dk) + ko0;
+  __bf16* dBp = reinterpret_cast<__bf16*>(a.db) + ko0;
+  float* pQp = part ? a.Pq + ko0 : nullptr;
+  float* pKp = part ? a.Pk + ko0 : nullptr;
+  float* pBp = part ? a.Pb + ko0 : nullptr;
+  float* dGp = a.dg + ko0;
   const __bf16* Vp = reinterpret_cast<const __bf16*>(a.v) + vb0;
   const __bf16* Wp = reinterpret_cast<const __bf16*>(a.w) + vb0;
   const __bf16* dOp = reinterpret_cast<const __bf16*>(a.dout) + vb0;
@@ -157,7 +166,7 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   const float* Hc = a.Hs + ch * DK * DV;
   const float* DHc = a.DH + ch * DK * DV;
   const float* Rc = a.Rs + ch * CH * DV;
-  const int kst = H * DK, vst = H * DV;
+  const int kst = HK * DK, kso = part ? H * DK : kst, vst = H * DV;
 
   // staging role: chunk row grow (block = wave), channels 16 cb + 4 cq + (0..3)
   const int rl = lane >> 2, cq = lane & 3, grow = 16 * wave + rl;
@@ -527,11 +536,17 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
           }
         }
       }
-      const int o = (rb + u) * kst + c;
+      const int o = (rb + u) * kso + c;
       if (rb + u < len) {
-        dQp[o] = (__bf16)dq;
-        dKp[o] = (__bf16)(dEg * bv + dKg);
-        dBp[o] = (__bf16)(dEg * kv);
+        if (part) {
+          pQp[o] = dq;
+          pKp[o] = dEg * bv + dKg;
+          pBp[o] = dEg * kv;
+        } else {
+          dQp[o] = (__bf16)dq;
+          dKp[o] = (__bf16)(dEg * bv + dKg);
+          dBp[o] = (__bf16)(dEg * kv);
+        }
       }
       dgl[u] = dq * qv - dKg * kv + dEg * bv * kv;
       tailp += x3[u] * kv * tl;
@@ -561,10 +576,10 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       off += sTL[(par * 4 + i2) * 16 + r16];
       if (i2 > i) off += sBT[(par * 4 + i2) * 16 + r16];
     }
-    if (rb + 0 < len) dGp[(rb + 0) * kst + c] = s0 + off;
-    if (rb + 1 < len) dGp[(rb + 1) * kst + c] = s1 + off;
-    if (rb + 2 < len) dGp[(rb + 2) * kst + c] = s2 + off;
-    if (rb + 3 < len) dGp[(rb + 3) * kst + c] = s3 + off;
+    if (rb + 0 < len) dGp[(rb + 0) * kso + c] = s0 + off;
+    if (rb + 1 < len) dGp[(rb + 1) * kso + c] = s1 + off;
+    if (rb + 2 < len) dGp[(rb + 2) * kso + c] = s2 + off;
+    if (rb + 3 < len) dGp[(rb + 3) * kso + c] = s3 + off;
     if (cb + 1 < NCB) GDR2_STAGE(par ^ 1)
     __syncthreads();
   }

@@ -165,10 +165,10 @@ __global__ __launch_bounds__(512) void bwd_wy_kernel(BwdChunkArgs<TIn> a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int H = a.H;
-  const size_t rs = (size_t)H * DK, rsv = (size_t)H * DV;
+  const size_t rs = (size_t)(H / a.G) * DK, rsv = (size_t)H * DV;  // key side on the H / G key heads
   const size_t row0 = cp.row0;
   const int len = cp.len;  // rows in use: the rest read as zero and are not written
-  const size_t kbase = row0 * rs + (size_t)h * DK;
+  const size_t kbase = row0 * rs + (size_t)(h / a.G) * DK;
   const size_t vbase = row0 * rsv + (size_t)h * DV;
   const size_t ch = cp.ch;
 
@@ -391,10 +391,15 @@ __global__ __launch_bounds__(512) void bwd_intra_kernel(BwdChunkArgs<TIn> a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int H = a.H;
-  const size_t rs = (size_t)H * DK, rsv = (size_t)H * DV;
+  const size_t rs = (size_t)(H / a.G) * DK, rsv = (size_t)H * DV;  // key side on the H / G key heads
   const size_t row0 = cp.row0;
   const int len = cp.len;  // rows in use: the rest read as zero and are not written
-  const size_t kbase = row0 * rs + (size_t)h * DK;
+  const size_t kbase = row0 * rs + (size_t)(h / a.G) * DK;
+  // key-side gradients: with grouped value heads (G > 1) this value head's
+  // contribution goes, on the value-head axis, to the fp32 partials the group
+  // reduction sums
+  const size_t rso = a.G > 1 ? (size_t)H * DK : rs;
+  const size_t kobase = a.G > 1 ? row0 * rso + (size_t)h * DK : kbase;
   const size_t vbase = row0 * rsv + (size_t)h * DV;
   const size_t ch = cp.ch;
 
@@ -509,7 +514,7 @@ __global__ __launch_bounds__(512) void bwd_intra_kernel(BwdChunkArgs<TIn> a) {
       const float rf = expf(sG[(16 * i + 15) * LS + c] - G);
       const float gam = expf(G);
       const float tail = expf(sG[(CH - 1) * LS + c] - G);
-      const size_t off = kbase + r * rs + c;
+      const size_t off = kbase + r * rs + c, offo = kobase + r * rso + c;
       const bool rin = r < len;
       const float kv = to_fz(a.k + off, rin), bv = to_fz(a.b + off, rin), qv = to_fz(a.q + off, rin);
       float dEg = DEg[r * DK + c] + lf * P1[u];
@@ -533,9 +538,9 @@ __global__ __launch_bounds__(512) void bwd_intra_kernel(BwdChunkArgs<TIn> a) {
         }
       }
       if (rin) {
-        put(a.db + off, dEg * kv);
-        put(a.dk + off, dEg * bv + dKg);
-        put(a.dq + off, dq);
+        put(a.db + offo, dEg * kv);
+        put(a.dk + offo, dEg * bv + dKg);
+        put(a.dq + offo, dq);
       }
       keep[q][u] = dq * qv - dKg * kv + dEg * bv * kv;
       tailpart += dKt[u] * kv * tail;
@@ -576,7 +581,7 @@ __global__ __launch_bounds__(512) void bwd_intra_kernel(BwdChunkArgs<TIn> a) {
     for (int s = seg + 1; s < NSEG; ++s) off += sdG[(s * RPS) * LS + c];
     __syncthreads();
     for (int r = seg * RPS; r < (seg + 1) * RPS; ++r)
-      if (r < len) a.dg[kbase + r * rs + c] = sdG[r * LS + c] + off;
+      if (r < len) a.dg[kobase + r * rso + c] = sdG[r * LS + c] + off;
   }
 }
 

@@ -32,10 +32,10 @@ __global__ __launch_bounds__(512) void fwd_intra_kernel(IntraArgs<TIn> a) {
   const int h = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int H = a.H;
-  const size_t rs = (size_t)H * DK, rsv = (size_t)H * DV;
+  const size_t rs = (size_t)(H / a.G) * DK, rsv = (size_t)H * DV;  // key side on the H / G key heads
   const size_t row0 = cp.row0;
   const int len = cp.len;  // rows in use: the rest read as zero and are not written
-  const size_t kbase = row0 * rs + (size_t)h * DK;
+  const size_t kbase = row0 * rs + (size_t)(h / a.G) * DK;
   const size_t vbase = row0 * rsv + (size_t)h * DV;
   const size_t ch = cp.ch;
 

@@ -111,7 +111,9 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
   const __bf16* Bg = reinterpret_cast<const __bf16*>(a.b);
   const __bf16* Wg = reinterpret_cast<const __bf16*>(a.w);
   const size_t row0 = cp.row0;
-  auto kofs = [&](int r) -> size_t { return (row0 + min(r, len - 1)) * ((size_t)H * DK) + (size_t)h * DK; };
+  // key-side tensors (q, k, g, b) live on the H / G key heads: value head h reads key head h / G
+  const int HK = H / a.G, hk = h / a.G;
+  auto kofs = [&](int r) -> size_t { return (row0 + min(r, len - 1)) * ((size_t)HK * DK) + (size_t)hk * DK; };
   auto vofs = [&](int r) -> size_t { return (row0 + min(r, len - 1)) * ((size_t)H * DV) + (size_t)h * DV; };
 
   // ---- loads: g in scan layout (NG rows of 4 channels per thread), k

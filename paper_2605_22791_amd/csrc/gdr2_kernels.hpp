@@ -92,6 +92,7 @@ struct IntraArgs {
   float* GC;
   int T, H, NT;
   Varlen vl{};
+  int G = 1;  // grouped value heads: H value heads share H / G key heads (q, k, g, b)
 };
 
 // Arguments of the sequential forward state kernel.
@@ -157,6 +158,7 @@ struct BwdChunkArgs {
   int T, H, NT;
   float scale;
   Varlen vl{};
+  int G = 1;  // grouped value heads (as in IntraArgs); G > 1: dq, dk, db, dg are per-value-head partials
 };
 
 // One recurrent (decode) call over T tokens, state updated in place.
@@ -173,6 +175,7 @@ struct RecurArgs {
   int T, H;
   float scale;
   const int* cu = nullptr;  // packed sequences: tokens cu[s] .. cu[s+1) of sequence s (B = 1)
+  int G = 1;                // grouped value heads (as in IntraArgs)
 };
 
 // ---------------------------------------------------------------------------
@@ -223,6 +226,7 @@ struct IntraBf16Args {
   unsigned char* Am;  // nullable: A for the backward
   int B, T, H, NT;
   Varlen vl{};
+  int G = 1;  // grouped value heads: H value heads share H / G key heads (q, k, g, b)
 };
 
 // Sequence-parallel scans: with nseg > 1 every sequence is cut into nseg
@@ -309,6 +313,14 @@ struct BChunkBf16Args {
   int B, T, H, NT;
   float scale;
   Varlen vl{};
+  // grouped value heads: H value heads share H / G key heads.  With G > 1 the
+  // key-side gradients of each value head go, in fp32 and on the value-head
+  // axis, to Pq, Pk, Pb and to dg (then a (B*T, H, Dk) fp32 partial), and the
+  // group reduction sums them.
+  int G = 1;
+  float* Pq = nullptr;
+  float* Pk = nullptr;
+  float* Pb = nullptr;
 };
 
 template <int DK, int DV>
@@ -334,6 +346,11 @@ template <int DK, int DV, typename TIn>
 hipError_t launch_bwd_intra(const BwdChunkArgs<TIn>& a, int B, hipStream_t st);
 template <int DK, int DV, typename TIn>
 hipError_t launch_recurrent(const RecurArgs<TIn>& a, int B, hipStream_t st);
+
+// Grouped value heads: out[r, h, c] = sum_{j < G} P[r, h * G + j, c] for rows
+// r < rows, key heads h < Hk, channels c < D (P fp32 on the value-head axis).
+template <typename TOut>
+hipError_t launch_group_reduce(const float* P, TOut* out, size_t rows, int Hk, int G, int D, hipStream_t st);
 
 // Builds the chunk table of a packed call (Varlen) from cu_seqlens: lengths
 // are clamped into [0, T] and the chunk count to ncmax, so malformed offsets

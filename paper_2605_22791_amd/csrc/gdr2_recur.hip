@@ -42,15 +42,16 @@ __global__ __launch_bounds__(256) void recurrent_kernel(RecurArgs<TIn> a) {
     t1 = min(max(a.cu[bb + 1], t0), T);
     rbase = 0;
   }
+  const int HK = H / a.G, hk = h / a.G;  // key side (q, k, g, b) on the H / G key heads
   for (int t = t0; t < t1; ++t) {
-    const size_t row = (rbase + t) * H + h;
+    const size_t row = (rbase + t) * H + h, rowk = (rbase + t) * HK + hk;
     float kq = 0.f;
     for (int c = tid; c < DK; c += NTHR) {
-      const float kv = to_f(a.k[row * DK + c]), qv = to_f(a.q[row * DK + c]);
-      sAl[c] = expf(a.g[row * DK + c]);
+      const float kv = to_f(a.k[rowk * DK + c]), qv = to_f(a.q[rowk * DK + c]);
+      sAl[c] = expf(a.g[rowk * DK + c]);
       sK[c] = kv;
       sQ[c] = qv;
-      sE[c] = to_f(a.b[row * DK + c]) * kv;
+      sE[c] = to_f(a.b[rowk * DK + c]) * kv;
       kq += kv * qv;
     }
     for (int v = tid; v < DV; v += NTHR) sZ[v] = to_f(a.w[row * DV + v]) * to_f(a.v[row * DV + v]);

@@ -160,6 +160,19 @@ def make_packed(lengths, H, Dk, Dv, seed, dtype="bf16", decay_shift=0.0, s0_std=
     return d
 
 
+def make_grouped(B, T, H, Hv, Dk, Dv, seed, dtype="bf16", decay_shift=0.0, s0_std=0.0, with_dST=False):
+    """Grouped value heads (Hv = G * H): the key side (q, k, log_alpha, b) is
+    drawn with H heads and the value side (v, w, do and the states) with Hv
+    heads, each exactly as make_inputs draws it."""
+    kd = make_inputs(B, T, H, Dk, Dv, seed, dtype=dtype, decay_shift=decay_shift)
+    vd = make_inputs(B, T, Hv, Dk, Dv, seed + 7919, dtype=dtype, s0_std=s0_std, with_dST=with_dST)
+    d = dict(kd)
+    for n in ("v", "w", "do", "S0", "dST"):
+        d[n] = vd[n]
+    d["H"], d["Hv"] = H, Hv
+    return d
+
+
 def config(idx, decay="channel", **overrides):
     """Inputs of workload ``idx`` (config 1 takes decay="channel" or "scalar")."""
     c = dict(CONFIGS[idx])

@@ -304,3 +304,23 @@ def test_varlen_workspace_size():
             _, total, NC = ws_layout_bf16(1, T, H, Dk, Dv, bwd=bool(bwd), nseq=N)
             assert NC == H * (T // 64 + N)
             assert g2.gdr2_varlen_workspace_bytes(p, N, bwd) == total, (T, N, bwd)
+
+
+def test_grouped_value_heads_validation_and_workspace():
+    """Hv must be a multiple of H (0 means Hv = H).  A grouped problem runs per
+    value head (workspace of the Hv-head problem) and its backward adds four fp32
+    (B, T, Hv, Dk) regions for the per-value-head key-side gradients."""
+    from tests.gpu_common import ws_layout_bf16, seg_buffer_bytes
+    assert _fwd(_prob(H=4, Hv=6)) == g2.GDR2_EINVAL
+    assert _bwd(_prob(H=4, Hv=-4)) == g2.GDR2_EINVAL
+    n = ctypes.c_size_t(0)
+    assert g2.lib().gdr2_chunk_workspace_bytes(ctypes.byref(_prob(H=4, Hv=10)), 1, ctypes.byref(n)) == \
+        g2.GDR2_EINVAL
+    r = lambda x: (x * 4 + 255) // 256 * 256
+    for (B, T, H, Hv, Dk, Dv) in [(2, 256, 4, 8, 128, 64), (1, 100, 2, 8, 64, 128), (2, 128, 4, 4, 128, 128)]:
+        p = _prob(B=B, T=T, H=H, Hv=Hv, Dk=Dk, Dv=Dv)
+        same = _prob(B=B, T=T, H=Hv, Dk=Dk, Dv=Dv)   # the value-head problem
+        assert g2.gdr2_chunk_workspace_bytes(p, 0) == g2.gdr2_chunk_workspace_bytes(same, 0)
+        _, base, _ = ws_layout_bf16(B, T, Hv, Dk, Dv, bwd=True)
+        part = 4 * r(B * T * Hv * Dk) if Hv > H else 0
+        assert g2.gdr2_chunk_workspace_bytes(p, 1) == base + part + seg_buffer_bytes(B, T, Hv, Dk, Dv)

@@ -182,3 +182,41 @@ def test_packed_adjoint_matches_finite_differences():
         num = fd.fd_directional(fwd, inputs, direction, do, dST, h=1e-6)
         ana = float(np.sum(g[key[n]] * direction[n]))
         assert abs(num - ana) < 1e-6 * (1 + abs(ana)), (n, num, ana)
+
+
+def test_grouped_value_heads_adjoint():
+    """Grouped value heads (Sec. 3.5, App. C.1): G = 1 is the plain operator; for
+    G = 3 every gradient of the grouped forward matches central finite
+    differences along random directions (key-side ones are sums over the group),
+    and value heads that receive identical v, w and S0 give identical outputs."""
+    from oracle import gdr2_grouped_fwd, gdr2_grouped_bwd, gdr2_recurrent_fwd
+    from oracle import fd
+    d = small_problem(1, 9, 2, 4, 3, seed=31)
+    o1, S1 = gdr2_grouped_fwd(d["q"], d["k"], d["v"], d["log_alpha"], d["b"], d["w"], d["S0"], d["scale"])
+    o0, S0r = gdr2_recurrent_fwd(d["q"], d["k"], d["v"], d["log_alpha"], d["b"], d["w"], d["S0"], d["scale"])
+    assert np.array_equal(o1, o0) and np.array_equal(S1, S0r)
+    rng = np.random.default_rng(7)
+    G, Hv = 3, 6
+    v = rng.standard_normal((1, 9, Hv, 3))
+    w = 1 / (1 + np.exp(-rng.standard_normal((1, 9, Hv, 3))))
+    S0 = rng.standard_normal((1, Hv, 4, 3))
+    inputs = {n: d[n].astype(np.float64) for n in ("q", "k", "log_alpha", "b")}
+    inputs.update(v=v, w=w, S0=S0)
+    do = rng.standard_normal((1, 9, Hv, 3))
+    dST = rng.standard_normal((1, Hv, 4, 3))
+
+    def fwd(q, k, v, log_alpha, b, w, S0):
+        return gdr2_grouped_fwd(q, k, v, log_alpha, b, w, S0, d["scale"])
+
+    g = gdr2_grouped_bwd(inputs["q"], inputs["k"], v, inputs["log_alpha"], inputs["b"], w, S0, do, dST, d["scale"])
+    assert g["dq"].shape == d["q"].shape and g["dv"].shape == v.shape
+    key = {"q": "dq", "k": "dk", "v": "dv", "log_alpha": "dg", "b": "db", "w": "dw", "S0": "dS0"}
+    for n in key:
+        direction = {n: rng.standard_normal(inputs[n].shape)}
+        num = fd.fd_directional(fwd, inputs, direction, do, dST, h=1e-6)
+        ana = float(np.sum(g[key[n]] * direction[n]))
+        assert abs(num - ana) < 1e-6 * (1 + abs(ana)), (n, num, ana)
+    v2, w2, S02 = v.copy(), w.copy(), S0.copy()
+    v2[:, :, 1], w2[:, :, 1], S02[:, 1] = v2[:, :, 0], w2[:, :, 0], S02[:, 0]   # heads 0, 1 share key head 0
+    o2, _ = fwd(inputs["q"], inputs["k"], v2, inputs["log_alpha"], inputs["b"], w2, S02)
+    assert np.array_equal(o2[:, :, 0], o2[:, :, 1])
