@@ -26,6 +26,10 @@ Modules:
                 linear attention, Mamba-2 decay, KDA and Gated DeltaNet (Sec. 2).
   brute      -- dense products of explicit per-token transition matrices.
   fd         -- central finite differences of a scalar loss.
+  layer      -- the input stage around the operator: per-head L2 normalisation
+                of q and k (App. D.2) and the fp32 log-decay activation
+                g = -exp(a) softplus(f + delta) (App. C.1), their adjoints, and
+                the fused operator (stage, then the recurrence) with its backward.
 
 Parity pins (tests/test_oracle_*.py) tie each function to something other than
 itself: closed forms, tied-gate reductions, brute force and finite differences.
@@ -34,4 +38,5 @@ itself: closed forms, tied-gate reductions, brute force and finite differences.
 from .recurrent import gdr2_recurrent_fwd, gdr2_recurrent_bwd, gdr2_step_states  # noqa: F401
 from .recurrent import gdr2_packed_fwd, gdr2_packed_bwd, gdr2_grouped_fwd, gdr2_grouped_bwd  # noqa: F401
 from .chunkwise import gdr2_chunk_fwd_ref, gdr2_chunk_bwd_ref  # noqa: F401
-from . import limits, brute, fd  # noqa: F401
+from .layer import gdr2_fused_fwd, gdr2_fused_bwd  # noqa: F401
+from . import limits, brute, fd, layer  # noqa: F401

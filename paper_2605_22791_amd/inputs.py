@@ -26,7 +26,7 @@ from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
 
-__all__ = ["bf16_round", "make_inputs", "config", "CONFIGS", "decode_inputs"]
+__all__ = ["bf16_round", "make_inputs", "config", "CONFIGS", "decode_inputs", "make_fused"]
 
 
 def bf16_round(x):
@@ -171,6 +171,53 @@ def make_grouped(B, T, H, Hv, Dk, Dv, seed, dtype="bf16", decay_shift=0.0, s0_st
         d[n] = vd[n]
     d["H"], d["Hv"] = H, Hv
     return d
+
+
+def make_fused(B, T, H, Dk, Dv, seed, dtype="bf16", Hv=None, lengths=None, s0_std=0.0, with_dST=False):
+    """Raw projections for the fused input stage (normalisation and decay
+    activation in the operator): q and k as the projections leave them
+    (normal, not normalised), the decay projection output f, one decay
+    magnitude a per key head and one bias delta per key channel.
+
+    Recipe (children of SeedSequence(seed), one per draw, in this order):
+      q, k ~ N(0, 1)                              (B, T, H, Dk), bf16-rounded for bf16
+      v ~ N(0, 1), w = sigmoid(N(0, 1))           (B, T, Hv, Dv), bf16-rounded
+      f ~ N(0, 1)                                 (B, T, H, Dk), float32
+      b = sigmoid(N(0, 1))                        (B, T, H, Dk), bf16-rounded
+      a = log(U[1, 16])                           (H,), float32
+      delta ~ U[-6.9, -2.25]                      (H, Dk), float32 (the usual range of the
+                                                  decay-bias initialisation: softplus(delta) in
+                                                  about [1e-3, 1e-1])
+      S0 = s0_std N(0, 1), do ~ N(0, 1), dS_T ~ N(0, 1) on the value heads.
+    lengths: a packed batch (B = 1, T = sum) with cu_seqlens and per-sequence
+    states (n_seqs, Hv, Dk, Dv)."""
+    f32 = np.float32
+    Hv = H if Hv is None else Hv
+    if lengths is not None:
+        lengths = [int(x) for x in lengths]
+        B, T = 1, sum(lengths)
+        if T <= 0:
+            raise ValueError("a packed batch needs at least one token")
+    NS = len(lengths) if lengths is not None else B
+    kids = np.random.SeedSequence(seed).spawn(11)
+    rnd = (lambda x: bf16_round(x)) if dtype == "bf16" else (lambda x: x)
+    q = _draw(kids[0], (B, T, H, Dk), rnd)
+    k = _draw(kids[1], (B, T, H, Dk), rnd)
+    v = _draw(kids[2], (B, T, Hv, Dv), rnd)
+    f = _draw(kids[3], (B, T, H, Dk))
+    b = _draw(kids[4], (B, T, H, Dk), lambda x: rnd(_sigmoid(x)))
+    w = _draw(kids[5], (B, T, Hv, Dv), lambda x: rnd(_sigmoid(x)))
+    a = np.log(np.random.default_rng(kids[6]).uniform(1.0, 16.0, size=H)).astype(f32)
+    delta = np.random.default_rng(kids[7]).uniform(-6.9, -2.25, size=(H, Dk)).astype(f32)
+    S0 = _draw(kids[8], (NS, Hv, Dk, Dv), lambda x: (s0_std * x).astype(f32)) if s0_std > 0 else None
+    do = _draw(kids[9], (B, T, Hv, Dv), rnd)
+    dST = _draw(kids[10], (NS, Hv, Dk, Dv)) if with_dST else None
+    out = dict(q=q, k=k, v=v, f=f, a=a, delta=delta, b=b, w=w, S0=S0, do=do, dST=dST,
+               scale=float(1.0 / np.sqrt(Dk)), dtype=dtype, B=B, T=T, H=H, Hv=Hv, Dk=Dk, Dv=Dv, eps=1e-6)
+    if lengths is not None:
+        out["cu_seqlens"] = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int32)
+        out["lengths"] = lengths
+    return out
 
 
 def config(idx, decay="channel", **overrides):

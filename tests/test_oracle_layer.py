@@ -1,0 +1,190 @@
+"""Pins of the layer-side input stage of the oracle (App. C.1, App. D.1 - D.2).
+
+The query/key normalisation, the log-decay activation g = -exp(a) softplus(f +
+delta) and their adjoints are tied to hand-worked values, closed forms the
+functions reduce to, invariances and central finite differences; the fused
+operator is tied to the plain recurrence on inputs chosen so that the stage is
+the identity, and its adjoint to finite differences of the whole chain.  A
+planted mistake (a dropped radial term in the normalisation VJP) must fail.
+CPU only.
+"""
+
+import numpy as np
+import pytest
+
+from oracle import fd, gdr2_recurrent_fwd
+from oracle.layer import (decay_activation, decay_activation_vjp, gdr2_fused_bwd, gdr2_fused_fwd, l2norm,
+                          l2norm_vjp, softplus)
+from paper_2605_22791_amd.inputs import make_fused
+from tests.helpers import rel_l2
+
+
+def test_L1_l2norm_worked_values():
+    # (3, 4) has norm 5; with eps = 11 the divisor is sqrt(25 + 11) = 6
+    assert np.allclose(l2norm(np.array([3.0, 4.0]), eps=0.0), [0.6, 0.8], rtol=0, atol=1e-15)
+    assert np.allclose(l2norm(np.array([3.0, 4.0]), eps=11.0), [0.5, 2.0 / 3.0], rtol=0, atol=1e-15)
+    # rows are independent; the last axis is the one normalised
+    x = np.array([[[1.0, 0.0, 0.0]], [[0.0, -2.0, 0.0]]])
+    assert np.array_equal(l2norm(x, eps=0.0), np.array([[[1.0, 0.0, 0.0]], [[0.0, -1.0, 0.0]]]))
+
+
+def test_L2_l2norm_unit_norm_and_scale_invariance():
+    rng = np.random.default_rng(1)
+    x = rng.standard_normal((5, 7, 16))
+    y = l2norm(x, eps=0.0)
+    assert np.allclose(np.linalg.norm(y, axis=-1), 1.0, atol=1e-14)
+    assert np.allclose(l2norm(3.7 * x, eps=0.0), y, atol=1e-14)
+    # same direction: y ||x|| == x
+    assert np.allclose(y * np.linalg.norm(x, axis=-1, keepdims=True), x, atol=1e-13)
+
+
+@pytest.mark.parametrize("eps", [0.0, 1e-6, 0.5])
+def test_L3_l2norm_vjp_finite_differences(eps):
+    rng = np.random.default_rng(2)
+    x = rng.standard_normal((3, 6))
+    dy = rng.standard_normal((3, 6))
+    got = l2norm_vjp(x, dy, eps)
+    h = 1e-6
+    fdg = np.zeros_like(x)
+    for i in np.ndindex(x.shape):
+        xp, xm = x.copy(), x.copy()
+        xp[i] += h
+        xm[i] -= h
+        fdg[i] = (np.sum(l2norm(xp, eps) * dy) - np.sum(l2norm(xm, eps) * dy)) / (2 * h)
+    assert rel_l2(got, fdg) < 1e-8
+
+
+def test_L4_l2norm_vjp_is_orthogonal_to_x_without_eps():
+    """Scale invariance of x / ||x|| makes its gradient tangent: <x, dx> = 0."""
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((4, 32))
+    dx = l2norm_vjp(x, rng.standard_normal((4, 32)), eps=0.0)
+    assert np.max(np.abs(np.sum(x * dx, axis=-1))) < 1e-13
+
+
+def test_L5_planted_vjp_mistake_is_caught():
+    """A VJP without the radial term (dx = r dy) fails the finite-difference pin."""
+    rng = np.random.default_rng(4)
+    x = rng.standard_normal((2, 5))
+    dy = rng.standard_normal((2, 5))
+    wrong = dy / np.sqrt(np.sum(x * x, axis=-1, keepdims=True) + 1e-6)
+    h = 1e-6
+    fdg = np.zeros_like(x)
+    for i in np.ndindex(x.shape):
+        xp, xm = x.copy(), x.copy()
+        xp[i] += h
+        xm[i] -= h
+        fdg[i] = (np.sum(l2norm(xp) * dy) - np.sum(l2norm(xm) * dy)) / (2 * h)
+    assert rel_l2(wrong, fdg) > 1e-2
+    assert rel_l2(l2norm_vjp(x, dy), fdg) < 1e-8
+
+
+def test_L6_softplus_closed_forms():
+    assert abs(softplus(0.0) - np.log(2.0)) < 1e-16
+    x = np.linspace(-30.0, 30.0, 121)
+    # softplus(x) - softplus(-x) = x and e^{softplus(x)} = 1 + e^x
+    assert np.max(np.abs(softplus(x) - softplus(-x) - x)) < 1e-13
+    assert np.max(np.abs(np.exp(softplus(x)) / (1.0 + np.exp(x)) - 1.0)) < 1e-13
+    # far tails: x + e^-x for large x, e^x (not 0) for very negative x
+    assert softplus(60.0) == 60.0
+    assert abs(softplus(-60.0) / np.exp(-60.0) - 1.0) < 1e-14
+
+
+def test_L7_decay_activation_closed_forms():
+    """exp(g) = (1 + e^{f + delta})^(-exp(a)): the logistic sigma(-(f + delta))
+    for a = 0, its square for a = log 2."""
+    rng = np.random.default_rng(5)
+    f = rng.standard_normal((2, 3, 2, 4)) * 3.0
+    delta = rng.standard_normal((2, 4))
+    x = f + delta
+    g0 = decay_activation(f, np.zeros(2), delta)
+    assert np.max(np.abs(np.exp(g0) - 1.0 / (1.0 + np.exp(x)))) < 1e-14
+    g1 = decay_activation(f, np.array([np.log(2.0), 0.0]), delta)
+    assert np.max(np.abs(np.exp(g1[:, :, 0]) - (1.0 + np.exp(x[:, :, 0])) ** -2)) < 1e-14
+    assert np.max(np.abs(g1[:, :, 1] - g0[:, :, 1])) < 1e-15
+    # a per key head, delta per key channel: shifting delta[h, c] moves exactly channel c of head h
+    d2 = delta.copy()
+    d2[1, 2] += 0.3
+    g2 = decay_activation(f, np.zeros(2), d2)
+    changed = np.abs(g2 - g0) > 0
+    assert changed[:, :, 1, 2].all() and changed.sum() == changed[:, :, 1, 2].size
+
+
+def test_L8_decay_activation_vjp_finite_differences():
+    rng = np.random.default_rng(6)
+    f = rng.standard_normal((2, 3, 2, 4))
+    a = rng.standard_normal(2) * 0.5
+    delta = rng.standard_normal((2, 4))
+    dg = rng.standard_normal(f.shape)
+    df, da, dd = decay_activation_vjp(f, a, delta, dg)
+    h = 1e-6
+
+    def L(f_, a_, d_):
+        return float(np.sum(decay_activation(f_, a_, d_) * dg))
+
+    for x, got, mk in ((f, df, lambda z: (z, a, delta)), (a, da, lambda z: (f, z, delta)),
+                       (delta, dd, lambda z: (f, a, z))):
+        fdg = np.zeros_like(x)
+        for i in np.ndindex(x.shape):
+            xp, xm = x.copy(), x.copy()
+            xp[i] += h
+            xm[i] -= h
+            fdg[i] = (L(*mk(xp)) - L(*mk(xm))) / (2 * h)
+        assert rel_l2(got, fdg) < 1e-8
+    # delta enters only through f + delta: its gradient is df summed over (b, t)
+    assert np.allclose(dd, df.sum(axis=(0, 1)), atol=1e-14)
+
+
+def test_L9_fused_forward_reduces_to_the_recurrence():
+    """Unit-norm q, k (eps = 0) and f = softplus^{-1}(-g e^{-a}) - delta make the
+    stage the identity: the fused forward is then the plain recurrence on g."""
+    rng = np.random.default_rng(7)
+    B, T, H, Dk, Dv = 1, 9, 2, 4, 3
+    q = rng.standard_normal((B, T, H, Dk))
+    k = rng.standard_normal((B, T, H, Dk))
+    q /= np.linalg.norm(q, axis=-1, keepdims=True)
+    k /= np.linalg.norm(k, axis=-1, keepdims=True)
+    g = -rng.uniform(0.01, 1.0, (B, T, H, Dk))
+    a = np.array([0.3, -0.2])
+    delta = rng.standard_normal((H, Dk))
+    sp = -g * np.exp(-a)[:, None]
+    f = np.log(np.expm1(sp)) - delta
+    v = rng.standard_normal((B, T, H, Dv))
+    b = rng.uniform(0, 1, (B, T, H, Dk))
+    w = rng.uniform(0, 1, (B, T, H, Dv))
+    S0 = rng.standard_normal((B, H, Dk, Dv)) * 0.1
+    o1, s1 = gdr2_fused_fwd(q, k, v, f, a, delta, b, w, S0, 0.5, eps=0.0)
+    o2, s2 = gdr2_recurrent_fwd(q, k, v, g, b, w, S0, 0.5)
+    assert rel_l2(o1, o2) < 1e-13 and rel_l2(s1, s2) < 1e-13
+
+
+def _fused_fd_check(d, names):
+    eps = d["eps"]
+    cu = d.get("cu_seqlens")
+    x = {n: np.asarray(d[n], dtype=np.float64) for n in ("q", "k", "v", "f", "a", "delta", "b", "w")}
+    x["S0"] = np.asarray(d["S0"], dtype=np.float64)
+
+    def fwd(q, k, v, f, a, delta, b, w, S0):
+        return gdr2_fused_fwd(q, k, v, f, a, delta, b, w, S0, d["scale"], eps, cu)
+
+    dST = np.asarray(d["dST"], dtype=np.float64)
+    do = np.asarray(d["do"], dtype=np.float64)
+    got = gdr2_fused_bwd(*[x[n] for n in ("q", "k", "v", "f", "a", "delta", "b", "w", "S0")], do, dST,
+                         d["scale"], eps, cu)
+    for n in names:
+        fdg = fd.fd_grad(fwd, x, n, do, dST, h=1e-6)
+        assert rel_l2(got["d" + n], fdg) < 1e-7, n
+
+
+def test_L10_fused_adjoint_finite_differences():
+    d = make_fused(1, 7, 2, 4, 3, seed=11, dtype="fp32", s0_std=0.1, with_dST=True)
+    _fused_fd_check(d, ("q", "k", "f", "a", "delta", "b", "v", "w", "S0"))
+
+
+def test_L11_fused_adjoint_grouped_and_packed():
+    """Grouped value heads (G = 2) and a packed batch: the key-side gradients
+    (normalisation and activation included) by finite differences."""
+    d = make_fused(1, 6, 1, 4, 3, seed=12, dtype="fp32", Hv=2, s0_std=0.1, with_dST=True)
+    _fused_fd_check(d, ("q", "k", "f", "a", "delta", "b"))
+    d = make_fused(0, 0, 2, 4, 3, seed=13, dtype="fp32", lengths=[3, 0, 4], s0_std=0.1, with_dST=True)
+    _fused_fd_check(d, ("q", "k", "f", "a", "delta"))
