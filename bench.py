@@ -301,6 +301,41 @@ def varlen_bench(steps=10, stored=True):
             "ms_per_step": ms, "tokens_per_s": T / (ms * 1e-3), "kernels_avg_us": kern}
 
 
+def grouped_bench(steps=10, stored=True):
+    """Grouped value heads: the headline step's 32768 tokens with H = 8 key heads
+    shared by Hv = 16 value heads (G = 2), d = 128, bf16.  fwd+bwd step time."""
+    import torch
+    import paper_2605_22791_amd as g2
+    from paper_2605_22791_amd.inputs import make_grouped
+    d = make_grouped(8, 4096, 8, 16, 128, 128, seed=41, dtype="bf16", decay_shift=-2.0)
+    tb = lambda x: torch.from_numpy(x).cuda().to(torch.bfloat16).contiguous()
+    q, k, v, b, w, do = (tb(d[n]) for n in ("q", "k", "v", "b", "w", "do"))
+    la = torch.from_numpy(d["log_alpha"]).cuda().contiguous()
+    prob = g2.Gdr2Problem(8, 4096, 8, 128, 128, 64, d["scale"], g2.GDR2_BF16, 16)
+    ws = torch.empty(g2.gdr2_chunk_workspace_bytes(prob, 1), dtype=torch.uint8, device="cuda")
+
+    def step():
+        g2.gdr2_chunk_fwd(q, k, v, la, b, w, None, scale=d["scale"], ws=ws, save=stored)
+        g2.gdr2_chunk_bwd(q, k, v, la, b, w, None, do, None, scale=d["scale"], ws=ws, saved=stored)
+
+    for _ in range(2):
+        step()
+    torch.cuda.synchronize()
+    g2.gdr2_profile_enable(True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    per_kernel = g2.gdr2_profile_collect()
+    g2.gdr2_profile_enable(False)
+    ms = e0.elapsed_time(e1) / steps
+    kern = {n: round(kms / cnt * 1e3, 1) for n, (kms, cnt) in per_kernel.items() if cnt}
+    return {"workload": "grouped value heads B8 T4096 H8 Hv16 d128 bf16", "training_path": "stored" if stored else "recompute",
+            "ms_per_step": ms, "tokens_per_s": 8 * 4096 / (ms * 1e-3), "kernels_avg_us": kern}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -469,6 +504,8 @@ def main():
         out["long_context"] = config3_bench(stored=stored)
         print("[bench] packed variable-length batch", file=sys.stderr, flush=True)
         out["varlen"] = varlen_bench(stored=stored)
+        print("[bench] grouped value heads", file=sys.stderr, flush=True)
+        out["grouped"] = grouped_bench(stored=stored)
     if not args.no_cpu:
         print("[bench] cpu oracle baseline", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(d, args.cpu_heads)

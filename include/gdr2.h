@@ -202,6 +202,63 @@ gdr2_status gdr2_recurrent_varlen(const gdr2_problem* problem, const int32_t* cu
                                   const void* q, const void* k, const void* v, const float* log_alpha,
                                   const void* b, const void* w, float* S, void* o, hipStream_t stream);
 
+/* ---- fused input stage (App. C.1; App. D.1 - D.2) -------------------------
+ * Variants of the calls above that take the layer's raw projections and do
+ * the two steps between them and the recurrence inside the kernels:
+ *   * q and k are L2-normalised per (token, key head) before the update
+ *     (App. D.2), read here as  y = x * (sum_c x_c^2 + eps)^(-1/2)  (the paper
+ *     gives no epsilon; eps = 0 is the plain x / ||x||, which is not finite for
+ *     an all-zero row);
+ *   * the log-decay is formed in fp32 from the decay projection f as
+ *     g = -exp(a_log[h]) * softplus(f + delta[h][c])  (eq. eq_gdn2_decay_param,
+ *     App. C.1): one a_log per key head, broadcast over its Dk channels, and
+ *     one delta per key channel.
+ * The normalised q, k and g never exist in memory.  The backward returns the
+ * gradients of the raw inputs: dq, dk through the normalisation VJP
+ * dx = r (dy - y <y, dy>) (r the inverse norm, y = r x), df = dg * (-exp(a)
+ * sigmoid(f + delta)), da[h] = sum over tokens, value heads of the group and
+ * channels of dg * g, ddelta[h][c] = sum over tokens and group of df.
+ * Everything else (shapes, S0, states, grouped value heads, packed batches with
+ * cu_seqlens and n_seqs > 0, or n_seqs = 0 and cu_seqlens ignored for fixed
+ * length, the stored and recomputing training paths) is as in the plain calls;
+ * q, k and f take the places of q, k and log_alpha with the same shapes
+ * ((B,T,H,Dk); f fp32).  The chunk calls run the bf16 path only (fp32 problems:
+ * GDR2_EUNSUPPORTED); the recurrent call takes both dtypes.  The workspace
+ * (gdr2_fused_workspace_bytes) adds the inverse norms of q and k (saving
+ * forward and backward) and the decay-parameter partials (backward); a saving
+ * forward and the backward that reads it need the same stage. */
+typedef struct gdr2_stage {
+  const float* a_log; /* (H) fp32, device, 4-byte aligned */
+  const float* delta; /* (H, Dk) fp32, device, 16-byte aligned */
+  float eps;          /* finite, >= 0 */
+} gdr2_stage;
+
+/* Workspace bytes of a fused chunk call (n_seqs = 0: fixed length; for_backward
+ * as in gdr2_chunk_workspace_bytes: 1 for a saving forward and the backward). */
+gdr2_status gdr2_fused_workspace_bytes(const gdr2_problem* problem, int32_t n_seqs, int for_backward,
+                                       size_t* bytes);
+
+/* Chunk forward from the raw projections (save as in gdr2_chunk_fwd_varlen). */
+gdr2_status gdr2_fused_fwd(const gdr2_problem* problem, const gdr2_stage* stage, const int32_t* cu_seqlens,
+                           int32_t n_seqs, const void* q, const void* k, const void* v, const float* f,
+                           const void* b, const void* w, const float* S0, void* o, float* S_T, void* ws,
+                           size_t ws_bytes, int save, hipStream_t stream);
+
+/* Chunk backward from the raw projections: dq, dk (B,T,H,Dk) in the dtype,
+ * df (B,T,H,Dk) fp32, da (H) fp32, ddelta (H,Dk) fp32 (16-byte aligned); the
+ * other gradients as in gdr2_chunk_bwd.  All outputs are overwritten. */
+gdr2_status gdr2_fused_bwd(const gdr2_problem* problem, const gdr2_stage* stage, const int32_t* cu_seqlens,
+                           int32_t n_seqs, const void* q, const void* k, const void* v, const float* f,
+                           const void* b, const void* w, const float* S0, const void* dout, const float* dS_T,
+                           void* dq, void* dk, void* dv, float* df, float* da, float* ddelta, void* db, void* dw,
+                           float* dS0, void* ws, size_t ws_bytes, int saved, hipStream_t stream);
+
+/* Recurrent forward (decoding) from the raw projections (App. C.5): as
+ * gdr2_recurrent_step / gdr2_recurrent_varlen; normalisation in fp32. */
+gdr2_status gdr2_fused_recurrent(const gdr2_problem* problem, const gdr2_stage* stage, const int32_t* cu_seqlens,
+                                 int32_t n_seqs, const void* q, const void* k, const void* v, const float* f,
+                                 const void* b, const void* w, float* S, void* o, hipStream_t stream);
+
 /* Static, human-readable name of a status code. */
 const char* gdr2_status_str(gdr2_status status);
 
@@ -217,7 +274,9 @@ typedef enum gdr2_kernel_id {
   GDR2_K_BWD_INTRA = 6,           /* backward: intra-chunk VJP + decay chain (bf16
                                      problems: with the WY VJP, one kernel)      */
   GDR2_K_RECURRENT = 7,           /* recurrent / decode                           */
-  GDR2_NUM_KERNELS = 8
+  GDR2_K_STAGE_BWD = 8,           /* fused stage: normalisation VJP, decay-
+                                     parameter sums                              */
+  GDR2_NUM_KERNELS = 9
 } gdr2_kernel_id;
 
 /* Per-thread kernel timing for benchmarks: while enabled, each kernel launched

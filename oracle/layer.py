@@ -26,7 +26,12 @@ Two steps sit between the projections and the recurrence:
 
 The fused operator is the recurrence of oracle/recurrent.py run on
 (l2norm(q), l2norm(k), v, g, b, w); its backward is that recurrence's adjoint
-followed by the two VJPs above.  Grouped value heads (Sec. 3.5) and packed
+followed by the two VJPs above.  The kernels take q and k in the model dtype
+(App. D.3: only the state and the accumulators are fp32), so for a bf16
+operator the normalised q and k are rounded to bf16 (nearest, ties to even)
+before the recurrence, as the cast between an unfused normalisation and the
+operator would; the rounding passes gradients through unchanged, so the VJP is
+taken at the unrounded y.  Grouped value heads (Sec. 3.5) and packed
 batches (App. C.6) compose the same way: the normalisation and the activation
 act on the key heads, before any repetition over a group.
 """
@@ -37,7 +42,23 @@ from .recurrent import (gdr2_grouped_bwd, gdr2_grouped_fwd, gdr2_packed_bwd, gdr
                         gdr2_recurrent_bwd, gdr2_recurrent_fwd)
 
 __all__ = ["l2norm", "l2norm_vjp", "softplus", "decay_activation", "decay_activation_vjp",
-           "gdr2_fused_fwd", "gdr2_fused_bwd"]
+           "round_bf16", "gdr2_fused_fwd", "gdr2_fused_bwd"]
+
+
+def round_bf16(x):
+    """Nearest bfloat16 value of each element (ties to the even significand),
+    as float64.  A bfloat16 keeps 8 significant bits: with x = m 2^e, m in
+    [1, 2), the spacing is 2^(e - 7); values are rounded on that grid.  Zero,
+    infinities and NaN pass through; values beyond the largest bfloat16 are
+    rounded on the top binade's grid (overflow to infinity is not modelled)."""
+    x = np.asarray(x, dtype=np.float64)
+    out = np.array(x, dtype=np.float64)
+    fin = np.isfinite(x) & (x != 0)
+    e = np.floor(np.log2(np.abs(x[fin])))
+    e = np.maximum(e, -126.0)  # subnormal bfloat16 share the smallest normal spacing
+    step = np.exp2(e - 7.0)
+    out[fin] = np.round(x[fin] / step) * step  # np.round: half to even
+    return out
 
 
 def l2norm(x, eps=1e-6):
@@ -88,14 +109,18 @@ def decay_activation_vjp(f, a, delta, dg):
     return df, da, ddelta
 
 
-def _stage(q, k, f, a, delta, eps):
-    return l2norm(q, eps), l2norm(k, eps), decay_activation(f, a, delta)
+def _stage(q, k, f, a, delta, eps, dtype):
+    qn, kn = l2norm(q, eps), l2norm(k, eps)
+    if dtype == "bf16":
+        qn, kn = round_bf16(qn), round_bf16(kn)
+    return qn, kn, decay_activation(f, a, delta)
 
 
-def gdr2_fused_fwd(q, k, v, f, a, delta, b, w, S0=None, scale=1.0, eps=1e-6, cu_seqlens=None):
+def gdr2_fused_fwd(q, k, v, f, a, delta, b, w, S0=None, scale=1.0, eps=1e-6, cu_seqlens=None, dtype="fp64"):
     """Forward from the raw projections: (o, S_T).  q, k, f, b on H key heads;
-    v, w on Hv = G H value heads; cu_seqlens (packed batch, B = 1) or None."""
-    qn, kn, g = _stage(q, k, f, a, delta, eps)
+    v, w on Hv = G H value heads; cu_seqlens (packed batch, B = 1) or None;
+    dtype: the operator's q / k dtype ("bf16" rounds the normalised q, k)."""
+    qn, kn, g = _stage(q, k, f, a, delta, eps, dtype)
     G = np.shape(v)[2] // np.shape(q)[2]
     if cu_seqlens is not None:
         if G > 1:
@@ -106,10 +131,11 @@ def gdr2_fused_fwd(q, k, v, f, a, delta, b, w, S0=None, scale=1.0, eps=1e-6, cu_
     return gdr2_recurrent_fwd(qn, kn, v, g, b, w, S0, scale)
 
 
-def gdr2_fused_bwd(q, k, v, f, a, delta, b, w, S0, do, dS_T=None, scale=1.0, eps=1e-6, cu_seqlens=None):
+def gdr2_fused_bwd(q, k, v, f, a, delta, b, w, S0, do, dS_T=None, scale=1.0, eps=1e-6, cu_seqlens=None,
+                   dtype="fp64"):
     """Adjoint of gdr2_fused_fwd: dict dq, dk (raw q, k), df, da, ddelta, db,
     dv, dw, dS0."""
-    qn, kn, g = _stage(q, k, f, a, delta, eps)
+    qn, kn, g = _stage(q, k, f, a, delta, eps, dtype)
     H, Hv = np.shape(q)[2], np.shape(v)[2]
     G = Hv // H
     if cu_seqlens is not None:

@@ -19,7 +19,8 @@ __all__ = [
     "gdr2_chunk_bwd_saved", "gdr2_varlen_workspace_bytes", "gdr2_chunk_fwd_varlen", "gdr2_chunk_bwd_varlen",
     "gdr2_recurrent_varlen",
     "gdr2_recurrent_step", "gdr2_status_str", "CHUNK", "KERNEL_NAMES",
-    "gdr2_profile_enable", "gdr2_profile_collect",
+    "gdr2_profile_enable", "gdr2_profile_collect", "Gdr2Stage", "gdr2_fused_workspace_bytes",
+    "gdr2_fused_fwd", "gdr2_fused_bwd", "gdr2_fused_recurrent",
 ]
 
 GDR2_OK, GDR2_EINVAL, GDR2_EUNSUPPORTED, GDR2_EWORKSPACE, GDR2_EHIP = 0, 1, 2, 3, 4
@@ -27,7 +28,7 @@ GDR2_BF16, GDR2_FP32 = 0, 1
 CHUNK = 64
 # kernel ids of the measurement support (gdr2_kernel_id in include/gdr2.h)
 KERNEL_NAMES = ["fwd_intra", "fwd_state", "bwd_recompute_intra", "bwd_recompute_state",
-                "bwd_state", "bwd_wy", "bwd_intra", "recurrent"]
+                "bwd_state", "bwd_wy", "bwd_intra", "recurrent", "stage_bwd"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 
@@ -40,6 +41,10 @@ class Gdr2Problem(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int32), ("T", ctypes.c_int32), ("H", ctypes.c_int32),
                 ("Dk", ctypes.c_int32), ("Dv", ctypes.c_int32), ("chunk", ctypes.c_int32),
                 ("scale", ctypes.c_float), ("dtype", ctypes.c_int32), ("Hv", ctypes.c_int32)]
+
+
+class Gdr2Stage(ctypes.Structure):
+    _fields_ = [("a_log", ctypes.c_void_p), ("delta", ctypes.c_void_p), ("eps", ctypes.c_float)]
 
 
 class Gdr2Error(RuntimeError):
@@ -83,6 +88,15 @@ def lib():
         L.gdr2_chunk_bwd_varlen.restype = ctypes.c_int
         L.gdr2_recurrent_varlen.argtypes = [P, vp, i32] + [vp] * 8 + [vp]
         L.gdr2_recurrent_varlen.restype = ctypes.c_int
+        S = ctypes.POINTER(Gdr2Stage)
+        L.gdr2_fused_workspace_bytes.restype = ctypes.c_int
+        L.gdr2_fused_workspace_bytes.argtypes = [P, i32, ctypes.c_int, ctypes.POINTER(ctypes.c_size_t)]
+        L.gdr2_fused_fwd.restype = ctypes.c_int
+        L.gdr2_fused_fwd.argtypes = [P, S, vp, i32] + [vp] * 10 + [ctypes.c_size_t, ctypes.c_int, vp]
+        L.gdr2_fused_bwd.restype = ctypes.c_int
+        L.gdr2_fused_bwd.argtypes = [P, S, vp, i32] + [vp] * 19 + [ctypes.c_size_t, ctypes.c_int, vp]
+        L.gdr2_fused_recurrent.restype = ctypes.c_int
+        L.gdr2_fused_recurrent.argtypes = [P, S, vp, i32] + [vp] * 8 + [vp]
         L.gdr2_profile_enable.argtypes = [ctypes.c_int]
         L.gdr2_profile_enable.restype = ctypes.c_int
         L.gdr2_profile_collect.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_longlong),
@@ -350,3 +364,102 @@ def gdr2_profile_collect():
     cnt = (ctypes.c_longlong * n)()
     _check(lib().gdr2_profile_collect(ms, cnt, n), "gdr2_profile_collect")
     return {KERNEL_NAMES[i]: (ms[i], cnt[i]) for i in range(n)}
+
+
+# --------------------------------------------------------------------------- fused input stage
+def _stage(a_log, delta, H, Dk, eps):
+    torch = _torch()
+    _require("a_log", a_log, (H,), torch.float32)
+    _require("delta", delta, (H, Dk), torch.float32)
+    return Gdr2Stage(a_log.data_ptr(), delta.data_ptr(), float(eps))
+
+
+def gdr2_fused_workspace_bytes(problem, n_seqs, for_backward):
+    """Bytes of workspace of a fused chunk call (n_seqs = 0: fixed length)."""
+    n = ctypes.c_size_t(0)
+    _check(lib().gdr2_fused_workspace_bytes(ctypes.byref(problem), int(n_seqs), int(for_backward),
+                                            ctypes.byref(n)), "gdr2_fused_workspace_bytes")
+    return n.value
+
+
+def _fused_shapes(q, k, v, f, b, w, cu_seqlens):
+    B, T, H, Dk, Dv = _validate(q, k, v, f, b, w)
+    N = _cu(cu_seqlens, T) if cu_seqlens is not None else 0
+    return B, T, H, Dk, Dv, N
+
+
+def gdr2_fused_fwd(q, k, v, f, a_log, delta, b, w, S0=None, *, cu_seqlens=None, scale=None, eps=1e-6, o=None,
+                   S_T=None, want_state=True, ws=None, save=False):
+    """Forward from the raw projections: q, k (not normalised), f the decay
+    projection (fp32, (B, T, H, Dk)), a_log (H,), delta (H, Dk).  Returns (o, S_T)."""
+    torch = _torch()
+    B, T, Hv, Dk, Dv, N = _fused_shapes(q, k, v, f, b, w, cu_seqlens)
+    NS = N if N > 0 else B
+    stg = _stage(a_log, delta, q.shape[2], Dk, eps)
+    _require("S0", S0, (NS, Hv, Dk, Dv), torch.float32)
+    prob = _problem(q, v, scale)
+    if o is None:
+        o = torch.empty((B, T, Hv, Dv), dtype=q.dtype, device=q.device)
+    _require("o", o, (B, T, Hv, Dv), q.dtype)
+    if S_T is None and want_state:
+        S_T = torch.empty((NS, Hv, Dk, Dv), dtype=torch.float32, device=q.device)
+    _require("S_T", S_T, (NS, Hv, Dk, Dv), torch.float32)
+    if ws is None:
+        if save:
+            raise ValueError("save=True needs the workspace that the backward will read")
+        ws = torch.empty(gdr2_fused_workspace_bytes(prob, N, 0), dtype=torch.uint8, device=q.device)
+    st = lib().gdr2_fused_fwd(ctypes.byref(prob), ctypes.byref(stg), _ptr(cu_seqlens), N, _ptr(q), _ptr(k),
+                              _ptr(v), _ptr(f), _ptr(b), _ptr(w), _ptr(S0), _ptr(o), _ptr(S_T), _ptr(ws),
+                              ws.numel(), 1 if save else 0, _stream())
+    _check(st, "gdr2_fused_fwd")
+    return o, S_T
+
+
+def gdr2_fused_bwd(q, k, v, f, a_log, delta, b, w, S0, dout, dS_T=None, *, cu_seqlens=None, scale=None,
+                   eps=1e-6, grads=None, want_dS0=True, ws=None, saved=False):
+    """Backward from the raw projections; returns dict dq, dk (raw q, k), dv,
+    df, da, ddelta, db, dw, dS0."""
+    torch = _torch()
+    B, T, Hv, Dk, Dv, N = _fused_shapes(q, k, v, f, b, w, cu_seqlens)
+    NS = N if N > 0 else B
+    H = q.shape[2]
+    stg = _stage(a_log, delta, H, Dk, eps)
+    _require("S0", S0, (NS, Hv, Dk, Dv), torch.float32)
+    _require("dout", dout, (B, T, Hv, Dv), q.dtype)
+    _require("dS_T", dS_T, (NS, Hv, Dk, Dv), torch.float32)
+    prob = _problem(q, v, scale)
+    g = dict(grads or {})
+    for n, like in (("dq", q), ("dk", k), ("dv", v), ("df", f), ("db", b), ("dw", w), ("da", a_log),
+                    ("ddelta", delta)):
+        g.setdefault(n, torch.empty_like(like))
+    if want_dS0:
+        g.setdefault("dS0", torch.empty((NS, Hv, Dk, Dv), dtype=torch.float32, device=q.device))
+    else:
+        g.setdefault("dS0", None)
+    if ws is None:
+        if saved:
+            raise ValueError("saved=True needs the workspace of the saving forward")
+        ws = torch.empty(gdr2_fused_workspace_bytes(prob, N, 1), dtype=torch.uint8, device=q.device)
+    st = lib().gdr2_fused_bwd(ctypes.byref(prob), ctypes.byref(stg), _ptr(cu_seqlens), N, _ptr(q), _ptr(k),
+                              _ptr(v), _ptr(f), _ptr(b), _ptr(w), _ptr(S0), _ptr(dout), _ptr(dS_T), _ptr(g["dq"]),
+                              _ptr(g["dk"]), _ptr(g["dv"]), _ptr(g["df"]), _ptr(g["da"]), _ptr(g["ddelta"]),
+                              _ptr(g["db"]), _ptr(g["dw"]), _ptr(g["dS0"]), _ptr(ws), ws.numel(),
+                              1 if saved else 0, _stream())
+    _check(st, "gdr2_fused_bwd")
+    return g
+
+
+def gdr2_fused_recurrent(q, k, v, f, a_log, delta, b, w, S, *, cu_seqlens=None, scale=None, eps=1e-6, o=None):
+    """Token-by-token forward from the raw projections; S updated in place.  Returns o."""
+    torch = _torch()
+    B, T, Hv, Dk, Dv, N = _fused_shapes(q, k, v, f, b, w, cu_seqlens)
+    NS = N if N > 0 else B
+    stg = _stage(a_log, delta, q.shape[2], Dk, eps)
+    _require("S", S, (NS, Hv, Dk, Dv), torch.float32)
+    prob = _problem(q, v, scale)
+    if o is None:
+        o = torch.empty((B, T, Hv, Dv), dtype=q.dtype, device=q.device)
+    st = lib().gdr2_fused_recurrent(ctypes.byref(prob), ctypes.byref(stg), _ptr(cu_seqlens), N, _ptr(q), _ptr(k),
+                                    _ptr(v), _ptr(f), _ptr(b), _ptr(w), _ptr(S), _ptr(o), _stream())
+    _check(st, "gdr2_fused_recurrent")
+    return o

@@ -71,8 +71,12 @@ struct Layout {
   int nseg, seg_len;
   size_t vcoff, vct0, vclen, vsord;      // chunk table and scan order of a packed call (int32)
   size_t pQ, pK, pB, pG;                 // grouped value heads: fp32 key-side gradient partials
+  size_t RQ, RK;                         // fused stage: inverse norms of q, k rows (rows, Hk)
+  size_t PD, PA, PT;                     // fused backward: decay-parameter partials, range sums
   size_t total;
 };
+
+constexpr int kParamSplits = 64;  // slot ranges of the first decay-parameter reduction pass
 
 // Sequence-parallel scans (bf16 path).  The state scans run one workgroup per
 // (sequence, 64-wide value slice); when there are too few of those to occupy
@@ -100,8 +104,9 @@ void scan_segments(const gdr2_problem* p, int& nseg, int& seg_len) {
   nseg = (NT + seg_len - 1) / seg_len;
 }
 
-// p: the value view (value_view); G > 1 adds the backward's group partials.
-Layout layout(const gdr2_problem* p, bool bwd, int nseq = 0, int G = 1) {
+// p: the value view (value_view); G > 1 adds the backward's group partials;
+// fused adds the fused stage's regions (bwd: saving forward and backward).
+Layout layout(const gdr2_problem* p, bool bwd, int nseq = 0, int G = 1, bool fused = false) {
   const size_t NC = nseq > 0 ? (size_t)p->H * varlen_slots(p, nseq) : (size_t)p->B * p->H * chunks_per_seq(p);
   const size_t Dk = p->Dk, Dv = p->Dv;
   Layout L{};
@@ -160,12 +165,25 @@ Layout layout(const gdr2_problem* p, bool bwd, int nseq = 0, int G = 1) {
   } else {
     scan_segments(p, L.nseg, L.seg_len);
   }
-  if (bwd && G > 1) {
+  if (bwd && (G > 1 || fused)) {
+    // fp32 key-side gradients on the value-head axis: dq, dk for grouped heads
+    // and for the fused stage (its VJP rounds once), db, dg for grouped heads
     const size_t n = (size_t)p->B * p->T * p->H * Dk;
     L.pQ = take(n);
     L.pK = take(n);
-    L.pB = take(n);
-    L.pG = take(n);
+    if (G > 1) {
+      L.pB = take(n);
+      L.pG = take(n);
+    }
+  }
+  if (fused && bwd) {
+    const size_t rows = (size_t)p->B * p->T, Hk = (size_t)(p->H / G);
+    const size_t nslots = nseq > 0 ? (size_t)varlen_slots(p, nseq) : (size_t)p->B * chunks_per_seq(p);
+    L.RQ = take(rows * Hk);
+    L.RK = take(rows * Hk);
+    L.PD = take(nslots * p->H * 4 * Dk);
+    L.PA = take(nslots * p->H * 4);
+    L.PT = take((size_t)kParamSplits * Hk * (Dk + 1));
   }
   if (L.nseg > 1) {
     const size_t nvs = (size_t)p->B * p->H * L.nseg;
@@ -191,13 +209,24 @@ struct Geo {
   int nscan;
   Varlen vl;
   int G;  // value heads per key head
+  Stage st;  // fused input stage (st.a_log null: off); RQ / RK set when the layout has them
 };
 
-// p: the value view; G: value heads per key head
-Geo make_geo(const gdr2_problem* p, bool bwd, int nseq, const int* cu, void* ws, int grp = 1) {
+// p: the value view; G: value heads per key head; stage: the fused stage or null
+Geo make_geo(const gdr2_problem* p, bool bwd, int nseq, const int* cu, void* ws, int grp = 1,
+             const gdr2_stage* stage = nullptr) {
   Geo G{};
   G.G = grp;
-  G.L = layout(p, bwd, nseq, grp);
+  G.L = layout(p, bwd, nseq, grp, stage != nullptr);
+  if (stage != nullptr) {
+    G.st.a_log = stage->a_log;
+    G.st.delta = stage->delta;
+    G.st.eps = stage->eps;
+    if (bwd) {
+      G.st.RQ = at<float>(ws, G.L.RQ);
+      G.st.RK = at<float>(ws, G.L.RK);
+    }
+  }
   if (nseq > 0) {
     G.NT = varlen_slots(p, nseq);
     G.nscan = nseq;
@@ -285,16 +314,55 @@ hipError_t timed(int id, hipStream_t st, F&& launch) {
 }
 
 // ---- grouped value heads: sum each key head's G partials into dq, dk, db, dlog_alpha
-// (p: the value view, so the key heads are p->H / G)
+// (p: the value view, so the key heads are p->H / G); dq, dk null: left to the
+// fused stage's normalisation VJP, which sums their partials itself
 template <typename TIn>
 hipError_t group_reduce(const gdr2_problem* p, const Geo& G, const Layout& L, void* ws, void* dq, void* dk,
                         void* db, float* dg, hipStream_t st) {
   const size_t rows = (size_t)p->B * p->T;
   const int Hk = p->H / G.G;
-  hipError_t e = launch_group_reduce<TIn>(at<float>(ws, L.pQ), static_cast<TIn*>(dq), rows, Hk, G.G, p->Dk, st);
-  if (e == hipSuccess) e = launch_group_reduce<TIn>(at<float>(ws, L.pK), static_cast<TIn*>(dk), rows, Hk, G.G, p->Dk, st);
+  hipError_t e = hipSuccess;
+  if (dq != nullptr)
+    e = launch_group_reduce<TIn>(at<float>(ws, L.pQ), static_cast<TIn*>(dq), rows, Hk, G.G, p->Dk, st);
+  if (e == hipSuccess && dk != nullptr)
+    e = launch_group_reduce<TIn>(at<float>(ws, L.pK), static_cast<TIn*>(dk), rows, Hk, G.G, p->Dk, st);
   if (e == hipSuccess) e = launch_group_reduce<TIn>(at<float>(ws, L.pB), static_cast<TIn*>(db), rows, Hk, G.G, p->Dk, st);
   if (e == hipSuccess) e = launch_group_reduce<float>(at<float>(ws, L.pG), dg, rows, Hk, G.G, p->Dk, st);
+  return e;
+}
+
+// ---- fused stage, backward tail: the normalisation VJP of q and k (from the
+// gradients of the normalised tensors in dq, dk, or in the group partials) and
+// the two-pass sums of the decay-parameter partials into ddelta and da
+template <int DK>
+hipError_t stage_bwd(const gdr2_problem* p, const Geo& G, void* ws, const void* q, const void* k, void* dq,
+                     void* dk, float* da, float* ddelta, hipStream_t st) {
+  const Layout& L = G.L;
+  const int Hk = p->H / G.G;
+  NormVjpArgs na{};
+  na.x[0] = static_cast<const bf16_t*>(q);
+  na.x[1] = static_cast<const bf16_t*>(k);
+  na.rinv[0] = G.st.RQ;
+  na.rinv[1] = G.st.RK;
+  na.DY[0] = static_cast<const bf16_t*>(dq);
+  na.DY[1] = static_cast<const bf16_t*>(dk);
+  na.P[0] = at<float>(ws, L.pQ);
+  na.P[1] = at<float>(ws, L.pK);
+  na.dx[0] = static_cast<bf16_t*>(dq);
+  na.dx[1] = static_cast<bf16_t*>(dk);
+  na.rows = (size_t)p->B * p->T;
+  na.Hk = Hk;
+  na.G = G.G;
+  hipError_t e = launch_norm_vjp<DK>(na, st);
+  if (e != hipSuccess) return e;
+  const int nslots = G.vl.ct0 != nullptr ? G.vl.ncmax : p->B * G.NT;
+  const int splits = nslots < kParamSplits ? nslots : kParamSplits;
+  float* PT = at<float>(ws, L.PT);
+  float* PT1 = PT + (size_t)kParamSplits * Hk * DK;
+  e = launch_param_reduce_pass(at<float>(ws, L.PD), PT, nslots, Hk, 4 * G.G, DK, splits, st);
+  if (e == hipSuccess) e = launch_param_reduce_pass(PT, ddelta, splits, Hk, 1, DK, 1, st);
+  if (e == hipSuccess) e = launch_param_reduce_pass(at<float>(ws, L.PA), PT1, nslots, Hk, 4 * G.G, 1, splits, st);
+  if (e == hipSuccess) e = launch_param_reduce_pass(PT1, da, splits, Hk, 1, 1, 1, st);
   return e;
 }
 
@@ -391,6 +459,7 @@ struct FwdRun {
                        save ? at<unsigned char>(ws, L.bAm) : nullptr, p->B, p->T, p->H, NT};
       ia.vl = G.vl;
       ia.G = G.G;
+      ia.st = G.st;
       hipError_t e = timed(GDR2_K_FWD_INTRA, st, [&] { return launch_intra_bf16<DK, DV>(ia, st); });
       if (e != hipSuccess) return e;
       ScanArgs sa{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.U, ia.GC, S0, ST, static_cast<bf16_t*>(o),
@@ -430,9 +499,10 @@ struct BwdRun {
                         const float* g, const void* b, const void* w, const float* S0,
                         const void* dout, const float* dST, void* dq, void* dk, void* dv,
                         float* dg, void* db, void* dw, float* dS0, void* ws, bool saved, const Geo& G,
-                        hipStream_t st) {
+                        float* da, float* ddelta, hipStream_t st) {
     const Layout& L = G.L;
     const int NT = G.NT;
+    const bool fused = G.st.a_log != nullptr;
     hipError_t e = hipSuccess;
     if (std::is_same<TIn, bf16_t>::value) {
       IntraBf16Args ia{static_cast<const bf16_t*>(q), static_cast<const bf16_t*>(k),
@@ -443,6 +513,7 @@ struct BwdRun {
                        at<unsigned char>(ws, L.bAm), p->B, p->T, p->H, NT};
       ia.vl = G.vl;
       ia.G = G.G;
+      ia.st = G.st;
       if (!saved) {
         // recompute: intra-chunk tiles (with A), then the forward scan storing the chunk states and R
         e = timed(GDR2_K_BWD_RECOMPUTE_INTRA, st, [&] { return launch_intra_bf16<DK, DV>(ia, st); });
@@ -478,11 +549,21 @@ struct BwdRun {
         ca.Pb = at<float>(ws, L.pB);
         ca.dg = at<float>(ws, L.pG);
       }
-      return timed(GDR2_K_BWD_INTRA, st, [&] {
+      if (fused) {
+        ca.st = G.st;
+        ca.PD = at<float>(ws, L.PD);
+        ca.PA = at<float>(ws, L.PA);
+        ca.Pq = at<float>(ws, L.pQ);
+        ca.Pk = at<float>(ws, L.pK);
+      }
+      e = timed(GDR2_K_BWD_INTRA, st, [&] {
         hipError_t r = launch_bchunk_bf16<DK, DV>(ca, st);
-        if (r == hipSuccess && G.G > 1) r = group_reduce<bf16_t>(p, G, L, ws, dq, dk, db, dg, st);
+        if (r == hipSuccess && G.G > 1)
+          r = group_reduce<bf16_t>(p, G, L, ws, fused ? nullptr : dq, fused ? nullptr : dk, db, dg, st);
         return r;
       });
+      if (e != hipSuccess || !fused) return e;
+      return timed(GDR2_K_STAGE_BWD, st, [&] { return stage_bwd<DK>(p, G, ws, q, k, dq, dk, da, ddelta, st); });
     }
     IntraArgs<TIn> ia{static_cast<const TIn*>(q), static_cast<const TIn*>(k),
                       static_cast<const TIn*>(v), g, static_cast<const TIn*>(b),
@@ -535,12 +616,17 @@ template <int DK, int DV, typename TIn>
 struct RecRun {
   static hipError_t run(const gdr2_problem* p, const void* q, const void* k, const void* v,
                         const float* g, const void* b, const void* w, float* S, void* o, const int* cu,
-                        int nseq, int grp, hipStream_t st) {
+                        int nseq, int grp, const gdr2_stage* stage, hipStream_t st) {
     RecurArgs<TIn> ra{static_cast<const TIn*>(q), static_cast<const TIn*>(k),
                       static_cast<const TIn*>(v), g, static_cast<const TIn*>(b),
                       static_cast<const TIn*>(w), S, static_cast<TIn*>(o), p->T, p->H, p->scale};
     ra.cu = cu;
     ra.G = grp;
+    if (stage != nullptr) {
+      ra.st.a_log = stage->a_log;
+      ra.st.delta = stage->delta;
+      ra.st.eps = stage->eps;
+    }
     const int nb = cu != nullptr ? nseq : p->B;
     return timed(GDR2_K_RECURRENT, st, [&] { return launch_recurrent<DK, DV, TIn>(ra, nb, st); });
   }
@@ -560,6 +646,13 @@ bool opt_ok(std::initializer_list<const void*> opt) {
 
 bool cu_ok(const int32_t* cu) { return cu != nullptr && (reinterpret_cast<uintptr_t>(cu) & 3u) == 0; }
 
+// The fused stage's parameters: a_log 4-byte aligned, delta 16-byte aligned, eps finite and >= 0.
+bool stage_ok(const gdr2_stage* s) {
+  if (s == nullptr || s->a_log == nullptr || s->delta == nullptr) return false;
+  if ((reinterpret_cast<uintptr_t>(s->a_log) & 3u) != 0 || !aligned16(s->delta)) return false;
+  return std::isfinite(s->eps) && s->eps >= 0.f;
+}
+
 }  // namespace
 
 extern "C" {
@@ -575,16 +668,28 @@ gdr2_status gdr2_chunk_workspace_bytes(const gdr2_problem* p, int for_backward, 
 
 namespace {
 
+// A call with the fused stage checks it and runs on the bf16 path only.
+gdr2_status check_stage(const gdr2_problem* p, const gdr2_stage* stage, bool chunked) {
+  if (stage == nullptr) return GDR2_OK;
+  if (!stage_ok(stage)) return GDR2_EINVAL;
+  if (chunked && p->dtype != GDR2_BF16) return GDR2_EUNSUPPORTED;
+  return GDR2_OK;
+}
+
 // nseq > 0 (with cu): packed variable-length call
+// stage: the fused input stage (log_alpha then holds the decay projection f) or null
 gdr2_status chunk_fwd(const gdr2_problem* p, const int32_t* cu, int nseq, const void* q, const void* k,
                       const void* v, const float* log_alpha, const void* b, const void* w, const float* S0,
-                      void* o, float* S_T, void* ws, size_t ws_bytes, bool save, hipStream_t stream) {
+                      void* o, float* S_T, void* ws, size_t ws_bytes, bool save, hipStream_t stream,
+                      const gdr2_stage* stage = nullptr) {
   gdr2_status s = check_problem(p, true, nseq);
+  if (s != GDR2_OK) return s;
+  s = check_stage(p, stage, true);
   if (s != GDR2_OK) return s;
   if (!all_ok({q, k, v, log_alpha, b, w, o, ws}) || !opt_ok({S0, S_T})) return GDR2_EINVAL;
   if (nseq > 0 && !cu_ok(cu)) return GDR2_EINVAL;
   const gdr2_problem pv = value_view(p);
-  const Geo G = make_geo(&pv, save, nseq, cu, ws, group_of(p));
+  const Geo G = make_geo(&pv, save, nseq, cu, ws, group_of(p), stage);
   if (ws_bytes < G.L.total) return GDR2_EWORKSPACE;
   hipError_t e = build_table(&pv, G, stream);
   if (e != hipSuccess) return GDR2_EHIP;
@@ -595,44 +700,55 @@ gdr2_status chunk_fwd(const gdr2_problem* p, const int32_t* cu, int nseq, const 
   return hip_status(e, stream);
 }
 
+// stage: the fused input stage (log_alpha holds f, dlog_alpha receives df; da
+// and ddelta receive the parameter gradients) or null
 gdr2_status chunk_bwd(const gdr2_problem* p, const int32_t* cu, int nseq, const void* q, const void* k,
                       const void* v, const float* log_alpha, const void* b, const void* w, const float* S0,
                       const void* dout, const float* dS_T, void* dq, void* dk, void* dv,
                       float* dlog_alpha, void* db, void* dw, float* dS0, void* ws, size_t ws_bytes,
-                      bool saved, hipStream_t stream) {
+                      bool saved, hipStream_t stream, const gdr2_stage* stage = nullptr, float* da = nullptr,
+                      float* ddelta = nullptr) {
   gdr2_status s = check_problem(p, true, nseq);
+  if (s != GDR2_OK) return s;
+  s = check_stage(p, stage, true);
   if (s != GDR2_OK) return s;
   if (!all_ok({q, k, v, log_alpha, b, w, dout, dq, dk, dv, dlog_alpha, db, dw, ws}) ||
       !opt_ok({S0, dS_T, dS0}))
     return GDR2_EINVAL;
+  if (stage != nullptr && (da == nullptr || (reinterpret_cast<uintptr_t>(da) & 3u) != 0 || !all_ok({ddelta})))
+    return GDR2_EINVAL;
   if (nseq > 0 && !cu_ok(cu)) return GDR2_EINVAL;
   const gdr2_problem pv = value_view(p);
-  const Geo G = make_geo(&pv, true, nseq, cu, ws, group_of(p));
+  const Geo G = make_geo(&pv, true, nseq, cu, ws, group_of(p), stage);
   if (ws_bytes < G.L.total) return GDR2_EWORKSPACE;
   hipError_t e = build_table(&pv, G, stream);
   if (e != hipSuccess) return GDR2_EHIP;
   if (p->dtype == GDR2_BF16)
     e = dispatch<BwdRun, bf16_t>(p->Dk, p->Dv, &pv, q, k, v, log_alpha, b, w, S0, dout, dS_T, dq,
-                                 dk, dv, dlog_alpha, db, dw, dS0, ws, saved, G, stream);
+                                 dk, dv, dlog_alpha, db, dw, dS0, ws, saved, G, da, ddelta, stream);
   else
     e = dispatch<BwdRun, float>(p->Dk, p->Dv, &pv, q, k, v, log_alpha, b, w, S0, dout, dS_T, dq,
-                                dk, dv, dlog_alpha, db, dw, dS0, ws, saved, G, stream);
+                                dk, dv, dlog_alpha, db, dw, dS0, ws, saved, G, da, ddelta, stream);
   return hip_status(e, stream);
 }
 
 gdr2_status recurrent(const gdr2_problem* p, const int32_t* cu, int nseq, const void* q, const void* k,
                       const void* v, const float* log_alpha, const void* b, const void* w, float* S, void* o,
-                      hipStream_t stream) {
+                      hipStream_t stream, const gdr2_stage* stage = nullptr) {
   gdr2_status s = check_problem(p, false, nseq);
+  if (s != GDR2_OK) return s;
+  s = check_stage(p, stage, false);
   if (s != GDR2_OK) return s;
   if (!all_ok({q, k, v, log_alpha, b, w, S, o})) return GDR2_EINVAL;
   if (nseq > 0 && !cu_ok(cu)) return GDR2_EINVAL;
   hipError_t e;
   const gdr2_problem pv = value_view(p);
   if (p->dtype == GDR2_BF16)
-    e = dispatch<RecRun, bf16_t>(p->Dk, p->Dv, &pv, q, k, v, log_alpha, b, w, S, o, cu, nseq, group_of(p), stream);
+    e = dispatch<RecRun, bf16_t>(p->Dk, p->Dv, &pv, q, k, v, log_alpha, b, w, S, o, cu, nseq, group_of(p), stage,
+                                 stream);
   else
-    e = dispatch<RecRun, float>(p->Dk, p->Dv, &pv, q, k, v, log_alpha, b, w, S, o, cu, nseq, group_of(p), stream);
+    e = dispatch<RecRun, float>(p->Dk, p->Dv, &pv, q, k, v, log_alpha, b, w, S, o, cu, nseq, group_of(p), stage,
+                                stream);
   return hip_status(e, stream);
 }
 
@@ -709,6 +825,42 @@ gdr2_status gdr2_recurrent_varlen(const gdr2_problem* p, const int32_t* cu_seqle
                                   const void* b, const void* w, float* S, void* o, hipStream_t stream) {
   if (n_seqs <= 0) return GDR2_EINVAL;
   return recurrent(p, cu_seqlens, n_seqs, q, k, v, log_alpha, b, w, S, o, stream);
+}
+
+gdr2_status gdr2_fused_workspace_bytes(const gdr2_problem* p, int32_t n_seqs, int for_backward, size_t* bytes) {
+  if (bytes == nullptr || n_seqs < 0) return GDR2_EINVAL;
+  const gdr2_status s = check_problem(p, true, n_seqs);
+  if (s != GDR2_OK) return s;
+  if (p->dtype != GDR2_BF16) return GDR2_EUNSUPPORTED;
+  const gdr2_problem pv = value_view(p);
+  *bytes = layout(&pv, for_backward != 0, n_seqs, group_of(p), true).total;
+  return GDR2_OK;
+}
+
+gdr2_status gdr2_fused_fwd(const gdr2_problem* p, const gdr2_stage* stage, const int32_t* cu_seqlens,
+                           int32_t n_seqs, const void* q, const void* k, const void* v, const float* f,
+                           const void* b, const void* w, const float* S0, void* o, float* S_T, void* ws,
+                           size_t ws_bytes, int save, hipStream_t stream) {
+  if (stage == nullptr || n_seqs < 0) return GDR2_EINVAL;
+  return chunk_fwd(p, n_seqs > 0 ? cu_seqlens : nullptr, n_seqs, q, k, v, f, b, w, S0, o, S_T, ws, ws_bytes,
+                   save != 0, stream, stage);
+}
+
+gdr2_status gdr2_fused_bwd(const gdr2_problem* p, const gdr2_stage* stage, const int32_t* cu_seqlens,
+                           int32_t n_seqs, const void* q, const void* k, const void* v, const float* f,
+                           const void* b, const void* w, const float* S0, const void* dout, const float* dS_T,
+                           void* dq, void* dk, void* dv, float* df, float* da, float* ddelta, void* db, void* dw,
+                           float* dS0, void* ws, size_t ws_bytes, int saved, hipStream_t stream) {
+  if (stage == nullptr || n_seqs < 0) return GDR2_EINVAL;
+  return chunk_bwd(p, n_seqs > 0 ? cu_seqlens : nullptr, n_seqs, q, k, v, f, b, w, S0, dout, dS_T, dq, dk, dv, df,
+                   db, dw, dS0, ws, ws_bytes, saved != 0, stream, stage, da, ddelta);
+}
+
+gdr2_status gdr2_fused_recurrent(const gdr2_problem* p, const gdr2_stage* stage, const int32_t* cu_seqlens,
+                                 int32_t n_seqs, const void* q, const void* k, const void* v, const float* f,
+                                 const void* b, const void* w, float* S, void* o, hipStream_t stream) {
+  if (stage == nullptr || n_seqs < 0) return GDR2_EINVAL;
+  return recurrent(p, n_seqs > 0 ? cu_seqlens : nullptr, n_seqs, q, k, v, f, b, w, S, o, stream, stage);
 }
 
 gdr2_status gdr2_profile_enable(int on) {

@@ -38,6 +38,14 @@
 // diagonal block whose decay exceeds e^60 is formed element by element.
 //
 // Precision: every product is fp32-accurate (split hi/lo; dO is exact bf16).
+//
+// Fused input stage (FUSED; App. C.1, App. D.2): q and k arrive raw and are
+// normalised as they are staged, with the inverse norms the forward kept; the
+// log-decay is formed from the decay projection f on staging, and the stored
+// gradient is df = dg * (-exp(a) sigmoid(f + delta)) instead of dg, with the
+// per-workgroup sums that give ddelta and da.  dq and dk remain the gradients
+// of the normalised q, k: the normalisation VJP needs whole rows and follows in
+// its own kernel.
 
 #include "gdr2_kernels.hpp"
 #include "gdr2_bf16.hpp"
@@ -70,10 +78,16 @@ struct BChunkCfg {
   static constexpr int OFF_BT = OFF_HH + 2 * 16 * 4;      // dG block totals     [2][4][16]
   static constexpr int OFF_TL = OFF_BT + 2 * 4 * 16 * 4;  // tail-key sums       [2][4][16]
   static constexpr int LDS = OFF_TL + 2 * 4 * 16 * 4;
+  // fused stage: f + delta of the staged key block [16][LGT], the decay bias of
+  // the key head [DK], the inverse norms of the chunk's q and k rows [2][64]
+  static constexpr int OFF_XS = LDS;
+  static constexpr int OFF_DL = OFF_XS + 16 * LGT * 4;
+  static constexpr int OFF_RN = OFF_DL + DK * 4;
+  static constexpr int LDS_FUSED = OFF_RN + 2 * 64 * 4;
   static constexpr int NLD = (SZ_DR + SZ_AM) / (16 * NTHR);  // 16-byte prologue loads per thread
   static_assert(SZ_DR <= SZ_T && SZ_AM <= OFF_END_S - OFF_S, "prologue operands fit their regions");
   static_assert((SZ_DR + SZ_AM) % (16 * NTHR) == 0 && SZ_DR % (16 * NTHR) == 0, "whole prologue slices");
-  static_assert(LDS <= 80 * 1024, "two workgroups per CU");
+  static_assert(LDS_FUSED <= 80 * 1024, "two workgroups per CU");
   static_assert(16 * DV / 8 <= NTHR, "one 8-value piece of h / dh per thread");
 };
 
@@ -96,7 +110,7 @@ __device__ __forceinline__ float pick4(const float (&x)[4], int j) {
 // the permuted K order (lane group G holds 4 G.. and 16 + 4 G.. as one 8-run)
 __device__ __forceinline__ int perm_pos(int a) { return a < 4 ? 8 * a : 8 * (a - 4) + 4; }
 
-template <int DK, int DV>
+template <int DK, int DV, bool FUSED>
 __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   using C = BChunkCfg<DK, DV>;
   constexpr int NCB = C::NCB, NVB = C::NVB, KV = C::KV, NLD = C::NLD;
@@ -123,11 +137,22 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   float* sHH = reinterpret_cast<float*>(smem + C::OFF_HH);
   float* sBT = reinterpret_cast<float*>(smem + C::OFF_BT);
   float* sTL = reinterpret_cast<float*>(smem + C::OFF_TL);
+  float* sXS = reinterpret_cast<float*>(smem + C::OFF_XS);  // fused stage: f + delta [c][s]
+  float* sDL = reinterpret_cast<float*>(smem + C::OFF_DL);  // fused stage: delta [c]
+  float* sRN = reinterpret_cast<float*>(smem + C::OFF_RN);  // fused stage: 1/||q||, 1/||k|| [2][64]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, r16 = lane & 15;
   ChunkPos cp;
-  if (!chunk_pos(a.vl, blockIdx.x, blockIdx.y, blockIdx.z, a.T, a.H, a.NT, cp)) return;
+  // fused stage: this workgroup's slot of the decay-parameter partials
+  const size_t pslot = ((size_t)(blockIdx.z * gridDim.x + blockIdx.x) * a.H + blockIdx.y) * 4 + wave;
+  if (!chunk_pos(a.vl, blockIdx.x, blockIdx.y, blockIdx.z, a.T, a.H, a.NT, cp)) {
+    if constexpr (FUSED) {  // an unused slot of a packed grid adds zeros
+      for (int c = lane; c < DK; c += 64) a.PD[pslot * DK + c] = 0.f;
+      if (lane == 0) a.PA[pslot] = 0.f;
+    }
+    return;
+  }
   const int h = blockIdx.y, H = a.H;
   const size_t ch = cp.ch, row0 = cp.row0;
   // Rows in use.  Loads read in-range rows only (rows past a partial chunk's
@@ -136,10 +161,14 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   // dT, dA_qk, dR and dG are zero), and their outputs are not written.
   const int len = cp.len;
   // key-side inputs (q, k, g, b) live on the H / G key heads (value head h reads
-  // key head h / G); with G > 1 (part) the key-side gradients of this value head
-  // go to fp32 partials on the value-head axis, which the group reduction sums
+  // key head h / G); with G > 1 the key-side gradients of this value head go to
+  // fp32 partials on the value-head axis, which the group reduction sums (partq:
+  // dq, dk; partb: db and dg, the latter through a.dg).  The fused stage keeps
+  // dq, dk in fp32 also for G = 1 (one rounding after its normalisation VJP);
+  // for G = 1 both axes coincide.
   const int HK = H / a.G, hk = h / a.G;
-  const bool part = a.Pq != nullptr;
+  const bool partq = a.Pq != nullptr, partb = a.Pb != nullptr;
+  const bool part = partq || partb;
   const size_t KST = (size_t)HK * DK, VST = (size_t)H * DV;  // token strides
   const size_t kb0 = row0 * KST + (size_t)hk * DK, vb0 = row0 * VST + (size_t)h * DV;
   const size_t ko0 = part ? row0 * ((size_t)H * DK) + (size_t)h * DK : kb0;  // key-side outputs
@@ -154,9 +183,9 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   __bf16* dQp = reinterpret_cast<__bf16*>(a.dq) + ko0;
   __bf16* dKp = reinterpret_cast<__bf16*>(a.dk) + ko0;
   __bf16* dBp = reinterpret_cast<__bf16*>(a.db) + ko0;
-  float* pQp = part ? a.Pq + ko0 : nullptr;
-  float* pKp = part ? a.Pk + ko0 : nullptr;
-  float* pBp = part ? a.Pb + ko0 : nullptr;
+  float* pQp = partq ? a.Pq + ko0 : nullptr;
+  float* pKp = partq ? a.Pk + ko0 : nullptr;
+  float* pBp = partb ? a.Pb + ko0 : nullptr;
   float* dGp = a.dg + ko0;
   const __bf16* Vp = reinterpret_cast<const __bf16*>(a.v) + vb0;
   const __bf16* Wp = reinterpret_cast<const __bf16*>(a.w) + vb0;
@@ -176,6 +205,17 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   const int hc = (8 * tid) / DV, hv = (8 * tid) % DV;
   const bool hact = tid < 2 * DV;
   const int hp0 = (hv & ~31) + perm_pos((hv & 31) >> 2), hp1 = (hv & ~31) + perm_pos(((hv & 31) >> 2) + 1);
+  // fused stage: exp(a) of the key head; its decay bias and the chunk's inverse
+  // norms go to LDS (visible after the barrier that follows the prologue)
+  float Adec = 0.f;
+  if constexpr (FUSED) {
+    Adec = expf(a.st.a_log[hk]);
+    if (tid < DK) sDL[tid] = a.st.delta[(size_t)hk * DK + tid];
+    if (tid < 128) {
+      const float* rn = tid < 64 ? a.st.RQ : a.st.RK;
+      sRN[tid] = rn[(row0 + min(tid & 63, len - 1)) * HK + hk];
+    }
+  }
 
   // ---- loads in flight from the start: dR and A (cooperative), this wave's dO
   // rows and the operands of key block 0
@@ -225,8 +265,21 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   // Writes key block CB's staged operands (parity PAR for the small arrays):
   // in-block cumulative sums of the log2-decay and their factor tables, the
   // block totals and first rows, k / b / q columns, h / dh rows, rowsum(dh * h).
-#define GDR2_STAGE(PAR)                                                                    \
+#define GDR2_STAGE(PAR, CBS)                                                               \
   {                                                                                        \
+    const int cbs_ = (CBS);                                                                \
+    if constexpr (FUSED) {                                                                 \
+      const float4 dl_ = *reinterpret_cast<const float4*>(sDL + 16 * cbs_ + 4 * cq);       \
+      const float x_[4] = {pg.x + dl_.x, pg.y + dl_.y, pg.z + dl_.z, pg.w + dl_.w};        \
+      const float rq_ = sRN[grow], rk_ = sRN[64 + grow];                                   \
+      _Pragma("unroll") for (int u_ = 0; u_ < 4; ++u_) {                                   \
+        sXS[(4 * cq + u_) * LGT + grow] = x_[u_];                                          \
+        pk[u_] = (__bf16)((float)pk[u_] * rk_);                                            \
+        pq[u_] = (__bf16)((float)pq[u_] * rq_);                                            \
+      }                                                                                    \
+      pg = make_float4(-Adec * softplus_f(x_[0]), -Adec * softplus_f(x_[1]),               \
+                       -Adec * softplus_f(x_[2]), -Adec * softplus_f(x_[3]));              \
+    }                                                                                      \
     if (!grin) {                                                                           \
       pg = make_float4(0.f, 0.f, 0.f, 0.f);                                                \
       pk = bf4{};                                                                          \
@@ -398,10 +451,11 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     st4split(sTh + s * LT + rr, sTl + s * LT + rr, f4zero());
     st4split(sAh + s * LT + rr, sAl + s * LT + rr, f4zero());
   }
-  GDR2_STAGE(0)
+  GDR2_STAGE(0, 0)
   __syncthreads();
 
   const float scale = a.scale;
+  float pa_acc = 0.f;  // fused stage: sum of dg * g over this lane's outputs
 #pragma unroll 1
   for (int cb = 0; cb < NCB; ++cb) {
     const int par = cb & 1;
@@ -503,6 +557,8 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     const bf4 k4 = *reinterpret_cast<const bf4*>(sKc + r16 * LXT + rb);
     const bf4 b4 = *reinterpret_cast<const bf4*>(sBc + r16 * LXT + rb);
     const bf4 q4 = *reinterpret_cast<const bf4*>(sQc + r16 * LXT + rb);
+    float4 xs4 = make_float4(0.f, 0.f, 0.f, 0.f);  // fused stage: f + delta of rows rb + u, key c
+    if constexpr (FUSED) xs4 = *reinterpret_cast<const float4*>(sXS + r16 * LGT + rb);
     const float gam0 = ex2(G2fi), tb = ex2(G2l[3] - G2li);
     float dgl[4], tailp = 0.f;
 #pragma unroll
@@ -538,15 +594,17 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       }
       const int o = (rb + u) * kso + c;
       if (rb + u < len) {
-        if (part) {
+        if (partq) {
           pQp[o] = dq;
           pKp[o] = dEg * bv + dKg;
-          pBp[o] = dEg * kv;
         } else {
           dQp[o] = (__bf16)dq;
           dKp[o] = (__bf16)(dEg * bv + dKg);
-          dBp[o] = (__bf16)(dEg * kv);
         }
+        if (partb)
+          pBp[o] = dEg * kv;
+        else
+          dBp[o] = (__bf16)(dEg * kv);
       }
       dgl[u] = dq * qv - dKg * kv + dEg * bv * kv;
       tailp += x3[u] * kv * tl;
@@ -576,26 +634,57 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       off += sTL[(par * 4 + i2) * 16 + r16];
       if (i2 > i) off += sBT[(par * 4 + i2) * 16 + r16];
     }
-    if (rb + 0 < len) dGp[(rb + 0) * kso + c] = s0 + off;
-    if (rb + 1 < len) dGp[(rb + 1) * kso + c] = s1 + off;
-    if (rb + 2 < len) dGp[(rb + 2) * kso + c] = s2 + off;
-    if (rb + 3 < len) dGp[(rb + 3) * kso + c] = s3 + off;
-    if (cb + 1 < NCB) GDR2_STAGE(par ^ 1)
+    if constexpr (FUSED) {
+      // df = dg * dg/df, dg/df = -exp(a) sigmoid(f + delta); partial sums for ddelta and da
+      const float dgv[4] = {s0 + off, s1 + off, s2 + off, s3 + off};
+      const float xv[4] = {xs4.x, xs4.y, xs4.z, xs4.w};
+      float pdc = 0.f;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (rb + u < len) {
+          const float dfv = dgv[u] * (-Adec * sigmoid_f(xv[u]));
+          dGp[(rb + u) * kso + c] = dfv;
+          pdc += dfv;
+          pa_acc += dgv[u] * (-Adec * softplus_f(xv[u]));
+        }
+      }
+      pdc += __shfl_xor(pdc, 16);
+      pdc += __shfl_xor(pdc, 32);
+      if (g == 0) a.PD[pslot * DK + 16 * cb + r16] = pdc;
+    } else {
+      if (rb + 0 < len) dGp[(rb + 0) * kso + c] = s0 + off;
+      if (rb + 1 < len) dGp[(rb + 1) * kso + c] = s1 + off;
+      if (rb + 2 < len) dGp[(rb + 2) * kso + c] = s2 + off;
+      if (rb + 3 < len) dGp[(rb + 3) * kso + c] = s3 + off;
+    }
+    if (cb + 1 < NCB) GDR2_STAGE(par ^ 1, cb + 1)
     __syncthreads();
+  }
+  if constexpr (FUSED) {
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) pa_acc += __shfl_xor(pa_acc, o);
+    if (lane == 0) a.PA[pslot] = pa_acc;
   }
 #undef GDR2_PREFETCH
 #undef GDR2_STAGE
 }
 
-template <int DK, int DV>
-hipError_t launch_bchunk_bf16(const BChunkBf16Args& a, hipStream_t st) {
+template <int DK, int DV, bool FUSED>
+hipError_t launch_bchunk_bf16_t(const BChunkBf16Args& a, hipStream_t st) {
   using C = BChunkCfg<DK, DV>;
-  const void* fn = reinterpret_cast<const void*>(&bchunk_bf16_kernel<DK, DV>);
-  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+  constexpr int lds = FUSED ? C::LDS_FUSED : C::LDS;
+  const void* fn = reinterpret_cast<const void*>(&bchunk_bf16_kernel<DK, DV, FUSED>);
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) return e;
   dim3 grid(a.vl.ct0 ? a.vl.ncmax : a.NT, a.H, a.vl.ct0 ? 1 : a.B);
-  hipLaunchKernelGGL((bchunk_bf16_kernel<DK, DV>), grid, dim3(C::NTHR), C::LDS, st, a);
+  hipLaunchKernelGGL((bchunk_bf16_kernel<DK, DV, FUSED>), grid, dim3(C::NTHR), lds, st, a);
   return hipGetLastError();
+}
+
+template <int DK, int DV>
+hipError_t launch_bchunk_bf16(const BChunkBf16Args& a, hipStream_t st) {
+  return a.st.a_log != nullptr ? launch_bchunk_bf16_t<DK, DV, true>(a, st)
+                               : launch_bchunk_bf16_t<DK, DV, false>(a, st);
 }
 
 template hipError_t launch_bchunk_bf16<64, 64>(const BChunkBf16Args&, hipStream_t);

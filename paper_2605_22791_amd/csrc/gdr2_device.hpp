@@ -78,6 +78,20 @@ __device__ __forceinline__ float f4at(const float4& v, int u) {
 }
 
 __device__ __forceinline__ int pair_index(int i, int j) { return (i * (i + 1)) / 2 + j; }
+
+// ---- fused input stage (App. C.1, App. D.1 - D.2) ---------------------------
+// log(1 + e^x) as max(x, 0) + log1p(e^-|x|): no overflow for large x, and the
+// tiny values of very negative x keep their relative accuracy.
+__device__ __forceinline__ float softplus_f(float x) { return fmaxf(x, 0.f) + log1pf(expf(-fabsf(x))); }
+// logistic function, the derivative of softplus
+__device__ __forceinline__ float sigmoid_f(float x) {
+  const float e = expf(-fabsf(x)), r = 1.f / (1.f + e);
+  return x >= 0.f ? r : e * r;
+}
+// log-decay from the decay projection: g = -A softplus(f + delta), A = exp(a) of the key head
+__device__ __forceinline__ float decay_act(float f, float delta, float A) { return -A * softplus_f(f + delta); }
+// inverse norm of the L2 normalisation y = x (sum x^2 + eps)^(-1/2)
+__device__ __forceinline__ float inv_norm(float ss, float eps) { return 1.f / sqrtf(ss + eps); }
 __device__ __forceinline__ void pair_of(int p, int& i, int& j) {
   i = (p >= 6) ? 3 : (p >= 3) ? 2 : (p >= 1) ? 1 : 0;
   j = p - (i * (i + 1)) / 2;

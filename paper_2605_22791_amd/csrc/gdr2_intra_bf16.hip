@@ -13,9 +13,8 @@
 // fragment order (layout in gdr2_kernels.hpp) for the state scan; the
 // backward's recompute also keeps A itself (split hi/lo).
 //
-// Precision: T uses one bf16 pass; A enters Y and U as a bf16 operand (the
-// solve itself is fp32) and Y is stored in bf16; A_qk, Q_g, Ktail, Ebar, Z are
-// split hi/lo so their products are fp32-accurate.
+// Precision: every product is fp32-accurate (split hi/lo operands: T, the
+// solve, A in Y and U, A_qk, Q_g, Ktail, Ebar, Z); Y is stored in bf16.
 //
 // Decay factors are 2^(G2_r - G2_s) for r >= s, formed relative to the first
 // row p = 16 i of the row block i of r: 2^(G2_r - G2_p) * 2^(G2_p - G2_s); the
@@ -26,6 +25,13 @@
 // T and A_qk are computed transposed (rows = keys) so that each lane's four
 // outputs are consecutive keys of one query row: T goes to LDS as float4 rows
 // and A_qk / Y land directly in the permuted fragment order.
+//
+// Fused input stage (FUSED; App. C.1, App. D.2): q and k arrive raw and are
+// L2-normalised in registers as they are loaded (the lanes holding one row
+// reduce its sum of squares by shuffles), and the log-decay is formed in fp32
+// from the decay projection as -exp(a) softplus(f + delta) before the
+// cumulative sum, so the normalised tensors and g never exist in HBM.  The
+// inverse norms go to the workspace for the backward.
 
 #include "gdr2_kernels.hpp"
 #include "gdr2_bf16.hpp"
@@ -47,7 +53,8 @@ struct IntraCfg {
   static constexpr int OFF_K = SZ_X;
   static constexpr int OFF_TA = OFF_K + 64 * LKB * 2;
   static constexpr int OFF_MISC = OFF_TA + 64 * LTA * 4;
-  static constexpr int LDS = OFF_MISC + 16;
+  static constexpr int OFF_RQ = OFF_MISC + 16;  // fused stage: inverse norms of the q rows [64]
+  static constexpr int LDS = OFF_RQ + 64 * 4;
   static_assert(LDS <= 80 * 1024, "two workgroups per CU");
 };
 
@@ -75,7 +82,7 @@ __device__ __forceinline__ int zero_tile(int z) {
   }
 }
 
-template <int DK, int DV>
+template <int DK, int DV, bool FUSED>
 __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
   using C = IntraCfg<DK, DV>;
   constexpr int KS = C::KS, NCB = C::NCB, NVB = C::NVB;
@@ -90,6 +97,7 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
   __bf16* sK = reinterpret_cast<__bf16*>(smem + C::OFF_K);
   float* sTA = reinterpret_cast<float*>(smem + C::OFF_TA);
   int* unsafe = reinterpret_cast<int*>(smem + C::OFF_MISC);
+  float* sRQ = reinterpret_cast<float*>(smem + C::OFF_RQ);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, r16 = lane & 15;
@@ -123,6 +131,14 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
   float4 gr[NG];
 #pragma unroll
   for (int m = 0; m < NG; ++m) gr[m] = *reinterpret_cast<const float4*>(a.g + kofs(NG * gsg + m) + 4 * gcg);
+  // fused stage: decay bias of this thread's 4 channels and exp(a) of the key head
+  float4 dlt = make_float4(0.f, 0.f, 0.f, 0.f);
+  float Adec = 0.f;
+  if constexpr (FUSED) {
+    dlt = *reinterpret_cast<const float4*>(a.st.delta + (size_t)hk * DK + 4 * gcg);
+    Adec = expf(a.st.a_log[hk]);
+  }
+  const bool wr_norm = FUSED && (h % a.G) == 0;  // one value head of the group writes the inverse norms
   u4v kst[NKC];
 #pragma unroll
   for (int m = 0; m < NKC; ++m) {
@@ -158,12 +174,38 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
     float4 run = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
     for (int m = 0; m < NG; ++m) {
+      if constexpr (FUSED) {
+        gr[m].x = decay_act(gr[m].x, dlt.x, Adec);
+        gr[m].y = decay_act(gr[m].y, dlt.y, Adec);
+        gr[m].z = decay_act(gr[m].z, dlt.z, Adec);
+        gr[m].w = decay_act(gr[m].w, dlt.w, Adec);
+      }
       if (NG * gsg + m >= len) gr[m] = make_float4(0.f, 0.f, 0.f, 0.f);
       run.x += gr[m].x * kLog2e; run.y += gr[m].y * kLog2e;
       run.z += gr[m].z * kLog2e; run.w += gr[m].w * kLog2e;
       gr[m] = run;
     }
     tot[gsg * GCG + gcg] = run;
+    if constexpr (FUSED) {
+      // k rows: the DK / 8 consecutive lanes holding a row reduce its sum of squares
+#pragma unroll
+      for (int m = 0; m < NKC; ++m) {
+        const int e = tid + 256 * m, r = e / (DK / 8);
+        float kf[8];
+        unpack8(kst[m], kf);
+        float ss = 0.f;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) ss += kf[u] * kf[u];
+#pragma unroll
+        for (int o = 1; o < DK / 8; o <<= 1) ss += __shfl_xor(ss, o);
+        const float rk = inv_norm(ss, a.st.eps);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) kf[u] *= rk;
+        kst[m] = __builtin_bit_cast(u4v, round8(kf));
+        if (wr_norm && a.st.RK != nullptr && (e % (DK / 8)) == 0 && r < len)
+          a.st.RK[(row0 + r) * HK + hk] = rk;
+      }
+    }
 #pragma unroll
     for (int m = 0; m < NKC; ++m) {
       const int e = tid + 256 * m, r = e / (DK / 8), c8 = (e % (DK / 8)) * 8;
@@ -186,6 +228,35 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
     if (sG[(16 * i) * LG + c] - sG[(16 * i + 15) * LG + c] > kDiagLimit2) unsafe[i] = 1;
   }
   for (int c = tid; c < DK; c += 256) a.GC[ch * (WsBf16::gc(DK) / 4) + c] = ex2(sG[(CH - 1) * LG + c]);
+  if constexpr (FUSED) {
+    // q rows: the four lane groups of a row reduce its sum of squares
+#pragma unroll
+    for (int sl = 0; sl < 2; ++sl) {
+      if (sl == 1 && wave != 0) continue;
+      float qf[KS][8];
+      float ss = 0.f;
+#pragma unroll
+      for (int p = 0; p < KS; ++p) {
+        unpack8(qreg[sl][p], qf[p]);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) ss += qf[p][u] * qf[p][u];
+      }
+      ss += __shfl_xor(ss, 16);
+      ss += __shfl_xor(ss, 32);
+      const float rq = inv_norm(ss, a.st.eps);
+#pragma unroll
+      for (int p = 0; p < KS; ++p) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) qf[p][u] *= rq;
+        qreg[sl][p] = __builtin_bit_cast(u4v, round8(qf[p]));
+      }
+      const int row = 16 * (sl == 0 ? rbA : 1) + r16;
+      if (g == 0 && !(sl == 0 && wave == 3)) {  // wave 3 holds a copy of wave 2's rows
+        sRQ[row] = rq;
+        if (wr_norm && a.st.RQ != nullptr && row < len) a.st.RQ[(row0 + row) * HK + hk] = rq;
+      }
+    }
+  }
   for (int e = tid; e < 6 * 256; e += 256) {  // upper blocks of T/A (the region held scratch)
     const int blk = e >> 8, rr = (e & 255) >> 4, cc = e & 15;
     const int bi = blk < 3 ? 0 : (blk < 5 ? 1 : 2);
@@ -251,7 +322,10 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
             for (int c = 0; c < DK; ++c) {
               const float e = ex2(sG[r * LG + c] - sG[s * LG + c]) * (float)sK[s * LKB + c];
               tt += (float)Bg[kofs(r) + c] * (float)sK[r * LKB + c] * e;
-              ta += (float)Q[kofs(r) + c] * e;
+              if constexpr (FUSED)
+                ta += (float)(__bf16)((float)Q[kofs(r) + c] * sRQ[r]) * e;
+              else
+                ta += (float)Q[kofs(r) + c] * e;
             }
           }
 #pragma unroll
@@ -284,7 +358,7 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
             lq[e] = qr[e] * f;
           }
           const Fr rkf = split8(rk);
-          accT = mma(rkf.hi, round8(le), accT);
+          accT = mma3(rkf, split8(le), accT);
           accA = mma3(rkf, split8(lq), accA);
         }
       }
@@ -444,7 +518,7 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
         for (int kb = 0; kb <= (i >> 1); ++kb) {
           float av[8];
           ldf8(sTA + (16 * i + r16) * LTA + 32 * kb + 8 * g, av);
-          acc = mma2a(ef[kb], round8(av), acc);
+          acc = mma3(ef[kb], split8(av), acc);
         }
         st4(reinterpret_cast<__bf16*>(Yo + (size_t)(i * KS + (cb >> 1)) * 1024 + 16 * lane + 8 * (cb & 1)), acc[0],
             acc[1], acc[2], acc[3]);
@@ -484,7 +558,7 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
         for (int kb = 0; kb <= (i >> 1); ++kb) {
           float av[8];
           ldf8(sTA + (16 * i + r16) * LTA + 32 * kb + 8 * g, av);
-          acc = mma2b(round8(av), zf[kb], acc);
+          acc = mma3(split8(av), zf[kb], acc);
         }
         *reinterpret_cast<f4*>(Uo + ((size_t)(vb * 4 + i) * 64 + lane) * 4) = acc;
       }
@@ -492,15 +566,20 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
   }
 }
 
-template <int DK, int DV>
-hipError_t launch_intra_bf16(const IntraBf16Args& a, hipStream_t st) {
+template <int DK, int DV, bool FUSED>
+hipError_t launch_intra_bf16_t(const IntraBf16Args& a, hipStream_t st) {
   using C = IntraCfg<DK, DV>;
-  const void* fn = reinterpret_cast<const void*>(&intra_bf16_kernel<DK, DV>);
+  const void* fn = reinterpret_cast<const void*>(&intra_bf16_kernel<DK, DV, FUSED>);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
   if (e != hipSuccess) return e;
   dim3 grid(a.vl.ct0 ? a.vl.ncmax : a.NT, a.H, a.vl.ct0 ? 1 : a.B);
-  hipLaunchKernelGGL((intra_bf16_kernel<DK, DV>), grid, dim3(C::NTHR), C::LDS, st, a);
+  hipLaunchKernelGGL((intra_bf16_kernel<DK, DV, FUSED>), grid, dim3(C::NTHR), C::LDS, st, a);
   return hipGetLastError();
+}
+
+template <int DK, int DV>
+hipError_t launch_intra_bf16(const IntraBf16Args& a, hipStream_t st) {
+  return a.st.a_log != nullptr ? launch_intra_bf16_t<DK, DV, true>(a, st) : launch_intra_bf16_t<DK, DV, false>(a, st);
 }
 
 template hipError_t launch_intra_bf16<64, 64>(const IntraBf16Args&, hipStream_t);

@@ -73,6 +73,21 @@ __device__ __forceinline__ void scan_rows(const Varlen& vl, int q, int H, int T,
   }
 }
 
+// Fused input stage (App. C.1, App. D.2), active when a_log is set: q and k
+// are the raw projections and are L2-normalised per (token, key head) on load,
+// y = x (sum x^2 + eps)^(-1/2), rounded to bf16 as the operands of the bf16
+// path; g holds the decay projection f, and the log-decay is formed on load in
+// fp32 as -exp(a_log[hk]) softplus(f + delta[hk][c]).  The intra-chunk kernel
+// writes the inverse norms to RQ / RK ((rows, H / G) fp32, nullable) for the
+// backward, which reads them there.
+struct Stage {
+  const float* a_log = nullptr;  // (H / G) decay magnitude per key head
+  const float* delta = nullptr;  // (H / G, Dk) decay bias per key channel
+  float eps = 0.f;
+  float* RQ = nullptr;
+  float* RK = nullptr;
+};
+
 // Arguments of the intra-chunk forward kernel.  Inputs use the operator's
 // token-major layouts; outputs are per-chunk-head workspace tiles, chunk-head
 // index ch = (b * H + h) * NT + n.
@@ -176,6 +191,7 @@ struct RecurArgs {
   float scale;
   const int* cu = nullptr;  // packed sequences: tokens cu[s] .. cu[s+1) of sequence s (B = 1)
   int G = 1;                // grouped value heads (as in IntraArgs)
+  Stage st{};               // fused input stage (RQ, RK unused)
 };
 
 // ---------------------------------------------------------------------------
@@ -227,6 +243,7 @@ struct IntraBf16Args {
   int B, T, H, NT;
   Varlen vl{};
   int G = 1;  // grouped value heads: H value heads share H / G key heads (q, k, g, b)
+  Stage st{};
 };
 
 // Sequence-parallel scans: with nseg > 1 every sequence is cut into nseg
@@ -316,11 +333,21 @@ struct BChunkBf16Args {
   // grouped value heads: H value heads share H / G key heads.  With G > 1 the
   // key-side gradients of each value head go, in fp32 and on the value-head
   // axis, to Pq, Pk, Pb and to dg (then a (B*T, H, Dk) fp32 partial), and the
-  // group reduction sums them.
+  // group reduction sums them.  Pq / Pk and Pb are independent: the fused stage
+  // sets Pq, Pk alone for G = 1.
   int G = 1;
   float* Pq = nullptr;
   float* Pk = nullptr;
   float* Pb = nullptr;
+  // fused input stage: q, k raw (normalised with the stored inverse norms), g
+  // holds f and dg receives df = dg * dg/df; dq and dk stay the gradients of the
+  // normalised q, k (the normalisation VJP follows in its own kernel).  Per
+  // workgroup (chunk slot s = z * gridDim.x + x, value head h, wave i) PD gets
+  // sum_rows df over each key channel and PA sum_{rows, channels} dg * g:
+  // PD ((s * H + h) * 4 + i) * Dk + c, PA (s * H + h) * 4 + i.
+  Stage st{};
+  float* PD = nullptr;
+  float* PA = nullptr;
 };
 
 template <int DK, int DV>
@@ -351,6 +378,30 @@ hipError_t launch_recurrent(const RecurArgs<TIn>& a, int B, hipStream_t st);
 // r < rows, key heads h < Hk, channels c < D (P fp32 on the value-head axis).
 template <typename TOut>
 hipError_t launch_group_reduce(const float* P, TOut* out, size_t rows, int Hk, int G, int D, hipStream_t st);
+
+// Normalisation VJP of the fused stage (App. D.2): for rows r < rows, key
+// heads hk < Hk, dx = rinv (dy - y <y, dy>), y = rinv x, with x the raw q or
+// k (bf16), rinv its stored inverse norm and dy the gradient of the normalised
+// tensor: the sum of the G fp32 partials P[r, hk * G + j, :], or bf16 DY when
+// P is null (dx may alias it).  Two tensors (q, k) per launch.
+struct NormVjpArgs {
+  const bf16_t* x[2];
+  const float* rinv[2];
+  const bf16_t* DY[2];
+  const float* P[2];
+  bf16_t* dx[2];
+  size_t rows;
+  int Hk, G;
+};
+template <int DK>
+hipError_t launch_norm_vjp(const NormVjpArgs& a, hipStream_t st);
+
+// Sums of the per-workgroup partials of the decay parameters, one pass:
+// out[(z * Hk + hk) * D + c] = sum over the slots s of range z (nslots cut into
+// `splits` ranges) and m < M of P[((s * Hk + hk) * M + m) * D + c].  A second
+// pass with nslots = splits, M = 1, splits = 1 adds the ranges.
+hipError_t launch_param_reduce_pass(const float* P, float* out, int nslots, int Hk, int M, int D, int splits,
+                                    hipStream_t st);
 
 // Builds the chunk table of a packed call (Varlen) from cu_seqlens: lengths
 // are clamped into [0, T] and the chunk count to ncmax, so malformed offsets

@@ -7,10 +7,27 @@
 //     o    = scale * S^T q = scale * (Sbar^T q + (w*v - r) (k . q)),
 // so S is read and written once per call; the column sums r and Sbar^T q are
 // reduced across the row groups through LDS in a fixed order.
+//
+// Fused input stage (a.st.a_log set; App. C.1, App. D.2): q and k are the raw
+// projections, L2-normalised per token in fp32 and rounded to the operand
+// dtype, as the chunk path does; the log-decay is -exp(a) softplus(f + delta)
+// from the decay projection f.
 
 #include "gdr2_kernels.hpp"
 
 namespace gdr2 {
+
+// x rounded to the operand dtype (nearest, ties to even)
+template <typename TIn>
+__device__ __forceinline__ float round_as(float x);
+template <>
+__device__ __forceinline__ float round_as<float>(float x) { return x; }
+template <>
+__device__ __forceinline__ float round_as<bf16_t>(float x) {
+  bf16_t t;
+  put(&t, x);
+  return to_f(t);
+}
 
 template <int DK, int DV, typename TIn>
 __global__ __launch_bounds__(256) void recurrent_kernel(RecurArgs<TIn> a) {
@@ -19,6 +36,7 @@ __global__ __launch_bounds__(256) void recurrent_kernel(RecurArgs<TIn> a) {
   constexpr int RG = NTHR / CG;     // row groups
   constexpr int RPG = DK / RG;      // rows per thread
   static_assert(NTHR % CG == 0 && DK % RG == 0, "thread split");
+  static_assert(DK <= NTHR, "one key channel per thread");
   const int seq = blockIdx.x;
   const int bb = seq / a.H, h = seq % a.H;
   const int tid = threadIdx.x, cg = tid % CG, rg = tid / CG;
@@ -27,7 +45,7 @@ __global__ __launch_bounds__(256) void recurrent_kernel(RecurArgs<TIn> a) {
   __shared__ float sAl[DK], sE[DK], sK[DK], sQ[DK], sZ[DV];
   __shared__ float redR[RG * DV], redP[RG * DV];
   __shared__ float sRes[DV], sP[DV];
-  __shared__ float sKQ[NTHR / 64];
+  __shared__ float sKQ[NTHR / 64], sKK[NTHR / 64], sQQ[NTHR / 64];
 
   float* Sg = a.S + (size_t)seq * DK * DV;
   float4 S[RPG];
@@ -43,18 +61,49 @@ __global__ __launch_bounds__(256) void recurrent_kernel(RecurArgs<TIn> a) {
     rbase = 0;
   }
   const int HK = H / a.G, hk = h / a.G;  // key side (q, k, g, b) on the H / G key heads
+  const bool fused = a.st.a_log != nullptr;
+  const float Adec = fused ? expf(a.st.a_log[hk]) : 0.f;
   for (int t = t0; t < t1; ++t) {
     const size_t row = (rbase + t) * H + h, rowk = (rbase + t) * HK + hk;
+    // thread c < DK holds key channel c of this token (DK <= NTHR)
+    const int c = tid;
+    float kv = 0.f, qv = 0.f;
+    if (c < DK) {
+      kv = to_f(a.k[rowk * DK + c]);
+      qv = to_f(a.q[rowk * DK + c]);
+      const float gv = a.g[rowk * DK + c];
+      sAl[c] = expf(fused ? decay_act(gv, a.st.delta[(size_t)hk * DK + c], Adec) : gv);
+    }
+    for (int v = tid; v < DV; v += NTHR) sZ[v] = to_f(a.w[row * DV + v]) * to_f(a.v[row * DV + v]);
+    if (fused) {
+      // fused stage: sums of squares over the row, then y = x (sum x^2 + eps)^(-1/2) in the operand dtype
+      float kk = kv * kv, qq = qv * qv;
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) {
+        kk += __shfl_xor(kk, m);
+        qq += __shfl_xor(qq, m);
+      }
+      if ((tid & 63) == 0) {
+        sKK[tid >> 6] = kk;
+        sQQ[tid >> 6] = qq;
+      }
+      __syncthreads();
+      float sk = 0.f, sq = 0.f;
+#pragma unroll
+      for (int w2 = 0; w2 < NTHR / 64; ++w2) {
+        sk += sKK[w2];
+        sq += sQQ[w2];
+      }
+      kv = round_as<TIn>(kv * inv_norm(sk, a.st.eps));
+      qv = round_as<TIn>(qv * inv_norm(sq, a.st.eps));
+    }
     float kq = 0.f;
-    for (int c = tid; c < DK; c += NTHR) {
-      const float kv = to_f(a.k[rowk * DK + c]), qv = to_f(a.q[rowk * DK + c]);
-      sAl[c] = expf(a.g[rowk * DK + c]);
+    if (c < DK) {
       sK[c] = kv;
       sQ[c] = qv;
       sE[c] = to_f(a.b[rowk * DK + c]) * kv;
-      kq += kv * qv;
+      kq = kv * qv;
     }
-    for (int v = tid; v < DV; v += NTHR) sZ[v] = to_f(a.w[row * DV + v]) * to_f(a.v[row * DV + v]);
 #pragma unroll
     for (int m = 32; m >= 1; m >>= 1) kq += __shfl_xor(kq, m);
     if ((tid & 63) == 0) sKQ[tid >> 6] = kq;

@@ -35,7 +35,8 @@ def test_header_declares_the_entry_points():
                                           "gdr2_varlen_workspace_bytes", "gdr2_chunk_fwd_varlen",
                                           "gdr2_chunk_bwd_varlen", "gdr2_recurrent_varlen",
                                           "gdr2_status_str", "gdr2_profile_enable",
-                                          "gdr2_profile_collect"])
+                                          "gdr2_profile_collect", "gdr2_fused_workspace_bytes",
+                                          "gdr2_fused_fwd", "gdr2_fused_bwd", "gdr2_fused_recurrent"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -53,13 +54,14 @@ def test_status_strings():
 
 def test_profile_collect_without_launches():
     L = g2.lib()
-    ms = (ctypes.c_double * 8)()
-    n = (ctypes.c_longlong * 8)()
-    assert L.gdr2_profile_collect(ms, n, 7) == g2.GDR2_EINVAL
+    k = len(g2.KERNEL_NAMES)
+    ms = (ctypes.c_double * k)()
+    n = (ctypes.c_longlong * k)()
+    assert L.gdr2_profile_collect(ms, n, k - 1) == g2.GDR2_EINVAL
     assert L.gdr2_profile_enable(1) == g2.GDR2_OK
-    assert L.gdr2_profile_collect(ms, n, 8) == g2.GDR2_OK
+    assert L.gdr2_profile_collect(ms, n, k) == g2.GDR2_OK
     assert L.gdr2_profile_enable(0) == g2.GDR2_OK
-    assert list(n) == [0] * 8 and list(ms) == [0.0] * 8
+    assert list(n) == [0] * k and list(ms) == [0.0] * k
 
 
 def _prob(**kw):
@@ -324,3 +326,80 @@ def test_grouped_value_heads_validation_and_workspace():
         _, base, _ = ws_layout_bf16(B, T, Hv, Dk, Dv, bwd=True)
         part = 4 * r(B * T * Hv * Dk) if Hv > H else 0
         assert g2.gdr2_chunk_workspace_bytes(p, 1) == base + part + seg_buffer_bytes(B, T, Hv, Dk, Dv)
+
+
+# --------------------------------------------------------------------------- fused input stage
+def _stg(a=FAKE, d=FAKE, eps=1e-6):
+    return g2.Gdr2Stage(a, d, eps)
+
+
+def _ffwd(prob, stage, cu=None, n=0, ws_bytes=1 << 40, save=0):
+    L = g2.lib()
+    p = [FAKE] * 6 + [None, FAKE, None, FAKE]
+    return L.gdr2_fused_fwd(ctypes.byref(prob), ctypes.byref(stage) if stage is not None else None,
+                            ctypes.c_void_p(cu) if cu else None, n,
+                            *[ctypes.c_void_p(x) if x else None for x in p], ws_bytes, save, None)
+
+
+def _fbwd(prob, stage, da=FAKE, ddelta=FAKE, ws_bytes=1 << 40, saved=0):
+    L = g2.lib()
+    p = [FAKE] * 6 + [None, FAKE, None] + [FAKE] * 4 + [da, ddelta] + [FAKE, FAKE, None, FAKE]
+    return L.gdr2_fused_bwd(ctypes.byref(prob), ctypes.byref(stage) if stage is not None else None, None, 0,
+                            *[ctypes.c_void_p(x) if x else None for x in p], ws_bytes, saved, None)
+
+
+def test_fused_stage_validation():
+    """The stage needs a_log (4-byte aligned), delta (16-byte aligned) and a finite
+    eps >= 0; the chunk calls are bf16 only; the backward needs da and an aligned
+    ddelta -- all rejected before any launch."""
+    L = g2.lib()
+    p = _prob()
+    for call in (_ffwd, _fbwd):
+        assert call(p, None) == g2.GDR2_EINVAL
+        assert call(p, _stg(a=0)) == g2.GDR2_EINVAL
+        assert call(p, _stg(d=0)) == g2.GDR2_EINVAL
+        assert call(p, _stg(a=FAKE + 2)) == g2.GDR2_EINVAL
+        assert call(p, _stg(d=FAKE + 4)) == g2.GDR2_EINVAL
+        assert call(p, _stg(eps=-1e-6)) == g2.GDR2_EINVAL
+        assert call(p, _stg(eps=float("nan"))) == g2.GDR2_EINVAL
+        assert call(_prob(dtype=g2.GDR2_FP32), _stg()) == g2.GDR2_EUNSUPPORTED
+        assert call(_prob(Dk=96), _stg()) == g2.GDR2_EUNSUPPORTED
+    assert _fbwd(p, _stg(), da=0) == g2.GDR2_EINVAL
+    assert _fbwd(p, _stg(), ddelta=FAKE + 4) == g2.GDR2_EINVAL
+    n = ctypes.c_size_t(0)
+    assert L.gdr2_fused_workspace_bytes(ctypes.byref(_prob(dtype=g2.GDR2_FP32)), 0, 0, ctypes.byref(n)) == \
+        g2.GDR2_EUNSUPPORTED
+    assert L.gdr2_fused_workspace_bytes(ctypes.byref(p), -1, 0, ctypes.byref(n)) == g2.GDR2_EINVAL
+    fwd = g2.gdr2_fused_workspace_bytes(p, 0, 0)
+    bwd = g2.gdr2_fused_workspace_bytes(p, 0, 1)
+    assert _ffwd(p, _stg(), ws_bytes=fwd - 1) == g2.GDR2_EWORKSPACE
+    assert _ffwd(p, _stg(), ws_bytes=fwd, save=1) == g2.GDR2_EWORKSPACE
+    assert _fbwd(p, _stg(), ws_bytes=bwd - 1) == g2.GDR2_EWORKSPACE
+    # packed: B must be 1, cu_seqlens needed when n_seqs > 0
+    assert _ffwd(_prob(B=2), _stg(), cu=FAKE, n=3) == g2.GDR2_EINVAL
+    assert _ffwd(_prob(B=1), _stg(), cu=None, n=3) == g2.GDR2_EINVAL
+    vp = lambda xs: [ctypes.c_void_p(x) if x else None for x in xs]
+    st = _stg(d=FAKE + 4)
+    assert L.gdr2_fused_recurrent(ctypes.byref(p), ctypes.byref(st), None, 0, *vp([FAKE] * 8), None) == \
+        g2.GDR2_EINVAL
+    assert L.gdr2_fused_recurrent(ctypes.byref(p), None, None, 0, *vp([FAKE] * 8), None) == g2.GDR2_EINVAL
+
+
+def test_fused_workspace_size():
+    """The fused forward needs what the plain one needs; a saving forward and the
+    backward add the inverse norms of q and k ((B T, H) fp32 each), the per-
+    workgroup decay-parameter partials (slots x Hv x 4 waves x (Dk + 1)), the
+    64-range sums (64 x H x (Dk + 1)) and, for Hv = H, fp32 gradients of the
+    normalised q and k ((B T, Hv, Dk) each)."""
+    r = lambda x: (x * 4 + 255) // 256 * 256
+    for (B, T, H, Hv, Dk, Dv, N) in [(2, 256, 4, 4, 128, 64, 0), (1, 100, 2, 8, 64, 128, 0),
+                                     (1, 1000, 4, 4, 128, 128, 3)]:
+        p = _prob(B=B, T=T, H=H, Hv=Hv, Dk=Dk, Dv=Dv)
+        plain = (lambda bwd: g2.gdr2_varlen_workspace_bytes(p, N, bwd)) if N else \
+            (lambda bwd: g2.gdr2_chunk_workspace_bytes(p, bwd))
+        assert g2.gdr2_fused_workspace_bytes(p, N, 0) == plain(0)
+        slots = T // 64 + N if N else B * (-(-T // 64))
+        extra = 2 * r(B * T * H) + r(slots * Hv * 4 * Dk) + r(slots * Hv * 4) + r(64 * H * (Dk + 1))
+        if Hv == H:   # fp32 dq, dk of the normalised tensors (grouped calls have them already)
+            extra += 2 * r(B * T * Hv * Dk)
+        assert g2.gdr2_fused_workspace_bytes(p, N, 1) == plain(1) + extra, (B, T, H, Hv, N)

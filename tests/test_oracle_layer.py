@@ -14,7 +14,7 @@ import pytest
 
 from oracle import fd, gdr2_recurrent_fwd
 from oracle.layer import (decay_activation, decay_activation_vjp, gdr2_fused_bwd, gdr2_fused_fwd, l2norm,
-                          l2norm_vjp, softplus)
+                          l2norm_vjp, round_bf16, softplus)
 from paper_2605_22791_amd.inputs import make_fused
 from tests.helpers import rel_l2
 
@@ -188,3 +188,47 @@ def test_L11_fused_adjoint_grouped_and_packed():
     _fused_fd_check(d, ("q", "k", "f", "a", "delta", "b"))
     d = make_fused(0, 0, 2, 4, 3, seed=13, dtype="fp32", lengths=[3, 0, 4], s0_std=0.1, with_dST=True)
     _fused_fd_check(d, ("q", "k", "f", "a", "delta"))
+
+
+def test_L12_bf16_rounding_is_the_nearest_bf16_value():
+    """Against brute force: the two bfloat16 neighbours of x (all 2^16 bit
+    patterns, decoded by their definition sign * 2^(e - 127) * 1.m) and the
+    nearer one, ties to the even significand."""
+    bits = np.arange(1 << 15, dtype=np.int64)            # non-negative patterns
+    ex = (bits >> 7) & 0xFF
+    man = bits & 0x7F
+    ok = ex < 255
+    vals = np.where(ex == 0, man * 2.0 ** -133, (1.0 + man / 128.0) * np.exp2(ex.astype(np.float64) - 127.0))
+    vals, codes = vals[ok], bits[ok]
+    rng = np.random.default_rng(8)
+    x = np.concatenate([rng.standard_normal(3000) * np.exp2(rng.integers(-40, 40, 3000)),
+                        # exact midpoints between neighbours (ties)
+                        (vals[1000:1100] + vals[1001:1101]) / 2, -(vals[5000:5050] + vals[5001:5051]) / 2])
+    got = round_bf16(x)
+    for xi, gi in zip(x, got):
+        a = abs(xi)
+        j = np.searchsorted(vals, a)
+        lo, hi = vals[j - 1], vals[j]
+        if a - lo < hi - a:
+            want = lo
+        elif hi - a < a - lo:
+            want = hi
+        else:
+            want = lo if codes[j - 1] % 2 == 0 else hi
+        assert gi == np.copysign(want, xi), (xi, gi, want)
+    assert round_bf16(0.0) == 0.0 and np.isinf(round_bf16(np.inf))
+
+
+def test_L13_bf16_operator_rounds_the_normalised_inputs():
+    """With dtype bf16 the fused forward equals the fp64 one on the rounded
+    normalised q, k (same g), and differs from the unrounded one."""
+    d = make_fused(1, 9, 2, 8, 4, seed=14, dtype="bf16", s0_std=0.1)
+    args = [d[n] for n in ("q", "k", "v", "f", "a", "delta", "b", "w", "S0")]
+    o_b, s_b = gdr2_fused_fwd(*args, d["scale"], d["eps"], dtype="bf16")
+    o_f, _ = gdr2_fused_fwd(*args, d["scale"], d["eps"])
+    qn = round_bf16(l2norm(d["q"], d["eps"]))
+    kn = round_bf16(l2norm(d["k"], d["eps"]))
+    g = decay_activation(d["f"], d["a"], d["delta"])
+    o_r, s_r = gdr2_recurrent_fwd(qn, kn, d["v"], g, d["b"], d["w"], d["S0"], d["scale"])
+    assert np.array_equal(o_b, o_r) and np.array_equal(s_b, s_r)
+    assert rel_l2(o_b, o_f) > 1e-5
