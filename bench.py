@@ -336,6 +336,75 @@ def grouped_bench(steps=10, stored=True):
             "ms_per_step": ms, "tokens_per_s": 8 * 4096 / (ms * 1e-3), "kernels_avg_us": kern}
 
 
+def fused_bench(steps=10, stored=True):
+    """Fused input stage at the headline shape (B8 T4096 H16 d128 bf16): the
+    step from the raw projections (q, k unnormalised, the decay projection f,
+    a, delta) with normalisation and activation inside the kernels, against
+    the same step composed from separate torch passes (normalise q, k, form
+    g, run the plain operator, then the two VJPs)."""
+    import torch
+    import torch.nn.functional as F
+    import paper_2605_22791_amd as g2
+    from paper_2605_22791_amd.inputs import make_fused
+    d = make_fused(8, 4096, 16, 128, 128, seed=51, dtype="bf16")
+    tb = lambda x: torch.from_numpy(x).cuda().to(torch.bfloat16).contiguous()
+    tf = lambda x: torch.from_numpy(x).cuda().contiguous()
+    q, k, v, b, w, do = (tb(d[n]) for n in ("q", "k", "v", "b", "w", "do"))
+    f, a, delta = tf(d["f"]), tf(d["a"]), tf(d["delta"])
+    sc, eps = d["scale"], d["eps"]
+    prob = g2.Gdr2Problem(8, 4096, 16, 128, 128, 64, sc, g2.GDR2_BF16)
+    ws_f = torch.empty(g2.gdr2_fused_workspace_bytes(prob, 0, 1), dtype=torch.uint8, device="cuda")
+    ws_p = torch.empty(g2.gdr2_chunk_workspace_bytes(prob, 1), dtype=torch.uint8, device="cuda")
+
+    def fused():
+        g2.gdr2_fused_fwd(q, k, v, f, a, delta, b, w, None, scale=sc, eps=eps, ws=ws_f, save=stored)
+        g2.gdr2_fused_bwd(q, k, v, f, a, delta, b, w, None, do, None, scale=sc, eps=eps, ws=ws_f, saved=stored)
+
+    def composed():
+        qf, kf = q.float(), k.float()
+        rq = torch.rsqrt((qf * qf).sum(-1, keepdim=True) + eps)
+        rk = torch.rsqrt((kf * kf).sum(-1, keepdim=True) + eps)
+        A = a.exp()[:, None]
+        x = f + delta
+        g = (-A * F.softplus(x)).contiguous()
+        qn, kn = (qf * rq).bfloat16(), (kf * rk).bfloat16()
+        g2.gdr2_chunk_fwd(qn, kn, v, g, b, w, None, scale=sc, ws=ws_p, save=stored)
+        gr = g2.gdr2_chunk_bwd(qn, kn, v, g, b, w, None, do, None, scale=sc, ws=ws_p, saved=stored)
+        for xf, r, dy in ((qf, rq, gr["dq"]), (kf, rk, gr["dk"])):
+            y, dyf = xf * r, dy.float()
+            (r * (dyf - y * (y * dyf).sum(-1, keepdim=True))).bfloat16()
+        dg = gr["dlog_alpha"]
+        df = dg * (-A * torch.sigmoid(x))
+        df.sum((0, 1))
+        (dg * g).sum((0, 1, 3))
+
+    def timed(fn, prof=False):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        if prof:
+            g2.gdr2_profile_enable(True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        kern = None
+        if prof:
+            per_kernel = g2.gdr2_profile_collect()
+            g2.gdr2_profile_enable(False)
+            kern = {n: round(kms / cnt * 1e3, 1) for n, (kms, cnt) in per_kernel.items() if cnt}
+        return e0.elapsed_time(e1) / steps, kern
+
+    ms_f, kern = timed(fused, prof=True)
+    ms_c, _ = timed(composed)
+    return {"workload": "fused input stage, B8 T4096 H16 d128 bf16 (raw q, k, decay projection f)",
+            "training_path": "stored" if stored else "recompute", "ms_per_step": ms_f,
+            "tokens_per_s": 8 * 4096 / (ms_f * 1e-3), "kernels_avg_us": kern,
+            "composed_ms_per_step": ms_c, "composed": "torch passes for the stage and its VJPs around the plain operator"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -353,6 +422,9 @@ def main():
     ap.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
                     help="run one copy-like elementwise kernel (torch.neg) over MIB MiB of fp32 before the "
                          "timed steps: the reference that scales rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes")
+    ap.add_argument("--fused-only", action="store_true",
+                    help="time only the fused input stage step (raw projections, B8 T4096 H16) and its composed "
+                         "counterpart and print their figures")
     ap.add_argument("--varlen-only", action="store_true",
                     help="time only the packed variable-length batch (32768 tokens, H=16) and print its figures")
     ap.add_argument("--long-context-only", action="store_true",
@@ -368,6 +440,9 @@ def main():
         return
     if args.varlen_only:
         print(json.dumps(varlen_bench(steps=args.steps, stored=args.path == "stored")), flush=True)
+        return
+    if args.fused_only:
+        print(json.dumps(fused_bench(steps=args.steps, stored=args.path == "stored")), flush=True)
         return
 
     import torch
@@ -506,6 +581,8 @@ def main():
         out["varlen"] = varlen_bench(stored=stored)
         print("[bench] grouped value heads", file=sys.stderr, flush=True)
         out["grouped"] = grouped_bench(stored=stored)
+        print("[bench] fused input stage", file=sys.stderr, flush=True)
+        out["fused"] = fused_bench(stored=stored)
     if not args.no_cpu:
         print("[bench] cpu oracle baseline", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(d, args.cpu_heads)
