@@ -54,7 +54,11 @@ struct IntraCfg {
   static constexpr int OFF_TA = OFF_K + 64 * LKB * 2;
   static constexpr int OFF_MISC = OFF_TA + 64 * LTA * 4;
   static constexpr int OFF_RQ = OFF_MISC + 16;  // fused stage: inverse norms of the q rows [64]
-  static constexpr int LDS = OFF_RQ + 64 * 4;
+  // A split hi / lo, bf16 [64][LA]: hi over the k tile (dead by then), lo after the rest
+  static constexpr int LA = 64 + 8;
+  static constexpr int OFF_AL = OFF_RQ + 64 * 4;
+  static constexpr int LDS = OFF_AL + 64 * LA * 2;
+  static_assert(64 * LA * 2 <= 64 * LKB * 2, "A hi plane fits the k tile");
   static_assert(LDS <= 80 * 1024, "two workgroups per CU");
 };
 
@@ -86,7 +90,7 @@ template <int DK, int DV, bool FUSED>
 __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
   using C = IntraCfg<DK, DV>;
   constexpr int KS = C::KS, NCB = C::NCB, NVB = C::NVB;
-  constexpr int LG = C::LG, LE = C::LE, LVW = C::LVW, LKB = C::LKB, LTA = C::LTA;
+  constexpr int LG = C::LG, LE = C::LE, LVW = C::LVW, LKB = C::LKB, LTA = C::LTA, LA = C::LA;
 
   extern __shared__ __align__(16) unsigned char smem[];
   float* sG = reinterpret_cast<float*>(smem + C::OFF_X);
@@ -98,6 +102,8 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
   float* sTA = reinterpret_cast<float*>(smem + C::OFF_TA);
   int* unsafe = reinterpret_cast<int*>(smem + C::OFF_MISC);
   float* sRQ = reinterpret_cast<float*>(smem + C::OFF_RQ);
+  __bf16* sAh = reinterpret_cast<__bf16*>(smem + C::OFF_K);  // A hi (after the k tile is dead)
+  __bf16* sAl = reinterpret_cast<__bf16*>(smem + C::OFF_AL);  // A lo
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, r16 = lane & 15;
@@ -497,6 +503,19 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
         st8(sElo + r * LE + 32 * p + 8 * g, ef[sl][p].lo);
       }
     }
+    // A split once into bf16 hi / lo planes (the k tile is dead): the Y and U
+    // products read their A fragments from there (row r, 16 values per thread)
+    {
+      const int r = tid >> 2, c0 = 16 * (tid & 3);
+      float x[8];
+#pragma unroll
+      for (int h8 = 0; h8 < 2; ++h8) {
+        ldf8(sTA + r * LTA + c0 + 8 * h8, x);
+        const Fr f = split8(x);
+        st8(sAh + r * LA + c0 + 8 * h8, f.hi);
+        st8(sAl + r * LA + c0 + 8 * h8, f.lo);
+      }
+    }
     __syncthreads();
   }
 
@@ -516,9 +535,10 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
         f4 acc = f4zero();
 #pragma unroll
         for (int kb = 0; kb <= (i >> 1); ++kb) {
-          float av[8];
-          ldf8(sTA + (16 * i + r16) * LTA + 32 * kb + 8 * g, av);
-          acc = mma3(ef[kb], split8(av), acc);
+          Fr af;
+          af.hi = ld8(sAh + (16 * i + r16) * LA + 32 * kb + 8 * g);
+          af.lo = ld8(sAl + (16 * i + r16) * LA + 32 * kb + 8 * g);
+          acc = mma3(ef[kb], af, acc);
         }
         st4(reinterpret_cast<__bf16*>(Yo + (size_t)(i * KS + (cb >> 1)) * 1024 + 16 * lane + 8 * (cb & 1)), acc[0],
             acc[1], acc[2], acc[3]);
@@ -556,9 +576,10 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
         f4 acc = f4zero();
 #pragma unroll
         for (int kb = 0; kb <= (i >> 1); ++kb) {
-          float av[8];
-          ldf8(sTA + (16 * i + r16) * LTA + 32 * kb + 8 * g, av);
-          acc = mma3(split8(av), zf[kb], acc);
+          Fr af;
+          af.hi = ld8(sAh + (16 * i + r16) * LA + 32 * kb + 8 * g);
+          af.lo = ld8(sAl + (16 * i + r16) * LA + 32 * kb + 8 * g);
+          acc = mma3(af, zf[kb], acc);
         }
         *reinterpret_cast<f4*>(Uo + ((size_t)(vb * 4 + i) * 64 + lane) * 4) = acc;
       }
