@@ -80,13 +80,24 @@ __device__ __forceinline__ float f4at(const float4& v, int u) {
 __device__ __forceinline__ int pair_index(int i, int j) { return (i * (i + 1)) / 2 + j; }
 
 // ---- fused input stage (App. C.1, App. D.1 - D.2) ---------------------------
-// log(1 + e^x) as max(x, 0) + log1p(e^-|x|): no overflow for large x, and the
-// tiny values of very negative x keep their relative accuracy.
-__device__ __forceinline__ float softplus_f(float x) { return fmaxf(x, 0.f) + log1pf(expf(-fabsf(x))); }
-// logistic function, the derivative of softplus
+// Both on the transcendental unit (v_exp_f32 = 2^x, v_log_f32 = log2 x,
+// v_rcp_f32, each within about an ulp), written so that no step loses relative
+// accuracy: u = e^-|x| in (0, 1], and log1p(u) by the identity
+// log1p(u) = u log(w) / (w - 1) with w = fl(1 + u) (exact to a few ulps, u
+// itself when w rounds to 1), so the tiny values of very negative x keep their
+// relative accuracy and large x cannot overflow.
+__device__ __forceinline__ float softplus_f(float x) {
+  constexpr float kL2e = 1.4426950408889634f, kLn2 = 0.6931471805599453f;
+  const float u = __builtin_amdgcn_exp2f(-fabsf(x) * kL2e);
+  const float w = 1.f + u;
+  const float l = w == 1.f ? u : __builtin_amdgcn_logf(w) * kLn2 * u * __builtin_amdgcn_rcpf(w - 1.f);
+  return fmaxf(x, 0.f) + l;
+}
+// logistic function, the derivative of softplus: 1 / (1 + e^-x), e^x / (1 + e^x) for x < 0
 __device__ __forceinline__ float sigmoid_f(float x) {
-  const float e = expf(-fabsf(x)), r = 1.f / (1.f + e);
-  return x >= 0.f ? r : e * r;
+  constexpr float kL2e = 1.4426950408889634f;
+  const float u = __builtin_amdgcn_exp2f(-fabsf(x) * kL2e), r = __builtin_amdgcn_rcpf(1.f + u);
+  return x >= 0.f ? r : u * r;
 }
 // log-decay from the decay projection: g = -A softplus(f + delta), A = exp(a) of the key head
 __device__ __forceinline__ float decay_act(float f, float delta, float A) { return -A * softplus_f(f + delta); }
