@@ -29,7 +29,7 @@ __device__ __forceinline__ float round_as<bf16_t>(float x) {
   return to_f(t);
 }
 
-template <int DK, int DV, typename TIn>
+template <int DK, int DV, typename TIn, bool FUSED>
 __global__ __launch_bounds__(256) void recurrent_kernel(RecurArgs<TIn> a) {
   constexpr int NTHR = 256;
   constexpr int CG = DV / 4;        // column groups of 4
@@ -61,21 +61,27 @@ __global__ __launch_bounds__(256) void recurrent_kernel(RecurArgs<TIn> a) {
     rbase = 0;
   }
   const int HK = H / a.G, hk = h / a.G;  // key side (q, k, g, b) on the H / G key heads
-  const bool fused = a.st.a_log != nullptr;
-  const float Adec = fused ? expf(a.st.a_log[hk]) : 0.f;
+  const float Adec = FUSED ? expf(a.st.a_log[hk]) : 0.f;
   for (int t = t0; t < t1; ++t) {
     const size_t row = (rbase + t) * H + h, rowk = (rbase + t) * HK + hk;
     // thread c < DK holds key channel c of this token (DK <= NTHR)
     const int c = tid;
-    float kv = 0.f, qv = 0.f;
+    float kv = 0.f, qv = 0.f, bv = 0.f, kq = 0.f;
     if (c < DK) {
       kv = to_f(a.k[rowk * DK + c]);
       qv = to_f(a.q[rowk * DK + c]);
+      bv = to_f(a.b[rowk * DK + c]);
       const float gv = a.g[rowk * DK + c];
-      sAl[c] = expf(fused ? decay_act(gv, a.st.delta[(size_t)hk * DK + c], Adec) : gv);
+      sAl[c] = expf(FUSED ? decay_act(gv, a.st.delta[(size_t)hk * DK + c], Adec) : gv);
+      if constexpr (!FUSED) {
+        sK[c] = kv;
+        sQ[c] = qv;
+        sE[c] = bv * kv;
+        kq = kv * qv;
+      }
     }
     for (int v = tid; v < DV; v += NTHR) sZ[v] = to_f(a.w[row * DV + v]) * to_f(a.v[row * DV + v]);
-    if (fused) {
+    if constexpr (FUSED) {
       // fused stage: sums of squares over the row, then y = x (sum x^2 + eps)^(-1/2) in the operand dtype
       float kk = kv * kv, qq = qv * qv;
 #pragma unroll
@@ -96,13 +102,12 @@ __global__ __launch_bounds__(256) void recurrent_kernel(RecurArgs<TIn> a) {
       }
       kv = round_as<TIn>(kv * inv_norm(sk, a.st.eps));
       qv = round_as<TIn>(qv * inv_norm(sq, a.st.eps));
-    }
-    float kq = 0.f;
-    if (c < DK) {
-      sK[c] = kv;
-      sQ[c] = qv;
-      sE[c] = to_f(a.b[rowk * DK + c]) * kv;
-      kq = kv * qv;
+      if (c < DK) {
+        sK[c] = kv;
+        sQ[c] = qv;
+        sE[c] = bv * kv;
+        kq = kv * qv;
+      }
     }
 #pragma unroll
     for (int m = 32; m >= 1; m >>= 1) kq += __shfl_xor(kq, m);
@@ -150,7 +155,10 @@ __global__ __launch_bounds__(256) void recurrent_kernel(RecurArgs<TIn> a) {
 
 template <int DK, int DV, typename TIn>
 hipError_t launch_recurrent(const RecurArgs<TIn>& a, int B, hipStream_t st) {
-  hipLaunchKernelGGL((recurrent_kernel<DK, DV, TIn>), dim3(B * a.H), dim3(256), 0, st, a);
+  if (a.st.a_log != nullptr)
+    hipLaunchKernelGGL((recurrent_kernel<DK, DV, TIn, true>), dim3(B * a.H), dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL((recurrent_kernel<DK, DV, TIn, false>), dim3(B * a.H), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

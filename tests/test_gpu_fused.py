@@ -164,3 +164,22 @@ def test_fused_full_size_sampled_heads():
         part = {n: got[n][b:b + 1, :, h:h + 1] for n in ("o", "dq", "dk", "dv", "df", "db", "dw")}
         part["S_T"] = got["S_T"][b:b + 1, h:h + 1]
         _check(part, ref, TOL["bf16"], names=tuple(part))
+
+
+def test_fused_decay_activation_over_its_domain():
+    """fp32 decoding with f + delta spread over [-40, 40]: both tails of softplus
+    (e^x for very negative x, x for large x) and the middle, against the fp64
+    activation; the state after 24 tokens carries every token's decay."""
+    import paper_2605_22791_amd as g2
+    d = make_fused(1, 24, 2, 64, 64, seed=316, dtype="fp32", s0_std=0.5)
+    rng = np.random.default_rng(17)
+    d["f"] = (rng.uniform(-40.0, 40.0, d["f"].shape) - d["delta"][None, None]).astype(np.float32)
+    d["a"] = np.array([-3.0, 0.5], dtype=np.float32)  # small magnitudes keep the large-x tokens' decay finite-sized
+    _case("fused recurrent fp32, f + delta over [-40, 40]")
+    x = _dev(d)
+    S = x["S0"].clone()
+    o = g2.gdr2_fused_recurrent(*[x[n] for n in ARGS], S, scale=d["scale"], eps=d["eps"])
+    ref = _oracle(d, backward=False)
+    e_o, e_s = rel_l2(host(o), ref["o"]), rel_l2(host(S), ref["S_T"])
+    print("o", e_o, "S", e_s)
+    assert e_o < 1e-5 and e_s < 1e-5
