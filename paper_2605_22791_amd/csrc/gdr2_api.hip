@@ -344,8 +344,6 @@ hipError_t stage_bwd(const gdr2_problem* p, const Geo& G, void* ws, const void* 
   na.x[1] = static_cast<const bf16_t*>(k);
   na.rinv[0] = G.st.RQ;
   na.rinv[1] = G.st.RK;
-  na.DY[0] = static_cast<const bf16_t*>(dq);
-  na.DY[1] = static_cast<const bf16_t*>(dk);
   na.P[0] = at<float>(ws, L.pQ);
   na.P[1] = at<float>(ws, L.pK);
   na.dx[0] = static_cast<bf16_t*>(dq);

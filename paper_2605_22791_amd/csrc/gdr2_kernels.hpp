@@ -382,12 +382,11 @@ hipError_t launch_group_reduce(const float* P, TOut* out, size_t rows, int Hk, i
 // Normalisation VJP of the fused stage (App. D.2): for rows r < rows, key
 // heads hk < Hk, dx = rinv (dy - y <y, dy>), y = rinv x, with x the raw q or
 // k (bf16), rinv its stored inverse norm and dy the gradient of the normalised
-// tensor: the sum of the G fp32 partials P[r, hk * G + j, :], or bf16 DY when
-// P is null (dx may alias it).  Two tensors (q, k) per launch.
+// tensor, the sum of the G fp32 partials P[r, hk * G + j, :] (G = 1: the fp32
+// gradient itself).  Two tensors (q, k) per launch.
 struct NormVjpArgs {
   const bf16_t* x[2];
   const float* rinv[2];
-  const bf16_t* DY[2];
   const float* P[2];
   bf16_t* dx[2];
   size_t rows;

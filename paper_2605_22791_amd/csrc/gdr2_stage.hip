@@ -31,17 +31,13 @@ __global__ __launch_bounds__(256) void norm_vjp_kernel(NormVjpArgs a) {
     const float ri = RI[R];
     float x[8], dy[8];
     unpack8(ldg16(X + R * DK + c0), x);
-    if (a.P[z] == nullptr) {
-      unpack8(ldg16(a.DY[z] + R * DK + c0), dy);
-    } else {
-      const float* p = a.P[z] + (size_t)a.G * R * DK + c0;
-      ldf8(p, dy);
-      for (int j = 1; j < a.G; ++j) {
-        float t[8];
-        ldf8(p + (size_t)j * DK, t);
+    const float* p = a.P[z] + (size_t)a.G * R * DK + c0;
+    ldf8(p, dy);
+    for (int j = 1; j < a.G; ++j) {
+      float t[8];
+      ldf8(p + (size_t)j * DK, t);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) dy[e] += t[e];
-      }
+      for (int e = 0; e < 8; ++e) dy[e] += t[e];
     }
     float dot = 0.f;
 #pragma unroll
