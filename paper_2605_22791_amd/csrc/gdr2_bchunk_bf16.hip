@@ -102,6 +102,46 @@ __device__ __forceinline__ Fr split_f44(const float4& x, const float4& y) {
   const float v[8] = {x.x, x.y, x.z, x.w, y.x, y.y, y.z, y.w};
   return split8(v);
 }
+// 4 x 4 transpose inside each quad of lanes (lanes 4m + j, j = 0..3): on entry
+// lane j holds v[u] = M[j][u], on exit v[k] = M[k][j].  Two stages of 2 x 2
+// block swaps with DPP quad permutations (xor 1, then xor 2).
+__device__ __forceinline__ float dpp_quad(float x, int ctrl_xor) {
+  const int v = __float_as_int(x);
+  return __int_as_float(ctrl_xor == 1 ? __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false)
+                                      : __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false));
+}
+__device__ __forceinline__ void quad_transpose(float (&v)[4], int j) {
+  {
+    const bool odd = (j & 1) != 0;
+    const float a = dpp_quad(odd ? v[0] : v[1], 1), b = dpp_quad(odd ? v[2] : v[3], 1);
+    if (odd) {
+      v[0] = a;
+      v[2] = b;
+    } else {
+      v[1] = a;
+      v[3] = b;
+    }
+  }
+  {
+    const bool hi = (j & 2) != 0;
+    const float a = dpp_quad(hi ? v[0] : v[2], 2), b = dpp_quad(hi ? v[1] : v[3], 2);
+    if (hi) {
+      v[0] = a;
+      v[1] = b;
+    } else {
+      v[2] = a;
+      v[3] = b;
+    }
+  }
+}
+// four consecutive outputs of one row: 8-byte bf16 or 16-byte fp32 store
+__device__ __forceinline__ void store_row4(__bf16* p, const float (&v)[4]) {
+  *reinterpret_cast<bf4*>(p) = bf4{(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
+}
+__device__ __forceinline__ void store_row4(float* p, const float (&v)[4]) {
+  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+}
+
 // element j (0..3) of four per-block values, j lane-dependent
 __device__ __forceinline__ float pick4(const float (&x)[4], int j) {
   return j == 0 ? x[0] : (j == 1 ? x[1] : (j == 2 ? x[2] : x[3]));
@@ -561,6 +601,7 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     if constexpr (FUSED) xs4 = *reinterpret_cast<const float4*>(sXS + r16 * LGT + rb);
     const float gam0 = ex2(G2fi), tb = ex2(G2l[3] - G2li);
     float dgl[4], tailp = 0.f;
+    float oq[4], ok[4], ob[4];  // dq, dk, db of rows rb + u, key c
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const float lf = elv[u], rf = erv[u], gam = lf * gam0, tl = rf * tb;
@@ -592,22 +633,31 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
           }
         }
       }
-      const int o = (rb + u) * kso + c;
-      if (rb + u < len) {
-        if (partq) {
-          pQp[o] = dq;
-          pKp[o] = dEg * bv + dKg;
-        } else {
-          dQp[o] = (__bf16)dq;
-          dKp[o] = (__bf16)(dEg * bv + dKg);
-        }
-        if (partb)
-          pBp[o] = dEg * kv;
-        else
-          dBp[o] = (__bf16)(dEg * kv);
-      }
+      oq[u] = dq;
+      ok[u] = dEg * bv + dKg;
+      ob[u] = dEg * kv;
       dgl[u] = dq * qv - dKg * kv + dEg * bv * kv;
       tailp += x3[u] * kv * tl;
+    }
+    // outputs leave as row pieces: after a transpose inside each quad of lanes,
+    // lane (g, 4 m + j) holds row 16 i + 4 g + j, keys 16 cb + 4 m .. + 3
+    const int jq = r16 & 3, orow = 16 * i + 4 * g + jq;
+    const int oo = orow * kso + 16 * cb + 4 * (r16 >> 2);
+    quad_transpose(oq, jq);
+    quad_transpose(ok, jq);
+    quad_transpose(ob, jq);
+    if (orow < len) {
+      if (partq) {
+        store_row4(pQp + oo, oq);
+        store_row4(pKp + oo, ok);
+      } else {
+        store_row4(dQp + oo, oq);
+        store_row4(dKp + oo, ok);
+      }
+      if (partb)
+        store_row4(pBp + oo, ob);
+      else
+        store_row4(dBp + oo, ob);
     }
     // reverse cumulative sum of dG: within the lane, over the lane groups, then blocks
     const float s3 = dgl[3], s2 = s3 + dgl[2], s1 = s2 + dgl[1], s0 = s1 + dgl[0];
@@ -638,24 +688,24 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       // df = dg * dg/df, dg/df = -exp(a) sigmoid(f + delta); partial sums for ddelta and da
       const float dgv[4] = {s0 + off, s1 + off, s2 + off, s3 + off};
       const float xv[4] = {xs4.x, xs4.y, xs4.z, xs4.w};
-      float pdc = 0.f;
+      float pdc = 0.f, dfv[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
+        dfv[u] = dgv[u] * (-Adec * sigmoid_f(xv[u]));
         if (rb + u < len) {
-          const float dfv = dgv[u] * (-Adec * sigmoid_f(xv[u]));
-          dGp[(rb + u) * kso + c] = dfv;
-          pdc += dfv;
+          pdc += dfv[u];
           pa_acc += dgv[u] * (-Adec * softplus_f(xv[u]));
         }
       }
+      quad_transpose(dfv, jq);
+      if (orow < len) store_row4(dGp + oo, dfv);
       pdc += __shfl_xor(pdc, 16);
       pdc += __shfl_xor(pdc, 32);
       if (g == 0) a.PD[pslot * DK + 16 * cb + r16] = pdc;
     } else {
-      if (rb + 0 < len) dGp[(rb + 0) * kso + c] = s0 + off;
-      if (rb + 1 < len) dGp[(rb + 1) * kso + c] = s1 + off;
-      if (rb + 2 < len) dGp[(rb + 2) * kso + c] = s2 + off;
-      if (rb + 3 < len) dGp[(rb + 3) * kso + c] = s3 + off;
+      float dgv[4] = {s0 + off, s1 + off, s2 + off, s3 + off};
+      quad_transpose(dgv, jq);
+      if (orow < len) store_row4(dGp + oo, dgv);
     }
     if (cb + 1 < NCB) GDR2_STAGE(par ^ 1, cb + 1)
     __syncthreads();
