@@ -122,12 +122,14 @@ Layout layout(const gdr2_problem* p, bool bwd, int nseq = 0, int G = 1, bool fus
       off += round_up(bytes);
       return at;
     };
-    L.bY = takeb(NC * WsBf16::y(p->Dk));
-    L.bQ = takeb(NC * WsBf16::qg(p->Dk));
-    L.bA = takeb(NC * WsBf16::aqk());
-    L.bK = takeb(NC * WsBf16::ktt(p->Dk));
+    // the key-side tiles (all but U) once per key-head chunk: shared by the G value heads
+    const size_t NCk = NC / G;
+    L.bY = takeb(NCk * WsBf16::y(p->Dk));
+    L.bQ = takeb(NCk * WsBf16::qg(p->Dk));
+    L.bA = takeb(NCk * WsBf16::aqk());
+    L.bK = takeb(NCk * WsBf16::ktt(p->Dk));
     L.bU = takeb(NC * WsBf16::u(p->Dv));
-    L.bG = takeb(NC * WsBf16::gc(p->Dk));
+    L.bG = takeb(NCk * WsBf16::gc(p->Dk));
   } else {
     L.Y = take(NC * CH * Dk);
     L.U = take(NC * CH * Dv);
@@ -145,7 +147,7 @@ Layout layout(const gdr2_problem* p, bool bwd, int nseq = 0, int G = 1, bool fus
       L.bDR = off;
       off += round_up(NC * WsBf16::dr(p->Dv));
       L.bAm = off;
-      off += round_up(NC * WsBf16::am());
+      off += round_up(NC / G * WsBf16::am());  // A per key-head chunk
     } else {
       L.DR = take(NC * CH * Dv);
       L.DAqk = take(NC * CH * CH);
@@ -464,6 +466,7 @@ struct FwdRun {
                   save ? at<float>(ws, L.Hs) : nullptr, save ? at<float>(ws, L.Rs) : nullptr,
                   G.nscan, p->T, p->H, NT, p->scale};
       sa.vl = G.vl;
+      sa.G = G.G;
       return timed(GDR2_K_FWD_STATE, st, [&] {
         return scan_fwd_bf16<DK, DV>(sa, L, ws, [&](const ScanArgs& x) {
           return save ? launch_scan_bf16<DK, DV, true, true>(x, st) : launch_scan_bf16<DK, DV, true, false>(x, st);
@@ -519,6 +522,7 @@ struct BwdRun {
         ScanArgs sa{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.U, ia.GC, S0, nullptr, nullptr, at<float>(ws, L.Hs),
                     at<float>(ws, L.Rs), G.nscan, p->T, p->H, NT, p->scale};
         sa.vl = G.vl;
+        sa.G = G.G;
         e = timed(GDR2_K_BWD_RECOMPUTE_STATE, st, [&] {
           return scan_fwd_bf16<DK, DV>(sa, L, ws, [&](const ScanArgs& x) {
             return launch_scan_bf16<DK, DV, false, true>(x, st);
@@ -529,6 +533,7 @@ struct BwdRun {
       BScanArgs ba{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.GC, static_cast<const bf16_t*>(dout), dST, dS0,
                    at<float>(ws, L.DH), at<unsigned char>(ws, L.bDR), G.nscan, p->T, p->H, NT, p->scale};
       ba.vl = G.vl;
+      ba.G = G.G;
       e = timed(GDR2_K_BWD_STATE, st, [&] { return scan_bwd_bf16<DK, DV>(ba, L, ws, st); });
       if (e != hipSuccess) return e;
       // the WY VJP and the intra-chunk VJP in one chunk-parallel kernel

@@ -262,7 +262,7 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   u4v ldv[NLD];
   {
     const unsigned char* DRc = a.DR + ch * WsBf16::dr(DV);
-    const unsigned char* Amc = a.Am + ch * WsBf16::am();
+    const unsigned char* Amc = a.Am + key_ch(a.vl, ch, H, a.G, a.NT) * WsBf16::am();  // A: per key head
 #pragma unroll
     for (int m = 0; m < NLD; ++m) {
       const int off = 16 * (tid + C::NTHR * m);

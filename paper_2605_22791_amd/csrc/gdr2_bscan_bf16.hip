@@ -75,10 +75,14 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
   // independent scans: (sequence, segment) pairs, vs = seq * nseg + seg
   const int nseg = a.nseg, nvirt = a.B * H * nseg;
   int vs, slice;
-  if (NS > 1 && (nvirt & 7) == 0) {
-    const int xcd = blockIdx.x & 7, j = blockIdx.x >> 3;
-    vs = (j / NS) * 8 + xcd;
-    slice = j % NS;
+  if ((NS > 1 || a.G > 1) && ((nvirt / a.G) & 7) == 0) {
+    // the NS value slices of the G value heads that read one key head's tiles
+    // run on one XCD (consecutive blocks of an XCD), so they share its L2
+    const int xcd = blockIdx.x & 7, j = blockIdx.x >> 3, per = a.G * NS;
+    const int unit = (j / per) * 8 + xcd, rem = j % per;
+    const int HKs = H / a.G, qk = unit / nseg;
+    vs = ((qk / HKs) * H + (qk % HKs) * a.G + rem / NS) * nseg + unit % nseg;
+    slice = rem % NS;
   } else {
     vs = blockIdx.x / NS;
     slice = blockIdx.x % NS;
@@ -100,10 +104,11 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
   // ---- staging: operand blocks, the dO slice and gamma_C of one chunk
   u4v stg[NSTG], sto;
   float gcur[4], gnext[4];
-  const size_t chs = rng.chs;
+  const size_t chs = rng.chs;                        // value-head chunks: dh, dR
+  const size_t chk = key_ch(a.vl, chs, H, a.G, NT);  // key-head chunks: Y, Q_g, A_qk, K_tail, gamma_C
 #define GDR2_LOAD_CHUNK(N_)                                                                               \
   {                                                                                                    \
-    const size_t chx = chs + (N_);                                                                     \
+    const size_t chx = chk + (N_);                                                                     \
     _Pragma("unroll") for (int m = 0; m < NSTG; ++m) {                                                 \
       const unsigned char* src;                                                                        \
       if (m < E_Y)                                                                                     \

@@ -1,5 +1,7 @@
 // Intra-chunk kernel of the bf16 path (gfx950): one 4-wave workgroup per
-// chunk-head, two workgroups per CU.  Per chunk of C = 64 tokens it forms
+// key-head chunk, two workgroups per CU (grouped value heads share everything
+// but U, which is formed for each value head of the group).  Per chunk of
+// C = 64 tokens it forms
 //
 //   G2 = log2(e) * cumsum(g)                          eq. eq_gdn2_gamma (fp32)
 //   Q_g = q * gamma,  Ktail^T = (k * gamma_C / gamma)^T    eqs. eq_gdn2_gate_matrices,
@@ -107,10 +109,12 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, r16 = lane & 15;
+  // one workgroup per key-head chunk: the key-side tiles (everything but U) are
+  // shared by the G value heads of the group; U is formed for each of them
+  const int H = a.H, HK = H / a.G, hk = blockIdx.y;
   ChunkPos cp;
-  if (!chunk_pos(a.vl, blockIdx.x, blockIdx.y, blockIdx.z, a.T, a.H, a.NT, cp)) return;
-  const int h = blockIdx.y, H = a.H;
-  const size_t ch = cp.ch;
+  if (!chunk_pos(a.vl, blockIdx.x, hk, blockIdx.z, a.T, HK, a.NT, cp)) return;
+  const size_t ch = cp.ch;  // key-head chunk
   // Rows in use.  Every load below reads an in-range row (rows past a partial
   // chunk's end re-read its last row); g, k and v of those rows are then taken
   // as zero, which makes their T / A_qk entries, Ebar, Z, Ktail and decay
@@ -125,10 +129,11 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
   const __bf16* Bg = reinterpret_cast<const __bf16*>(a.b);
   const __bf16* Wg = reinterpret_cast<const __bf16*>(a.w);
   const size_t row0 = cp.row0;
-  // key-side tensors (q, k, g, b) live on the H / G key heads: value head h reads key head h / G
-  const int HK = H / a.G, hk = h / a.G;
+  // key-side tensors (q, k, g, b) on the H / G key heads; v, w of value head hv
   auto kofs = [&](int r) -> size_t { return (row0 + min(r, len - 1)) * ((size_t)HK * DK) + (size_t)hk * DK; };
-  auto vofs = [&](int r) -> size_t { return (row0 + min(r, len - 1)) * ((size_t)H * DV) + (size_t)h * DV; };
+  auto vofs = [&](int hv, int r) -> size_t {
+    return (row0 + min(r, len - 1)) * ((size_t)H * DV) + (size_t)hv * DV;
+  };
 
   // ---- loads: g in scan layout (NG rows of 4 channels per thread), k
   constexpr int GCG = DK / 4, GSEG = 256 / GCG, NG = 64 / GSEG;
@@ -144,7 +149,7 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
     dlt = *reinterpret_cast<const float4*>(a.st.delta + (size_t)hk * DK + 4 * gcg);
     Adec = expf(a.st.a_log[hk]);
   }
-  const bool wr_norm = FUSED && (h % a.G) == 0;  // one value head of the group writes the inverse norms
+  constexpr bool wr_norm = FUSED;
   u4v kst[NKC];
 #pragma unroll
   for (int m = 0; m < NKC; ++m) {
@@ -415,14 +420,15 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
 #pragma unroll
     for (int rr = 0; rr < 16; ++rr) sTA[(16 * blk + rr) * LTA + 16 * blk + cc] = x[rr];
   }
-  // v, w for U = A Z, loaded while the solve runs
+  // v, w of the group's first value head for U = A Z, loaded while the solve runs
   constexpr int NVC = DV / 32;  // 16-byte chunks of v (and of w) per thread
+  const int h0 = hk * a.G;
   u4v vst[NVC], wst[NVC];
 #pragma unroll
   for (int m = 0; m < NVC; ++m) {
     const int e = tid + 256 * m, r = e / (DV / 8), c8 = (e % (DV / 8)) * 8;
-    vst[m] = ldg16(Vg + vofs(r) + c8);
-    wst[m] = ldg16(Wg + vofs(r) + c8);
+    vst[m] = ldg16(Vg + vofs(h0, r) + c8);
+    wst[m] = ldg16(Wg + vofs(h0, r) + c8);
   }
   __syncthreads();
 #pragma unroll 1
@@ -545,43 +551,53 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
       }
     }
   }
-  __syncthreads();  // Ebar is dead; its region takes v and w
-
-  // ---- U = A (W * V): fp32 accumulator tiles
-#pragma unroll
-  for (int m = 0; m < NVC; ++m) {
-    const int e = tid + 256 * m, r = e / (DV / 8), c8 = (e % (DV / 8)) * 8;
-    sts16(sV + r * LVW + c8, r < len ? vst[m] : u4v{0u, 0u, 0u, 0u});
-    sts16(sW + r * LVW + c8, wst[m]);
-  }
-  __syncthreads();
-  {
-    float* Uo = a.U + ch * (WsBf16::u(DV) / 4);
-    constexpr int VPW = NVB / 4;  // value blocks per wave
+  // ---- U = A (W * V) for every value head of the group: fp32 accumulator tiles
 #pragma unroll 1
-    for (int t = 0; t < VPW; ++t) {
-      const int vb = wave * VPW + t;
-      Fr zf[2];
+  for (int j = 0; j < a.G; ++j) {
+    if (j > 0) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        float vf[8], wf[8], z[8];
-        unpack8(ld_tr8(sV, LVW, 32 * kb, 16 * vb, lane), vf);
-        unpack8(ld_tr8(sW, LVW, 32 * kb, 16 * vb, lane), wf);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) z[e] = vf[e] * wf[e];
-        zf[kb] = split8(z);
+      for (int m = 0; m < NVC; ++m) {
+        const int e = tid + 256 * m, r = e / (DV / 8), c8 = (e % (DV / 8)) * 8;
+        vst[m] = ldg16(Vg + vofs(h0 + j, r) + c8);
+        wst[m] = ldg16(Wg + vofs(h0 + j, r) + c8);
       }
+    }
+    __syncthreads();  // Ebar (then the previous value head's v, w) is dead; the region takes v and w
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        f4 acc = f4zero();
+    for (int m = 0; m < NVC; ++m) {
+      const int e = tid + 256 * m, r = e / (DV / 8), c8 = (e % (DV / 8)) * 8;
+      sts16(sV + r * LVW + c8, r < len ? vst[m] : u4v{0u, 0u, 0u, 0u});
+      sts16(sW + r * LVW + c8, wst[m]);
+    }
+    __syncthreads();
+    {
+      float* Uo = a.U + value_ch(a.vl, blockIdx.x, h0 + j, blockIdx.z, H, a.NT) * (WsBf16::u(DV) / 4);
+      constexpr int VPW = NVB / 4;  // value blocks per wave
+#pragma unroll 1
+      for (int t = 0; t < VPW; ++t) {
+        const int vb = wave * VPW + t;
+        Fr zf[2];
 #pragma unroll
-        for (int kb = 0; kb <= (i >> 1); ++kb) {
-          Fr af;
-          af.hi = ld8(sAh + (16 * i + r16) * LA + 32 * kb + 8 * g);
-          af.lo = ld8(sAl + (16 * i + r16) * LA + 32 * kb + 8 * g);
-          acc = mma3(af, zf[kb], acc);
+        for (int kb = 0; kb < 2; ++kb) {
+          float vf[8], wf[8], z[8];
+          unpack8(ld_tr8(sV, LVW, 32 * kb, 16 * vb, lane), vf);
+          unpack8(ld_tr8(sW, LVW, 32 * kb, 16 * vb, lane), wf);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) z[e] = vf[e] * wf[e];
+          zf[kb] = split8(z);
         }
-        *reinterpret_cast<f4*>(Uo + ((size_t)(vb * 4 + i) * 64 + lane) * 4) = acc;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          f4 acc = f4zero();
+#pragma unroll
+          for (int kb = 0; kb <= (i >> 1); ++kb) {
+            Fr af;
+            af.hi = ld8(sAh + (16 * i + r16) * LA + 32 * kb + 8 * g);
+            af.lo = ld8(sAl + (16 * i + r16) * LA + 32 * kb + 8 * g);
+            acc = mma3(af, zf[kb], acc);
+          }
+          *reinterpret_cast<f4*>(Uo + ((size_t)(vb * 4 + i) * 64 + lane) * 4) = acc;
+        }
       }
     }
   }
@@ -593,7 +609,7 @@ hipError_t launch_intra_bf16_t(const IntraBf16Args& a, hipStream_t st) {
   const void* fn = reinterpret_cast<const void*>(&intra_bf16_kernel<DK, DV, FUSED>);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
   if (e != hipSuccess) return e;
-  dim3 grid(a.vl.ct0 ? a.vl.ncmax : a.NT, a.H, a.vl.ct0 ? 1 : a.B);
+  dim3 grid(a.vl.ct0 ? a.vl.ncmax : a.NT, a.H / a.G, a.vl.ct0 ? 1 : a.B);
   hipLaunchKernelGGL((intra_bf16_kernel<DK, DV, FUSED>), grid, dim3(C::NTHR), C::LDS, st, a);
   return hipGetLastError();
 }

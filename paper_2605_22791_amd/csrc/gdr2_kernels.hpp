@@ -52,6 +52,23 @@ __device__ __forceinline__ bool chunk_pos(const Varlen& vl, int x, int h, int bb
   return true;
 }
 
+// Chunk index of chunk x of value head hv: the per-value-head workspace tiles
+// (U, the states, R, dR) of grouped problems whose key-side tiles are indexed
+// by the key head (chunk_pos with the key heads).
+__device__ __forceinline__ size_t value_ch(const Varlen& vl, int x, int hv, int bb, int H, int NT) {
+  return vl.ct0 != nullptr ? (size_t)hv * vl.ncmax + x : ((size_t)bb * H + hv) * NT + x;
+}
+// Key-head chunk of value-head chunk ch = value_ch(x, hv, ...) (G value heads per key head).
+__device__ __forceinline__ size_t key_ch(const Varlen& vl, size_t ch, int H, int G, int NT) {
+  if (G == 1) return ch;
+  if (vl.ct0 != nullptr) {
+    const size_t hv = ch / vl.ncmax;
+    return (hv / G) * vl.ncmax + ch % vl.ncmax;
+  }
+  const size_t bh = ch / NT, bb = bh / H, hv = bh % H;
+  return (bb * (H / G) + hv / G) * NT + ch % NT;
+}
+
 // Chunks of the scanned pair q = s * H + h (sequence s, head h): ch = chs + c
 // for c in [c0, c1).
 struct ScanRange {
@@ -242,7 +259,10 @@ struct IntraBf16Args {
   unsigned char* Am;  // nullable: A for the backward
   int B, T, H, NT;
   Varlen vl{};
-  int G = 1;  // grouped value heads: H value heads share H / G key heads (q, k, g, b)
+  // grouped value heads: H value heads share H / G key heads (q, k, g, b); the
+  // kernel runs per key-head chunk and writes Y, Q_g, A_qk, K_tail, gamma_C and A
+  // once there (chunk_pos over the key heads) and U for each value head (value_ch)
+  int G = 1;
   Stage st{};
 };
 
@@ -272,6 +292,7 @@ struct ScanArgs {
   float* STseg = nullptr;        // nullable: end state of every segment (B*H*nseg, Dk, DV)
   int flags = 0;                 // ScanFlags
   Varlen vl{};
+  int G = 1;                     // value heads per key head: Y, Q_g, A_qk, K_tail, gamma_C per key head
 };
 
 struct BScanArgs {
@@ -292,6 +313,7 @@ struct BScanArgs {
   float* dSseg_out = nullptr;      // nullable: gradient at the start of every segment
   int flags = 0;                   // ScanFlags (kScanNoInput: dO = 0)
   Varlen vl{};
+  int G = 1;                       // as in ScanArgs
 };
 
 // Chaining of segment maps: X <- M_k X + N_k over the segments of each sequence

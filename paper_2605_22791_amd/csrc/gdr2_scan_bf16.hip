@@ -82,10 +82,14 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
   // independent scans: (sequence, segment) pairs, vs = seq * nseg + seg
   const int nseg = a.nseg, nvirt = a.B * H * nseg;
   int vs, slice;
-  if (NS > 1 && (nvirt & 7) == 0) {
-    const int xcd = blockIdx.x & 7, j = blockIdx.x >> 3;
-    vs = (j / NS) * 8 + xcd;
-    slice = j % NS;
+  if ((NS > 1 || a.G > 1) && ((nvirt / a.G) & 7) == 0) {
+    // the NS value slices of the G value heads that read one key head's tiles
+    // run on one XCD (consecutive blocks of an XCD), so they share its L2
+    const int xcd = blockIdx.x & 7, j = blockIdx.x >> 3, per = a.G * NS;
+    const int unit = (j / per) * 8 + xcd, rem = j % per;
+    const int HKs = H / a.G, qk = unit / nseg;
+    vs = ((qk / HKs) * H + (qk % HKs) * a.G + rem / NS) * nseg + unit % nseg;
+    slice = rem % NS;
   } else {
     vs = blockIdx.x / NS;
     slice = blockIdx.x % NS;
@@ -115,7 +119,8 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
   u4v stg[NSTG];
   f4 ucur[NVB / 2], unext[NVB / 2];
   float gcur[4], gnext[4];
-  const size_t chs = rng.chs;
+  const size_t chs = rng.chs;                        // value-head chunks: U, h, R
+  const size_t chk = key_ch(a.vl, chs, H, a.G, NT);  // key-head chunks: Y, Q_g, A_qk, K_tail, gamma_C
 #define GDR2_LOAD_OPS(CHX)                                                                                   \
   _Pragma("unroll") for (int m = 0; m < NSTG; ++m) {                                                     \
     const unsigned char* src;                                                                            \
@@ -132,7 +137,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
 #define GDR2_STORE_OPS()                                                                                     \
   _Pragma("unroll") for (int m = 0; m < NSTG; ++m) sts16(sOp + m * SLICE + 16 * tid, stg[m]);
   // U tiles (value blocks vbO.., row block iO) and gamma_C rows of the state tiles
-#define GDR2_LOAD_UG(CHX, UARR, GARR)                                                                        \
+#define GDR2_LOAD_UG(CHX, CHKX, UARR, GARR)                                                                  \
   _Pragma("unroll") for (int t = 0; t < NVB / 2; ++t) {                                                  \
     const int vb_ = v0 / 16 + vbO + t;                                                                   \
     UARR[t] = no_input ? f4zero()                                                                        \
@@ -140,7 +145,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
                                                       ((size_t)(vb_ * 4 + iO) * 64 + lane) * 4);         \
   }                                                                                                      \
   _Pragma("unroll") for (int u2 = 0; u2 < 4; ++u2) GARR[u2] =                                            \
-      a.GC[(CHX) * (WsBf16::gc(DK) / 4) + 16 * cs + 4 * g + u2];
+      a.GC[(CHKX) * (WsBf16::gc(DK) / 4) + 16 * cs + 4 * g + u2];
 
   // ---- state: identity columns, the given segment start, S0 (first segment) or zero
   const bool eye = (a.flags & kScanEye) != 0;  // (DV == DK)
@@ -166,8 +171,8 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
              sreg[t]);
   }
   if (n0 < n1) {
-    GDR2_LOAD_OPS(chs + n0)
-    GDR2_LOAD_UG(chs + n0, ucur, gcur)
+    GDR2_LOAD_OPS(chk + n0)
+    GDR2_LOAD_UG(chs + n0, chk + n0, ucur, gcur)
     GDR2_STORE_OPS()
   }
   __syncthreads();
@@ -202,8 +207,8 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
     // would be drained by the wait that frees the registers of the previous
     // chunk's stores (one vmcnt counts loads and stores alike)
     if (n + 1 < n1) {
-      GDR2_LOAD_OPS(ch + 1)
-      GDR2_LOAD_UG(ch + 1, unext, gnext)
+      GDR2_LOAD_OPS(chk + n + 1)
+      GDR2_LOAD_UG(ch + 1, chk + n + 1, unext, gnext)
     }
     __syncthreads();
 

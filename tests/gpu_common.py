@@ -77,14 +77,17 @@ def bf16_bits_to_f32(u16):
     return (u16.astype(np.uint32) << 16).view(np.float32)
 
 
-def ws_layout_bf16(B, T, H, Dk, Dv, bwd=False, nseq=0):
+def ws_layout_bf16(B, T, H, Dk, Dv, bwd=False, nseq=0, G=1):
     """Byte offsets / per-chunk-head sizes of the bf16 workspace regions
     (mirrors WsBf16 in the library: fragment-ordered tiles; the backward adds
     fp32 chunk states Hs, R and dH, then dR and A as fragment blocks).  A
     packed call (nseq > 0) has H * (T // 64 + nseq) chunk-heads and appends
-    its chunk table (int32: nseq + 1 offsets, two slot arrays, the scan order)."""
+    its chunk table (int32: nseq + 1 offsets, two slot arrays, the scan order).
+    H counts value heads; with G value heads per key head the key-side tiles
+    (all but U and the backward's states, R, dH, dR) exist once per key head."""
     NC = H * (T // CH + nseq) if nseq > 0 else B * H * (-(-T // CH))
     gc = (Dk * 4 + 255) // 256 * 256
+    key = {"Y", "Qg", "Aqk", "KtT", "GC", "Am"}
     sizes = [("Y", 4 * (Dk // 32) * 1024), ("Qg", 4 * (Dk // 32) * 2048), ("Aqk", 8 * 2048),
              ("KtT", (Dk // 16) * 2 * 2048), ("U", (Dv // 16) * 4 * 1024), ("GC", gc)]
     if bwd:
@@ -93,7 +96,7 @@ def ws_layout_bf16(B, T, H, Dk, Dv, bwd=False, nseq=0):
     off, out = 0, {}
     for n, per in sizes:
         out[n] = (off, per)
-        off += (NC * per + 255) // 256 * 256
+        off += ((NC // G if n in key else NC) * per + 255) // 256 * 256
     if nseq > 0:
         slots = T // CH + nseq
         for n, cnt in (("coff", nseq + 1), ("ct0", slots), ("clen", slots), ("sorder", nseq)):

@@ -309,9 +309,10 @@ def test_varlen_workspace_size():
 
 
 def test_grouped_value_heads_validation_and_workspace():
-    """Hv must be a multiple of H (0 means Hv = H).  A grouped problem runs per
-    value head (workspace of the Hv-head problem) and its backward adds four fp32
-    (B, T, Hv, Dk) regions for the per-value-head key-side gradients."""
+    """Hv must be a multiple of H (0 means Hv = H).  A grouped problem keeps the
+    key-side tiles once per key head and U (and the backward's per-value-head
+    regions) per value head; its backward adds four fp32 (B, T, Hv, Dk) regions
+    for the per-value-head key-side gradients."""
     from tests.gpu_common import ws_layout_bf16, seg_buffer_bytes
     assert _fwd(_prob(H=4, Hv=6)) == g2.GDR2_EINVAL
     assert _bwd(_prob(H=4, Hv=-4)) == g2.GDR2_EINVAL
@@ -321,9 +322,10 @@ def test_grouped_value_heads_validation_and_workspace():
     r = lambda x: (x * 4 + 255) // 256 * 256
     for (B, T, H, Hv, Dk, Dv) in [(2, 256, 4, 8, 128, 64), (1, 100, 2, 8, 64, 128), (2, 128, 4, 4, 128, 128)]:
         p = _prob(B=B, T=T, H=H, Hv=Hv, Dk=Dk, Dv=Dv)
-        same = _prob(B=B, T=T, H=Hv, Dk=Dk, Dv=Dv)   # the value-head problem
-        assert g2.gdr2_chunk_workspace_bytes(p, 0) == g2.gdr2_chunk_workspace_bytes(same, 0)
-        _, base, _ = ws_layout_bf16(B, T, Hv, Dk, Dv, bwd=True)
+        G = Hv // H
+        _, fwd, _ = ws_layout_bf16(B, T, Hv, Dk, Dv, bwd=False, G=G)
+        assert g2.gdr2_chunk_workspace_bytes(p, 0) == fwd + seg_buffer_bytes(B, T, Hv, Dk, Dv)
+        _, base, _ = ws_layout_bf16(B, T, Hv, Dk, Dv, bwd=True, G=G)
         part = 4 * r(B * T * Hv * Dk) if Hv > H else 0
         assert g2.gdr2_chunk_workspace_bytes(p, 1) == base + part + seg_buffer_bytes(B, T, Hv, Dk, Dv)
 
