@@ -76,6 +76,17 @@ def test_grouped_saved_path_and_head_dims():
     _check(got_r, _oracle(d), TOL["bf16"])
 
 
+@pytest.mark.parametrize("B,H,Hv,Dv", [(2, 4, 8, 128), (4, 2, 4, 64), (4, 2, 8, 128)])
+def test_grouped_scans_grouped_on_xcds(B, H, Hv, Dv):
+    """Enough (batch, key head) pairs (a multiple of 8) for the scans to place the
+    value slices of one key head's value heads on one XCD (the grouped block
+    order); G = 2 and 4, one and two value slices per head."""
+    d = make_grouped(B, 192, H, Hv, 128, Dv, seed=150 + B + Hv + Dv, dtype="bf16", s0_std=0.05, with_dST=True)
+    assert (B * H) % 8 == 0
+    _case(f"grouped bf16 B{B} T192 H{H} Hv{Hv} Dv{Dv}: XCD-grouped scan order")
+    _check(_run(d), _oracle(d), TOL["bf16"])
+
+
 def test_grouped_long_sequence_parallel_scans():
     """B1 H1 Hv2 T2048: few scans and long sequences switch the sequence-parallel scans on."""
     from tests.gpu_common import scan_segments
