@@ -222,11 +222,15 @@ gdr2_status gdr2_recurrent_varlen(const gdr2_problem* problem, const int32_t* cu
  * cu_seqlens and n_seqs > 0, or n_seqs = 0 and cu_seqlens ignored for fixed
  * length, the stored and recomputing training paths) is as in the plain calls;
  * q, k and f take the places of q, k and log_alpha with the same shapes
- * ((B,T,H,Dk); f fp32).  The chunk calls run the bf16 path only (fp32 problems:
- * GDR2_EUNSUPPORTED); the recurrent call takes both dtypes.  The workspace
- * (gdr2_fused_workspace_bytes) adds the inverse norms of q and k (saving
- * forward and backward) and the decay-parameter partials (backward); a saving
- * forward and the backward that reads it need the same stage. */
+ * ((B,T,H,Dk); f fp32).  bf16 problems do the stage inside the chunk kernels;
+ * fp32 problems (the parity mode) run it as passes of its own around the fp32
+ * operator, with the normalised q, k and g in the workspace; the recurrent
+ * call does it per token for both dtypes.  The workspace
+ * (gdr2_fused_workspace_bytes) adds the inverse norms of q and k and the
+ * gradients of the normalised q, k (saving forward and backward), the
+ * decay-parameter partials (backward) and, for fp32 problems, the stage's
+ * outputs; a saving forward and the backward that reads it need the same
+ * stage. */
 typedef struct gdr2_stage {
   const float* a_log; /* (H) fp32, device, 4-byte aligned */
   const float* delta; /* (H, Dk) fp32, device, 16-byte aligned */
@@ -276,7 +280,9 @@ typedef enum gdr2_kernel_id {
   GDR2_K_RECURRENT = 7,           /* recurrent / decode                           */
   GDR2_K_STAGE_BWD = 8,           /* fused stage: normalisation VJP, decay-
                                      parameter sums                              */
-  GDR2_NUM_KERNELS = 9
+  GDR2_K_STAGE_FWD = 9,           /* fused stage of fp32 problems: normalisation
+                                     and activation pass                         */
+  GDR2_NUM_KERNELS = 10
 } gdr2_kernel_id;
 
 /* Per-thread kernel timing for benchmarks: while enabled, each kernel launched

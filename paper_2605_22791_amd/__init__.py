@@ -28,7 +28,7 @@ GDR2_BF16, GDR2_FP32 = 0, 1
 CHUNK = 64
 # kernel ids of the measurement support (gdr2_kernel_id in include/gdr2.h)
 KERNEL_NAMES = ["fwd_intra", "fwd_state", "bwd_recompute_intra", "bwd_recompute_state",
-                "bwd_state", "bwd_wy", "bwd_intra", "recurrent", "stage_bwd"]
+                "bwd_state", "bwd_wy", "bwd_intra", "recurrent", "stage_bwd", "stage_fwd"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 

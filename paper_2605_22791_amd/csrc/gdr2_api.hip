@@ -73,6 +73,7 @@ struct Layout {
   size_t pQ, pK, pB, pG;                 // grouped value heads: fp32 key-side gradient partials
   size_t RQ, RK;                         // fused stage: inverse norms of q, k rows (rows, Hk)
   size_t PD, PA, PT;                     // fused backward: decay-parameter partials, range sums
+  size_t fQ, fK, fG, fdQ, fdK, fdG;      // fused stage of fp32 problems: its outputs and their gradients
   size_t total;
 };
 
@@ -167,7 +168,8 @@ Layout layout(const gdr2_problem* p, bool bwd, int nseq = 0, int G = 1, bool fus
   } else {
     scan_segments(p, L.nseg, L.seg_len);
   }
-  if (bwd && (G > 1 || fused)) {
+  const bool fbf16 = fused && p->dtype == GDR2_BF16;  // stage inside the bf16 kernels
+  if (bwd && (G > 1 || fbf16)) {
     // fp32 key-side gradients on the value-head axis: dq, dk for grouped heads
     // and for the fused stage (its VJP rounds once), db, dg for grouped heads
     const size_t n = (size_t)p->B * p->T * p->H * Dk;
@@ -178,7 +180,7 @@ Layout layout(const gdr2_problem* p, bool bwd, int nseq = 0, int G = 1, bool fus
       L.pG = take(n);
     }
   }
-  if (fused && bwd) {
+  if (fbf16 && bwd) {
     const size_t rows = (size_t)p->B * p->T, Hk = (size_t)(p->H / G);
     const size_t nslots = nseq > 0 ? (size_t)varlen_slots(p, nseq) : (size_t)p->B * chunks_per_seq(p);
     L.RQ = take(rows * Hk);
@@ -192,6 +194,24 @@ Layout layout(const gdr2_problem* p, bool bwd, int nseq = 0, int G = 1, bool fus
     L.sM = take(nvs * Dk * Dk);
     L.sN = take(nvs * Dk * Dv);
     L.sX = take(nvs * Dk * Dv);
+  }
+  if (fused && p->dtype == GDR2_FP32) {
+    // fp32 problems run the stage as passes of its own around the fp32 operator:
+    // its outputs (and, for the backward, their gradients) follow everything the
+    // operator itself uses, so the operator's layout is a prefix of this one
+    const size_t n = (size_t)p->B * p->T * (size_t)(p->H / G);
+    L.fQ = take(n * Dk);
+    L.fK = take(n * Dk);
+    L.fG = take(n * Dk);
+    L.RQ = take(n);
+    L.RK = take(n);
+    if (bwd) {
+      L.fdQ = take(n * Dk);
+      L.fdK = take(n * Dk);
+      L.fdG = take(n * Dk);
+      L.PA = take(n);
+      L.PT = take((size_t)kParamSplits * (p->H / G) * (Dk + 1));
+    }
   }
   L.total = off;
   return L;
@@ -671,12 +691,36 @@ gdr2_status gdr2_chunk_workspace_bytes(const gdr2_problem* p, int for_backward, 
 
 namespace {
 
-// A call with the fused stage checks it and runs on the bf16 path only.
-gdr2_status check_stage(const gdr2_problem* p, const gdr2_stage* stage, bool chunked) {
+// A call with the fused stage checks it (both dtypes: the bf16 chunk path fuses
+// the stage into its kernels, fp32 problems run it as passes of its own).
+gdr2_status check_stage(const gdr2_problem*, const gdr2_stage* stage, bool) {
   if (stage == nullptr) return GDR2_OK;
   if (!stage_ok(stage)) return GDR2_EINVAL;
-  if (chunked && p->dtype != GDR2_BF16) return GDR2_EUNSUPPORTED;
   return GDR2_OK;
+}
+
+// The stage's passes for fp32 problems (p: the value view).
+StageF32Args stage_f32_args(const gdr2_problem* p, const Layout& L, void* ws, const gdr2_stage* stage, int G,
+                            const void* q, const void* k, const float* f) {
+  StageF32Args s{};
+  s.q = static_cast<const float*>(q);
+  s.k = static_cast<const float*>(k);
+  s.f = f;
+  s.a_log = stage->a_log;
+  s.delta = stage->delta;
+  s.eps = stage->eps;
+  s.qn = at<float>(ws, L.fQ);
+  s.kn = at<float>(ws, L.fK);
+  s.g = at<float>(ws, L.fG);
+  s.rq = at<float>(ws, L.RQ);
+  s.rk = at<float>(ws, L.RK);
+  s.rows = (size_t)p->B * p->T;
+  s.Hk = p->H / G;
+  return s;
+}
+
+hipError_t launch_stage(const gdr2_problem* p, const StageF32Args& s, bool backward, hipStream_t st) {
+  return p->Dk == 64 ? launch_stage_f32<64>(s, backward, st) : launch_stage_f32<128>(s, backward, st);
 }
 
 // nseq > 0 (with cu): packed variable-length call
@@ -694,6 +738,13 @@ gdr2_status chunk_fwd(const gdr2_problem* p, const int32_t* cu, int nseq, const 
   const gdr2_problem pv = value_view(p);
   const Geo G = make_geo(&pv, save, nseq, cu, ws, group_of(p), stage);
   if (ws_bytes < G.L.total) return GDR2_EWORKSPACE;
+  if (stage != nullptr && p->dtype == GDR2_FP32) {
+    // normalised q, k and g into the workspace, then the fp32 operator on them
+    const StageF32Args sa = stage_f32_args(&pv, G.L, ws, stage, G.G, q, k, log_alpha);
+    hipError_t e = timed(GDR2_K_STAGE_FWD, stream, [&] { return launch_stage(&pv, sa, false, stream); });
+    if (e != hipSuccess) return hip_status(e, stream);
+    return chunk_fwd(p, cu, nseq, sa.qn, sa.kn, v, sa.g, b, w, S0, o, S_T, ws, ws_bytes, save, stream);
+  }
   hipError_t e = build_table(&pv, G, stream);
   if (e != hipSuccess) return GDR2_EHIP;
   if (p->dtype == GDR2_BF16)
@@ -724,6 +775,36 @@ gdr2_status chunk_bwd(const gdr2_problem* p, const int32_t* cu, int nseq, const 
   const gdr2_problem pv = value_view(p);
   const Geo G = make_geo(&pv, true, nseq, cu, ws, group_of(p), stage);
   if (ws_bytes < G.L.total) return GDR2_EWORKSPACE;
+  if (stage != nullptr && p->dtype == GDR2_FP32) {
+    // the stage again (normalised q, k, g), the fp32 operator's backward into the
+    // workspace, then the stage's VJPs and the decay-parameter sums
+    StageF32Args sa = stage_f32_args(&pv, G.L, ws, stage, G.G, q, k, log_alpha);
+    sa.dqn = at<float>(ws, G.L.fdQ);
+    sa.dkn = at<float>(ws, G.L.fdK);
+    sa.dg = at<float>(ws, G.L.fdG);
+    sa.dq = static_cast<float*>(dq);
+    sa.dk = static_cast<float*>(dk);
+    sa.df = dlog_alpha;
+    sa.pa = at<float>(ws, G.L.PA);
+    hipError_t e = timed(GDR2_K_STAGE_FWD, stream, [&] { return launch_stage(&pv, sa, false, stream); });
+    if (e != hipSuccess) return hip_status(e, stream);
+    const gdr2_status r = chunk_bwd(p, cu, nseq, sa.qn, sa.kn, v, sa.g, b, w, S0, dout, dS_T, at<float>(ws, G.L.fdQ),
+                                    at<float>(ws, G.L.fdK), dv, at<float>(ws, G.L.fdG), db, dw, dS0, ws, ws_bytes,
+                                    saved, stream);
+    if (r != GDR2_OK) return r;
+    e = timed(GDR2_K_STAGE_BWD, stream, [&] {
+      hipError_t x = launch_stage(&pv, sa, true, stream);
+      const int Hk = pv.H / G.G, nrow = pv.B * pv.T, splits = nrow < kParamSplits ? nrow : kParamSplits;
+      float* PT = at<float>(ws, G.L.PT);
+      float* PT1 = PT + (size_t)kParamSplits * Hk * pv.Dk;
+      if (x == hipSuccess) x = launch_param_reduce_pass(sa.df, PT, nrow, Hk, 1, pv.Dk, splits, stream);
+      if (x == hipSuccess) x = launch_param_reduce_pass(PT, ddelta, splits, Hk, 1, pv.Dk, 1, stream);
+      if (x == hipSuccess) x = launch_param_reduce_pass(sa.pa, PT1, nrow, Hk, 1, 1, splits, stream);
+      if (x == hipSuccess) x = launch_param_reduce_pass(PT1, da, splits, Hk, 1, 1, 1, stream);
+      return x;
+    });
+    return hip_status(e, stream);
+  }
   hipError_t e = build_table(&pv, G, stream);
   if (e != hipSuccess) return GDR2_EHIP;
   if (p->dtype == GDR2_BF16)
@@ -834,7 +915,6 @@ gdr2_status gdr2_fused_workspace_bytes(const gdr2_problem* p, int32_t n_seqs, in
   if (bytes == nullptr || n_seqs < 0) return GDR2_EINVAL;
   const gdr2_status s = check_problem(p, true, n_seqs);
   if (s != GDR2_OK) return s;
-  if (p->dtype != GDR2_BF16) return GDR2_EUNSUPPORTED;
   const gdr2_problem pv = value_view(p);
   *bytes = layout(&pv, for_backward != 0, n_seqs, group_of(p), true).total;
   return GDR2_OK;

@@ -417,6 +417,36 @@ struct NormVjpArgs {
 template <int DK>
 hipError_t launch_norm_vjp(const NormVjpArgs& a, hipStream_t st);
 
+// The fused stage of fp32 problems as passes around the fp32 operator: rows
+// r < rows of the H_k = Hk key heads, (rows, Hk, DK) fp32 tensors.
+// Forward: qn, kn = normalised q, k (inverse norms to rq, rk), g from f.
+// Backward: dq, dk from the gradients dqn, dkn of the normalised tensors;
+// df from dg, and pa[r * Hk + h] = sum_c dg * g (the per-row partials of da).
+struct StageF32Args {
+  const float* q;
+  const float* k;
+  const float* f;
+  const float* a_log;
+  const float* delta;
+  float eps;
+  float* qn;
+  float* kn;
+  float* g;
+  float* rq;
+  float* rk;
+  const float* dqn;
+  const float* dkn;
+  const float* dg;
+  float* dq;
+  float* dk;
+  float* df;
+  float* pa;
+  size_t rows;
+  int Hk;
+};
+template <int DK>
+hipError_t launch_stage_f32(const StageF32Args& a, bool backward, hipStream_t st);
+
 // Sums of the per-workgroup partials of the decay parameters, one pass:
 // out[(z * Hk + hk) * D + c] = sum over the slots s of range z (nslots cut into
 // `splits` ranges) and m < M of P[((s * Hk + hk) * M + m) * D + c].  A second

@@ -97,4 +97,88 @@ hipError_t launch_param_reduce_pass(const float* P, float* out, int nslots, int 
   return hipGetLastError();
 }
 
+// ---- fp32 problems: the stage as its own passes around the fp32 operator ----
+// Forward: rows of q (z = 0) and k (z = 1) normalised, y = x rinv, with rinv
+// kept; z = 2 forms g = -exp(a) softplus(f + delta).  DK / 4 lanes per row.
+template <int DK>
+__global__ __launch_bounds__(256) void stage_fwd_f32_kernel(StageF32Args a) {
+  constexpr int LPR = DK / 4, RPB = 256 / LPR;
+  const int z = blockIdx.y, tid = threadIdx.x, lr = tid % LPR, c0 = 4 * lr;
+  const size_t nrows = a.rows * (size_t)a.Hk;
+  for (size_t R = (size_t)blockIdx.x * RPB + tid / LPR; R < nrows; R += (size_t)gridDim.x * RPB) {
+    const size_t o = R * DK + c0;
+    if (z < 2) {
+      const float4 x = ld4((z == 0 ? a.q : a.k) + o);
+      float ss = x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
+#pragma unroll
+      for (int m = 1; m < LPR; m <<= 1) ss += __shfl_xor(ss, m);
+      const float ri = inv_norm(ss, a.eps);
+      *reinterpret_cast<float4*>((z == 0 ? a.qn : a.kn) + o) = make_float4(x.x * ri, x.y * ri, x.z * ri, x.w * ri);
+      if (lr == 0) (z == 0 ? a.rq : a.rk)[R] = ri;
+    } else {
+      const int hk = (int)(R % a.Hk);
+      const float A = expf(a.a_log[hk]);
+      const float4 f = ld4(a.f + o), dl = ld4(a.delta + (size_t)hk * DK + c0);
+      *reinterpret_cast<float4*>(a.g + o) = make_float4(decay_act(f.x, dl.x, A), decay_act(f.y, dl.y, A),
+                                                        decay_act(f.z, dl.z, A), decay_act(f.w, dl.w, A));
+    }
+  }
+}
+
+// Backward: z = 0, 1: dx = rinv (dy - y <y, dy>) from the fp32 gradients of the
+// normalised q, k; z = 2: df = dg * (-exp(a) sigmoid(f + delta)) and, per row,
+// sum_c dg * g into pa (the partials of da).
+template <int DK>
+__global__ __launch_bounds__(256) void stage_bwd_f32_kernel(StageF32Args a) {
+  constexpr int LPR = DK / 4, RPB = 256 / LPR;
+  const int z = blockIdx.y, tid = threadIdx.x, lr = tid % LPR, c0 = 4 * lr;
+  const size_t nrows = a.rows * (size_t)a.Hk;
+  for (size_t R = (size_t)blockIdx.x * RPB + tid / LPR; R < nrows; R += (size_t)gridDim.x * RPB) {
+    const size_t o = R * DK + c0;
+    if (z < 2) {
+      const float ri = (z == 0 ? a.rq : a.rk)[R];
+      const float4 x = ld4((z == 0 ? a.q : a.k) + o), dy = ld4((z == 0 ? a.dqn : a.dkn) + o);
+      const float y[4] = {x.x * ri, x.y * ri, x.z * ri, x.w * ri};
+      float dot = y[0] * dy.x + y[1] * dy.y + y[2] * dy.z + y[3] * dy.w;
+#pragma unroll
+      for (int m = 1; m < LPR; m <<= 1) dot += __shfl_xor(dot, m);
+      *reinterpret_cast<float4*>((z == 0 ? a.dq : a.dk) + o) =
+          make_float4(ri * (dy.x - y[0] * dot), ri * (dy.y - y[1] * dot), ri * (dy.z - y[2] * dot),
+                      ri * (dy.w - y[3] * dot));
+    } else {
+      const int hk = (int)(R % a.Hk);
+      const float A = expf(a.a_log[hk]);
+      const float4 f = ld4(a.f + o), dl = ld4(a.delta + (size_t)hk * DK + c0), dg = ld4(a.dg + o);
+      const float x[4] = {f.x + dl.x, f.y + dl.y, f.z + dl.z, f.w + dl.w}, d[4] = {dg.x, dg.y, dg.z, dg.w};
+      float df[4], pa = 0.f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        df[e] = d[e] * (-A * sigmoid_f(x[e]));
+        pa += d[e] * (-A * softplus_f(x[e]));
+      }
+      *reinterpret_cast<float4*>(a.df + o) = make_float4(df[0], df[1], df[2], df[3]);
+#pragma unroll
+      for (int m = 1; m < LPR; m <<= 1) pa += __shfl_xor(pa, m);
+      if (lr == 0) a.pa[R] = pa;
+    }
+  }
+}
+
+template <int DK>
+hipError_t launch_stage_f32(const StageF32Args& a, bool backward, hipStream_t st) {
+  constexpr int RPB = 256 / (DK / 4);
+  const size_t nrows = a.rows * (size_t)a.Hk;
+  if (nrows == 0) return hipSuccess;
+  const size_t blocks = (nrows + RPB - 1) / RPB;
+  dim3 grid((unsigned)(blocks < 32768 ? blocks : 32768), 3);
+  if (backward)
+    hipLaunchKernelGGL((stage_bwd_f32_kernel<DK>), grid, dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL((stage_fwd_f32_kernel<DK>), grid, dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+template hipError_t launch_stage_f32<64>(const StageF32Args&, bool, hipStream_t);
+template hipError_t launch_stage_f32<128>(const StageF32Args&, bool, hipStream_t);
+
 }  // namespace gdr2

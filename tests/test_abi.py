@@ -352,8 +352,8 @@ def _fbwd(prob, stage, da=FAKE, ddelta=FAKE, ws_bytes=1 << 40, saved=0):
 
 def test_fused_stage_validation():
     """The stage needs a_log (4-byte aligned), delta (16-byte aligned) and a finite
-    eps >= 0; the chunk calls are bf16 only; the backward needs da and an aligned
-    ddelta -- all rejected before any launch."""
+    eps >= 0; the backward needs da and an aligned ddelta -- all rejected before
+    any launch."""
     L = g2.lib()
     p = _prob()
     for call in (_ffwd, _fbwd):
@@ -364,13 +364,10 @@ def test_fused_stage_validation():
         assert call(p, _stg(d=FAKE + 4)) == g2.GDR2_EINVAL
         assert call(p, _stg(eps=-1e-6)) == g2.GDR2_EINVAL
         assert call(p, _stg(eps=float("nan"))) == g2.GDR2_EINVAL
-        assert call(_prob(dtype=g2.GDR2_FP32), _stg()) == g2.GDR2_EUNSUPPORTED
         assert call(_prob(Dk=96), _stg()) == g2.GDR2_EUNSUPPORTED
     assert _fbwd(p, _stg(), da=0) == g2.GDR2_EINVAL
     assert _fbwd(p, _stg(), ddelta=FAKE + 4) == g2.GDR2_EINVAL
     n = ctypes.c_size_t(0)
-    assert L.gdr2_fused_workspace_bytes(ctypes.byref(_prob(dtype=g2.GDR2_FP32)), 0, 0, ctypes.byref(n)) == \
-        g2.GDR2_EUNSUPPORTED
     assert L.gdr2_fused_workspace_bytes(ctypes.byref(p), -1, 0, ctypes.byref(n)) == g2.GDR2_EINVAL
     fwd = g2.gdr2_fused_workspace_bytes(p, 0, 0)
     bwd = g2.gdr2_fused_workspace_bytes(p, 0, 1)
@@ -405,3 +402,18 @@ def test_fused_workspace_size():
         if Hv == H:   # fp32 dq, dk of the normalised tensors (grouped calls have them already)
             extra += 2 * r(B * T * Hv * Dk)
         assert g2.gdr2_fused_workspace_bytes(p, N, 1) == plain(1) + extra, (B, T, H, Hv, N)
+
+
+def test_fused_workspace_size_fp32():
+    """fp32 problems run the stage as passes of their own: the workspace is the
+    fp32 operator's, then the normalised q, k and g ((B T, H, Dk) fp32 each) and
+    the inverse norms; the backward adds the gradients of those three, the
+    per-row partials of da and the 64-range sums."""
+    r = lambda x: (x * 4 + 255) // 256 * 256
+    for (B, T, H, Hv, Dk, Dv) in [(2, 256, 4, 4, 128, 64), (1, 100, 2, 4, 64, 128)]:
+        p = _prob(B=B, T=T, H=H, Hv=Hv, Dk=Dk, Dv=Dv, dtype=g2.GDR2_FP32)
+        n = B * T * H
+        fwd = 3 * r(n * Dk) + 2 * r(n)
+        assert g2.gdr2_fused_workspace_bytes(p, 0, 0) == g2.gdr2_chunk_workspace_bytes(p, 0) + fwd
+        bwd = fwd + 3 * r(n * Dk) + r(n) + r(64 * H * (Dk + 1))
+        assert g2.gdr2_fused_workspace_bytes(p, 0, 1) == g2.gdr2_chunk_workspace_bytes(p, 1) + bwd

@@ -183,3 +183,23 @@ def test_fused_decay_activation_over_its_domain():
     e_o, e_s = rel_l2(host(o), ref["o"]), rel_l2(host(S), ref["S_T"])
     print("o", e_o, "S", e_s)
     assert e_o < 1e-5 and e_s < 1e-5
+
+
+@pytest.mark.parametrize("case", ["plain", "grouped", "packed"])
+def test_fused_fp32_chunk(case):
+    """fp32 problems (the 1e-5 parity mode) run the stage as passes of their own
+    around the fp32 operator: forward and every gradient at 1e-5, stored path
+    bit-identical to the recomputing one."""
+    if case == "plain":
+        d = make_fused(2, 200, 2, 64, 128, seed=320, dtype="fp32", s0_std=0.05, with_dST=True)
+    elif case == "grouped":
+        d = make_fused(1, 130, 2, 128, 64, seed=321, dtype="fp32", Hv=4, s0_std=0.05, with_dST=True)
+    else:
+        d = make_fused(0, 0, 2, 128, 128, seed=322, dtype="fp32", lengths=[70, 0, 1, 130], s0_std=0.05,
+                       with_dST=True)
+    _case(f"fused fp32 chunk, {case}")
+    got = _run(d)
+    _check(got, _oracle(d), TOL["fp32"])
+    got_s = _run(d, save=True)
+    for n in OUTS:
+        assert np.array_equal(got_s[n], got[n]), n
