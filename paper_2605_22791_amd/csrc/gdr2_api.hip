@@ -170,9 +170,11 @@ Layout layout(const gdr2_problem* p, bool bwd, int nseq = 0, int G = 1, bool fus
   }
   const bool fbf16 = fused && p->dtype == GDR2_BF16;  // stage inside the bf16 kernels
   if (bwd && (G > 1 || fbf16)) {
-    // fp32 key-side gradients on the value-head axis: dq, dk for grouped heads
-    // and for the fused stage (its VJP rounds once), db, dg for grouped heads
-    const size_t n = (size_t)p->B * p->T * p->H * Dk;
+    // fp32 key-side gradients: bf16 problems sum a group's value heads in them
+    // on the key-head axis (and the fused stage keeps dq, dk there for its VJP,
+    // which rounds once); fp32 problems keep one partial per value head
+    const size_t heads = p->dtype == GDR2_BF16 ? (size_t)(p->H / G) : (size_t)p->H;
+    const size_t n = (size_t)p->B * p->T * heads * Dk;
     L.pQ = take(n);
     L.pK = take(n);
     if (G > 1) {
@@ -335,9 +337,8 @@ hipError_t timed(int id, hipStream_t st, F&& launch) {
   return hipSuccess;
 }
 
-// ---- grouped value heads: sum each key head's G partials into dq, dk, db, dlog_alpha
-// (p: the value view, so the key heads are p->H / G); dq, dk null: left to the
-// fused stage's normalisation VJP, which sums their partials itself
+// ---- grouped value heads of fp32 problems: sum each key head's G partials into
+// dq, dk, db, dlog_alpha (p: the value view, so the key heads are p->H / G)
 template <typename TIn>
 hipError_t group_reduce(const gdr2_problem* p, const Geo& G, const Layout& L, void* ws, void* dq, void* dk,
                         void* db, float* dg, hipStream_t st) {
@@ -366,13 +367,13 @@ hipError_t stage_bwd(const gdr2_problem* p, const Geo& G, void* ws, const void* 
   na.x[1] = static_cast<const bf16_t*>(k);
   na.rinv[0] = G.st.RQ;
   na.rinv[1] = G.st.RK;
-  na.P[0] = at<float>(ws, L.pQ);
+  na.P[0] = at<float>(ws, L.pQ);  // summed over the group already (key-head axis)
   na.P[1] = at<float>(ws, L.pK);
   na.dx[0] = static_cast<bf16_t*>(dq);
   na.dx[1] = static_cast<bf16_t*>(dk);
   na.rows = (size_t)p->B * p->T;
   na.Hk = Hk;
-  na.G = G.G;
+  na.G = 1;
   hipError_t e = launch_norm_vjp<DK>(na, st);
   if (e != hipSuccess) return e;
   const int nslots = G.vl.ct0 != nullptr ? G.vl.ncmax : p->B * G.NT;
@@ -566,11 +567,11 @@ struct BwdRun {
                         p->B, p->T, p->H, NT, p->scale};
       ca.vl = G.vl;
       ca.G = G.G;
-      if (G.G > 1) {
-        ca.Pq = at<float>(ws, L.pQ);
-        ca.Pk = at<float>(ws, L.pK);
-        ca.Pb = at<float>(ws, L.pB);
-        ca.dg = at<float>(ws, L.pG);
+      if (G.G > 1) {  // the group's key-side gradients add up on the key-head axis
+        ca.Aq = at<float>(ws, L.pQ);
+        ca.Ak = at<float>(ws, L.pK);
+        ca.Ab = at<float>(ws, L.pB);
+        ca.Ag = at<float>(ws, L.pG);
       }
       if (fused) {
         ca.st = G.st;
@@ -580,9 +581,13 @@ struct BwdRun {
         ca.Pk = at<float>(ws, L.pK);
       }
       e = timed(GDR2_K_BWD_INTRA, st, [&] {
-        hipError_t r = launch_bchunk_bf16<DK, DV>(ca, st);
-        if (r == hipSuccess && G.G > 1)
-          r = group_reduce<bf16_t>(p, G, L, ws, fused ? nullptr : dq, fused ? nullptr : dk, db, dg, st);
+        // one launch per value head of the groups, in order (G = 1: one launch)
+        hipError_t r = hipSuccess;
+        for (int j = 0; j < G.G && r == hipSuccess; ++j) {
+          ca.gj = j;
+          ca.gmode = G.G == 1 ? 0 : (j == 0 ? 1 : (j + 1 < G.G ? 2 : 3));
+          r = launch_bchunk_bf16<DK, DV>(ca, st);
+        }
         return r;
       });
       if (e != hipSuccess || !fused) return e;

@@ -141,6 +141,13 @@ __device__ __forceinline__ void store_row4(__bf16* p, const float (&v)[4]) {
 __device__ __forceinline__ void store_row4(float* p, const float (&v)[4]) {
   *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
 }
+__device__ __forceinline__ void add_row4(const float* p, float (&v)[4]) {
+  const float4 x = *reinterpret_cast<const float4*>(p);
+  v[0] += x.x;
+  v[1] += x.y;
+  v[2] += x.z;
+  v[3] += x.w;
+}
 
 // element j (0..3) of four per-block values, j lane-dependent
 __device__ __forceinline__ float pick4(const float (&x)[4], int j) {
@@ -184,34 +191,32 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, r16 = lane & 15;
   ChunkPos cp;
+  // the grid covers the key heads; this launch takes value head gj of each group
+  const int h = blockIdx.y * a.G + a.gj, H = a.H;
   // fused stage: this workgroup's slot of the decay-parameter partials
-  const size_t pslot = ((size_t)(blockIdx.z * gridDim.x + blockIdx.x) * a.H + blockIdx.y) * 4 + wave;
-  if (!chunk_pos(a.vl, blockIdx.x, blockIdx.y, blockIdx.z, a.T, a.H, a.NT, cp)) {
+  const size_t pslot = ((size_t)(blockIdx.z * gridDim.x + blockIdx.x) * H + h) * 4 + wave;
+  if (!chunk_pos(a.vl, blockIdx.x, h, blockIdx.z, a.T, H, a.NT, cp)) {
     if constexpr (FUSED) {  // an unused slot of a packed grid adds zeros
       for (int c = lane; c < DK; c += 64) a.PD[pslot * DK + c] = 0.f;
       if (lane == 0) a.PA[pslot] = 0.f;
     }
     return;
   }
-  const int h = blockIdx.y, H = a.H;
   const size_t ch = cp.ch, row0 = cp.row0;
   // Rows in use.  Loads read in-range rows only (rows past a partial chunk's
   // end re-read its last row); g, k and dO of those rows are then taken as
   // zero, which makes every term they could add to a valid row vanish (their
   // dT, dA_qk, dR and dG are zero), and their outputs are not written.
   const int len = cp.len;
-  // key-side inputs (q, k, g, b) live on the H / G key heads (value head h reads
-  // key head h / G); with G > 1 the key-side gradients of this value head go to
-  // fp32 partials on the value-head axis, which the group reduction sums (partq:
-  // dq, dk; partb: db and dg, the latter through a.dg).  The fused stage keeps
-  // dq, dk in fp32 also for G = 1 (one rounding after its normalisation VJP);
-  // for G = 1 both axes coincide.
-  const int HK = H / a.G, hk = h / a.G;
-  const bool partq = a.Pq != nullptr, partb = a.Pb != nullptr;
-  const bool part = partq || partb;
+  // key-side inputs (q, k, g, b) and gradients live on the H / G key heads
+  // (value head h reads key head h / G); the fused stage keeps dq, dk in fp32
+  // (partq; one rounding after its normalisation VJP)
+  const int HK = H / a.G, hk = blockIdx.y;
+  const bool partq = a.Pq != nullptr;
+  const int gmode = a.gmode;  // 0: direct, 1 / 2 / 3: first / middle / last value head of a group
   const size_t KST = (size_t)HK * DK, VST = (size_t)H * DV;  // token strides
   const size_t kb0 = row0 * KST + (size_t)hk * DK, vb0 = row0 * VST + (size_t)h * DV;
-  const size_t ko0 = part ? row0 * ((size_t)H * DK) + (size_t)h * DK : kb0;  // key-side outputs
+  const size_t ko0 = kb0;  // key-side outputs
   const int i = wave;  // the row block this wave owns
   const int kbl = i >> 1;
 
@@ -225,7 +230,6 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   __bf16* dBp = reinterpret_cast<__bf16*>(a.db) + ko0;
   float* pQp = partq ? a.Pq + ko0 : nullptr;
   float* pKp = partq ? a.Pk + ko0 : nullptr;
-  float* pBp = partb ? a.Pb + ko0 : nullptr;
   float* dGp = a.dg + ko0;
   const __bf16* Vp = reinterpret_cast<const __bf16*>(a.v) + vb0;
   const __bf16* Wp = reinterpret_cast<const __bf16*>(a.w) + vb0;
@@ -235,7 +239,7 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   const float* Hc = a.Hs + ch * DK * DV;
   const float* DHc = a.DH + ch * DK * DV;
   const float* Rc = a.Rs + ch * CH * DV;
-  const int kst = HK * DK, kso = part ? H * DK : kst, vst = H * DV;
+  const int kst = HK * DK, kso = kst, vst = H * DV;
 
   // staging role: chunk row grow (block = wave), channels 16 cb + 4 cq + (0..3)
   const int rl = lane >> 2, cq = lane & 3, grow = 16 * wave + rl;
@@ -647,17 +651,26 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     quad_transpose(ok, jq);
     quad_transpose(ob, jq);
     if (orow < len) {
-      if (partq) {
-        store_row4(pQp + oo, oq);
-        store_row4(pKp + oo, ok);
-      } else {
-        store_row4(dQp + oo, oq);
-        store_row4(dKp + oo, ok);
+      const size_t ao = ko0 + oo;
+      if (gmode >= 2) {  // the earlier value heads' sums
+        add_row4(a.Aq + ao, oq);
+        add_row4(a.Ak + ao, ok);
+        add_row4(a.Ab + ao, ob);
       }
-      if (partb)
-        store_row4(pBp + oo, ob);
-      else
+      if (gmode == 1 || gmode == 2) {
+        store_row4(a.Aq + ao, oq);
+        store_row4(a.Ak + ao, ok);
+        store_row4(a.Ab + ao, ob);
+      } else {
+        if (partq) {
+          store_row4(pQp + oo, oq);
+          store_row4(pKp + oo, ok);
+        } else {
+          store_row4(dQp + oo, oq);
+          store_row4(dKp + oo, ok);
+        }
         store_row4(dBp + oo, ob);
+      }
     }
     // reverse cumulative sum of dG: within the lane, over the lane groups, then blocks
     const float s3 = dgl[3], s2 = s3 + dgl[2], s1 = s2 + dgl[1], s0 = s1 + dgl[0];
@@ -698,14 +711,20 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
         }
       }
       quad_transpose(dfv, jq);
-      if (orow < len) store_row4(dGp + oo, dfv);
+      if (orow < len) {
+        if (gmode >= 2) add_row4(a.Ag + ko0 + oo, dfv);
+        store_row4((gmode == 1 || gmode == 2) ? a.Ag + ko0 + oo : dGp + oo, dfv);
+      }
       pdc += __shfl_xor(pdc, 16);
       pdc += __shfl_xor(pdc, 32);
       if (g == 0) a.PD[pslot * DK + 16 * cb + r16] = pdc;
     } else {
       float dgv[4] = {s0 + off, s1 + off, s2 + off, s3 + off};
       quad_transpose(dgv, jq);
-      if (orow < len) store_row4(dGp + oo, dgv);
+      if (orow < len) {
+        if (gmode >= 2) add_row4(a.Ag + ko0 + oo, dgv);
+        store_row4((gmode == 1 || gmode == 2) ? a.Ag + ko0 + oo : dGp + oo, dgv);
+      }
     }
     if (cb + 1 < NCB) GDR2_STAGE(par ^ 1, cb + 1)
     __syncthreads();
@@ -726,7 +745,7 @@ hipError_t launch_bchunk_bf16_t(const BChunkBf16Args& a, hipStream_t st) {
   const void* fn = reinterpret_cast<const void*>(&bchunk_bf16_kernel<DK, DV, FUSED>);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) return e;
-  dim3 grid(a.vl.ct0 ? a.vl.ncmax : a.NT, a.H, a.vl.ct0 ? 1 : a.B);
+  dim3 grid(a.vl.ct0 ? a.vl.ncmax : a.NT, a.H / a.G, a.vl.ct0 ? 1 : a.B);
   hipLaunchKernelGGL((bchunk_bf16_kernel<DK, DV, FUSED>), grid, dim3(C::NTHR), lds, st, a);
   return hipGetLastError();
 }

@@ -353,14 +353,22 @@ struct BChunkBf16Args {
   float scale;
   Varlen vl{};
   // grouped value heads: H value heads share H / G key heads.  With G > 1 the
-  // key-side gradients of each value head go, in fp32 and on the value-head
-  // axis, to Pq, Pk, Pb and to dg (then a (B*T, H, Dk) fp32 partial), and the
-  // group reduction sums them.  Pq / Pk and Pb are independent: the fused stage
-  // sets Pq, Pk alone for G = 1.
+  // kernel is launched once per value head of every group (gj = 0 .. G - 1, in
+  // order; the grid covers the key heads) and the key-side gradients add up in
+  // fp32 on the key-head axis in Aq, Ak, Ab, Ag ((rows, H / G, Dk) each): gmode
+  // 1 stores the first value head's, 2 adds the next, 3 adds the last and
+  // writes the outputs (gmode 0: G = 1, outputs written directly).  The sums
+  // run in the order of the value heads, so the result is deterministic.
   int G = 1;
+  int gj = 0, gmode = 0;
+  float* Aq = nullptr;
+  float* Ak = nullptr;
+  float* Ab = nullptr;
+  float* Ag = nullptr;
+  // Pq, Pk set: dq, dk leave in fp32 there (key-head axis) instead of in the
+  // output dtype (the fused stage's normalisation VJP reads them)
   float* Pq = nullptr;
   float* Pk = nullptr;
-  float* Pb = nullptr;
   // fused input stage: q, k raw (normalised with the stored inverse norms), g
   // holds f and dg receives df = dg * dg/df; dq and dk stay the gradients of the
   // normalised q, k (the normalisation VJP follows in its own kernel).  Per

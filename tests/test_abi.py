@@ -311,8 +311,8 @@ def test_varlen_workspace_size():
 def test_grouped_value_heads_validation_and_workspace():
     """Hv must be a multiple of H (0 means Hv = H).  A grouped problem keeps the
     key-side tiles once per key head and U (and the backward's per-value-head
-    regions) per value head; its backward adds four fp32 (B, T, Hv, Dk) regions
-    for the per-value-head key-side gradients."""
+    regions) per value head; its backward adds four fp32 (B, T, H, Dk) regions in
+    which the key-side gradients of a group's value heads add up."""
     from tests.gpu_common import ws_layout_bf16, seg_buffer_bytes
     assert _fwd(_prob(H=4, Hv=6)) == g2.GDR2_EINVAL
     assert _bwd(_prob(H=4, Hv=-4)) == g2.GDR2_EINVAL
@@ -326,7 +326,7 @@ def test_grouped_value_heads_validation_and_workspace():
         _, fwd, _ = ws_layout_bf16(B, T, Hv, Dk, Dv, bwd=False, G=G)
         assert g2.gdr2_chunk_workspace_bytes(p, 0) == fwd + seg_buffer_bytes(B, T, Hv, Dk, Dv)
         _, base, _ = ws_layout_bf16(B, T, Hv, Dk, Dv, bwd=True, G=G)
-        part = 4 * r(B * T * Hv * Dk) if Hv > H else 0
+        part = 4 * r(B * T * H * Dk) if Hv > H else 0  # fp32 group sums on the key-head axis
         assert g2.gdr2_chunk_workspace_bytes(p, 1) == base + part + seg_buffer_bytes(B, T, Hv, Dk, Dv)
 
 
