@@ -1,8 +1,9 @@
 // Grouped value heads (Sec. 3.5, App. C.1): q, k, the log-decay and b of a key
 // head are shared by the G value heads of its group, so their gradients are
-// the sums of the per-value-head contributions, which the chunk backward
-// leaves in fp32 on the value-head axis.  One thread per 4 consecutive
-// outputs; the G partials are added in a fixed order (deterministic).
+// the sums of the per-value-head contributions, which the fp32 chunk backward
+// leaves in fp32 on the value-head axis (the bf16 one adds them up itself).
+// One thread per 4 consecutive outputs; the G partials are added in a fixed
+// order (deterministic).
 
 #include "gdr2_kernels.hpp"
 
