@@ -87,6 +87,18 @@ def test_grouped_scans_grouped_on_xcds(B, H, Hv, Dv):
     _check(_run(d), _oracle(d), TOL["bf16"])
 
 
+def test_grouped_segmented_scans_grouped_on_xcds():
+    """B1 H2 Hv4 T4096: four segments per sequence and a multiple of 8 (key head,
+    segment) units, so the sequence-parallel scans take the XCD-grouped order."""
+    from tests.gpu_common import scan_segments
+    nseg = scan_segments(1, 4096, 4, 128)[0]
+    assert nseg > 1 and (2 * nseg) % 8 == 0
+    d = make_grouped(1, 4096, 2, 4, 128, 128, seed=149, dtype="bf16", decay_shift=-2.0, s0_std=0.05,
+                     with_dST=True)
+    _case(f"grouped bf16 B1 T4096 H2 Hv4, {nseg} segments, XCD-grouped order")
+    _check(_run(d), _oracle(d), TOL["bf16"])
+
+
 def test_grouped_long_sequence_parallel_scans():
     """B1 H1 Hv2 T2048: few scans and long sequences switch the sequence-parallel scans on."""
     from tests.gpu_common import scan_segments
