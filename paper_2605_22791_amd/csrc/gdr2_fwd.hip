@@ -3,8 +3,8 @@
 //   fwd_intra  one workgroup per (chunk, head, batch): the decay scan, the
 //              gate-absorbed tiles, the Gram T and scores A_qk on MFMA, the
 //              fp32 WY solve and the auxiliaries Y = A Ebar, U = A (W*V)
-//              (Sec. 3.3; App. A; App. C.2 "intra-chunk products", "WY solve",
-//              "auxiliary construction").
+//              (Sec. 3.3; App. A; App. C.2: the intra-chunk products, the WY
+//              solve and the construction of the auxiliaries).
 //   fwd_state  one workgroup per (value slice, head, batch): the sequential
 //              inter-chunk recurrence (eq. eq_gdn2_chunk_state) with the fp32
 //              state slice resident in LDS, fused with the chunk output
