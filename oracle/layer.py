@@ -9,7 +9,7 @@ Two steps sit between the projections and the recurrence:
     epsilon; this build reads the normalisation as
         y = x * (sum_c x_c^2 + eps)^(-1/2)
     with a small eps (1e-6 by default), which is the plain x / ||x|| for eps = 0.
-    Its vector-Jacobian product ("the standard L2-normalisation VJP") is, with
+    Its vector-Jacobian product (the usual one of an L2 normalisation) is, with
     r = (sum x^2 + eps)^(-1/2) and y = r x,
         dx = r * (dy - y <y, dy>),
     exact for every eps (d r / d x = -r^3 x).
