@@ -164,6 +164,47 @@ def test_bf16_long_memory_decay(Dk, Dv):
     _compare(_run_bwd(d), _adjoint(d), TOL["bf16"])
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+@pytest.mark.parametrize("case", ["no_erase_no_write", "no_erase", "no_decay"])
+def test_degenerate_gates(dtype, case):
+    """Gates at the ends of their range (Sec. 3.1): b = 0 erases nothing, w = 0
+    writes nothing, log_alpha = 0 keeps the state.  With b = w = 0 the state
+    only decays, so Ebar, Z, U, R and the Gram T vanish and A = I; with b = 0,
+    w = 1 the rule is a decayed linear-attention write; with no decay every
+    gamma is 1.  Forward and backward against the fp64 recurrence; a gradient
+    whose exact value is zero (dv = dZ * w with w = 0) must come out exactly
+    zero."""
+    b_val, w_val = {"no_erase_no_write": (0.0, 0.0), "no_erase": (0.0, 1.0), "no_decay": (None, None)}[case]
+    from oracle import gdr2_recurrent_fwd
+    import paper_2605_22791_amd as g2
+    d = make_inputs(2, 160, 2, 128, 64, seed=71, dtype=dtype, s0_std=0.05, with_dST=True)
+    if case == "no_decay":
+        d["log_alpha"] = np.zeros_like(d["log_alpha"])
+    else:
+        d["b"] = np.full_like(d["b"], b_val)
+        d["w"] = np.full_like(d["w"], w_val)
+        # a weak decay: with nothing written, S_T is S0 times the decay of all
+        # 160 tokens, which at the usual decay (about e^-112) is below fp32's range
+        d["log_alpha"] = (0.05 * d["log_alpha"]).astype(np.float32)
+    _case(f"{dtype} degenerate gates: {case}")
+    x = dev_inputs(d)
+    o, ST = g2.gdr2_chunk_fwd(x["q"], x["k"], x["v"], x["log_alpha"], x["b"], x["w"], x["S0"], scale=d["scale"])
+    o_ref, S_ref = gdr2_recurrent_fwd(d["q"], d["k"], d["v"], d["log_alpha"], d["b"], d["w"], d["S0"], d["scale"])
+    e_o, e_s = rel_l2(host(o), o_ref), rel_l2(host(ST), S_ref)
+    print("o", e_o, "S_T", e_s)
+    assert e_o < TOL[dtype] and e_s < TOL[dtype]
+    got, ref = _run_bwd(d), _adjoint(d)
+    for gn, rn in NAMES + [("dS0", "dS0")]:
+        if not np.any(ref[rn]):
+            assert not np.any(got[gn]), gn
+            continue
+        err = rel_l2(got[gn], ref[rn])
+        print(gn, f"{err:.2e}")
+        assert err < TOL[dtype], (gn, err)
+    if w_val == 0.0:
+        assert not np.any(ref["dv"])
+
+
 def test_bf16_backward_single_chunk_no_state():
     d = make_inputs(1, 64, 2, 128, 128, seed=65, dtype="bf16")
     _case("bf16 bwd one chunk, S0 = 0, dS_T = 0")
