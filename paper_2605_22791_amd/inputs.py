@@ -125,6 +125,33 @@ def make_inputs(B, T, H, Dk, Dv, seed, dtype="bf16", decay_shift=0.0,
     return out
 
 
+def make_inputs_device(B, T, H, Dk, Dv, seed, decay_shift=0.0, device="cuda"):
+    """make_inputs' bf16 channel-gate recipe drawn on the device with torch's
+    generator, for shapes whose host copies would take tens of GB: q, k unit
+    rows, v, b = sigmoid, w = sigmoid and do in bf16, log_alpha =
+    -softplus(N(0,1) + decay_shift) in fp32, no S0.  Returns a dict of device
+    tensors (the same distributions as make_inputs, not the same values)."""
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+    bf = torch.bfloat16
+
+    def normal(*shape):
+        return torch.randn(shape, generator=gen, device=device, dtype=torch.float32)
+
+    def unit_rows(x):
+        return (x / torch.sqrt((x * x).sum(dim=-1, keepdim=True))).to(bf)
+
+    out = dict(q=unit_rows(normal(B, T, H, Dk)), k=unit_rows(normal(B, T, H, Dk)),
+               v=normal(B, T, H, Dv).to(bf))
+    out["log_alpha"] = -torch.nn.functional.softplus(normal(B, T, H, Dk) + decay_shift)
+    out["b"] = torch.sigmoid(normal(B, T, H, Dk)).to(bf)
+    out["w"] = torch.sigmoid(normal(B, T, H, Dv)).to(bf)
+    out["do"] = normal(B, T, H, Dv).to(bf)
+    out["scale"] = float(1.0 / np.sqrt(Dk))
+    return out
+
+
 # The five workloads (shape, precision, distributions).  Seeds: config i uses seed i.
 CONFIGS = {
     0: dict(B=1, H=2, T=256, Dk=64, Dv=64, dtype="fp32", decay_shift=0.0, s0_std=0.0,
