@@ -148,12 +148,38 @@ def _problem(q, v, scale, chunk=CHUNK):
     return Gdr2Problem(B, T, H, Dk, Dv, chunk, float(scale), _dtype_code(q), Hv)
 
 
-def _require(name, t, shape, dtype):
+def _require(name, t, shape, dtype, device=None):
+    """t is None or a contiguous device tensor of this shape and dtype (on
+    `device` when given: every buffer of a call lives on its inputs' GPU)."""
     if t is None:
         return
     if tuple(t.shape) != tuple(shape) or t.dtype != dtype or not t.is_contiguous() or not t.is_cuda:
         raise ValueError(f"{name}: expected contiguous {dtype} device tensor of shape {tuple(shape)}, "
                          f"got {t.dtype} {tuple(t.shape)} (contiguous={t.is_contiguous()}, cuda={t.is_cuda})")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name}: on {t.device}, the call's inputs are on {device}")
+
+
+def _require_ws(ws, need, device):
+    """The workspace: a contiguous uint8 tensor on the inputs' GPU (its numel is
+    the byte count handed to the library, which rejects one below `need`)."""
+    torch = _torch()
+    _require("ws", ws, (ws.numel(),), torch.uint8, device)
+    if ws.numel() < need:
+        raise ValueError(f"ws: {ws.numel()} bytes, the call needs {need}")
+
+
+def _require_grads(g, shapes, device):
+    """Caller-supplied gradient buffers: each of the shape and dtype the
+    library writes (shapes: name -> (shape, dtype))."""
+    for n, (shape, dtype) in shapes.items():
+        _require(n, g.get(n), shape, dtype, device)
+
+
+def _on(t):
+    """Context that makes t's GPU current for the library call (its stream is
+    that device's current stream)."""
+    return _torch().cuda.device(t.device)
 
 
 def _validate(q, k, v, log_alpha, b, w):
@@ -165,11 +191,12 @@ def _validate(q, k, v, log_alpha, b, w):
     Hv, Dv = v.shape[2], v.shape[-1]
     if Hv % H != 0:
         raise ValueError(f"value heads ({Hv}) must be a multiple of key heads ({H})")
+    dev = q.device
     for n, t in (("q", q), ("k", k), ("b", b)):
-        _require(n, t, (B, T, H, Dk), q.dtype)
+        _require(n, t, (B, T, H, Dk), q.dtype, dev)
     for n, t in (("v", v), ("w", w)):
-        _require(n, t, (B, T, Hv, Dv), q.dtype)
-    _require("log_alpha", log_alpha, (B, T, H, Dk), torch.float32)
+        _require(n, t, (B, T, Hv, Dv), q.dtype, dev)
+    _require("log_alpha", log_alpha, (B, T, H, Dk), torch.float32, dev)
     return B, T, Hv, Dk, Dv
 
 
@@ -190,22 +217,24 @@ def gdr2_chunk_fwd(q, k, v, log_alpha, b, w, S0=None, *, scale=None, o=None, S_T
     holds the intermediates that gdr2_chunk_bwd(..., saved=True) reads."""
     torch = _torch()
     B, T, H, Dk, Dv = _validate(q, k, v, log_alpha, b, w)
-    _require("S0", S0, (B, H, Dk, Dv), torch.float32)
+    _require("S0", S0, (B, H, Dk, Dv), torch.float32, q.device)
     prob = _problem(q, v, scale)
     if o is None:
         o = torch.empty((B, T, H, Dv), dtype=q.dtype, device=q.device)
-    _require("o", o, (B, T, H, Dv), q.dtype)
+    _require("o", o, (B, T, H, Dv), q.dtype, q.device)
     if S_T is None and want_state:
         S_T = torch.empty((B, H, Dk, Dv), dtype=torch.float32, device=q.device)
-    _require("S_T", S_T, (B, H, Dk, Dv), torch.float32)
+    _require("S_T", S_T, (B, H, Dk, Dv), torch.float32, q.device)
     need = gdr2_chunk_workspace_bytes(prob, 1 if save else 0)
     if ws is None:
         if save:
             raise ValueError("save=True needs the workspace that the backward will read")
         ws = torch.empty(need, dtype=torch.uint8, device=q.device)
+    _require_ws(ws, need, q.device)
     fn = lib().gdr2_chunk_fwd_save if save else lib().gdr2_chunk_fwd
-    st = fn(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(b),
-                              _ptr(w), _ptr(S0), _ptr(o), _ptr(S_T), _ptr(ws), ws.numel(), _stream())
+    with _on(q):
+        st = fn(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(b),
+                                  _ptr(w), _ptr(S0), _ptr(o), _ptr(S_T), _ptr(ws), ws.numel(), _stream())
     _check(st, "gdr2_chunk_fwd_save" if save else "gdr2_chunk_fwd")
     return o, S_T
 
@@ -217,9 +246,9 @@ def gdr2_chunk_bwd(q, k, v, log_alpha, b, w, S0, dout, dS_T=None, *, scale=None,
     saved=True calls gdr2_chunk_bwd_saved on the ws a save=True forward filled."""
     torch = _torch()
     B, T, H, Dk, Dv = _validate(q, k, v, log_alpha, b, w)
-    _require("S0", S0, (B, H, Dk, Dv), torch.float32)
-    _require("dout", dout, (B, T, H, Dv), q.dtype)
-    _require("dS_T", dS_T, (B, H, Dk, Dv), torch.float32)
+    _require("S0", S0, (B, H, Dk, Dv), torch.float32, q.device)
+    _require("dout", dout, (B, T, H, Dv), q.dtype, q.device)
+    _require("dS_T", dS_T, (B, H, Dk, Dv), torch.float32, q.device)
     prob = _problem(q, v, scale)
     g = dict(grads or {})
     dev = q.device
@@ -238,11 +267,16 @@ def gdr2_chunk_bwd(q, k, v, log_alpha, b, w, S0, dout, dS_T=None, *, scale=None,
         if saved:
             raise ValueError("saved=True needs the workspace of the saving forward")
         ws = torch.empty(need, dtype=torch.uint8, device=dev)
+    _require_ws(ws, need, dev)
+    _require_grads(g, {"dq": (q.shape, q.dtype), "dk": (k.shape, q.dtype), "dv": (v.shape, q.dtype),
+                       "dlog_alpha": (log_alpha.shape, torch.float32), "db": (b.shape, q.dtype),
+                       "dw": (w.shape, q.dtype), "dS0": ((B, H, Dk, Dv), torch.float32)}, dev)
     fn = lib().gdr2_chunk_bwd_saved if saved else lib().gdr2_chunk_bwd
-    st = fn(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(b),
-                              _ptr(w), _ptr(S0), _ptr(dout), _ptr(dS_T), _ptr(g["dq"]), _ptr(g["dk"]),
-                              _ptr(g["dv"]), _ptr(g["dlog_alpha"]), _ptr(g["db"]), _ptr(g["dw"]),
-                              _ptr(g["dS0"]), _ptr(ws), ws.numel(), _stream())
+    with _on(q):
+        st = fn(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(b),
+                                  _ptr(w), _ptr(S0), _ptr(dout), _ptr(dS_T), _ptr(g["dq"]), _ptr(g["dk"]),
+                                  _ptr(g["dv"]), _ptr(g["dlog_alpha"]), _ptr(g["db"]), _ptr(g["dw"]),
+                                  _ptr(g["dS0"]), _ptr(ws), ws.numel(), _stream())
     _check(st, "gdr2_chunk_bwd_saved" if saved else "gdr2_chunk_bwd")
     return g
 
@@ -251,22 +285,24 @@ def gdr2_recurrent_step(q, k, v, log_alpha, b, w, S, *, scale=None, o=None):
     """Token-by-token forward over q.shape[1] tokens; S (fp32) updated in place.  Returns o."""
     torch = _torch()
     B, T, H, Dk, Dv = _validate(q, k, v, log_alpha, b, w)
-    _require("S", S, (B, H, Dk, Dv), torch.float32)
+    _require("S", S, (B, H, Dk, Dv), torch.float32, q.device)
     prob = _problem(q, v, scale)
     if o is None:
         o = torch.empty((B, T, H, Dv), dtype=q.dtype, device=q.device)
-    st = lib().gdr2_recurrent_step(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha),
-                                   _ptr(b), _ptr(w), _ptr(S), _ptr(o), _stream())
+    _require("o", o, (B, T, H, Dv), q.dtype, q.device)
+    with _on(q):
+        st = lib().gdr2_recurrent_step(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha),
+                                       _ptr(b), _ptr(w), _ptr(S), _ptr(o), _stream())
     _check(st, "gdr2_recurrent_step")
     return o
 
 
 # --------------------------------------------------------------------------- packed sequences
-def _cu(cu_seqlens, T):
+def _cu(cu_seqlens, T, device=None):
     torch = _torch()
     if cu_seqlens.dim() != 1 or cu_seqlens.numel() < 2:
         raise ValueError("cu_seqlens: expected a 1-D tensor of n_seqs + 1 offsets")
-    _require("cu_seqlens", cu_seqlens, (cu_seqlens.numel(),), torch.int32)
+    _require("cu_seqlens", cu_seqlens, (cu_seqlens.numel(),), torch.int32, device)
     return cu_seqlens.numel() - 1
 
 
@@ -285,23 +321,25 @@ def gdr2_chunk_fwd_varlen(q, k, v, log_alpha, b, w, cu_seqlens, S0=None, *, scal
     (n_seqs, H, Dk, Dv).  Returns (o, S_T); save=True as in gdr2_chunk_fwd."""
     torch = _torch()
     B, T, H, Dk, Dv = _validate(q, k, v, log_alpha, b, w)
-    N = _cu(cu_seqlens, T)
-    _require("S0", S0, (N, H, Dk, Dv), torch.float32)
+    N = _cu(cu_seqlens, T, q.device)
+    _require("S0", S0, (N, H, Dk, Dv), torch.float32, q.device)
     prob = _problem(q, v, scale)
     if o is None:
         o = torch.empty((B, T, H, Dv), dtype=q.dtype, device=q.device)
-    _require("o", o, (B, T, H, Dv), q.dtype)
+    _require("o", o, (B, T, H, Dv), q.dtype, q.device)
     if S_T is None and want_state:
         S_T = torch.empty((N, H, Dk, Dv), dtype=torch.float32, device=q.device)
-    _require("S_T", S_T, (N, H, Dk, Dv), torch.float32)
+    _require("S_T", S_T, (N, H, Dk, Dv), torch.float32, q.device)
     need = gdr2_varlen_workspace_bytes(prob, N, 1 if save else 0)
     if ws is None:
         if save:
             raise ValueError("save=True needs the workspace that the backward will read")
         ws = torch.empty(need, dtype=torch.uint8, device=q.device)
-    st = lib().gdr2_chunk_fwd_varlen(ctypes.byref(prob), _ptr(cu_seqlens), N, _ptr(q), _ptr(k), _ptr(v),
-                                     _ptr(log_alpha), _ptr(b), _ptr(w), _ptr(S0), _ptr(o), _ptr(S_T), _ptr(ws),
-                                     ws.numel(), 1 if save else 0, _stream())
+    _require_ws(ws, need, q.device)
+    with _on(q):
+        st = lib().gdr2_chunk_fwd_varlen(ctypes.byref(prob), _ptr(cu_seqlens), N, _ptr(q), _ptr(k), _ptr(v),
+                                         _ptr(log_alpha), _ptr(b), _ptr(w), _ptr(S0), _ptr(o), _ptr(S_T), _ptr(ws),
+                                         ws.numel(), 1 if save else 0, _stream())
     _check(st, "gdr2_chunk_fwd_varlen")
     return o, S_T
 
@@ -311,10 +349,10 @@ def gdr2_chunk_bwd_varlen(q, k, v, log_alpha, b, w, cu_seqlens, S0, dout, dS_T=N
     """Backward of a packed batch; returns dict dq, dk, dv, dlog_alpha, db, dw, dS0."""
     torch = _torch()
     B, T, H, Dk, Dv = _validate(q, k, v, log_alpha, b, w)
-    N = _cu(cu_seqlens, T)
-    _require("S0", S0, (N, H, Dk, Dv), torch.float32)
-    _require("dout", dout, (B, T, H, Dv), q.dtype)
-    _require("dS_T", dS_T, (N, H, Dk, Dv), torch.float32)
+    N = _cu(cu_seqlens, T, q.device)
+    _require("S0", S0, (N, H, Dk, Dv), torch.float32, q.device)
+    _require("dout", dout, (B, T, H, Dv), q.dtype, q.device)
+    _require("dS_T", dS_T, (N, H, Dk, Dv), torch.float32, q.device)
     prob = _problem(q, v, scale)
     g = dict(grads or {})
     for n, like in (("dq", q), ("dk", k), ("dv", v), ("dlog_alpha", log_alpha), ("db", b), ("dw", w)):
@@ -328,11 +366,16 @@ def gdr2_chunk_bwd_varlen(q, k, v, log_alpha, b, w, cu_seqlens, S0, dout, dS_T=N
         if saved:
             raise ValueError("saved=True needs the workspace of the saving forward")
         ws = torch.empty(need, dtype=torch.uint8, device=q.device)
-    st = lib().gdr2_chunk_bwd_varlen(ctypes.byref(prob), _ptr(cu_seqlens), N, _ptr(q), _ptr(k), _ptr(v),
-                                     _ptr(log_alpha), _ptr(b), _ptr(w), _ptr(S0), _ptr(dout), _ptr(dS_T),
-                                     _ptr(g["dq"]), _ptr(g["dk"]), _ptr(g["dv"]), _ptr(g["dlog_alpha"]),
-                                     _ptr(g["db"]), _ptr(g["dw"]), _ptr(g["dS0"]), _ptr(ws), ws.numel(),
-                                     1 if saved else 0, _stream())
+    _require_ws(ws, need, q.device)
+    _require_grads(g, {"dq": (q.shape, q.dtype), "dk": (k.shape, q.dtype), "dv": (v.shape, q.dtype),
+                       "dlog_alpha": (log_alpha.shape, torch.float32), "db": (b.shape, q.dtype),
+                       "dw": (w.shape, q.dtype), "dS0": ((N, H, Dk, Dv), torch.float32)}, q.device)
+    with _on(q):
+        st = lib().gdr2_chunk_bwd_varlen(ctypes.byref(prob), _ptr(cu_seqlens), N, _ptr(q), _ptr(k), _ptr(v),
+                                         _ptr(log_alpha), _ptr(b), _ptr(w), _ptr(S0), _ptr(dout), _ptr(dS_T),
+                                         _ptr(g["dq"]), _ptr(g["dk"]), _ptr(g["dv"]), _ptr(g["dlog_alpha"]),
+                                         _ptr(g["db"]), _ptr(g["dw"]), _ptr(g["dS0"]), _ptr(ws), ws.numel(),
+                                         1 if saved else 0, _stream())
     _check(st, "gdr2_chunk_bwd_varlen")
     return g
 
@@ -341,13 +384,15 @@ def gdr2_recurrent_varlen(q, k, v, log_alpha, b, w, cu_seqlens, S, *, scale=None
     """Token-by-token forward of a packed batch; S (n_seqs, H, Dk, Dv) updated in place.  Returns o."""
     torch = _torch()
     B, T, H, Dk, Dv = _validate(q, k, v, log_alpha, b, w)
-    N = _cu(cu_seqlens, T)
-    _require("S", S, (N, H, Dk, Dv), torch.float32)
+    N = _cu(cu_seqlens, T, q.device)
+    _require("S", S, (N, H, Dk, Dv), torch.float32, q.device)
     prob = _problem(q, v, scale)
     if o is None:
         o = torch.empty((B, T, H, Dv), dtype=q.dtype, device=q.device)
-    st = lib().gdr2_recurrent_varlen(ctypes.byref(prob), _ptr(cu_seqlens), N, _ptr(q), _ptr(k), _ptr(v),
-                                     _ptr(log_alpha), _ptr(b), _ptr(w), _ptr(S), _ptr(o), _stream())
+    _require("o", o, (B, T, H, Dv), q.dtype, q.device)
+    with _on(q):
+        st = lib().gdr2_recurrent_varlen(ctypes.byref(prob), _ptr(cu_seqlens), N, _ptr(q), _ptr(k), _ptr(v),
+                                         _ptr(log_alpha), _ptr(b), _ptr(w), _ptr(S), _ptr(o), _stream())
     _check(st, "gdr2_recurrent_varlen")
     return o
 
@@ -367,10 +412,10 @@ def gdr2_profile_collect():
 
 
 # --------------------------------------------------------------------------- fused input stage
-def _stage(a_log, delta, H, Dk, eps):
+def _stage(a_log, delta, H, Dk, eps, device):
     torch = _torch()
-    _require("a_log", a_log, (H,), torch.float32)
-    _require("delta", delta, (H, Dk), torch.float32)
+    _require("a_log", a_log, (H,), torch.float32, device)
+    _require("delta", delta, (H, Dk), torch.float32, device)
     return Gdr2Stage(a_log.data_ptr(), delta.data_ptr(), float(eps))
 
 
@@ -384,7 +429,7 @@ def gdr2_fused_workspace_bytes(problem, n_seqs, for_backward):
 
 def _fused_shapes(q, k, v, f, b, w, cu_seqlens):
     B, T, H, Dk, Dv = _validate(q, k, v, f, b, w)
-    N = _cu(cu_seqlens, T) if cu_seqlens is not None else 0
+    N = _cu(cu_seqlens, T, q.device) if cu_seqlens is not None else 0
     return B, T, H, Dk, Dv, N
 
 
@@ -395,22 +440,24 @@ def gdr2_fused_fwd(q, k, v, f, a_log, delta, b, w, S0=None, *, cu_seqlens=None, 
     torch = _torch()
     B, T, Hv, Dk, Dv, N = _fused_shapes(q, k, v, f, b, w, cu_seqlens)
     NS = N if N > 0 else B
-    stg = _stage(a_log, delta, q.shape[2], Dk, eps)
-    _require("S0", S0, (NS, Hv, Dk, Dv), torch.float32)
+    stg = _stage(a_log, delta, q.shape[2], Dk, eps, q.device)
+    _require("S0", S0, (NS, Hv, Dk, Dv), torch.float32, q.device)
     prob = _problem(q, v, scale)
     if o is None:
         o = torch.empty((B, T, Hv, Dv), dtype=q.dtype, device=q.device)
-    _require("o", o, (B, T, Hv, Dv), q.dtype)
+    _require("o", o, (B, T, Hv, Dv), q.dtype, q.device)
     if S_T is None and want_state:
         S_T = torch.empty((NS, Hv, Dk, Dv), dtype=torch.float32, device=q.device)
-    _require("S_T", S_T, (NS, Hv, Dk, Dv), torch.float32)
+    _require("S_T", S_T, (NS, Hv, Dk, Dv), torch.float32, q.device)
     if ws is None:
         if save:
             raise ValueError("save=True needs the workspace that the backward will read")
         ws = torch.empty(gdr2_fused_workspace_bytes(prob, N, 0), dtype=torch.uint8, device=q.device)
-    st = lib().gdr2_fused_fwd(ctypes.byref(prob), ctypes.byref(stg), _ptr(cu_seqlens), N, _ptr(q), _ptr(k),
-                              _ptr(v), _ptr(f), _ptr(b), _ptr(w), _ptr(S0), _ptr(o), _ptr(S_T), _ptr(ws),
-                              ws.numel(), 1 if save else 0, _stream())
+    _require_ws(ws, gdr2_fused_workspace_bytes(prob, N, 1 if save else 0), q.device)
+    with _on(q):
+        st = lib().gdr2_fused_fwd(ctypes.byref(prob), ctypes.byref(stg), _ptr(cu_seqlens), N, _ptr(q), _ptr(k),
+                                  _ptr(v), _ptr(f), _ptr(b), _ptr(w), _ptr(S0), _ptr(o), _ptr(S_T), _ptr(ws),
+                                  ws.numel(), 1 if save else 0, _stream())
     _check(st, "gdr2_fused_fwd")
     return o, S_T
 
@@ -423,10 +470,10 @@ def gdr2_fused_bwd(q, k, v, f, a_log, delta, b, w, S0, dout, dS_T=None, *, cu_se
     B, T, Hv, Dk, Dv, N = _fused_shapes(q, k, v, f, b, w, cu_seqlens)
     NS = N if N > 0 else B
     H = q.shape[2]
-    stg = _stage(a_log, delta, H, Dk, eps)
-    _require("S0", S0, (NS, Hv, Dk, Dv), torch.float32)
-    _require("dout", dout, (B, T, Hv, Dv), q.dtype)
-    _require("dS_T", dS_T, (NS, Hv, Dk, Dv), torch.float32)
+    stg = _stage(a_log, delta, H, Dk, eps, q.device)
+    _require("S0", S0, (NS, Hv, Dk, Dv), torch.float32, q.device)
+    _require("dout", dout, (B, T, Hv, Dv), q.dtype, q.device)
+    _require("dS_T", dS_T, (NS, Hv, Dk, Dv), torch.float32, q.device)
     prob = _problem(q, v, scale)
     g = dict(grads or {})
     for n, like in (("dq", q), ("dk", k), ("dv", v), ("df", f), ("db", b), ("dw", w), ("da", a_log),
@@ -440,11 +487,17 @@ def gdr2_fused_bwd(q, k, v, f, a_log, delta, b, w, S0, dout, dS_T=None, *, cu_se
         if saved:
             raise ValueError("saved=True needs the workspace of the saving forward")
         ws = torch.empty(gdr2_fused_workspace_bytes(prob, N, 1), dtype=torch.uint8, device=q.device)
-    st = lib().gdr2_fused_bwd(ctypes.byref(prob), ctypes.byref(stg), _ptr(cu_seqlens), N, _ptr(q), _ptr(k),
-                              _ptr(v), _ptr(f), _ptr(b), _ptr(w), _ptr(S0), _ptr(dout), _ptr(dS_T), _ptr(g["dq"]),
-                              _ptr(g["dk"]), _ptr(g["dv"]), _ptr(g["df"]), _ptr(g["da"]), _ptr(g["ddelta"]),
-                              _ptr(g["db"]), _ptr(g["dw"]), _ptr(g["dS0"]), _ptr(ws), ws.numel(),
-                              1 if saved else 0, _stream())
+    _require_ws(ws, gdr2_fused_workspace_bytes(prob, N, 1), q.device)
+    _require_grads(g, {"dq": (q.shape, q.dtype), "dk": (k.shape, q.dtype), "dv": (v.shape, q.dtype),
+                       "df": (f.shape, torch.float32), "db": (b.shape, q.dtype), "dw": (w.shape, q.dtype),
+                       "da": (a_log.shape, torch.float32), "ddelta": (delta.shape, torch.float32),
+                       "dS0": ((NS, Hv, Dk, Dv), torch.float32)}, q.device)
+    with _on(q):
+        st = lib().gdr2_fused_bwd(ctypes.byref(prob), ctypes.byref(stg), _ptr(cu_seqlens), N, _ptr(q), _ptr(k),
+                                  _ptr(v), _ptr(f), _ptr(b), _ptr(w), _ptr(S0), _ptr(dout), _ptr(dS_T), _ptr(g["dq"]),
+                                  _ptr(g["dk"]), _ptr(g["dv"]), _ptr(g["df"]), _ptr(g["da"]), _ptr(g["ddelta"]),
+                                  _ptr(g["db"]), _ptr(g["dw"]), _ptr(g["dS0"]), _ptr(ws), ws.numel(),
+                                  1 if saved else 0, _stream())
     _check(st, "gdr2_fused_bwd")
     return g
 
@@ -454,12 +507,14 @@ def gdr2_fused_recurrent(q, k, v, f, a_log, delta, b, w, S, *, cu_seqlens=None, 
     torch = _torch()
     B, T, Hv, Dk, Dv, N = _fused_shapes(q, k, v, f, b, w, cu_seqlens)
     NS = N if N > 0 else B
-    stg = _stage(a_log, delta, q.shape[2], Dk, eps)
-    _require("S", S, (NS, Hv, Dk, Dv), torch.float32)
+    stg = _stage(a_log, delta, q.shape[2], Dk, eps, q.device)
+    _require("S", S, (NS, Hv, Dk, Dv), torch.float32, q.device)
     prob = _problem(q, v, scale)
     if o is None:
         o = torch.empty((B, T, Hv, Dv), dtype=q.dtype, device=q.device)
-    st = lib().gdr2_fused_recurrent(ctypes.byref(prob), ctypes.byref(stg), _ptr(cu_seqlens), N, _ptr(q), _ptr(k),
-                                    _ptr(v), _ptr(f), _ptr(b), _ptr(w), _ptr(S), _ptr(o), _stream())
+    _require("o", o, (B, T, Hv, Dv), q.dtype, q.device)
+    with _on(q):
+        st = lib().gdr2_fused_recurrent(ctypes.byref(prob), ctypes.byref(stg), _ptr(cu_seqlens), N, _ptr(q), _ptr(k),
+                                        _ptr(v), _ptr(f), _ptr(b), _ptr(w), _ptr(S), _ptr(o), _stream())
     _check(st, "gdr2_fused_recurrent")
     return o

@@ -205,6 +205,39 @@ def test_degenerate_gates(dtype, case):
         assert not np.any(ref["dv"])
 
 
+def test_binding_refuses_bad_buffers():
+    """Buffers that would send a kernel out of bounds are refused by the binding
+    before any launch: a gradient buffer of the wrong shape or dtype, a
+    workspace on the host, of the wrong dtype or too small, an output of the
+    wrong shape."""
+    import torch
+    import paper_2605_22791_amd as g2
+    d = make_inputs(1, 64, 2, 64, 64, seed=72, dtype="bf16")
+    x = dev_inputs(d)
+    args = [x[n] for n in ("q", "k", "v", "log_alpha", "b", "w")]
+    _case("binding: bad buffers refused")
+    bad_grads = ({"dq": torch.empty(1, 64, 2, 32, dtype=torch.bfloat16, device="cuda")},
+                 {"dlog_alpha": torch.empty(1, 64, 2, 64, dtype=torch.bfloat16, device="cuda")},
+                 {"dS0": torch.empty(1, 2, 64, 32, dtype=torch.float32, device="cuda")})
+    for g in bad_grads:
+        with pytest.raises(ValueError):
+            g2.gdr2_chunk_bwd(*args, None, x["do"], scale=d["scale"], grads=g)
+    prob = g2._problem(x["q"], x["v"], d["scale"])
+    need = g2.gdr2_chunk_workspace_bytes(prob, 0)
+    for ws in (torch.empty(need, dtype=torch.uint8),
+               torch.empty(need, dtype=torch.float32, device="cuda"),
+               torch.empty(need - 1, dtype=torch.uint8, device="cuda")):
+        with pytest.raises(ValueError):
+            g2.gdr2_chunk_fwd(*args, scale=d["scale"], ws=ws)
+    S = torch.zeros(1, 2, 64, 64, dtype=torch.float32, device="cuda")
+    with pytest.raises(ValueError):
+        g2.gdr2_recurrent_step(*args, S, scale=d["scale"], o=torch.empty(1, 64, 2, 32, dtype=torch.bfloat16,
+                                                                          device="cuda"))
+    # the same call with correct buffers runs
+    o, _ = g2.gdr2_chunk_fwd(*args, scale=d["scale"], ws=torch.empty(need, dtype=torch.uint8, device="cuda"))
+    assert torch.isfinite(o.float()).all()
+
+
 def test_bf16_backward_single_chunk_no_state():
     d = make_inputs(1, 64, 2, 128, 128, seed=65, dtype="bf16")
     _case("bf16 bwd one chunk, S0 = 0, dS_T = 0")
