@@ -172,14 +172,6 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
   for (int n = n1 - 1; n >= n0; --n) {
     const size_t ch = chs + n;
     if (n > n0) GDR2_LOAD_CHUNK(n - 1)
-    // gradient of this chunk's end state
-    if (a.DH) {
-#pragma unroll
-      for (int t = 0; t < TPW; ++t)
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-          a.DH[(ch * DK + 16 * cs + 4 * g + u) * DV + v0 + 16 * (sv0 + t) + r16] = sreg[t][u];
-    }
 
     // ---- dR = scale * A_qk^T dO + Ktail dS   (tiles: row block iO, value blocks vbO..)
     f4 racc[NVB / 2], aacc[NVB / 2];
@@ -225,6 +217,14 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
         const int vb = vbO + t;
         aacc[t] = mma2a(af, ld_tr8(sdO, LDO, 32 * kb, 16 * vb, lane), aacc[t]);
       }
+    }
+    // gradient of this chunk's end state (sreg is not updated before the barrier below)
+    if (a.DH) {
+#pragma unroll
+      for (int t = 0; t < TPW; ++t)
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          a.DH[(ch * DK + 16 * cs + 4 * g + u) * DV + v0 + 16 * (sv0 + t) + r16] = sreg[t][u];
     }
     const float sc = a.scale;
 #pragma unroll
