@@ -227,20 +227,14 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
           a.DH[(ch * DK + 16 * cs + 4 * g + u) * DV + v0 + 16 * (sv0 + t) + r16] = sreg[t][u];
     }
     const float sc = a.scale;
+    f4 rkeep[NVB / 2];
 #pragma unroll
     for (int t = 0; t < NVB / 2; ++t) {
       const int vb = vbO + t;
-      f4 r;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) r[u] = racc[t][u] + sc * aacc[t][u];
-      st4split(sRhi + (16 * vb + r16) * LDR + 16 * iO + 4 * g, sRlo + (16 * vb + r16) * LDR + 16 * iO + 4 * g, r);
-      // dR as permuted fragment blocks (row = value, K = chunk row): this lane's
-      // four rows 16 iO + 4 g + u are half of its 16-byte slot
-      if (a.DR) {
-        const size_t doff = ch * WsBf16::dr(DV) + (size_t)((v0 / 16 + vb) * 2 + (iO >> 1)) * 2048 + 16 * lane +
-                            8 * (iO & 1);
-        st4split(reinterpret_cast<__bf16*>(a.DR + doff), reinterpret_cast<__bf16*>(a.DR + doff + 1024), r);
-      }
+      for (int u = 0; u < 4; ++u) rkeep[t][u] = racc[t][u] + sc * aacc[t][u];
+      st4split(sRhi + (16 * vb + r16) * LDR + 16 * iO + 4 * g, sRlo + (16 * vb + r16) * LDR + 16 * iO + 4 * g,
+               rkeep[t]);
     }
     __syncthreads();
 
@@ -288,6 +282,18 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
     for (int t = 0; t < TPW; ++t)
 #pragma unroll
       for (int u = 0; u < 4; ++u) sreg[t][u] += sc * qacc[t][u];
+    // dR as permuted fragment blocks (row = value, K = chunk row): this lane's
+    // four rows 16 iO + 4 g + u are half of its 16-byte slot.  Like the dh
+    // stores, these leave after the chunk's products are issued.
+    if (a.DR) {
+#pragma unroll
+      for (int t = 0; t < NVB / 2; ++t) {
+        const int vb = vbO + t;
+        const size_t doff = ch * WsBf16::dr(DV) + (size_t)((v0 / 16 + vb) * 2 + (iO >> 1)) * 2048 + 16 * lane +
+                            8 * (iO & 1);
+        st4split(reinterpret_cast<__bf16*>(a.DR + doff), reinterpret_cast<__bf16*>(a.DR + doff + 1024), rkeep[t]);
+      }
+    }
     __syncthreads();
 
 #pragma unroll

@@ -198,14 +198,11 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
       const int vb = vbO + t;
       st4split(sRhi + (16 * vb + r16) * LR + 16 * iO + 4 * g, sRlo + (16 * vb + r16) * LR + 16 * iO + 4 * g,
                racc[t]);
-      if (STORE_H) {
-#pragma unroll
-        for (int u = 0; u < 4; ++u) a.Rs[(ch * CH + 16 * iO + 4 * g + u) * DV + v0 + 16 * vb + r16] = racc[t][u];
-      }
     }
     // the next chunk's operands are fetched only now: a fetch issued before R
     // would be drained by the wait that frees the registers of the previous
-    // chunk's stores (one vmcnt counts loads and stores alike)
+    // chunk's stores (one vmcnt counts loads and stores alike); R itself goes
+    // to the workspace at the end of the step, behind this chunk's products
     if (n + 1 < n1) {
       GDR2_LOAD_OPS(chk + n + 1)
       GDR2_LOAD_UG(ch + 1, chk + n + 1, unext, gnext)
@@ -299,6 +296,13 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int t = 0; t < TPW; ++t) sreg[t] = mma3(kf[kb], rfs[kb][t], sreg[t]);
+    }
+    if (STORE_H) {
+#pragma unroll
+      for (int t = 0; t < NVB / 2; ++t)
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          a.Rs[(ch * CH + 16 * iO + 4 * g + u) * DV + v0 + 16 * (vbO + t) + r16] = racc[t][u];
     }
     __syncthreads();
 
