@@ -179,6 +179,14 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
 
   for (int n = n0; n < n1; ++n) {
     const size_t ch = chs + n;
+    // the next chunk's operands, fetched first: one vmcnt counts loads and
+    // stores in issue order, so waiting for these also waits for every store
+    // issued before them; this step's stores (R, O, h) therefore come after
+    // its products, and the previous step's have had that whole step
+    if (n + 1 < n1) {
+      GDR2_LOAD_OPS(chk + n + 1)
+      GDR2_LOAD_UG(ch + 1, chk + n + 1, unext, gnext)
+    }
 
     // ---- R = U - Y S
     f4 racc[NVB / 2];
@@ -198,14 +206,6 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
       const int vb = vbO + t;
       st4split(sRhi + (16 * vb + r16) * LR + 16 * iO + 4 * g, sRlo + (16 * vb + r16) * LR + 16 * iO + 4 * g,
                racc[t]);
-    }
-    // the next chunk's operands are fetched only now: a fetch issued before R
-    // would be drained by the wait that frees the registers of the previous
-    // chunk's stores (one vmcnt counts loads and stores alike); R itself goes
-    // to the workspace at the end of the step, behind this chunk's products
-    if (n + 1 < n1) {
-      GDR2_LOAD_OPS(chk + n + 1)
-      GDR2_LOAD_UG(ch + 1, chk + n + 1, unext, gnext)
     }
     __syncthreads();
 
