@@ -69,6 +69,44 @@ def kernel_model(B, T, H, Dk, Dv, stored=True):
     return {k: (fl * NC, by * NC) for k, (fl, by) in m.items()}
 
 
+def method_bytes(B, T, H, Dk, Dv):
+    """The method's own HBM bytes per launch of each kernel of the bf16 path:
+    what the kernel's step of the chunkwise algorithm must move at the least,
+    with model-dtype (bf16) operands and fp32 log-decay and state, counted per
+    token-head and multiplied by the B * T * H token-heads of one launch.
+
+      fwd_intra  (Gram, solve, auxiliaries; Sec. 3.3, App. C.2): reads q, k, b,
+                 v, w (bf16) and g (fp32) = 14 d, writes A_qk (bf16, C values
+                 per token) and Y, U (bf16) = 2 C + 4 d          -> 2432 B at d = 128
+      fwd_state  (state recurrence with the output fused): reads Y, U, K_tail
+                 (bf16, 6 d), writes the chunk states (fp32, 4 d^2 / C per
+                 token) and R (bf16, 2 d); the output adds Q_g, A_qk in and
+                 o out (2 d + 2 C + 2 d)                         -> 2688 B
+      bwd_state  (reverse state recurrence): reads Y, K_tail, Q_g, dO (bf16,
+                 8 d) and A_qk (2 C), writes the chunk-state gradients (fp32,
+                 4 d^2 / C) and dR (bf16, 2 d)                   -> 2432 B
+      bwd_intra  (gate-aware WY VJP and intra-chunk VJP): the backward's own
+                 I/O, q, k, v, b, w, dO in (bf16) and g in (fp32) = 16 d,
+                 dq, dk, dv, db, dw out (bf16) and dlog_alpha out (fp32) = 14 d
+                                                                  -> 3840 B
+    These are the per-token figures of the flop and byte accounting of the
+    chunkwise form (App. B's products and each step's operands); the
+    decomposition's own stored intermediates (split planes, fp32 U and R, the
+    per-chunk states read back by the chunk backward) are counted by
+    kernel_model instead."""
+    C = 64
+    d = Dk
+    per = {
+        "fwd_intra": 14 * d + 2 * C + 4 * d,
+        "fwd_state": 6 * d + 4 * Dk * Dv // C + 2 * Dv + (2 * d + 2 * C + 2 * Dv),
+        "bwd_state": 8 * d + 2 * C + 4 * Dk * Dv // C + 2 * Dv,
+        "bwd_intra": 30 * d,
+    }
+    per["bwd_recompute_intra"] = per["fwd_intra"]
+    per["bwd_recompute_state"] = 6 * d + 4 * Dk * Dv // C + 2 * Dv
+    return {k: v * B * T * H for k, v in per.items()}
+
+
 KERNEL_SOURCES = {"fwd_intra": "gdr2_intra_bf16.hip", "bwd_recompute_intra": "gdr2_intra_bf16.hip",
                   "fwd_state": "gdr2_scan_bf16.hip", "bwd_recompute_state": "gdr2_scan_bf16.hip",
                   "bwd_state": "gdr2_bscan_bf16.hip", "bwd_intra": "gdr2_bchunk_bf16.hip"}
@@ -140,7 +178,8 @@ def cpu_baseline(d, heads_sample):
     H = d["H"]
     tokens = d["T"] * heads_sample / H           # token = one (b, t) position across all H heads
     fwd_share = sum(p[0] for p in parts) / max(1e-12, sum(p[0] + p[1] for p in parts))
-    return {"value": tokens / wall, "unit": "tokens/s", "cores": workers, "kind": "oracle",
+    return {"value": tokens / wall, "unit": "tokens/s", "cores": workers, "workers": workers,
+            "host_cores": ncores, "kind": "oracle",
             "sample": f"fp64 numpy token recurrence + adjoint, batch row 0, {heads_sample} of {H} heads, "
                       f"T={d['T']} (= {tokens:.0f} tokens of the workload), {workers} single-threaded workers",
             "wall_s": wall, "fwd_value": tokens / (wall * fwd_share)}
@@ -231,13 +270,13 @@ def config3_bench(steps=3, stored=True):
     per_kernel = g2.gdr2_profile_collect()
     g2.gdr2_profile_enable(False)
     ms = e0.elapsed_time(e1) / steps
-    model = kernel_model(B, T, H, Dk, Dv, stored)
+    mbytes = method_bytes(B, T, H, Dk, Dv)
     kern = {}
     for name, (kms, cnt) in per_kernel.items():
         if cnt:
             avg = kms / cnt
             kern[name] = {"avg_us": round(avg * 1e3, 1),
-                          "hbm_frac": round(model[name][1] / (avg * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+                          "hbm_frac": round(mbytes[name] / (avg * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
     return {"workload": "B1 H16 T65536 d128 bf16, S0 != 0", "training_path": "stored" if stored else "recompute",
             "ms_per_step": ms, "tokens_per_s": B * T / (ms * 1e-3), "kernels": kern}
 
@@ -509,14 +548,20 @@ def main():
     print(f"[bench] {ms_step:.3f} ms/step ({wall / args.steps * 1e3:.3f} ms wall)", file=sys.stderr, flush=True)
 
     model = kernel_model(B, T, H, Dk, Dv, stored)
+    mbytes = method_bytes(B, T, H, Dk, Dv)
     kern = {}
     for name, (ms, cnt) in per_kernel.items():
         if cnt == 0:
             continue
         avg = ms / cnt
         fl, by = model[name]
-        kern[name] = {"avg_us": avg * 1e3, "launches": cnt, "GBs": by / (avg * 1e-3) / 1e9,
-                      "TFLOPs": fl / (avg * 1e-3) / 1e12, "alg_bytes": by, "alg_flops": fl}
+        mb = mbytes[name]
+        traffic = measured_traffic(name)
+        kern[name] = {"avg_us": avg * 1e3, "launches": cnt, "GBs": mb / (avg * 1e-3) / 1e9,
+                      "hbm_frac": mb / (avg * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                      "TFLOPs": fl / (avg * 1e-3) / 1e12, "alg_bytes": mb, "alg_flops": fl,
+                      "decomposition_bytes": by, "traffic": traffic,
+                      "traffic_GBs": None if traffic is None else traffic / (avg * 1e-3) / 1e9}
     dom = max(kern, key=lambda n: kern[n]["avg_us"] * kern[n]["launches"])
     kd = kern[dom]
     peak_fl = PEAK_TFLOPS[MFMA_DTYPE]
@@ -528,9 +573,11 @@ def main():
     else:
         roof = {"bound": "hbm", "achieved": kd["GBs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": kd["GBs"] / HBM_PEAK_GBS}
-    traffic = measured_traffic(dom)
+    traffic = kd["traffic"]
     roof.update({"traffic": traffic, "kernel": dom, "avg_us": kd["avg_us"],
-                 "alg_bytes": kd["alg_bytes"], "traffic_over_alg": None if traffic is None else traffic / kd["alg_bytes"],
+                 "alg_bytes": kd["alg_bytes"], "decomposition_bytes": kd["decomposition_bytes"],
+                 "traffic_over_alg": None if traffic is None else traffic / kd["alg_bytes"],
+                 "traffic_GBs": kd["traffic_GBs"],
                  "mfma_dtype": MFMA_DTYPE, "arith_intensity": ai, "ridge": ridge})
 
     # the other training path, same number of steps, no per-kernel events

@@ -52,6 +52,10 @@
  *       GDR2_EWORKSPACE    ws_bytes below gdr2_chunk_workspace_bytes();
  *       GDR2_EHIP          a launch reported an error (hipGetLastError).
  *   * No C++ exception crosses this interface.
+ *   * Setting the environment variable GDR2_DEBUG_SYNC=1 (read once, at the
+ *     first call) makes every call wait for its stream after its launches and
+ *     report an asynchronous kernel failure as GDR2_EHIP; it changes no result
+ *     and no schedule.  Nothing else in the environment is read.
  *   * Inputs outside the documented domain (log_alpha > 0, NaN/Inf values)
  *     are not checked; results are then undefined.
  */

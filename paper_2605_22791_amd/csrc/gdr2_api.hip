@@ -85,22 +85,16 @@ constexpr int kParamSplits = 64;  // slot ranges of the first decay-parameter re
 // that are scanned side by side (segment maps, then a short chain over the
 // segments, then the segments again from their true start states).  Segments
 // are doubled while the scan grid stays within one workgroup per compute unit
-// and a segment keeps at least 8 chunks.  GDR2_SCAN_SEGMENTS=<n> overrides the
-// count (1 turns the mode off).
+// and a segment keeps at least 8 chunks.  The rule depends on the problem's
+// shape alone, so a problem always runs the same schedule (and rounds the same
+// way).
 void scan_segments(const gdr2_problem* p, int& nseg, int& seg_len) {
   const int NT = chunks_per_seq(p);
   const long long slices = (long long)p->B * p->H * (p->Dv / 64);
-  static const int forced = [] {
-    const char* e = std::getenv("GDR2_SCAN_SEGMENTS");
-    return e != nullptr ? std::atoi(e) : 0;
-  }();
   int n = 1;
-  if (forced > 0) {
-    n = forced < NT ? forced : NT;
-  } else if (p->dtype == GDR2_BF16 && slices < 128 && NT >= 16) {
+  if (p->dtype == GDR2_BF16 && slices < 128 && NT >= 16) {
     while (slices * n * 2 <= 256 && n * 2 * 8 <= NT) n *= 2;
   }
-  if (p->dtype != GDR2_BF16 || n < 1) n = 1;
   seg_len = (NT + n - 1) / n;
   nseg = (NT + seg_len - 1) / seg_len;
 }

@@ -152,6 +152,32 @@ def make_inputs_device(B, T, H, Dk, Dv, seed, decay_shift=0.0, device="cuda"):
     return out
 
 
+def make_decode_device(steps, B=256, H=16, D=128, seed=4, decay_shift=-2.0, device="cuda"):
+    """Decode inputs for `steps` consecutive one-token calls, drawn on the device
+    with torch's generator (make_inputs' bf16 channel-gate recipe, as in
+    make_inputs_device): q, k, v, b, w bf16 and log_alpha fp32, each of shape
+    (steps, B, 1, H, D), so call t takes x[t].  At B = 256 and 1024 steps every
+    tensor holds 537 M values, which is why they are not drawn on the host."""
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+    bf = torch.bfloat16
+    shape = (steps, B, 1, H, D)
+
+    def normal():
+        return torch.randn(shape, generator=gen, device=device, dtype=torch.float32)
+
+    def unit_rows(x):
+        return (x / torch.sqrt((x * x).sum(dim=-1, keepdim=True))).to(bf)
+
+    out = dict(q=unit_rows(normal()), k=unit_rows(normal()), v=normal().to(bf))
+    out["log_alpha"] = -torch.nn.functional.softplus(normal() + decay_shift)
+    out["b"] = torch.sigmoid(normal()).to(bf)
+    out["w"] = torch.sigmoid(normal()).to(bf)
+    out["scale"] = float(1.0 / np.sqrt(D))
+    return out
+
+
 # The five workloads (shape, precision, distributions).  Seeds: config i uses seed i.
 CONFIGS = {
     0: dict(B=1, H=2, T=256, Dk=64, Dv=64, dtype="fp32", decay_shift=0.0, s0_std=0.0,

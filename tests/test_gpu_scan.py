@@ -1,9 +1,11 @@
 """GPU parity of the bf16 fused chunkwise scan (forward) against the fp64 oracle.
 
-The bf16 path rounds only the Gram T, the solve side of A and Y (App. D's
-model-dtype auxiliaries) to bfloat16; every other product is fp32-accurate, so
-the fp32-typed final state S_T must stay well inside the 2e-3 bound: these
-tests hold it to 1e-3 (o is bounded by its own bf16 rounding, ~1.66e-3).
+Precision of the bf16 path: Y is stored in bfloat16 (App. D's model-dtype
+auxiliaries) and Y S reads the bf16 part of the state; every other product,
+the Gram T and A's products into Y and U included, is fp32-accurate (split
+hi/lo bf16), and the solve runs in fp32.  The fp32-typed final state S_T must
+therefore stay well inside the 2e-3 bound: these tests hold it to 1e-3 (o is
+bounded by its own bf16 rounding, ~1.66e-3).
 """
 
 import numpy as np
@@ -98,8 +100,10 @@ def test_bf16_state_passing():
 @pytest.mark.parametrize("Dk,Dv", [(64, 128), (128, 128)])
 def test_bf16_workspace_intermediates(Dk, Dv):
     """Fragment-ordered workspace of the intra-chunk kernel against App. A's chunk
-    algebra: Q_g, Ktail, A_qk, gamma_C are fp32-accurate (split hi/lo); Y and U
-    carry the bf16 solve side of A (and Y its own bf16 storage)."""
+    algebra: Q_g, Ktail, A_qk, gamma_C are fp32-accurate (split hi/lo); U = A Z
+    comes from fp32-accurate products and the fp32 solve, so it stays near fp32
+    rounding (a bf16 operand anywhere in T or A would put it near 1e-3);
+    Y is stored in bf16, so its error is its own rounding (~1.7e-3 rel-L2)."""
     import torch
     from oracle.chunkwise import gdr2_chunk_fwd_ref
     from tests.gpu_common import ws_layout_bf16, decode_frag_blocks, decode_u_tiles, CH
@@ -140,5 +144,5 @@ def test_bf16_workspace_intermediates(Dk, Dv):
     print({k_: f"{v_:.2e}" for k_, v_ in worst.items()})
     for k_ in ("Qg", "Aqk", "Kt", "GC"):
         assert worst[k_] < 1e-4, (k_, worst[k_])
-    for k_ in ("Y", "U"):
-        assert worst[k_] < 1e-2, (k_, worst[k_])
+    assert worst["U"] < 1e-5, worst["U"]   # about 3e-7
+    assert worst["Y"] < 3e-3, worst["Y"]

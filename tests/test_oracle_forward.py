@@ -243,3 +243,30 @@ def test_P12_negative_eigenvalue_reflection_preserves_the_state_norm():
     d2 = {n: (x[:, :2] if isinstance(x, np.ndarray) and x.ndim == 4 and x.shape[1] == 40 else x) for n, x in d.items()}
     _, S2 = _fwd(d2)
     assert rel_l2(S2, S0) < 1e-12
+
+
+def test_P13_scalar_erase_gate_is_KDA_with_rescaled_values():
+    """Table 5's scalar-erase mode, b = beta 1 with a channel-wise w: the update
+    (I - beta k k^T) D S + k (w . v)^T is KDA's (I - beta k k^T) D S + beta k v'^T
+    with v' = (w . v) / beta, so the oracle must equal the independent KDA
+    recurrence run on v'."""
+    d = small_problem(2, 40, 2, 8, 6, seed=12)
+    beta = d["b"].mean(axis=-1)
+    d["b"] = np.ascontiguousarray(np.broadcast_to(beta[..., None], d["b"].shape))
+    o, S = _fwd(d)
+    v_kda = d["w"].astype(np.float64) * d["v"] / beta[..., None]
+    o_k, S_k = limits.kda_fwd(d["q"], d["k"], v_kda, d["log_alpha"], beta, d["S0"], d["scale"])
+    assert rel_l2(o, o_k) < 1e-12
+    assert rel_l2(S, S_k) < 1e-12
+
+
+def test_P13_scalar_write_gate_against_brute_force():
+    """Table 5's scalar-write mode, a channel-wise b with w = omega 1: the oracle
+    against explicit transition products (the write becomes omega k v^T)."""
+    d = small_problem(1, 12, 2, 4, 3, seed=13)
+    omega = d["w"].mean(axis=-1)
+    d["w"] = np.ascontiguousarray(np.broadcast_to(omega[..., None], d["w"].shape))
+    o, S = _fwd(d)
+    o_b, S_b = brute.gdr2_brute_fwd(d["q"], d["k"], d["v"], d["log_alpha"], d["b"], d["w"], d["S0"], d["scale"])
+    assert rel_l2(o, o_b) < 1e-12
+    assert rel_l2(S, S_b) < 1e-12
