@@ -34,7 +34,9 @@
  * Ownership and errors:
  *   * The caller owns every buffer; the library never allocates device memory
  *     and keeps no mutable global state (apart from the opt-in, per-thread
- *     kernel timing at the end of this header), so calls are re-entrant.
+ *     kernel timing at the end of this header, and the fixed per-GPU array of
+ *     gdr2_chunk_fwd_noalloc), so calls are re-entrant (gdr2_chunk_fwd_noalloc:
+ *     see its own rules).
  *     Work is enqueued on `stream` and the call returns without waiting.
  *   * Outputs are overwritten, never accumulated.  Workspace contents are
  *     undefined after a call.  Inputs and outputs must not alias (except S in
@@ -113,6 +115,30 @@ gdr2_status gdr2_chunk_fwd(const gdr2_problem* problem, const void* q, const voi
                            const void* v, const float* log_alpha, const void* b,
                            const void* w, const float* S0, void* o, float* S_T, void* ws,
                            size_t ws_bytes, hipStream_t stream);
+
+/* Maximum workspace of gdr2_chunk_fwd_noalloc: the size of its fixed array. */
+#define GDR2_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): exactly
+ * gdr2_chunk_fwd, with no workspace argument.  Its workspace is one fixed
+ * __device__ array of GDR2_NOALLOC_SCRATCH_BYTES (64 MiB) per GPU, which the
+ * library holds on every GPU it runs on until the process ends; the call
+ * itself allocates nothing and issues no memset.
+ *   * Runs on the current device; `stream` must belong to it.
+ *   * GDR2_EWORKSPACE: the problem needs more than GDR2_NOALLOC_SCRATCH_BYTES
+ *     of workspace (gdr2_chunk_workspace_bytes(p, 0) tells), e.g. more than
+ *     about 450 chunk-heads at Dk = Dv = 128; nothing is launched.
+ *   * Every call on one GPU uses that GPU's array: calls that overlap on one
+ *     GPU (other streams, other threads, without ordering between them) race
+ *     and give undefined results.  Calls ordered on one stream are safe.
+ *   * Other arguments, validation (before any HIP call) and errors as in
+ *     gdr2_chunk_fwd; GDR2_EHIP also when the array's device address cannot be
+ *     looked up. */
+gdr2_status gdr2_chunk_fwd_noalloc(const gdr2_problem* problem, const void* q, const void* k,
+                                   const void* v, const float* log_alpha, const void* b,
+                                   const void* w, const float* S0, void* o, float* S_T,
+                                   hipStream_t stream);
 
 /* Gate-aware chunkwise backward (Sec. 3.4; App. B; App. C.3) of
  *     L = sum_t <o_t, dout_t> + <S_T, dS_T>

@@ -20,12 +20,14 @@ __all__ = [
     "gdr2_recurrent_varlen",
     "gdr2_recurrent_step", "gdr2_status_str", "CHUNK", "KERNEL_NAMES",
     "gdr2_profile_enable", "gdr2_profile_collect", "Gdr2Stage", "gdr2_fused_workspace_bytes",
-    "gdr2_fused_fwd", "gdr2_fused_bwd", "gdr2_fused_recurrent",
+    "gdr2_fused_fwd", "gdr2_fused_bwd", "gdr2_fused_recurrent", "gdr2_chunk_fwd_noalloc",
+    "NOALLOC_SCRATCH_BYTES",
 ]
 
 GDR2_OK, GDR2_EINVAL, GDR2_EUNSUPPORTED, GDR2_EWORKSPACE, GDR2_EHIP = 0, 1, 2, 3, 4
 GDR2_BF16, GDR2_FP32 = 0, 1
 CHUNK = 64
+NOALLOC_SCRATCH_BYTES = 64 << 20   # GDR2_NOALLOC_SCRATCH_BYTES in include/gdr2.h
 # kernel ids of the measurement support (gdr2_kernel_id in include/gdr2.h)
 KERNEL_NAMES = ["fwd_intra", "fwd_state", "bwd_recompute_intra", "bwd_recompute_state",
                 "bwd_state", "bwd_wy", "bwd_intra", "recurrent", "stage_bwd", "stage_fwd"]
@@ -73,6 +75,8 @@ def lib():
         L.gdr2_chunk_fwd.restype = ctypes.c_int
         L.gdr2_chunk_bwd.argtypes = [P] + [vp] * 17 + [ctypes.c_size_t, vp]
         L.gdr2_chunk_bwd.restype = ctypes.c_int
+        L.gdr2_chunk_fwd_noalloc.argtypes = [P] + [vp] * 10
+        L.gdr2_chunk_fwd_noalloc.restype = ctypes.c_int
         L.gdr2_chunk_fwd_save.argtypes = L.gdr2_chunk_fwd.argtypes
         L.gdr2_chunk_fwd_save.restype = ctypes.c_int
         L.gdr2_chunk_bwd_saved.argtypes = L.gdr2_chunk_bwd.argtypes
@@ -236,6 +240,29 @@ def gdr2_chunk_fwd(q, k, v, log_alpha, b, w, S0=None, *, scale=None, o=None, S_T
         st = fn(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha), _ptr(b),
                                   _ptr(w), _ptr(S0), _ptr(o), _ptr(S_T), _ptr(ws), ws.numel(), _stream())
     _check(st, "gdr2_chunk_fwd_save" if save else "gdr2_chunk_fwd")
+    return o, S_T
+
+
+def gdr2_chunk_fwd_noalloc(q, k, v, log_alpha, b, w, S0=None, *, scale=None, o=None, S_T=None,
+                           want_state=True):
+    """Chunkwise GDR-2 forward without a workspace argument (gdr2_chunk_fwd_noalloc:
+    the library's fixed per-GPU array, NOALLOC_SCRATCH_BYTES).  Returns (o, S_T).
+    Pass o (and S_T) to keep the call free of allocations; the C call itself
+    allocates nothing."""
+    torch = _torch()
+    B, T, H, Dk, Dv = _validate(q, k, v, log_alpha, b, w)
+    _require("S0", S0, (B, H, Dk, Dv), torch.float32, q.device)
+    prob = _problem(q, v, scale)
+    if o is None:
+        o = torch.empty((B, T, H, Dv), dtype=q.dtype, device=q.device)
+    _require("o", o, (B, T, H, Dv), q.dtype, q.device)
+    if S_T is None and want_state:
+        S_T = torch.empty((B, H, Dk, Dv), dtype=torch.float32, device=q.device)
+    _require("S_T", S_T, (B, H, Dk, Dv), torch.float32, q.device)
+    with _on(q):
+        st = lib().gdr2_chunk_fwd_noalloc(ctypes.byref(prob), _ptr(q), _ptr(k), _ptr(v), _ptr(log_alpha),
+                                          _ptr(b), _ptr(w), _ptr(S0), _ptr(o), _ptr(S_T), _stream())
+    _check(st, "gdr2_chunk_fwd_noalloc")
     return o, S_T
 
 

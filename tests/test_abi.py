@@ -36,7 +36,8 @@ def test_header_declares_the_entry_points():
                                           "gdr2_chunk_bwd_varlen", "gdr2_recurrent_varlen",
                                           "gdr2_status_str", "gdr2_profile_enable",
                                           "gdr2_profile_collect", "gdr2_fused_workspace_bytes",
-                                          "gdr2_fused_fwd", "gdr2_fused_bwd", "gdr2_fused_recurrent"])
+                                          "gdr2_fused_fwd", "gdr2_fused_bwd", "gdr2_fused_recurrent",
+                                          "gdr2_chunk_fwd_noalloc"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -417,3 +418,42 @@ def test_fused_workspace_size_fp32():
         assert g2.gdr2_fused_workspace_bytes(p, 0, 0) == g2.gdr2_chunk_workspace_bytes(p, 0) + fwd
         bwd = fwd + 3 * r(n * Dk) + r(n) + r(64 * H * (Dk + 1))
         assert g2.gdr2_fused_workspace_bytes(p, 0, 1) == g2.gdr2_chunk_workspace_bytes(p, 1) + bwd
+
+
+def _noalloc(prob, ptrs=None):
+    L = g2.lib()
+    p = [FAKE] * 6 + [None, FAKE, None]
+    if ptrs:
+        for i, val in ptrs.items():
+            p[i] = val
+    pp = ctypes.byref(prob) if prob is not None else None
+    return L.gdr2_chunk_fwd_noalloc(pp, *[ctypes.c_void_p(x) if x else None for x in p], None)
+
+
+def test_noalloc_forward_validation():
+    """gdr2_chunk_fwd_noalloc checks everything before its first HIP call: the
+    problem, every pointer, and that the forward's workspace fits its fixed
+    array (the training shape's 1.08 GB does not: GDR2_EWORKSPACE)."""
+    assert _noalloc(None) == g2.GDR2_EINVAL
+    assert _noalloc(_prob(B=0)) == g2.GDR2_EINVAL
+    assert _noalloc(_prob(Dk=96)) == g2.GDR2_EUNSUPPORTED
+    for idx in (0, 1, 2, 3, 4, 5, 7):
+        assert _noalloc(_prob(), ptrs={idx: None}) == g2.GDR2_EINVAL, idx
+        assert _noalloc(_prob(), ptrs={idx: FAKE + 8}) == g2.GDR2_EINVAL, idx
+    for idx in (6, 8):
+        assert _noalloc(_prob(), ptrs={idx: FAKE + 4}) == g2.GDR2_EINVAL, idx
+    big = _prob(B=8, T=4096, H=16)
+    assert g2.gdr2_chunk_workspace_bytes(big, 0) > g2.NOALLOC_SCRATCH_BYTES
+    assert _noalloc(big) == g2.GDR2_EWORKSPACE
+    # the largest fixed-length problem of this head size that fits, and one chunk more
+    per = g2.gdr2_chunk_workspace_bytes(_prob(B=1, H=1, T=64), 0)
+    n = g2.NOALLOC_SCRATCH_BYTES // per
+    while g2.gdr2_chunk_workspace_bytes(_prob(B=1, H=1, T=64 * n), 0) > g2.NOALLOC_SCRATCH_BYTES:
+        n -= 1
+    assert _noalloc(_prob(B=1, H=1, T=64 * (n + 1))) == g2.GDR2_EWORKSPACE
+
+
+def test_noalloc_scratch_size_matches_header():
+    m = re.search(r"#define\s+GDR2_NOALLOC_SCRATCH_BYTES\s+\(\(size_t\)(\d+)\s*<<\s*(\d+)\)", open(HEADER).read())
+    assert m is not None
+    assert int(m.group(1)) << int(m.group(2)) == g2.NOALLOC_SCRATCH_BYTES
