@@ -466,6 +466,10 @@ def main():
                          "counterpart and print their figures")
     ap.add_argument("--varlen-only", action="store_true",
                     help="time only the packed variable-length batch (32768 tokens, H=16) and print its figures")
+    ap.add_argument("--decode-only", action="store_true",
+                    help="time only the decode leg (1024 one-token calls) and print its figures")
+    ap.add_argument("--decode-batch", type=int, default=256,
+                    help="sequences of the decode leg (256: the 256 MiB fp32 state of the decode workload)")
     ap.add_argument("--long-context-only", action="store_true",
                     help="time only the long-context step (B=1, H=16, T=65536) for --steps steps and print "
                          "its figures (not the benchmark line)")
@@ -474,6 +478,9 @@ def main():
         print(f"bench.py measures one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
               file=sys.stderr)
         sys.exit(2)
+    if args.decode_only:
+        print(json.dumps(decode_bench(1024, B=args.decode_batch)), flush=True)
+        return
     if args.long_context_only:
         print(json.dumps(config3_bench(steps=args.steps, stored=args.path == "stored")), flush=True)
         return

@@ -65,6 +65,7 @@ int varlen_slots(const gdr2_problem* p, int nseq) { return p->T / CH + nseq; }
 struct Layout {
   size_t Y, U, Kt, Qg, Aqk, GC;          // fp32 forward tiles
   size_t Hs, Rs, DH, DR, DAqk, DT, DEg;  // backward extras
+  size_t Hsc, DHsc;                      // bf16 backward: scales of the fp16 chunk states
   size_t bY, bQ, bA, bK, bU, bG;         // bf16 forward (fragment order)
   size_t bDR, bAm;                       // bf16 backward extras (fragment order)
   size_t sM, sN, sX;                     // segment maps and entry states (sequence-parallel scans)
@@ -133,10 +134,24 @@ Layout layout(const gdr2_problem* p, bool bwd, int nseq = 0, int G = 1, bool fus
     L.Aqk = take(NC * CH * CH);
     L.GC = take(NC * Dk);
   }
-  if (bwd) {
+  if (bwd && p->dtype == GDR2_BF16) {
+    // fp16 chunk states with their block scales (store_state_f16), fp32 R
+    auto takeb = [&](size_t bytes) {
+      const size_t at = off;
+      off += round_up(bytes);
+      return at;
+    };
+    L.Hs = takeb(NC * WsBf16::hs(p->Dk, p->Dv));
+    L.Hsc = takeb(NC * WsBf16::hsc(p->Dk, p->Dv));
+    L.Rs = take(NC * CH * Dv);
+    L.DH = takeb(NC * WsBf16::hs(p->Dk, p->Dv));
+    L.DHsc = takeb(NC * WsBf16::hsc(p->Dk, p->Dv));
+  } else if (bwd) {
     L.Hs = take(NC * Dk * Dv);
     L.Rs = take(NC * CH * Dv);
     L.DH = take(NC * Dk * Dv);
+  }
+  if (bwd) {
     if (p->dtype == GDR2_BF16) {
       // fragment-ordered dR and A for the chunk-parallel backward
       L.bDR = off;
@@ -392,7 +407,8 @@ hipError_t scan_fwd_bf16(const ScanArgs& sa, const Layout& L, void* ws, Last&& l
   pn.S0 = nullptr;
   pn.ST = nullptr;
   pn.o = nullptr;
-  pn.Hs = pn.Rs = nullptr;
+  pn.Hs = nullptr;
+  pn.Rs = nullptr;
   pn.nseg = L.nseg;
   pn.seg_len = L.seg_len;
   pn.STseg = at<float>(ws, L.sN);
@@ -478,8 +494,9 @@ struct FwdRun {
       hipError_t e = timed(GDR2_K_FWD_INTRA, st, [&] { return launch_intra_bf16<DK, DV>(ia, st); });
       if (e != hipSuccess) return e;
       ScanArgs sa{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.U, ia.GC, S0, ST, static_cast<bf16_t*>(o),
-                  save ? at<float>(ws, L.Hs) : nullptr, save ? at<float>(ws, L.Rs) : nullptr,
+                  save ? at<_Float16>(ws, L.Hs) : nullptr, save ? at<float>(ws, L.Rs) : nullptr,
                   G.nscan, p->T, p->H, NT, p->scale};
+      sa.Hsc = save ? at<float>(ws, L.Hsc) : nullptr;
       sa.vl = G.vl;
       sa.G = G.G;
       return timed(GDR2_K_FWD_STATE, st, [&] {
@@ -534,8 +551,9 @@ struct BwdRun {
         // recompute: intra-chunk tiles (with A), then the forward scan storing the chunk states and R
         e = timed(GDR2_K_BWD_RECOMPUTE_INTRA, st, [&] { return launch_intra_bf16<DK, DV>(ia, st); });
         if (e != hipSuccess) return e;
-        ScanArgs sa{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.U, ia.GC, S0, nullptr, nullptr, at<float>(ws, L.Hs),
+        ScanArgs sa{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.U, ia.GC, S0, nullptr, nullptr, at<_Float16>(ws, L.Hs),
                     at<float>(ws, L.Rs), G.nscan, p->T, p->H, NT, p->scale};
+        sa.Hsc = at<float>(ws, L.Hsc);
         sa.vl = G.vl;
         sa.G = G.G;
         e = timed(GDR2_K_BWD_RECOMPUTE_STATE, st, [&] {
@@ -546,7 +564,8 @@ struct BwdRun {
         if (e != hipSuccess) return e;
       }
       BScanArgs ba{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.GC, static_cast<const bf16_t*>(dout), dST, dS0,
-                   at<float>(ws, L.DH), at<unsigned char>(ws, L.bDR), G.nscan, p->T, p->H, NT, p->scale};
+                   at<_Float16>(ws, L.DH), at<unsigned char>(ws, L.bDR), G.nscan, p->T, p->H, NT, p->scale};
+      ba.DHsc = at<float>(ws, L.DHsc);
       ba.vl = G.vl;
       ba.G = G.G;
       e = timed(GDR2_K_BWD_STATE, st, [&] { return scan_bwd_bf16<DK, DV>(ba, L, ws, st); });
@@ -554,11 +573,13 @@ struct BwdRun {
       // the WY VJP and the intra-chunk VJP in one chunk-parallel kernel
       BChunkBf16Args ca{static_cast<const bf16_t*>(q), static_cast<const bf16_t*>(k),
                         static_cast<const bf16_t*>(v), g, static_cast<const bf16_t*>(b),
-                        static_cast<const bf16_t*>(w), static_cast<const bf16_t*>(dout), at<float>(ws, L.Hs),
-                        at<float>(ws, L.DH), at<float>(ws, L.Rs), at<unsigned char>(ws, L.bDR),
+                        static_cast<const bf16_t*>(w), static_cast<const bf16_t*>(dout), at<_Float16>(ws, L.Hs),
+                        at<_Float16>(ws, L.DH), at<float>(ws, L.Rs), at<unsigned char>(ws, L.bDR),
                         at<unsigned char>(ws, L.bAm), static_cast<bf16_t*>(dq), static_cast<bf16_t*>(dk),
                         static_cast<bf16_t*>(dv), static_cast<bf16_t*>(db), static_cast<bf16_t*>(dw), dg,
                         p->B, p->T, p->H, NT, p->scale};
+      ca.Hsc = at<float>(ws, L.Hsc);
+      ca.DHsc = at<float>(ws, L.DHsc);
       ca.vl = G.vl;
       ca.G = G.G;
       if (G.G > 1) {  // the group's key-side gradients add up on the key-head axis

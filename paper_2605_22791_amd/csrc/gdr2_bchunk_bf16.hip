@@ -2,7 +2,8 @@
 // kernel: one 4-wave workgroup per chunk-head, two workgroups per CU.
 //
 // Per chunk it reads the chunk-start state h = S_0 and the gradient dh of the
-// chunk-end state (fp32 [Dk][Dv]), R (fp32 [C][Dv]) from the recompute scan, dR
+// chunk-end state (fp16 [Dk][Dv] with block scales, store_state_f16), R (fp32
+// [C][Dv]) from the recompute scan, dR
 // from the reverse scan and A = (I + T)^{-1} from the intra-chunk recompute
 // (both split bf16 fragment blocks), and q, k, v, b, w, g, dO.
 //
@@ -101,38 +102,6 @@ __device__ __forceinline__ float4 ldg_f4(const float* p) { return *reinterpret_c
 __device__ __forceinline__ Fr split_f44(const float4& x, const float4& y) {
   const float v[8] = {x.x, x.y, x.z, x.w, y.x, y.y, y.z, y.w};
   return split8(v);
-}
-// 4 x 4 transpose inside each quad of lanes (lanes 4m + j, j = 0..3): on entry
-// lane j holds v[u] = M[j][u], on exit v[k] = M[k][j].  Two stages of 2 x 2
-// block swaps with DPP quad permutations (xor 1, then xor 2).
-__device__ __forceinline__ float dpp_quad(float x, int ctrl_xor) {
-  const int v = __float_as_int(x);
-  return __int_as_float(ctrl_xor == 1 ? __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false)
-                                      : __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false));
-}
-__device__ __forceinline__ void quad_transpose(float (&v)[4], int j) {
-  {
-    const bool odd = (j & 1) != 0;
-    const float a = dpp_quad(odd ? v[0] : v[1], 1), b = dpp_quad(odd ? v[2] : v[3], 1);
-    if (odd) {
-      v[0] = a;
-      v[2] = b;
-    } else {
-      v[1] = a;
-      v[3] = b;
-    }
-  }
-  {
-    const bool hi = (j & 2) != 0;
-    const float a = dpp_quad(hi ? v[0] : v[2], 2), b = dpp_quad(hi ? v[1] : v[3], 2);
-    if (hi) {
-      v[0] = a;
-      v[1] = b;
-    } else {
-      v[2] = a;
-      v[3] = b;
-    }
-  }
 }
 // four consecutive outputs of one row: 8-byte bf16 or 16-byte fp32 store
 __device__ __forceinline__ void store_row4(__bf16* p, const float (&v)[4]) {
@@ -236,8 +205,10 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   const __bf16* dOp = reinterpret_cast<const __bf16*>(a.dout) + vb0;
   __bf16* dVp = reinterpret_cast<__bf16*>(a.dv) + vb0;
   __bf16* dWp = reinterpret_cast<__bf16*>(a.dw) + vb0;
-  const float* Hc = a.Hs + ch * DK * DV;
-  const float* DHc = a.DH + ch * DK * DV;
+  const _Float16* Hc = a.Hs + ch * DK * DV;
+  const _Float16* DHc = a.DH + ch * DK * DV;
+  const float* Hscc = a.Hsc + ch * (WsBf16::hsc(DK, DV) / 4);
+  const float* DHscc = a.DHsc + ch * (WsBf16::hsc(DK, DV) / 4);
   const float* Rc = a.Rs + ch * CH * DV;
   const int kst = HK * DK, kso = kst, vst = H * DV;
 
@@ -289,7 +260,9 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       rblk[2 * p + 1] = ldg_f4(rp + 16);
     }
   }
-  float4 pg, ph0, ph1, pd0, pd1;
+  float4 pg;
+  u4v ph, pd;     // 8 fp16 values of h and dh
+  float psh, psd;  // their inverse scales
   bf4 pk, pb, pq;
 #define GDR2_PREFETCH(CB)                                                                  \
   {                                                                                        \
@@ -300,10 +273,10 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     pq = *reinterpret_cast<const bf4*>(Qp + o_);                                           \
     if (hact) {                                                                            \
       const int so_ = (16 * (CB) + hc) * DV + hv;                                          \
-      ph0 = ldg_f4(Hc + so_);                                                              \
-      ph1 = ldg_f4(Hc + so_ + 4);                                                          \
-      pd0 = ldg_f4(DHc + so_);                                                             \
-      pd1 = ldg_f4(DHc + so_ + 4);                                                         \
+      ph = ldg16(Hc + so_);                                                                \
+      pd = ldg16(DHc + so_);                                                               \
+      psh = Hscc[(CB) * (DV / 32) + hv / 32];                                              \
+      psd = DHscc[(CB) * (DV / 32) + hv / 32];                                             \
     }                                                                                      \
   }
   // Writes key block CB's staged operands (parity PAR for the small arrays):
@@ -348,7 +321,10 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       sQc[(4 * cq + u_) * LXT + grow] = pq[u_];                                            \
     }                                                                                      \
     if (hact) {                                                                            \
-      const Fr hf_ = split_f44(ph0, ph1), df_ = split_f44(pd0, pd1);                       \
+      float hx_[8], dx_[8];                                                                \
+      load_state8(ph, psh, hx_);                                                           \
+      load_state8(pd, psd, dx_);                                                           \
+      const Fr hf_ = split8(hx_), df_ = split8(dx_);                                       \
       __bf16* bh_ = sHh + hc * LH;                                                         \
       *reinterpret_cast<bf4*>(bh_ + hp0) = bf4{hf_.hi[0], hf_.hi[1], hf_.hi[2], hf_.hi[3]}; \
       *reinterpret_cast<bf4*>(bh_ + hp1) = bf4{hf_.hi[4], hf_.hi[5], hf_.hi[6], hf_.hi[7]}; \
@@ -361,8 +337,8 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       bh_ = sDl + hc * LH;                                                                 \
       *reinterpret_cast<bf4*>(bh_ + hp0) = bf4{df_.lo[0], df_.lo[1], df_.lo[2], df_.lo[3]}; \
       *reinterpret_cast<bf4*>(bh_ + hp1) = bf4{df_.lo[4], df_.lo[5], df_.lo[6], df_.lo[7]}; \
-      float hh_ = ph0.x * pd0.x + ph0.y * pd0.y + ph0.z * pd0.z + ph0.w * pd0.w +          \
-                  ph1.x * pd1.x + ph1.y * pd1.y + ph1.z * pd1.z + ph1.w * pd1.w;           \
+      float hh_ = hx_[0] * dx_[0];                                                         \
+      _Pragma("unroll") for (int e_ = 1; e_ < 8; ++e_) hh_ += hx_[e_] * dx_[e_];           \
       _Pragma("unroll") for (int o_ = DV / 16; o_ >= 1; o_ >>= 1) hh_ += __shfl_xor(hh_, o_); \
       if ((tid % (DV / 8)) == 0) sHH[(PAR) * 16 + hc] = hh_;                               \
     }                                                                                      \

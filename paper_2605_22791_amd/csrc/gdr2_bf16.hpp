@@ -159,6 +159,126 @@ __device__ __forceinline__ bf8 ld_tr8p(const __bf16* p0, const __bf16* p1) {
   return r;
 }
 
+// 4 x 4 transpose inside each quad of lanes (lanes 4m + j, j = 0..3): on entry
+// lane j holds v[u] = M[j][u], on exit v[k] = M[k][j].  Two stages of 2 x 2
+// block swaps with DPP quad permutations (xor 1, then xor 2).
+__device__ __forceinline__ float dpp_quad(float x, int ctrl_xor) {
+  const int v = __float_as_int(x);
+  return __int_as_float(ctrl_xor == 1 ? __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false)
+                                      : __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false));
+}
+__device__ __forceinline__ void quad_transpose(float (&v)[4], int j) {
+  {
+    const bool odd = (j & 1) != 0;
+    const float a = dpp_quad(odd ? v[0] : v[1], 1), b = dpp_quad(odd ? v[2] : v[3], 1);
+    if (odd) {
+      v[0] = a;
+      v[2] = b;
+    } else {
+      v[1] = a;
+      v[3] = b;
+    }
+  }
+  {
+    const bool hi = (j & 2) != 0;
+    const float a = dpp_quad(hi ? v[0] : v[2], 2), b = dpp_quad(hi ? v[1] : v[3], 2);
+    if (hi) {
+      v[0] = a;
+      v[1] = b;
+    } else {
+      v[2] = a;
+      v[3] = b;
+    }
+  }
+}
+
+// ---- chunk states between the scans and the chunk backward -----------------
+// The bf16 path keeps the chunk-start states h_n (forward scan) and the
+// gradients dh_n of the chunk-end states (reverse scan) for the chunk backward
+// in fp16 with one power-of-two scale per 16 x 32 block (16 key rows, 32 value
+// columns): the block's largest magnitude m is mapped into [2^14, 2^15), so no
+// value overflows fp16 and every value within 2^28 of m keeps fp16's 11
+// significant bits.  The state recursions themselves stay in fp32; only the
+// copies the chunk backward reads are rounded (relative 2^-12 per element,
+// against the bf16 rounding 2^-9 of the operator's outputs).
+//   H16 (Dk x Dv)            fp16, row-major, per chunk-head
+//   HSC (Dk / 16, Dv / 32)   fp32 inverse scales (x = fp16 value * HSC)
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+
+// Largest value over the wave (x >= 0): DPP steps inside each 16-lane row
+// (quad swaps, then the half-row and row mirrors), then the four row maxima
+// read as scalars.
+template <int CTRL>
+__device__ __forceinline__ float dppf(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float wave_max(float x) {
+  x = fmaxf(x, dppf<0xB1>(x));   // quad_perm [1, 0, 3, 2]
+  x = fmaxf(x, dppf<0x4E>(x));   // quad_perm [2, 3, 0, 1]
+  x = fmaxf(x, dppf<0x141>(x));  // row_half_mirror
+  x = fmaxf(x, dppf<0x140>(x));  // row_mirror
+  const int b = __float_as_int(x);
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(b, 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(b, 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(b, 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(b, 48));
+  return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
+}
+// Power-of-two exponent that maps the block maximum m >= 0 into [2^14, 2^15)
+// (0 for m = 0 or a non-finite m, whose values then pass through unscaled).
+__device__ __forceinline__ int state_shift(float m) {
+  if (!(m > 0.f) || !(m <= 3.0e38f)) return 0;
+  int e;
+  (void)frexpf(m, &e);  // m = f 2^e, f in [0.5, 1)
+  const int sh = 15 - e;
+  return sh < -120 ? -120 : (sh > 120 ? 120 : sh);
+}
+// The wave's state tiles s[t] are an MFMA accumulator layout: lane (g, r16)
+// holds rows 4 g + u of the wave's 16 key rows, column 16 t + r16 of its
+// columns; value blocks t, t + 1 share one scale (TPW even).
+// state_shifts: the scale exponent of each of the wave's TPW / 2 blocks.
+template <int TPW>
+__device__ __forceinline__ void state_shifts(const f4 (&s)[TPW], int (&sh)[TPW / 2]) {
+  static_assert(TPW % 2 == 0, "pairs of 16-column tiles per scale block");
+#pragma unroll
+  for (int t2 = 0; t2 < TPW; t2 += 2) {
+    float mx = 0.f;
+#pragma unroll
+    for (int t = t2; t < t2 + 2; ++t)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) mx = fmaxf(mx, fabsf(s[t][u]));
+    sh[t2 / 2] = state_shift(wave_max(mx));
+  }
+}
+// store_state_f16: the tiles as fp16 with their scales.  h0 points at the
+// wave's first row and column in the chunk's H16 (row stride ld), sc at its
+// first block's scale.  A quad transpose gives each lane four consecutive
+// columns of one row, so every store is 8 bytes.
+template <int TPW>
+__device__ __forceinline__ void store_state_f16(const f4 (&s)[TPW], const int (&sh)[TPW / 2], _Float16* h0, int ld,
+                                                float* sc, int lane) {
+  const int g = lane >> 4, r16 = lane & 15, m = r16 >> 2, j = r16 & 3;
+#pragma unroll
+  for (int t = 0; t < TPW; ++t) {
+    const float f = ldexpf(1.f, sh[t / 2]);
+    float v[4] = {s[t][0] * f, s[t][1] * f, s[t][2] * f, s[t][3] * f};
+    quad_transpose(v, j);
+    const f16x4 hv = {(_Float16)v[0], (_Float16)v[1], (_Float16)v[2], (_Float16)v[3]};
+    *reinterpret_cast<f16x4*>(h0 + (size_t)(4 * g + j) * ld + 16 * t + 4 * m) = hv;
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int t2 = 0; t2 < TPW / 2; ++t2) sc[t2] = ldexpf(1.f, -sh[t2]);
+  }
+}
+// Eight consecutive values of one row of a stored state, back in fp32.
+__device__ __forceinline__ void load_state8(u4v raw, float inv, float (&x)[8]) {
+  const f16x8 h = __builtin_bit_cast(f16x8, raw);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) x[e] = (float)h[e] * inv;
+}
+
 // v_mfma_f32_16x16x4_f32: lane l supplies A[l%16][l/16] and B[l/16][l%16].
 __device__ __forceinline__ f4 mfma_f32(float a, float b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);

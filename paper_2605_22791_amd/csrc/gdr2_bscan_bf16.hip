@@ -5,7 +5,8 @@
 //   dR  = scale * A_qk^T dO + Ktail dS
 //   dS <- Diag(gamma_C) dS + scale * Q_g^T dO - Y^T dR
 //
-// writing dS before each update (the gradient of that chunk's end state), dR
+// writing dS before each update (the gradient of that chunk's end state, fp16
+// with block scales as store_state_f16 keeps it for the chunk backward), dR
 // (split hi/lo, in the fragment order the chunk backward reads), and finally dS0.
 // With nseg > 1 each workgroup runs one segment of a sequence, from the
 // gradient at the segment's end to the one at its start (BScanArgs).  The operands are the forward's fragment-ordered tiles
@@ -173,6 +174,11 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
     const size_t ch = chs + n;
     if (n > n0) GDR2_LOAD_CHUNK(n - 1)
 
+    // scale exponents of the fp16 copy of dS, early in the step so that their
+    // cross-lane reductions overlap the products below
+    int dsh[TPW / 2];
+    if (a.DH) state_shifts<TPW>(sreg, dsh);
+
     // ---- dR = scale * A_qk^T dO + Ktail dS   (tiles: row block iO, value blocks vbO..)
     f4 racc[NVB / 2], aacc[NVB / 2];
 #pragma unroll
@@ -220,11 +226,9 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
     }
     // gradient of this chunk's end state (sreg is not updated before the barrier below)
     if (a.DH) {
-#pragma unroll
-      for (int t = 0; t < TPW; ++t)
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-          a.DH[(ch * DK + 16 * cs + 4 * g + u) * DV + v0 + 16 * (sv0 + t) + r16] = sreg[t][u];
+      const int col0 = v0 + 16 * sv0;
+      store_state_f16<TPW>(sreg, dsh, a.DH + (ch * DK + 16 * cs) * DV + col0, DV,
+                           a.DHsc + ch * (WsBf16::hsc(DK, DV) / 4) + cs * (DV / 32) + col0 / 32, lane);
     }
     const float sc = a.scale;
     f4 rkeep[NVB / 2];

@@ -228,6 +228,8 @@ struct RecurArgs {
 //                   lane l holds U[16 i + 4 (l / 16) + u][16 vb + l % 16]
 //   GC   (Dk)       gamma_C, fp32
 // and, for the backward:
+//   Hs, DH (Dk x Dv) chunk-start states and chunk-end state gradients, fp16 with
+//                   per-block scales (store_state_f16 in gdr2_bf16.hpp)
 //   Am   (64 x 64)  A = (I + T)^{-1}, bf16 hi/lo, permuted blocks [key s block 4][row r block 2]
 //                   (row R = s, permuted K = r): the B operand of A^T-products
 //   DR   (64 x Dv)  dR, bf16 hi/lo, permuted blocks [value block Dv/16][row block 2]
@@ -241,6 +243,9 @@ struct WsBf16 {
   static constexpr size_t gc(int dk) { return (size_t)((dk * 4 + 255) / 256) * 256; }
   static constexpr size_t am() { return (size_t)8 * 2048; }
   static constexpr size_t dr(int dv) { return (size_t)(dv / 16) * 2 * 2048; }
+  // chunk states of the backward: fp16 (Dk x Dv) and one fp32 scale per 16 x 32 block
+  static constexpr size_t hs(int dk, int dv) { return (size_t)dk * dv * 2; }
+  static constexpr size_t hsc(int dk, int dv) { return (size_t)(dk / 16) * (dv / 32) * 4; }
 };
 
 struct IntraBf16Args {
@@ -283,10 +288,11 @@ struct ScanArgs {
   const float* S0;  // nullable
   float* ST;        // nullable
   bf16_t* o;        // written when the output is fused in
-  float* Hs;        // chunk-start states (backward recompute)
+  _Float16* Hs;     // chunk-start states for the backward, fp16 (store_state_f16 layout)
   float* Rs;        // R per chunk (backward recompute)
   int B, T, H, NT;
   float scale;
+  float* Hsc = nullptr;          // their inverse scales (WsBf16::hsc per chunk-head)
   int nseg = 1, seg_len = 0;     // segments per sequence and their length in chunks (0: NT)
   const float* S0seg = nullptr;  // nullable: start state of every segment (B*H*nseg, Dk, DV)
   float* STseg = nullptr;        // nullable: end state of every segment (B*H*nseg, Dk, DV)
@@ -304,10 +310,11 @@ struct BScanArgs {
   const bf16_t* dout;
   const float* dST;  // nullable
   float* dS0;        // nullable
-  float* DH;         // nullable: gradient of each chunk's end state (B,H,NT,Dk,Dv)
+  _Float16* DH;      // nullable: gradient of each chunk's end state, fp16 (store_state_f16 layout)
   unsigned char* DR; // nullable: dR per chunk, WsBf16 fragment blocks
   int B, T, H, NT;
   float scale;
+  float* DHsc = nullptr;           // the inverse scales of DH
   int nseg = 1, seg_len = 0;       // as in ScanArgs; the scan runs from a segment's end to its start
   const float* dSseg_in = nullptr; // nullable: gradient at the end of every segment (B*H*nseg, Dk, DV)
   float* dSseg_out = nullptr;      // nullable: gradient at the start of every segment
@@ -338,8 +345,8 @@ struct BChunkBf16Args {
   const bf16_t* b;
   const bf16_t* w;
   const bf16_t* dout;
-  const float* Hs;          // chunk-start states (B,H,NT,Dk,Dv)
-  const float* DH;          // gradients of the chunk-end states (B,H,NT,Dk,Dv)
+  const _Float16* Hs;       // chunk-start states, fp16 (store_state_f16 layout)
+  const _Float16* DH;       // gradients of the chunk-end states, fp16
   const float* Rs;          // R per chunk (B,H,NT,C,Dv)
   const unsigned char* DR;  // dR, WsBf16 fragment blocks
   const unsigned char* Am;  // A, WsBf16 fragment blocks
@@ -351,6 +358,8 @@ struct BChunkBf16Args {
   float* dg;
   int B, T, H, NT;
   float scale;
+  const float* Hsc = nullptr;   // inverse scales of Hs and DH (WsBf16::hsc per chunk-head)
+  const float* DHsc = nullptr;
   Varlen vl{};
   // grouped value heads: H value heads share H / G key heads.  With G > 1 the
   // kernel is launched once per value head of every group (gj = 0 .. G - 1, in

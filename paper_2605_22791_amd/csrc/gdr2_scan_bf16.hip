@@ -12,8 +12,9 @@
 // the current chunk's step and copied to LDS at its end, with the step's own
 // stores (R, O, the chunk state) behind its products.  The two value slices
 // of one head run on the same XCD so that their shared reads hit one L2.
-// With STORE_H the chunk-start states and R are written for the backward
-// (alone in the backward's recompute, or with the output when the forward keeps them).
+// With STORE_H the chunk-start states (fp16 with block scales, store_state_f16)
+// and R are written for the backward (alone in the backward's recompute, or
+// with the output when the forward keeps them).
 // With nseg > 1 each workgroup scans one segment of a sequence from a given
 // start state (ScanArgs), which the sequence-parallel mode builds on.
 //
@@ -189,6 +190,11 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
       GDR2_LOAD_UG(ch + 1, chk + n + 1, unext, gnext)
     }
 
+    // scale exponents of this chunk-start state's fp16 copy, early in the step
+    // so that their cross-lane reductions overlap the products below
+    int hsh[TPW / 2];
+    if (STORE_H) state_shifts<TPW>(sreg, hsh);
+
     // ---- R = U - Y S
     f4 racc[NVB / 2];
 #pragma unroll
@@ -266,15 +272,14 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
 
     // ---- S <- Diag(gamma_C) S + Ktail^T R
     if (STORE_H) {
-      // from a copy: the state registers change right below
+      // the chunk-start state for the backward, fp16 with its block scales
+      // (from a copy: the state registers change right below)
       f4 hcopy[TPW];
 #pragma unroll
       for (int t = 0; t < TPW; ++t) hcopy[t] = sreg[t];
-#pragma unroll
-      for (int t = 0; t < TPW; ++t)
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-          a.Hs[(ch * DK + 16 * cs + 4 * g + u) * DV + v0 + 16 * (sv0 + t) + r16] = hcopy[t][u];
+      const int col0 = v0 + 16 * sv0;
+      store_state_f16<TPW>(hcopy, hsh, a.Hs + (ch * DK + 16 * cs) * DV + col0, DV,
+                           a.Hsc + ch * (WsBf16::hsc(DK, DV) / 4) + cs * (DV / 32) + col0 / 32, lane);
     }
     {
       Fr kf[2], rfs[2][TPW];

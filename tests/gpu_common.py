@@ -80,7 +80,8 @@ def bf16_bits_to_f32(u16):
 def ws_layout_bf16(B, T, H, Dk, Dv, bwd=False, nseq=0, G=1):
     """Byte offsets / per-chunk-head sizes of the bf16 workspace regions
     (mirrors WsBf16 in the library: fragment-ordered tiles; the backward adds
-    fp32 chunk states Hs, R and dH, then dR and A as fragment blocks).  A
+    the chunk states Hs and dH (fp16, with fp32 scales Hsc, DHsc per 16 x 32
+    block) and R (fp32), then dR and A as fragment blocks).  A
     packed call (nseq > 0) has H * (T // 64 + nseq) chunk-heads and appends
     its chunk table (int32: nseq + 1 offsets, two slot arrays, the scan order).
     H counts value heads; with G value heads per key head the key-side tiles
@@ -91,7 +92,8 @@ def ws_layout_bf16(B, T, H, Dk, Dv, bwd=False, nseq=0, G=1):
     sizes = [("Y", 4 * (Dk // 32) * 1024), ("Qg", 4 * (Dk // 32) * 2048), ("Aqk", 8 * 2048),
              ("KtT", (Dk // 16) * 2 * 2048), ("U", (Dv // 16) * 4 * 1024), ("GC", gc)]
     if bwd:
-        sizes += [("Hs", Dk * Dv * 4), ("Rs", CH * Dv * 4), ("DH", Dk * Dv * 4),
+        hsc = (Dk // 16) * (Dv // 32) * 4
+        sizes += [("Hs", Dk * Dv * 2), ("Hsc", hsc), ("Rs", CH * Dv * 4), ("DH", Dk * Dv * 2), ("DHsc", hsc),
                   ("DR", (Dv // 16) * 2 * 2048), ("Am", 8 * 2048)]
     off, out = 0, {}
     for n, per in sizes:
@@ -168,3 +170,10 @@ def seg_buffer_bytes(B, T, H, Dk, Dv, dtype="bf16"):
     r = lambda n: (n * 4 + 255) // 256 * 256
     nvs = B * H * nseg
     return r(nvs * Dk * Dk) + 2 * r(nvs * Dk * Dv)
+
+
+def decode_states_f16(raw_f16, raw_scales, NC, Dk, Dv):
+    """fp16 chunk states with their per-(16 x 32)-block scales -> (NC, Dk, Dv) float64."""
+    h = raw_f16.view(np.float16).astype(np.float64).reshape(NC, Dk, Dv)
+    sc = raw_scales.view(np.float32).astype(np.float64).reshape(NC, Dk // 16, Dv // 32)
+    return h * np.repeat(np.repeat(sc, 16, axis=1), 32, axis=2)

@@ -17,7 +17,8 @@ from oracle import gdr2_recurrent_bwd, gdr2_recurrent_fwd
 from oracle.chunkwise import gdr2_chunk_fwd_ref
 from paper_2605_22791_amd.inputs import make_inputs
 from tests.helpers import rel_l2
-from tests.gpu_common import dev_inputs, host, scan_segments, seg_buffer_bytes, ws_layout_bf16, CH
+from tests.gpu_common import dev_inputs, host, scan_segments, seg_buffer_bytes, ws_layout_bf16, CH, \
+    decode_states_f16
 
 pytestmark = pytest.mark.gpu
 
@@ -85,13 +86,18 @@ def test_segmented_saved_path_and_chunk_states():
     o_s, S_s, g_s = _fwd_bwd(d, ws=ws, save=True)
     torch.cuda.synchronize()
     off, per = lay["Hs"]
+    soff, sper = lay["Hsc"]
     NT = T // CH
-    Hs = ws[off:off + NC * per].view(torch.float32).cpu().numpy().reshape(B, H, NT, Dk, Dv)
+    raw = ws.cpu().numpy()
+    Hs = decode_states_f16(raw[off:off + NC * per], raw[soff:soff + NC * sper], NC, Dk, Dv).reshape(B, H, NT, Dk, Dv)
     _, _, it = gdr2_chunk_fwd_ref(d["q"], d["k"], d["v"], d["log_alpha"], d["b"], d["w"], d["S0"],
                                   d["scale"], C=CH, keep=True)
     err_h = rel_l2(Hs, it["h"])
     print("chunk states rel", f"{err_h:.2e}")
-    assert err_h < TOL
+    # the copies are fp16 with one power-of-two scale per 16 x 32 block that puts
+    # the block's largest value in [2^14, 2^15): 11 significant bits each, about
+    # 1.5e-4 rel-L2 over the states; a scale off by 2^k would show as 2^k times that
+    assert err_h < 4e-4
     o_r, S_r, g_r = _fwd_bwd(d)
     assert np.array_equal(o_s, o_r) and np.array_equal(S_s, S_r)
     for n in GRADS:
