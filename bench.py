@@ -213,9 +213,42 @@ def decode_bench(steps, B=256, H=16, D=128, distinct=64):
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
     bytes_step = B * H * (2 * D * D * 4 + 5 * D * 2 + D * 4 + D * 2)
-    return {"steps_per_s": 1000.0 / ms, "us_per_step": ms * 1000.0,
-            "hbm_GBs": bytes_step / (ms * 1e-3) / 1e9, "hbm_frac": bytes_step / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
-            "config": {"B": B, "H": H, "d": D, "steps": steps}}
+    out = {"steps_per_s": 1000.0 / ms, "us_per_step": ms * 1000.0, "alg_bytes_per_call": bytes_step,
+           "hbm_GBs": bytes_step / (ms * 1e-3) / 1e9, "hbm_frac": bytes_step / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+           "config": {"B": B, "H": H, "d": D, "steps": steps}}
+    counted = measured_decode_traffic(B)
+    if counted is not None:
+        out["counter_bytes_per_call"] = counted
+        out["counter_GBs"] = counted / (ms * 1e-3) / 1e9
+    return out
+
+
+def measured_decode_traffic(B):
+    """FETCH_SIZE + WRITE_SIZE bytes per decode call at batch B from the committed
+    rocprofv3 summary (None when it has no row for B)."""
+    here = os.path.dirname(os.path.abspath(__file__))
+    path = os.path.join(here, "profiles", "recurrent_decode_B256_B512_counters.md")
+    if not os.path.exists(path):
+        return None
+    for line in open(path):
+        cells = [c.strip() for c in line.strip().strip("|").split("|")]
+        if len(cells) >= 5 and cells[0] == str(B):
+            return int((float(cells[3]) + float(cells[4])) * 1e6)
+    return None
+
+
+def calibration_copy(mib):
+    """One copy-like elementwise kernel (torch.neg) over `mib` MiB of fp32: the
+    reference that scales rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src_c = torch.ones(n, device="cuda")
+    dst_c = torch.empty_like(src_c)
+    torch.cuda.synchronize()
+    torch.neg(src_c, out=dst_c)               # one elementwise kernel: n*4 bytes in, n*4 out
+    torch.cuda.synchronize()
+    print(f"[bench] calibration copy: {mib} MiB read + {mib} MiB written", file=sys.stderr, flush=True)
+    del src_c, dst_c
 
 
 def copy_bandwidth(mib=2048, reps=5):
@@ -479,6 +512,8 @@ def main():
               file=sys.stderr)
         sys.exit(2)
     if args.decode_only:
+        if args.calib_copy > 0:
+            calibration_copy(args.calib_copy)
         print(json.dumps(decode_bench(1024, B=args.decode_batch)), flush=True)
         return
     if args.long_context_only:
@@ -521,15 +556,7 @@ def main():
     step = make_step(stored)
 
     if args.calib_copy > 0:
-        n = args.calib_copy * (1 << 20) // 4
-        src_c = torch.ones(n, device=dev)
-        dst_c = torch.empty_like(src_c)
-        torch.cuda.synchronize()
-        torch.neg(src_c, out=dst_c)               # one elementwise kernel: n*4 bytes in, n*4 out
-        torch.cuda.synchronize()
-        print(f"[bench] calibration copy: {args.calib_copy} MiB read + {args.calib_copy} MiB written",
-              file=sys.stderr, flush=True)
-        del src_c, dst_c
+        calibration_copy(args.calib_copy)
 
     print("[bench] warmup", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
@@ -628,6 +655,8 @@ def main():
     if not args.no_decode and not args.no_extra:
         print("[bench] decode (1024 one-token calls, B=256)", file=sys.stderr, flush=True)
         out["decode"] = decode_bench(1024)
+        # twice the state: larger than the Infinity Cache, so the state read-modify-write runs from HBM
+        out["decode_B512"] = decode_bench(1024, B=512)
     if not args.no_extra:
         print("[bench] long context (config 3)", file=sys.stderr, flush=True)
         out["long_context"] = config3_bench(stored=stored)
