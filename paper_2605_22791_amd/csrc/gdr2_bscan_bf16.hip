@@ -111,6 +111,7 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
   {                                                                                                    \
     const size_t chx = chk + (N_);                                                                     \
     _Pragma("unroll") for (int m = 0; m < NSTG; ++m) {                                                 \
+      if (no_input && m >= E_Y && m < E_A) continue; /* Q_g, A_qk only multiply dO */                 \
       const unsigned char* src;                                                                        \
       if (m < E_Y)                                                                                     \
         src = a.Y + chx * C::SZ_Y + m * SLICE;                                                         \
@@ -134,7 +135,8 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
   }
 #define GDR2_STORE_CHUNK()                                                                               \
   {                                                                                                    \
-    _Pragma("unroll") for (int m = 0; m < NSTG; ++m) sts16(sOp + m * SLICE + 16 * tid, stg[m]);        \
+    _Pragma("unroll") for (int m = 0; m < NSTG; ++m)                                                   \
+        if (!no_input || m < E_Y || m >= E_A) sts16(sOp + m * SLICE + 16 * tid, stg[m]);                \
     const int r_ = tid / (DVS / 8), c8_ = (tid % (DVS / 8)) * 8;                                       \
     sts16(sdO + r_ * LDO + c8_, sto);                                                                  \
     _Pragma("unroll") for (int u2 = 0; u2 < 4; ++u2) gcur[u2] = gnext[u2];                             \
@@ -207,8 +209,9 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
         racc[t] = mma3(kf, df, racc[t]);
       }
     }
+    // (without dO the A_qk and Q_g products vanish: their tiles are not even loaded)
 #pragma unroll
-    for (int kb = (iO >> 1); kb < 2; ++kb) {
+    for (int kb = (iO >> 1); kb < 2 && !no_input; ++kb) {
       // A_qk[i][j], i = 32 kb + 8 g + e (query), j = 16 iO + r16 (key)
       Fr af;
       {
@@ -262,10 +265,12 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
         const __bf16* y0 = reinterpret_cast<const __bf16*>(sY + yoff);
         yf = neg8(ld_tr8p(y0, y0 + 32));
       }
+      if (!no_input) {
 #pragma unroll
-      for (int t = 0; t < TPW; ++t) {
-        const int vb = sv0 + t;
-        qacc[t] = mma2a(qf, ld_tr8(sdO, LDO, 32 * kb, 16 * vb, lane), qacc[t]);
+        for (int t = 0; t < TPW; ++t) {
+          const int vb = sv0 + t;
+          qacc[t] = mma2a(qf, ld_tr8(sdO, LDO, 32 * kb, 16 * vb, lane), qacc[t]);
+        }
       }
       if (kb == 0) {
 #pragma unroll

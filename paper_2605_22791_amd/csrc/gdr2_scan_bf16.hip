@@ -123,8 +123,11 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
   float gcur[4], gnext[4];
   const size_t chs = rng.chs;                        // value-head chunks: U, h, R
   const size_t chk = key_ch(a.vl, chs, H, a.G, NT);  // key-head chunks: Y, Q_g, A_qk, K_tail, gamma_C
+  // Q_g and A_qk feed the output only: a scan without it moves Y and Ktail^T alone
+#define GDR2_OP_USED(M_) (WITH_O || (M_) < E_Y || (M_) >= E_A)
 #define GDR2_LOAD_OPS(CHX)                                                                                   \
   _Pragma("unroll") for (int m = 0; m < NSTG; ++m) {                                                     \
+    if (!GDR2_OP_USED(m)) continue;                                                                      \
     const unsigned char* src;                                                                            \
     if (m < E_Y)                                                                                         \
       src = a.Y + (CHX) * C::SZ_Y + m * SLICE;                                                           \
@@ -137,7 +140,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
     stg[m] = ldg16(src + 16 * tid);                                            \
   }
 #define GDR2_STORE_OPS()                                                                                     \
-  _Pragma("unroll") for (int m = 0; m < NSTG; ++m) sts16(sOp + m * SLICE + 16 * tid, stg[m]);
+  _Pragma("unroll") for (int m = 0; m < NSTG; ++m) if (GDR2_OP_USED(m)) sts16(sOp + m * SLICE + 16 * tid, stg[m]);
   // U tiles (value blocks vbO.., row block iO) and gamma_C rows of the state tiles
 #define GDR2_LOAD_UG(CHX, CHKX, UARR, GARR)                                                                  \
   _Pragma("unroll") for (int t = 0; t < NVB / 2; ++t) {                                                  \
@@ -331,6 +334,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
 
 #undef GDR2_LOAD_OPS
 #undef GDR2_STORE_OPS
+#undef GDR2_OP_USED
 #undef GDR2_LOAD_UG
   float* send = a.STseg ? a.STseg + (size_t)vs * DK * DV
                         : ((a.ST && seg == nseg - 1) ? a.ST + (size_t)seq * DK * DV : nullptr);
