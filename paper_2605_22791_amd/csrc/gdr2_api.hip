@@ -65,7 +65,7 @@ int varlen_slots(const gdr2_problem* p, int nseq) { return p->T / CH + nseq; }
 struct Layout {
   size_t Y, U, Kt, Qg, Aqk, GC;          // fp32 forward tiles
   size_t Hs, Rs, DH, DR, DAqk, DT, DEg;  // backward extras
-  size_t Hsc, DHsc;                      // bf16 backward: scales of the fp16 chunk states
+  size_t Hsc, DHsc, Rsc;                 // bf16 backward: scales of the fp16 chunk states and R
   size_t bY, bQ, bA, bK, bU, bG;         // bf16 forward (fragment order)
   size_t bDR, bAm;                       // bf16 backward extras (fragment order)
   size_t sM, sN, sX;                     // segment maps and entry states (sequence-parallel scans)
@@ -143,7 +143,8 @@ Layout layout(const gdr2_problem* p, bool bwd, int nseq = 0, int G = 1, bool fus
     };
     L.Hs = takeb(NC * WsBf16::hs(p->Dk, p->Dv));
     L.Hsc = takeb(NC * WsBf16::hsc(p->Dk, p->Dv));
-    L.Rs = take(NC * CH * Dv);
+    L.Rs = takeb(NC * WsBf16::rs(p->Dv));
+    L.Rsc = takeb(NC * WsBf16::rsc(p->Dv));
     L.DH = takeb(NC * WsBf16::hs(p->Dk, p->Dv));
     L.DHsc = takeb(NC * WsBf16::hsc(p->Dk, p->Dv));
   } else if (bwd) {
@@ -494,9 +495,10 @@ struct FwdRun {
       hipError_t e = timed(GDR2_K_FWD_INTRA, st, [&] { return launch_intra_bf16<DK, DV>(ia, st); });
       if (e != hipSuccess) return e;
       ScanArgs sa{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.U, ia.GC, S0, ST, static_cast<bf16_t*>(o),
-                  save ? at<_Float16>(ws, L.Hs) : nullptr, save ? at<float>(ws, L.Rs) : nullptr,
+                  save ? at<_Float16>(ws, L.Hs) : nullptr, save ? at<_Float16>(ws, L.Rs) : nullptr,
                   G.nscan, p->T, p->H, NT, p->scale};
       sa.Hsc = save ? at<float>(ws, L.Hsc) : nullptr;
+      sa.Rsc = save ? at<float>(ws, L.Rsc) : nullptr;
       sa.vl = G.vl;
       sa.G = G.G;
       return timed(GDR2_K_FWD_STATE, st, [&] {
@@ -552,8 +554,9 @@ struct BwdRun {
         e = timed(GDR2_K_BWD_RECOMPUTE_INTRA, st, [&] { return launch_intra_bf16<DK, DV>(ia, st); });
         if (e != hipSuccess) return e;
         ScanArgs sa{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.U, ia.GC, S0, nullptr, nullptr, at<_Float16>(ws, L.Hs),
-                    at<float>(ws, L.Rs), G.nscan, p->T, p->H, NT, p->scale};
+                    at<_Float16>(ws, L.Rs), G.nscan, p->T, p->H, NT, p->scale};
         sa.Hsc = at<float>(ws, L.Hsc);
+        sa.Rsc = at<float>(ws, L.Rsc);
         sa.vl = G.vl;
         sa.G = G.G;
         e = timed(GDR2_K_BWD_RECOMPUTE_STATE, st, [&] {
@@ -574,12 +577,13 @@ struct BwdRun {
       BChunkBf16Args ca{static_cast<const bf16_t*>(q), static_cast<const bf16_t*>(k),
                         static_cast<const bf16_t*>(v), g, static_cast<const bf16_t*>(b),
                         static_cast<const bf16_t*>(w), static_cast<const bf16_t*>(dout), at<_Float16>(ws, L.Hs),
-                        at<_Float16>(ws, L.DH), at<float>(ws, L.Rs), at<unsigned char>(ws, L.bDR),
+                        at<_Float16>(ws, L.DH), at<_Float16>(ws, L.Rs), at<unsigned char>(ws, L.bDR),
                         at<unsigned char>(ws, L.bAm), static_cast<bf16_t*>(dq), static_cast<bf16_t*>(dk),
                         static_cast<bf16_t*>(dv), static_cast<bf16_t*>(db), static_cast<bf16_t*>(dw), dg,
                         p->B, p->T, p->H, NT, p->scale};
       ca.Hsc = at<float>(ws, L.Hsc);
       ca.DHsc = at<float>(ws, L.DHsc);
+      ca.Rsc = at<float>(ws, L.Rsc);
       ca.vl = G.vl;
       ca.G = G.G;
       if (G.G > 1) {  // the group's key-side gradients add up on the key-head axis

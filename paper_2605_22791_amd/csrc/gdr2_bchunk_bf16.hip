@@ -2,8 +2,8 @@
 // kernel: one 4-wave workgroup per chunk-head, two workgroups per CU.
 //
 // Per chunk it reads the chunk-start state h = S_0 and the gradient dh of the
-// chunk-end state (fp16 [Dk][Dv] with block scales, store_state_f16), R (fp32
-// [C][Dv]) from the recompute scan, dR
+// chunk-end state (fp16 [Dk][Dv] with block scales, store_state_f16), R (fp16
+// fragment blocks with block scales, store_frag_f16) from the scan, dR
 // from the reverse scan and A = (I + T)^{-1} from the intra-chunk recompute
 // (both split bf16 fragment blocks), and q, k, v, b, w, g, dO.
 //
@@ -85,9 +85,13 @@ struct BChunkCfg {
   static constexpr int OFF_DL = OFF_XS + 16 * LGT * 4;
   static constexpr int OFF_RN = OFF_DL + DK * 4;
   static constexpr int LDS_FUSED = OFF_RN + 2 * 64 * 4;
-  static constexpr int NLD = (SZ_DR + SZ_AM) / (16 * NTHR);  // 16-byte prologue loads per thread
-  static_assert(SZ_DR <= SZ_T && SZ_AM <= OFF_END_S - OFF_S, "prologue operands fit their regions");
-  static_assert((SZ_DR + SZ_AM) % (16 * NTHR) == 0 && SZ_DR % (16 * NTHR) == 0, "whole prologue slices");
+  // prologue: dR into region 1, A then R (fp16 fragment blocks) into region 2, by
+  // direct global -> LDS loads of 1 KB per wave instruction
+  static constexpr int SZ_R = (int)WsBf16::rs(DV);
+  static constexpr int OFF_R = OFF_S + SZ_AM;
+  static constexpr int NKB = (SZ_DR + SZ_AM + SZ_R) / 1024;
+  static_assert(SZ_DR <= SZ_T && SZ_AM + SZ_R <= OFF_END_S - OFF_S, "prologue operands fit their regions");
+  static_assert(NKB % (NTHR / 64) == 0 && SZ_DR % 1024 == 0 && SZ_AM % 1024 == 0, "whole blocks per wave");
   static_assert(LDS_FUSED <= 80 * 1024, "two workgroups per CU");
   static_assert(16 * DV / 8 <= NTHR, "one 8-value piece of h / dh per thread");
 };
@@ -99,10 +103,6 @@ __device__ __forceinline__ bf8 cat8(bf4 x, bf4 y) {
   return r;
 }
 __device__ __forceinline__ float4 ldg_f4(const float* p) { return *reinterpret_cast<const float4*>(p); }
-__device__ __forceinline__ Fr split_f44(const float4& x, const float4& y) {
-  const float v[8] = {x.x, x.y, x.z, x.w, y.x, y.y, y.z, y.w};
-  return split8(v);
-}
 // four consecutive outputs of one row: 8-byte bf16 or 16-byte fp32 store
 __device__ __forceinline__ void store_row4(__bf16* p, const float (&v)[4]) {
   *reinterpret_cast<bf4*>(p) = bf4{(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
@@ -129,7 +129,7 @@ __device__ __forceinline__ int perm_pos(int a) { return a < 4 ? 8 * a : 8 * (a -
 template <int DK, int DV, bool FUSED>
 __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   using C = BChunkCfg<DK, DV>;
-  constexpr int NCB = C::NCB, NVB = C::NVB, KV = C::KV, NLD = C::NLD;
+  constexpr int NCB = C::NCB, NVB = C::NVB, KV = C::KV, NKB = C::NKB;
   constexpr int LT = C::LT, LGT = C::LGT, LXT = C::LXT, LH = C::LH;
 
   extern __shared__ __align__(16) unsigned char smem[];
@@ -139,6 +139,7 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   __bf16* sAl = sAh + 64 * LT;
   const unsigned char* sDR = smem + C::OFF_T;  // prologue: dR fragment blocks
   const unsigned char* sAm = smem + C::OFF_S;  // prologue: A fragment blocks
+  const unsigned char* sR = smem + C::OFF_R;   // prologue: R, fp16 fragment blocks [row block][KV]
   float* sG = reinterpret_cast<float*>(smem + C::OFF_G);    // in-block cumsum of log2-decay [c][s]
   float* sEL = reinterpret_cast<float*>(smem + C::OFF_EL);  // 2^(G2_s - G2 at its block's first row)
   float* sER = reinterpret_cast<float*>(smem + C::OFF_ER);  // 2^(G2 at its block's last row - G2_s)
@@ -209,7 +210,8 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   const _Float16* DHc = a.DH + ch * DK * DV;
   const float* Hscc = a.Hsc + ch * (WsBf16::hsc(DK, DV) / 4);
   const float* DHscc = a.DHsc + ch * (WsBf16::hsc(DK, DV) / 4);
-  const float* Rc = a.Rs + ch * CH * DV;
+  const _Float16* Rc = a.Rs + ch * (WsBf16::rs(DV) / 2);
+  const float* Rscc = a.Rsc + ch * (WsBf16::rsc(DV) / 4);
   const int kst = HK * DK, kso = kst, vst = H * DV;
 
   // staging role: chunk row grow (block = wave), channels 16 cb + 4 cq + (0..3)
@@ -234,31 +236,37 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
 
   // ---- loads in flight from the start: dR and A (cooperative), this wave's dO
   // rows and the operands of key block 0
-  u4v ldv[NLD];
   {
+    // wave w moves the 1 KB blocks w, w + 4, ... of dR | A | R straight into LDS
     const unsigned char* DRc = a.DR + ch * WsBf16::dr(DV);
     const unsigned char* Amc = a.Am + key_ch(a.vl, ch, H, a.G, a.NT) * WsBf16::am();  // A: per key head
+    const unsigned char* Rcb = reinterpret_cast<const unsigned char*>(Rc);
 #pragma unroll
-    for (int m = 0; m < NLD; ++m) {
-      const int off = 16 * (tid + C::NTHR * m);
-      ldv[m] = off < C::SZ_DR ? ldg16(DRc + off) : ldg16(Amc + (off - C::SZ_DR));
+    for (int m = 0; m < NKB / 4; ++m) {
+      const int off = 1024 * (4 * m + wave);
+      const unsigned char* src;
+      unsigned char* dst;
+      if (off < C::SZ_DR) {
+        src = DRc + off;
+        dst = smem + C::OFF_T + off;
+      } else if (off < C::SZ_DR + C::SZ_AM) {
+        src = Amc + (off - C::SZ_DR);
+        dst = smem + C::OFF_S + (off - C::SZ_DR);
+      } else {
+        src = Rcb + (off - C::SZ_DR - C::SZ_AM);
+        dst = smem + C::OFF_R + (off - C::SZ_DR - C::SZ_AM);
+      }
+      __builtin_amdgcn_global_load_lds((void*)(src + 16 * lane), (GDR2_LDS void*)dst, 16, 0, 0);
     }
   }
+  // R's block scales: lane j * KV + p holds that of row block j, value block p
+  const float rscl = lane < 4 * KV ? Rscc[lane] : 0.f;
+  const auto rsc = [&](int blk) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(rscl), blk)); };
   bf8 dof[KV];
 #pragma unroll
   for (int p = 0; p < KV; ++p) {
     const int o = (min(16 * i + r16, len - 1)) * vst + 32 * p + 4 * g;
     dof[p] = cat8(*reinterpret_cast<const bf4*>(dOp + o), *reinterpret_cast<const bf4*>(dOp + o + 16));
-  }
-  // R rows of block 0 (permuted K) for the first dT / dA_qk tile of waves 1..3
-  float4 rblk[2 * KV];
-  if (i > 0) {
-#pragma unroll
-    for (int p = 0; p < KV; ++p) {
-      const float* rp = Rc + r16 * DV + 32 * p + 4 * g;
-      rblk[2 * p] = ldg_f4(rp);
-      rblk[2 * p + 1] = ldg_f4(rp + 16);
-    }
   }
   float4 pg;
   u4v ph, pd;     // 8 fp16 values of h and dh
@@ -343,25 +351,7 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       if ((tid % (DV / 8)) == 0) sHH[(PAR) * 16 + hc] = hh_;                               \
     }                                                                                      \
   }
-  GDR2_PREFETCH(0)
-
-  // ---- dR and A into LDS (regions that later hold dT / dA_qk and the staged key block)
-#pragma unroll
-  for (int m = 0; m < NLD; ++m) {
-    const int off = 16 * (tid + C::NTHR * m);
-    if (off < C::SZ_DR)
-      sts16(smem + C::OFF_T + off, ldv[m]);
-    else
-      sts16(smem + C::OFF_S + (off - C::SZ_DR), ldv[m]);
-  }
-  // this wave's R rows (permuted K) and v, w for dv / dw, in flight across the barrier
-  float4 rraw[2 * KV];
-#pragma unroll
-  for (int p = 0; p < KV; ++p) {
-    const float* rp = Rc + (16 * i + r16) * DV + 32 * p + 4 * g;
-    rraw[2 * p] = ldg_f4(rp);
-    rraw[2 * p + 1] = ldg_f4(rp + 16);
-  }
+  // v, w for dv / dw, in flight across the barrier
   bf4 vvr[NVB], wwr[NVB];
 #pragma unroll
   for (int vb = 0; vb < NVB; ++vb) {
@@ -369,7 +359,9 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     vvr[vb] = *reinterpret_cast<const bf4*>(Vp + o);
     wwr[vb] = *reinterpret_cast<const bf4*>(Wp + o);
   }
-  __syncthreads();
+  __syncthreads();  // dR, A and R are in LDS (the barrier waits for the direct loads)
+  // key block 0's operands, in flight while the prologue computes
+  GDR2_PREFETCH(0)
 
   // ---- dZ^T = dR^T A for the key rows s of block i: lane gets
   //      dZ[s = 16 i + r16][v = 16 vb + 4 g + u];  dv = dZ * w, dw = dZ * v
@@ -420,40 +412,29 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       x[4 + u] = zacc[2 * p + 1][u];
     }
     zf[p] = split8(x);
-    rfr[p] = split_f44(rraw[2 * p], rraw[2 * p + 1]);
+    rfr[p] = frag_f16_split(*reinterpret_cast<const u4v*>(sR + (i * KV + p) * 1024 + 16 * lane), rsc(i * KV + p));
   }
-  __syncthreads();  // dR and A are dead
+  __syncthreads();  // dR and A are dead (R stays until the tiles below are done)
   if (16 * i + r16 >= len) {
 #pragma unroll
     for (int p = 0; p < KV; ++p) dof[p] = bf8{};
   }
 
   // ---- dT = -tril(dZ R^T, -1) and dA_qk = tril(scale dO R^T), tiles (i, j <= i),
-  //      stored transposed: plane[s][r].  The R rows of block j + 1 are in flight
-  //      while tile j computes (those of block 0 since the kernel start).
+  //      stored transposed: plane[s][r].  The R rows of block j come from the fp16
+  //      fragment blocks in LDS.
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     if (j > i) break;
     const int s = 16 * j + r16;
-    float4 rnext[2 * KV];
-    if (j + 1 < i) {
-#pragma unroll
-      for (int p = 0; p < KV; ++p) {
-        const float* rp = Rc + (s + 16) * DV + 32 * p + 4 * g;
-        rnext[2 * p] = ldg_f4(rp);
-        rnext[2 * p + 1] = ldg_f4(rp + 16);
-      }
-    }
     f4 ta = f4zero(), aa = f4zero();
 #pragma unroll
     for (int p = 0; p < KV; ++p) {
-      const Fr rj = (j == i) ? rfr[p] : split_f44(rblk[2 * p], rblk[2 * p + 1]);
+      const Fr rj = (j == i) ? rfr[p]
+                             : frag_f16_split(*reinterpret_cast<const u4v*>(sR + (j * KV + p) * 1024 + 16 * lane),
+                                              rsc(j * KV + p));
       ta = mma3(zf[p], rj, ta);
       aa = mma2b(dof[p], rj, aa);
-    }
-    if (j + 1 < i) {
-#pragma unroll
-      for (int p = 0; p < 2 * KV; ++p) rblk[p] = rnext[p];
     }
     const int rr = 16 * i + 4 * g;
     f4 tv, av;
@@ -471,6 +452,7 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     st4split(sTh + s * LT + rr, sTl + s * LT + rr, f4zero());
     st4split(sAh + s * LT + rr, sAl + s * LT + rr, f4zero());
   }
+  __syncthreads();  // R is dead: key block 0 is staged over it
   GDR2_STAGE(0, 0)
   __syncthreads();
 

@@ -272,6 +272,34 @@ __device__ __forceinline__ void store_state_f16(const f4 (&s)[TPW], const int (&
     for (int t2 = 0; t2 < TPW / 2; ++t2) sc[t2] = ldexpf(1.f, -sh[t2]);
   }
 }
+// store_frag_f16: a 16 x 32 tile held as two MFMA accumulator tiles (s[0]:
+// columns 0..15, s[1]: columns 16..31; lane (g, r16) holds rows 4 g + u,
+// column r16) as one fp16 permuted fragment block (1 KB, the layout of
+// gdr2_kernels.hpp's permuted blocks: lane l holds row l % 16 and columns
+// 4 (l / 16) + e, 16 + 4 (l / 16) + e), scaled by 2^sh.  After a quad
+// transpose each lane holds four consecutive columns of one row from either
+// tile, which are exactly the two halves of one fragment lane's 16 bytes.
+__device__ __forceinline__ void store_frag_f16(const f4 (&s)[2], int sh, _Float16* blk, int lane) {
+  const int g = lane >> 4, r16 = lane & 15, m = r16 >> 2, j = r16 & 3;
+  const float f = ldexpf(1.f, sh);
+  float v0[4] = {s[0][0] * f, s[0][1] * f, s[0][2] * f, s[0][3] * f};
+  float v1[4] = {s[1][0] * f, s[1][1] * f, s[1][2] * f, s[1][3] * f};
+  quad_transpose(v0, j);
+  quad_transpose(v1, j);
+  const f16x8 hv = {(_Float16)v0[0], (_Float16)v0[1], (_Float16)v0[2], (_Float16)v0[3],
+                    (_Float16)v1[0], (_Float16)v1[1], (_Float16)v1[2], (_Float16)v1[3]};
+  // row 4 g + j, column group m -> fragment lane (m, 4 g + j)
+  *reinterpret_cast<f16x8*>(blk + 8 * (16 * m + 4 * g + j)) = hv;
+}
+// One lane's fp16 fragment (8 values), scaled back and split hi / lo.
+__device__ __forceinline__ Fr frag_f16_split(u4v raw, float inv) {
+  const f16x8 h = __builtin_bit_cast(f16x8, raw);
+  float x[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) x[e] = (float)h[e] * inv;
+  return split8(x);
+}
+
 // Eight consecutive values of one row of a stored state, back in fp32.
 __device__ __forceinline__ void load_state8(u4v raw, float inv, float (&x)[8]) {
   const f16x8 h = __builtin_bit_cast(f16x8, raw);

@@ -230,6 +230,8 @@ struct RecurArgs {
 // and, for the backward:
 //   Hs, DH (Dk x Dv) chunk-start states and chunk-end state gradients, fp16 with
 //                   per-block scales (store_state_f16 in gdr2_bf16.hpp)
+//   Rs   (64 x Dv)  R, fp16 permuted blocks [row block 4][value block Dv/32] with one
+//                   scale per block (store_frag_f16): the R operands of the chunk backward
 //   Am   (64 x 64)  A = (I + T)^{-1}, bf16 hi/lo, permuted blocks [key s block 4][row r block 2]
 //                   (row R = s, permuted K = r): the B operand of A^T-products
 //   DR   (64 x Dv)  dR, bf16 hi/lo, permuted blocks [value block Dv/16][row block 2]
@@ -246,6 +248,10 @@ struct WsBf16 {
   // chunk states of the backward: fp16 (Dk x Dv) and one fp32 scale per 16 x 32 block
   static constexpr size_t hs(int dk, int dv) { return (size_t)dk * dv * 2; }
   static constexpr size_t hsc(int dk, int dv) { return (size_t)(dk / 16) * (dv / 32) * 4; }
+  // R of the backward: fp16 permuted fragment blocks [row block 4][value block Dv/32]
+  // (1 KB each) and one fp32 scale per block
+  static constexpr size_t rs(int dv) { return (size_t)4 * (dv / 32) * 1024; }
+  static constexpr size_t rsc(int dv) { return (size_t)4 * (dv / 32) * 4; }
 };
 
 struct IntraBf16Args {
@@ -289,10 +295,11 @@ struct ScanArgs {
   float* ST;        // nullable
   bf16_t* o;        // written when the output is fused in
   _Float16* Hs;     // chunk-start states for the backward, fp16 (store_state_f16 layout)
-  float* Rs;        // R per chunk (backward recompute)
+  _Float16* Rs;     // R per chunk for the backward, fp16 fragment blocks (WsBf16::rs)
   int B, T, H, NT;
   float scale;
   float* Hsc = nullptr;          // their inverse scales (WsBf16::hsc per chunk-head)
+  float* Rsc = nullptr;          // R's inverse scales (WsBf16::rsc per chunk-head)
   int nseg = 1, seg_len = 0;     // segments per sequence and their length in chunks (0: NT)
   const float* S0seg = nullptr;  // nullable: start state of every segment (B*H*nseg, Dk, DV)
   float* STseg = nullptr;        // nullable: end state of every segment (B*H*nseg, Dk, DV)
@@ -347,7 +354,7 @@ struct BChunkBf16Args {
   const bf16_t* dout;
   const _Float16* Hs;       // chunk-start states, fp16 (store_state_f16 layout)
   const _Float16* DH;       // gradients of the chunk-end states, fp16
-  const float* Rs;          // R per chunk (B,H,NT,C,Dv)
+  const _Float16* Rs;       // R per chunk, fp16 fragment blocks (WsBf16::rs)
   const unsigned char* DR;  // dR, WsBf16 fragment blocks
   const unsigned char* Am;  // A, WsBf16 fragment blocks
   bf16_t* dq;
@@ -360,6 +367,7 @@ struct BChunkBf16Args {
   float scale;
   const float* Hsc = nullptr;   // inverse scales of Hs and DH (WsBf16::hsc per chunk-head)
   const float* DHsc = nullptr;
+  const float* Rsc = nullptr;   // inverse scales of Rs (WsBf16::rsc per chunk-head)
   Varlen vl{};
   // grouped value heads: H value heads share H / G key heads.  With G > 1 the
   // kernel is launched once per value head of every group (gj = 0 .. G - 1, in

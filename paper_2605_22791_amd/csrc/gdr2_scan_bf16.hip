@@ -200,6 +200,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
 
     // ---- R = U - Y S
     f4 racc[NVB / 2];
+    int rsh[1] = {0};
 #pragma unroll
     for (int t = 0; t < NVB / 2; ++t) racc[t] = ucur[t];
 #pragma unroll
@@ -217,6 +218,8 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
       st4split(sRhi + (16 * vb + r16) * LR + 16 * iO + 4 * g, sRlo + (16 * vb + r16) * LR + 16 * iO + 4 * g,
                racc[t]);
     }
+    // the fp16 copy's scale, taken here so its reduction overlaps the output products
+    if (STORE_H) state_shifts<NVB / 2>(racc, rsh);
     __syncthreads();
 
     // ---- O^T = S^T Q_g^T + R^T A_qk^T  (lane: O[16 iO + r16][16 vb + 4 g + u]);
@@ -307,11 +310,12 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
         for (int t = 0; t < TPW; ++t) sreg[t] = mma3(kf[kb], rfs[kb][t], sreg[t]);
     }
     if (STORE_H) {
-#pragma unroll
-      for (int t = 0; t < NVB / 2; ++t)
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-          a.Rs[(ch * CH + 16 * iO + 4 * g + u) * DV + v0 + 16 * (vbO + t) + r16] = racc[t][u];
+      // R for the backward: this wave's 16 x 32 tile as one fp16 fragment block
+      static_assert(NVB / 2 == 2, "one 32-column block per wave");
+      const int vblk = (v0 + 16 * vbO) / 32;
+      const size_t blk = (size_t)ch * (WsBf16::rs(DV) / 1024) + (size_t)iO * (DV / 32) + vblk;
+      store_frag_f16(racc, rsh[0], a.Rs + blk * 512, lane);
+      if (lane == 0) a.Rsc[blk] = ldexpf(1.f, -rsh[0]);
     }
     __syncthreads();
 

@@ -81,7 +81,8 @@ def ws_layout_bf16(B, T, H, Dk, Dv, bwd=False, nseq=0, G=1):
     """Byte offsets / per-chunk-head sizes of the bf16 workspace regions
     (mirrors WsBf16 in the library: fragment-ordered tiles; the backward adds
     the chunk states Hs and dH (fp16, with fp32 scales Hsc, DHsc per 16 x 32
-    block) and R (fp32), then dR and A as fragment blocks).  A
+    block) and R (fp16 fragment blocks with scales Rsc), then dR and A as
+    fragment blocks).  A
     packed call (nseq > 0) has H * (T // 64 + nseq) chunk-heads and appends
     its chunk table (int32: nseq + 1 offsets, two slot arrays, the scan order).
     H counts value heads; with G value heads per key head the key-side tiles
@@ -93,7 +94,9 @@ def ws_layout_bf16(B, T, H, Dk, Dv, bwd=False, nseq=0, G=1):
              ("KtT", (Dk // 16) * 2 * 2048), ("U", (Dv // 16) * 4 * 1024), ("GC", gc)]
     if bwd:
         hsc = (Dk // 16) * (Dv // 32) * 4
-        sizes += [("Hs", Dk * Dv * 2), ("Hsc", hsc), ("Rs", CH * Dv * 4), ("DH", Dk * Dv * 2), ("DHsc", hsc),
+        rsc = 4 * (Dv // 32) * 4
+        sizes += [("Hs", Dk * Dv * 2), ("Hsc", hsc), ("Rs", CH * Dv * 2), ("Rsc", rsc), ("DH", Dk * Dv * 2),
+                  ("DHsc", hsc),
                   ("DR", (Dv // 16) * 2 * 2048), ("Am", 8 * 2048)]
     off, out = 0, {}
     for n, per in sizes:
