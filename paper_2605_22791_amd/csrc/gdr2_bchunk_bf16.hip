@@ -272,13 +272,28 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   u4v ph, pd;     // 8 fp16 values of h and dh
   float psh, psd;  // their inverse scales
   bf4 pk, pb, pq;
+  // q, k, b, g of two key blocks are fetched together (they share cache lines);
+  // the second block's values wait in registers for the next prefetch
+  float4 pg2;
+  bf4 pk2, pb2, pq2;
 #define GDR2_PREFETCH(CB)                                                                  \
   {                                                                                        \
-    const int o_ = growc * kst + 16 * (CB) + 4 * cq;                                       \
-    pg = ldg_f4(Gp0 + o_);                                                                 \
-    pk = *reinterpret_cast<const bf4*>(Kp + o_);                                           \
-    pb = *reinterpret_cast<const bf4*>(Bp + o_);                                           \
-    pq = *reinterpret_cast<const bf4*>(Qp + o_);                                           \
+    if (((CB) & 1) == 0) {                                                                 \
+      const int o_ = growc * kst + 16 * (CB) + 4 * cq;                                     \
+      pg = ldg_f4(Gp0 + o_);                                                               \
+      pk = *reinterpret_cast<const bf4*>(Kp + o_);                                         \
+      pb = *reinterpret_cast<const bf4*>(Bp + o_);                                         \
+      pq = *reinterpret_cast<const bf4*>(Qp + o_);                                         \
+      pg2 = ldg_f4(Gp0 + o_ + 16);                                                         \
+      pk2 = *reinterpret_cast<const bf4*>(Kp + o_ + 16);                                   \
+      pb2 = *reinterpret_cast<const bf4*>(Bp + o_ + 16);                                   \
+      pq2 = *reinterpret_cast<const bf4*>(Qp + o_ + 16);                                   \
+    } else {                                                                               \
+      pg = pg2;                                                                            \
+      pk = pk2;                                                                            \
+      pb = pb2;                                                                            \
+      pq = pq2;                                                                            \
+    }                                                                                      \
     if (hact) {                                                                            \
       const int so_ = (16 * (CB) + hc) * DV + hv;                                          \
       ph = ldg16(Hc + so_);                                                                \
@@ -476,7 +491,6 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       x1 = mma3(zf[p], hf, x1);
       x2 = mma2b(dof[p], hf, x2);
       x3 = mma3(rfr[p], df, x3);
-      __builtin_amdgcn_sched_barrier(0);  // keep one K-step of operands live at a time
     }
 
     // G2 at the first (G2f) and last (G2l) row of every 16-row block, channel c
@@ -518,7 +532,6 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       af.lo = ld_tr8(sAl, LT, 32 * kb, 16 * i, lane);
       p1 = mma3(tf, kf, p1);
       p2 = mma3(af, kf, p2);
-      __builtin_amdgcn_sched_barrier(0);
     }
     // P3 = dT^T ((b k) 2^(G2_r - G2_e)) + dA_qk^T (q 2^(G2_r - G2_e)),  e = 16 i + 15, r >= 16 i;
     // for r in block j the factor is eL_r * 2^(G2f_j - G2l_i)
@@ -547,7 +560,6 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       af.lo = ld8(sAl + (16 * i + r16) * LT + r0);
       p3 = mma3(tf, split8(lb), p3);
       p3 = mma3(af, split8(lq), p3);
-      __builtin_amdgcn_sched_barrier(0);
     }
 
     // ---- elementwise chain (App. B.4) on rows rb + u, key c:
