@@ -36,8 +36,9 @@ def kernel_model(B, T, H, Dk, Dv, stored=True):
     counts C^2 D flops (half of the dense 2 C^2 D).  Bytes are each kernel's
     inputs read once plus its outputs written once, in the dtypes they have:
     q/k/v/b/w/dO/o and their gradients bf16, log-decay and its gradient fp32,
-    chunk states and R fp32, the fragment-ordered workspace tiles as stored
-    (split tiles hi + lo, Y single bf16, U fp32).
+    the fragment-ordered workspace tiles as stored (split tiles hi + lo, Y
+    single bf16, U fp32), and the backward's copies of the chunk states, their
+    gradients and R in fp16 with one fp32 scale per 16 x 32 block.
     """
     C = 64
     NC = B * H * (T // C)
@@ -49,6 +50,8 @@ def kernel_model(B, T, H, Dk, Dv, stored=True):
     kin, vin = C * Dk * h, C * Dv * h          # bf16 (C x D) tiles
     kf, vf = C * Dk * f, C * Dv * f            # fp32 (C x D) tiles
     st = Dk * Dv * f                          # fp32 state
+    st16 = Dk * Dv * h + (Dk // 16) * (Dv // 32) * f   # fp16 state copy + scales
+    r16 = C * Dv * h + (C // 16) * (Dv // 32) * f      # fp16 R + scales
     ws_y, ws_q, ws_a = C * Dk * h, C * Dk * 2 * h, C * C * 2 * h
     ws_k, ws_u, ws_g = C * Dk * 2 * h, C * Dv * f, -(-Dk * f // 256) * 256
     ws_am, ws_dr = C * C * 2 * h, C * Dv * 2 * h
@@ -58,14 +61,14 @@ def kernel_model(B, T, H, Dk, Dv, stored=True):
     intra_by = 3 * kin + kf + 2 * vin + ws_y + ws_q + ws_a + ws_k + ws_u + ws_g
     m["fwd_intra"] = (intra_fl, intra_by + (ws_am if stored else 0))
     m["fwd_state"] = (3 * mm + triv, ws_y + ws_q + ws_a + ws_k + ws_u + ws_g + vin + seq_state
-                      + (st + vf if stored else 0))
+                      + (st16 + r16 if stored else 0))
     m["bwd_recompute_intra"] = (intra_fl, intra_by + ws_am)
-    m["bwd_recompute_state"] = (2 * mm, ws_y + ws_k + ws_u + ws_g + st / NT + st + vf)
-    m["bwd_state"] = (triv + 3 * mm, ws_y + ws_q + ws_a + ws_k + ws_g + vin + seq_state + st + ws_dr)
+    m["bwd_recompute_state"] = (2 * mm, ws_y + ws_k + ws_u + ws_g + st / NT + st16 + r16)
+    m["bwd_state"] = (triv + 3 * mm, ws_y + ws_q + ws_a + ws_k + ws_g + vin + seq_state + st16 + ws_dr)
     # dZ = A^T dR, dT = -dZ R^T, dA_qk = dO R^T (causal); dZ h^T, dO h^T, R dh^T;
     # the three decay products with dT / dA_qk (causal)
     m["bwd_intra"] = (3 * triv + 3 * mm + 4 * tri,
-                      3 * kin + kf + 3 * vin + 2 * st + vf + ws_dr + ws_am + 3 * kin + 2 * vin + kf)
+                      3 * kin + kf + 3 * vin + 2 * st16 + r16 + ws_dr + ws_am + 3 * kin + 2 * vin + kf)
     return {k: (fl * NC, by * NC) for k, (fl, by) in m.items()}
 
 
