@@ -2,8 +2,9 @@
 // kernel: one 4-wave workgroup per chunk-head, two workgroups per CU.
 //
 // Per chunk it reads the chunk-start state h = S_0 and the gradient dh of the
-// chunk-end state (fp16 [Dk][Dv] with block scales, store_state_f16), R (fp16
-// fragment blocks with block scales, store_frag_f16) from the scan, dR
+// chunk-end state (fp16 [Dk][Dv] with block scales and each 32-value group in
+// the permuted K order, store_state_f16), R (fp16 fragment blocks with block
+// scales, store_frag_f16) from the scan, dR
 // from the reverse scan and A = (I + T)^{-1} from the intra-chunk recompute
 // (both split bf16 fragment blocks), and q, k, v, b, w, g, dO.
 //
@@ -23,6 +24,9 @@
 //     dG_{C-1} += gamma_C rowsum(dh * h) + sum_r X3_r k_r tail_r
 //     dlog_alpha = reverse cumulative sum of dG over the chunk
 // (tail_r = gamma_C / gamma_r).
+//
+// X3 is formed from the fp16 copies of R and dh as they are stored (their
+// products are exact in fp32); X1 and X2 from the split h.
 //
 // Work split: wave i owns the 16 chunk rows of block i: its dZ rows, the dT /
 // dA_qk tiles (i, j <= i) and every output tile (i, key block).  The key
@@ -53,36 +57,60 @@
 
 namespace gdr2 {
 
+// LDS layouts.  Rows are unpadded and the 16-byte pieces of a row are
+// permuted by an XOR with a function of the row, chosen so that every access
+// of the key-block loop is free of bank conflicts on gfx950: a 16-byte read
+// serves 16 lanes per cycle over 64 banks (the two lane quads of each half
+// wave with even, then odd, quad-index parity), 8-byte reads 32 lanes over 64
+// banks, and 4-byte accesses and all writes 32 banks.  Every element of an
+// array is addressed through its function below, writes and reads alike.
+//   dT^T, dA_qk^T planes [64][64] bf16:   8-element pieces ^ ((r & 3) ^ (((r >> 3) & 1) << 2))
+//   log2-decay tables [16][80] fp32:      4-element pieces ^ (((r >> 2) & 1) ^ (((r >> 2) & 3) << 1))
+//   k, b, q columns [16][64] bf16:        8-element pieces ^ ((r >> 1) & 7)
+//   h (bf16 hi / lo), dh (fp16) rows [16][DV + 16]:  8-element pieces ^ (r & 1)
+// Among the conflict-free choices these keep the loop's addresses few: most
+// accesses differ from another by a lane-independent constant.
+__device__ __forceinline__ int plane_ix(int r, int c) {
+  return r * 64 + ((((c >> 3) ^ (r & 3) ^ (((r >> 3) & 1) << 2)) << 3) | (c & 7));
+}
+constexpr int kTabLd = 80;
+__device__ __forceinline__ int tab_ix(int r, int c) {
+  return r * kTabLd + ((((c >> 2) ^ ((r >> 2) & 1) ^ (((r >> 2) & 3) << 1)) << 2) | (c & 3));
+}
+__device__ __forceinline__ int col_ix(int r, int c) { return r * 64 + ((((c >> 3) ^ ((r >> 1) & 7)) << 3) | (c & 7)); }
+template <int LH>
+__device__ __forceinline__ int row_ix(int r, int c) {
+  return r * LH + ((((c >> 3) ^ (r & 1)) << 3) | (c & 7));
+}
+
 template <int DK, int DV>
 struct BChunkCfg {
   static constexpr int NTHR = 256;
   static constexpr int NCB = DK / 16, NVB = DV / 16, KV = DV / 32;
-  static constexpr int LT = 64 + 8;   // dT^T, dA_qk^T planes, bf16 [64][LT]
-  static constexpr int LGT = 64 + 4;  // per-key-block fp32 tables [16][LGT]: G2, eL, eR
-  static constexpr int LXT = 64 + 8;  // k, b, q columns of a key block, bf16 [16][LXT]
-  static constexpr int LH = DV + 8;   // h, dh rows of a key block, bf16 hi/lo [16][LH]
-  // region 1: dR (fragment blocks, prologue) -> dT^T / dA_qk^T planes
+  static constexpr int LH = DV + 16;  // h (bf16 hi, lo) and dh (fp16) rows of a key block [16][LH] (row_ix)
+  // region 1: dR (fragment blocks, prologue) -> dT^T / dA_qk^T planes (plane_ix)
   static constexpr int SZ_DR = (int)WsBf16::dr(DV), SZ_AM = (int)WsBf16::am();
   static constexpr int OFF_T = 0;
-  static constexpr int SZ_T = 4 * 64 * LT * 2;
+  static constexpr int SZ_T = 4 * 64 * 64 * 2;
   // region 2: A (fragment blocks, prologue) -> the staged key block
   static constexpr int OFF_S = OFF_T + SZ_T;
-  static constexpr int OFF_G = OFF_S;
-  static constexpr int OFF_EL = OFF_G + 16 * LGT * 4;
-  static constexpr int OFF_ER = OFF_EL + 16 * LGT * 4;
-  static constexpr int OFF_X = OFF_ER + 16 * LGT * 4;
-  static constexpr int OFF_H = OFF_X + 3 * 16 * LXT * 2;
-  static constexpr int OFF_END_S = OFF_H + 4 * 16 * LH * 2;
+  static constexpr int SZ_TAB = 16 * kTabLd * 4;
+  static constexpr int OFF_G = OFF_S;                 // tables [16][64] fp32 (tab_ix): G2, eL, eR
+  static constexpr int OFF_EL = OFF_G + SZ_TAB;
+  static constexpr int OFF_ER = OFF_EL + SZ_TAB;
+  static constexpr int OFF_X = OFF_ER + SZ_TAB;       // k, b, q columns [16][64] bf16 (col_ix)
+  static constexpr int OFF_H = OFF_X + 3 * 16 * 64 * 2;
+  static constexpr int OFF_END_S = OFF_H + 3 * 16 * LH * 2;
   // small exchange arrays
   static constexpr int OFF_BK = OFF_END_S;              // block totals / first rows [2][4][16]
   static constexpr int OFF_HH = OFF_BK + 2 * 4 * 16 * 4;  // rowsum(dh * h)      [2][16]
   static constexpr int OFF_BT = OFF_HH + 2 * 16 * 4;      // dG block totals     [2][4][16]
   static constexpr int OFF_TL = OFF_BT + 2 * 4 * 16 * 4;  // tail-key sums       [2][4][16]
   static constexpr int LDS = OFF_TL + 2 * 4 * 16 * 4;
-  // fused stage: f + delta of the staged key block [16][LGT], the decay bias of
-  // the key head [DK], the inverse norms of the chunk's q and k rows [2][64]
+  // fused stage: f + delta of the staged key block [16][64] (tab_ix), the decay
+  // bias of the key head [DK], the inverse norms of the chunk's q and k rows [2][64]
   static constexpr int OFF_XS = LDS;
-  static constexpr int OFF_DL = OFF_XS + 16 * LGT * 4;
+  static constexpr int OFF_DL = OFF_XS + SZ_TAB;
   static constexpr int OFF_RN = OFF_DL + DK * 4;
   static constexpr int LDS_FUSED = OFF_RN + 2 * 64 * 4;
   // prologue: dR into region 1, A then R (fp16 fragment blocks) into region 2, by
@@ -93,7 +121,7 @@ struct BChunkCfg {
   static_assert(SZ_DR <= SZ_T && SZ_AM + SZ_R <= OFF_END_S - OFF_S, "prologue operands fit their regions");
   static_assert(NKB % (NTHR / 64) == 0 && SZ_DR % 1024 == 0 && SZ_AM % 1024 == 0, "whole blocks per wave");
   static_assert(LDS_FUSED <= 80 * 1024, "two workgroups per CU");
-  static_assert(16 * DV / 8 <= NTHR, "one 8-value piece of h / dh per thread");
+  static_assert(16 * DV / 8 <= NTHR, "one 16-byte piece of h / dh per thread");
 };
 
 __device__ __forceinline__ bf8 cat8(bf4 x, bf4 y) {
@@ -122,21 +150,25 @@ __device__ __forceinline__ void add_row4(const float* p, float (&v)[4]) {
 __device__ __forceinline__ float pick4(const float (&x)[4], int j) {
   return j == 0 ? x[0] : (j == 1 ? x[1] : (j == 2 ? x[2] : x[3]));
 }
-// position, inside its 32-value step, of the four values 32 p + 4 a + (0..3) in
-// the permuted K order (lane group G holds 4 G.. and 16 + 4 G.. as one 8-run)
-__device__ __forceinline__ int perm_pos(int a) { return a < 4 ? 8 * a : 8 * (a - 4) + 4; }
+// eight floats from two 16-byte pieces
+__device__ __forceinline__ void ldf4x2(const float* p0, const float* p1, float (&o)[8]) {
+  const float4 a = *reinterpret_cast<const float4*>(p0);
+  const float4 b = *reinterpret_cast<const float4*>(p1);
+  o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w;
+  o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
+}
 
 template <int DK, int DV, bool FUSED>
 __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   using C = BChunkCfg<DK, DV>;
   constexpr int NCB = C::NCB, NVB = C::NVB, KV = C::KV, NKB = C::NKB;
-  constexpr int LT = C::LT, LGT = C::LGT, LXT = C::LXT, LH = C::LH;
+  constexpr int LH = C::LH;
 
   extern __shared__ __align__(16) unsigned char smem[];
   __bf16* sTh = reinterpret_cast<__bf16*>(smem + C::OFF_T);  // dT^T [s][r]
-  __bf16* sTl = sTh + 64 * LT;
-  __bf16* sAh = sTl + 64 * LT;  // dA_qk^T [s][r]
-  __bf16* sAl = sAh + 64 * LT;
+  __bf16* sTl = sTh + 64 * 64;
+  __bf16* sAh = sTl + 64 * 64;  // dA_qk^T [s][r]
+  __bf16* sAl = sAh + 64 * 64;
   const unsigned char* sDR = smem + C::OFF_T;  // prologue: dR fragment blocks
   const unsigned char* sAm = smem + C::OFF_S;  // prologue: A fragment blocks
   const unsigned char* sR = smem + C::OFF_R;   // prologue: R, fp16 fragment blocks [row block][KV]
@@ -144,12 +176,11 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   float* sEL = reinterpret_cast<float*>(smem + C::OFF_EL);  // 2^(G2_s - G2 at its block's first row)
   float* sER = reinterpret_cast<float*>(smem + C::OFF_ER);  // 2^(G2 at its block's last row - G2_s)
   __bf16* sKc = reinterpret_cast<__bf16*>(smem + C::OFF_X);  // k [c][s]
-  __bf16* sBc = sKc + 16 * LXT;
-  __bf16* sQc = sBc + 16 * LXT;
+  __bf16* sBc = sKc + 16 * 64;
+  __bf16* sQc = sBc + 16 * 64;
   __bf16* sHh = reinterpret_cast<__bf16*>(smem + C::OFF_H);  // h [c][v], permuted K order
   __bf16* sHl = sHh + 16 * LH;
-  __bf16* sDh = sHl + 16 * LH;  // dh [c][v], permuted K order
-  __bf16* sDl = sDh + 16 * LH;
+  _Float16* sD16 = reinterpret_cast<_Float16*>(sHl + 16 * LH);  // dh [c][v] as stored: fp16, permuted K order
   float* sBK = reinterpret_cast<float*>(smem + C::OFF_BK);  // [0]: block totals, [1]: first rows
   float* sHH = reinterpret_cast<float*>(smem + C::OFF_HH);
   float* sBT = reinterpret_cast<float*>(smem + C::OFF_BT);
@@ -218,10 +249,36 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   const int rl = lane >> 2, cq = lane & 3, grow = 16 * wave + rl;
   const bool grin = grow < len;
   const int growc = min(grow, len - 1);
-  // h / dh staging role: row hc of the key block, values hv .. hv + 7
+  // h / dh staging role: row hc of the key block, 16-byte piece hv / 8 (the fp16
+  // copies keep each 32-value group in the permuted K order, so a piece is one
+  // lane's fragment run: values 32 p + 4 q + (0..3) and 32 p + 16 + 4 q + (0..3))
   const int hc = (8 * tid) / DV, hv = (8 * tid) % DV;
   const bool hact = tid < 2 * DV;
-  const int hp0 = (hv & ~31) + perm_pos((hv & 31) >> 2), hp1 = (hv & ~31) + perm_pos(((hv & 31) >> 2) + 1);
+  // Per-lane bases of the swizzled LDS accesses (element offsets; each equals
+  // its index function, with the per-step part a compile-time offset):
+  //   aH + 32 p         = row_ix(r16, 32 p + 8 g)                h, dh fragments
+  //   aHs               = row_ix(hc, hv)                         h, dh staging
+  //   aTr + 64 (32 kb + 4 e) = plane_ix(32 kb + 8 g + r16 / 4 + 4 e, 16 i + 4 (r16 % 4))
+  //   aP3[kb]           = plane_ix(16 i + r16, 32 kb + 8 g)
+  //   aTb[e] + 32 kb    = tab_ix(r16, 32 kb + 8 g + 4 e)         eR, eL pieces
+  //   aE                = tab_ix(r16, 16 i + 4 g)
+  //   aTs + 80 u        = tab_ix(4 cq + u, 16 i + rl)            table staging
+  //   aK[kb]            = col_ix(r16, 32 kb + 8 g),  aK4 = col_ix(r16, 16 i + 4 g)
+  //   aKs[u / 2] + 64 (u % 2) = col_ix(4 cq + u, 16 i + rl)       column staging
+  const int fT = ((r16 >> 2) & 1) ^ (((r16 >> 2) & 3) << 1), fTs = (cq & 1) ^ ((cq & 3) << 1);
+  const int fP = (r16 & 3) ^ (((r16 >> 3) & 1) << 2), fK = (r16 >> 1) & 7;
+  const int aH = r16 * LH + 8 * (g ^ (r16 & 1));
+  const int aHs = hc * LH + 8 * ((hv >> 3) ^ (hc & 1));
+  const int aTr = (8 * g + (r16 >> 2)) * 64 + 8 * ((2 * i + ((r16 & 3) >> 1)) ^ ((r16 >> 2) & 3) ^ ((g & 1) << 2)) +
+                  4 * (r16 & 1);
+  const int aP3[2] = {(16 * i + r16) * 64 + 8 * (g ^ fP), (16 * i + r16) * 64 + 8 * ((4 + g) ^ fP)};
+  const int aTb[2] = {r16 * kTabLd + 4 * ((2 * g) ^ fT), r16 * kTabLd + 4 * ((2 * g + 1) ^ fT)};
+  const int aE = r16 * kTabLd + 4 * ((4 * i + g) ^ fT);
+  const int aTs = 4 * cq * kTabLd + 4 * ((4 * i + (rl >> 2)) ^ fTs) + (rl & 3);
+  const int aK[2] = {r16 * 64 + 8 * (g ^ fK), r16 * 64 + 8 * ((4 + g) ^ fK)};
+  const int aK4 = r16 * 64 + 8 * ((2 * i + (g >> 1)) ^ fK) + 4 * (g & 1);
+  const int aKs[2] = {4 * cq * 64 + 8 * ((2 * i + (rl >> 3)) ^ ((2 * cq) & 7)) + (rl & 7),
+                      (4 * cq + 2) * 64 + 8 * ((2 * i + (rl >> 3)) ^ ((2 * cq + 1) & 7)) + (rl & 7)};
   // fused stage: exp(a) of the key head; its decay bias and the chunk's inverse
   // norms go to LDS (visible after the barrier that follows the prologue)
   float Adec = 0.f;
@@ -271,6 +328,8 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   float4 pg;
   u4v ph, pd;     // 8 fp16 values of h and dh
   float psh, psd;  // their inverse scales
+  float pds;       // lane p < KV: the scale of dh's value block p (key block of the prefetch)
+  float dscl;      //   the same for the staged key block
   bf4 pk, pb, pq;
   // q, k, b, g of two key blocks are fetched together (they share cache lines);
   // the second block's values wait in registers for the next prefetch
@@ -301,6 +360,7 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       psh = Hscc[(CB) * (DV / 32) + hv / 32];                                              \
       psd = DHscc[(CB) * (DV / 32) + hv / 32];                                             \
     }                                                                                      \
+    pds = lane < KV ? DHscc[(CB) * KV + lane] : 0.f;                                       \
   }
   // Writes key block CB's staged operands (parity PAR for the small arrays):
   // in-block cumulative sums of the log2-decay and their factor tables, the
@@ -313,7 +373,7 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       const float x_[4] = {pg.x + dl_.x, pg.y + dl_.y, pg.z + dl_.z, pg.w + dl_.w};        \
       const float rq_ = sRN[grow], rk_ = sRN[64 + grow];                                   \
       _Pragma("unroll") for (int u_ = 0; u_ < 4; ++u_) {                                   \
-        sXS[(4 * cq + u_) * LGT + grow] = x_[u_];                                          \
+        sXS[aTs + kTabLd * u_] = x_[u_];                                                   \
         pk[u_] = (__bf16)((float)pk[u_] * rk_);                                            \
         pq[u_] = (__bf16)((float)pq[u_] * rq_);                                            \
       }                                                                                    \
@@ -333,38 +393,31 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     }                                                                                      \
     _Pragma("unroll") for (int u_ = 0; u_ < 4; ++u_) {                                     \
       const float f_ = __shfl(x_[u_], cq), l_ = __shfl(x_[u_], 60 + cq);                   \
-      const int at_ = (4 * cq + u_) * LGT + grow;                                          \
+      const int at_ = aTs + kTabLd * u_;                                                   \
       sG[at_] = x_[u_];                                                                    \
       sEL[at_] = ex2(x_[u_] - f_);                                                         \
       sER[at_] = ex2(l_ - x_[u_]);                                                         \
       if (rl == 15) sBK[(0 * 4 + wave) * 16 + 4 * cq + u_] = x_[u_];                       \
       if (rl == 0) sBK[(1 * 4 + wave) * 16 + 4 * cq + u_] = x_[u_];                        \
-      sKc[(4 * cq + u_) * LXT + grow] = pk[u_];                                            \
-      sBc[(4 * cq + u_) * LXT + grow] = pb[u_];                                            \
-      sQc[(4 * cq + u_) * LXT + grow] = pq[u_];                                            \
+      const int ac_ = aKs[u_ >> 1] + 64 * (u_ & 1);                                        \
+      sKc[ac_] = pk[u_];                                                                   \
+      sBc[ac_] = pb[u_];                                                                   \
+      sQc[ac_] = pq[u_];                                                                   \
     }                                                                                      \
     if (hact) {                                                                            \
       float hx_[8], dx_[8];                                                                \
       load_state8(ph, psh, hx_);                                                           \
       load_state8(pd, psd, dx_);                                                           \
-      const Fr hf_ = split8(hx_), df_ = split8(dx_);                                       \
-      __bf16* bh_ = sHh + hc * LH;                                                         \
-      *reinterpret_cast<bf4*>(bh_ + hp0) = bf4{hf_.hi[0], hf_.hi[1], hf_.hi[2], hf_.hi[3]}; \
-      *reinterpret_cast<bf4*>(bh_ + hp1) = bf4{hf_.hi[4], hf_.hi[5], hf_.hi[6], hf_.hi[7]}; \
-      bh_ = sHl + hc * LH;                                                                 \
-      *reinterpret_cast<bf4*>(bh_ + hp0) = bf4{hf_.lo[0], hf_.lo[1], hf_.lo[2], hf_.lo[3]}; \
-      *reinterpret_cast<bf4*>(bh_ + hp1) = bf4{hf_.lo[4], hf_.lo[5], hf_.lo[6], hf_.lo[7]}; \
-      bh_ = sDh + hc * LH;                                                                 \
-      *reinterpret_cast<bf4*>(bh_ + hp0) = bf4{df_.hi[0], df_.hi[1], df_.hi[2], df_.hi[3]}; \
-      *reinterpret_cast<bf4*>(bh_ + hp1) = bf4{df_.hi[4], df_.hi[5], df_.hi[6], df_.hi[7]}; \
-      bh_ = sDl + hc * LH;                                                                 \
-      *reinterpret_cast<bf4*>(bh_ + hp0) = bf4{df_.lo[0], df_.lo[1], df_.lo[2], df_.lo[3]}; \
-      *reinterpret_cast<bf4*>(bh_ + hp1) = bf4{df_.lo[4], df_.lo[5], df_.lo[6], df_.lo[7]}; \
+      const Fr hf_ = split8(hx_);                                                          \
+      st8(sHh + aHs, hf_.hi);                                                              \
+      st8(sHl + aHs, hf_.lo);                                                              \
+      sts16(sD16 + aHs, pd);                                                               \
       float hh_ = hx_[0] * dx_[0];                                                         \
       _Pragma("unroll") for (int e_ = 1; e_ < 8; ++e_) hh_ += hx_[e_] * dx_[e_];           \
       _Pragma("unroll") for (int o_ = DV / 16; o_ >= 1; o_ >>= 1) hh_ += __shfl_xor(hh_, o_); \
       if ((tid % (DV / 8)) == 0) sHH[(PAR) * 16 + hc] = hh_;                               \
     }                                                                                      \
+    dscl = pds;                                                                            \
   }
   // v, w for dv / dw, in flight across the barrier
   bf4 vvr[NVB], wwr[NVB];
@@ -417,7 +470,8 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   }
   // dZ, dO and R rows of block i as A operands over the values, permuted K:
   // K-step p holds values 32 p + 4 g + (0..3) and 32 p + 16 + 4 g + (0..3)
-  Fr zf[KV], rfr[KV];
+  Fr zf[KV];
+  u4v rfr16[KV];  // R rows of block i, fp16 as stored (scale rsc(i * KV + p))
 #pragma unroll
   for (int p = 0; p < KV; ++p) {
     float x[8];
@@ -427,7 +481,7 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       x[4 + u] = zacc[2 * p + 1][u];
     }
     zf[p] = split8(x);
-    rfr[p] = frag_f16_split(*reinterpret_cast<const u4v*>(sR + (i * KV + p) * 1024 + 16 * lane), rsc(i * KV + p));
+    rfr16[p] = *reinterpret_cast<const u4v*>(sR + (i * KV + p) * 1024 + 16 * lane);
   }
   __syncthreads();  // dR and A are dead (R stays until the tiles below are done)
   if (16 * i + r16 >= len) {
@@ -445,9 +499,8 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     f4 ta = f4zero(), aa = f4zero();
 #pragma unroll
     for (int p = 0; p < KV; ++p) {
-      const Fr rj = (j == i) ? rfr[p]
-                             : frag_f16_split(*reinterpret_cast<const u4v*>(sR + (j * KV + p) * 1024 + 16 * lane),
-                                              rsc(j * KV + p));
+      const Fr rj = frag_f16_split(j == i ? rfr16[p] : *reinterpret_cast<const u4v*>(sR + (j * KV + p) * 1024 + 16 * lane),
+                                   rsc(j * KV + p));
       ta = mma3(zf[p], rj, ta);
       aa = mma2b(dof[p], rj, aa);
     }
@@ -458,14 +511,16 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       tv[u] = (rr + u > s) ? -ta[u] : 0.f;
       av[u] = (rr + u >= s) ? a.scale * aa[u] : 0.f;
     }
-    st4split(sTh + s * LT + rr, sTl + s * LT + rr, tv);
-    st4split(sAh + s * LT + rr, sAl + s * LT + rr, av);
+    const int at = plane_ix(s, rr);
+    st4split(sTh + at, sTl + at, tv);
+    st4split(sAh + at, sAl + at, av);
   }
   // tiles (0,1) and (2,3) above the diagonal share 32-wide operand steps with causal tiles
   if (i == 0 || i == 2) {
     const int s = 16 * (i + 1) + r16, rr = 16 * i + 4 * g;
-    st4split(sTh + s * LT + rr, sTl + s * LT + rr, f4zero());
-    st4split(sAh + s * LT + rr, sAl + s * LT + rr, f4zero());
+    const int at = plane_ix(s, rr);
+    st4split(sTh + at, sTl + at, f4zero());
+    st4split(sAh + at, sAl + at, f4zero());
   }
   __syncthreads();  // R is dead: key block 0 is staged over it
   GDR2_STAGE(0, 0)
@@ -479,18 +534,22 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     if (cb + 1 < NCB) GDR2_PREFETCH(cb + 1)
     const int c = 16 * cb + r16;  // this lane's key channel in every output tile
 
-    // X1 = dZ h^T, X2 = dO h^T, X3 = R dh^T   (rows 16 i + 4 g + u, key c)
+    // X1 = dZ h^T, X2 = dO h^T, X3 = R dh^T   (rows 16 i + 4 g + u, key c).
+    // X3 multiplies the fp16 copies of R and dh directly (exact products), one
+    // K-step per 32-value block, each scaled by the two blocks' scales.
     f4 x1 = f4zero(), x2 = f4zero(), x3 = f4zero();
 #pragma unroll
     for (int p = 0; p < KV; ++p) {
-      Fr hf, df;
-      hf.hi = ld8(sHh + r16 * LH + 32 * p + 8 * g);
-      hf.lo = ld8(sHl + r16 * LH + 32 * p + 8 * g);
-      df.hi = ld8(sDh + r16 * LH + 32 * p + 8 * g);
-      df.lo = ld8(sDl + r16 * LH + 32 * p + 8 * g);
+      Fr hf;
+      hf.hi = ld8(sHh + aH + 32 * p);
+      hf.lo = ld8(sHl + aH + 32 * p);
+      const f16x8 d16 = *reinterpret_cast<const f16x8*>(sD16 + aH + 32 * p);
       x1 = mma3(zf[p], hf, x1);
       x2 = mma2b(dof[p], hf, x2);
-      x3 = mma3(rfr[p], df, x3);
+      const f4 t = mma_f16(__builtin_bit_cast(f16x8, rfr16[p]), d16, f4zero());
+      const float sp = rsc(i * KV + p) * __int_as_float(__builtin_amdgcn_readlane(__float_as_int(dscl), p));
+#pragma unroll
+      for (int u = 0; u < 4; ++u) x3[u] += t[u] * sp;
     }
 
     // G2 at the first (G2f) and last (G2l) row of every 16-row block, channel c
@@ -507,8 +566,6 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     const float G2fi = pick4(G2f, i), G2li = pick4(G2l, i);
     // a diagonal block whose decay exceeds e^60 anywhere in this key block is formed element by element
     const bool uns = __ballot(G2fi - G2li > kDiagLimit2) != 0ull;
-    const float* elc = sEL + r16 * LGT;
-    const float* erc = sER + r16 * LGT;
 
     // P1 = dT (k 2^(G2_p - G2_s)),  P2 = dA_qk (k 2^(G2_p - G2_s)),  p = 16 i, s <= 16 i + 15;
     // for s in block j the factor is eR_s * 2^(G2f_i - G2l_j)
@@ -516,20 +573,22 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       if (kb > kbl) break;
-      const int s0 = 32 * kb + 8 * g, j = 2 * kb + (g >> 1);
+      const int j = 2 * kb + (g >> 1);  // block of keys s = 32 kb + 8 g ..
       const bool inc = j < i || (j == i && !uns);
       const float br = inc ? ex2(G2fi - pick4(G2l, j)) : 0.f;
       float er[8], ks[8], x[8];
-      ldf8(erc + s0, er);
-      unpack8(ld8(sKc + r16 * LXT + s0), ks);
+      ldf4x2(sER + aTb[0] + 32 * kb, sER + aTb[1] + 32 * kb, er);
+      unpack8(ld8(sKc + aK[kb]), ks);
 #pragma unroll
       for (int e = 0; e < 8; ++e) x[e] = ks[e] * er[e] * br;
       const Fr kf = split8(x);
       Fr tf, af;
-      tf.hi = ld_tr8(sTh, LT, 32 * kb, 16 * i, lane);
-      tf.lo = ld_tr8(sTl, LT, 32 * kb, 16 * i, lane);
-      af.hi = ld_tr8(sAh, LT, 32 * kb, 16 * i, lane);
-      af.lo = ld_tr8(sAl, LT, 32 * kb, 16 * i, lane);
+      // transposed reads: lane (G, 4 a + q) contributes rows 32 kb + 8 G + a (+ 4), columns 16 i + 4 q ..
+      const int t0 = aTr + 64 * 32 * kb, t1 = t0 + 64 * 4;
+      tf.hi = ld_tr8p(sTh + t0, sTh + t1);
+      tf.lo = ld_tr8p(sTl + t0, sTl + t1);
+      af.hi = ld_tr8p(sAh + t0, sAh + t1);
+      af.lo = ld_tr8p(sAl + t0, sAl + t1);
       p1 = mma3(tf, kf, p1);
       p2 = mma3(af, kf, p2);
     }
@@ -539,14 +598,15 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       if (kb < kbl) continue;
-      const int r0 = 32 * kb + 8 * g, j = 2 * kb + (g >> 1);
+      const int j = 2 * kb + (g >> 1);  // block of rows r = 32 kb + 8 g ..
       const bool inc = j > i || (j == i && !uns);
       const float br = inc ? ex2(pick4(G2f, j) - G2li) : 0.f;
       float el[8], kr[8], bv[8], qv[8], lb[8], lq[8];
-      ldf8(elc + r0, el);
-      unpack8(ld8(sKc + r16 * LXT + r0), kr);
-      unpack8(ld8(sBc + r16 * LXT + r0), bv);
-      unpack8(ld8(sQc + r16 * LXT + r0), qv);
+      ldf4x2(sEL + aTb[0] + 32 * kb, sEL + aTb[1] + 32 * kb, el);
+      const int ac = aK[kb];
+      unpack8(ld8(sKc + ac), kr);
+      unpack8(ld8(sBc + ac), bv);
+      unpack8(ld8(sQc + ac), qv);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float f = el[e] * br;
@@ -554,10 +614,11 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
         lq[e] = qv[e] * f;
       }
       Fr tf, af;
-      tf.hi = ld8(sTh + (16 * i + r16) * LT + r0);
-      tf.lo = ld8(sTl + (16 * i + r16) * LT + r0);
-      af.hi = ld8(sAh + (16 * i + r16) * LT + r0);
-      af.lo = ld8(sAl + (16 * i + r16) * LT + r0);
+      const int at = aP3[kb];
+      tf.hi = ld8(sTh + at);
+      tf.lo = ld8(sTl + at);
+      af.hi = ld8(sAh + at);
+      af.lo = ld8(sAl + at);
       p3 = mma3(tf, split8(lb), p3);
       p3 = mma3(af, split8(lq), p3);
     }
@@ -565,14 +626,15 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     // ---- elementwise chain (App. B.4) on rows rb + u, key c:
     // gamma_r = eL_r 2^(G2f_i),  tail_r = eR_r 2^(G2_{C-1} - G2l_i)
     const int rb = 16 * i + 4 * g;
-    const float4 eL4 = *reinterpret_cast<const float4*>(elc + rb);
-    const float4 eR4 = *reinterpret_cast<const float4*>(erc + rb);
+    const int ae = aE, ak = aK4;
+    const float4 eL4 = *reinterpret_cast<const float4*>(sEL + ae);
+    const float4 eR4 = *reinterpret_cast<const float4*>(sER + ae);
     const float elv[4] = {eL4.x, eL4.y, eL4.z, eL4.w}, erv[4] = {eR4.x, eR4.y, eR4.z, eR4.w};
-    const bf4 k4 = *reinterpret_cast<const bf4*>(sKc + r16 * LXT + rb);
-    const bf4 b4 = *reinterpret_cast<const bf4*>(sBc + r16 * LXT + rb);
-    const bf4 q4 = *reinterpret_cast<const bf4*>(sQc + r16 * LXT + rb);
+    const bf4 k4 = *reinterpret_cast<const bf4*>(sKc + ak);
+    const bf4 b4 = *reinterpret_cast<const bf4*>(sBc + ak);
+    const bf4 q4 = *reinterpret_cast<const bf4*>(sQc + ak);
     float4 xs4 = make_float4(0.f, 0.f, 0.f, 0.f);  // fused stage: f + delta of rows rb + u, key c
-    if constexpr (FUSED) xs4 = *reinterpret_cast<const float4*>(sXS + r16 * LGT + rb);
+    if constexpr (FUSED) xs4 = *reinterpret_cast<const float4*>(sXS + ae);
     const float gam0 = ex2(G2fi), tb = ex2(G2l[3] - G2li);
     float dgl[4], tailp = 0.f;
     float oq[4], ok[4], ob[4];  // dq, dk, db of rows rb + u, key c
@@ -587,23 +649,26 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
         // diagonal block element by element (in-block sums of the log2-decay):
         // every factor has exponent <= 0
         const int r = rb + u;
-        const float G = sG[r16 * LGT + r];
+        const float G = sG[tab_ix(r16, r)];
 #pragma unroll 1
         for (int s = 16 * i; s < 16 * i + 16; ++s) {
-          const float Gs = sG[r16 * LGT + s];
-          const float ks = (float)sKc[r16 * LXT + s];
+          const float Gs = sG[tab_ix(r16, s)];
+          const int as = col_ix(r16, s);
+          const float ks = (float)sKc[as];
           if (s <= r) {
             const float e = ex2(G - Gs);
-            const float dTv = (s < r) ? (float)sTh[s * LT + r] + (float)sTl[s * LT + r] : 0.f;
-            const float dAv = (float)sAh[s * LT + r] + (float)sAl[s * LT + r];
+            const int sr = plane_ix(s, r);
+            const float dTv = (s < r) ? (float)sTh[sr] + (float)sTl[sr] : 0.f;
+            const float dAv = (float)sAh[sr] + (float)sAl[sr];
             dEg += dTv * ks * e;
             dq += dAv * ks * e;
           }
           if (s >= r) {
             const float e = ex2(Gs - G);
-            const float dTv = (s > r) ? (float)sTh[r * LT + s] + (float)sTl[r * LT + s] : 0.f;
-            const float dAv = (float)sAh[r * LT + s] + (float)sAl[r * LT + s];
-            dKg += (dTv * (float)sBc[r16 * LXT + s] * ks + dAv * (float)sQc[r16 * LXT + s]) * e;
+            const int rs = plane_ix(r, s);
+            const float dTv = (s > r) ? (float)sTh[rs] + (float)sTl[rs] : 0.f;
+            const float dAv = (float)sAh[rs] + (float)sAl[rs];
+            dKg += (dTv * (float)sBc[as] * ks + dAv * (float)sQc[as]) * e;
           }
         }
       }

@@ -201,10 +201,16 @@ __device__ __forceinline__ void quad_transpose(float (&v)[4], int j) {
 // significant bits.  The state recursions themselves stay in fp32; only the
 // copies the chunk backward reads are rounded (relative 2^-12 per element,
 // against the bf16 rounding 2^-9 of the operator's outputs).
-//   H16 (Dk x Dv)            fp16, row-major, per chunk-head
+//   H16 (Dk x Dv)            fp16 rows, each 32-value group in the permuted K order
+//                            (store_state_f16), per chunk-head
 //   HSC (Dk / 16, Dv / 32)   fp32 inverse scales (x = fp16 value * HSC)
 typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+// 16 x 16 x 32 product of fp16 fragments, fp32 accumulation: the products of
+// fp16 values are exact in fp32
+__device__ __forceinline__ f4 mma_f16(f16x8 a, f16x8 b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
 
 // Largest value over the wave (x >= 0): DPP steps inside each 16-lane row
 // (quad swaps, then the half-row and row mirrors), then the four row maxima
@@ -251,21 +257,28 @@ __device__ __forceinline__ void state_shifts(const f4 (&s)[TPW], int (&sh)[TPW /
     sh[t2 / 2] = state_shift(wave_max(mx));
   }
 }
-// store_state_f16: the tiles as fp16 with their scales.  h0 points at the
-// wave's first row and column in the chunk's H16 (row stride ld), sc at its
-// first block's scale.  A quad transpose gives each lane four consecutive
-// columns of one row, so every store is 8 bytes.
+// store_state_f16: the tiles as fp16 with their scales, each 32-column group
+// in the permuted K order of the fragments (columns 4 m + e and 16 + 4 m + e,
+// e = 0..3, side by side at 8 m + e and 8 m + 4 + e).  h0 points at the wave's
+// first row and column in the chunk's H16 (row stride ld; the column a multiple
+// of 32), sc at its first block's scale; tiles 2 t2 and 2 t2 + 1 form 32-column
+// block t2.  A quad transpose gives each lane four consecutive columns of one
+// row from both tiles of a block: one 16-byte store.
 template <int TPW>
 __device__ __forceinline__ void store_state_f16(const f4 (&s)[TPW], const int (&sh)[TPW / 2], _Float16* h0, int ld,
                                                 float* sc, int lane) {
+  static_assert(TPW % 2 == 0, "whole 32-column blocks");
   const int g = lane >> 4, r16 = lane & 15, m = r16 >> 2, j = r16 & 3;
 #pragma unroll
-  for (int t = 0; t < TPW; ++t) {
-    const float f = ldexpf(1.f, sh[t / 2]);
-    float v[4] = {s[t][0] * f, s[t][1] * f, s[t][2] * f, s[t][3] * f};
-    quad_transpose(v, j);
-    const f16x4 hv = {(_Float16)v[0], (_Float16)v[1], (_Float16)v[2], (_Float16)v[3]};
-    *reinterpret_cast<f16x4*>(h0 + (size_t)(4 * g + j) * ld + 16 * t + 4 * m) = hv;
+  for (int t2 = 0; t2 < TPW / 2; ++t2) {
+    const float f = ldexpf(1.f, sh[t2]);
+    float v0[4] = {s[2 * t2][0] * f, s[2 * t2][1] * f, s[2 * t2][2] * f, s[2 * t2][3] * f};
+    float v1[4] = {s[2 * t2 + 1][0] * f, s[2 * t2 + 1][1] * f, s[2 * t2 + 1][2] * f, s[2 * t2 + 1][3] * f};
+    quad_transpose(v0, j);
+    quad_transpose(v1, j);
+    const f16x8 hv = {(_Float16)v0[0], (_Float16)v0[1], (_Float16)v0[2], (_Float16)v0[3],
+                      (_Float16)v1[0], (_Float16)v1[1], (_Float16)v1[2], (_Float16)v1[3]};
+    *reinterpret_cast<f16x8*>(h0 + (size_t)(4 * g + j) * ld + 32 * t2 + 8 * m) = hv;
   }
   if (lane == 0) {
 #pragma unroll

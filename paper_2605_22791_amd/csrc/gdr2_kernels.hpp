@@ -228,8 +228,9 @@ struct RecurArgs {
 //                   lane l holds U[16 i + 4 (l / 16) + u][16 vb + l % 16]
 //   GC   (Dk)       gamma_C, fp32
 // and, for the backward:
-//   Hs, DH (Dk x Dv) chunk-start states and chunk-end state gradients, fp16 with
-//                   per-block scales (store_state_f16 in gdr2_bf16.hpp)
+//   Hs, DH (Dk x Dv) chunk-start states and chunk-end state gradients, fp16 rows with
+//                   each 32-value group in the permuted K order and one scale per
+//                   16 x 32 block (store_state_f16 in gdr2_bf16.hpp)
 //   Rs   (64 x Dv)  R, fp16 permuted blocks [row block 4][value block Dv/32] with one
 //                   scale per block (store_frag_f16): the R operands of the chunk backward
 //   Am   (64 x 64)  A = (I + T)^{-1}, bf16 hi/lo, permuted blocks [key s block 4][row r block 2]

@@ -176,7 +176,12 @@ def seg_buffer_bytes(B, T, H, Dk, Dv, dtype="bf16"):
 
 
 def decode_states_f16(raw_f16, raw_scales, NC, Dk, Dv):
-    """fp16 chunk states with their per-(16 x 32)-block scales -> (NC, Dk, Dv) float64."""
-    h = raw_f16.view(np.float16).astype(np.float64).reshape(NC, Dk, Dv)
+    """fp16 chunk states with their per-(16 x 32)-block scales -> (NC, Dk, Dv) float64.
+
+    Each 32-column group is stored in the fragments' permuted order: column
+    4 m + e sits at 8 m + e and column 16 + 4 m + e at 8 m + 4 + e (e < 4)."""
+    c = np.arange(Dv)
+    pos = (c & ~31) + 8 * ((c & 15) >> 2) + 4 * ((c >> 4) & 1) + (c & 3)
+    h = raw_f16.view(np.float16).astype(np.float64).reshape(NC, Dk, Dv)[:, :, pos]
     sc = raw_scales.view(np.float32).astype(np.float64).reshape(NC, Dk // 16, Dv // 32)
     return h * np.repeat(np.repeat(sc, 16, axis=1), 32, axis=2)
