@@ -38,7 +38,8 @@ def kernel_model(B, T, H, Dk, Dv, stored=True):
     q/k/v/b/w/dO/o and their gradients bf16, log-decay and its gradient fp32,
     the fragment-ordered workspace tiles as stored (split tiles hi + lo, Y
     single bf16, U fp32), and the backward's copies of the chunk states, their
-    gradients and R in fp16 with one fp32 scale per 16 x 32 block.
+    gradients and R in fp16 with one fp32 scale per 16 x 32 block, A in fp16
+    with one fp32 scale per 16 x 16 block.
     """
     C = 64
     NC = B * H * (T // C)
@@ -54,7 +55,8 @@ def kernel_model(B, T, H, Dk, Dv, stored=True):
     r16 = C * Dv * h + (C // 16) * (Dv // 32) * f      # fp16 R + scales
     ws_y, ws_q, ws_a = C * Dk * h, C * Dk * 2 * h, C * C * 2 * h
     ws_k, ws_u, ws_g = C * Dk * 2 * h, C * Dv * f, -(-Dk * f // 256) * 256
-    ws_am, ws_dr = C * C * 2 * h, C * Dv * 2 * h
+    ws_am = C * C * h + (C // 16) * (C // 16) * f     # fp16 A, 16 x 16 blocks + scales
+    ws_dr = C * Dv * 2 * h                            # split bf16 dR
     seq_state = 2 * st / NT                   # S0 read + S_T write, per sequence
     m = {}
     intra_fl = tri + tri + solve + tri + triv

@@ -67,7 +67,7 @@ struct Layout {
   size_t Hs, Rs, DH, DR, DAqk, DT, DEg;  // backward extras
   size_t Hsc, DHsc, Rsc;                 // bf16 backward: scales of the fp16 chunk states and R
   size_t bY, bQ, bA, bK, bU, bG;         // bf16 forward (fragment order)
-  size_t bDR, bAm;                       // bf16 backward extras (fragment order)
+  size_t bDR, bAm, bAmsc;                // bf16 backward extras (dR split, A fp16 with scales)
   size_t sM, sN, sX;                     // segment maps and entry states (sequence-parallel scans)
   int nseg, seg_len;
   size_t vcoff, vct0, vclen, vsord;      // chunk table and scan order of a packed call (int32)
@@ -154,11 +154,13 @@ Layout layout(const gdr2_problem* p, bool bwd, int nseq = 0, int G = 1, bool fus
   }
   if (bwd) {
     if (p->dtype == GDR2_BF16) {
-      // fragment-ordered dR and A for the chunk-parallel backward
+      // dR (split bf16) and A (fp16 with block scales) for the chunk-parallel backward
       L.bDR = off;
       off += round_up(NC * WsBf16::dr(p->Dv));
       L.bAm = off;
       off += round_up(NC / G * WsBf16::am());  // A per key-head chunk
+      L.bAmsc = off;
+      off += round_up(NC / G * WsBf16::amsc());
     } else {
       L.DR = take(NC * CH * Dv);
       L.DAqk = take(NC * CH * CH);
@@ -488,7 +490,8 @@ struct FwdRun {
                        static_cast<const bf16_t*>(w), at<unsigned char>(ws, L.bY),
                        at<unsigned char>(ws, L.bQ), at<unsigned char>(ws, L.bA),
                        at<unsigned char>(ws, L.bK), at<float>(ws, L.bU), at<float>(ws, L.bG),
-                       save ? at<unsigned char>(ws, L.bAm) : nullptr, p->B, p->T, p->H, NT};
+                       save ? at<_Float16>(ws, L.bAm) : nullptr, p->B, p->T, p->H, NT};
+      ia.Amsc = save ? at<float>(ws, L.bAmsc) : nullptr;
       ia.vl = G.vl;
       ia.G = G.G;
       ia.st = G.st;
@@ -545,7 +548,8 @@ struct BwdRun {
                        static_cast<const bf16_t*>(w), at<unsigned char>(ws, L.bY),
                        at<unsigned char>(ws, L.bQ), at<unsigned char>(ws, L.bA),
                        at<unsigned char>(ws, L.bK), at<float>(ws, L.bU), at<float>(ws, L.bG),
-                       at<unsigned char>(ws, L.bAm), p->B, p->T, p->H, NT};
+                       at<_Float16>(ws, L.bAm), p->B, p->T, p->H, NT};
+      ia.Amsc = at<float>(ws, L.bAmsc);
       ia.vl = G.vl;
       ia.G = G.G;
       ia.st = G.st;
@@ -567,7 +571,7 @@ struct BwdRun {
         if (e != hipSuccess) return e;
       }
       BScanArgs ba{ia.Y, ia.Qg, ia.Aqk, ia.KtT, ia.GC, static_cast<const bf16_t*>(dout), dST, dS0,
-                   at<_Float16>(ws, L.DH), at<unsigned char>(ws, L.bDR), G.nscan, p->T, p->H, NT, p->scale};
+                   at<_Float16>(ws, L.DH), at<__bf16>(ws, L.bDR), G.nscan, p->T, p->H, NT, p->scale};
       ba.DHsc = at<float>(ws, L.DHsc);
       ba.vl = G.vl;
       ba.G = G.G;
@@ -577,13 +581,14 @@ struct BwdRun {
       BChunkBf16Args ca{static_cast<const bf16_t*>(q), static_cast<const bf16_t*>(k),
                         static_cast<const bf16_t*>(v), g, static_cast<const bf16_t*>(b),
                         static_cast<const bf16_t*>(w), static_cast<const bf16_t*>(dout), at<_Float16>(ws, L.Hs),
-                        at<_Float16>(ws, L.DH), at<_Float16>(ws, L.Rs), at<unsigned char>(ws, L.bDR),
-                        at<unsigned char>(ws, L.bAm), static_cast<bf16_t*>(dq), static_cast<bf16_t*>(dk),
+                        at<_Float16>(ws, L.DH), at<_Float16>(ws, L.Rs), at<__bf16>(ws, L.bDR),
+                        at<_Float16>(ws, L.bAm), static_cast<bf16_t*>(dq), static_cast<bf16_t*>(dk),
                         static_cast<bf16_t*>(dv), static_cast<bf16_t*>(db), static_cast<bf16_t*>(dw), dg,
                         p->B, p->T, p->H, NT, p->scale};
       ca.Hsc = at<float>(ws, L.Hsc);
       ca.DHsc = at<float>(ws, L.DHsc);
       ca.Rsc = at<float>(ws, L.Rsc);
+      ca.Amsc = at<float>(ws, L.bAmsc);
       ca.vl = G.vl;
       ca.G = G.G;
       if (G.G > 1) {  // the group's key-side gradients add up on the key-head axis

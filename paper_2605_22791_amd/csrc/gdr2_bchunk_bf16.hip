@@ -4,9 +4,9 @@
 // Per chunk it reads the chunk-start state h = S_0 and the gradient dh of the
 // chunk-end state (fp16 [Dk][Dv] with block scales and each 32-value group in
 // the permuted K order, store_state_f16), R (fp16 fragment blocks with block
-// scales, store_frag_f16) from the scan, dR
-// from the reverse scan and A = (I + T)^{-1} from the intra-chunk recompute
-// (both split bf16 fragment blocks), and q, k, v, b, w, g, dO.
+// scales, store_frag_f16) from the scan, dR from the reverse scan and
+// A = (I + T)^{-1} from the intra-chunk recompute (16 x 16 blocks: dR split
+// bf16, A fp16 with block scales, store_tile_f16), and q, k, v, b, w, g, dO.
 //
 // Because R = A (Z - Ebar h) (App. A.2), the gate-aware WY VJP of App. B.2
 // needs neither dA nor dY:
@@ -30,19 +30,26 @@
 //
 // Work split: wave i owns the 16 chunk rows of block i: its dZ rows, the dT /
 // dA_qk tiles (i, j <= i) and every output tile (i, key block).  The key
-// blocks run in a loop; each stages its h and dh rows and its G2, k, b, q
-// columns in LDS while the next block's loads are in flight.  dT and dA_qk
-// live in LDS transposed ([s][r], split hi/lo) so that both the row-r and the
-// column-s operands of the decay products are plain or transposed reads.
+// blocks run in a loop; each stages its h and dh rows, its G2, k, b, q columns
+// and the decay-scaled operands of the decay products in LDS while the next
+// block's loads are in flight.  dT and dA_qk live in LDS transposed ([s][r],
+// split hi/lo) so that both the row-r and the column-s operands of the decay
+// products are plain or transposed reads.
 //
-// Decay factors (App. D.4 / the forward kernels): for the products over s <= r
-// of row block i the factor is split at p = 16 i, 2^(G2_r - G2_p) after the
-// product and 2^(G2_p - G2_s) inside the operand; for the products over r >= s
-// of key-row block i it is split at e = 16 i + 15.  Both inner factors are <= 1
-// outside the diagonal block and bounded by one block's decay inside it; a
-// diagonal block whose decay exceeds e^60 is formed element by element.
+// Decay factors (App. D.4 / the forward kernels), with 16-row blocks j and
+// G2f_j, G2l_j the cumulative log2-decay at their first and last rows: for the
+// products over s <= r of row block i the factor 2^(G2_r - G2_s) is
+//     2^(G2_r - G2f_i) * 2^(G2f_i - G2l_j) * 2^(G2l_j - G2_s)        (s in block j),
+// the last part inside the operand k_s eR_s, which is the same for every row
+// block and is built once per key block, the middle one applied to block j's
+// 16-deep product, the first one after the sum.  The products over r >= s of
+// key-row block i use b_r k_r eL_r and q_r eL_r with eL_r = 2^(G2_r - G2f_j)
+// and the block factor 2^(G2f_j - G2l_i).  Every part is <= 1 except a
+// diagonal block's factor, bounded by one block's decay; a diagonal block
+// whose decay exceeds e^60 is formed element by element.
 //
-// Precision: every product is fp32-accurate (split hi/lo; dO is exact bf16).
+// Precision: every product is fp32-accurate on its operands (split hi/lo; dO
+// is exact bf16; X3 multiplies the fp16 copies exactly).
 //
 // Fused input stage (FUSED; App. C.1, App. D.2): q and k arrive raw and are
 // normalised as they are staged, with the inverse norms the forward kept; the
@@ -57,21 +64,30 @@
 
 namespace gdr2 {
 
-// LDS layouts.  Rows are unpadded and the 16-byte pieces of a row are
-// permuted by an XOR with a function of the row, chosen so that every access
-// of the key-block loop is free of bank conflicts on gfx950: a 16-byte read
-// serves 16 lanes per cycle over 64 banks (the two lane quads of each half
-// wave with even, then odd, quad-index parity), 8-byte reads 32 lanes over 64
-// banks, and 4-byte accesses and all writes 32 banks.  Every element of an
-// array is addressed through its function below, writes and reads alike.
-//   dT^T, dA_qk^T planes [64][64] bf16:   8-element pieces ^ ((r & 3) ^ (((r >> 3) & 1) << 2))
-//   log2-decay tables [16][80] fp32:      4-element pieces ^ (((r >> 2) & 1) ^ (((r >> 2) & 3) << 1))
+// LDS layouts.  The 16-byte pieces of a row are permuted by an XOR with a
+// function of the row, chosen so that every access of the key-block loop is
+// free of bank conflicts on gfx950: a 16-byte read serves 16 lanes per cycle
+// over 64 banks (the two lane quads of each half wave with even, then odd,
+// quad-index parity), 8-byte reads 32 lanes over 64 banks, and 4-byte accesses
+// and all writes 32 banks.  Every element of an array is addressed through its
+// function below, writes and reads alike.
+//   dT^T, dA_qk^T planes [64][LP] bf16:   8-element pieces ^ ((r >> 3) & 1)                   (LP = 80)
+//                                         8-element pieces ^ ((r & 7) ^ ((r >> 3) & 1))       (LP = 64)
+//   log2-decay sums [16][80] fp32:        4-element pieces ^ (((r >> 2) & 1) ^ (((r >> 2) & 3) << 1))
 //   k, b, q columns [16][64] bf16:        8-element pieces ^ ((r >> 1) & 7)
 //   h (bf16 hi / lo), dh (fp16) rows [16][DV + 16]:  8-element pieces ^ (r & 1)
+//   decay-scaled operands [64][16] bf16 hi / lo (rows s, key channels): plain
 // Among the conflict-free choices these keep the loop's addresses few: most
-// accesses differ from another by a lane-independent constant.
+// accesses differ from another by a lane-independent constant.  The padded
+// planes (LP = 80) need 8 KB more than LP = 64, which the fused stage's
+// tables leave no room for.  Consecutive planes and k / b / q arrays sit 16
+// bytes further apart than their size: reads of the same element in two of
+// them are then not paired into one ds_read2st64_b64, whose halves are served
+// like 8-byte writes (32 banks, 16 lanes per cycle) and conflict here.
+template <int LP>
 __device__ __forceinline__ int plane_ix(int r, int c) {
-  return r * 64 + ((((c >> 3) ^ (r & 3) ^ (((r >> 3) & 1) << 2)) << 3) | (c & 7));
+  const int f = LP == 80 ? ((r >> 3) & 1) : ((r & 7) ^ ((r >> 3) & 1));
+  return r * LP + ((((c >> 3) ^ f) << 3) | (c & 7));
 }
 constexpr int kTabLd = 80;
 __device__ __forceinline__ int tab_ix(int r, int c) {
@@ -83,36 +99,38 @@ __device__ __forceinline__ int row_ix(int r, int c) {
   return r * LH + ((((c >> 3) ^ (r & 1)) << 3) | (c & 7));
 }
 
-template <int DK, int DV>
+template <int DK, int DV, bool FUSED>
 struct BChunkCfg {
   static constexpr int NTHR = 256;
   static constexpr int NCB = DK / 16, NVB = DV / 16, KV = DV / 32;
-  static constexpr int LH = DV + 16;  // h (bf16 hi, lo) and dh (fp16) rows of a key block [16][LH] (row_ix)
-  // region 1: dR (fragment blocks, prologue) -> dT^T / dA_qk^T planes (plane_ix)
+  static constexpr int LP = FUSED ? 64 : 80;  // dT^T / dA_qk^T plane rows (plane_ix)
+  static constexpr int LH = DV + 16;          // h (bf16 hi, lo) and dh (fp16) rows of a key block [16][LH] (row_ix)
+  // region 1: dR (fragment blocks, prologue) -> dT^T / dA_qk^T planes
   static constexpr int SZ_DR = (int)WsBf16::dr(DV), SZ_AM = (int)WsBf16::am();
   static constexpr int OFF_T = 0;
-  static constexpr int SZ_T = 4 * 64 * 64 * 2;
+  static constexpr int PSZ = 64 * LP + 8;  // one plane, elements
+  static constexpr int CSZ = 16 * 64 + 8;  // one k / b / q array, elements
+  static constexpr int SZ_T = 4 * PSZ * 2;
   // region 2: A (fragment blocks, prologue) -> the staged key block
   static constexpr int OFF_S = OFF_T + SZ_T;
   static constexpr int SZ_TAB = 16 * kTabLd * 4;
-  static constexpr int OFF_G = OFF_S;                 // tables [16][64] fp32 (tab_ix): G2, eL, eR
-  static constexpr int OFF_EL = OFF_G + SZ_TAB;
-  static constexpr int OFF_ER = OFF_EL + SZ_TAB;
-  static constexpr int OFF_X = OFF_ER + SZ_TAB;       // k, b, q columns [16][64] bf16 (col_ix)
-  static constexpr int OFF_H = OFF_X + 3 * 16 * 64 * 2;
+  static constexpr int OFF_G = OFF_S;            // in-block log2-decay sums [16][64] fp32 (tab_ix)
+  static constexpr int OFF_XO = OFF_G + SZ_TAB;  // k eR, b k eL, q eL, hi / lo [6][64][16] bf16
+  static constexpr int OFF_X = OFF_XO + 6 * 64 * 16 * 2;  // k, b, q columns [16][64] bf16 (col_ix)
+  static constexpr int OFF_H = OFF_X + 3 * CSZ * 2;
   static constexpr int OFF_END_S = OFF_H + 3 * 16 * LH * 2;
   // small exchange arrays
   static constexpr int OFF_BK = OFF_END_S;              // block totals / first rows [2][4][16]
   static constexpr int OFF_HH = OFF_BK + 2 * 4 * 16 * 4;  // rowsum(dh * h)      [2][16]
   static constexpr int OFF_BT = OFF_HH + 2 * 16 * 4;      // dG block totals     [2][4][16]
   static constexpr int OFF_TL = OFF_BT + 2 * 4 * 16 * 4;  // tail-key sums       [2][4][16]
-  static constexpr int LDS = OFF_TL + 2 * 4 * 16 * 4;
+  static constexpr int LDS_BASE = OFF_TL + 2 * 4 * 16 * 4;
   // fused stage: f + delta of the staged key block [16][64] (tab_ix), the decay
   // bias of the key head [DK], the inverse norms of the chunk's q and k rows [2][64]
-  static constexpr int OFF_XS = LDS;
+  static constexpr int OFF_XS = LDS_BASE;
   static constexpr int OFF_DL = OFF_XS + SZ_TAB;
   static constexpr int OFF_RN = OFF_DL + DK * 4;
-  static constexpr int LDS_FUSED = OFF_RN + 2 * 64 * 4;
+  static constexpr int LDS = FUSED ? OFF_RN + 2 * 64 * 4 : LDS_BASE;
   // prologue: dR into region 1, A then R (fp16 fragment blocks) into region 2, by
   // direct global -> LDS loads of 1 KB per wave instruction
   static constexpr int SZ_R = (int)WsBf16::rs(DV);
@@ -120,9 +138,28 @@ struct BChunkCfg {
   static constexpr int NKB = (SZ_DR + SZ_AM + SZ_R) / 1024;
   static_assert(SZ_DR <= SZ_T && SZ_AM + SZ_R <= OFF_END_S - OFF_S, "prologue operands fit their regions");
   static_assert(NKB % (NTHR / 64) == 0 && SZ_DR % 1024 == 0 && SZ_AM % 1024 == 0, "whole blocks per wave");
-  static_assert(LDS_FUSED <= 80 * 1024, "two workgroups per CU");
+  static_assert(LDS <= 80 * 1024, "two workgroups per CU");
   static_assert(16 * DV / 8 <= NTHR, "one 16-byte piece of h / dh per thread");
 };
+
+// 16 x 16 x 16 products on split operands (lane l: row / column l % 16, K
+// elements 4 (l / 16) + e): one decay-scaled key block per K-step
+struct Fr4 {
+  bf4 hi, lo;
+};
+typedef short s4v __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ f4 mma16(bf4 a, bf4 b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s4v, a), __builtin_bit_cast(s4v, b), c, 0, 0, 0);
+}
+// the cross terms first, as in mma3
+__device__ __forceinline__ f4 mma3_16(const Fr4& a, const Fr4& b, f4 c) {
+  c = mma16(a.lo, b.hi, c);
+  c = mma16(a.hi, b.lo, c);
+  return mma16(a.hi, b.hi, c);
+}
+__device__ __forceinline__ bf4 ld_tr4(const __bf16* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((GDR2_LDS bf4*)(p));
+}
 
 __device__ __forceinline__ bf8 cat8(bf4 x, bf4 y) {
   bf8 r;
@@ -150,34 +187,34 @@ __device__ __forceinline__ void add_row4(const float* p, float (&v)[4]) {
 __device__ __forceinline__ float pick4(const float (&x)[4], int j) {
   return j == 0 ? x[0] : (j == 1 ? x[1] : (j == 2 ? x[2] : x[3]));
 }
-// eight floats from two 16-byte pieces
-__device__ __forceinline__ void ldf4x2(const float* p0, const float* p1, float (&o)[8]) {
-  const float4 a = *reinterpret_cast<const float4*>(p0);
-  const float4 b = *reinterpret_cast<const float4*>(p1);
-  o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w;
-  o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
-}
 
 template <int DK, int DV, bool FUSED>
 __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
-  using C = BChunkCfg<DK, DV>;
+  using C = BChunkCfg<DK, DV, FUSED>;
   constexpr int NCB = C::NCB, NVB = C::NVB, KV = C::KV, NKB = C::NKB;
-  constexpr int LH = C::LH;
+  constexpr int LH = C::LH, LP = C::LP;
 
   extern __shared__ __align__(16) unsigned char smem[];
   __bf16* sTh = reinterpret_cast<__bf16*>(smem + C::OFF_T);  // dT^T [s][r]
-  __bf16* sTl = sTh + 64 * 64;
-  __bf16* sAh = sTl + 64 * 64;  // dA_qk^T [s][r]
-  __bf16* sAl = sAh + 64 * 64;
+  __bf16* sTl = sTh + C::PSZ;
+  __bf16* sAh = sTl + C::PSZ;  // dA_qk^T [s][r]
+  __bf16* sAl = sAh + C::PSZ;
   const unsigned char* sDR = smem + C::OFF_T;  // prologue: dR fragment blocks
   const unsigned char* sAm = smem + C::OFF_S;  // prologue: A fragment blocks
   const unsigned char* sR = smem + C::OFF_R;   // prologue: R, fp16 fragment blocks [row block][KV]
   float* sG = reinterpret_cast<float*>(smem + C::OFF_G);    // in-block cumsum of log2-decay [c][s]
-  float* sEL = reinterpret_cast<float*>(smem + C::OFF_EL);  // 2^(G2_s - G2 at its block's first row)
-  float* sER = reinterpret_cast<float*>(smem + C::OFF_ER);  // 2^(G2 at its block's last row - G2_s)
+  // decay-scaled operands of the products over the key block, split hi / lo, [s][c]:
+  // k_s eR_s (eR_s = 2^(G2 at the last row of s's 16-row block - G2_s)), b_r k_r eL_r
+  // and q_r eL_r (eL_r = 2^(G2_r - G2 at the first row of r's block))
+  __bf16* sXh = reinterpret_cast<__bf16*>(smem + C::OFF_XO);
+  __bf16* sXl = sXh + 64 * 16;
+  __bf16* sBh = sXl + 64 * 16;
+  __bf16* sBl = sBh + 64 * 16;
+  __bf16* sQh = sBl + 64 * 16;
+  __bf16* sQl = sQh + 64 * 16;
   __bf16* sKc = reinterpret_cast<__bf16*>(smem + C::OFF_X);  // k [c][s]
-  __bf16* sBc = sKc + 16 * 64;
-  __bf16* sQc = sBc + 16 * 64;
+  __bf16* sBc = sKc + C::CSZ;
+  __bf16* sQc = sBc + C::CSZ;
   __bf16* sHh = reinterpret_cast<__bf16*>(smem + C::OFF_H);  // h [c][v], permuted K order
   __bf16* sHl = sHh + 16 * LH;
   _Float16* sD16 = reinterpret_cast<_Float16*>(sHl + 16 * LH);  // dh [c][v] as stored: fp16, permuted K order
@@ -204,6 +241,7 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     return;
   }
   const size_t ch = cp.ch, row0 = cp.row0;
+  const size_t kch = key_ch(a.vl, ch, a.H, a.G, a.NT);  // the key head's chunk (A)
   // Rows in use.  Loads read in-range rows only (rows past a partial chunk's
   // end re-read its last row); g, k and dO of those rows are then taken as
   // zero, which makes every term they could add to a valid row vanish (their
@@ -219,7 +257,6 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   const size_t kb0 = row0 * KST + (size_t)hk * DK, vb0 = row0 * VST + (size_t)h * DV;
   const size_t ko0 = kb0;  // key-side outputs
   const int i = wave;  // the row block this wave owns
-  const int kbl = i >> 1;
 
   // per-chunk bases (uniform) and 32-bit lane offsets: KST = (H / G) Dk, VST = H Dv
   const __bf16* Qp = reinterpret_cast<const __bf16*>(a.q) + kb0;
@@ -256,26 +293,24 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   const bool hact = tid < 2 * DV;
   // Per-lane bases of the swizzled LDS accesses (element offsets; each equals
   // its index function, with the per-step part a compile-time offset):
-  //   aH + 32 p         = row_ix(r16, 32 p + 8 g)                h, dh fragments
-  //   aHs               = row_ix(hc, hv)                         h, dh staging
-  //   aTr + 64 (32 kb + 4 e) = plane_ix(32 kb + 8 g + r16 / 4 + 4 e, 16 i + 4 (r16 % 4))
-  //   aP3[kb]           = plane_ix(16 i + r16, 32 kb + 8 g)
-  //   aTb[e] + 32 kb    = tab_ix(r16, 32 kb + 8 g + 4 e)         eR, eL pieces
-  //   aE                = tab_ix(r16, 16 i + 4 g)
-  //   aTs + 80 u        = tab_ix(4 cq + u, 16 i + rl)            table staging
-  //   aK[kb]            = col_ix(r16, 32 kb + 8 g),  aK4 = col_ix(r16, 16 i + 4 g)
-  //   aKs[u / 2] + 64 (u % 2) = col_ix(4 cq + u, 16 i + rl)       column staging
+  //   aH + 32 p              = row_ix(r16, 32 p + 8 g)                   h, dh fragments
+  //   aHs                    = row_ix(hc, hv)                            h, dh staging
+  //   aTr + 16 LP j          = plane_ix(16 j + 4 g + r16 / 4, 16 i + 4 (r16 % 4))   transposed plane reads
+  //   aP3 + 16 j             = plane_ix(16 i + r16, 16 j + 4 g)          plane rows (LP = 80)
+  //   aXr + 256 j            = (16 j + 4 g + r16 / 4) * 16 + 4 (r16 % 4)   decay-scaled operands, transposed
+  //   aXs                    = grow * 16 + 4 cq                          their staging
+  //   aE                     = tab_ix(r16, 16 i + 4 g),  aTs + 80 u = tab_ix(4 cq + u, 16 i + rl)
+  //   aK4                    = col_ix(r16, 16 i + 4 g),  aKs[u / 2] + 64 (u % 2) = col_ix(4 cq + u, 16 i + rl)
   const int fT = ((r16 >> 2) & 1) ^ (((r16 >> 2) & 3) << 1), fTs = (cq & 1) ^ ((cq & 3) << 1);
-  const int fP = (r16 & 3) ^ (((r16 >> 3) & 1) << 2), fK = (r16 >> 1) & 7;
+  const int fK = (r16 >> 1) & 7;
   const int aH = r16 * LH + 8 * (g ^ (r16 & 1));
   const int aHs = hc * LH + 8 * ((hv >> 3) ^ (hc & 1));
-  const int aTr = (8 * g + (r16 >> 2)) * 64 + 8 * ((2 * i + ((r16 & 3) >> 1)) ^ ((r16 >> 2) & 3) ^ ((g & 1) << 2)) +
-                  4 * (r16 & 1);
-  const int aP3[2] = {(16 * i + r16) * 64 + 8 * (g ^ fP), (16 * i + r16) * 64 + 8 * ((4 + g) ^ fP)};
-  const int aTb[2] = {r16 * kTabLd + 4 * ((2 * g) ^ fT), r16 * kTabLd + 4 * ((2 * g + 1) ^ fT)};
+  const int aTr = plane_ix<LP>(4 * g + (r16 >> 2), 16 * i + 4 * (r16 & 3));
+  const int aP3 = plane_ix<LP>(16 * i + r16, 4 * g);
+  const int aXr = (4 * g + (r16 >> 2)) * 16 + 4 * (r16 & 3);
+  const int aXs = grow * 16 + 4 * cq;
   const int aE = r16 * kTabLd + 4 * ((4 * i + g) ^ fT);
   const int aTs = 4 * cq * kTabLd + 4 * ((4 * i + (rl >> 2)) ^ fTs) + (rl & 3);
-  const int aK[2] = {r16 * 64 + 8 * (g ^ fK), r16 * 64 + 8 * ((4 + g) ^ fK)};
   const int aK4 = r16 * 64 + 8 * ((2 * i + (g >> 1)) ^ fK) + 4 * (g & 1);
   const int aKs[2] = {4 * cq * 64 + 8 * ((2 * i + (rl >> 3)) ^ ((2 * cq) & 7)) + (rl & 7),
                       (4 * cq + 2) * 64 + 8 * ((2 * i + (rl >> 3)) ^ ((2 * cq + 1) & 7)) + (rl & 7)};
@@ -295,8 +330,8 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   // rows and the operands of key block 0
   {
     // wave w moves the 1 KB blocks w, w + 4, ... of dR | A | R straight into LDS
-    const unsigned char* DRc = a.DR + ch * WsBf16::dr(DV);
-    const unsigned char* Amc = a.Am + key_ch(a.vl, ch, H, a.G, a.NT) * WsBf16::am();  // A: per key head
+    const unsigned char* DRc = reinterpret_cast<const unsigned char*>(a.DR) + ch * WsBf16::dr(DV);
+    const unsigned char* Amc = reinterpret_cast<const unsigned char*>(a.Am) + kch * WsBf16::am();  // A: per key head
     const unsigned char* Rcb = reinterpret_cast<const unsigned char*>(Rc);
 #pragma unroll
     for (int m = 0; m < NKB / 4; ++m) {
@@ -316,6 +351,8 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       __builtin_amdgcn_global_load_lds((void*)(src + 16 * lane), (GDR2_LDS void*)dst, 16, 0, 0);
     }
   }
+  // A's block scales (key block i, row block rb) in lanes rb < 4
+  const float ascl = lane < 4 ? a.Amsc[kch * (WsBf16::amsc() / 4) + 4 * i + lane] : 0.f;
   // R's block scales: lane j * KV + p holds that of row block j, value block p
   const float rscl = lane < 4 * KV ? Rscc[lane] : 0.f;
   const auto rsc = [&](int blk) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(rscl), blk)); };
@@ -363,8 +400,9 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     pds = lane < KV ? DHscc[(CB) * KV + lane] : 0.f;                                       \
   }
   // Writes key block CB's staged operands (parity PAR for the small arrays):
-  // in-block cumulative sums of the log2-decay and their factor tables, the
-  // block totals and first rows, k / b / q columns, h / dh rows, rowsum(dh * h).
+  // in-block cumulative sums of the log2-decay, the block totals and first
+  // rows, the decay-scaled operands, k / b / q columns, h / dh rows,
+  // rowsum(dh * h).
 #define GDR2_STAGE(PAR, CBS)                                                               \
   {                                                                                        \
     const int cbs_ = (CBS);                                                                \
@@ -391,12 +429,15 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
         x_[u_] += lane >= o_ ? y_ : 0.f;                                                   \
       }                                                                                    \
     }                                                                                      \
+    f4 xk_, xb_, xq_;                                                                      \
     _Pragma("unroll") for (int u_ = 0; u_ < 4; ++u_) {                                     \
       const float f_ = __shfl(x_[u_], cq), l_ = __shfl(x_[u_], 60 + cq);                   \
-      const int at_ = aTs + kTabLd * u_;                                                   \
-      sG[at_] = x_[u_];                                                                    \
-      sEL[at_] = ex2(x_[u_] - f_);                                                         \
-      sER[at_] = ex2(l_ - x_[u_]);                                                         \
+      sG[aTs + kTabLd * u_] = x_[u_];                                                      \
+      const float el_ = ex2(x_[u_] - f_), er_ = ex2(l_ - x_[u_]);                          \
+      const float kv_ = (float)pk[u_];                                                     \
+      xk_[u_] = kv_ * er_;                                                                 \
+      xb_[u_] = (float)pb[u_] * kv_ * el_;                                                 \
+      xq_[u_] = (float)pq[u_] * el_;                                                       \
       if (rl == 15) sBK[(0 * 4 + wave) * 16 + 4 * cq + u_] = x_[u_];                       \
       if (rl == 0) sBK[(1 * 4 + wave) * 16 + 4 * cq + u_] = x_[u_];                        \
       const int ac_ = aKs[u_ >> 1] + 64 * (u_ & 1);                                        \
@@ -404,6 +445,9 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       sBc[ac_] = pb[u_];                                                                   \
       sQc[ac_] = pq[u_];                                                                   \
     }                                                                                      \
+    st4split(sXh + aXs, sXl + aXs, xk_);                                                   \
+    st4split(sBh + aXs, sBl + aXs, xb_);                                                   \
+    st4split(sQh + aXs, sQl + aXs, xq_);                                                   \
     if (hact) {                                                                            \
       float hx_[8], dx_[8];                                                                \
       load_state8(ph, psh, hx_);                                                           \
@@ -432,25 +476,40 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   GDR2_PREFETCH(0)
 
   // ---- dZ^T = dR^T A for the key rows s of block i: lane gets
-  //      dZ[s = 16 i + r16][v = 16 vb + 4 g + u];  dv = dZ * w, dw = dZ * v
+  //      dZ[s = 16 i + r16][v = 16 vb + 4 g + u];  dv = dZ * w, dw = dZ * v.
+  //      16-deep products over the chunk-row blocks rb >= i (A is lower
+  //      triangular).  A's fp16 copy, scaled back by its power-of-two block
+  //      scale, splits exactly into bf16 hi and lo (11 significant bits).
   f4 zacc[NVB];
   {
-    Fr af[2];
+    Fr4 af[4];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      af[kb].hi = ld8(reinterpret_cast<const __bf16*>(sAm + (2 * i + kb) * 2048 + 16 * lane));
-      af[kb].lo = ld8(reinterpret_cast<const __bf16*>(sAm + (2 * i + kb) * 2048 + 1024 + 16 * lane));
+    for (int rb = 0; rb < 4; ++rb) {
+      if (rb < i) continue;
+      const f16x4 a16 = *reinterpret_cast<const f16x4*>(sAm + (4 * i + rb) * 512 + 8 * lane);
+      const float s = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ascl), rb));
+      f4 x;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[e] = (float)a16[e] * s;
+      bf4 hi, lo;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        hi[e] = (__bf16)x[e];
+        lo[e] = (__bf16)(x[e] - (float)hi[e]);
+      }
+      af[rb].hi = hi;
+      af[rb].lo = lo;
     }
 #pragma unroll
     for (int vb = 0; vb < NVB; ++vb) {
       zacc[vb] = f4zero();
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        if (kb < kbl) continue;
-        Fr rf;
-        rf.hi = ld8(reinterpret_cast<const __bf16*>(sDR + (2 * vb + kb) * 2048 + 16 * lane));
-        rf.lo = ld8(reinterpret_cast<const __bf16*>(sDR + (2 * vb + kb) * 2048 + 1024 + 16 * lane));
-        zacc[vb] = mma3(rf, af[kb], zacc[vb]);
+      for (int rb = 0; rb < 4; ++rb) {
+        if (rb < i) continue;
+        Fr4 rf;
+        rf.hi = *reinterpret_cast<const bf4*>(sDR + (4 * vb + rb) * 1024 + 8 * lane);
+        rf.lo = *reinterpret_cast<const bf4*>(sDR + (4 * vb + rb) * 1024 + 512 + 8 * lane);
+        zacc[vb] = mma3_16(rf, af[rb], zacc[vb]);
       }
     }
   }
@@ -511,16 +570,9 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       tv[u] = (rr + u > s) ? -ta[u] : 0.f;
       av[u] = (rr + u >= s) ? a.scale * aa[u] : 0.f;
     }
-    const int at = plane_ix(s, rr);
+    const int at = plane_ix<LP>(s, rr);
     st4split(sTh + at, sTl + at, tv);
     st4split(sAh + at, sAl + at, av);
-  }
-  // tiles (0,1) and (2,3) above the diagonal share 32-wide operand steps with causal tiles
-  if (i == 0 || i == 2) {
-    const int s = 16 * (i + 1) + r16, rr = 16 * i + 4 * g;
-    const int at = plane_ix(s, rr);
-    st4split(sTh + at, sTl + at, f4zero());
-    st4split(sAh + at, sAl + at, f4zero());
   }
   __syncthreads();  // R is dead: key block 0 is staged over it
   GDR2_STAGE(0, 0)
@@ -567,69 +619,63 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     // a diagonal block whose decay exceeds e^60 anywhere in this key block is formed element by element
     const bool uns = __ballot(G2fi - G2li > kDiagLimit2) != 0ull;
 
-    // P1 = dT (k 2^(G2_p - G2_s)),  P2 = dA_qk (k 2^(G2_p - G2_s)),  p = 16 i, s <= 16 i + 15;
-    // for s in block j the factor is eR_s * 2^(G2f_i - G2l_j)
+    // P1 = dT (k 2^(G2_p - G2_s)),  P2 = dA_qk (k 2^(G2_p - G2_s)),  p = 16 i, s <= 16 i + 15:
+    // per key-row block j <= i one 16-deep step on the shared operand k eR, whose
+    // product takes the block factor 2^(G2f_i - G2l_j)
     f4 p1 = f4zero(), p2 = f4zero();
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      if (kb > kbl) break;
-      const int j = 2 * kb + (g >> 1);  // block of keys s = 32 kb + 8 g ..
-      const bool inc = j < i || (j == i && !uns);
-      const float br = inc ? ex2(G2fi - pick4(G2l, j)) : 0.f;
-      float er[8], ks[8], x[8];
-      ldf4x2(sER + aTb[0] + 32 * kb, sER + aTb[1] + 32 * kb, er);
-      unpack8(ld8(sKc + aK[kb]), ks);
+    for (int j = 0; j < 4; ++j) {
+      if (j > i) break;
+      if (j == i && uns) continue;
+      Fr4 xf, tf, af;
+      xf.hi = ld_tr4(sXh + aXr + 256 * j);
+      xf.lo = ld_tr4(sXl + aXr + 256 * j);
+      // dT, dA_qk rows of block i, keys of block j: transposed reads of the planes
+      const int t0 = aTr + 16 * LP * j;
+      tf.hi = ld_tr4(sTh + t0);
+      tf.lo = ld_tr4(sTl + t0);
+      af.hi = ld_tr4(sAh + t0);
+      af.lo = ld_tr4(sAl + t0);
+      const float br = ex2(G2fi - pick4(G2l, j));
+      const f4 t1 = mma3_16(tf, xf, f4zero()), t2 = mma3_16(af, xf, f4zero());
 #pragma unroll
-      for (int e = 0; e < 8; ++e) x[e] = ks[e] * er[e] * br;
-      const Fr kf = split8(x);
-      Fr tf, af;
-      // transposed reads: lane (G, 4 a + q) contributes rows 32 kb + 8 G + a (+ 4), columns 16 i + 4 q ..
-      const int t0 = aTr + 64 * 32 * kb, t1 = t0 + 64 * 4;
-      tf.hi = ld_tr8p(sTh + t0, sTh + t1);
-      tf.lo = ld_tr8p(sTl + t0, sTl + t1);
-      af.hi = ld_tr8p(sAh + t0, sAh + t1);
-      af.lo = ld_tr8p(sAl + t0, sAl + t1);
-      p1 = mma3(tf, kf, p1);
-      p2 = mma3(af, kf, p2);
+      for (int u = 0; u < 4; ++u) {
+        p1[u] += br * t1[u];
+        p2[u] += br * t2[u];
+      }
     }
-    // P3 = dT^T ((b k) 2^(G2_r - G2_e)) + dA_qk^T (q 2^(G2_r - G2_e)),  e = 16 i + 15, r >= 16 i;
-    // for r in block j the factor is eL_r * 2^(G2f_j - G2l_i)
+    // P3 = dT^T ((b k) 2^(G2_r - G2_e)) + dA_qk^T (q 2^(G2_r - G2_e)),  e = 16 i + 15, r >= 16 i:
+    // per row block j >= i one 16-deep step on the shared operands b k eL and q eL,
+    // the product taking 2^(G2f_j - G2l_i)
     f4 p3 = f4zero();
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      if (kb < kbl) continue;
-      const int j = 2 * kb + (g >> 1);  // block of rows r = 32 kb + 8 g ..
-      const bool inc = j > i || (j == i && !uns);
-      const float br = inc ? ex2(pick4(G2f, j) - G2li) : 0.f;
-      float el[8], kr[8], bv[8], qv[8], lb[8], lq[8];
-      ldf4x2(sEL + aTb[0] + 32 * kb, sEL + aTb[1] + 32 * kb, el);
-      const int ac = aK[kb];
-      unpack8(ld8(sKc + ac), kr);
-      unpack8(ld8(sBc + ac), bv);
-      unpack8(ld8(sQc + ac), qv);
+    for (int j = 0; j < 4; ++j) {
+      if (j < i || (j == i && uns)) continue;
+      Fr4 bf, qf, tf, af;
+      bf.hi = ld_tr4(sBh + aXr + 256 * j);
+      bf.lo = ld_tr4(sBl + aXr + 256 * j);
+      qf.hi = ld_tr4(sQh + aXr + 256 * j);
+      qf.lo = ld_tr4(sQl + aXr + 256 * j);
+      const int at = LP == 80 ? aP3 + 16 * j : plane_ix<LP>(16 * i + r16, 16 * j + 4 * g);
+      tf.hi = *reinterpret_cast<const bf4*>(sTh + at);
+      tf.lo = *reinterpret_cast<const bf4*>(sTl + at);
+      af.hi = *reinterpret_cast<const bf4*>(sAh + at);
+      af.lo = *reinterpret_cast<const bf4*>(sAl + at);
+      const float br = ex2(pick4(G2f, j) - G2li);
+      const f4 t = mma3_16(af, qf, mma3_16(tf, bf, f4zero()));
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float f = el[e] * br;
-        lb[e] = bv[e] * kr[e] * f;
-        lq[e] = qv[e] * f;
-      }
-      Fr tf, af;
-      const int at = aP3[kb];
-      tf.hi = ld8(sTh + at);
-      tf.lo = ld8(sTl + at);
-      af.hi = ld8(sAh + at);
-      af.lo = ld8(sAl + at);
-      p3 = mma3(tf, split8(lb), p3);
-      p3 = mma3(af, split8(lq), p3);
+      for (int u = 0; u < 4; ++u) p3[u] += br * t[u];
     }
 
     // ---- elementwise chain (App. B.4) on rows rb + u, key c:
     // gamma_r = eL_r 2^(G2f_i),  tail_r = eR_r 2^(G2_{C-1} - G2l_i)
     const int rb = 16 * i + 4 * g;
     const int ae = aE, ak = aK4;
-    const float4 eL4 = *reinterpret_cast<const float4*>(sEL + ae);
-    const float4 eR4 = *reinterpret_cast<const float4*>(sER + ae);
-    const float elv[4] = {eL4.x, eL4.y, eL4.z, eL4.w}, erv[4] = {eR4.x, eR4.y, eR4.z, eR4.w};
+    // eL_r, eR_r of the lane's rows from the in-block sums (as staged)
+    const float4 G4 = *reinterpret_cast<const float4*>(sG + ae);
+    const float gf = sBK[(4 + i) * 16 + r16], gl = sBK[i * 16 + r16];
+    const float elv[4] = {ex2(G4.x - gf), ex2(G4.y - gf), ex2(G4.z - gf), ex2(G4.w - gf)};
+    const float erv[4] = {ex2(gl - G4.x), ex2(gl - G4.y), ex2(gl - G4.z), ex2(gl - G4.w)};
     const bf4 k4 = *reinterpret_cast<const bf4*>(sKc + ak);
     const bf4 b4 = *reinterpret_cast<const bf4*>(sBc + ak);
     const bf4 q4 = *reinterpret_cast<const bf4*>(sQc + ak);
@@ -657,7 +703,7 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
           const float ks = (float)sKc[as];
           if (s <= r) {
             const float e = ex2(G - Gs);
-            const int sr = plane_ix(s, r);
+            const int sr = plane_ix<LP>(s, r);
             const float dTv = (s < r) ? (float)sTh[sr] + (float)sTl[sr] : 0.f;
             const float dAv = (float)sAh[sr] + (float)sAl[sr];
             dEg += dTv * ks * e;
@@ -665,7 +711,7 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
           }
           if (s >= r) {
             const float e = ex2(Gs - G);
-            const int rs = plane_ix(r, s);
+            const int rs = plane_ix<LP>(r, s);
             const float dTv = (s > r) ? (float)sTh[rs] + (float)sTl[rs] : 0.f;
             const float dAv = (float)sAh[rs] + (float)sAl[rs];
             dKg += (dTv * (float)sBc[as] * ks + dAv * (float)sQc[as]) * e;
@@ -775,8 +821,8 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
 
 template <int DK, int DV, bool FUSED>
 hipError_t launch_bchunk_bf16_t(const BChunkBf16Args& a, hipStream_t st) {
-  using C = BChunkCfg<DK, DV>;
-  constexpr int lds = FUSED ? C::LDS_FUSED : C::LDS;
+  using C = BChunkCfg<DK, DV, FUSED>;
+  constexpr int lds = C::LDS;
   const void* fn = reinterpret_cast<const void*>(&bchunk_bf16_kernel<DK, DV, FUSED>);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) return e;

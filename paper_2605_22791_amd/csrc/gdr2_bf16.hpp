@@ -285,6 +285,21 @@ __device__ __forceinline__ void store_state_f16(const f4 (&s)[TPW], const int (&
     for (int t2 = 0; t2 < TPW / 2; ++t2) sc[t2] = ldexpf(1.f, -sh[t2]);
   }
 }
+// store_tile_f16: one 16 x 16 accumulator tile (lane (g, r16) holds rows
+// 4 g + u, column r16) as a 512-byte fp16 block of 16 x 16 x 16 operand
+// fragments, scaled by 2^sh (sh = state_shift of the tile's largest
+// magnitude): lane l's 8 bytes hold column l % 16 (the fragment's row or
+// column) and rows 4 (l / 16) + u (its K elements).  Lane 0 writes the inverse
+// scale to *sc.
+__device__ __forceinline__ void store_tile_f16(const f4& x, int sh, _Float16* blk, float* sc, int lane) {
+  const float f = ldexpf(1.f, sh);
+  const f16x4 v = {(_Float16)(x[0] * f), (_Float16)(x[1] * f), (_Float16)(x[2] * f), (_Float16)(x[3] * f)};
+  *reinterpret_cast<f16x4*>(blk + 4 * lane) = v;
+  if (lane == 0) *sc = ldexpf(1.f, -sh);
+}
+__device__ __forceinline__ int tile_shift(const f4& x) {
+  return state_shift(wave_max(fmaxf(fmaxf(fabsf(x[0]), fabsf(x[1])), fmaxf(fabsf(x[2]), fabsf(x[3])))));
+}
 // store_frag_f16: a 16 x 32 tile held as two MFMA accumulator tiles (s[0]:
 // columns 0..15, s[1]: columns 16..31; lane (g, r16) holds rows 4 g + u,
 // column r16) as one fp16 permuted fragment block (1 KB, the layout of

@@ -7,7 +7,7 @@
 //
 // writing dS before each update (the gradient of that chunk's end state, fp16
 // with block scales as store_state_f16 keeps it for the chunk backward), dR
-// (split hi/lo, in the fragment order the chunk backward reads), and finally dS0.
+// (split bf16 16 x 16 blocks), and finally dS0.
 // With nseg > 1 each workgroup runs one segment of a sequence, from the
 // gradient at the segment's end to the one at its start (BScanArgs).  The operands are the forward's fragment-ordered tiles
 // (gdr2_kernels.hpp): the transposed fragments these products need come out
@@ -291,16 +291,15 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
     for (int t = 0; t < TPW; ++t)
 #pragma unroll
       for (int u = 0; u < 4; ++u) sreg[t][u] += sc * qacc[t][u];
-    // dR as permuted fragment blocks (row = value, K = chunk row): this lane's
-    // four rows 16 iO + 4 g + u are half of its 16-byte slot.  Like the dh
-    // stores, these leave after the chunk's products are issued.
+    // dR for the chunk backward: each of the wave's 16 x 16 tiles (chunk rows
+    // 16 iO .., values 16 vb ..) as one split block, lane l's four values
+    // (value l % 16, rows 4 (l / 16) + u) at 8 l of the hi and lo halves.  Like
+    // the dh stores, these leave after the chunk's products are issued.
     if (a.DR) {
 #pragma unroll
       for (int t = 0; t < NVB / 2; ++t) {
-        const int vb = vbO + t;
-        const size_t doff = ch * WsBf16::dr(DV) + (size_t)((v0 / 16 + vb) * 2 + (iO >> 1)) * 2048 + 16 * lane +
-                            8 * (iO & 1);
-        st4split(reinterpret_cast<__bf16*>(a.DR + doff), reinterpret_cast<__bf16*>(a.DR + doff + 1024), rkeep[t]);
+        const size_t blk = ch * (WsBf16::dr(DV) / 1024) + (size_t)(v0 / 16 + vbO + t) * 4 + iO;
+        st4split(a.DR + blk * 512 + 4 * lane, a.DR + blk * 512 + 256 + 4 * lane, rkeep[t]);
       }
     }
     __syncthreads();

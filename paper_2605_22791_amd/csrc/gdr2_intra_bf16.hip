@@ -461,20 +461,18 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
     __syncthreads();
   }
 
-  // ---- A for the backward: permuted blocks (row = key s, K = chunk row r)
+  // ---- A for the backward: fp16 16 x 16 blocks (key s block, chunk row r block)
+  //      with one scale each, the B operand of the chunk backward's dR^T A
   if (a.Am) {
-    unsigned char* Ao = a.Am + ch * WsBf16::am();
-    for (int blk = wave; blk < 8; blk += 4) {
-      const int sb = blk >> 1, kb = blk & 1;
-      float x[8];
+    _Float16* Ao = a.Am + ch * (WsBf16::am() / 2);
+    float* Asc = a.Amsc + ch * (WsBf16::amsc() / 4);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int r = 32 * kb + (e < 4 ? 4 * g + e : 16 + 4 * g + (e - 4));
-        x[e] = sTA[r * LTA + 16 * sb + r16];
-      }
-      const Fr f = split8(x);
-      st8(reinterpret_cast<__bf16*>(Ao + blk * 2048 + 16 * lane), f.hi);
-      st8(reinterpret_cast<__bf16*>(Ao + blk * 2048 + 1024 + 16 * lane), f.lo);
+    for (int blk = wave; blk < 16; blk += 4) {
+      const int sb = blk >> 2, rb = blk & 3;
+      f4 x;  // A[r = 16 rb + 4 g + e][s = 16 sb + r16]
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[e] = sTA[(16 * rb + 4 * g + e) * LTA + 16 * sb + r16];
+      store_tile_f16(x, tile_shift(x), Ao + blk * 256, Asc + blk, lane);
     }
   }
 

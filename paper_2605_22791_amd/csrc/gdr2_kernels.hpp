@@ -233,10 +233,12 @@ struct RecurArgs {
 //                   16 x 32 block (store_state_f16 in gdr2_bf16.hpp)
 //   Rs   (64 x Dv)  R, fp16 permuted blocks [row block 4][value block Dv/32] with one
 //                   scale per block (store_frag_f16): the R operands of the chunk backward
-//   Am   (64 x 64)  A = (I + T)^{-1}, bf16 hi/lo, permuted blocks [key s block 4][row r block 2]
-//                   (row R = s, permuted K = r): the B operand of A^T-products
-//   DR   (64 x Dv)  dR, bf16 hi/lo, permuted blocks [value block Dv/16][row block 2]
-//                   (row R = value, permuted K = chunk row): the A operand of dR^T A
+//   Am   (64 x 64)  A = (I + T)^{-1}, fp16 16 x 16 blocks [key s block 4][row r block 4] with
+//                   one scale per block (store_tile_f16; lane l: s = l % 16, r = 4 (l / 16) + e):
+//                   the B operand of the 16-deep fp16 products dR^T A
+//   DR   (64 x Dv)  dR, bf16 hi/lo 16 x 16 blocks [value block Dv/16][row block 4] (hi 512
+//                   bytes, then lo; lane l: value l % 16, chunk row 4 (l / 16) + e): the A
+//                   operand of the 16-deep products dR^T A
 struct WsBf16 {
   static constexpr size_t y(int dk) { return (size_t)4 * (dk / 32) * 1024; }
   static constexpr size_t qg(int dk) { return (size_t)4 * (dk / 32) * 2048; }
@@ -244,8 +246,11 @@ struct WsBf16 {
   static constexpr size_t ktt(int dk) { return (size_t)(dk / 16) * 2 * 2048; }
   static constexpr size_t u(int dv) { return (size_t)(dv / 16) * 4 * 1024; }
   static constexpr size_t gc(int dk) { return (size_t)((dk * 4 + 255) / 256) * 256; }
-  static constexpr size_t am() { return (size_t)8 * 2048; }
-  static constexpr size_t dr(int dv) { return (size_t)(dv / 16) * 2 * 2048; }
+  // A of the backward: fp16 16 x 16 blocks (512 bytes) and one fp32 scale per block;
+  // dR: split bf16 16 x 16 blocks (1 KB)
+  static constexpr size_t am() { return (size_t)16 * 512; }
+  static constexpr size_t amsc() { return (size_t)16 * 4; }
+  static constexpr size_t dr(int dv) { return (size_t)(dv / 16) * 4 * 1024; }
   // chunk states of the backward: fp16 (Dk x Dv) and one fp32 scale per 16 x 32 block
   static constexpr size_t hs(int dk, int dv) { return (size_t)dk * dv * 2; }
   static constexpr size_t hsc(int dk, int dv) { return (size_t)(dk / 16) * (dv / 32) * 4; }
@@ -268,7 +273,7 @@ struct IntraBf16Args {
   unsigned char* KtT;
   float* U;
   float* GC;
-  unsigned char* Am;  // nullable: A for the backward
+  _Float16* Am;  // nullable: A for the backward (WsBf16::am, with Amsc)
   int B, T, H, NT;
   Varlen vl{};
   // grouped value heads: H value heads share H / G key heads (q, k, g, b); the
@@ -276,6 +281,7 @@ struct IntraBf16Args {
   // once there (chunk_pos over the key heads) and U for each value head (value_ch)
   int G = 1;
   Stage st{};
+  float* Amsc = nullptr;  // the inverse scales of Am's blocks
 };
 
 // Sequence-parallel scans: with nseg > 1 every sequence is cut into nseg
@@ -319,7 +325,7 @@ struct BScanArgs {
   const float* dST;  // nullable
   float* dS0;        // nullable
   _Float16* DH;      // nullable: gradient of each chunk's end state, fp16 (store_state_f16 layout)
-  unsigned char* DR; // nullable: dR per chunk, WsBf16 fragment blocks
+  __bf16* DR;        // nullable: dR per chunk, split bf16 16 x 16 blocks (WsBf16::dr)
   int B, T, H, NT;
   float scale;
   float* DHsc = nullptr;           // the inverse scales of DH
@@ -356,8 +362,8 @@ struct BChunkBf16Args {
   const _Float16* Hs;       // chunk-start states, fp16 (store_state_f16 layout)
   const _Float16* DH;       // gradients of the chunk-end states, fp16
   const _Float16* Rs;       // R per chunk, fp16 fragment blocks (WsBf16::rs)
-  const unsigned char* DR;  // dR, WsBf16 fragment blocks
-  const unsigned char* Am;  // A, WsBf16 fragment blocks
+  const __bf16* DR;         // dR, split bf16 16 x 16 blocks (WsBf16::dr)
+  const _Float16* Am;       // A, fp16 16 x 16 blocks (WsBf16::am)
   bf16_t* dq;
   bf16_t* dk;
   bf16_t* dv;
@@ -369,6 +375,7 @@ struct BChunkBf16Args {
   const float* Hsc = nullptr;   // inverse scales of Hs and DH (WsBf16::hsc per chunk-head)
   const float* DHsc = nullptr;
   const float* Rsc = nullptr;   // inverse scales of Rs (WsBf16::rsc per chunk-head)
+  const float* Amsc = nullptr;  // inverse scales of Am (WsBf16::amsc per key-head chunk)
   Varlen vl{};
   // grouped value heads: H value heads share H / G key heads.  With G > 1 the
   // kernel is launched once per value head of every group (gj = 0 .. G - 1, in

@@ -89,7 +89,7 @@ def ws_layout_bf16(B, T, H, Dk, Dv, bwd=False, nseq=0, G=1):
     (all but U and the backward's states, R, dH, dR) exist once per key head."""
     NC = H * (T // CH + nseq) if nseq > 0 else B * H * (-(-T // CH))
     gc = (Dk * 4 + 255) // 256 * 256
-    key = {"Y", "Qg", "Aqk", "KtT", "GC", "Am"}
+    key = {"Y", "Qg", "Aqk", "KtT", "GC", "Am", "Amsc"}
     sizes = [("Y", 4 * (Dk // 32) * 1024), ("Qg", 4 * (Dk // 32) * 2048), ("Aqk", 8 * 2048),
              ("KtT", (Dk // 16) * 2 * 2048), ("U", (Dv // 16) * 4 * 1024), ("GC", gc)]
     if bwd:
@@ -97,7 +97,7 @@ def ws_layout_bf16(B, T, H, Dk, Dv, bwd=False, nseq=0, G=1):
         rsc = 4 * (Dv // 32) * 4
         sizes += [("Hs", Dk * Dv * 2), ("Hsc", hsc), ("Rs", CH * Dv * 2), ("Rsc", rsc), ("DH", Dk * Dv * 2),
                   ("DHsc", hsc),
-                  ("DR", (Dv // 16) * 2 * 2048), ("Am", 8 * 2048)]
+                  ("DR", (Dv // 16) * 4 * 1024), ("Am", 16 * 512), ("Amsc", 16 * 4)]
     off, out = 0, {}
     for n, per in sizes:
         out[n] = (off, per)
@@ -134,6 +134,52 @@ def decode_frag_blocks(raw_u16, nrb, nkb, split, permuted):
     for rb in range(nrb):
         for kb in range(nkb):
             out[16 * rb + row, 32 * kb + key] = vals[rb, kb]
+    return out
+
+
+def decode_tiles_f16(raw_f16, raw_scales, ncb, nrb):
+    """fp16 16 x 16 blocks [column block ncb][row block nrb] with one scale each
+    -> dense (16 nrb, 16 ncb) float64; lane l of a block holds column l % 16 and
+    rows 4 (l // 16) + e, e < 4."""
+    vals = raw_f16.view(np.float16).astype(np.float64).reshape(ncb, nrb, 64, 4)
+    sc = raw_scales.view(np.float32).astype(np.float64).reshape(ncb, nrb)
+    lane = np.arange(64)[:, None]
+    e = np.arange(4)[None, :]
+    col = np.broadcast_to(lane % 16, (64, 4))
+    row = np.broadcast_to(4 * (lane // 16) + e, (64, 4))
+    out = np.zeros((16 * nrb, 16 * ncb))
+    for cb in range(ncb):
+        for rb in range(nrb):
+            out[16 * rb + row, 16 * cb + col] = vals[cb, rb] * sc[cb, rb]
+    return out
+
+
+def decode_tiles_split(raw_u16, ncb, nrb):
+    """split bf16 16 x 16 blocks [column block ncb][row block nrb] (hi 256 values,
+    then lo) -> dense (16 nrb, 16 ncb) float64, lanes as in decode_tiles_f16."""
+    vals = bf16_bits_to_f32(raw_u16.view(np.uint16).reshape(ncb, nrb, 2, 64, 4)).astype(np.float64).sum(axis=2)
+    lane = np.arange(64)[:, None]
+    e = np.arange(4)[None, :]
+    col = np.broadcast_to(lane % 16, (64, 4))
+    row = np.broadcast_to(4 * (lane // 16) + e, (64, 4))
+    out = np.zeros((16 * nrb, 16 * ncb))
+    for cb in range(ncb):
+        for rb in range(nrb):
+            out[16 * rb + row, 16 * cb + col] = vals[cb, rb]
+    return out
+
+
+def round_tiles_f16(x):
+    """x rounded as the fp16 block copies round it: per 16 x 16 block a power of
+    two maps the largest magnitude m = f 2^e (f in [0.5, 1)) to [2^14, 2^15)
+    (exponent 15 - e, clamped to +-120; 1 for m = 0), then fp16."""
+    out = np.empty_like(x, dtype=np.float64)
+    for r0 in range(0, x.shape[0], 16):
+        for c0 in range(0, x.shape[1], 16):
+            blk = x[r0:r0 + 16, c0:c0 + 16].astype(np.float64)
+            m = np.abs(blk).max()
+            sh = 0 if m == 0 else int(np.clip(15 - np.frexp(m)[1], -120, 120))
+            out[r0:r0 + 16, c0:c0 + 16] = np.ldexp(np.ldexp(blk, sh).astype(np.float16).astype(np.float64), -sh)
     return out
 
 

@@ -167,10 +167,13 @@ def test_workspace_size_and_check(dtype):
         exp_bwd = exp_fwd + extras
     else:
         # chunk states and their gradients in fp16 with one fp32 scale per 16 x 32 block,
-        # R in fp16 fragment blocks; dR and A as split bf16 fragment blocks
+        # R in fp16 fragment blocks; dR as split bf16 16 x 16 blocks, A as fp16 16 x 16
+        # blocks with one fp32 scale each
         states = rb(NC * 128 * 64 * 2) + rb(NC * (128 // 16) * (64 // 32) * 4)
         rfrag = rb(NC * 4 * (64 // 32) * 1024) + rb(NC * 4 * (64 // 32) * 4)     # R: fp16 blocks + scales
-        exp_bwd = exp_fwd + 2 * states + rfrag + rb(NC * (64 // 16) * 2 * 2048) + rb(NC * 8 * 2048)
+        dr = rb(NC * (64 // 16) * 4 * 1024)                                       # dR
+        am = rb(NC * 16 * 512) + rb(NC * 16 * 4)                                  # A
+        exp_bwd = exp_fwd + 2 * states + rfrag + dr + am
     assert fwd == exp_fwd and bwd == exp_bwd
     assert _fwd(p, ws_bytes=fwd - 1) == g2.GDR2_EWORKSPACE
     assert _bwd(p, ws_bytes=bwd - 1) == g2.GDR2_EWORKSPACE
