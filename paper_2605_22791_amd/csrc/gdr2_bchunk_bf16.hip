@@ -49,7 +49,9 @@
 // whose decay exceeds e^60 is formed element by element.
 //
 // Precision: every product is fp32-accurate on its operands (split hi/lo; dO
-// is exact bf16; X3 multiplies the fp16 copies exactly).
+// is exact bf16; X3 and the dT / dA_qk tiles multiply fp16 operands exactly:
+// the stored copies of R and dh, and dZ split in fp16 hi / lo under a
+// power-of-two scale, which keeps 22 bits relative to the wave's largest dZ).
 //
 // Fused input stage (FUSED; App. C.1, App. D.2): q and k arrive raw and are
 // normalised as they are staged, with the inverse norms the forward kept; the
@@ -500,17 +502,25 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       af[rb].hi = hi;
       af[rb].lo = lo;
     }
+    // chunk-row block outer and each of the three passes across the value
+    // blocks: consecutive products are independent
 #pragma unroll
-    for (int vb = 0; vb < NVB; ++vb) {
-      zacc[vb] = f4zero();
+    for (int vb = 0; vb < NVB; ++vb) zacc[vb] = f4zero();
 #pragma unroll
-      for (int rb = 0; rb < 4; ++rb) {
-        if (rb < i) continue;
-        Fr4 rf;
-        rf.hi = *reinterpret_cast<const bf4*>(sDR + (4 * vb + rb) * 1024 + 8 * lane);
-        rf.lo = *reinterpret_cast<const bf4*>(sDR + (4 * vb + rb) * 1024 + 512 + 8 * lane);
-        zacc[vb] = mma3_16(rf, af[rb], zacc[vb]);
+    for (int rb = 0; rb < 4; ++rb) {
+      if (rb < i) continue;
+      Fr4 rf[NVB];
+#pragma unroll
+      for (int vb = 0; vb < NVB; ++vb) {
+        rf[vb].hi = *reinterpret_cast<const bf4*>(sDR + (4 * vb + rb) * 1024 + 8 * lane);
+        rf[vb].lo = *reinterpret_cast<const bf4*>(sDR + (4 * vb + rb) * 1024 + 512 + 8 * lane);
       }
+#pragma unroll
+      for (int vb = 0; vb < NVB; ++vb) zacc[vb] = mma16(rf[vb].lo, af[rb].hi, zacc[vb]);
+#pragma unroll
+      for (int vb = 0; vb < NVB; ++vb) zacc[vb] = mma16(rf[vb].hi, af[rb].lo, zacc[vb]);
+#pragma unroll
+      for (int vb = 0; vb < NVB; ++vb) zacc[vb] = mma16(rf[vb].hi, af[rb].hi, zacc[vb]);
     }
   }
 #pragma unroll
@@ -528,9 +538,30 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     }
   }
   // dZ, dO and R rows of block i as A operands over the values, permuted K:
-  // K-step p holds values 32 p + 4 g + (0..3) and 32 p + 16 + 4 g + (0..3)
+  // K-step p holds values 32 p + 4 g + (0..3) and 32 p + 16 + 4 g + (0..3).
+  // zf (split bf16) serves the key-block loop; for the tiles below dZ is also
+  // split into fp16 hi / lo and dO converted to fp16, each under one
+  // power-of-two scale for the wave (the largest magnitude into [2^14, 2^15)),
+  // so that the tiles multiply R's stored fp16 copy directly.
   Fr zf[KV];
   u4v rfr16[KV];  // R rows of block i, fp16 as stored (scale rsc(i * KV + p))
+  f16x8 zh16[KV], zl16[KV], do16[KV];
+  float zmx = 0.f, omx = 0.f;
+  if (16 * i + r16 >= len) {
+#pragma unroll
+    for (int p = 0; p < KV; ++p) dof[p] = bf8{};
+  }
+#pragma unroll
+  for (int vb = 0; vb < NVB; ++vb)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) zmx = fmaxf(zmx, fabsf(zacc[vb][u]));
+#pragma unroll
+  for (int p = 0; p < KV; ++p)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) omx = fmaxf(omx, fabsf((float)dof[p][e]));
+  const int zsh = state_shift(wave_max(zmx)), osh = state_shift(wave_max(omx));
+  const float zs = ldexpf(1.f, zsh), os = ldexpf(1.f, osh);
+  const float izs = ldexpf(1.f, -zsh), ios = ldexpf(1.f, -osh);
 #pragma unroll
   for (int p = 0; p < KV; ++p) {
     float x[8];
@@ -540,41 +571,60 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       x[4 + u] = zacc[2 * p + 1][u];
     }
     zf[p] = split8(x);
-    rfr16[p] = *reinterpret_cast<const u4v*>(sR + (i * KV + p) * 1024 + 16 * lane);
-  }
-  __syncthreads();  // dR and A are dead (R stays until the tiles below are done)
-  if (16 * i + r16 >= len) {
 #pragma unroll
-    for (int p = 0; p < KV; ++p) dof[p] = bf8{};
+    for (int e = 0; e < 8; ++e) {
+      const float y = x[e] * zs;
+      zh16[p][e] = (_Float16)y;
+      zl16[p][e] = (_Float16)(y - (float)zh16[p][e]);
+      do16[p][e] = (_Float16)((float)dof[p][e] * os);
+    }
+    rfr16[p] = *reinterpret_cast<const u4v*>(sR + (i * KV + p) * 1024 + 16 * lane);
   }
 
   // ---- dT = -tril(dZ R^T, -1) and dA_qk = tril(scale dO R^T), tiles (i, j <= i),
-  //      stored transposed: plane[s][r].  The R rows of block j come from the fp16
-  //      fragment blocks in LDS.
+  //      stored transposed: plane[s][r].  The R rows of block j are the fp16
+  //      fragment blocks in LDS; every product is exact (fp16 operands), each
+  //      K-step scaled by R's block scale and the wave's dZ / dO scale.  The
+  //      tiles of one K-step are formed together (independent products).  They
+  //      stay in registers until every wave is done with dR (region 1, which
+  //      the planes take over) and with A and R (region 2, which key block 0
+  //      takes over), so dZ and the tiles run without a barrier between them.
+  f4 ta[4], aa[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) ta[j] = aa[j] = f4zero();
+#pragma unroll
+  for (int p = 0; p < KV; ++p) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (j > i) break;
+      const f16x8 rv = __builtin_bit_cast(
+          f16x8, j == i ? rfr16[p] : *reinterpret_cast<const u4v*>(sR + (j * KV + p) * 1024 + 16 * lane));
+      const f4 t = mma_f16(zl16[p], rv, mma_f16(zh16[p], rv, f4zero()));
+      const f4 t2 = mma_f16(do16[p], rv, f4zero());
+      const float rs = rsc(j * KV + p), cz = rs * izs, co = rs * ios;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        ta[j][u] += t[u] * cz;
+        aa[j][u] += t2[u] * co;
+      }
+    }
+  }
+  __syncthreads();  // dR, A and R are dead: the planes and key block 0 go over them
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     if (j > i) break;
     const int s = 16 * j + r16;
-    f4 ta = f4zero(), aa = f4zero();
-#pragma unroll
-    for (int p = 0; p < KV; ++p) {
-      const Fr rj = frag_f16_split(j == i ? rfr16[p] : *reinterpret_cast<const u4v*>(sR + (j * KV + p) * 1024 + 16 * lane),
-                                   rsc(j * KV + p));
-      ta = mma3(zf[p], rj, ta);
-      aa = mma2b(dof[p], rj, aa);
-    }
     const int rr = 16 * i + 4 * g;
     f4 tv, av;
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      tv[u] = (rr + u > s) ? -ta[u] : 0.f;
-      av[u] = (rr + u >= s) ? a.scale * aa[u] : 0.f;
+      tv[u] = (rr + u > s) ? -ta[j][u] : 0.f;
+      av[u] = (rr + u >= s) ? a.scale * aa[j][u] : 0.f;
     }
     const int at = plane_ix<LP>(s, rr);
     st4split(sTh + at, sTl + at, tv);
     st4split(sAh + at, sAl + at, av);
   }
-  __syncthreads();  // R is dead: key block 0 is staged over it
   GDR2_STAGE(0, 0)
   __syncthreads();
 
