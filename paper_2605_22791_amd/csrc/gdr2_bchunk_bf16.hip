@@ -228,7 +228,8 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   float* sDL = reinterpret_cast<float*>(smem + C::OFF_DL);  // fused stage: delta [c]
   float* sRN = reinterpret_cast<float*>(smem + C::OFF_RN);  // fused stage: 1/||q||, 1/||k|| [2][64]
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wave index as a scalar: branches on the row block are uniform
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, r16 = lane & 15;
   ChunkPos cp;
   // the grid covers the key heads; this launch takes value head gj of each group
