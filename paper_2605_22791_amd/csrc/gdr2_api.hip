@@ -415,13 +415,20 @@ hipError_t scan_fwd_bf16(const ScanArgs& sa, const Layout& L, void* ws, Last&& l
   pn.nseg = L.nseg;
   pn.seg_len = L.seg_len;
   pn.STseg = at<float>(ws, L.sN);
-  hipError_t e = launch_scan_bf16<DK, DV, false, false>(pn, st);
-  if (e != hipSuccess) return e;
-  ScanArgs pm = pn;
-  pm.U = nullptr;
-  pm.flags = kScanNoInput | kScanEye;
-  pm.STseg = at<float>(ws, L.sM);
-  e = launch_scan_bf16<DK, DK, false, false>(pm, st);
+  hipError_t e;
+  if constexpr (DK == DV) {
+    // N and M in one launch: each map's full width in one workgroup
+    pn.STseg_m = at<float>(ws, L.sM);
+    e = launch_scan_map_bf16<DK>(pn, st);
+  } else {
+    e = launch_scan_bf16<DK, DV, false, false>(pn, st);
+    if (e != hipSuccess) return e;
+    ScanArgs pm = pn;
+    pm.U = nullptr;
+    pm.flags = kScanNoInput | kScanEye;
+    pm.STseg = at<float>(ws, L.sM);
+    e = launch_scan_bf16<DK, DK, false, false>(pm, st);
+  }
   if (e != hipSuccess) return e;
   const SegCombineArgs ca{at<float>(ws, L.sM), at<float>(ws, L.sN), sa.S0, at<float>(ws, L.sX),
                           sa.B * sa.H, L.nseg, 0};
@@ -434,8 +441,11 @@ hipError_t scan_fwd_bf16(const ScanArgs& sa, const Layout& L, void* ws, Last&& l
   return last(p3);
 }
 
-// Reverse: the same three steps from the segment ends, then every segment
-// again from the gradient at its end (writing dH, dR and dS0).
+// Reverse: the same steps from the segment ends, then every segment again
+// from the gradient at its end (writing dH, dR and dS0).  For a square state
+// the reverse segment maps are the transposes of the forward ones, which the
+// forward phase of this backward (or the saving forward) left in sM: the map
+// pass of the reverse scan is then skipped.
 template <int DK, int DV>
 hipError_t scan_bwd_bf16(const BScanArgs& ba, const Layout& L, void* ws, hipStream_t st) {
   if (L.nseg == 1) return launch_bscan_bf16<DK, DV>(ba, st);
@@ -449,14 +459,17 @@ hipError_t scan_bwd_bf16(const BScanArgs& ba, const Layout& L, void* ws, hipStre
   pn.dSseg_out = at<float>(ws, L.sN);
   hipError_t e = launch_bscan_bf16<DK, DV>(pn, st);
   if (e != hipSuccess) return e;
-  BScanArgs pm = pn;
-  pm.dout = nullptr;
-  pm.flags = kScanNoInput | kScanEye;
-  pm.dSseg_out = at<float>(ws, L.sM);
-  e = launch_bscan_bf16<DK, DK>(pm, st);
-  if (e != hipSuccess) return e;
-  const SegCombineArgs ca{at<float>(ws, L.sM), at<float>(ws, L.sN), ba.dST, at<float>(ws, L.sX),
-                          ba.B * ba.H, L.nseg, 1};
+  if constexpr (DK != DV) {
+    BScanArgs pm = pn;
+    pm.dout = nullptr;
+    pm.flags = kScanNoInput | kScanEye;
+    pm.dSseg_out = at<float>(ws, L.sM);
+    e = launch_bscan_bf16<DK, DK>(pm, st);
+    if (e != hipSuccess) return e;
+  }
+  SegCombineArgs ca{at<float>(ws, L.sM), at<float>(ws, L.sN), ba.dST, at<float>(ws, L.sX),
+                    ba.B * ba.H, L.nseg, 1};
+  ca.transpose_m = DK == DV;
   e = launch_segcombine<DK, DV>(ca, st);
   if (e != hipSuccess) return e;
   BScanArgs p3 = ba;

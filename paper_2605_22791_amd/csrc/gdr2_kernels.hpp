@@ -313,6 +313,7 @@ struct ScanArgs {
   int flags = 0;                 // ScanFlags
   Varlen vl{};
   int G = 1;                     // value heads per key head: Y, Q_g, A_qk, K_tail, gamma_C per key head
+  float* STseg_m = nullptr;      // the map pass (Dk = DV): M of every segment (B*H*nseg, Dk, Dk)
 };
 
 struct BScanArgs {
@@ -348,6 +349,7 @@ struct SegCombineArgs {
   float* Xs;
   int nseq, nseg;
   int reverse;
+  int transpose_m = 0;  // use M_k^T (the reverse chain with the forward's maps, Dk = DV)
 };
 
 // Chunk-parallel backward of the bf16 path (App. B.2 - B.5).
@@ -411,6 +413,10 @@ template <int DK, int DV>
 hipError_t launch_bscan_bf16(const BScanArgs& a, hipStream_t st);
 template <int DK, int DV, bool WITH_O, bool STORE_H>
 hipError_t launch_scan_bf16(const ScanArgs& a, hipStream_t st);
+// both segment maps of the sequence-parallel forward scan in one launch (Dk = Dv = D):
+// N into a.STseg, M into a.STseg_m
+template <int D>
+hipError_t launch_scan_map_bf16(const ScanArgs& a, hipStream_t st);
 template <int DK, int DV>
 hipError_t launch_bchunk_bf16(const BChunkBf16Args& a, hipStream_t st);
 template <int DK, int DV>

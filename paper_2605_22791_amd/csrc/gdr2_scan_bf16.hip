@@ -16,28 +16,37 @@
 // and R are written for the backward (alone in the backward's recompute, or
 // with the output when the forward keeps them).
 // With nseg > 1 each workgroup scans one segment of a sequence from a given
-// start state (ScanArgs), which the sequence-parallel mode builds on.
+// start state (ScanArgs), which the sequence-parallel mode builds on.  Its
+// map pass (MAP, Dk = DV) forms both segment maps in one launch: per segment
+// one workgroup takes the whole value width of N (zero start, input U) and
+// one the whole of M (identity start, no input), on the same XCD, so the Y
+// and Ktail^T blocks of a step are read by two workgroups rather than by the
+// four that two passes of 64-wide slices need.  Its Y S products use both
+// parts of S, so the maps are fp32-accurate: the reverse scan chains the
+// gradient with M^T (its segment map), the exact transpose of this one.
 //
-// Precision: Y S uses the bf16 part of S (Y itself is bf16); every other
-// product is split hi/lo and fp32-accurate.
+// Precision: Y S uses the bf16 part of S (Y itself is bf16), except in the
+// map pass, which adds the lo part; every other product is split hi/lo and
+// fp32-accurate.
 
 #include "gdr2_kernels.hpp"
 #include "gdr2_bf16.hpp"
 
 namespace gdr2 {
 
-template <int DK, int DV>
+template <int DK, int DV, bool MAP = false>
 struct ScanCfg2 {
   static constexpr int NTHR = 512;
-  static constexpr int DVS = DV < 64 ? DV : 64;
-  static constexpr int NS = DV / DVS;
+  // MAP: two "slices" of the full width, the N map and the M map
+  static constexpr int DVS = MAP ? DV : (DV < 64 ? DV : 64);
+  static constexpr int NS = MAP ? 2 : DV / DVS;
   static constexpr int KS = DK / 32, NCB = DK / 16, NVB = DVS / 16;
   static constexpr int TPW = NCB * NVB / 8;  // state tiles per wave
   static constexpr int LSS = DK + 8;         // S hi/lo [DVS][LSS] bf16
   static constexpr int LR = 64 + 8;          // R hi/lo [DVS][LR] bf16
-  // operand blocks, copied verbatim (contiguous Y | Qg | Aqk | KtT)
-  static constexpr int SZ_Y = (int)WsBf16::y(DK), SZ_Q = (int)WsBf16::qg(DK);
-  static constexpr int SZ_A = (int)WsBf16::aqk(), SZ_K = (int)WsBf16::ktt(DK);
+  // operand blocks, copied verbatim (contiguous Y | Qg | Aqk | KtT; MAP: Y | KtT)
+  static constexpr int SZ_Y = (int)WsBf16::y(DK), SZ_Q = MAP ? 0 : (int)WsBf16::qg(DK);
+  static constexpr int SZ_A = MAP ? 0 : (int)WsBf16::aqk(), SZ_K = (int)WsBf16::ktt(DK);
   static constexpr int SZ_OP = SZ_Y + SZ_Q + SZ_A + SZ_K;
   static constexpr int NSTG = SZ_OP / (16 * NTHR);  // 16-byte chunks per thread
   static constexpr int OFF_S = 0;
@@ -47,6 +56,7 @@ struct ScanCfg2 {
   static_assert(SZ_OP % (16 * NTHR) == 0, "operand staging split");
   static_assert(LDS <= 160 * 1024, "LDS budget");
   static_assert(TPW >= 1 && NVB % 2 == 0, "wave split");
+  static_assert(!MAP || DK == DV, "map pass: square maps");
 };
 
 // B fragment of S for Y S in the permuted key order of Y's fragments:
@@ -60,9 +70,10 @@ __device__ __forceinline__ bf8 ld_perm8(const __bf16* row, int k0, int g) {
   return r;
 }
 
-template <int DK, int DV, bool WITH_O, bool STORE_H>
+template <int DK, int DV, bool WITH_O, bool STORE_H, bool MAP>
 __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
-  using C = ScanCfg2<DK, DV>;
+  static_assert(!MAP || (!WITH_O && !STORE_H), "the map pass writes the maps only");
+  using C = ScanCfg2<DK, DV, MAP>;
   constexpr int DVS = C::DVS, NS = C::NS, KS = C::KS, NCB = C::NCB, NVB = C::NVB, TPW = C::TPW;
   constexpr int LSS = C::LSS, LR = C::LR, NSTG = C::NSTG;
 
@@ -100,9 +111,10 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
   const ScanRange rng = scan_range(a.vl, seq, H, NT);
   const int seg_len = a.seg_len > 0 ? a.seg_len : rng.c1 - rng.c0;
   const int n0 = rng.c0 + seg * seg_len, n1 = min(rng.c1, n0 + seg_len);
-  const bool no_input = (a.flags & kScanNoInput) != 0;
+  // MAP: slice 0 is the N map (input U, zero start), slice 1 the M map
+  const bool no_input = MAP ? slice == 1 : (a.flags & kScanNoInput) != 0;
   const int h = seq % H;
-  const int v0 = slice * DVS;
+  const int v0 = MAP ? 0 : slice * DVS;
   __bf16* O = reinterpret_cast<__bf16*>(a.o);
 
   // wave roles
@@ -153,7 +165,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
       a.GC[(CHKX) * (WsBf16::gc(DK) / 4) + 16 * cs + 4 * g + u2];
 
   // ---- state: identity columns, the given segment start, S0 (first segment) or zero
-  const bool eye = (a.flags & kScanEye) != 0;  // (DV == DK)
+  const bool eye = MAP ? slice == 1 : (a.flags & kScanEye) != 0;  // (DV == DK)
   const float* init = eye ? nullptr
                           : (a.S0seg ? a.S0seg + (size_t)vs * DK * DV
                                      : ((a.S0 && seg == 0) ? a.S0 + (size_t)seq * DK * DV : nullptr));
@@ -196,7 +208,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
     // scale exponents of this chunk-start state's fp16 copy, early in the step
     // so that their cross-lane reductions overlap the products below
     int hsh[TPW / 2];
-    if (STORE_H) state_shifts<TPW>(sreg, hsh);
+    if constexpr (STORE_H) state_shifts<TPW>(sreg, hsh);
 
     // ---- R = U - Y S
     f4 racc[NVB / 2];
@@ -210,6 +222,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
       for (int t = 0; t < NVB / 2; ++t) {
         const int vb = vbO + t;
         racc[t] = mma(yf, ld_perm8(sShi + (16 * vb + r16) * LSS, 32 * p, g), racc[t]);
+        if constexpr (MAP) racc[t] = mma(yf, ld_perm8(sSlo + (16 * vb + r16) * LSS, 32 * p, g), racc[t]);
       }
     }
 #pragma unroll
@@ -219,12 +232,12 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
                racc[t]);
     }
     // the fp16 copy's scale, taken here so its reduction overlaps the output products
-    if (STORE_H) state_shifts<NVB / 2>(racc, rsh);
+    if constexpr (STORE_H) state_shifts<NVB / 2>(racc, rsh);
     __syncthreads();
 
     // ---- O^T = S^T Q_g^T + R^T A_qk^T  (lane: O[16 iO + r16][16 vb + 4 g + u]);
     //      each K-step's fragments are read from LDS one step ahead
-    if (WITH_O) {
+    if constexpr (WITH_O) {
       f4 accO[NVB / 2];
 #pragma unroll
       for (int t = 0; t < NVB / 2; ++t) accO[t] = f4zero();
@@ -277,7 +290,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
     }
 
     // ---- S <- Diag(gamma_C) S + Ktail^T R
-    if (STORE_H) {
+    if constexpr (STORE_H) {
       // the chunk-start state for the backward, fp16 with its block scales
       // (from a copy: the state registers change right below)
       f4 hcopy[TPW];
@@ -309,7 +322,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
 #pragma unroll
         for (int t = 0; t < TPW; ++t) sreg[t] = mma3(kf[kb], rfs[kb][t], sreg[t]);
     }
-    if (STORE_H) {
+    if constexpr (STORE_H) {
       // R for the backward: this wave's 16 x 32 tile as one fp16 fragment block
       static_assert(NVB / 2 == 2, "one 32-column block per wave");
       const int vblk = (v0 + 16 * vbO) / 32;
@@ -340,8 +353,9 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
 #undef GDR2_STORE_OPS
 #undef GDR2_OP_USED
 #undef GDR2_LOAD_UG
-  float* send = a.STseg ? a.STseg + (size_t)vs * DK * DV
-                        : ((a.ST && seg == nseg - 1) ? a.ST + (size_t)seq * DK * DV : nullptr);
+  float* send = MAP ? (slice == 0 ? a.STseg : a.STseg_m) + (size_t)vs * DK * DV
+                    : (a.STseg ? a.STseg + (size_t)vs * DK * DV
+                               : ((a.ST && seg == nseg - 1) ? a.ST + (size_t)seq * DK * DV : nullptr));
   if (send) {
 #pragma unroll
     for (int t = 0; t < TPW; ++t)
@@ -350,16 +364,28 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
   }
 }
 
-template <int DK, int DV, bool WITH_O, bool STORE_H>
-hipError_t launch_scan_bf16(const ScanArgs& a, hipStream_t st) {
-  using C = ScanCfg2<DK, DV>;
-  const void* fn = reinterpret_cast<const void*>(&scan_bf16_kernel<DK, DV, WITH_O, STORE_H>);
+template <int DK, int DV, bool WITH_O, bool STORE_H, bool MAP>
+hipError_t launch_scan_bf16_t(const ScanArgs& a, hipStream_t st) {
+  using C = ScanCfg2<DK, DV, MAP>;
+  const void* fn = reinterpret_cast<const void*>(&scan_bf16_kernel<DK, DV, WITH_O, STORE_H, MAP>);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
   if (e != hipSuccess) return e;
   dim3 grid(a.B * a.H * a.nseg * C::NS);
-  hipLaunchKernelGGL((scan_bf16_kernel<DK, DV, WITH_O, STORE_H>), grid, dim3(C::NTHR), C::LDS, st, a);
+  hipLaunchKernelGGL((scan_bf16_kernel<DK, DV, WITH_O, STORE_H, MAP>), grid, dim3(C::NTHR), C::LDS, st, a);
   return hipGetLastError();
 }
+
+template <int DK, int DV, bool WITH_O, bool STORE_H>
+hipError_t launch_scan_bf16(const ScanArgs& a, hipStream_t st) {
+  return launch_scan_bf16_t<DK, DV, WITH_O, STORE_H, false>(a, st);
+}
+
+template <int D>
+hipError_t launch_scan_map_bf16(const ScanArgs& a, hipStream_t st) {
+  return launch_scan_bf16_t<D, D, false, false, true>(a, st);
+}
+template hipError_t launch_scan_map_bf16<64>(const ScanArgs&, hipStream_t);
+template hipError_t launch_scan_map_bf16<128>(const ScanArgs&, hipStream_t);
 
 #define GDR2_INST_SCAN2(DK, DV)                                                          \
   template hipError_t launch_scan_bf16<DK, DV, true, false>(const ScanArgs&, hipStream_t); \

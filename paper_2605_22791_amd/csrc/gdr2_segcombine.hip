@@ -9,7 +9,10 @@
 // the gradient is affine the same way (App. B.1).  This kernel walks the
 // segments of each sequence in order (forward) or backwards (reverse),
 // X <- M_k X + N_k, and writes the value entering every segment; the segments
-// are then re-scanned in parallel from those values.
+// are then re-scanned in parallel from those values.  With no input a chunk's
+// reverse step, dS <- Diag(gamma_C) dS - Y^T (Ktail dS), is the transpose of
+// its forward step, so the reverse chain of a square state can use the
+// forward's maps as M_k^T (transpose_m).
 //
 // One 4-wave workgroup per (sequence, 64-wide value slice).  X lives in fp32
 // MFMA accumulators and, for the product, as a split bf16 copy X^T in LDS;
@@ -91,7 +94,13 @@ __global__ __launch_bounds__(256) void segcombine_kernel(SegCombineArgs a) {
 #pragma unroll
       for (int cc = 0; cc < CPW; ++cc) {
         float m[8];
-        ldf8(M + (size_t)(16 * (CPW * wave + cc) + r16) * DK + 32 * p + 8 * g, m);
+        const int mr = 16 * (CPW * wave + cc) + r16, mc = 32 * p + 8 * g;
+        if (a.transpose_m) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) m[e] = M[(size_t)(mc + e) * DK + mr];
+        } else {
+          ldf8(M + (size_t)mr * DK + mc, m);
+        }
         const Fr mf = split8(m);
 #pragma unroll
         for (int vb = 0; vb < 4; ++vb) x[cc][vb] = mma3(mf, xf[vb], x[cc][vb]);
