@@ -233,10 +233,14 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   const int g = lane >> 4, r16 = lane & 15;
   ChunkPos cp;
   // the grid covers the key heads; this launch takes value head gj of each group
-  const int h = blockIdx.y * a.G + a.gj, H = a.H;
+  // workgroups in launch order take the key heads fastest, then the chunks: the
+  // ones resident together read and write neighbouring parts of the same token rows
+  const int lin = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+  const int bx = (lin / gridDim.y) % gridDim.x, by = lin % gridDim.y, bz = lin / (gridDim.y * gridDim.x);
+  const int h = by * a.G + a.gj, H = a.H;
   // fused stage: this workgroup's slot of the decay-parameter partials
-  const size_t pslot = ((size_t)(blockIdx.z * gridDim.x + blockIdx.x) * H + h) * 4 + wave;
-  if (!chunk_pos(a.vl, blockIdx.x, h, blockIdx.z, a.T, H, a.NT, cp)) {
+  const size_t pslot = ((size_t)(bz * gridDim.x + bx) * H + h) * 4 + wave;
+  if (!chunk_pos(a.vl, bx, h, bz, a.T, H, a.NT, cp)) {
     if constexpr (FUSED) {  // an unused slot of a packed grid adds zeros
       for (int c = lane; c < DK; c += 64) a.PD[pslot * DK + c] = 0.f;
       if (lane == 0) a.PA[pslot] = 0.f;
@@ -253,7 +257,7 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   // key-side inputs (q, k, g, b) and gradients live on the H / G key heads
   // (value head h reads key head h / G); the fused stage keeps dq, dk in fp32
   // (partq; one rounding after its normalisation VJP)
-  const int HK = H / a.G, hk = blockIdx.y;
+  const int HK = H / a.G, hk = by;
   const bool partq = a.Pq != nullptr;
   const int gmode = a.gmode;  // 0: direct, 1 / 2 / 3: first / middle / last value head of a group
   const size_t KST = (size_t)HK * DK, VST = (size_t)H * DV;  // token strides
