@@ -42,7 +42,9 @@ struct ScanCfg2 {
   static constexpr int NS = MAP ? 2 : DV / DVS;
   static constexpr int KS = DK / 32, NCB = DK / 16, NVB = DVS / 16;
   static constexpr int TPW = NCB * NVB / 8;  // state tiles per wave
-  static constexpr int LSS = DK + 8;         // S hi/lo [DVS][LSS] bf16
+  // S hi/lo [DVS][LSS] bf16; the map pass keeps it in the permuted K order of
+  // Y's fragments, unpadded, its 16-byte pieces XOR'd with the row (map_s_ix)
+  static constexpr int LSS = MAP ? DK : DK + 8;
   static constexpr int LR = 64 + 8;          // R hi/lo [DVS][LR] bf16
   // operand blocks, copied verbatim (contiguous Y | Qg | Aqk | KtT; MAP: Y | KtT)
   static constexpr int SZ_Y = (int)WsBf16::y(DK), SZ_Q = MAP ? 0 : (int)WsBf16::qg(DK);
@@ -58,6 +60,22 @@ struct ScanCfg2 {
   static_assert(TPW >= 1 && NVB % 2 == 0, "wave split");
   static_assert(!MAP || DK == DV, "map pass: square maps");
 };
+
+// Map pass: element (row v, key c) of S^T in LDS, keys in the permuted order of
+// Y's fragments (4 m + e and 16 + 4 m + e side by side at 8 m + e, 8 m + 4 + e
+// of each 32-key group) and the 16-byte pieces of a row XOR'd with v % 16, so
+// that Y's B fragment is one 16-byte read and those reads are free of bank
+// conflicts.  c4 is a multiple of 4: the 4 keys c4 .. c4 + 3 stay together.
+template <int LD>
+__device__ __forceinline__ int map_s_ix(int v, int c4) {
+  const int a = (c4 & 31) >> 2, pos = (c4 & ~31) + (a < 4 ? 8 * a : 8 * (a - 4) + 4);
+  return v * LD + ((((pos >> 3) ^ (v & 15)) << 3) | (pos & 7));
+}
+// its B fragment for K-step p: keys 32 p + 4 g + (0..3) and 32 p + 16 + 4 g + (0..3)
+template <int LD>
+__device__ __forceinline__ int map_s_frag(int v, int p, int g) {
+  return v * LD + (((4 * p + g) ^ (v & 15)) << 3);
+}
 
 // B fragment of S for Y S in the permuted key order of Y's fragments:
 // S[c][v] for c = k0 + 4 g + u and k0 + 16 + 4 g + u (stored [v][c]).
@@ -184,8 +202,8 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
 #pragma unroll
   for (int t = 0; t < TPW; ++t) {
     const int vb = sv0 + t;
-    st4split(sShi + (16 * vb + r16) * LSS + 16 * cs + 4 * g, sSlo + (16 * vb + r16) * LSS + 16 * cs + 4 * g,
-             sreg[t]);
+    const int so = MAP ? map_s_ix<LSS>(16 * vb + r16, 16 * cs + 4 * g) : (16 * vb + r16) * LSS + 16 * cs + 4 * g;
+    st4split(sShi + so, sSlo + so, sreg[t]);
   }
   if (n0 < n1) {
     GDR2_LOAD_OPS(chk + n0)
@@ -221,8 +239,13 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
 #pragma unroll
       for (int t = 0; t < NVB / 2; ++t) {
         const int vb = vbO + t;
-        racc[t] = mma(yf, ld_perm8(sShi + (16 * vb + r16) * LSS, 32 * p, g), racc[t]);
-        if constexpr (MAP) racc[t] = mma(yf, ld_perm8(sSlo + (16 * vb + r16) * LSS, 32 * p, g), racc[t]);
+        if constexpr (MAP) {
+          const int sf = map_s_frag<LSS>(16 * vb + r16, p, g);
+          racc[t] = mma(yf, ld8(sShi + sf), racc[t]);
+          racc[t] = mma(yf, ld8(sSlo + sf), racc[t]);
+        } else {
+          racc[t] = mma(yf, ld_perm8(sShi + (16 * vb + r16) * LSS, 32 * p, g), racc[t]);
+        }
       }
     }
 #pragma unroll
@@ -301,26 +324,48 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
                            a.Hsc + ch * (WsBf16::hsc(DK, DV) / 4) + cs * (DV / 32) + col0 / 32, lane);
     }
     {
-      Fr kf[2], rfs[2][TPW];
+      if constexpr (MAP) {
+        // the full-width map: R fragments one key-row block at a time
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        kf[kb].hi = ld8(reinterpret_cast<const __bf16*>(sK + (cs * 2 + kb) * 2048 + 16 * lane));
-        kf[kb].lo = ld8(reinterpret_cast<const __bf16*>(sK + (cs * 2 + kb) * 2048 + 1024 + 16 * lane));
+        for (int t = 0; t < TPW; ++t)
 #pragma unroll
-        for (int t = 0; t < TPW; ++t) {
-          const int vb = sv0 + t;
-          rfs[kb][t].hi = ld8(sRhi + (16 * vb + r16) * LR + 32 * kb + 8 * g);
-          rfs[kb][t].lo = ld8(sRlo + (16 * vb + r16) * LR + 32 * kb + 8 * g);
+          for (int u = 0; u < 4; ++u) sreg[t][u] *= gcur[u];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+          Fr kf, rf[TPW];
+          kf.hi = ld8(reinterpret_cast<const __bf16*>(sK + (cs * 2 + kb) * 2048 + 16 * lane));
+          kf.lo = ld8(reinterpret_cast<const __bf16*>(sK + (cs * 2 + kb) * 2048 + 1024 + 16 * lane));
+#pragma unroll
+          for (int t = 0; t < TPW; ++t) {
+            const int vb = sv0 + t;
+            rf[t].hi = ld8(sRhi + (16 * vb + r16) * LR + 32 * kb + 8 * g);
+            rf[t].lo = ld8(sRlo + (16 * vb + r16) * LR + 32 * kb + 8 * g);
+          }
+#pragma unroll
+          for (int t = 0; t < TPW; ++t) sreg[t] = mma3(kf, rf[t], sreg[t]);
         }
+      } else {
+        Fr kf[2], rfs[2][TPW];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+          kf[kb].hi = ld8(reinterpret_cast<const __bf16*>(sK + (cs * 2 + kb) * 2048 + 16 * lane));
+          kf[kb].lo = ld8(reinterpret_cast<const __bf16*>(sK + (cs * 2 + kb) * 2048 + 1024 + 16 * lane));
+#pragma unroll
+          for (int t = 0; t < TPW; ++t) {
+            const int vb = sv0 + t;
+            rfs[kb][t].hi = ld8(sRhi + (16 * vb + r16) * LR + 32 * kb + 8 * g);
+            rfs[kb][t].lo = ld8(sRlo + (16 * vb + r16) * LR + 32 * kb + 8 * g);
+          }
+        }
+#pragma unroll
+        for (int t = 0; t < TPW; ++t)
+#pragma unroll
+          for (int u = 0; u < 4; ++u) sreg[t][u] *= gcur[u];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int t = 0; t < TPW; ++t) sreg[t] = mma3(kf[kb], rfs[kb][t], sreg[t]);
       }
-#pragma unroll
-      for (int t = 0; t < TPW; ++t)
-#pragma unroll
-        for (int u = 0; u < 4; ++u) sreg[t][u] *= gcur[u];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int t = 0; t < TPW; ++t) sreg[t] = mma3(kf[kb], rfs[kb][t], sreg[t]);
     }
     if constexpr (STORE_H) {
       // R for the backward: this wave's 16 x 32 tile as one fp16 fragment block
@@ -336,8 +381,8 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
 #pragma unroll
     for (int t = 0; t < TPW; ++t) {
       const int vb = sv0 + t;
-      st4split(sShi + (16 * vb + r16) * LSS + 16 * cs + 4 * g, sSlo + (16 * vb + r16) * LSS + 16 * cs + 4 * g,
-               sreg[t]);
+      const int so = MAP ? map_s_ix<LSS>(16 * vb + r16, 16 * cs + 4 * g) : (16 * vb + r16) * LSS + 16 * cs + 4 * g;
+      st4split(sShi + so, sSlo + so, sreg[t]);
     }
     if (n + 1 < n1) {
       GDR2_STORE_OPS()
