@@ -635,6 +635,12 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
 
   const float scale = a.scale;
   float pa_acc = 0.f;  // fused stage: sum of dg * g over this lane's outputs
+  // the outputs of two key blocks leave together: an even block's row pieces wait
+  // in registers for the odd one, so that each row's 64 bytes (bf16) or 128 bytes
+  // (fp32) of the two blocks are written at once rather than as halves some
+  // microseconds apart, which the L2 may write back separately
+  static_assert(NCB % 2 == 0, "key blocks leave in pairs");
+  float wq[4], wk[4], wb[4], wg[4];
 #pragma unroll 1
   for (int cb = 0; cb < NCB; ++cb) {
     const int par = cb & 1;
@@ -786,27 +792,34 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     quad_transpose(oq, jq);
     quad_transpose(ok, jq);
     quad_transpose(ob, jq);
-    if (orow < len) {
-      const size_t ao = ko0 + oo;
+    auto emit_qkb = [&](int o, float(&vq)[4], float(&vk)[4], float(&vb)[4]) {
+      const size_t ao = ko0 + o;
       if (gmode >= 2) {  // the earlier value heads' sums
-        add_row4(a.Aq + ao, oq);
-        add_row4(a.Ak + ao, ok);
-        add_row4(a.Ab + ao, ob);
+        add_row4(a.Aq + ao, vq);
+        add_row4(a.Ak + ao, vk);
+        add_row4(a.Ab + ao, vb);
       }
       if (gmode == 1 || gmode == 2) {
-        store_row4(a.Aq + ao, oq);
-        store_row4(a.Ak + ao, ok);
-        store_row4(a.Ab + ao, ob);
+        store_row4(a.Aq + ao, vq);
+        store_row4(a.Ak + ao, vk);
+        store_row4(a.Ab + ao, vb);
       } else {
         if (partq) {
-          store_row4(pQp + oo, oq);
-          store_row4(pKp + oo, ok);
+          store_row4(pQp + o, vq);
+          store_row4(pKp + o, vk);
         } else {
-          store_row4(dQp + oo, oq);
-          store_row4(dKp + oo, ok);
+          store_row4(dQp + o, vq);
+          store_row4(dKp + o, vk);
         }
-        store_row4(dBp + oo, ob);
+        store_row4(dBp + o, vb);
       }
+    };
+    if (par == 0) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) wq[u] = oq[u], wk[u] = ok[u], wb[u] = ob[u];
+    } else if (orow < len) {
+      emit_qkb(oo - 16, wq, wk, wb);
+      emit_qkb(oo, oq, ok, ob);
     }
     // reverse cumulative sum of dG: within the lane, over the lane groups, then blocks
     const float s3 = dgl[3], s2 = s3 + dgl[2], s1 = s2 + dgl[1], s0 = s1 + dgl[0];
@@ -833,6 +846,19 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       off += sTL[(par * 4 + i2) * 16 + r16];
       if (i2 > i) off += sBT[(par * 4 + i2) * 16 + r16];
     }
+    auto emit_g = [&](float(&v)[4]) {
+      auto one = [&](int o, float(&x)[4]) {
+        if (gmode >= 2) add_row4(a.Ag + ko0 + o, x);
+        store_row4((gmode == 1 || gmode == 2) ? a.Ag + ko0 + o : dGp + o, x);
+      };
+      if (par == 0) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) wg[u] = v[u];
+      } else if (orow < len) {
+        one(oo - 16, wg);
+        one(oo, v);
+      }
+    };
     if constexpr (FUSED) {
       // df = dg * dg/df, dg/df = -exp(a) sigmoid(f + delta); partial sums for ddelta and da
       const float dgv[4] = {s0 + off, s1 + off, s2 + off, s3 + off};
@@ -847,20 +873,14 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
         }
       }
       quad_transpose(dfv, jq);
-      if (orow < len) {
-        if (gmode >= 2) add_row4(a.Ag + ko0 + oo, dfv);
-        store_row4((gmode == 1 || gmode == 2) ? a.Ag + ko0 + oo : dGp + oo, dfv);
-      }
+      emit_g(dfv);
       pdc += __shfl_xor(pdc, 16);
       pdc += __shfl_xor(pdc, 32);
       if (g == 0) a.PD[pslot * DK + 16 * cb + r16] = pdc;
     } else {
       float dgv[4] = {s0 + off, s1 + off, s2 + off, s3 + off};
       quad_transpose(dgv, jq);
-      if (orow < len) {
-        if (gmode >= 2) add_row4(a.Ag + ko0 + oo, dgv);
-        store_row4((gmode == 1 || gmode == 2) ? a.Ag + ko0 + oo : dGp + oo, dgv);
-      }
+      emit_g(dgv);
     }
     if (cb + 1 < NCB) GDR2_STAGE(par ^ 1, cb + 1)
     __syncthreads();
