@@ -177,6 +177,10 @@ __device__ __forceinline__ void store_row4(__bf16* p, const float (&v)[4]) {
 __device__ __forceinline__ void store_row4(float* p, const float (&v)[4]) {
   *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
 }
+// four outputs as bf16, packed for a later 8-byte store
+__device__ __forceinline__ uint2 pack_bf4(const float (&v)[4]) {
+  return __builtin_bit_cast(uint2, bf4{(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]});
+}
 __device__ __forceinline__ void add_row4(const float* p, float (&v)[4]) {
   const float4 x = *reinterpret_cast<const float4*>(p);
   v[0] += x.x;
@@ -635,12 +639,18 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
 
   const float scale = a.scale;
   float pa_acc = 0.f;  // fused stage: sum of dg * g over this lane's outputs
-  // the outputs of two key blocks leave together: an even block's row pieces wait
-  // in registers for the odd one, so that each row's 64 bytes (bf16) or 128 bytes
-  // (fp32) of the two blocks are written at once rather than as halves some
-  // microseconds apart, which the L2 may write back separately
-  static_assert(NCB % 2 == 0, "key blocks leave in pairs");
-  float wq[4], wk[4], wb[4], wg[4];
+  // outputs leave as whole 128-byte row lines where they can: with bf16 dq, dk,
+  // db the row pieces of three key blocks wait in registers (packed bf16) for the
+  // fourth; fp32 outputs (dg, and the fp32 partial or group sums) wait one block.
+  // Stored one 16-key block at a time, the pieces of a line would be written some
+  // microseconds apart, and the L2 often writes such a line back in parts.
+  static_assert(NCB % 4 == 0, "key blocks leave in fours");
+  const bool narrow = !FUSED && gmode == 0 && !partq;  // dq, dk, db all bf16
+  // narrow: blocks cb & 3 < 3 as bf16 (q, k, b); wide: the even block's fp32 q, k, b
+  // in the first twelve words
+  uint2 wn[9];
+  float wq[4], wk[4], wb[4];  // fused stage: the even block's q, k, b
+  float wg[4];                // dg of the even block
 #pragma unroll 1
   for (int cb = 0; cb < NCB; ++cb) {
     const int par = cb & 1;
@@ -792,8 +802,11 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     quad_transpose(oq, jq);
     quad_transpose(ok, jq);
     quad_transpose(ob, jq);
-    auto emit_qkb = [&](int o, float(&vq)[4], float(&vk)[4], float(&vb)[4]) {
+    auto emit_qkb = [&](int o, const float(&xq)[4], const float(&xk)[4], const float(&xb)[4]) {
       const size_t ao = ko0 + o;
+      float vq[4], vk[4], vb[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) vq[u] = xq[u], vk[u] = xk[u], vb[u] = xb[u];
       if (gmode >= 2) {  // the earlier value heads' sums
         add_row4(a.Aq + ao, vq);
         add_row4(a.Ak + ao, vk);
@@ -814,10 +827,47 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
         store_row4(dBp + o, vb);
       }
     };
-    if (par == 0) {
+    if (narrow) {
+      const uint2 pq = pack_bf4(oq), pk = pack_bf4(ok), pb = pack_bf4(ob);
+      switch (cb & 3) {  // uniform; constant register indices
+        case 0: wn[0] = pq, wn[1] = pk, wn[2] = pb; break;
+        case 1: wn[3] = pq, wn[4] = pk, wn[5] = pb; break;
+        case 2: wn[6] = pq, wn[7] = pk, wn[8] = pb; break;
+        default:
+          if (orow < len) {
+#pragma unroll
+            for (int t = 0; t < 3; ++t) {
+              const int o = oo - 16 * (3 - t);
+              *reinterpret_cast<uint2*>(dQp + o) = wn[3 * t];
+              *reinterpret_cast<uint2*>(dKp + o) = wn[3 * t + 1];
+              *reinterpret_cast<uint2*>(dBp + o) = wn[3 * t + 2];
+            }
+            *reinterpret_cast<uint2*>(dQp + oo) = pq;
+            *reinterpret_cast<uint2*>(dKp + oo) = pk;
+            *reinterpret_cast<uint2*>(dBp + oo) = pb;
+          }
+      }
+    } else if (FUSED) {
+      if (par != 0 && orow < len) {
+        emit_qkb(oo - 16, wq, wk, wb);
+        emit_qkb(oo, oq, ok, ob);
+      }
 #pragma unroll
       for (int u = 0; u < 4; ++u) wq[u] = oq[u], wk[u] = ok[u], wb[u] = ob[u];
+    } else if (par == 0) {
+#pragma unroll
+      for (int u = 0; u < 4; u += 2) {
+        wn[u / 2] = uint2{__float_as_uint(oq[u]), __float_as_uint(oq[u + 1])};
+        wn[2 + u / 2] = uint2{__float_as_uint(ok[u]), __float_as_uint(ok[u + 1])};
+        wn[4 + u / 2] = uint2{__float_as_uint(ob[u]), __float_as_uint(ob[u + 1])};
+      }
     } else if (orow < len) {
+#pragma unroll
+      for (int u = 0; u < 4; u += 2) {
+        wq[u] = __uint_as_float(wn[u / 2].x), wq[u + 1] = __uint_as_float(wn[u / 2].y);
+        wk[u] = __uint_as_float(wn[2 + u / 2].x), wk[u + 1] = __uint_as_float(wn[2 + u / 2].y);
+        wb[u] = __uint_as_float(wn[4 + u / 2].x), wb[u + 1] = __uint_as_float(wn[4 + u / 2].y);
+      }
       emit_qkb(oo - 16, wq, wk, wb);
       emit_qkb(oo, oq, ok, ob);
     }
@@ -847,17 +897,19 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       if (i2 > i) off += sBT[(par * 4 + i2) * 16 + r16];
     }
     auto emit_g = [&](float(&v)[4]) {
-      auto one = [&](int o, float(&x)[4]) {
+      auto one = [&](int o, const float(&y)[4]) {
+        float x[4] = {y[0], y[1], y[2], y[3]};
         if (gmode >= 2) add_row4(a.Ag + ko0 + o, x);
         store_row4((gmode == 1 || gmode == 2) ? a.Ag + ko0 + o : dGp + o, x);
       };
-      if (par == 0) {
-#pragma unroll
-        for (int u = 0; u < 4; ++u) wg[u] = v[u];
-      } else if (orow < len) {
+      if (par != 0 && orow < len) {
         one(oo - 16, wg);
         one(oo, v);
       }
+      // held unconditionally (an odd block's copy is not used): a branch here
+      // would let the compiler merge it with the stores above and keep wg in memory
+#pragma unroll
+      for (int u = 0; u < 4; ++u) wg[u] = v[u];
     };
     if constexpr (FUSED) {
       // df = dg * dg/df, dg/df = -exp(a) sigmoid(f + delta); partial sums for ddelta and da
