@@ -22,11 +22,20 @@ struct Varlen {
   int nseq = 0, ncmax = 0;    // sequences; chunk slots (grid and workspace extent)
 };
 
+// Entry i of a chunk table.  The tables are written before any kernel that
+// reads them starts and never while it runs, so they are read through the
+// constant address space: with a uniform index that is a scalar load, which
+// the kernels' waits for their vector loads (the next chunk's operands, counted
+// in issue order) do not have to wait behind.
+__device__ __forceinline__ int ld_table(const int* p, int i) {
+  return ((const __attribute__((address_space(4))) int*)p)[i];
+}
+
 // Scanned pair (sequence, head) of a scan workgroup's index q: for packed
 // calls the sequences are taken longest first, so that the longest scans start
 // with the grid and the short ones fill in behind them.
 __device__ __forceinline__ int scan_pair(const Varlen& vl, int q, int H) {
-  return vl.sorder != nullptr ? vl.sorder[q / H] * H + q % H : q;
+  return vl.sorder != nullptr ? ld_table(vl.sorder, q / H) * H + q % H : q;
 }
 
 struct ChunkPos {
@@ -40,9 +49,9 @@ struct ChunkPos {
 __device__ __forceinline__ bool chunk_pos(const Varlen& vl, int x, int h, int bb, int T, int H, int NT,
                                           ChunkPos& p) {
   if (vl.ct0 != nullptr) {
-    if (x >= vl.coff[vl.nseq]) return false;
-    p.row0 = (size_t)vl.ct0[x];
-    p.len = vl.clen[x];
+    if (x >= ld_table(vl.coff, vl.nseq)) return false;
+    p.row0 = (size_t)ld_table(vl.ct0, x);
+    p.len = ld_table(vl.clen, x);
     p.ch = (size_t)h * vl.ncmax + x;
   } else {
     p.row0 = (size_t)bb * T + (size_t)x * CH;
@@ -76,14 +85,14 @@ struct ScanRange {
   int c0, c1;
 };
 __device__ __forceinline__ ScanRange scan_range(const Varlen& vl, int q, int H, int NT) {
-  if (vl.coff != nullptr) return {(size_t)(q % H) * vl.ncmax, vl.coff[q / H], vl.coff[q / H + 1]};
+  if (vl.coff != nullptr) return {(size_t)(q % H) * vl.ncmax, ld_table(vl.coff, q / H), ld_table(vl.coff, q / H + 1)};
   return {(size_t)q * NT, 0, NT};
 }
 // First token row and rows in use of chunk c of the scanned pair q.
 __device__ __forceinline__ void scan_rows(const Varlen& vl, int q, int H, int T, int c, size_t& row0, int& len) {
   if (vl.ct0 != nullptr) {
-    row0 = (size_t)vl.ct0[c];
-    len = vl.clen[c];
+    row0 = (size_t)ld_table(vl.ct0, c);
+    len = ld_table(vl.clen, c);
   } else {
     row0 = (size_t)(q / H) * T + (size_t)c * CH;
     len = min(CH, T - c * CH);

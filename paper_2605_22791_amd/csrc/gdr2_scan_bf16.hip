@@ -155,8 +155,9 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
   const size_t chk = key_ch(a.vl, chs, H, a.G, NT);  // key-head chunks: Y, Q_g, A_qk, K_tail, gamma_C
   // Q_g and A_qk feed the output only: a scan without it moves Y and Ktail^T alone
 #define GDR2_OP_USED(M_) (WITH_O || (M_) < E_Y || (M_) >= E_A)
-#define GDR2_LOAD_OPS(CHX)                                                                                   \
-  _Pragma("unroll") for (int m = 0; m < NSTG; ++m) {                                                     \
+// operand slices [M0, M1) of chunk CHX (the slices a step's products do not read are skipped)
+#define GDR2_LOAD_OPS(CHX, M0, M1)                                                                           \
+  _Pragma("unroll") for (int m = (M0); m < (M1) && m < NSTG; ++m) {                                      \
     if (!GDR2_OP_USED(m)) continue;                                                                      \
     const unsigned char* src;                                                                            \
     if (m < E_Y)                                                                                         \
@@ -167,7 +168,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
       src = a.Aqk + (CHX) * C::SZ_A + (m - E_Q) * SLICE;                                                 \
     else                                                                                                 \
       src = a.KtT + (CHX) * C::SZ_K + (m - E_A) * SLICE;                                                 \
-    stg[m] = ldg16(src + 16 * tid);                                            \
+    stg[m] = ldg16(src + 16 * tid);                                                                      \
   }
 #define GDR2_STORE_OPS()                                                                                     \
   _Pragma("unroll") for (int m = 0; m < NSTG; ++m) if (GDR2_OP_USED(m)) sts16(sOp + m * SLICE + 16 * tid, stg[m]);
@@ -206,7 +207,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
     st4split(sShi + so, sSlo + so, sreg[t]);
   }
   if (n0 < n1) {
-    GDR2_LOAD_OPS(chk + n0)
+    GDR2_LOAD_OPS(chk + n0, 0, NSTG)
     GDR2_LOAD_UG(chs + n0, chk + n0, ucur, gcur)
     GDR2_STORE_OPS()
   }
@@ -214,12 +215,15 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
 
   for (int n = n0; n < n1; ++n) {
     const size_t ch = chs + n;
-    // the next chunk's operands, fetched first: one vmcnt counts loads and
+    // the next chunk's operands, fetched in groups over the step (the first
+    // here, the others after R, inside the output products and after them):
+    // all at once, the second wave of each SIMD waits behind the first one's
+    // loads before it can start its products.  One vmcnt counts loads and
     // stores in issue order, so waiting for these also waits for every store
-    // issued before them; this step's stores (R, O, h) therefore come after
-    // its products, and the previous step's have had that whole step
-    if (n + 1 < n1) {
-      GDR2_LOAD_OPS(chk + n + 1)
+    // issued before them; this step's stores (R, O, h) come after the last group
+    const bool more = n + 1 < n1;
+    if (more) {
+      GDR2_LOAD_OPS(chk + n + 1, 0, 3)
       GDR2_LOAD_UG(ch + 1, chk + n + 1, unext, gnext)
     }
 
@@ -256,6 +260,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
     }
     // the fp16 copy's scale, taken here so its reduction overlaps the output products
     if constexpr (STORE_H) state_shifts<NVB / 2>(racc, rsh);
+    if (more) GDR2_LOAD_OPS(chk + n + 1, 3, WITH_O ? 6 : 10)
     __syncthreads();
 
     // ---- O^T = S^T Q_g^T + R^T A_qk^T  (lane: O[16 iO + r16][16 vb + 4 g + u]);
@@ -294,6 +299,8 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
         const bool live = p < KS || (p - KS) <= (iO >> 1);
         const bool next = p + 1 < NKO && (p + 1 < KS || (p + 1 - KS) <= (iO >> 1));
         if (next) GDR2_O_FRAGS(p + 1, (p + 1) & 1)
+        if (more && p == 1) GDR2_LOAD_OPS(chk + n + 1, 6, 8)
+        if (more && p == 3) GDR2_LOAD_OPS(chk + n + 1, 8, 10)
         if (live) {
 #pragma unroll
           for (int t = 0; t < NVB / 2; ++t) accO[t] = mma3(fb[p & 1][t], fa[p & 1], accO[t]);
@@ -312,6 +319,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
       }
     }
 
+    if (more) GDR2_LOAD_OPS(chk + n + 1, 10, NSTG)
     // ---- S <- Diag(gamma_C) S + Ktail^T R
     if constexpr (STORE_H) {
       // the chunk-start state for the backward, fp16 with its block scales
@@ -384,7 +392,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
       const int so = MAP ? map_s_ix<LSS>(16 * vb + r16, 16 * cs + 4 * g) : (16 * vb + r16) * LSS + 16 * cs + 4 * g;
       st4split(sShi + so, sSlo + so, sreg[t]);
     }
-    if (n + 1 < n1) {
+    if (more) {
       GDR2_STORE_OPS()
 #pragma unroll
       for (int t = 0; t < NVB / 2; ++t) ucur[t] = unext[t];
