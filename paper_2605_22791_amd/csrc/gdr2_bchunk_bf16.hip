@@ -235,6 +235,7 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   // the wave index as a scalar: branches on the row block are uniform
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, r16 = lane & 15;
+  const bool podd = (g & 1) != 0, pup = g >= 2;  // the lane's 16-lane row: odd; 2 or 3
   ChunkPos cp;
   // the grid covers the key heads; this launch takes value head gj of each group
   // workgroups in launch order take the key heads fastest, then the chunks: the
@@ -434,15 +435,32 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       pk = bf4{};                                                                          \
     }                                                                                      \
     float x_[4] = {pg.x * kLog2e, pg.y * kLog2e, pg.z * kLog2e, pg.w * kLog2e};            \
-    _Pragma("unroll") for (int o_ = 4; o_ < 64; o_ <<= 1) {                                \
-      _Pragma("unroll") for (int u_ = 0; u_ < 4; ++u_) {                                   \
-        const float y_ = __shfl_up(x_[u_], o_);                                            \
-        x_[u_] += lane >= o_ ? y_ : 0.f;                                                   \
-      }                                                                                    \
+    /* inclusive sums over the block's 16 rows (lanes 4 rl + cq), with the first  */     \
+    /* row's value f_ and the total l_: DPP shifts by 4 and 8 lanes inside each    */     \
+    /* 16-lane row, the row totals spread over the row by rotations, then the     */     \
+    /* earlier rows' totals from the partner rows (no LDS round trips)             */     \
+    float fs_[4], ls_[4];                                                                  \
+    _Pragma("unroll") for (int u_ = 0; u_ < 4; ++u_) {                                     \
+      float x1_ = x_[u_];                                                                  \
+      float f1_ = lane < 4 ? x1_ : 0.f;                                                    \
+      x1_ += dppf<0x114>(x1_); /* row_shr:4 */                                             \
+      x1_ += dppf<0x118>(x1_); /* row_shr:8 */                                             \
+      float t1_ = (rl & 3) == 3 ? x1_ : 0.f;                                               \
+      t1_ += dppf<0x124>(t1_); /* row_ror:4 */                                             \
+      t1_ += dppf<0x128>(t1_); /* row_ror:8 */                                             \
+      f1_ += dppf<0x124>(f1_);                                                             \
+      f1_ += dppf<0x128>(f1_);                                                             \
+      const float p1_ = row_partner16(t1_, podd);                                          \
+      const float s1_ = t1_ + p1_;                                                         \
+      const float q1_ = row_partner32(s1_, pup);                                           \
+      x_[u_] = x1_ + (podd ? p1_ : 0.f) + (pup ? q1_ : 0.f);                               \
+      ls_[u_] = s1_ + q1_;                                                                 \
+      f1_ += row_partner16(f1_, podd);                                                     \
+      fs_[u_] = f1_ + row_partner32(f1_, pup);                                             \
     }                                                                                      \
     f4 xk_, xb_, xq_;                                                                      \
     _Pragma("unroll") for (int u_ = 0; u_ < 4; ++u_) {                                     \
-      const float f_ = __shfl(x_[u_], cq), l_ = __shfl(x_[u_], 60 + cq);                   \
+      const float f_ = fs_[u_], l_ = ls_[u_];                                              \
       sG[aTs + kTabLd * u_] = x_[u_];                                                      \
       const float el_ = ex2(x_[u_] - f_), er_ = ex2(l_ - x_[u_]);                          \
       const float kv_ = (float)pk[u_];                                                     \
@@ -469,7 +487,7 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       sts16(sD16 + aHs, pd);                                                               \
       float hh_ = hx_[0] * dx_[0];                                                         \
       _Pragma("unroll") for (int e_ = 1; e_ < 8; ++e_) hh_ += hx_[e_] * dx_[e_];           \
-      _Pragma("unroll") for (int o_ = DV / 16; o_ >= 1; o_ >>= 1) hh_ += __shfl_xor(hh_, o_); \
+      hh_ = row_sum<DV == 64>(hh_); /* the DV / 8 lanes of row hc */                     \
       if ((tid % (DV / 8)) == 0) sHH[(PAR) * 16 + hc] = hh_;                               \
     }                                                                                      \
     dscl = pds;                                                                            \
@@ -875,14 +893,14 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     const float s3 = dgl[3], s2 = s3 + dgl[2], s1 = s2 + dgl[1], s0 = s1 + dgl[0];
     float y = s0;
     {
-      const float t1 = __shfl_down(y, 16);
-      y += g < 3 ? t1 : 0.f;
-      const float t2 = __shfl_down(y, 32);
-      y += g < 2 ? t2 : 0.f;
+      // suffix over the four lane groups g (16-lane rows): pair sums, then the other pair
+      const float py = y + row_partner16(y, podd);
+      const float qy = row_partner32(py, pup);
+      y = (podd ? y : py) + (pup ? 0.f : qy);
     }
     float tp = tailp;
-    tp += __shfl_xor(tp, 16);
-    tp += __shfl_xor(tp, 32);
+    tp += row_partner16(tp, podd);
+    tp += row_partner32(tp, pup);
     if (g == 0) {
       sBT[(par * 4 + i) * 16 + r16] = y;
       sTL[(par * 4 + i) * 16 + r16] = tp;
@@ -926,8 +944,8 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       }
       quad_transpose(dfv, jq);
       emit_g(dfv);
-      pdc += __shfl_xor(pdc, 16);
-      pdc += __shfl_xor(pdc, 32);
+      pdc += row_partner16(pdc, podd);
+      pdc += row_partner32(pdc, pup);
       if (g == 0) a.PD[pslot * DK + 16 * cb + r16] = pdc;
     } else {
       float dgv[4] = {s0 + off, s1 + off, s2 + off, s3 + off};

@@ -231,6 +231,28 @@ __device__ __forceinline__ float wave_max(float x) {
   const float r3 = __int_as_float(__builtin_amdgcn_readlane(b, 48));
   return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
 }
+// The value the same lane holds in the partner 16-lane row: rows 2k and 2k + 1
+// (row_partner16), rows k and k + 2 (row_partner32), from one v_permlane16_swap
+// / v_permlane32_swap of the value with itself (VALU, no LDS round trip).  odd:
+// the lane's row is odd; upper: its row is 2 or 3.
+__device__ __forceinline__ float row_partner16(float x, bool odd) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(odd ? r[0] : r[1]);
+}
+__device__ __forceinline__ float row_partner32(float x, bool upper) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(upper ? r[0] : r[1]);
+}
+// Sum over the 16 lanes of each row (every lane gets it): quad swaps, then the
+// half-row and row mirrors; with HALF, over each 8-lane half-row instead.
+template <bool HALF = false>
+__device__ __forceinline__ float row_sum(float x) {
+  x += dppf<0xB1>(x);   // quad_perm [1, 0, 3, 2]
+  x += dppf<0x4E>(x);   // quad_perm [2, 3, 0, 1]
+  x += dppf<0x141>(x);  // row_half_mirror
+  if constexpr (!HALF) x += dppf<0x140>(x);  // row_mirror
+  return x;
+}
 // Power-of-two exponent that maps the block maximum m >= 0 into [2^14, 2^15)
 // (0 for m = 0 or a non-finite m, whose values then pass through unscaled).
 __device__ __forceinline__ int state_shift(float m) {
