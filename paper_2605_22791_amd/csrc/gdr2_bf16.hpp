@@ -243,6 +243,28 @@ __device__ __forceinline__ float row_partner32(float x, bool upper) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   return __uint_as_float(upper ? r[0] : r[1]);
 }
+// 4 x 4 transpose across the four 16-lane rows, lane by lane: on entry row R
+// holds v[u] = M[R][u], on exit v[u] = M[u][R].  permlane16_swap(a, b) trades
+// a's odd rows for b's even rows, permlane32_swap(a, b) a's rows 2, 3 for b's
+// rows 0, 1.
+__device__ __forceinline__ void row_transpose4(f4& v) {
+  auto sw16 = [](float& a, float& b) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+    a = __uint_as_float(r[0]);
+    b = __uint_as_float(r[1]);
+  };
+  auto sw32 = [](float& a, float& b) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+    a = __uint_as_float(r[0]);
+    b = __uint_as_float(r[1]);
+  };
+  float x0 = v[0], x1 = v[1], x2 = v[2], x3 = v[3];
+  sw16(x0, x1);
+  sw16(x2, x3);
+  sw32(x0, x2);
+  sw32(x1, x3);
+  v[0] = x0, v[1] = x1, v[2] = x2, v[3] = x3;
+}
 // Sum over the 16 lanes of each row (every lane gets it): quad swaps, then the
 // half-row and row mirrors; with HALF, over each 8-lane half-row instead.
 template <bool HALF = false>

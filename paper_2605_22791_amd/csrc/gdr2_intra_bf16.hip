@@ -207,8 +207,7 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
         float ss = 0.f;
 #pragma unroll
         for (int u = 0; u < 8; ++u) ss += kf[u] * kf[u];
-#pragma unroll
-        for (int o = 1; o < DK / 8; o <<= 1) ss += __shfl_xor(ss, o);
+        ss = row_sum<DK == 64>(ss);  // the DK / 8 lanes of row r
         const float rk = inv_norm(ss, a.st.eps);
 #pragma unroll
         for (int u = 0; u < 8; ++u) kf[u] *= rk;
@@ -252,8 +251,8 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
 #pragma unroll
         for (int u = 0; u < 8; ++u) ss += qf[p][u] * qf[p][u];
       }
-      ss += __shfl_xor(ss, 16);
-      ss += __shfl_xor(ss, 32);
+      ss += row_partner16(ss, (g & 1) != 0);
+      ss += row_partner32(ss, g >= 2);
       const float rq = inv_norm(ss, a.st.eps);
 #pragma unroll
       for (int p = 0; p < KS; ++p) {
@@ -444,14 +443,13 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
           M = mfma_f32(sTA[(16 * i + r16) * LTA + kk], sTA[kk * LTA + 16 * j + r16], M);
         }
       }
+      // B operand of the next product: lane (g, r16) takes element g of lane
+      // (st, r16)'s accumulator for K-step st, a 4 x 4 transpose across the
+      // 16-lane rows (two stages of 2 x 2 swaps with the permlane swaps)
+      row_transpose4(M);
 #pragma unroll
-      for (int st = 0; st < 4; ++st) {
-        const int src = r16 + 16 * st;
-        const float m0 = __shfl(M[0], src), m1 = __shfl(M[1], src);
-        const float m2 = __shfl(M[2], src), m3 = __shfl(M[3], src);
-        const float mv = g == 0 ? m0 : (g == 1 ? m1 : (g == 2 ? m2 : m3));
-        res = mfma_f32(sTA[(16 * i + r16) * LTA + 16 * i + 4 * st + g], mv, res);
-      }
+      for (int st = 0; st < 4; ++st)
+        res = mfma_f32(sTA[(16 * i + r16) * LTA + 16 * i + 4 * st + g], M[st], res);
     }
     __syncthreads();
     if (wave < i) {
