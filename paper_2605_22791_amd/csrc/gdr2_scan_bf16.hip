@@ -46,10 +46,15 @@ struct ScanCfg2 {
   // Y's fragments, unpadded, its 16-byte pieces XOR'd with the row (map_s_ix)
   static constexpr int LSS = MAP ? DK : DK + 8;
   static constexpr int LR = 64 + 8;          // R hi/lo [DVS][LR] bf16
-  // operand blocks, copied verbatim (contiguous Y | Qg | Aqk | KtT; MAP: Y | KtT)
+  // operand blocks, copied verbatim (contiguous Y | Qg | Aqk | KtT; MAP: Y | KtT;
+  // KtT only without KD)
   static constexpr int SZ_Y = (int)WsBf16::y(DK), SZ_Q = MAP ? 0 : (int)WsBf16::qg(DK);
   static constexpr int SZ_A = MAP ? 0 : (int)WsBf16::aqk(), SZ_K = (int)WsBf16::ktt(DK);
-  static constexpr int SZ_OP = SZ_Y + SZ_Q + SZ_A + SZ_K;
+  // with eight key blocks every wave's state tiles have a key block of their
+  // own, so its K_tail^T blocks go from memory straight into its registers
+  // (no LDS round trip); otherwise two waves share one and it is staged
+  static constexpr bool KD = NCB == 8;
+  static constexpr int SZ_OP = SZ_Y + SZ_Q + SZ_A + (KD ? 0 : SZ_K);
   static constexpr int NSTG = SZ_OP / (16 * NTHR);  // 16-byte chunks per thread
   static constexpr int OFF_S = 0;
   static constexpr int OFF_R = OFF_S + 2 * DVS * LSS * 2;
@@ -213,6 +218,15 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
   }
   __syncthreads();
 
+  // K_tail^T blocks of the wave's key block (KD), one chunk ahead
+  u4v kreg[4];
+  if constexpr (C::KD) {
+    if (n0 < n1) {
+      const unsigned char* kp = a.KtT + (chk + n0) * C::SZ_K + cs * 2 * 2048 + 16 * lane;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) kreg[q] = ldg16(kp + 1024 * q);
+    }
+  }
   for (int n = n0; n < n1; ++n) {
     const size_t ch = chs + n;
     // the next chunk's operands, fetched in groups over the step (the first
@@ -341,8 +355,13 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
           Fr kf, rf[TPW];
-          kf.hi = ld8(reinterpret_cast<const __bf16*>(sK + (cs * 2 + kb) * 2048 + 16 * lane));
-          kf.lo = ld8(reinterpret_cast<const __bf16*>(sK + (cs * 2 + kb) * 2048 + 1024 + 16 * lane));
+          if constexpr (C::KD) {
+            kf.hi = __builtin_bit_cast(bf8, kreg[2 * kb]);
+            kf.lo = __builtin_bit_cast(bf8, kreg[2 * kb + 1]);
+          } else {
+            kf.hi = ld8(reinterpret_cast<const __bf16*>(sK + (cs * 2 + kb) * 2048 + 16 * lane));
+            kf.lo = ld8(reinterpret_cast<const __bf16*>(sK + (cs * 2 + kb) * 2048 + 1024 + 16 * lane));
+          }
 #pragma unroll
           for (int t = 0; t < TPW; ++t) {
             const int vb = sv0 + t;
@@ -356,8 +375,13 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
         Fr kf[2], rfs[2][TPW];
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
-          kf[kb].hi = ld8(reinterpret_cast<const __bf16*>(sK + (cs * 2 + kb) * 2048 + 16 * lane));
-          kf[kb].lo = ld8(reinterpret_cast<const __bf16*>(sK + (cs * 2 + kb) * 2048 + 1024 + 16 * lane));
+          if constexpr (C::KD) {
+            kf[kb].hi = __builtin_bit_cast(bf8, kreg[2 * kb]);
+            kf[kb].lo = __builtin_bit_cast(bf8, kreg[2 * kb + 1]);
+          } else {
+            kf[kb].hi = ld8(reinterpret_cast<const __bf16*>(sK + (cs * 2 + kb) * 2048 + 16 * lane));
+            kf[kb].lo = ld8(reinterpret_cast<const __bf16*>(sK + (cs * 2 + kb) * 2048 + 1024 + 16 * lane));
+          }
 #pragma unroll
           for (int t = 0; t < TPW; ++t) {
             const int vb = sv0 + t;
@@ -373,6 +397,13 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
           for (int t = 0; t < TPW; ++t) sreg[t] = mma3(kf[kb], rfs[kb][t], sreg[t]);
+      }
+    }
+    if constexpr (C::KD) {
+      if (more) {
+        const unsigned char* kp = a.KtT + (chk + n + 1) * C::SZ_K + cs * 2 * 2048 + 16 * lane;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) kreg[q] = ldg16(kp + 1024 * q);
       }
     }
     if constexpr (STORE_H) {
