@@ -34,7 +34,12 @@
 // and the decay-scaled operands of the decay products in LDS while the next
 // block's loads are in flight.  dT and dA_qk live in LDS transposed ([s][r],
 // split hi/lo) so that both the row-r and the column-s operands of the decay
-// products are plain or transposed reads.
+// products are plain or transposed reads.  Cross-lane sums (the staging's
+// prefix sums over a block's rows, the dh.h row sums, the dG suffix sums) use
+// DPP moves inside 16-lane rows and the permlane swaps across rows, never an
+// LDS round trip.  The outputs leave as whole 128-byte row lines (bf16 dq, dk,
+// db of four key blocks, fp32 ones of two), and workgroups take the key heads
+// fastest in launch order, so that the resident ones share token rows.
 //
 // Decay factors (App. D.4 / the forward kernels), with 16-row blocks j and
 // G2f_j, G2l_j the cumulative log2-decay at their first and last rows: for the

@@ -8,10 +8,12 @@
 // reading Y, Q_g, A_qk, Ktail^T, U and gamma_C that the intra-chunk kernel
 // left in fragment order.  The fp32 state slice lives in registers as MFMA
 // accumulators (plus a bf16 hi/lo copy in LDS for the products that read it);
-// the next chunk's operand blocks are fetched into registers at the start of
+// the next chunk's operand blocks are fetched into registers in groups over
 // the current chunk's step and copied to LDS at its end, with the step's own
-// stores (R, O, the chunk state) behind its products.  The two value slices
-// of one head run on the same XCD so that their shared reads hit one L2.
+// stores (R, O, the chunk state) behind its products.  With eight key blocks
+// each wave's K_tail^T blocks (no other wave reads them) go from memory
+// straight into its registers, one chunk ahead.  The two value slices of one
+// head run on the same XCD so that their shared reads hit one L2.
 // With STORE_H the chunk-start states (fp16 with block scales, store_state_f16)
 // and R are written for the backward (alone in the backward's recompute, or
 // with the output when the forward keeps them).
