@@ -175,6 +175,25 @@ __device__ __forceinline__ bf8 cat8(bf4 x, bf4 y) {
   return r;
 }
 __device__ __forceinline__ float4 ldg_f4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+// An empty asm that reads and rewrites x: the loads that produced x have
+// completed there.  One vmcnt counts loads and stores in issue order, and a
+// wait for a load that has stores of a path-dependent count behind it becomes
+// vmcnt(0); settling the prefetched operands before a key block's stores keeps
+// the later waits for them from waiting for those stores too.
+__device__ __forceinline__ void settle(unsigned& x) { asm volatile("" : "+v"(x)::"memory"); }
+__device__ __forceinline__ void settle(float& x) { asm volatile("" : "+v"(x)::"memory"); }
+__device__ __forceinline__ void settle(u4v& x) { asm volatile("" : "+v"(x)::"memory"); }
+__device__ __forceinline__ void settle(bf4& x) {
+  typedef unsigned u2v __attribute__((ext_vector_type(2)));
+  u2v u = __builtin_bit_cast(u2v, x);
+  asm volatile("" : "+v"(u)::"memory");
+  x = __builtin_bit_cast(bf4, u);
+}
+__device__ __forceinline__ void settle(float4& x) {
+  f4 u = __builtin_bit_cast(f4, x);
+  asm volatile("" : "+v"(u)::"memory");
+  x = __builtin_bit_cast(float4, u);
+}
 // four consecutive outputs of one row: 8-byte bf16 or 16-byte fp32 store
 __device__ __forceinline__ void store_row4(__bf16* p, const float (&v)[4]) {
   *reinterpret_cast<bf4*>(p) = bf4{(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
@@ -825,6 +844,12 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
     quad_transpose(oq, jq);
     quad_transpose(ok, jq);
     quad_transpose(ob, jq);
+    // the next block's operands (prefetched at the top of this one) have arrived
+    // long before this point: settle them ahead of this block's stores (on every
+    // path, the last block's too, so that no later wait sees them as pending)
+    settle(pg), settle(pk), settle(pb), settle(pq);
+    settle(pg2), settle(pk2), settle(pb2), settle(pq2);
+    settle(ph), settle(pd), settle(psh), settle(psd), settle(pds);
     auto emit_qkb = [&](int o, const float(&xq)[4], const float(&xk)[4], const float(&xb)[4]) {
       const size_t ao = ko0 + o;
       float vq[4], vk[4], vb[4];

@@ -295,6 +295,15 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
     // 16 iO .., values 16 vb ..) as one split block, lane l's four values
     // (value l % 16, rows 4 (l / 16) + u) at 8 l of the hi and lo halves.  Like
     // the dh stores, these leave after the chunk's products are issued.
+    // the next chunk's staged values (loaded at the top of the step) have
+    // arrived by now: settle them ahead of the dR stores, on every path, so that
+    // neither their copy to LDS nor the next step's reuse of their registers
+    // waits for those stores (one vmcnt counts loads and stores in issue order)
+#pragma unroll
+    for (int m = 0; m < NSTG; ++m) asm volatile("" : "+v"(stg[m])::"memory");
+    asm volatile("" : "+v"(sto)::"memory");
+#pragma unroll
+    for (int u = 0; u < 4; ++u) asm volatile("" : "+v"(gnext[u])::"memory");
     if (a.DR) {
 #pragma unroll
       for (int t = 0; t < NVB / 2; ++t) {

@@ -236,12 +236,14 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
     // all at once, the second wave of each SIMD waits behind the first one's
     // loads before it can start its products.  One vmcnt counts loads and
     // stores in issue order, so waiting for these also waits for every store
-    // issued before them; this step's stores (R, O, h) come after the last group
+    // issued before them; this step's stores (R, O, h) come after the last group.
+    // The last step loads its own chunk again (unused): with the same loads
+    // issued on every path the compiler counts them exactly, and the state
+    // update waits for its K_tail^T fragments alone, not for every load since
     const bool more = n + 1 < n1;
-    if (more) {
-      GDR2_LOAD_OPS(chk + n + 1, 0, 3)
-      GDR2_LOAD_UG(ch + 1, chk + n + 1, unext, gnext)
-    }
+    const int nn = more ? n + 1 : n;
+    GDR2_LOAD_OPS(chk + nn, 0, 3)
+    GDR2_LOAD_UG(chs + nn, chk + nn, unext, gnext)
 
     // scale exponents of this chunk-start state's fp16 copy, early in the step
     // so that their cross-lane reductions overlap the products below
@@ -276,7 +278,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
     }
     // the fp16 copy's scale, taken here so its reduction overlaps the output products
     if constexpr (STORE_H) state_shifts<NVB / 2>(racc, rsh);
-    if (more) GDR2_LOAD_OPS(chk + n + 1, 3, WITH_O ? 6 : 10)
+    GDR2_LOAD_OPS(chk + nn, 3, WITH_O ? 6 : 10)
     __syncthreads();
 
     // ---- O^T = S^T Q_g^T + R^T A_qk^T  (lane: O[16 iO + r16][16 vb + 4 g + u]);
@@ -315,8 +317,8 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
         const bool live = p < KS || (p - KS) <= (iO >> 1);
         const bool next = p + 1 < NKO && (p + 1 < KS || (p + 1 - KS) <= (iO >> 1));
         if (next) GDR2_O_FRAGS(p + 1, (p + 1) & 1)
-        if (more && p == 1) GDR2_LOAD_OPS(chk + n + 1, 6, 8)
-        if (more && p == 3) GDR2_LOAD_OPS(chk + n + 1, 8, 10)
+        if (p == 1) GDR2_LOAD_OPS(chk + nn, 6, 8)
+        if (p == 3) GDR2_LOAD_OPS(chk + nn, 8, 10)
         if (live) {
 #pragma unroll
           for (int t = 0; t < NVB / 2; ++t) accO[t] = mma3(fb[p & 1][t], fa[p & 1], accO[t]);
@@ -335,7 +337,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
       }
     }
 
-    if (more) GDR2_LOAD_OPS(chk + n + 1, 10, NSTG)
+    GDR2_LOAD_OPS(chk + nn, 10, NSTG)
     // ---- S <- Diag(gamma_C) S + Ktail^T R
     if constexpr (STORE_H) {
       // the chunk-start state for the backward, fp16 with its block scales
@@ -402,11 +404,9 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
       }
     }
     if constexpr (C::KD) {
-      if (more) {
-        const unsigned char* kp = a.KtT + (chk + n + 1) * C::SZ_K + cs * 2 * 2048 + 16 * lane;
+      const unsigned char* kp = a.KtT + (chk + nn) * C::SZ_K + cs * 2 * 2048 + 16 * lane;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) kreg[q] = ldg16(kp + 1024 * q);
-      }
+      for (int q = 0; q < 4; ++q) kreg[q] = ldg16(kp + 1024 * q);
     }
     if constexpr (STORE_H) {
       // R for the backward: this wave's 16 x 32 tile as one fp16 fragment block
