@@ -12,7 +12,10 @@
 // gradient at the segment's end to the one at its start (BScanArgs).  The operands are the forward's fragment-ordered tiles
 // (gdr2_kernels.hpp): the transposed fragments these products need come out
 // of the same LDS blocks through ds_read_b64_tr_b16 with per-lane addresses,
-// since every 4 consecutive elements of a block row are contiguous.
+// since every 4 consecutive elements of a block row are contiguous.  The
+// next chunk's blocks are fetched into registers in four groups over a step
+// and copied to LDS at its end; they are settled before the step's dR stores,
+// so that no later wait for them also waits for those stores.
 //
 // Precision: every product is fp32-accurate (split hi/lo; dO and Y are exact
 // bf16 and keep a single part).
@@ -109,8 +112,14 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
   const size_t chk = key_ch(a.vl, chs, H, a.G, NT);  // key-head chunks: Y, Q_g, A_qk, K_tail, gamma_C
 #define GDR2_LOAD_CHUNK(N_)                                                                               \
   {                                                                                                    \
+    GDR2_LOAD_OPS(N_, 0, NSTG)                                                                         \
+    GDR2_LOAD_DOG(N_)                                                                                  \
+  }
+// operand slices [M0, M1) of chunk N_
+#define GDR2_LOAD_OPS(N_, M0, M1)                                                                         \
+  {                                                                                                    \
     const size_t chx = chk + (N_);                                                                     \
-    _Pragma("unroll") for (int m = 0; m < NSTG; ++m) {                                                 \
+    _Pragma("unroll") for (int m = (M0); m < (M1) && m < NSTG; ++m) {                                  \
       if (no_input && m >= E_Y && m < E_A) continue; /* Q_g, A_qk only multiply dO */                 \
       const unsigned char* src;                                                                        \
       if (m < E_Y)                                                                                     \
@@ -123,6 +132,11 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
         src = a.KtT + chx * C::SZ_K + (m - E_A) * SLICE;                                               \
       stg[m] = ldg16(src + 16 * tid);                                                                  \
     }                                                                                                  \
+  }
+// chunk N_'s dO slice and gamma_C
+#define GDR2_LOAD_DOG(N_)                                                                                 \
+  {                                                                                                    \
+    const size_t chx = chk + (N_);                                                                     \
     const int r_ = tid / (DVS / 8), c8_ = (tid % (DVS / 8)) * 8;                                       \
     size_t orow_;                                                                                      \
     int olen_;                                                                                         \
@@ -174,7 +188,14 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
 
   for (int n = n1 - 1; n >= n0; --n) {
     const size_t ch = chs + n;
-    if (n > n0) GDR2_LOAD_CHUNK(n - 1)
+    // the next chunk's loads in four groups over the step (here, between the
+    // two dR products, after them, at the start of the dS update): issued all
+    // at once, the second wave of each SIMD waits behind the first one's loads
+    // before it can start its products.  The first step loads its own chunk
+    // again (unused), so that the same loads are issued on every path
+    const int nn = n > n0 ? n - 1 : n;
+    GDR2_LOAD_OPS(nn, 0, 3)
+    GDR2_LOAD_DOG(nn)
 
     // scale exponents of the fp16 copy of dS, early in the step so that their
     // cross-lane reductions overlap the products below
@@ -209,6 +230,7 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
         racc[t] = mma3(kf, df, racc[t]);
       }
     }
+    GDR2_LOAD_OPS(nn, 3, 6)
     // (without dO the A_qk and Q_g products vanish: their tiles are not even loaded)
 #pragma unroll
     for (int kb = (iO >> 1); kb < 2 && !no_input; ++kb) {
@@ -227,6 +249,7 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
         aacc[t] = mma2a(af, ld_tr8(sdO, LDO, 32 * kb, 16 * vb, lane), aacc[t]);
       }
     }
+    GDR2_LOAD_OPS(nn, 6, 9)
     // gradient of this chunk's end state (sreg is not updated before the barrier below)
     if (a.DH) {
       const int col0 = v0 + 16 * sv0;
@@ -246,6 +269,7 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
     __syncthreads();
 
     // ---- dS <- Diag(gamma_C) dS + scale * Q_g^T dO - Y^T dR
+    GDR2_LOAD_OPS(nn, 9, NSTG)
     f4 qacc[TPW];
 #pragma unroll
     for (int t = 0; t < TPW; ++t) qacc[t] = f4zero();
@@ -323,6 +347,8 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
     __syncthreads();
   }
 #undef GDR2_LOAD_CHUNK
+#undef GDR2_LOAD_OPS
+#undef GDR2_LOAD_DOG
 #undef GDR2_STORE_CHUNK
 
   float* dstart = a.dSseg_out ? a.dSseg_out + (size_t)vs * DK * DV
