@@ -13,7 +13,7 @@
 // (gdr2_kernels.hpp): the transposed fragments these products need come out
 // of the same LDS blocks through ds_read_b64_tr_b16 with per-lane addresses,
 // since every 4 consecutive elements of a block row are contiguous.  The
-// next chunk's blocks are fetched into registers in four groups over a step
+// next chunk's blocks are fetched into registers in six groups over a step
 // and copied to LDS at its end; they are settled before the step's dR stores,
 // so that no later wait for them also waits for those stores.
 //
@@ -188,13 +188,14 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
 
   for (int n = n1 - 1; n >= n0; --n) {
     const size_t ch = chs + n;
-    // the next chunk's loads in four groups over the step (here, between the
-    // two dR products, after them, at the start of the dS update): issued all
-    // at once, the second wave of each SIMD waits behind the first one's loads
-    // before it can start its products.  The first step loads its own chunk
-    // again (unused), so that the same loads are issued on every path
+    // the next chunk's loads in six groups of two slices over the step (here,
+    // inside the Ktail dS product, before and after the A_qk^T dO product, and
+    // at the two K-steps of the dS update): issued all at once, the second
+    // wave of each SIMD waits behind the first one's loads before it can start
+    // its products.  The first step loads its own chunk again (unused), so
+    // that the same loads are issued on every path
     const int nn = n > n0 ? n - 1 : n;
-    GDR2_LOAD_OPS(nn, 0, 3)
+    GDR2_LOAD_OPS(nn, 0, 2)
     GDR2_LOAD_DOG(nn)
 
     // scale exponents of the fp16 copy of dS, early in the step so that their
@@ -229,8 +230,9 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
         df.lo = ld8(sDlo + (16 * vb + r16) * LSD + 32 * p + 8 * g);
         racc[t] = mma3(kf, df, racc[t]);
       }
+      if (p == 1) GDR2_LOAD_OPS(nn, 2, 4)
     }
-    GDR2_LOAD_OPS(nn, 3, 6)
+    GDR2_LOAD_OPS(nn, 4, 6)
     // (without dO the A_qk and Q_g products vanish: their tiles are not even loaded)
 #pragma unroll
     for (int kb = (iO >> 1); kb < 2 && !no_input; ++kb) {
@@ -249,7 +251,7 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
         aacc[t] = mma2a(af, ld_tr8(sdO, LDO, 32 * kb, 16 * vb, lane), aacc[t]);
       }
     }
-    GDR2_LOAD_OPS(nn, 6, 9)
+    GDR2_LOAD_OPS(nn, 6, 8)
     // gradient of this chunk's end state (sreg is not updated before the barrier below)
     if (a.DH) {
       const int col0 = v0 + 16 * sv0;
@@ -269,12 +271,13 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
     __syncthreads();
 
     // ---- dS <- Diag(gamma_C) dS + scale * Q_g^T dO - Y^T dR
-    GDR2_LOAD_OPS(nn, 9, NSTG)
+    GDR2_LOAD_OPS(nn, 8, 10)
     f4 qacc[TPW];
 #pragma unroll
     for (int t = 0; t < TPW; ++t) qacc[t] = f4zero();
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
+      if (kb == 1) GDR2_LOAD_OPS(nn, 10, NSTG)
       // Q_g[r][c], r = 32 kb + 8 g + e, c = 16 cs + r16
       Fr qf;
       bf8 yf;
