@@ -574,18 +574,39 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       for (int vb = 0; vb < NVB; ++vb) zacc[vb] = mma16(rf[vb].hi, af[rb].hi, zacc[vb]);
     }
   }
+  // value blocks in pairs: one permlane swap per dword turns the lane's two
+  // 4-value pieces (columns 32 p + 4 g .., 32 p + 16 + 4 g ..) into 8
+  // consecutive values of its row, at 32 p + {0, 16, 8, 24}[g], so that each
+  // lane stores 16 bytes per pair
+  static_assert(NVB % 2 == 0, "value blocks in pairs");
 #pragma unroll
-  for (int vb = 0; vb < NVB; ++vb) {
-    const int o = (16 * i + r16) * vst + 16 * vb + 4 * g;
-    bf4 odv, odw;
+  for (int p2 = 0; p2 < NVB / 2; ++p2) {
+    typedef unsigned u2v __attribute__((ext_vector_type(2)));
+    u2v av[2], aw[2];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      odv[u] = (__bf16)(zacc[vb][u] * (float)wwr[vb][u]);
-      odw[u] = (__bf16)(zacc[vb][u] * (float)vvr[vb][u]);
+    for (int h2 = 0; h2 < 2; ++h2) {
+      const int vb = 2 * p2 + h2;
+      bf4 odv, odw;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        odv[u] = (__bf16)(zacc[vb][u] * (float)wwr[vb][u]);
+        odw[u] = (__bf16)(zacc[vb][u] * (float)vvr[vb][u]);
+      }
+      av[h2] = __builtin_bit_cast(u2v, odv);
+      aw[h2] = __builtin_bit_cast(u2v, odw);
     }
+    u4v sv, sw;
+#pragma unroll
+    for (int d = 0; d < 2; ++d) {
+      const auto rv = __builtin_amdgcn_permlane16_swap(av[0][d], av[1][d], false, false);
+      const auto rw = __builtin_amdgcn_permlane16_swap(aw[0][d], aw[1][d], false, false);
+      sv[d] = rv[0], sv[2 + d] = rv[1];
+      sw[d] = rw[0], sw[2 + d] = rw[1];
+    }
+    const int o = (16 * i + r16) * vst + 32 * p2 + 8 * (((g & 1) << 1) | (g >> 1));
     if (16 * i + r16 < len) {
-      *reinterpret_cast<bf4*>(dVp + o) = odv;
-      *reinterpret_cast<bf4*>(dWp + o) = odw;
+      *reinterpret_cast<u4v*>(dVp + o) = sv;
+      *reinterpret_cast<u4v*>(dWp + o) = sw;
     }
   }
   // dZ, dO and R rows of block i as A operands over the values, permuted K:
