@@ -175,6 +175,15 @@ __device__ __forceinline__ bf8 cat8(bf4 x, bf4 y) {
   return r;
 }
 __device__ __forceinline__ float4 ldg_f4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+typedef unsigned u2v __attribute__((ext_vector_type(2)));
+// (x, y | z, w) -> one permlane16 swap of x with z and of y with w: between
+// "8 consecutive values at 32 p + {0, 16, 8, 24}[g]" and "4 values at 32 p + 4 g
+// then 4 at 32 p + 16 + 4 g" (g: the lane's 16-lane row), in either direction
+__device__ __forceinline__ u4v unswap_pair(u4v x) {
+  const auto r0 = __builtin_amdgcn_permlane16_swap(x[0], x[2], false, false);
+  const auto r1 = __builtin_amdgcn_permlane16_swap(x[1], x[3], false, false);
+  return u4v{r0[0], r1[0], r0[1], r1[1]};
+}
 // An empty asm that reads and rewrites x: the loads that produced x have
 // completed there.  One vmcnt counts loads and stores in issue order, and a
 // wait for a load that has stores of a path-dependent count behind it becomes
@@ -392,11 +401,16 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   // R's block scales: lane j * KV + p holds that of row block j, value block p
   const float rscl = lane < 4 * KV ? Rscc[lane] : 0.f;
   const auto rsc = [&](int blk) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(rscl), blk)); };
+  // dO rows of block i as fragments (values 32 p + 4 g .. and 32 p + 16 + 4 g ..):
+  // one 16-byte load of 8 consecutive values at 32 p + {0, 16, 8, 24}[g] and one
+  // permlane swap per dword, which puts the two 4-value pieces where they belong
+  // (the same swap, applied twice, is the identity)
+  const int goff = 8 * (((g & 1) << 1) | (g >> 1));
   bf8 dof[KV];
 #pragma unroll
   for (int p = 0; p < KV; ++p) {
-    const int o = (min(16 * i + r16, len - 1)) * vst + 32 * p + 4 * g;
-    dof[p] = cat8(*reinterpret_cast<const bf4*>(dOp + o), *reinterpret_cast<const bf4*>(dOp + o + 16));
+    const int o = (min(16 * i + r16, len - 1)) * vst + 32 * p + goff;
+    dof[p] = __builtin_bit_cast(bf8, unswap_pair(*reinterpret_cast<const u4v*>(dOp + o)));
   }
   float4 pg;
   u4v ph, pd;     // 8 fp16 values of h and dh
@@ -519,10 +533,14 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   // v, w for dv / dw, in flight across the barrier
   bf4 vvr[NVB], wwr[NVB];
 #pragma unroll
-  for (int vb = 0; vb < NVB; ++vb) {
-    const int o = min(16 * i + r16, len - 1) * vst + 16 * vb + 4 * g;
-    vvr[vb] = *reinterpret_cast<const bf4*>(Vp + o);
-    wwr[vb] = *reinterpret_cast<const bf4*>(Wp + o);
+  for (int p2 = 0; p2 < NVB / 2; ++p2) {
+    const int o = min(16 * i + r16, len - 1) * vst + 32 * p2 + goff;
+    const u4v xv = unswap_pair(*reinterpret_cast<const u4v*>(Vp + o));
+    const u4v xw = unswap_pair(*reinterpret_cast<const u4v*>(Wp + o));
+    vvr[2 * p2] = __builtin_bit_cast(bf4, u2v{xv[0], xv[1]});
+    vvr[2 * p2 + 1] = __builtin_bit_cast(bf4, u2v{xv[2], xv[3]});
+    wwr[2 * p2] = __builtin_bit_cast(bf4, u2v{xw[0], xw[1]});
+    wwr[2 * p2 + 1] = __builtin_bit_cast(bf4, u2v{xw[2], xw[3]});
   }
   __syncthreads();  // dR, A and R are in LDS (the barrier waits for the direct loads)
   // key block 0's operands, in flight while the prologue computes
@@ -581,7 +599,6 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
   static_assert(NVB % 2 == 0, "value blocks in pairs");
 #pragma unroll
   for (int p2 = 0; p2 < NVB / 2; ++p2) {
-    typedef unsigned u2v __attribute__((ext_vector_type(2)));
     u2v av[2], aw[2];
 #pragma unroll
     for (int h2 = 0; h2 < 2; ++h2) {
@@ -595,15 +612,9 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
       av[h2] = __builtin_bit_cast(u2v, odv);
       aw[h2] = __builtin_bit_cast(u2v, odw);
     }
-    u4v sv, sw;
-#pragma unroll
-    for (int d = 0; d < 2; ++d) {
-      const auto rv = __builtin_amdgcn_permlane16_swap(av[0][d], av[1][d], false, false);
-      const auto rw = __builtin_amdgcn_permlane16_swap(aw[0][d], aw[1][d], false, false);
-      sv[d] = rv[0], sv[2 + d] = rv[1];
-      sw[d] = rw[0], sw[2 + d] = rw[1];
-    }
-    const int o = (16 * i + r16) * vst + 32 * p2 + 8 * (((g & 1) << 1) | (g >> 1));
+    const u4v sv = unswap_pair(u4v{av[0][0], av[0][1], av[1][0], av[1][1]});
+    const u4v sw = unswap_pair(u4v{aw[0][0], aw[0][1], aw[1][0], aw[1][1]});
+    const int o = (16 * i + r16) * vst + 32 * p2 + goff;
     if (16 * i + r16 < len) {
       *reinterpret_cast<u4v*>(dVp + o) = sv;
       *reinterpret_cast<u4v*>(dWp + o) = sw;
