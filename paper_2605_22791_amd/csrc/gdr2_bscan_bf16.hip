@@ -121,6 +121,7 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
     const size_t chx = chk + (N_);                                                                     \
     _Pragma("unroll") for (int m = (M0); m < (M1) && m < NSTG; ++m) {                                  \
       if (no_input && m >= E_Y && m < E_A) continue; /* Q_g, A_qk only multiply dO */                 \
+      if (m == E_Q && (tid & 128) != 0) continue;    /* A_qk's all-zero blocks: not stored */         \
       const unsigned char* src;                                                                        \
       if (m < E_Y)                                                                                     \
         src = a.Y + chx * C::SZ_Y + m * SLICE;                                                         \
@@ -150,7 +151,8 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
 #define GDR2_STORE_CHUNK()                                                                               \
   {                                                                                                    \
     _Pragma("unroll") for (int m = 0; m < NSTG; ++m)                                                   \
-        if (!no_input || m < E_Y || m >= E_A) sts16(sOp + m * SLICE + 16 * tid, stg[m]);                \
+        if ((!no_input || m < E_Y || m >= E_A) && (m != E_Q || (tid & 128) == 0))                       \
+          sts16(sOp + m * SLICE + 16 * tid, stg[m]);                                                   \
     const int r_ = tid / (DVS / 8), c8_ = (tid % (DVS / 8)) * 8;                                       \
     sts16(sdO + r_ * LDO + c8_, sto);                                                                  \
     _Pragma("unroll") for (int u2 = 0; u2 < 4; ++u2) gcur[u2] = gnext[u2];                             \

@@ -76,17 +76,10 @@ __device__ __forceinline__ int tile_of(int wave, int t) {
     default: return t < 2 ? 14 + t : -1;
   }
 }
-// A_qk tiles above the diagonal that are written as zeros: (0,1) (2,3) (0,2) (0,3) (1,2) (1,3)
-__device__ __forceinline__ int zero_tile(int z) {
-  switch (z) {
-    case 0: return 1;
-    case 1: return 11;
-    case 2: return 2;
-    case 3: return 3;
-    case 4: return 6;
-    default: return 7;
-  }
-}
+// A_qk tiles above the diagonal that share fragment blocks with causal tiles,
+// written as zeros: (0,1) and (2,3).  (0,2) (0,3) (1,2) (1,3) make up two whole
+// blocks, which are not stored.
+__device__ __forceinline__ int zero_tile(int z) { return z == 0 ? 1 : 11; }
 
 template <int DK, int DV, bool FUSED>
 __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
@@ -386,14 +379,13 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
       const size_t off = (size_t)(i * 2 + (j >> 1)) * 2048 + 16 * lane + 8 * (j & 1);
       st4split(reinterpret_cast<__bf16*>(Ao + off), reinterpret_cast<__bf16*>(Ao + off + 1024), av);
     }
-    // zero A_qk tiles above the diagonal: (0,1) and (2,3) share fragment blocks
-    // with causal tiles; blocks (0, keys 32..63) and (1, keys 32..63) are all zero
-    {
-      for (int z = wave; z < 6; z += 4) {
-        const int i = zero_tile(z) >> 2, j = zero_tile(z) & 3;
-        const size_t off = (size_t)(i * 2 + (j >> 1)) * 2048 + 16 * lane + 8 * (j & 1);
-        st4split(reinterpret_cast<__bf16*>(Ao + off), reinterpret_cast<__bf16*>(Ao + off + 1024), f4zero());
-      }
+    // zero A_qk tiles above the diagonal that share fragment blocks with causal
+    // tiles, (0,1) and (2,3); the blocks of query rows 0..31 and keys 32..63 are
+    // all zero and are neither written nor read (the scans skip them)
+    if (wave < 2) {
+      const int i = zero_tile(wave) >> 2, j = zero_tile(wave) & 3;
+      const size_t off = (size_t)(i * 2 + (j >> 1)) * 2048 + 16 * lane + 8 * (j & 1);
+      st4split(reinterpret_cast<__bf16*>(Ao + off), reinterpret_cast<__bf16*>(Ao + off + 1024), f4zero());
     }
   }
   __syncthreads();

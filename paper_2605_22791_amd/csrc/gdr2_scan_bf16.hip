@@ -162,10 +162,15 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
   const size_t chk = key_ch(a.vl, chs, H, a.G, NT);  // key-head chunks: Y, Q_g, A_qk, K_tail, gamma_C
   // Q_g and A_qk feed the output only: a scan without it moves Y and Ktail^T alone
 #define GDR2_OP_USED(M_) (WITH_O || (M_) < E_Y || (M_) >= E_A)
+// the thread's 16 bytes of slice M_ lie in A_qk's all-zero blocks (query rows
+// 0..31, keys 32..63: blocks 1 and 3 of its first slice), which the intra-chunk
+// kernel does not write and the output products never read (the map pass
+// stages no A_qk: there E_Q is the first slice after Y)
+#define GDR2_OP_ZERO(M_) (C::SZ_A > 0 && (M_) == E_Q && (tid & 128) != 0)
 // operand slices [M0, M1) of chunk CHX (the slices a step's products do not read are skipped)
 #define GDR2_LOAD_OPS(CHX, M0, M1)                                                                           \
   _Pragma("unroll") for (int m = (M0); m < (M1) && m < NSTG; ++m) {                                      \
-    if (!GDR2_OP_USED(m)) continue;                                                                      \
+    if (!GDR2_OP_USED(m) || GDR2_OP_ZERO(m)) continue;                                                   \
     const unsigned char* src;                                                                            \
     if (m < E_Y)                                                                                         \
       src = a.Y + (CHX) * C::SZ_Y + m * SLICE;                                                           \
@@ -178,7 +183,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
     stg[m] = ldg16(src + 16 * tid);                                                                      \
   }
 #define GDR2_STORE_OPS()                                                                                     \
-  _Pragma("unroll") for (int m = 0; m < NSTG; ++m) if (GDR2_OP_USED(m)) sts16(sOp + m * SLICE + 16 * tid, stg[m]);
+  _Pragma("unroll") for (int m = 0; m < NSTG; ++m) if (GDR2_OP_USED(m) && !GDR2_OP_ZERO(m)) sts16(sOp + m * SLICE + 16 * tid, stg[m]);
   // U tiles (value blocks vbO.., row block iO) and gamma_C rows of the state tiles
 #define GDR2_LOAD_UG(CHX, CHKX, UARR, GARR)                                                                  \
   _Pragma("unroll") for (int t = 0; t < NVB / 2; ++t) {                                                  \
@@ -438,6 +443,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
 #undef GDR2_LOAD_OPS
 #undef GDR2_STORE_OPS
 #undef GDR2_OP_USED
+#undef GDR2_OP_ZERO
 #undef GDR2_LOAD_UG
   float* send = MAP ? (slice == 0 ? a.STseg : a.STseg_m) + (size_t)vs * DK * DV
                     : (a.STseg ? a.STseg + (size_t)vs * DK * DV
