@@ -387,6 +387,9 @@ __global__ __launch_bounds__(256, 2) void bchunk_bf16_kernel(BChunkBf16Args a) {
         src = DRc + off;
         dst = smem + C::OFF_T + off;
       } else if (off < C::SZ_DR + C::SZ_AM) {
+        // A's 1 KB pieces 4 and 6 hold tiles (sb, rb) = (2, 0..1) and (3, 0..1),
+        // above the diagonal: not stored, never read
+        if (off - C::SZ_DR == 4096 || off - C::SZ_DR == 6144) continue;
         src = Amc + (off - C::SZ_DR);
         dst = smem + C::OFF_S + (off - C::SZ_DR);
       } else {

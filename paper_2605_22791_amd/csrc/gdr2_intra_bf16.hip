@@ -459,6 +459,7 @@ __global__ __launch_bounds__(256, 2) void intra_bf16_kernel(IntraBf16Args a) {
 #pragma unroll
     for (int blk = wave; blk < 16; blk += 4) {
       const int sb = blk >> 2, rb = blk & 3;
+      if (rb < sb) continue;  // above the diagonal: zero, neither stored nor read
       f4 x;  // A[r = 16 rb + 4 g + e][s = 16 sb + r16]
 #pragma unroll
       for (int e = 0; e < 4; ++e) x[e] = sTA[(16 * rb + 4 * g + e) * LTA + 16 * sb + r16];

@@ -294,6 +294,10 @@ def test_bf16_backward_workspace_intermediates(Dk, Dv):
 
                 # A[r][s]: blocks [s][r];  dR[r][v]: blocks [v][r]
                 A = decode_tiles_f16(region("Am"), region("Amsc"), 4, 4)
+                # the tiles above the diagonal are zero and not stored
+                for rb_ in range(4):
+                    for sb_ in range(rb_ + 1, 4):
+                        A[16 * rb_:16 * rb_ + 16, 16 * sb_:16 * sb_ + 16] = 0.0
                 dRg = decode_tiles_split(region("DR"), Dv // 16, 4)
                 Aref = it["A"][bi, hi, n]
                 worst["A"] = max(worst["A"], rel_l2(A, Aref))
