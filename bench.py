@@ -39,7 +39,10 @@ def kernel_model(B, T, H, Dk, Dv, stored=True):
     the fragment-ordered workspace tiles as stored (split tiles hi + lo, Y
     single bf16, U fp32), and the backward's copies of the chunk states, their
     gradients and R in fp16 with one fp32 scale per 16 x 32 block, A in fp16
-    with one fp32 scale per 16 x 16 block.
+    with one fp32 scale per 16 x 16 block.  Blocks that are zero by causality
+    are not stored: two of A_qk's eight fragment blocks (query rows 0..31,
+    keys 32..63) and A's six tiles above the diagonal, of which the chunk
+    backward's copy skips the two 1 KB pieces that hold nothing else.
     """
     C = 64
     NC = B * H * (T // C)
@@ -53,9 +56,10 @@ def kernel_model(B, T, H, Dk, Dv, stored=True):
     st = Dk * Dv * f                          # fp32 state
     st16 = Dk * Dv * h + (Dk // 16) * (Dv // 32) * f   # fp16 state copy + scales
     r16 = C * Dv * h + (C // 16) * (Dv // 32) * f      # fp16 R + scales
-    ws_y, ws_q, ws_a = C * Dk * h, C * Dk * 2 * h, C * C * 2 * h
+    ws_y, ws_q, ws_a = C * Dk * h, C * Dk * 2 * h, C * C * 2 * h * 6 // 8
     ws_k, ws_u, ws_g = C * Dk * 2 * h, C * Dv * f, -(-Dk * f // 256) * 256
-    ws_am = C * C * h + (C // 16) * (C // 16) * f     # fp16 A, 16 x 16 blocks + scales
+    ws_am = 10 * 16 * 16 * h + 10 * f                # fp16 A written: 10 tiles + their scales
+    ws_am_rd = 6 * 1024 + (C // 16) * (C // 16) * f   # read by the chunk backward
     ws_dr = C * Dv * 2 * h                            # split bf16 dR
     seq_state = 2 * st / NT                   # S0 read + S_T write, per sequence
     m = {}
@@ -70,7 +74,7 @@ def kernel_model(B, T, H, Dk, Dv, stored=True):
     # dZ = A^T dR, dT = -dZ R^T, dA_qk = dO R^T (causal); dZ h^T, dO h^T, R dh^T;
     # the three decay products with dT / dA_qk (causal)
     m["bwd_intra"] = (3 * triv + 3 * mm + 4 * tri,
-                      3 * kin + kf + 3 * vin + 2 * st16 + r16 + ws_dr + ws_am + 3 * kin + 2 * vin + kf)
+                      3 * kin + kf + 3 * vin + 2 * st16 + r16 + ws_dr + ws_am_rd + 3 * kin + 2 * vin + kf)
     return {k: (fl * NC, by * NC) for k, (fl, by) in m.items()}
 
 
