@@ -324,10 +324,9 @@ __device__ __forceinline__ void store_state_f16(const f4 (&s)[TPW], const int (&
                       (_Float16)v1[0], (_Float16)v1[1], (_Float16)v1[2], (_Float16)v1[3]};
     *reinterpret_cast<f16x8*>(h0 + (size_t)(4 * g + j) * ld + 32 * t2 + 8 * m) = hv;
   }
-  if (lane == 0) {
+  // every lane writes the (wave-uniform) scales: no branch around the store
 #pragma unroll
-    for (int t2 = 0; t2 < TPW / 2; ++t2) sc[t2] = ldexpf(1.f, -sh[t2]);
-  }
+  for (int t2 = 0; t2 < TPW / 2; ++t2) sc[t2] = ldexpf(1.f, -sh[t2]);
 }
 // store_tile_f16: one 16 x 16 accumulator tile (lane (g, r16) holds rows
 // 4 g + u, column r16) as a 512-byte fp16 block of 16 x 16 x 16 operand

@@ -12,10 +12,14 @@
 // gradient at the segment's end to the one at its start (BScanArgs).  The operands are the forward's fragment-ordered tiles
 // (gdr2_kernels.hpp): the transposed fragments these products need come out
 // of the same LDS blocks through ds_read_b64_tr_b16 with per-lane addresses,
-// since every 4 consecutive elements of a block row are contiguous.  The
-// next chunk's blocks are fetched into registers in six groups over a step
-// and copied to LDS at its end; they are settled before the step's dR stores,
-// so that no later wait for them also waits for those stores.
+// since every 4 consecutive elements of a block row are contiguous.  A
+// chunk's blocks are fetched into one of two register buffers in six groups
+// over the step two steps before the one that computes it, settled before
+// the dR stores of the step in between (so that no later wait for them also
+// waits for those stores) and copied to LDS at its end.  The passes that write
+// dh and dR and those that do not (the segment maps) are separate kernels,
+// and the dO rows come through a range-checked buffer load, so that every
+// path issues the same loads and stores.
 //
 // Precision: every product is fp32-accurate (split hi/lo; dO and Y are exact
 // bf16 and keep a single part).
@@ -52,7 +56,8 @@ struct BScanCfg {
   static_assert(TPW >= 1 && NVB % 2 == 0, "wave split");
 };
 
-template <int DK, int DV>
+// STORE_D: the pass writes dh and dR (both set; the segment-map passes write neither)
+template <int DK, int DV, bool STORE_D>
 __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
   using C = BScanCfg<DK, DV>;
   constexpr int DVS = C::DVS, NS = C::NS, KS = C::KS, NCB = C::NCB, NVB = C::NVB, TPW = C::TPW;
@@ -105,22 +110,25 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
   const int cs = wave % NCB;               // key block of the dS tiles
   const int sv0 = (wave / NCB) * TPW;      // their value blocks
 
-  // ---- staging: operand blocks, the dO slice and gamma_C of one chunk
-  u4v stg[NSTG], sto;
-  float gcur[4], gnext[4];
+  // ---- staging: operand blocks, the dO slice and gamma_C of a chunk, in two
+  // register buffers (A, B): a chunk's values are fetched over the step two
+  // steps before the one that computes it and copied to LDS at the end of the
+  // step in between, so every load has a whole step to arrive
+  u4v stgA[NSTG], stoA, stgB[NSTG], stoB;
+  float gcur[4], gA[4], gB[4];
   const size_t chs = rng.chs;                        // value-head chunks: dh, dR
   const size_t chk = key_ch(a.vl, chs, H, a.G, NT);  // key-head chunks: Y, Q_g, A_qk, K_tail, gamma_C
-#define GDR2_LOAD_CHUNK(N_)                                                                               \
+#define GDR2_LOAD_CHUNK(N_, STG, STO, GN)                                                                 \
   {                                                                                                    \
-    GDR2_LOAD_OPS(N_, 0, NSTG)                                                                         \
-    GDR2_LOAD_DOG(N_)                                                                                  \
+    GDR2_LOAD_OPS(N_, 0, NSTG, STG)                                                                    \
+    GDR2_LOAD_DOG(N_, STO, GN)                                                                         \
   }
 // operand slices [M0, M1) of chunk N_
-#define GDR2_LOAD_OPS(N_, M0, M1)                                                                         \
+#define GDR2_LOAD_OPS(N_, M0, M1, STG)                                                                    \
   {                                                                                                    \
     const size_t chx = chk + (N_);                                                                     \
     _Pragma("unroll") for (int m = (M0); m < (M1) && m < NSTG; ++m) {                                  \
-      if (no_input && m >= E_Y && m < E_A) continue; /* Q_g, A_qk only multiply dO */                 \
+      /* (without dO, Q_g and A_qk are loaded all the same, but not staged) */                      \
       if (m == E_Q && (tid & 128) != 0) continue;    /* A_qk's all-zero blocks: not stored */         \
       const unsigned char* src;                                                                        \
       if (m < E_Y)                                                                                     \
@@ -131,31 +139,36 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
         src = a.Aqk + chx * C::SZ_A + (m - E_Q) * SLICE;                                               \
       else                                                                                             \
         src = a.KtT + chx * C::SZ_K + (m - E_A) * SLICE;                                               \
-      stg[m] = ldg16(src + 16 * tid);                                                                  \
+      STG[m] = ldg16(src + 16 * tid);                                                                  \
     }                                                                                                  \
   }
 // chunk N_'s dO slice and gamma_C
-#define GDR2_LOAD_DOG(N_)                                                                                 \
+#define GDR2_LOAD_DOG(N_, STO, GN)                                                                        \
   {                                                                                                    \
     const size_t chx = chk + (N_);                                                                     \
     const int r_ = tid / (DVS / 8), c8_ = (tid % (DVS / 8)) * 8;                                       \
     size_t orow_;                                                                                      \
     int olen_;                                                                                         \
     scan_rows(a.vl, seq, H, T, (N_), orow_, olen_);                                                    \
-    sto = (no_input || r_ >= olen_)                                                                    \
-              ? u4v{0u, 0u, 0u, 0u}                                                                    \
-              : ldg16(dO + (orow_ + r_) * ((size_t)H * DV) + (size_t)h * DV + v0 + c8_);               \
-    _Pragma("unroll") for (int u2 = 0; u2 < 4; ++u2) gnext[u2] =                                       \
+    /* through a buffer whose range ends with the chunk's last row (empty       */                  \
+    /* without dO): rows past it read as zero, with no branch around the load  */                  \
+    const unsigned pitch_ = (unsigned)(H * DV) * 2u;                                                   \
+    const __amdgpu_buffer_rsrc_t orsrc_ = __builtin_amdgcn_make_buffer_rsrc(                          \
+        no_input ? (void*)a.GC : (void*)(dO + orow_ * ((size_t)H * DV) + (size_t)h * DV + v0), 0,      \
+        no_input ? 0u : (unsigned)(olen_ - 1) * pitch_ + DVS * 2, 0x00020000);                         \
+    STO = __builtin_bit_cast(u4v, __builtin_amdgcn_raw_buffer_load_b128(                              \
+        orsrc_, (unsigned)r_ * pitch_ + c8_ * 2, 0, 0));                                               \
+    _Pragma("unroll") for (int u2 = 0; u2 < 4; ++u2) GN[u2] =                                          \
         a.GC[chx * (WsBf16::gc(DK) / 4) + 16 * cs + 4 * g + u2];                                       \
   }
-#define GDR2_STORE_CHUNK()                                                                               \
+#define GDR2_STORE_CHUNK(STG, STO, GN)                                                                   \
   {                                                                                                    \
     _Pragma("unroll") for (int m = 0; m < NSTG; ++m)                                                   \
         if ((!no_input || m < E_Y || m >= E_A) && (m != E_Q || (tid & 128) == 0))                       \
-          sts16(sOp + m * SLICE + 16 * tid, stg[m]);                                                   \
+          sts16(sOp + m * SLICE + 16 * tid, STG[m]);                                                   \
     const int r_ = tid / (DVS / 8), c8_ = (tid % (DVS / 8)) * 8;                                       \
-    sts16(sdO + r_ * LDO + c8_, sto);                                                                  \
-    _Pragma("unroll") for (int u2 = 0; u2 < 4; ++u2) gcur[u2] = gnext[u2];                             \
+    sts16(sdO + r_ * LDO + c8_, STO);                                                                  \
+    _Pragma("unroll") for (int u2 = 0; u2 < 4; ++u2) gcur[u2] = GN[u2];                                \
   }
 
   // ---- dS: tiles (key block cs, value blocks sv0..) as fp32 accumulators, starting
@@ -183,27 +196,40 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
              sreg[t]);
   }
   if (n0 < n1) {
-    GDR2_LOAD_CHUNK(n1 - 1)
-    GDR2_STORE_CHUNK()
+    // the last chunk into B and the one before it (or the first chunk again,
+    // unused) into A; B goes to LDS, and A is settled here so that the loop
+    // starts with no load pending (otherwise the registers the two paths into
+    // the loop give the buffers differ, and the loop top waits for stale loads)
+    GDR2_LOAD_CHUNK(n1 - 1, stgB, stoB, gB)
+    GDR2_LOAD_CHUNK(max(n1 - 2, n0), stgA, stoA, gA)
+    GDR2_STORE_CHUNK(stgB, stoB, gB)
+#pragma unroll
+    for (int m = 0; m < NSTG; ++m) asm volatile("" : "+v"(stgA[m])::"memory");
+    asm volatile("" : "+v"(stoA)::"memory");
+#pragma unroll
+    for (int u = 0; u < 4; ++u) asm volatile("" : "+v"(gA[u])::"memory");
   }
   __syncthreads();
 
-  for (int n = n1 - 1; n >= n0; --n) {
+  // one step: chunk n is in LDS, chunk n - 1 in the buffer (cstg, csto, cg),
+  // chunk n - 2 is fetched into the other one (nstg, nsto, ng)
+  auto step = [&](const int n, u4v(&cstg)[NSTG], u4v& csto, float(&cg)[4], u4v(&nstg)[NSTG], u4v& nsto,
+                  float(&ng)[4]) {
     const size_t ch = chs + n;
-    // the next chunk's loads in six groups of two slices over the step (here,
+    // chunk n - 2's loads in six groups of two slices over the step (here,
     // inside the Ktail dS product, before and after the A_qk^T dO product, and
     // at the two K-steps of the dS update): issued all at once, the second
     // wave of each SIMD waits behind the first one's loads before it can start
-    // its products.  The first step loads its own chunk again (unused), so
-    // that the same loads are issued on every path
-    const int nn = n > n0 ? n - 1 : n;
-    GDR2_LOAD_OPS(nn, 0, 2)
-    GDR2_LOAD_DOG(nn)
+    // its products.  The last two steps load the first chunk again (unused),
+    // so that the same loads are issued on every path
+    const int nn = max(n - 2, n0);
+    GDR2_LOAD_OPS(nn, 0, 2, nstg)
+    GDR2_LOAD_DOG(nn, nsto, ng)
 
     // scale exponents of the fp16 copy of dS, early in the step so that their
     // cross-lane reductions overlap the products below
     int dsh[TPW / 2];
-    if (a.DH) state_shifts<TPW>(sreg, dsh);
+    if constexpr (STORE_D) state_shifts<TPW>(sreg, dsh);
 
     // ---- dR = scale * A_qk^T dO + Ktail dS   (tiles: row block iO, value blocks vbO..)
     f4 racc[NVB / 2], aacc[NVB / 2];
@@ -232,9 +258,9 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
         df.lo = ld8(sDlo + (16 * vb + r16) * LSD + 32 * p + 8 * g);
         racc[t] = mma3(kf, df, racc[t]);
       }
-      if (p == 1) GDR2_LOAD_OPS(nn, 2, 4)
+      if (p == 1) GDR2_LOAD_OPS(nn, 2, 4, nstg)
     }
-    GDR2_LOAD_OPS(nn, 4, 6)
+    GDR2_LOAD_OPS(nn, 4, 6, nstg)
     // (without dO the A_qk and Q_g products vanish: their tiles are not even loaded)
 #pragma unroll
     for (int kb = (iO >> 1); kb < 2 && !no_input; ++kb) {
@@ -253,9 +279,9 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
         aacc[t] = mma2a(af, ld_tr8(sdO, LDO, 32 * kb, 16 * vb, lane), aacc[t]);
       }
     }
-    GDR2_LOAD_OPS(nn, 6, 8)
+    GDR2_LOAD_OPS(nn, 6, 8, nstg)
     // gradient of this chunk's end state (sreg is not updated before the barrier below)
-    if (a.DH) {
+    if constexpr (STORE_D) {
       const int col0 = v0 + 16 * sv0;
       store_state_f16<TPW>(sreg, dsh, a.DH + (ch * DK + 16 * cs) * DV + col0, DV,
                            a.DHsc + ch * (WsBf16::hsc(DK, DV) / 4) + cs * (DV / 32) + col0 / 32, lane);
@@ -273,13 +299,13 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
     __syncthreads();
 
     // ---- dS <- Diag(gamma_C) dS + scale * Q_g^T dO - Y^T dR
-    GDR2_LOAD_OPS(nn, 8, 10)
+    GDR2_LOAD_OPS(nn, 8, 10, nstg)
     f4 qacc[TPW];
 #pragma unroll
     for (int t = 0; t < TPW; ++t) qacc[t] = f4zero();
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
-      if (kb == 1) GDR2_LOAD_OPS(nn, 10, NSTG)
+      if (kb == 1) GDR2_LOAD_OPS(nn, 10, NSTG, nstg)
       // Q_g[r][c], r = 32 kb + 8 g + e, c = 16 cs + r16
       Fr qf;
       bf8 yf;
@@ -324,16 +350,16 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
     // 16 iO .., values 16 vb ..) as one split block, lane l's four values
     // (value l % 16, rows 4 (l / 16) + u) at 8 l of the hi and lo halves.  Like
     // the dh stores, these leave after the chunk's products are issued.
-    // the next chunk's staged values (loaded at the top of the step) have
-    // arrived by now: settle them ahead of the dR stores, on every path, so that
-    // neither their copy to LDS nor the next step's reuse of their registers
-    // waits for those stores (one vmcnt counts loads and stores in issue order)
+    // chunk n - 1's values (fetched over the previous step) have arrived by
+    // now: settle them ahead of the dR stores, on every path, so that neither
+    // their copy to LDS nor the reuse of their registers waits for those
+    // stores (one vmcnt counts loads and stores in issue order)
 #pragma unroll
-    for (int m = 0; m < NSTG; ++m) asm volatile("" : "+v"(stg[m])::"memory");
-    asm volatile("" : "+v"(sto)::"memory");
+    for (int m = 0; m < NSTG; ++m) asm volatile("" : "+v"(cstg[m])::"memory");
+    asm volatile("" : "+v"(csto)::"memory");
 #pragma unroll
-    for (int u = 0; u < 4; ++u) asm volatile("" : "+v"(gnext[u])::"memory");
-    if (a.DR) {
+    for (int u = 0; u < 4; ++u) asm volatile("" : "+v"(cg[u])::"memory");
+    if constexpr (STORE_D) {
 #pragma unroll
       for (int t = 0; t < NVB / 2; ++t) {
         const size_t blk = ch * (WsBf16::dr(DV) / 1024) + (size_t)(v0 / 16 + vbO + t) * 4 + iO;
@@ -348,8 +374,13 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
       st4split(sDhi + (16 * vb + r16) * LSD + 16 * cs + 4 * g, sDlo + (16 * vb + r16) * LSD + 16 * cs + 4 * g,
                sreg[t]);
     }
-    if (n > n0) GDR2_STORE_CHUNK()
+    if (n > n0) GDR2_STORE_CHUNK(cstg, csto, cg)
     __syncthreads();
+  };
+  // two steps per trip, so that the buffers trade roles without copies
+  for (int n = n1 - 1; n >= n0; n -= 2) {
+    step(n, stgA, stoA, gA, stgB, stoB, gB);
+    if (n - 1 >= n0) step(n - 1, stgB, stoB, gB, stgA, stoA, gA);
   }
 #undef GDR2_LOAD_CHUNK
 #undef GDR2_LOAD_OPS
@@ -367,15 +398,21 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
   }
 }
 
-template <int DK, int DV>
-hipError_t launch_bscan_bf16(const BScanArgs& a, hipStream_t st) {
+template <int DK, int DV, bool STORE_D>
+hipError_t launch_bscan_bf16_t(const BScanArgs& a, hipStream_t st) {
   using C = BScanCfg<DK, DV>;
-  const void* fn = reinterpret_cast<const void*>(&bscan_bf16_kernel<DK, DV>);
+  const void* fn = reinterpret_cast<const void*>(&bscan_bf16_kernel<DK, DV, STORE_D>);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
   if (e != hipSuccess) return e;
   dim3 grid(a.B * a.H * a.nseg * C::NS);
-  hipLaunchKernelGGL((bscan_bf16_kernel<DK, DV>), grid, dim3(C::NTHR), C::LDS, st, a);
+  hipLaunchKernelGGL((bscan_bf16_kernel<DK, DV, STORE_D>), grid, dim3(C::NTHR), C::LDS, st, a);
   return hipGetLastError();
+}
+
+template <int DK, int DV>
+hipError_t launch_bscan_bf16(const BScanArgs& a, hipStream_t st) {
+  if ((a.DH == nullptr) != (a.DR == nullptr)) return hipErrorInvalidValue;  // both or neither
+  return a.DH ? launch_bscan_bf16_t<DK, DV, true>(a, st) : launch_bscan_bf16_t<DK, DV, false>(a, st);
 }
 
 template hipError_t launch_bscan_bf16<64, 64>(const BScanArgs&, hipStream_t);
