@@ -189,11 +189,9 @@ __device__ __forceinline__ u4v unswap_pair(u4v x) {
 // wait for a load that has stores of a path-dependent count behind it becomes
 // vmcnt(0); settling the prefetched operands before a key block's stores keeps
 // the later waits for them from waiting for those stores too.
-__device__ __forceinline__ void settle(unsigned& x) { asm volatile("" : "+v"(x)::"memory"); }
 __device__ __forceinline__ void settle(float& x) { asm volatile("" : "+v"(x)::"memory"); }
 __device__ __forceinline__ void settle(u4v& x) { asm volatile("" : "+v"(x)::"memory"); }
 __device__ __forceinline__ void settle(bf4& x) {
-  typedef unsigned u2v __attribute__((ext_vector_type(2)));
   u2v u = __builtin_bit_cast(u2v, x);
   asm volatile("" : "+v"(u)::"memory");
   x = __builtin_bit_cast(bf4, u);
