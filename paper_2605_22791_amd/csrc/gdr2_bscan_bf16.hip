@@ -116,6 +116,7 @@ __global__ __launch_bounds__(512) void bscan_bf16_kernel(BScanArgs a) {
   // step in between, so every load has a whole step to arrive
   u4v stgA[NSTG], stoA, stgB[NSTG], stoB;
   float gcur[4], gA[4], gB[4];
+  static_assert(SLICE == 4 * 2048, "a staging slice is four 2 KB fragment blocks: thread t moves block t / 128");
   const size_t chs = rng.chs;                        // value-head chunks: dh, dR
   const size_t chk = key_ch(a.vl, chs, H, a.G, NT);  // key-head chunks: Y, Q_g, A_qk, K_tail, gamma_C
 #define GDR2_LOAD_CHUNK(N_, STG, STO, GN)                                                                 \

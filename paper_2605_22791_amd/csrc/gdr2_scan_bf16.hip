@@ -167,6 +167,7 @@ __global__ __launch_bounds__(512) void scan_bf16_kernel(ScanArgs a) {
 // kernel does not write and the output products never read (the map pass
 // stages no A_qk: there E_Q is the first slice after Y)
 #define GDR2_OP_ZERO(M_) (C::SZ_A > 0 && (M_) == E_Q && (tid & 128) != 0)
+  static_assert(SLICE == 4 * 2048, "a staging slice is four 2 KB fragment blocks: thread t moves block t / 128");
 // operand slices [M0, M1) of chunk CHX (the slices a step's products do not read are skipped)
 #define GDR2_LOAD_OPS(CHX, M0, M1)                                                                           \
   _Pragma("unroll") for (int m = (M0); m < (M1) && m < NSTG; ++m) {                                      \
