@@ -244,6 +244,50 @@ def test_bf16_backward_single_chunk_no_state():
     _compare(_run_bwd(d), _adjoint(d), TOL["bf16"])
 
 
+@pytest.mark.parametrize("T", [64, 100, 128, 192, 256])
+@pytest.mark.parametrize("Dk,Dv", [(128, 128), (64, 64)])
+def test_bf16_saved_path_few_chunks(T, Dk, Dv):
+    """The saved training path on sequences of one to four chunks (T = 100: a
+    full chunk and a partial one): the reverse scan walks two chunks per trip
+    with the next two chunks' operands in flight, and the first and last trips
+    load chunks they do not use, so an odd or even chunk count, one chunk and
+    two chunks are its edge cases.  The workspace is NaN-poisoned, so a read of
+    a region no kernel wrote (the causal zero blocks of A_qk and A are not
+    stored) would show in the outputs.  These tensors are small (8 K elements
+    at one chunk and d = 64), and the bf16 rounding of the exact result alone
+    then ranges over 1.5e-3 .. 2.1e-3 rel-L2 by seed: a bf16-typed output is
+    held to max(2e-3, 1.1 x that floor), computed here from the oracle."""
+    import torch
+    import paper_2605_22791_amd as g2
+    from oracle import gdr2_recurrent_fwd
+    d = make_inputs(1, T, 2, Dk, Dv, seed=80 + T + Dk, dtype="bf16", s0_std=0.05, with_dST=True)
+    _case(f"bf16 saved path B1 H2 T{T} Dk{Dk} Dv{Dv}")
+    x = dev_inputs(d)
+    args = [x[n] for n in ("q", "k", "v", "log_alpha", "b", "w")]
+    prob = g2._problem(x["q"], x["v"], d["scale"])
+    ws = torch.full((g2.gdr2_chunk_workspace_bytes(prob, 1),), 0xFF, dtype=torch.uint8, device="cuda")
+    o, ST = g2.gdr2_chunk_fwd(*args, x["S0"], scale=d["scale"], ws=ws, save=True)
+    g = g2.gdr2_chunk_bwd(*args, x["S0"], x["do"], x["dST"], scale=d["scale"], ws=ws, saved=True)
+    torch.cuda.synchronize()
+    o_ref, S_ref = gdr2_recurrent_fwd(d["q"], d["k"], d["v"], d["log_alpha"], d["b"], d["w"], d["S0"],
+                                      d["scale"])
+    ref = _adjoint(d)
+
+    def bound(x, bf16_typed):
+        if not bf16_typed:
+            return TOL["bf16"]
+        xb = torch.tensor(x, dtype=torch.float64).to(torch.bfloat16).to(torch.float64).numpy()
+        return max(TOL["bf16"], 1.1 * rel_l2(xb, x))
+
+    got = {n: host(t) for n, t in g.items()}
+    checks = [("o", host(o), o_ref, True), ("S_T", host(ST), S_ref, False), ("dS0", got["dS0"], ref["dS0"], False)]
+    checks += [(gn, got[gn], ref[rn], gn != "dlog_alpha") for gn, rn in NAMES]
+    for name, x, r, bf in checks:
+        err, lim = rel_l2(x, r), bound(r, bf)
+        print(f"{name}: {err:.2e} (bound {lim:.2e})")
+        assert err < lim, (name, err, lim)
+
+
 def test_bf16_extreme_decay_backward():
     """Decay spikes push a block's internal decay past e^60: the diagonal blocks
     of the decay products are then formed element by element."""
